@@ -1,0 +1,13 @@
+"""fp64 CPU oracle for the phase-split decoder forward pass.
+
+TEST INFRASTRUCTURE: only ``tests/``, ``__graft_entry__.smoke()`` and the benchmark's
+``cpu_baseline`` leg may import it.  The product path never routes through it.
+
+Parity status of each function (pins live in tests/test_oracle_pins.py):
+  rmsnorm, rope_frequencies, apply_rope, softmax, causal_gqa_attention, silu/swiglu,
+  argmax_lowest, top2_margin, OracleModel (prefill, decode, forward_full) -- all pinned.
+"""
+from .transformer import (  # noqa: F401
+    OracleModel, apply_rope, argmax_lowest, causal_gqa_attention, rmsnorm, rope_frequencies,
+    silu, softmax, split_prompts, swiglu, teacher_forced_run, top2_margin,
+)
