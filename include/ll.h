@@ -1,0 +1,137 @@
+/*
+ * ll.h -- C ABI of the phase-split decoder forward pass on one MI355X (gfx950).
+ *
+ * The paper frames inference as a target script with two phases whose kernels must be
+ * specialised separately (Sec. 2.1 "Motivating Evidence"; Sec. 3.1 "Hotspot Discovery and
+ * Phase-Aware Extraction"; appendix "Deployment Kernel Families", Table A.4):
+ *   - prefill: attention over a block of prompt queries (q_len > 1) that builds the KV cache;
+ *   - decode:  one query per sequence (q_len = 1) against the populated cache, which
+ *              appends exactly one entry per step.
+ * The library implements the forward pass of a pre-norm LLaMA-style decoder (RMSNorm,
+ * rotate-half RoPE, grouped-query attention, SwiGLU MLP, untied LM head, greedy argmax)
+ * for both phases, entirely in HIP kernels.
+ *
+ * Conventions for every call:
+ *   - No exceptions cross the boundary.  Every call validates its host-visible arguments
+ *     first and returns a status without enqueuing anything when they are wrong.
+ *   - The library never allocates device memory.  The caller passes one workspace buffer
+ *     (size from ll_workspace_size) that holds repacked weights, the KV cache, activations
+ *     and metadata for the model's lifetime.
+ *   - All device work is enqueued on the caller's HIP stream and the calls return without
+ *     synchronising; device faults surface at the caller's next synchronisation.
+ *   - A model handle is not thread-safe: use one host thread per handle.
+ *   - ll_last_error() returns a thread-local description of the last failure.
+ */
+#ifndef LL_H
+#define LL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ll_model ll_model; /* opaque, library-owned host object */
+
+typedef enum {
+  LL_OK = 0,
+  LL_ERR_INVALID_ARGUMENT = 1, /* null pointer, non-positive size, bad length */
+  LL_ERR_UNSUPPORTED = 2,      /* shape the kernels do not cover (rejected at load) */
+  LL_ERR_CAPACITY = 3,         /* batch, token or context limit of the config exceeded */
+  LL_ERR_STATE = 4,            /* prefill on a non-empty cache, decode before prefill */
+  LL_ERR_WORKSPACE = 5,        /* workspace missing, too small or misaligned */
+  LL_ERR_HIP = 6               /* a HIP runtime call or kernel launch failed */
+} ll_status;
+
+typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
+
+/* Model shape and capacity.  Supported: head_dim in {64, 128}; n_heads a multiple of
+ * n_kv_heads with n_heads / n_kv_heads in {1, 2, 4, 8}; d_model, n_heads*head_dim and
+ * (n_heads + 2 n_kv_heads)*head_dim and 2*ffn_dim multiples of 128; ffn_dim and d_model
+ * multiples of 64; vocab a multiple of 32; max_batch <= LL_MAX_BATCH. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+  float rms_eps;        /* RMSNorm epsilon (inside the square root) */
+  double rope_theta;    /* RoPE base: freq_i = theta^(-2i/head_dim) */
+  int32_t dtype;        /* ll_dtype: storage of weights, KV cache and GEMM inputs */
+  int32_t max_batch;          /* sequences per prefill / decode step */
+  int32_t max_prefill_tokens; /* total prompt tokens of one prefill */
+  int32_t max_ctx;            /* per-sequence cache capacity (prompt + decoded tokens) */
+} ll_config;
+
+#define LL_MAX_BATCH 256
+
+/* Weights: DEVICE pointers, element type = cfg.dtype, row-major [out][in] (y = x W^T).
+ * Per-layer fields are HOST arrays of n_layers device pointers.  They are read only
+ * during ll_model_load (repacked into the workspace); the caller may free them after
+ * synchronising the stream that ll_model_load used. */
+typedef struct {
+  const void *tok_embed;   /* [vocab, d_model] */
+  const void *final_norm;  /* [d_model] RMSNorm gain before the LM head */
+  const void *lm_head;     /* [vocab, d_model] (untied) */
+  const void *const *attn_norm; /* [d_model] */
+  const void *const *wq;        /* [n_heads*head_dim, d_model] */
+  const void *const *wk;        /* [n_kv_heads*head_dim, d_model] */
+  const void *const *wv;        /* [n_kv_heads*head_dim, d_model] */
+  const void *const *wo;        /* [d_model, n_heads*head_dim] */
+  const void *const *mlp_norm;  /* [d_model] */
+  const void *const *w_gate;    /* [ffn_dim, d_model] */
+  const void *const *w_up;      /* [ffn_dim, d_model] */
+  const void *const *w_down;    /* [d_model, ffn_dim] */
+} ll_weights;
+
+/* Bytes of workspace the config needs.  Host only, no HIP call. */
+ll_status ll_workspace_size(const ll_config *cfg, size_t *bytes);
+
+/* Validate cfg, repack the weights into `workspace` (device memory, >= ll_workspace_size
+ * bytes, 256-byte aligned) and build the RoPE table, all enqueued on `hip_stream`
+ * (a hipStream_t; NULL = the default stream).  On success *out owns host state only;
+ * the workspace stays the caller's and must outlive the model. */
+ll_status ll_model_load(const ll_config *cfg, const ll_weights *w, void *workspace,
+                        size_t workspace_bytes, void *hip_stream, ll_model **out);
+
+/* Prefill phase (q_len > 1 per sequence, empty cache).
+ * batch sequences with host lengths seq_lens_host[batch] (each >= 1); tokens_dev holds the
+ * sum(seq_lens) token ids packed in sequence order (device, int32, each in [0, vocab)).
+ * Writes next_tokens_dev[batch] (device) = argmax of the logits at each sequence's last
+ * prompt position (lowest index on ties) and, if logits_dev is not NULL, the fp32 logits
+ * [batch, vocab].  Afterwards sequence b has length seq_lens_host[b].
+ * LL_ERR_STATE if the cache is not empty (call ll_kv_reset first); LL_ERR_CAPACITY if
+ * batch > max_batch, sum(seq_lens) > max_prefill_tokens or a length > max_ctx. */
+ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
+                     const int32_t *tokens_dev, int32_t *next_tokens_dev, float *logits_dev);
+
+/* Decode phase (q_len = 1 against the populated cache): feeds in_tokens_dev[b] at position
+ * len[b] of every sequence of the last prefill, appends its key/value, writes
+ * next_tokens_dev[b] (and fp32 logits [batch, vocab] if logits_dev is not NULL) and
+ * advances every length by one.  in_tokens_dev may equal next_tokens_dev (greedy
+ * feedback).  The step runs as one HIP graph replay, captured on first use for each
+ * (in, out, logits) pointer triple.  LL_ERR_STATE before a prefill; LL_ERR_CAPACITY when
+ * some len[b] + 1 > max_ctx. */
+ll_status ll_decode_step(ll_model *m, const int32_t *in_tokens_dev, int32_t *next_tokens_dev,
+                         float *logits_dev);
+
+/* Forget every sequence (all lengths 0); the next call must be ll_prefill. */
+ll_status ll_kv_reset(ll_model *m);
+
+/* Current host-mirrored sequence lengths: writes min(cap, batch) values, *n = batch. */
+ll_status ll_seq_lengths(const ll_model *m, int32_t *out, int32_t cap, int32_t *n);
+
+/* Enable (1, default) or disable (0) HIP-graph replay of decode steps. */
+ll_status ll_set_decode_graph(ll_model *m, int32_t enable);
+
+/* Synchronise the model's stream and read the device error flags: bit 0 = a token id
+ * outside [0, vocab) was seen (it was replaced by 0, never read out of bounds). */
+ll_status ll_device_flags(ll_model *m, int32_t *flags);
+
+/* Release host state (graphs, handle).  The workspace is the caller's. */
+void ll_model_free(ll_model *m);
+
+/* Thread-local text of the last error ("" if none). */
+const char *ll_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LL_H */

@@ -1,0 +1,77 @@
+/*
+ * ll_ops.h -- per-kernel entry points of the hot path, for isolated qualification.
+ *
+ * The paper separates isolated qualification of a kernel (numerical correctness in a
+ * standalone harness) from deployment-time acceptance inside the model (Sec. 2.2
+ * "Formulation and Implications", first and third evaluation stages).  These calls run the
+ * same kernels that ll_prefill / ll_decode_step use, one at a time, so that each can be
+ * checked on its own; the model-level calls in ll.h are the acceptance path.
+ *
+ * All pointers are DEVICE pointers unless named *_host.  Element type "T" is float for
+ * LL_F32 and bfloat16 for LL_BF16.  Every call validates sizes first (no enqueue on error),
+ * enqueues on `stream` (hipStream_t, NULL = default) and returns without synchronising.
+ * The library allocates nothing: a call that needs scratch takes it from the caller.
+ */
+#ifndef LL_OPS_H
+#define LL_OPS_H
+
+#include "ll.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* y[r, :] = x[r, :] / sqrt(mean(x[r, :]^2) + eps) * gain   (Sec. 3 model block; RMSNorm).
+ * x fp32 [rows, d] row-major, gain T [d], y T [rows, d].  d a multiple of 4. */
+ll_status ll_op_rmsnorm(int32_t dtype, int32_t rows, int32_t d, const float *x,
+                        const void *gain, float eps, void *y, void *stream);
+
+/* Repack a row-major weight W (T [N, K]) into the tiled layout both GEMM paths stream:
+ * 16-row x (32 bf16 | 16 fp32)-column tiles of 1 KiB, each laid out in MFMA operand
+ * order, tiles of one 16-row block contiguous along K.  wt must hold N*K*sizeof(T) bytes.
+ * N a multiple of 16, K a multiple of 64. */
+ll_status ll_op_repack(int32_t dtype, int32_t n, int32_t k, const void *w, void *wt,
+                       void *stream);
+
+/* C[M, N] = A[M, K] W^T (accumulate = 0) or C += A W^T (accumulate = 1).
+ * A T row-major (lda = K), wt = repacked W, C fp32 row-major (ldc = N).
+ * path 0: prefill GEMM (LDS-tiled MFMA, N a multiple of 128);
+ * path 1: decode GEMM (weight-streaming MFMA, N a multiple of 32, any M). */
+ll_status ll_op_gemm(int32_t path, int32_t dtype, int32_t m, int32_t n, int32_t k,
+                     const void *a, const void *wt, float *c, int32_t accumulate, void *stream);
+
+/* Causal grouped-query prefill attention over packed ragged sequences (appendix
+ * "Deployment Kernel Families": one program per query tile and head, KV head from the head
+ * grouping, causal mask in the score update, fp32 online-softmax statistics).
+ * q T [sum(seq_lens), n_heads*head_dim]; kcache/vcache T [batch][n_kv_heads][max_ctx]
+ * [head_dim] holding positions 0..len-1 of each sequence; o T like q.
+ * scratch >= 1024 + 16*(batch + sum(seq_lens)) bytes (device metadata). */
+ll_status ll_op_attn_prefill(int32_t dtype, int32_t batch, const int32_t *seq_lens_host,
+                             int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
+                             int32_t max_ctx, const void *q, const void *kcache,
+                             const void *vcache, void *o, void *scratch, size_t scratch_bytes,
+                             void *stream);
+
+/* Decode attention: one query per sequence over ctx_lens_dev[b] cached keys (same
+ * appendix: each KV tile loaded once for its whole query-head group; split over the cache
+ * length with an fp32 log-sum-exp combine).  q T [batch, n_heads*head_dim]; caches as
+ * above; o T [batch, n_heads*head_dim].  1 <= ctx_lens_dev[b] <= max_ctx.
+ * scratch >= ll_op_attn_decode_scratch(...) bytes. */
+ll_status ll_op_attn_decode(int32_t dtype, int32_t batch, int32_t n_heads, int32_t n_kv_heads,
+                            int32_t head_dim, int32_t max_ctx, const void *q,
+                            const void *kcache, const void *vcache, const int32_t *ctx_lens_dev,
+                            void *o, void *scratch, size_t scratch_bytes, void *stream);
+size_t ll_op_attn_decode_scratch(int32_t batch, int32_t n_heads, int32_t n_kv_heads,
+                                 int32_t head_dim, int32_t max_ctx);
+
+/* LM head with fused greedy argmax: logits = h W^T, next[r] = argmax (lowest index on
+ * ties).  h T [rows, k], wt repacked [vocab, k], logits fp32 [rows, vocab] (nullable),
+ * next int32 [rows].  scratch >= 8 * rows * vocab / 32 bytes. */
+ll_status ll_op_lmhead_argmax(int32_t dtype, int32_t rows, int32_t vocab, int32_t k,
+                              const void *h, const void *wt, float *logits, int32_t *next,
+                              void *scratch, size_t scratch_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LL_OPS_H */

@@ -1,0 +1,308 @@
+"""ctypes binding of libll.so: argument marshalling only.
+
+Every step of the forward pass runs in the library's HIP kernels; PyTorch provides device
+memory (weights, workspace, tokens, logits) and the stream.  There is no fallback: if the
+library is missing, loading raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, c_char_p, c_double, c_float, c_int32, c_size_t, c_void_p
+from typing import Dict, List, Optional, Sequence, Tuple
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libll.so")
+
+LL_OK, LL_ERR_INVALID_ARGUMENT, LL_ERR_UNSUPPORTED, LL_ERR_CAPACITY, LL_ERR_STATE, \
+    LL_ERR_WORKSPACE, LL_ERR_HIP = range(7)
+STATUS_NAMES = ["LL_OK", "LL_ERR_INVALID_ARGUMENT", "LL_ERR_UNSUPPORTED", "LL_ERR_CAPACITY",
+                "LL_ERR_STATE", "LL_ERR_WORKSPACE", "LL_ERR_HIP"]
+LL_F32, LL_BF16 = 0, 1
+LL_MAX_BATCH = 256
+
+
+class LLConfig(ctypes.Structure):
+    _fields_ = [("n_layers", c_int32), ("d_model", c_int32), ("n_heads", c_int32),
+                ("n_kv_heads", c_int32), ("head_dim", c_int32), ("ffn_dim", c_int32),
+                ("vocab", c_int32), ("rms_eps", c_float), ("rope_theta", c_double),
+                ("dtype", c_int32), ("max_batch", c_int32), ("max_prefill_tokens", c_int32),
+                ("max_ctx", c_int32)]
+
+
+class LLWeights(ctypes.Structure):
+    _fields_ = [("tok_embed", c_void_p), ("final_norm", c_void_p), ("lm_head", c_void_p),
+                ("attn_norm", POINTER(c_void_p)), ("wq", POINTER(c_void_p)),
+                ("wk", POINTER(c_void_p)), ("wv", POINTER(c_void_p)), ("wo", POINTER(c_void_p)),
+                ("mlp_norm", POINTER(c_void_p)), ("w_gate", POINTER(c_void_p)),
+                ("w_up", POINTER(c_void_p)), ("w_down", POINTER(c_void_p))]
+
+
+# (name, restype, argtypes) of every exported symbol; include/ll.h and include/ll_ops.h
+# declare the same set.
+SIGNATURES = [
+    ("ll_workspace_size", c_int32, [POINTER(LLConfig), POINTER(c_size_t)]),
+    ("ll_model_load", c_int32, [POINTER(LLConfig), POINTER(LLWeights), c_void_p, c_size_t,
+                                c_void_p, POINTER(c_void_p)]),
+    ("ll_prefill", c_int32, [c_void_p, c_int32, POINTER(c_int32), c_void_p, c_void_p, c_void_p]),
+    ("ll_decode_step", c_int32, [c_void_p, c_void_p, c_void_p, c_void_p]),
+    ("ll_kv_reset", c_int32, [c_void_p]),
+    ("ll_seq_lengths", c_int32, [c_void_p, POINTER(c_int32), c_int32, POINTER(c_int32)]),
+    ("ll_set_decode_graph", c_int32, [c_void_p, c_int32]),
+    ("ll_device_flags", c_int32, [c_void_p, POINTER(c_int32)]),
+    ("ll_model_free", None, [c_void_p]),
+    ("ll_last_error", c_char_p, []),
+    ("ll_op_rmsnorm", c_int32, [c_int32, c_int32, c_int32, c_void_p, c_void_p, c_float,
+                                c_void_p, c_void_p]),
+    ("ll_op_repack", c_int32, [c_int32, c_int32, c_int32, c_void_p, c_void_p, c_void_p]),
+    ("ll_op_gemm", c_int32, [c_int32, c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
+                             c_void_p, c_int32, c_void_p]),
+    ("ll_op_attn_prefill", c_int32, [c_int32, c_int32, POINTER(c_int32), c_int32, c_int32,
+                                     c_int32, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                                     c_void_p, c_size_t, c_void_p]),
+    ("ll_op_attn_decode", c_int32, [c_int32, c_int32, c_int32, c_int32, c_int32, c_int32,
+                                    c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                    c_size_t, c_void_p]),
+    ("ll_op_attn_decode_scratch", c_size_t, [c_int32, c_int32, c_int32, c_int32, c_int32]),
+    ("ll_op_lmhead_argmax", c_int32, [c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
+                                      c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+]
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libll.so (built by paper_2608_21836_amd.build); raises if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} not found: build it with `python -m paper_2608_21836_amd.build`")
+    lib = ctypes.CDLL(path)
+    for name, res, args in SIGNATURES:
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+class LLError(RuntimeError):
+    def __init__(self, status: int, where: str, message: str):
+        self.status = status
+        self.message = message
+        super().__init__(f"{where}: {STATUS_NAMES[status] if 0 <= status < 7 else status}: {message}")
+
+
+def _check(status: int, where: str) -> None:
+    if status != LL_OK:
+        msg = load_library().ll_last_error()
+        raise LLError(status, where, msg.decode() if msg else "")
+
+
+def make_config(cfg, max_batch: int, max_prefill_tokens: int, max_ctx: int) -> LLConfig:
+    """LLConfig from a synth.configs.ModelConfig-like object."""
+    return LLConfig(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim,
+                    cfg.ffn_dim, cfg.vocab, float(cfg.rms_eps), float(cfg.rope_theta),
+                    LL_BF16 if cfg.dtype == "bf16" else LL_F32, max_batch, max_prefill_tokens,
+                    max_ctx)
+
+
+def workspace_size(cfg: LLConfig) -> int:
+    n = c_size_t(0)
+    _check(load_library().ll_workspace_size(ctypes.byref(cfg), ctypes.byref(n)), "ll_workspace_size")
+    return n.value
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream_handle(stream) -> int:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+class Model:
+    """One loaded model: workspace (a torch uint8 tensor), handle and stream.
+
+    ``weights`` maps synth.gen tensor names to CUDA tensors of the config's dtype.
+    """
+
+    def __init__(self, cfg, weights: Dict[str, "object"], max_batch: int,
+                 max_prefill_tokens: int, max_ctx: int, stream=None):
+        import torch
+        self.lib = load_library()
+        self.mcfg = cfg
+        self.cfg = make_config(cfg, max_batch, max_prefill_tokens, max_ctx)
+        self.stream = stream if stream is not None else torch.cuda.current_stream()
+        nbytes = workspace_size(self.cfg)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        nl = cfg.n_layers
+
+        def arr(key):
+            a = (c_void_p * nl)(*[weights[f"layers.{i}.{key}"].data_ptr() for i in range(nl)])
+            return ctypes.cast(a, POINTER(c_void_p)), a
+
+        keep = []
+        fields = {}
+        for key in ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "w_gate", "w_up", "w_down"):
+            p, a = arr(key)
+            keep.append(a)
+            fields[key] = p
+        w = LLWeights(weights["embed"].data_ptr(), weights["final_norm"].data_ptr(),
+                      weights["lm_head"].data_ptr(), **fields)
+        handle = c_void_p()
+        _check(self.lib.ll_model_load(ctypes.byref(self.cfg), ctypes.byref(w),
+                                      self.workspace.data_ptr(), nbytes,
+                                      self.stream.cuda_stream, ctypes.byref(handle)),
+               "ll_model_load")
+        self.handle = handle
+        self.batch = 0
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            self.lib.ll_model_free(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def prefill(self, seq_lens: Sequence[int], tokens, next_tokens=None, logits=None):
+        """tokens: int32 CUDA tensor of sum(seq_lens) ids.  Returns (next_tokens, logits)."""
+        import torch
+        b = len(seq_lens)
+        lens = (c_int32 * b)(*[int(x) for x in seq_lens])
+        if next_tokens is None:
+            next_tokens = torch.empty(b, dtype=torch.int32, device="cuda")
+        _check(self.lib.ll_prefill(self.handle, b, lens, tokens.data_ptr(), next_tokens.data_ptr(),
+                                   _ptr(logits)), "ll_prefill")
+        self.batch = b
+        return next_tokens, logits
+
+    def decode_step(self, in_tokens, next_tokens=None, logits=None):
+        import torch
+        if next_tokens is None:
+            next_tokens = torch.empty(self.batch, dtype=torch.int32, device="cuda")
+        _check(self.lib.ll_decode_step(self.handle, in_tokens.data_ptr(), next_tokens.data_ptr(),
+                                       _ptr(logits)), "ll_decode_step")
+        return next_tokens, logits
+
+    def kv_reset(self) -> None:
+        _check(self.lib.ll_kv_reset(self.handle), "ll_kv_reset")
+        self.batch = 0
+
+    def set_decode_graph(self, enable: bool) -> None:
+        _check(self.lib.ll_set_decode_graph(self.handle, 1 if enable else 0), "ll_set_decode_graph")
+
+    def seq_lengths(self) -> List[int]:
+        out = (c_int32 * LL_MAX_BATCH)()
+        n = c_int32(0)
+        _check(self.lib.ll_seq_lengths(self.handle, out, LL_MAX_BATCH, ctypes.byref(n)), "ll_seq_lengths")
+        return list(out[:n.value])
+
+    def device_flags(self) -> int:
+        f = c_int32(0)
+        _check(self.lib.ll_device_flags(self.handle, ctypes.byref(f)), "ll_device_flags")
+        return f.value
+
+
+# ------------------------------------------------------------------------------------------
+# Weights: numpy (synth.gen) -> CUDA tensors of the workload dtype
+# ------------------------------------------------------------------------------------------
+
+def to_device(arr, dtype: str):
+    """fp32 numpy array (bf16-exact for bf16 workloads) -> CUDA tensor of the storage type."""
+    import numpy as np
+    import torch
+    if dtype == "bf16":
+        bits = (np.ascontiguousarray(arr, dtype=np.float32).view(np.uint32) >> 16).astype(np.uint16)
+        return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32)).cuda()
+
+
+def upload_weights(cfg, weights) -> Dict[str, "object"]:
+    return {k: to_device(v, cfg.dtype) for k, v in weights.items()}
+
+
+# ------------------------------------------------------------------------------------------
+# Per-kernel entry points (isolated qualification)
+# ------------------------------------------------------------------------------------------
+
+def _dt(t) -> int:
+    import torch
+    return LL_BF16 if t.dtype == torch.bfloat16 else LL_F32
+
+
+def op_rmsnorm(x, gain, eps: float, stream=None):
+    import torch
+    y = torch.empty(x.shape, dtype=gain.dtype, device="cuda")
+    _check(load_library().ll_op_rmsnorm(_dt(gain), x.shape[0], x.shape[1], x.data_ptr(),
+                                        gain.data_ptr(), eps, y.data_ptr(), _stream_handle(stream)),
+           "ll_op_rmsnorm")
+    return y
+
+
+def op_repack(w, stream=None):
+    import torch
+    wt = torch.empty(w.numel() * w.element_size(), dtype=torch.uint8, device="cuda")
+    _check(load_library().ll_op_repack(_dt(w), w.shape[0], w.shape[1], w.data_ptr(), wt.data_ptr(),
+                                       _stream_handle(stream)), "ll_op_repack")
+    return wt
+
+
+def op_gemm(path: int, a, wt, n: int, c=None, accumulate: bool = False, stream=None):
+    import torch
+    m, k = a.shape
+    if c is None:
+        c = torch.empty(m, n, dtype=torch.float32, device="cuda")
+    _check(load_library().ll_op_gemm(path, _dt(a), m, n, k, a.data_ptr(), wt.data_ptr(),
+                                     c.data_ptr(), 1 if accumulate else 0, _stream_handle(stream)),
+           "ll_op_gemm")
+    return c
+
+
+def op_attn_prefill(seq_lens, q, kcache, vcache, n_heads, n_kv_heads, head_dim, max_ctx,
+                    stream=None):
+    import torch
+    b = len(seq_lens)
+    lens = (c_int32 * b)(*[int(x) for x in seq_lens])
+    o = torch.empty_like(q)
+    nbytes = 1024 + 16 * (b + int(sum(seq_lens)))
+    scratch = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    _check(load_library().ll_op_attn_prefill(_dt(q), b, lens, n_heads, n_kv_heads, head_dim,
+                                             max_ctx, q.data_ptr(), kcache.data_ptr(),
+                                             vcache.data_ptr(), o.data_ptr(), scratch.data_ptr(),
+                                             nbytes, _stream_handle(stream)), "ll_op_attn_prefill")
+    return o
+
+
+def op_attn_decode(q, kcache, vcache, ctx_lens, n_heads, n_kv_heads, head_dim, max_ctx,
+                   stream=None):
+    import torch
+    lib = load_library()
+    b = q.shape[0]
+    nbytes = lib.ll_op_attn_decode_scratch(b, n_heads, n_kv_heads, head_dim, max_ctx)
+    scratch = torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
+    o = torch.empty_like(q)
+    _check(lib.ll_op_attn_decode(_dt(q), b, n_heads, n_kv_heads, head_dim, max_ctx, q.data_ptr(),
+                                 kcache.data_ptr(), vcache.data_ptr(), ctx_lens.data_ptr(),
+                                 o.data_ptr(), scratch.data_ptr(), nbytes, _stream_handle(stream)),
+           "ll_op_attn_decode")
+    return o
+
+
+def op_lmhead_argmax(h, wt, vocab: int, want_logits: bool = True, stream=None):
+    import torch
+    rows, k = h.shape
+    logits = torch.empty(rows, vocab, dtype=torch.float32, device="cuda") if want_logits else None
+    nxt = torch.empty(rows, dtype=torch.int32, device="cuda")
+    nbytes = 8 * rows * (vocab // 32)
+    scratch = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    _check(load_library().ll_op_lmhead_argmax(_dt(h), rows, vocab, k, h.data_ptr(), wt.data_ptr(),
+                                              _ptr(logits), nxt.data_ptr(), scratch.data_ptr(),
+                                              nbytes, _stream_handle(stream)), "ll_op_lmhead_argmax")
+    return nxt, logits

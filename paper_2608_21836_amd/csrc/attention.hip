@@ -1,0 +1,354 @@
+// Phase-specialised causal grouped-query attention (appendix "Deployment Kernel Families",
+// Table A.4: a prefill kernel over query tiles with the causal mask inside the score update
+// and fp32 online-softmax statistics, and a decode kernel that loads each KV tile once for
+// the whole query-head group).
+//
+// Prefill: one block per (query tile of 64, query head); 4 waves x 16 queries.  Scores are
+// computed transposed, S^T = K Q^T, so that each lane owns one query column: the softmax
+// statistics and the O^T = V^T P^T accumulator are then lane-local, and P feeds the second
+// MFMA as its B operand without leaving registers.  K and V^T tiles are staged in LDS in
+// MFMA operand order.
+//
+// Decode: grid (split, kv head, sequence); a block streams `chunk` cached keys once for all
+// query heads of the group, keeps exact chunk scores in LDS and writes (max, sum, partial
+// output) per head; a combine kernel merges the splits with log-sum-exp weights.
+#include <algorithm>
+
+#include "device_common.h"
+#include "kernels.h"
+
+namespace ll {
+namespace {
+
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void k_attn_prefill(
+    const T *__restrict__ Q, int ldq, const T *__restrict__ Kc, const T *__restrict__ Vc,
+    T *__restrict__ O, int ldo, const int *__restrict__ cu, const int2 *__restrict__ qtiles,
+    int hq, int hkv, int max_ctx, float scale_log2) {
+  using F = typename Frag<T>::type;
+  constexpr int EPL = Frag<T>::EPL;
+  constexpr int KT = 4 * EPL;       // head dims per Q K^T chunk
+  constexpr int NQC = HD / KT;
+  constexpr int BKV = 64, NKS = BKV / 16;
+  constexpr int PVK = 4 * EPL;      // keys per P V chunk
+  constexpr int NPV = BKV / PVK;
+  constexpr int NDS = HD / 16;
+  constexpr int CPR = HD / EPL;     // 16-byte chunks per cached row
+  __shared__ F sK[NKS * NQC * 64];
+  __shared__ __attribute__((aligned(16))) T sV[NDS * NPV * 64 * EPL];
+
+  const int2 qt = qtiles[blockIdx.x];
+  const int b = qt.x, h = blockIdx.y, kvh = h / (hq / hkv);
+  const int tok0 = cu[b], L = cu[b + 1] - tok0;
+  const int q0 = qt.y * kAttnQTile;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int my_q = q0 + wave * 16 + (lane & 15);
+  const F fz = frag_zero<F>();
+
+  F qf[NQC];
+#pragma unroll
+  for (int c = 0; c < NQC; ++c)
+    qf[c] = my_q < L ? load_frag<F>(Q + (size_t)(tok0 + my_q) * ldq + h * HD + c * KT +
+                                    (lane >> 4) * EPL)
+                     : fz;
+  f32x4 acc[NDS];
+#pragma unroll
+  for (int ds = 0; ds < NDS; ++ds) acc[ds] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const int q_last = min(q0 + kAttnQTile - 1, L - 1);
+  const int ntiles = q_last / BKV + 1;
+  const size_t kvbase = ((size_t)b * hkv + kvh) * max_ctx * HD;
+  for (int kt = 0; kt < ntiles; ++kt) {
+    __syncthreads();
+    for (int c = tid; c < BKV * CPR; c += 256) {
+      const int key = c / CPR, dc = c % CPR;
+      const int gk = kt * BKV + key;
+      F kv = fz, vv = fz;
+      if (gk < L) {
+        kv = load_frag<F>(Kc + kvbase + (size_t)gk * HD + dc * EPL);
+        vv = load_frag<F>(Vc + kvbase + (size_t)gk * HD + dc * EPL);
+      }
+      sK[((key >> 4) * NQC + dc / 4) * 64 + (key & 15) + 16 * (dc & 3)] = kv;
+      const int kc = key / PVK, kk = key % PVK;
+      const int g = (kk & 15) >> 2, ee = (kk >> 4) * 4 + (kk & 3);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        const int d = dc * EPL + e;
+        sV[(((d >> 4) * NPV + kc) * 64 + (d & 15) + 16 * g) * EPL + ee] = vv[e];
+      }
+    }
+    __syncthreads();
+
+    f32x4 s[NKS];
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      s[ks] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < NQC; ++c) s[ks] = mma_chunk(sK[(ks * NQC + c) * 64 + lane], qf[c], s[ks]);
+    }
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = kt * BKV + ks * 16 + (lane >> 4) * 4 + r;
+        const float v = (key <= my_q && key < L) ? s[ks][r] * scale_log2 : -INFINITY;
+        s[ks][r] = v;
+        tmax = fmaxf(tmax, v);
+      }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+    const float m_new = fmaxf(m_run, tmax);
+    const float base = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = exp2f(m_run - base);
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int ds = 0; ds < NDS; ++ds) acc[ds] *= alpha;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float p = exp2f(s[ks][r] - base);
+        s[ks][r] = p;
+        l_run += p;
+      }
+#pragma unroll
+    for (int kc = 0; kc < NPV; ++kc) {
+      F pb;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) pb[e] = from_f32<T>(s[kc * (PVK / 16) + e / 4][e & 3]);
+#pragma unroll
+      for (int ds = 0; ds < NDS; ++ds)
+        acc[ds] = mma_chunk(*reinterpret_cast<const F *>(&sV[((ds * NPV + kc) * 64 + lane) * EPL]),
+                            pb, acc[ds]);
+    }
+  }
+  l_run += __shfl_xor(l_run, 16);
+  l_run += __shfl_xor(l_run, 32);
+  if (my_q < L) {
+    const float inv = 1.0f / l_run;
+    T *dst = O + (size_t)(tok0 + my_q) * ldo + h * HD + (lane >> 4) * 4;
+#pragma unroll
+    for (int ds = 0; ds < NDS; ++ds)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dst[ds * 16 + r] = from_f32<T>(acc[ds][r] * inv);
+  }
+}
+
+constexpr int kMaxChunk = 256;
+
+template <typename T, int HD, int G>
+__global__ __launch_bounds__(256) void k_attn_decode(
+    const T *__restrict__ Q, int ldq, const T *__restrict__ Kc, const T *__restrict__ Vc,
+    const int *__restrict__ lens, int len_add, int hkv, int max_ctx, int chunk, int nsplit,
+    float *__restrict__ part_o, float *__restrict__ part_ml, float scale_log2) {
+  using F = typename Frag<T>::type;
+  constexpr int EPL = Frag<T>::EPL;
+  constexpr int LPK = HD / EPL;     // lanes per cached row
+  constexpr int NSLOT = 256 / LPK;  // rows in flight per block
+  const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int S = min(lens[b] + len_add, max_ctx);  // never read past the cache capacity
+  const int j0 = split * chunk;
+  if (j0 >= S) return;
+  const int j1 = min(j0 + chunk, S), n = j1 - j0;
+  const int tid = threadIdx.x, dl = tid % LPK, slot = tid / LPK;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int hq = hkv * G;
+  __shared__ float s_p[G][kMaxChunk];
+  __shared__ float s_red[4][G][HD];
+  __shared__ float s_m[G], s_l[G];
+
+  float qv[G][EPL];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const F qq = load_frag<F>(Q + (size_t)b * ldq + (kvh * G + g) * HD + dl * EPL);
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) qv[g][e] = to_f32(qq[e]) * scale_log2;
+  }
+  const size_t kvbase = ((size_t)b * hkv + kvh) * max_ctx * HD;
+  const T *Kb = Kc + kvbase + dl * EPL;
+  const T *Vb = Vc + kvbase + dl * EPL;
+
+  for (int j = j0 + slot; j < j1; j += NSLOT) {
+    const F kk = load_frag_stream<F>(Kb + (size_t)j * HD);
+    float d[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float a = 0.f;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) a += qv[g][e] * to_f32(kk[e]);
+      d[g] = a;
+    }
+#pragma unroll
+    for (int o = LPK / 2; o > 0; o >>= 1)
+#pragma unroll
+      for (int g = 0; g < G; ++g) d[g] += __shfl_xor(d[g], o);
+    if (dl == 0)
+#pragma unroll
+      for (int g = 0; g < G; ++g) s_p[g][j - j0] = d[g];
+  }
+  __syncthreads();
+  for (int g = wave; g < G; g += 4) {
+    float mx = -INFINITY;
+    for (int i = lane; i < n; i += 64) mx = fmaxf(mx, s_p[g][i]);
+    mx = wave_max(mx);
+    float sum = 0.f;
+    for (int i = lane; i < n; i += 64) {
+      const float p = exp2f(s_p[g][i] - mx);
+      s_p[g][i] = p;
+      sum += p;
+    }
+    sum = wave_sum(sum);
+    if (lane == 0) {
+      s_m[g] = mx;
+      s_l[g] = sum;
+    }
+  }
+  __syncthreads();
+  float acc[G][EPL];
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) acc[g][e] = 0.f;
+  for (int j = j0 + slot; j < j1; j += NSLOT) {
+    const F vv = load_frag_stream<F>(Vb + (size_t)j * HD);
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float p = s_p[g][j - j0];
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[g][e] += p * to_f32(vv[e]);
+    }
+  }
+#pragma unroll
+  for (int o = LPK; o < 64; o <<= 1)
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[g][e] += __shfl_xor(acc[g][e], o);
+  if (lane < LPK)
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) s_red[wave][g][dl * EPL + e] = acc[g][e];
+  __syncthreads();
+  for (int i = tid; i < G * HD; i += 256) {
+    const int g = i / HD, d = i % HD;
+    const float v = s_red[0][g][d] + s_red[1][g][d] + s_red[2][g][d] + s_red[3][g][d];
+    const int h = kvh * G + g;
+    part_o[(((size_t)b * hq + h) * nsplit + split) * HD + d] = v;
+  }
+  if (tid < G) {
+    const int h = kvh * G + tid;
+    float *ml = part_ml + (((size_t)b * hq + h) * nsplit + split) * 2;
+    ml[0] = s_m[tid];
+    ml[1] = s_l[tid];
+  }
+}
+
+template <typename T, int HD>
+__global__ __launch_bounds__(HD) void k_attn_combine(const float *__restrict__ part_o,
+                                                      const float *__restrict__ part_ml,
+                                                      const int *__restrict__ lens, int len_add,
+                                                      int hq, int chunk, int nsplit,
+                                                      int max_ctx, T *__restrict__ O, int ldo) {
+  const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
+  const int S = min(lens[b] + len_add, max_ctx);
+  const int ns = (S + chunk - 1) / chunk;
+  const size_t base = ((size_t)b * hq + h) * nsplit;
+  float mx = -INFINITY;
+  for (int s = 0; s < ns; ++s) mx = fmaxf(mx, part_ml[(base + s) * 2]);
+  float num = 0.f, den = 0.f;
+  for (int s = 0; s < ns; ++s) {
+    const float w = exp2f(part_ml[(base + s) * 2] - mx);
+    num += w * part_o[(base + s) * HD + d];
+    den += w * part_ml[(base + s) * 2 + 1];
+  }
+  O[(size_t)b * ldo + h * HD + d] = from_f32<T>(num / den);
+}
+
+template <typename T, int HD>
+hipError_t run_prefill(const void *q, int ldq, const void *kc, const void *vc, void *o, int ldo,
+                       const int *cu, const int2 *qtiles, int n_qtiles, int hq, int hkv,
+                       int max_ctx, hipStream_t s) {
+  const float scale_log2 = kLog2e / sqrtf((float)HD);
+  hipLaunchKernelGGL((k_attn_prefill<T, HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
+                     reinterpret_cast<const T *>(q), ldq, reinterpret_cast<const T *>(kc),
+                     reinterpret_cast<const T *>(vc), reinterpret_cast<T *>(o), ldo, cu, qtiles,
+                     hq, hkv, max_ctx, scale_log2);
+  return hipGetLastError();
+}
+
+template <typename T, int HD, int G>
+hipError_t run_decode_g(const void *q, int ldq, const void *kc, const void *vc, const int *lens,
+                        int len_add, void *o, int ldo, int batch, int hkv, int max_ctx,
+                        int chunk, float *part_o, float *part_ml, hipStream_t s) {
+  const int nsplit = (max_ctx + chunk - 1) / chunk;
+  const float scale_log2 = kLog2e / sqrtf((float)HD);
+  hipLaunchKernelGGL((k_attn_decode<T, HD, G>), dim3(nsplit, hkv, batch), dim3(256), 0, s,
+                     reinterpret_cast<const T *>(q), ldq, reinterpret_cast<const T *>(kc),
+                     reinterpret_cast<const T *>(vc), lens, len_add, hkv, max_ctx, chunk, nsplit,
+                     part_o, part_ml, scale_log2);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3(hkv * G, batch), dim3(HD), 0, s, part_o,
+                     part_ml, lens, len_add, hkv * G, chunk, nsplit, max_ctx,
+                     reinterpret_cast<T *>(o), ldo);
+  return hipGetLastError();
+}
+
+template <typename T, int HD>
+hipError_t run_decode(int group, const void *q, int ldq, const void *kc, const void *vc,
+                      const int *lens, int len_add, void *o, int ldo, int batch, int hkv,
+                      int max_ctx, int chunk, float *part_o, float *part_ml, hipStream_t s) {
+  switch (group) {
+    case 1: return run_decode_g<T, HD, 1>(q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
+    case 2: return run_decode_g<T, HD, 2>(q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
+    case 4: return run_decode_g<T, HD, 4>(q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
+    case 8: return run_decode_g<T, HD, 8>(q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_attn_prefill(int dtype, int head_dim, const void *q, int ldq, const void *kc,
+                               const void *vc, void *o, int ldo, const int *cu,
+                               const int2 *qtiles, int n_qtiles, int hq, int hkv, int max_ctx,
+                               hipStream_t s) {
+  if (n_qtiles <= 0) return hipSuccess;
+  if (dtype == kF32) {
+    if (head_dim == 64) return run_prefill<float, 64>(q, ldq, kc, vc, o, ldo, cu, qtiles, n_qtiles, hq, hkv, max_ctx, s);
+    if (head_dim == 128) return run_prefill<float, 128>(q, ldq, kc, vc, o, ldo, cu, qtiles, n_qtiles, hq, hkv, max_ctx, s);
+  } else {
+    if (head_dim == 64) return run_prefill<bf16, 64>(q, ldq, kc, vc, o, ldo, cu, qtiles, n_qtiles, hq, hkv, max_ctx, s);
+    if (head_dim == 128) return run_prefill<bf16, 128>(q, ldq, kc, vc, o, ldo, cu, qtiles, n_qtiles, hq, hkv, max_ctx, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+int attn_decode_chunk(int batch, int hkv, int max_ctx) {
+  int chunk = kMaxChunk;
+  while (chunk > 64 && (long)batch * hkv * ((max_ctx + chunk - 1) / chunk) < 1024) chunk >>= 1;
+  return chunk;
+}
+
+hipError_t launch_attn_decode(int dtype, int head_dim, const void *q, int ldq, const void *kc,
+                              const void *vc, const int *lens, int len_add, void *o, int ldo,
+                              int batch, int hq, int hkv, int max_ctx, int chunk, float *part_o,
+                              float *part_ml, hipStream_t s) {
+  if (batch <= 0) return hipSuccess;
+  if (chunk > kMaxChunk || chunk <= 0 || hq % hkv) return hipErrorInvalidValue;
+  const int g = hq / hkv;
+  if (dtype == kF32) {
+    if (head_dim == 64) return run_decode<float, 64>(g, q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
+    if (head_dim == 128) return run_decode<float, 128>(g, q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
+  } else {
+    if (head_dim == 64) return run_decode<bf16, 64>(g, q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
+    if (head_dim == 128) return run_decode<bf16, 128>(g, q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace ll

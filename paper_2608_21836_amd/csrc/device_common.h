@@ -1,0 +1,74 @@
+// Device helpers shared by the gfx950 kernels: element types, 16-byte MFMA operand
+// fragments, conversions and wave reductions.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// One lane's 16-byte share of a 16-row MFMA operand tile.
+//   bf16: 8 elements, the tile spans 32 along the contraction axis (v_mfma_f32_16x16x32_bf16)
+//   fp32: 4 elements, the tile spans 16 along the contraction axis (4 x v_mfma_f32_16x16x4_f32)
+// Lane l covers row (l % 16) and contraction indices EPL * (l / 16) + e, e < EPL.
+template <typename T> struct Frag;
+template <> struct Frag<bf16> {
+  typedef bf16x8 type;
+  static constexpr int EPL = 8;
+};
+template <> struct Frag<float> {
+  typedef f32x4 type;
+  static constexpr int EPL = 4;
+};
+
+// 16x16 output tile += A-fragment x B-fragment over one 16-byte-per-lane chunk.
+// Output layout: lane l holds rows 4*(l/16) + r (r < 4) of column l % 16.
+__device__ __forceinline__ f32x4 mma_chunk(const bf16x8 &a, const bf16x8 &b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma_chunk(const f32x4 &a, const f32x4 &b, f32x4 c) {
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], c, 0, 0, 0);
+  return c;
+}
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16 x) { return static_cast<float>(x); }
+
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return static_cast<bf16>(x); }
+
+template <typename F> __device__ __forceinline__ F frag_zero() {
+  F z;
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(F) / sizeof(z[0])); ++i) z[i] = 0;
+  return z;
+}
+
+template <typename F> __device__ __forceinline__ F load_frag(const void *p) {
+  return *reinterpret_cast<const F *>(p);
+}
+
+// Streaming (read-once) 16-byte load that should not displace reused data in the caches.
+template <typename F> __device__ __forceinline__ F load_frag_stream(const void *p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const F *>(p));
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+__device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)); }
+
+constexpr float kLog2e = 1.4426950408889634f;

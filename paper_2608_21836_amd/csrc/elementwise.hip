@@ -1,0 +1,163 @@
+// Row-wise kernels of the decoder: embedding gather, RMSNorm, the final argmax reduction of
+// the LM head and the prefill metadata builder.
+#include <algorithm>
+
+#include "device_common.h"
+#include "kernels.h"
+
+namespace ll {
+namespace {
+
+// x[m, :] = E[tokens[m], :] in fp32.  An id outside [0, vocab) sets flag bit 0 and reads row 0.
+template <typename T>
+__global__ __launch_bounds__(256) void k_embed(const int *__restrict__ tokens,
+                                               const T *__restrict__ table, int vocab, int d,
+                                               float *__restrict__ x, int *err) {
+  const int m = blockIdx.x;
+  int t = tokens[m];
+  if (t < 0 || t >= vocab) {
+    if (threadIdx.x == 0 && err) atomicOr(err, 1);
+    t = 0;
+  }
+  const T *src = table + (size_t)t * d;
+  float *dst = x + (size_t)m * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) dst[i] = to_f32(src[i]);
+}
+
+// y[r, :] = x[src, :] / sqrt(mean(x[src, :]^2) + eps) * gain, src = rowmap ? rowmap[r] : r.
+template <typename T>
+__global__ __launch_bounds__(256) void k_rmsnorm(const float *__restrict__ x, int ldx,
+                                                 const int *__restrict__ rowmap, int d,
+                                                 const T *__restrict__ gain, float eps,
+                                                 T *__restrict__ y, int ldy) {
+  const int r = blockIdx.x;
+  const int src = rowmap ? rowmap[r] : r;
+  const float4 *xr = reinterpret_cast<const float4 *>(x + (size_t)src * ldx);
+  const int d4 = d >> 2;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d4; i += 256) {
+    const float4 v = xr[i];
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  __shared__ float part[4];
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = part[0] + part[1] + part[2] + part[3];
+  const float scale = 1.0f / sqrtf(tot / (float)d + eps);
+  T *yr = y + (size_t)r * ldy;
+  for (int i = threadIdx.x; i < d4; i += 256) {
+    const float4 v = xr[i];
+    yr[4 * i + 0] = from_f32<T>(v.x * scale * to_f32(gain[4 * i + 0]));
+    yr[4 * i + 1] = from_f32<T>(v.y * scale * to_f32(gain[4 * i + 1]));
+    yr[4 * i + 2] = from_f32<T>(v.z * scale * to_f32(gain[4 * i + 2]));
+    yr[4 * i + 3] = from_f32<T>(v.w * scale * to_f32(gain[4 * i + 3]));
+  }
+}
+
+__device__ __forceinline__ void better(float &bv, int &bi, float ov, int oi) {
+  if (ov > bv || (ov == bv && oi < bi)) {
+    bv = ov;
+    bi = oi;
+  }
+}
+
+// next[r] = column of the largest partial (lowest column on ties); lens_inc[r] += 1 if given.
+__global__ __launch_bounds__(256) void k_argmax_reduce(const float *__restrict__ pval,
+                                                       const int *__restrict__ pidx, int n_parts,
+                                                       int *__restrict__ next, int *lens_inc) {
+  const int r = blockIdx.x;
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int i = threadIdx.x; i < n_parts; i += 256)
+    better(bv, bi, pval[(size_t)r * n_parts + i], pidx[(size_t)r * n_parts + i]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) better(bv, bi, __shfl_xor(bv, o), __shfl_xor(bi, o));
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  if ((threadIdx.x & 63) == 0) {
+    sv[threadIdx.x >> 6] = bv;
+    si[threadIdx.x >> 6] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 4; ++w) better(bv, bi, sv[w], si[w]);
+    next[r] = bi;
+    if (lens_inc) lens_inc[r] += 1;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_prefill_meta(PrefillMeta pm, int total, int *cu,
+                                                      int *row_seq, int *row_pos, int *last_row,
+                                                      int *lens_dev, int2 *qtiles) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m < total) {
+    int b = 0, start = 0;
+    while (b < pm.batch - 1 && m >= start + pm.lens[b]) start += pm.lens[b++];
+    row_seq[m] = b;
+    row_pos[m] = m - start;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    int acc = 0, maxt = 0;
+    for (int b = 0; b < pm.batch; ++b) {
+      cu[b] = acc;
+      acc += pm.lens[b];
+      last_row[b] = acc - 1;
+      lens_dev[b] = pm.lens[b];
+      maxt = max(maxt, (pm.lens[b] + kAttnQTile - 1) / kAttnQTile);
+    }
+    cu[pm.batch] = acc;
+    // Longest causal work first: tile t of any sequence attends to (t + 1) * 64 keys.
+    int n = 0;
+    for (int t = maxt - 1; t >= 0; --t)
+      for (int b = 0; b < pm.batch; ++b)
+        if (t * kAttnQTile < pm.lens[b]) qtiles[n++] = make_int2(b, t);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_embed(int dtype, const int *tokens, int ntok, const void *table, int vocab,
+                        int d, float *x, int *err, hipStream_t s) {
+  if (ntok <= 0) return hipSuccess;
+  if (dtype == kF32)
+    hipLaunchKernelGGL(k_embed<float>, dim3(ntok), dim3(256), 0, s, tokens,
+                       reinterpret_cast<const float *>(table), vocab, d, x, err);
+  else
+    hipLaunchKernelGGL(k_embed<bf16>, dim3(ntok), dim3(256), 0, s, tokens,
+                       reinterpret_cast<const bf16 *>(table), vocab, d, x, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(int dtype, const float *x, int ldx, const int *rowmap, int rows, int d,
+                          const void *gain, float eps, void *y, int ldy, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (dtype == kF32)
+    hipLaunchKernelGGL(k_rmsnorm<float>, dim3(rows), dim3(256), 0, s, x, ldx, rowmap, d,
+                       reinterpret_cast<const float *>(gain), eps, reinterpret_cast<float *>(y),
+                       ldy);
+  else
+    hipLaunchKernelGGL(k_rmsnorm<bf16>, dim3(rows), dim3(256), 0, s, x, ldx, rowmap, d,
+                       reinterpret_cast<const bf16 *>(gain), eps, reinterpret_cast<bf16 *>(y),
+                       ldy);
+  return hipGetLastError();
+}
+
+hipError_t launch_argmax_reduce(const float *pval, const int *pidx, int rows, int n_parts,
+                                int *next, int *lens_inc, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_argmax_reduce, dim3(rows), dim3(256), 0, s, pval, pidx, n_parts, next,
+                     lens_inc);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_meta(const PrefillMeta &pm, int total, int *cu, int *row_seq,
+                               int *row_pos, int *last_row, int *lens_dev, int2 *qtiles,
+                               hipStream_t s) {
+  const int blocks = std::max(1, (total + 255) / 256);
+  hipLaunchKernelGGL(k_prefill_meta, dim3(blocks), dim3(256), 0, s, pm, total, cu, row_seq,
+                     row_pos, last_row, lens_dev, qtiles);
+  return hipGetLastError();
+}
+
+}  // namespace ll

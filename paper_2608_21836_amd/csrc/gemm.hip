@@ -1,0 +1,407 @@
+// Projection GEMMs of the decoder: C = A W^T with W in nn.Linear [out][in] layout.
+//
+//  * Weights are repacked once into 1 KiB tiles (16 output rows x one MFMA contraction chunk)
+//    stored in MFMA operand order, all tiles of a 16-row block contiguous along K.  A wave
+//    then fetches an operand with one fully coalesced 1 KiB read and LDS reads are
+//    conflict-free.
+//  * Prefill (M = prompt tokens): 128 x 128 block tiles, 4 waves of 64 x 64, double-buffered
+//    LDS, v_mfma_f32_16x16x32_bf16 (fp32 workloads: v_mfma_f32_16x16x4_f32).
+//  * Decode (M = batch <= 32 per launch): every weight byte is read once straight from HBM
+//    into MFMA B operands (non-temporal), A comes from L2; 8 waves split K, reduced in LDS.
+//  * Output columns come in units of 32 = two halves of 16 that land in the same lane, so the
+//    epilogues (RoPE pairs (i, i + hd/2), SwiGLU gate/up pairs) need no cross-lane traffic.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace ll {
+namespace {
+
+// ------------------------------------------------------------------------------------------
+// Repack
+// ------------------------------------------------------------------------------------------
+template <typename T>
+__global__ void k_repack(RepackSrc src, int n, int k, int perm, int hd, int ffn, uint8_t *wt) {
+  constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL;
+  const int kb_n = k / TK;
+  const size_t total = (size_t)n * k / EPL;  // 16-byte chunks
+  for (size_t c = (size_t)blockIdx.x * blockDim.x + threadIdx.x; c < total;
+       c += (size_t)gridDim.x * blockDim.x) {
+    const size_t tile = c >> 6;
+    const int ln = (int)(c & 63);
+    const int nb = (int)(tile / kb_n), kb = (int)(tile % kb_n);
+    const int nphys = nb * 16 + (ln & 15);
+    const int kk = kb * TK + (ln >> 4) * EPL;
+    int nlog = nphys;
+    if (perm == kPermRope) {
+      const int head = nphys / hd, within = nphys % hd;
+      const int j = within >> 5, half = (within >> 4) & 1, cc = within & 15;
+      nlog = head * hd + (half ? hd / 2 : 0) + 16 * j + cc;
+    } else if (perm == kPermGlu) {
+      const int u = nphys >> 5, half = (nphys >> 4) & 1, cc = nphys & 15;
+      nlog = half * ffn + 16 * u + cc;
+    }
+    int s = 0;
+    while (s < 2 && nlog >= src.rows[s]) nlog -= src.rows[s++];
+    const T *p = reinterpret_cast<const T *>(src.src[s]) + (size_t)nlog * k + kk;
+    *reinterpret_cast<uint4 *>(wt + c * 16) = *reinterpret_cast<const uint4 *>(p);
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Epilogues: called with (row m, 32-column unit u, lane column c, first-half value,
+// second-half value).
+// ------------------------------------------------------------------------------------------
+struct EpiStore {
+  float *out;
+  int ld;
+  static constexpr bool kArgmax = false;
+  __device__ void operator()(int m, int u, int c, float v0, float v1) const {
+    float *p = out + (size_t)m * ld + 32 * u + c;
+    p[0] = v0;
+    p[16] = v1;
+  }
+};
+
+struct EpiResid {
+  float *out;
+  int ld;
+  static constexpr bool kArgmax = false;
+  __device__ void operator()(int m, int u, int c, float v0, float v1) const {
+    float *p = out + (size_t)m * ld + 32 * u + c;
+    p[0] += v0;
+    p[16] += v1;
+  }
+};
+
+template <typename T> struct EpiSwiglu {
+  T *out;
+  int ld;
+  static constexpr bool kArgmax = false;
+  __device__ void operator()(int m, int u, int c, float g, float up) const {
+    out[(size_t)m * ld + 16 * u + c] = from_f32<T>(silu_f(g) * up);
+  }
+};
+
+template <typename T> struct EpiQkv {
+  T *q;
+  int ldq;
+  T *kc, *vc;
+  const int *row_seq, *row_pos;
+  const float *rcos, *rsin;
+  int hq, hkv, hd, max_ctx;
+  static constexpr bool kArgmax = false;
+  __device__ void operator()(int m, int u, int c, float v0, float v1) const {
+    const int n0 = u * 32;
+    const int head = n0 / hd;
+    const int j = (n0 - head * hd) >> 5;
+    const int half = hd >> 1;
+    const int i1 = 16 * j + c, i2 = half + i1;
+    const int pos = row_pos[m];
+    if (head < hq + hkv) {  // rotate-half RoPE on queries and keys
+      const float co = rcos[(size_t)pos * half + i1], si = rsin[(size_t)pos * half + i1];
+      const float a = v0 * co - v1 * si, b = v1 * co + v0 * si;
+      v0 = a;
+      v1 = b;
+    }
+    T *dst;
+    if (head < hq) {
+      dst = q + (size_t)m * ldq + head * hd;
+    } else {
+      const bool is_k = head < hq + hkv;
+      const int kvh = is_k ? head - hq : head - hq - hkv;
+      const int seq = row_seq ? row_seq[m] : m;
+      dst = (is_k ? kc : vc) + (((size_t)seq * hkv + kvh) * max_ctx + pos) * hd;
+    }
+    dst[i1] = from_f32<T>(v0);
+    dst[i2] = from_f32<T>(v1);
+  }
+};
+
+struct EpiArgmax {
+  float *logits;  // nullable
+  int ld;
+  float *pval;
+  int *pidx;
+  int n_parts;
+  static constexpr bool kArgmax = true;
+};
+
+// ------------------------------------------------------------------------------------------
+// Prefill GEMM
+// ------------------------------------------------------------------------------------------
+template <typename T, typename Epi>
+__global__ __launch_bounds__(256) void k_gemm_tiled(const T *__restrict__ A, int lda,
+                                                    const uint8_t *__restrict__ Wt, int M,
+                                                    int K, Epi epi) {
+  using F = typename Frag<T>::type;
+  constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL;
+  constexpr int BM = 128, BN = 128;
+  __shared__ uint4 sA[2][1024];  // [buf][(m-block * 2 + k-tile) * 64 + lane]
+  __shared__ uint4 sB[2][1024];  // [buf][(n-block * 2 + k-tile) * 64 + lane]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int kb_n = K / TK;
+  const int nsteps = kb_n / 2;
+  uint4 ra[4], rb[4];
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const uint8_t *wblk = Wt + (size_t)(n0 / 16) * kb_n * 1024;
+  auto gload = [&](int step) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = i * 256 + tid;
+      const int row = c >> 3, kc = c & 7;  // 8 chunks of 16 bytes per row and step
+      const int gm = m0 + row;
+      ra[i] = gm < M ? *reinterpret_cast<const uint4 *>(A + (size_t)gm * lda + step * 2 * TK +
+                                                        kc * EPL)
+                     : make_uint4(0u, 0u, 0u, 0u);
+      const int nbl = c >> 7, kbl = (c >> 6) & 1;
+      rb[i] = *reinterpret_cast<const uint4 *>(
+          wblk + (((size_t)nbl * kb_n + step * 2 + kbl) * 64 + (c & 63)) * 16);
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = i * 256 + tid;
+      const int row = c >> 3, kc = c & 7;
+      sA[buf][((row >> 4) * 2 + (kc >> 2)) * 64 + (row & 15) + 16 * (kc & 3)] = ra[i];
+      sB[buf][c] = rb[i];
+    }
+  };
+
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int step = 0; step < nsteps; ++step) {
+    const int cur = step & 1;
+    if (step + 1 < nsteps) gload(step + 1);
+#pragma unroll
+    for (int kbl = 0; kbl < 2; ++kbl) {
+      F a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        a[i] = *reinterpret_cast<const F *>(&sA[cur][((wm * 4 + i) * 2 + kbl) * 64 + lane]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        b[j] = *reinterpret_cast<const F *>(&sB[cur][((wn * 4 + j) * 2 + kbl) * 64 + lane]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mma_chunk(a[i], b[j], acc[i][j]);
+    }
+    if (step + 1 < nsteps) sstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  const int ubase = (n0 + wn * 64) >> 5;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + r;
+      if (m < M) {
+#pragma unroll
+        for (int p = 0; p < 2; ++p) epi(m, ubase + p, lane & 15, acc[i][2 * p][r], acc[i][2 * p + 1][r]);
+      }
+    }
+}
+
+// ------------------------------------------------------------------------------------------
+// Decode GEMM (one block per 32 output columns, 8 waves splitting K)
+// ------------------------------------------------------------------------------------------
+template <typename T, int MT, typename Epi>
+__global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, int lda,
+                                                     const uint8_t *__restrict__ Wt, int M,
+                                                     int m_base, int K, Epi epi) {
+  using F = typename Frag<T>::type;
+  constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL, NW = 8, U = 4;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int u = blockIdx.x;
+  const int kb_n = K / TK;
+  const int kb0 = (wave * kb_n) / NW, kb1 = ((wave + 1) * kb_n) / NW;
+  const uint8_t *w0 = Wt + ((size_t)(2 * u) * kb_n * 64 + lane) * 16;
+  const uint8_t *w1 = w0 + (size_t)kb_n * 1024;
+
+  f32x4 acc[MT][2];
+  const T *arow[MT];
+  bool aok[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    acc[mt][0] = acc[mt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int row = m_base + mt * 16 + (lane & 15);
+    aok[mt] = row < M;
+    arow[mt] = A + (size_t)(aok[mt] ? row : 0) * lda + (lane >> 4) * EPL;
+  }
+  const F fz = frag_zero<F>();
+  int kb = kb0;
+  for (; kb + U <= kb1; kb += U) {
+    F b0[U], b1[U];
+#pragma unroll
+    for (int q = 0; q < U; ++q) {
+      b0[q] = load_frag_stream<F>(w0 + (size_t)(kb + q) * 1024);
+      b1[q] = load_frag_stream<F>(w1 + (size_t)(kb + q) * 1024);
+    }
+#pragma unroll
+    for (int q = 0; q < U; ++q)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const F a = aok[mt] ? load_frag<F>(arow[mt] + (size_t)(kb + q) * TK) : fz;
+        acc[mt][0] = mma_chunk(a, b0[q], acc[mt][0]);
+        acc[mt][1] = mma_chunk(a, b1[q], acc[mt][1]);
+      }
+  }
+  for (; kb < kb1; ++kb) {
+    const F b0 = load_frag_stream<F>(w0 + (size_t)kb * 1024);
+    const F b1 = load_frag_stream<F>(w1 + (size_t)kb * 1024);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const F a = aok[mt] ? load_frag<F>(arow[mt] + (size_t)kb * TK) : fz;
+      acc[mt][0] = mma_chunk(a, b0, acc[mt][0]);
+      acc[mt][1] = mma_chunk(a, b1, acc[mt][1]);
+    }
+  }
+
+  __shared__ f32x4 red[NW][MT * 2][64];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    red[wave][mt * 2][lane] = acc[mt][0];
+    red[wave][mt * 2 + 1][lane] = acc[mt][1];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    f32x4 s0 = red[0][mt * 2][lane], s1 = red[0][mt * 2 + 1][lane];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) {
+      s0 += red[w][mt * 2][lane];
+      s1 += red[w][mt * 2 + 1][lane];
+    }
+    const int c = lane & 15;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = m_base + mt * 16 + (lane >> 4) * 4 + r;
+      if constexpr (Epi::kArgmax) {
+        const int col0 = 32 * u + c;
+        if (m < M && epi.logits) {
+          epi.logits[(size_t)m * epi.ld + col0] = s0[r];
+          epi.logits[(size_t)m * epi.ld + col0 + 16] = s1[r];
+        }
+        float bv = s0[r];
+        int bi = col0;
+        if (s1[r] > bv) {
+          bv = s1[r];
+          bi = col0 + 16;
+        }
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) {
+          const float ov = __shfl_xor(bv, o);
+          const int oi = __shfl_xor(bi, o);
+          if (ov > bv || (ov == bv && oi < bi)) {
+            bv = ov;
+            bi = oi;
+          }
+        }
+        if (m < M && c == 0) {
+          epi.pval[(size_t)m * epi.n_parts + u] = bv;
+          epi.pidx[(size_t)m * epi.n_parts + u] = bi;
+        }
+      } else {
+        if (m < M) epi(m, u, c, s0[r], s1[r]);
+      }
+    }
+  }
+}
+
+template <typename T, typename Epi>
+hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k, const Epi &epi,
+                     hipStream_t s) {
+  dim3 grid(n / 128, (m + 127) / 128);
+  hipLaunchKernelGGL((k_gemm_tiled<T, Epi>), grid, dim3(256), 0, s,
+                     reinterpret_cast<const T *>(a), lda,
+                     reinterpret_cast<const uint8_t *>(wt), m, k, epi);
+  return hipGetLastError();
+}
+
+template <typename T, typename Epi>
+hipError_t run_skinny(const void *a, int lda, const void *wt, int m, int n, int k, const Epi &epi,
+                      hipStream_t s) {
+  const T *ap = reinterpret_cast<const T *>(a);
+  const uint8_t *w = reinterpret_cast<const uint8_t *>(wt);
+  for (int mb = 0; mb < m; mb += 32) {
+    const int rows = m - mb;
+    if (rows <= 16)
+      hipLaunchKernelGGL((k_gemm_skinny<T, 1, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, w,
+                         m, mb, k, epi);
+    else
+      hipLaunchKernelGGL((k_gemm_skinny<T, 2, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, w,
+                         m, mb, k, epi);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+template <typename T, bool kTiled>
+hipError_t dispatch_epi(const void *a, int lda, const void *wt, int m, int n, int k,
+                        const EpiParams &ep, hipStream_t s) {
+  auto run = [&](const auto &epi) {
+    using E = std::decay_t<decltype(epi)>;
+    if constexpr (kTiled) {
+      if constexpr (E::kArgmax) return hipErrorInvalidValue;
+      else return run_tiled<T>(a, lda, wt, m, n, k, epi, s);
+    } else {
+      return run_skinny<T>(a, lda, wt, m, n, k, epi, s);
+    }
+  };
+  switch (ep.kind) {
+    case kEpiStore: return run(EpiStore{ep.out_f32, ep.ld_out});
+    case kEpiResid: return run(EpiResid{ep.out_f32, ep.ld_out});
+    case kEpiSwiglu: return run(EpiSwiglu<T>{reinterpret_cast<T *>(ep.act), ep.ld_act});
+    case kEpiQkv:
+      return run(EpiQkv<T>{reinterpret_cast<T *>(ep.act), ep.ld_act,
+                           reinterpret_cast<T *>(ep.kcache), reinterpret_cast<T *>(ep.vcache),
+                           ep.row_seq, ep.row_pos, ep.rope_cos, ep.rope_sin, ep.n_heads,
+                           ep.n_kv_heads, ep.head_dim, ep.max_ctx});
+    case kEpiArgmax:
+      return run(EpiArgmax{ep.out_f32, ep.ld_out, ep.part_val, ep.part_idx, ep.n_parts});
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_repack(int dtype, const RepackSrc &src, int n, int k, int perm, int head_dim,
+                         int ffn_dim, void *wt, hipStream_t s) {
+  const size_t chunks = (size_t)n * k * elem_bytes(dtype) / 16;
+  const int blocks = (int)std::min<size_t>((chunks + 255) / 256, 65536);
+  if (dtype == kF32)
+    hipLaunchKernelGGL(k_repack<float>, dim3(blocks), dim3(256), 0, s, src, n, k, perm,
+                       head_dim, ffn_dim, reinterpret_cast<uint8_t *>(wt));
+  else
+    hipLaunchKernelGGL(k_repack<bf16>, dim3(blocks), dim3(256), 0, s, src, n, k, perm,
+                       head_dim, ffn_dim, reinterpret_cast<uint8_t *>(wt));
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, int m, int n,
+                             int k, const EpiParams &ep, hipStream_t s) {
+  if (m <= 0) return hipSuccess;
+  return dtype == kF32 ? dispatch_epi<float, true>(a, lda, wt, m, n, k, ep, s)
+                       : dispatch_epi<bf16, true>(a, lda, wt, m, n, k, ep, s);
+}
+
+hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const void *wt, int m, int n,
+                              int k, const EpiParams &ep, hipStream_t s) {
+  if (m <= 0) return hipSuccess;
+  return dtype == kF32 ? dispatch_epi<float, false>(a, lda, wt, m, n, k, ep, s)
+                       : dispatch_epi<bf16, false>(a, lda, wt, m, n, k, ep, s);
+}
+
+}  // namespace ll

@@ -1,0 +1,100 @@
+// Host-side launch interface of the gfx950 kernels (implemented in the .hip files).
+// Every launcher enqueues on `s`, checks hipGetLastError and returns hipSuccess or the error.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ll {
+
+enum DType : int { kF32 = 0, kBF16 = 1 };
+
+inline size_t elem_bytes(int dtype) { return dtype == kF32 ? 4 : 2; }
+
+// Contraction-axis span of one 1 KiB weight tile (16 rows): 32 bf16 or 16 fp32 elements.
+inline int tile_k(int dtype) { return dtype == kF32 ? 16 : 32; }
+
+// Row order of a repacked weight.  Output columns are produced in units of 32 "physical"
+// columns: a first half of 16 and a second half of 16 that land in the same lanes, so an
+// epilogue can combine the two without moving data between lanes.
+enum RepackPerm : int {
+  kPermNone = 0,  // physical column == logical row
+  kPermRope = 1,  // per head of hd: unit j = dims [16j, 16j+16) | [hd/2 + 16j, hd/2 + 16j + 16)
+  kPermGlu = 2,   // unit u = gate rows [16u, 16u+16) | up rows [16u, 16u+16)
+};
+
+// Up to three row-major sources stacked along N (e.g. W_q, W_k, W_v), then permuted.
+struct RepackSrc {
+  const void *src[3];
+  int rows[3];
+};
+
+hipError_t launch_repack(int dtype, const RepackSrc &src, int n, int k, int perm, int head_dim,
+                         int ffn_dim, void *wt, hipStream_t s);
+
+enum EpiKind : int {
+  kEpiStore = 0,   // out_f32[m, n] = acc
+  kEpiResid = 1,   // out_f32[m, n] += acc   (residual stream update)
+  kEpiSwiglu = 2,  // act[m, j] = silu(gate) * up   (kPermGlu weights)
+  kEpiQkv = 3,     // RoPE on q, k; q -> act, k / v -> KV cache  (kPermRope weights)
+  kEpiArgmax = 4,  // logits (optional) + per-32-column (max, argmax) partials
+};
+
+struct EpiParams {
+  int kind = kEpiStore;
+  float *out_f32 = nullptr;  // Store / Resid target, Argmax logits (nullable)
+  int ld_out = 0;
+  void *act = nullptr;       // Swiglu output, Qkv query output (element type T)
+  int ld_act = 0;
+  // Qkv
+  void *kcache = nullptr, *vcache = nullptr;  // [max_batch][n_kv][max_ctx][hd] of this layer
+  const int *row_seq = nullptr;  // sequence of each row (nullptr: row index)
+  const int *row_pos = nullptr;  // position of each row
+  const float *rope_cos = nullptr, *rope_sin = nullptr;  // [max_ctx][hd/2]
+  int n_heads = 0, n_kv_heads = 0, head_dim = 0, max_ctx = 0;
+  // Argmax
+  float *part_val = nullptr;
+  int *part_idx = nullptr;
+  int n_parts = 0;  // partials per row (= N / 32)
+};
+
+// Prefill GEMM: LDS-tiled MFMA, 128 x 128 block tiles.  Requires N % 128 == 0, K % 64 == 0.
+hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, int m, int n,
+                             int k, const EpiParams &ep, hipStream_t s);
+// Decode GEMM: weights streamed once from HBM into MFMA operands, A read from L2.
+// Requires N % 32 == 0, K % 64 == 0; any M (rows handled 32 at a time).
+hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const void *wt, int m, int n,
+                              int k, const EpiParams &ep, hipStream_t s);
+
+hipError_t launch_embed(int dtype, const int *tokens, int ntok, const void *table, int vocab,
+                        int d, float *x, int *err_flags, hipStream_t s);
+hipError_t launch_rmsnorm(int dtype, const float *x, int ldx, const int *rowmap, int rows,
+                          int d, const void *gain, float eps, void *y, int ldy, hipStream_t s);
+hipError_t launch_argmax_reduce(const float *part_val, const int *part_idx, int rows,
+                                int n_parts, int *next, int *lens_inc, hipStream_t s);
+
+// Prefill metadata from host lengths (passed by value): cu_seqlens[B+1], row_seq[T],
+// row_pos[T], last_row[B], lens[B] and the query-tile list ordered by decreasing causal work.
+struct PrefillMeta {
+  int batch;
+  int lens[256];
+};
+hipError_t launch_prefill_meta(const PrefillMeta &pm, int total, int *cu_seqlens, int *row_seq,
+                               int *row_pos, int *last_row, int *lens_dev, int2 *qtiles,
+                               hipStream_t s);
+constexpr int kAttnQTile = 64;  // queries per prefill-attention block
+
+hipError_t launch_attn_prefill(int dtype, int head_dim, const void *q, int ldq,
+                               const void *kcache, const void *vcache, void *o, int ldo,
+                               const int *cu_seqlens, const int2 *qtiles, int n_qtiles,
+                               int n_heads, int n_kv_heads, int max_ctx, hipStream_t s);
+
+// Decode attention: split over the cache length (chunk keys per block) + combine.
+int attn_decode_chunk(int batch, int n_kv_heads, int max_ctx);
+hipError_t launch_attn_decode(int dtype, int head_dim, const void *q, int ldq,
+                              const void *kcache, const void *vcache, const int *lens,
+                              int len_add, void *o, int ldo, int batch, int n_heads,
+                              int n_kv_heads, int max_ctx, int chunk, float *part_o,
+                              float *part_ml, hipStream_t s);
+
+}  // namespace ll

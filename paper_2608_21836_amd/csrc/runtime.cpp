@@ -1,0 +1,660 @@
+// C-ABI runtime: config validation, workspace layout, weight repacking, phase dispatch
+// (prefill vs decode, Sec. 2.1 and Sec. 3.1 of the paper), decode-step HIP graphs and the
+// per-kernel entry points of ll_ops.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "ll.h"
+#include "ll_ops.h"
+
+using namespace ll;
+
+namespace {
+
+thread_local std::string g_err;
+
+ll_status fail(ll_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define LL_HIP(expr)                                                                  \
+  do {                                                                                \
+    hipError_t e_ = (expr);                                                           \
+    if (e_ != hipSuccess)                                                             \
+      return fail(LL_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));         \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Layout {
+  size_t embed = 0, final_norm = 0, lm_head = 0;
+  std::vector<size_t> wqkv, wo, wgu, wd, attn_norm, mlp_norm;
+  size_t kcache = 0, vcache = 0, rcos = 0, rsin = 0;
+  size_t x = 0, h = 0, q = 0, o = 0, act = 0, hf = 0;
+  size_t part_o = 0, part_ml = 0, pval = 0, pidx = 0;
+  size_t cu = 0, row_seq = 0, row_pos = 0, last_row = 0, lens = 0, qtiles = 0, err = 0;
+  size_t total = 0;
+  size_t kv_layer_elems = 0;
+  int chunk = 0, nsplit = 0, n_parts = 0, max_rows = 0, n_qkv = 0;
+};
+
+ll_status validate_config(const ll_config *c) {
+  if (!c) return fail(LL_ERR_INVALID_ARGUMENT, "cfg is NULL");
+  if (c->n_layers < 1 || c->d_model < 1 || c->n_heads < 1 || c->n_kv_heads < 1 ||
+      c->head_dim < 1 || c->ffn_dim < 1 || c->vocab < 1)
+    return fail(LL_ERR_INVALID_ARGUMENT, "model dimensions must be positive");
+  if (c->max_batch < 1 || c->max_prefill_tokens < 1 || c->max_ctx < 1)
+    return fail(LL_ERR_INVALID_ARGUMENT, "capacities must be positive");
+  if (!(c->rms_eps >= 0.f) || !std::isfinite(c->rms_eps))
+    return fail(LL_ERR_INVALID_ARGUMENT, "rms_eps must be finite and >= 0");
+  if (!(c->rope_theta > 0.0) || !std::isfinite(c->rope_theta))
+    return fail(LL_ERR_INVALID_ARGUMENT, "rope_theta must be finite and > 0");
+  if (c->dtype != LL_F32 && c->dtype != LL_BF16)
+    return fail(LL_ERR_UNSUPPORTED, "dtype %d unknown", c->dtype);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(LL_ERR_UNSUPPORTED, "head_dim %d not in {64, 128}", c->head_dim);
+  if (c->n_heads % c->n_kv_heads)
+    return fail(LL_ERR_UNSUPPORTED, "n_heads %d not a multiple of n_kv_heads %d", c->n_heads,
+                c->n_kv_heads);
+  const int g = c->n_heads / c->n_kv_heads;
+  if (g != 1 && g != 2 && g != 4 && g != 8)
+    return fail(LL_ERR_UNSUPPORTED, "head group %d not in {1, 2, 4, 8}", g);
+  if (c->d_model % 128)
+    return fail(LL_ERR_UNSUPPORTED, "d_model %d not a multiple of 128", c->d_model);
+  if (((c->n_heads + 2 * c->n_kv_heads) * c->head_dim) % 128)
+    return fail(LL_ERR_UNSUPPORTED, "(n_heads + 2 n_kv_heads) * head_dim not a multiple of 128");
+  if (c->ffn_dim % 64)
+    return fail(LL_ERR_UNSUPPORTED, "ffn_dim %d not a multiple of 64", c->ffn_dim);
+  if (c->vocab % 32) return fail(LL_ERR_UNSUPPORTED, "vocab %d not a multiple of 32", c->vocab);
+  if (c->max_batch > LL_MAX_BATCH)
+    return fail(LL_ERR_UNSUPPORTED, "max_batch %d > %d", c->max_batch, LL_MAX_BATCH);
+  return LL_OK;
+}
+
+Layout make_layout(const ll_config &c) {
+  Layout L;
+  const size_t eb = elem_bytes(c.dtype);
+  const size_t d = c.d_model, qd = (size_t)c.n_heads * c.head_dim;
+  L.n_qkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
+  L.max_rows = std::max(c.max_prefill_tokens, c.max_batch);
+  L.chunk = attn_decode_chunk(c.max_batch, c.n_kv_heads, c.max_ctx);
+  L.nsplit = (c.max_ctx + L.chunk - 1) / L.chunk;
+  L.n_parts = c.vocab / 32;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  L.embed = take((size_t)c.vocab * d * eb);
+  for (int l = 0; l < c.n_layers; ++l) {
+    L.wqkv.push_back(take((size_t)L.n_qkv * d * eb));
+    L.wo.push_back(take(d * qd * eb));
+    L.wgu.push_back(take(2 * (size_t)c.ffn_dim * d * eb));
+    L.wd.push_back(take(d * c.ffn_dim * eb));
+    L.attn_norm.push_back(take(d * eb));
+    L.mlp_norm.push_back(take(d * eb));
+  }
+  L.final_norm = take(d * eb);
+  L.lm_head = take((size_t)c.vocab * d * eb);
+  L.kv_layer_elems = (size_t)c.max_batch * c.n_kv_heads * c.max_ctx * c.head_dim;
+  L.kcache = take(L.kv_layer_elems * c.n_layers * eb);
+  L.vcache = take(L.kv_layer_elems * c.n_layers * eb);
+  L.rcos = take((size_t)c.max_ctx * (c.head_dim / 2) * 4);
+  L.rsin = take((size_t)c.max_ctx * (c.head_dim / 2) * 4);
+  const size_t R = L.max_rows;
+  L.x = take(R * d * 4);
+  L.h = take(R * d * eb);
+  L.q = take(R * qd * eb);
+  L.o = take(R * qd * eb);
+  L.act = take(R * c.ffn_dim * eb);
+  L.hf = take((size_t)c.max_batch * d * eb);
+  L.part_o = take((size_t)c.max_batch * c.n_heads * L.nsplit * c.head_dim * 4);
+  L.part_ml = take((size_t)c.max_batch * c.n_heads * L.nsplit * 2 * 4);
+  L.pval = take((size_t)c.max_batch * L.n_parts * 4);
+  L.pidx = take((size_t)c.max_batch * L.n_parts * 4);
+  L.cu = take((c.max_batch + 1) * 4);
+  L.row_seq = take(R * 4);
+  L.row_pos = take(R * 4);
+  L.last_row = take(c.max_batch * 4);
+  L.lens = take(c.max_batch * 4);
+  L.qtiles = take((R / kAttnQTile + c.max_batch + 1) * 8);
+  L.err = take(4);
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+
+struct ll_model {
+  ll_config cfg;
+  Layout L;
+  char *ws = nullptr;
+  hipStream_t stream = nullptr;
+  hipStream_t cap_stream = nullptr;  // records decode graphs (graphs then run on `stream`)
+  int batch = 0;
+  std::vector<int> lens;
+  bool use_graph = true;
+  struct Graph {
+    const void *in;
+    void *out;
+    void *logits;
+    int batch;
+    hipGraphExec_t exec;
+  };
+  std::vector<Graph> graphs;
+  std::vector<float> rope_host;
+
+  template <typename P = void> P *at(size_t off) const { return reinterpret_cast<P *>(ws + off); }
+  void *kc(int l) const { return ws + L.kcache + L.kv_layer_elems * l * elem_bytes(cfg.dtype); }
+  void *vc(int l) const { return ws + L.vcache + L.kv_layer_elems * l * elem_bytes(cfg.dtype); }
+  void drop_graphs() {
+    for (auto &g : graphs) (void)hipGraphExecDestroy(g.exec);
+    graphs.clear();
+  }
+};
+
+namespace {
+
+EpiParams qkv_epi(const ll_model *m, int l, const int *row_seq, const int *row_pos) {
+  EpiParams ep;
+  ep.kind = kEpiQkv;
+  ep.act = m->at(m->L.q);
+  ep.ld_act = m->cfg.n_heads * m->cfg.head_dim;
+  ep.kcache = m->kc(l);
+  ep.vcache = m->vc(l);
+  ep.row_seq = row_seq;
+  ep.row_pos = row_pos;
+  ep.rope_cos = m->at<float>(m->L.rcos);
+  ep.rope_sin = m->at<float>(m->L.rsin);
+  ep.n_heads = m->cfg.n_heads;
+  ep.n_kv_heads = m->cfg.n_kv_heads;
+  ep.head_dim = m->cfg.head_dim;
+  ep.max_ctx = m->cfg.max_ctx;
+  return ep;
+}
+
+EpiParams resid_epi(const ll_model *m) {
+  EpiParams ep;
+  ep.kind = kEpiResid;
+  ep.out_f32 = m->at<float>(m->L.x);
+  ep.ld_out = m->cfg.d_model;
+  return ep;
+}
+
+EpiParams swiglu_epi(const ll_model *m) {
+  EpiParams ep;
+  ep.kind = kEpiSwiglu;
+  ep.act = m->at(m->L.act);
+  ep.ld_act = m->cfg.ffn_dim;
+  return ep;
+}
+
+EpiParams argmax_epi(const ll_model *m, float *logits) {
+  EpiParams ep;
+  ep.kind = kEpiArgmax;
+  ep.out_f32 = logits;
+  ep.ld_out = m->cfg.vocab;
+  ep.part_val = m->at<float>(m->L.pval);
+  ep.part_idx = m->at<int>(m->L.pidx);
+  ep.n_parts = m->L.n_parts;
+  return ep;
+}
+
+// The decoder layers for `rows` rows.  decode: one row per sequence at position len[b].
+ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipStream_t s) {
+  const ll_config &c = m->cfg;
+  const int d = c.d_model, qd = c.n_heads * c.head_dim, F = c.ffn_dim;
+  const int dt = c.dtype;
+  auto gemm = decode ? launch_gemm_skinny : launch_gemm_tiled;
+  float *x = m->at<float>(m->L.x);
+  for (int l = 0; l < c.n_layers; ++l) {
+    LL_HIP(launch_rmsnorm(dt, x, d, nullptr, rows, d, m->at(m->L.attn_norm[l]), c.rms_eps,
+                          m->at(m->L.h), d, s));
+    const int *row_seq = decode ? nullptr : m->at<int>(m->L.row_seq);
+    const int *row_pos = decode ? m->at<int>(m->L.lens) : m->at<int>(m->L.row_pos);
+    LL_HIP(gemm(dt, m->at(m->L.h), d, m->at(m->L.wqkv[l]), rows, m->L.n_qkv, d,
+                qkv_epi(m, l, row_seq, row_pos), s));
+    if (decode) {
+      LL_HIP(launch_attn_decode(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
+                                m->at<int>(m->L.lens), 1, m->at(m->L.o), qd, rows, c.n_heads,
+                                c.n_kv_heads, c.max_ctx, m->L.chunk, m->at<float>(m->L.part_o),
+                                m->at<float>(m->L.part_ml), s));
+    } else {
+      LL_HIP(launch_attn_prefill(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
+                                 m->at(m->L.o), qd, m->at<int>(m->L.cu),
+                                 m->at<int2>(m->L.qtiles), n_qtiles, c.n_heads, c.n_kv_heads,
+                                 c.max_ctx, s));
+    }
+    LL_HIP(gemm(dt, m->at(m->L.o), qd, m->at(m->L.wo[l]), rows, d, qd, resid_epi(m), s));
+    LL_HIP(launch_rmsnorm(dt, x, d, nullptr, rows, d, m->at(m->L.mlp_norm[l]), c.rms_eps,
+                          m->at(m->L.h), d, s));
+    LL_HIP(gemm(dt, m->at(m->L.h), d, m->at(m->L.wgu[l]), rows, 2 * F, d, swiglu_epi(m), s));
+    LL_HIP(gemm(dt, m->at(m->L.act), F, m->at(m->L.wd[l]), rows, d, F, resid_epi(m), s));
+  }
+  return LL_OK;
+}
+
+// Final RMSNorm of one row per sequence, LM head with fused argmax partials, reduction.
+ll_status enqueue_head(ll_model *m, int batch, const int *rowmap, int *next, float *logits,
+                       int *lens_inc, hipStream_t s) {
+  const ll_config &c = m->cfg;
+  LL_HIP(launch_rmsnorm(c.dtype, m->at<float>(m->L.x), c.d_model, rowmap, batch, c.d_model,
+                        m->at(m->L.final_norm), c.rms_eps, m->at(m->L.hf), c.d_model, s));
+  LL_HIP(launch_gemm_skinny(c.dtype, m->at(m->L.hf), c.d_model, m->at(m->L.lm_head), batch,
+                            c.vocab, c.d_model, argmax_epi(m, logits), s));
+  LL_HIP(launch_argmax_reduce(m->at<float>(m->L.pval), m->at<int>(m->L.pidx), batch,
+                              m->L.n_parts, next, lens_inc, s));
+  return LL_OK;
+}
+
+ll_status enqueue_decode(ll_model *m, const int32_t *in, int32_t *out, float *logits,
+                         hipStream_t s) {
+  const ll_config &c = m->cfg;
+  LL_HIP(launch_embed(c.dtype, in, m->batch, m->at(m->L.embed), c.vocab, c.d_model,
+                      m->at<float>(m->L.x), m->at<int>(m->L.err), s));
+  ll_status st = enqueue_layers(m, m->batch, true, 0, s);
+  if (st != LL_OK) return st;
+  return enqueue_head(m, m->batch, nullptr, out, logits, m->at<int>(m->L.lens), s);
+}
+
+ll_status check_ws(const void *p) {
+  if (!p) return fail(LL_ERR_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(p) % kAlign)
+    return fail(LL_ERR_WORKSPACE, "workspace not %zu-byte aligned", kAlign);
+  return LL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *ll_last_error(void) { return g_err.c_str(); }
+
+ll_status ll_workspace_size(const ll_config *cfg, size_t *bytes) {
+  g_err.clear();
+  if (!bytes) return fail(LL_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  ll_status st = validate_config(cfg);
+  if (st != LL_OK) return st;
+  *bytes = make_layout(*cfg).total;
+  return LL_OK;
+}
+
+ll_status ll_model_load(const ll_config *cfg, const ll_weights *w, void *workspace,
+                        size_t workspace_bytes, void *hip_stream, ll_model **out) {
+  g_err.clear();
+  if (!out) return fail(LL_ERR_INVALID_ARGUMENT, "out is NULL");
+  *out = nullptr;
+  ll_status st = validate_config(cfg);
+  if (st != LL_OK) return st;
+  if (!w) return fail(LL_ERR_INVALID_ARGUMENT, "weights is NULL");
+  if (!w->tok_embed || !w->final_norm || !w->lm_head)
+    return fail(LL_ERR_INVALID_ARGUMENT, "tok_embed, final_norm and lm_head must be set");
+  const void *const *arrays[] = {w->attn_norm, w->wq, w->wk, w->wv, w->wo,
+                                 w->mlp_norm, w->w_gate, w->w_up, w->w_down};
+  for (auto a : arrays) {
+    if (!a) return fail(LL_ERR_INVALID_ARGUMENT, "a per-layer weight array is NULL");
+    for (int l = 0; l < cfg->n_layers; ++l)
+      if (!a[l]) return fail(LL_ERR_INVALID_ARGUMENT, "layer %d weight pointer is NULL", l);
+  }
+  if ((st = check_ws(workspace)) != LL_OK) return st;
+  const Layout L = make_layout(*cfg);
+  if (workspace_bytes < L.total)
+    return fail(LL_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, L.total);
+
+  ll_model *m = new ll_model();
+  m->cfg = *cfg;
+  m->L = L;
+  m->ws = reinterpret_cast<char *>(workspace);
+  m->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  const ll_config &c = *cfg;
+  const size_t eb = elem_bytes(c.dtype);
+  const int d = c.d_model, qd = c.n_heads * c.head_dim, kvd = c.n_kv_heads * c.head_dim;
+  hipStream_t s = m->stream;
+  auto bail = [&](ll_status e) {
+    delete m;
+    return e;
+  };
+#define LOAD_HIP(expr)                                                                    \
+  do {                                                                                    \
+    hipError_t e_ = (expr);                                                               \
+    if (e_ != hipSuccess)                                                                 \
+      return bail(fail(LL_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_)));       \
+  } while (0)
+
+  LOAD_HIP(hipMemcpyAsync(m->at(L.embed), w->tok_embed, (size_t)c.vocab * d * eb,
+                          hipMemcpyDeviceToDevice, s));
+  LOAD_HIP(hipMemcpyAsync(m->at(L.final_norm), w->final_norm, d * eb, hipMemcpyDeviceToDevice, s));
+  for (int l = 0; l < c.n_layers; ++l) {
+    RepackSrc qkv{{w->wq[l], w->wk[l], w->wv[l]}, {qd, kvd, kvd}};
+    LOAD_HIP(launch_repack(c.dtype, qkv, L.n_qkv, d, kPermRope, c.head_dim, c.ffn_dim,
+                           m->at(L.wqkv[l]), s));
+    RepackSrc wo{{w->wo[l], nullptr, nullptr}, {d, 0, 0}};
+    LOAD_HIP(launch_repack(c.dtype, wo, d, qd, kPermNone, c.head_dim, c.ffn_dim, m->at(L.wo[l]), s));
+    RepackSrc gu{{w->w_gate[l], w->w_up[l], nullptr}, {c.ffn_dim, c.ffn_dim, 0}};
+    LOAD_HIP(launch_repack(c.dtype, gu, 2 * c.ffn_dim, d, kPermGlu, c.head_dim, c.ffn_dim,
+                           m->at(L.wgu[l]), s));
+    RepackSrc wd{{w->w_down[l], nullptr, nullptr}, {d, 0, 0}};
+    LOAD_HIP(launch_repack(c.dtype, wd, d, c.ffn_dim, kPermNone, c.head_dim, c.ffn_dim,
+                           m->at(L.wd[l]), s));
+    LOAD_HIP(hipMemcpyAsync(m->at(L.attn_norm[l]), w->attn_norm[l], d * eb,
+                            hipMemcpyDeviceToDevice, s));
+    LOAD_HIP(hipMemcpyAsync(m->at(L.mlp_norm[l]), w->mlp_norm[l], d * eb,
+                            hipMemcpyDeviceToDevice, s));
+  }
+  RepackSrc lm{{w->lm_head, nullptr, nullptr}, {c.vocab, 0, 0}};
+  LOAD_HIP(launch_repack(c.dtype, lm, c.vocab, d, kPermNone, c.head_dim, c.ffn_dim,
+                         m->at(L.lm_head), s));
+  // RoPE table in fp64 on the host, stored as fp32: [pos][i] = cos / sin(pos * theta^(-2i/hd)).
+  const int half = c.head_dim / 2;
+  m->rope_host.resize((size_t)2 * c.max_ctx * half);
+  float *hc = m->rope_host.data(), *hs = hc + (size_t)c.max_ctx * half;
+  for (int p = 0; p < c.max_ctx; ++p)
+    for (int i = 0; i < half; ++i) {
+      const double ang = (double)p * std::pow(c.rope_theta, -2.0 * i / c.head_dim);
+      hc[(size_t)p * half + i] = (float)std::cos(ang);
+      hs[(size_t)p * half + i] = (float)std::sin(ang);
+    }
+  LOAD_HIP(hipMemcpyAsync(m->at(L.rcos), hc, (size_t)c.max_ctx * half * 4, hipMemcpyHostToDevice, s));
+  LOAD_HIP(hipMemcpyAsync(m->at(L.rsin), hs, (size_t)c.max_ctx * half * 4, hipMemcpyHostToDevice, s));
+  LOAD_HIP(hipMemsetAsync(m->at(L.err), 0, 4, s));
+#undef LOAD_HIP
+  *out = m;
+  return LL_OK;
+}
+
+ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
+                     const int32_t *tokens_dev, int32_t *next_tokens_dev, float *logits_dev) {
+  g_err.clear();
+  if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
+  if (!seq_lens_host || !tokens_dev || !next_tokens_dev)
+    return fail(LL_ERR_INVALID_ARGUMENT, "seq_lens_host, tokens_dev and next_tokens_dev must be set");
+  if (batch < 1) return fail(LL_ERR_INVALID_ARGUMENT, "batch %d < 1", batch);
+  const ll_config &c = m->cfg;
+  if (batch > c.max_batch) return fail(LL_ERR_CAPACITY, "batch %d > max_batch %d", batch, c.max_batch);
+  if (m->batch != 0) return fail(LL_ERR_STATE, "prefill on a non-empty cache (call ll_kv_reset)");
+  long total = 0;
+  int n_qtiles = 0;
+  PrefillMeta pm;
+  pm.batch = batch;
+  for (int b = 0; b < batch; ++b) {
+    const int L = seq_lens_host[b];
+    if (L < 1) return fail(LL_ERR_INVALID_ARGUMENT, "seq_lens[%d] = %d < 1", b, L);
+    if (L > c.max_ctx) return fail(LL_ERR_CAPACITY, "seq_lens[%d] = %d > max_ctx %d", b, L, c.max_ctx);
+    total += L;
+    n_qtiles += (L + kAttnQTile - 1) / kAttnQTile;
+    pm.lens[b] = L;
+  }
+  if (total > c.max_prefill_tokens)
+    return fail(LL_ERR_CAPACITY, "%ld prompt tokens > max_prefill_tokens %d", total, c.max_prefill_tokens);
+  const int T = (int)total;
+  hipStream_t s = m->stream;
+  const Layout &L = m->L;
+  LL_HIP(launch_prefill_meta(pm, T, m->at<int>(L.cu), m->at<int>(L.row_seq), m->at<int>(L.row_pos),
+                             m->at<int>(L.last_row), m->at<int>(L.lens), m->at<int2>(L.qtiles), s));
+  LL_HIP(launch_embed(c.dtype, tokens_dev, T, m->at(L.embed), c.vocab, c.d_model,
+                      m->at<float>(L.x), m->at<int>(L.err), s));
+  ll_status st = enqueue_layers(m, T, false, n_qtiles, s);
+  if (st != LL_OK) return st;
+  st = enqueue_head(m, batch, m->at<int>(L.last_row), next_tokens_dev, logits_dev, nullptr, s);
+  if (st != LL_OK) return st;
+  m->batch = batch;
+  m->lens.assign(seq_lens_host, seq_lens_host + batch);
+  return LL_OK;
+}
+
+ll_status ll_decode_step(ll_model *m, const int32_t *in_tokens_dev, int32_t *next_tokens_dev,
+                         float *logits_dev) {
+  g_err.clear();
+  if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
+  if (!in_tokens_dev || !next_tokens_dev)
+    return fail(LL_ERR_INVALID_ARGUMENT, "in_tokens_dev and next_tokens_dev must be set");
+  if (m->batch == 0) return fail(LL_ERR_STATE, "decode before prefill");
+  for (int b = 0; b < m->batch; ++b)
+    if (m->lens[b] + 1 > m->cfg.max_ctx)
+      return fail(LL_ERR_CAPACITY, "sequence %d at length %d is full (max_ctx %d)", b, m->lens[b],
+                  m->cfg.max_ctx);
+  if (m->use_graph) {
+    hipGraphExec_t exec = nullptr;
+    for (auto &g : m->graphs)
+      if (g.in == in_tokens_dev && g.out == next_tokens_dev && g.logits == logits_dev &&
+          g.batch == m->batch)
+        exec = g.exec;
+    if (!exec) {
+      if (!m->cap_stream) LL_HIP(hipStreamCreateWithFlags(&m->cap_stream, hipStreamNonBlocking));
+      LL_HIP(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
+      ll_status st = enqueue_decode(m, in_tokens_dev, next_tokens_dev, logits_dev, m->cap_stream);
+      hipGraph_t graph = nullptr;
+      hipError_t ec = hipStreamEndCapture(m->cap_stream, &graph);
+      if (st != LL_OK) {
+        if (graph) (void)hipGraphDestroy(graph);
+        return st;
+      }
+      if (ec != hipSuccess) return fail(LL_ERR_HIP, "hipStreamEndCapture: %s", hipGetErrorString(ec));
+      ec = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(graph);
+      if (ec != hipSuccess) return fail(LL_ERR_HIP, "hipGraphInstantiate: %s", hipGetErrorString(ec));
+      if (m->graphs.size() >= 8) {
+        (void)hipGraphExecDestroy(m->graphs.front().exec);
+        m->graphs.erase(m->graphs.begin());
+      }
+      m->graphs.push_back({in_tokens_dev, next_tokens_dev, logits_dev, m->batch, exec});
+    }
+    LL_HIP(hipGraphLaunch(exec, m->stream));
+  } else {
+    ll_status st = enqueue_decode(m, in_tokens_dev, next_tokens_dev, logits_dev, m->stream);
+    if (st != LL_OK) return st;
+  }
+  for (auto &l : m->lens) ++l;
+  return LL_OK;
+}
+
+ll_status ll_kv_reset(ll_model *m) {
+  g_err.clear();
+  if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
+  m->batch = 0;
+  m->lens.clear();
+  return LL_OK;
+}
+
+ll_status ll_seq_lengths(const ll_model *m, int32_t *out, int32_t cap, int32_t *n) {
+  g_err.clear();
+  if (!m || !n || (cap > 0 && !out)) return fail(LL_ERR_INVALID_ARGUMENT, "NULL argument");
+  *n = m->batch;
+  for (int b = 0; b < m->batch && b < cap; ++b) out[b] = m->lens[b];
+  return LL_OK;
+}
+
+ll_status ll_set_decode_graph(ll_model *m, int32_t enable) {
+  g_err.clear();
+  if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
+  m->use_graph = enable != 0;
+  return LL_OK;
+}
+
+ll_status ll_device_flags(ll_model *m, int32_t *flags) {
+  g_err.clear();
+  if (!m || !flags) return fail(LL_ERR_INVALID_ARGUMENT, "NULL argument");
+  LL_HIP(hipStreamSynchronize(m->stream));
+  LL_HIP(hipMemcpy(flags, m->at(m->L.err), 4, hipMemcpyDeviceToHost));
+  return LL_OK;
+}
+
+void ll_model_free(ll_model *m) {
+  if (!m) return;
+  m->drop_graphs();
+  if (m->cap_stream) (void)hipStreamDestroy(m->cap_stream);
+  delete m;
+}
+
+// ----------------------------------------------------------------------------------------
+// Per-kernel entry points
+// ----------------------------------------------------------------------------------------
+
+static ll_status check_dtype(int32_t dtype) {
+  if (dtype != LL_F32 && dtype != LL_BF16) return fail(LL_ERR_UNSUPPORTED, "dtype %d unknown", dtype);
+  return LL_OK;
+}
+
+ll_status ll_op_rmsnorm(int32_t dtype, int32_t rows, int32_t d, const float *x, const void *gain,
+                        float eps, void *y, void *stream) {
+  g_err.clear();
+  ll_status st = check_dtype(dtype);
+  if (st != LL_OK) return st;
+  if (rows < 0 || d < 4 || d % 4) return fail(LL_ERR_INVALID_ARGUMENT, "rows >= 0, d a multiple of 4");
+  if (rows && (!x || !gain || !y)) return fail(LL_ERR_INVALID_ARGUMENT, "NULL pointer");
+  LL_HIP(launch_rmsnorm(dtype, x, d, nullptr, rows, d, gain, eps, y, d, (hipStream_t)stream));
+  return LL_OK;
+}
+
+ll_status ll_op_repack(int32_t dtype, int32_t n, int32_t k, const void *w, void *wt, void *stream) {
+  g_err.clear();
+  ll_status st = check_dtype(dtype);
+  if (st != LL_OK) return st;
+  if (n < 16 || n % 16 || k < 64 || k % 64) return fail(LL_ERR_UNSUPPORTED, "n %% 16, k %% 64 required");
+  if (!w || !wt) return fail(LL_ERR_INVALID_ARGUMENT, "NULL pointer");
+  RepackSrc src{{w, nullptr, nullptr}, {n, 0, 0}};
+  LL_HIP(launch_repack(dtype, src, n, k, kPermNone, 64, 64, wt, (hipStream_t)stream));
+  return LL_OK;
+}
+
+ll_status ll_op_gemm(int32_t path, int32_t dtype, int32_t m, int32_t n, int32_t k, const void *a,
+                     const void *wt, float *c, int32_t accumulate, void *stream) {
+  g_err.clear();
+  ll_status st = check_dtype(dtype);
+  if (st != LL_OK) return st;
+  if (path != 0 && path != 1) return fail(LL_ERR_INVALID_ARGUMENT, "path must be 0 or 1");
+  if (m < 0 || n < 1 || k < 1) return fail(LL_ERR_INVALID_ARGUMENT, "bad sizes");
+  if (k % 64 || n % (path == 0 ? 128 : 32))
+    return fail(LL_ERR_UNSUPPORTED, "k %% 64 and n %% %d required", path == 0 ? 128 : 32);
+  if (m && (!a || !wt || !c)) return fail(LL_ERR_INVALID_ARGUMENT, "NULL pointer");
+  EpiParams ep;
+  ep.kind = accumulate ? kEpiResid : kEpiStore;
+  ep.out_f32 = c;
+  ep.ld_out = n;
+  LL_HIP(path == 0 ? launch_gemm_tiled(dtype, a, k, wt, m, n, k, ep, (hipStream_t)stream)
+                   : launch_gemm_skinny(dtype, a, k, wt, m, n, k, ep, (hipStream_t)stream));
+  return LL_OK;
+}
+
+static ll_status check_heads(int32_t n_heads, int32_t n_kv_heads, int32_t head_dim) {
+  if (head_dim != 64 && head_dim != 128) return fail(LL_ERR_UNSUPPORTED, "head_dim %d", head_dim);
+  if (n_heads < 1 || n_kv_heads < 1 || n_heads % n_kv_heads)
+    return fail(LL_ERR_UNSUPPORTED, "n_heads %% n_kv_heads");
+  const int g = n_heads / n_kv_heads;
+  if (g != 1 && g != 2 && g != 4 && g != 8) return fail(LL_ERR_UNSUPPORTED, "group %d", g);
+  return LL_OK;
+}
+
+ll_status ll_op_attn_prefill(int32_t dtype, int32_t batch, const int32_t *seq_lens_host,
+                             int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
+                             int32_t max_ctx, const void *q, const void *kcache,
+                             const void *vcache, void *o, void *scratch, size_t scratch_bytes,
+                             void *stream) {
+  g_err.clear();
+  ll_status st = check_dtype(dtype);
+  if (st == LL_OK) st = check_heads(n_heads, n_kv_heads, head_dim);
+  if (st != LL_OK) return st;
+  if (batch < 1 || batch > LL_MAX_BATCH || !seq_lens_host)
+    return fail(LL_ERR_INVALID_ARGUMENT, "batch in [1, %d] and seq_lens_host required", LL_MAX_BATCH);
+  if (!q || !kcache || !vcache || !o || !scratch) return fail(LL_ERR_INVALID_ARGUMENT, "NULL pointer");
+  PrefillMeta pm;
+  pm.batch = batch;
+  long total = 0;
+  int n_qtiles = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int L = seq_lens_host[b];
+    if (L < 1 || L > max_ctx) return fail(LL_ERR_INVALID_ARGUMENT, "seq_lens[%d] = %d outside [1, max_ctx]", b, L);
+    pm.lens[b] = L;
+    total += L;
+    n_qtiles += (L + kAttnQTile - 1) / kAttnQTile;
+  }
+  if ((st = check_ws(scratch)) != LL_OK) return st;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o2 = off; off = align_up(off + bytes); return o2; };
+  const size_t o_cu = take((batch + 1) * 4), o_seq = take(total * 4), o_pos = take(total * 4),
+               o_last = take(batch * 4), o_lens = take(batch * 4), o_qt = take((size_t)n_qtiles * 8);
+  if (off > scratch_bytes) return fail(LL_ERR_WORKSPACE, "scratch needs %zu bytes", off);
+  char *sc = reinterpret_cast<char *>(scratch);
+  hipStream_t s = (hipStream_t)stream;
+  LL_HIP(launch_prefill_meta(pm, (int)total, (int *)(sc + o_cu), (int *)(sc + o_seq),
+                             (int *)(sc + o_pos), (int *)(sc + o_last), (int *)(sc + o_lens),
+                             (int2 *)(sc + o_qt), s));
+  const int qd = n_heads * head_dim;
+  LL_HIP(launch_attn_prefill(dtype, head_dim, q, qd, kcache, vcache, o, qd, (int *)(sc + o_cu),
+                             (int2 *)(sc + o_qt), n_qtiles, n_heads, n_kv_heads, max_ctx, s));
+  return LL_OK;
+}
+
+size_t ll_op_attn_decode_scratch(int32_t batch, int32_t n_heads, int32_t n_kv_heads,
+                                 int32_t head_dim, int32_t max_ctx) {
+  if (batch < 1 || n_heads < 1 || n_kv_heads < 1 || head_dim < 1 || max_ctx < 1) return 0;
+  const int chunk = attn_decode_chunk(batch, n_kv_heads, max_ctx);
+  const size_t nsplit = (max_ctx + chunk - 1) / chunk;
+  return align_up((size_t)batch * n_heads * nsplit * head_dim * 4) +
+         align_up((size_t)batch * n_heads * nsplit * 2 * 4);
+}
+
+ll_status ll_op_attn_decode(int32_t dtype, int32_t batch, int32_t n_heads, int32_t n_kv_heads,
+                            int32_t head_dim, int32_t max_ctx, const void *q, const void *kcache,
+                            const void *vcache, const int32_t *ctx_lens_dev, void *o,
+                            void *scratch, size_t scratch_bytes, void *stream) {
+  g_err.clear();
+  ll_status st = check_dtype(dtype);
+  if (st == LL_OK) st = check_heads(n_heads, n_kv_heads, head_dim);
+  if (st != LL_OK) return st;
+  if (batch < 1 || max_ctx < 1) return fail(LL_ERR_INVALID_ARGUMENT, "batch, max_ctx >= 1");
+  if (!q || !kcache || !vcache || !ctx_lens_dev || !o) return fail(LL_ERR_INVALID_ARGUMENT, "NULL pointer");
+  if ((st = check_ws(scratch)) != LL_OK) return st;
+  const size_t need = ll_op_attn_decode_scratch(batch, n_heads, n_kv_heads, head_dim, max_ctx);
+  if (scratch_bytes < need) return fail(LL_ERR_WORKSPACE, "scratch needs %zu bytes", need);
+  const int chunk = attn_decode_chunk(batch, n_kv_heads, max_ctx);
+  const size_t nsplit = (max_ctx + chunk - 1) / chunk;
+  float *po = reinterpret_cast<float *>(scratch);
+  float *pml = reinterpret_cast<float *>(reinterpret_cast<char *>(scratch) +
+                                         align_up((size_t)batch * n_heads * nsplit * head_dim * 4));
+  const int qd = n_heads * head_dim;
+  LL_HIP(launch_attn_decode(dtype, head_dim, q, qd, kcache, vcache, ctx_lens_dev, 0, o, qd, batch,
+                            n_heads, n_kv_heads, max_ctx, chunk, po, pml, (hipStream_t)stream));
+  return LL_OK;
+}
+
+ll_status ll_op_lmhead_argmax(int32_t dtype, int32_t rows, int32_t vocab, int32_t k, const void *h,
+                              const void *wt, float *logits, int32_t *next, void *scratch,
+                              size_t scratch_bytes, void *stream) {
+  g_err.clear();
+  ll_status st = check_dtype(dtype);
+  if (st != LL_OK) return st;
+  if (rows < 1 || vocab < 32 || vocab % 32 || k < 64 || k % 64)
+    return fail(LL_ERR_UNSUPPORTED, "rows >= 1, vocab %% 32, k %% 64 required");
+  if (!h || !wt || !next || !scratch) return fail(LL_ERR_INVALID_ARGUMENT, "NULL pointer");
+  const size_t parts = (size_t)rows * (vocab / 32);
+  if (scratch_bytes < parts * 8) return fail(LL_ERR_WORKSPACE, "scratch needs %zu bytes", parts * 8);
+  EpiParams ep;
+  ep.kind = kEpiArgmax;
+  ep.out_f32 = logits;
+  ep.ld_out = vocab;
+  ep.part_val = reinterpret_cast<float *>(scratch);
+  ep.part_idx = reinterpret_cast<int *>(reinterpret_cast<char *>(scratch) + parts * 4);
+  ep.n_parts = vocab / 32;
+  hipStream_t s = (hipStream_t)stream;
+  LL_HIP(launch_gemm_skinny(dtype, h, k, wt, rows, vocab, k, ep, s));
+  LL_HIP(launch_argmax_reduce(ep.part_val, ep.part_idx, rows, ep.n_parts, next, nullptr, s));
+  return LL_OK;
+}
+
+}  // extern "C"

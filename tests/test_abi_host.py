@@ -1,0 +1,149 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports exactly the
+symbols the headers declare, sizes workspaces, and rejects bad arguments with the documented
+status codes before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_21836_amd import binding as B
+from synth import CONFIGS, TEST_CONFIGS
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = set()
+    for h in ("ll.h", "ll_ops.h"):
+        text = open(os.path.join(ROOT, "include", h)).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"\b(ll_\w+)\s*\(", text))
+    return names
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.skip("libll.so not built")
+    return B.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert names == {s[0] for s in B.SIGNATURES}
+    for n in names:
+        assert hasattr(lib, n), n
+    # the binding's signatures resolve against the shared object
+    for n, _, _ in B.SIGNATURES:
+        ctypes.cast(getattr(lib, n), ctypes.c_void_p)
+
+
+def cfg_for(name, **over):
+    c = {**CONFIGS, **TEST_CONFIGS}[name]
+    lens = c.prompt_list or ([c.prompt_len] * c.batch if c.prompt_len else [c.prompt_range[1]] * c.batch)
+    cfg = B.make_config(c, c.batch, sum(lens), max(lens) + c.n_decode)
+    for k, v in over.items():
+        setattr(cfg, k, v)
+    return cfg
+
+
+def status_of(lib, cfg):
+    n = ctypes.c_size_t(0)
+    return lib.ll_workspace_size(ctypes.byref(cfg), ctypes.byref(n)), n.value
+
+
+@pytest.mark.parametrize("name", sorted(CONFIGS) + sorted(TEST_CONFIGS))
+def test_workspace_size_of_every_workload(lib, name):
+    st, n = status_of(lib, cfg_for(name))
+    assert st == B.LL_OK, lib.ll_last_error()
+    c = {**CONFIGS, **TEST_CONFIGS}[name]
+    eb = 2 if c.dtype == "bf16" else 4
+    weights = (2 * c.vocab * c.d_model + c.n_layers * c.linear_params_per_layer()) * eb
+    assert n > weights
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("head_dim", 96, B.LL_ERR_UNSUPPORTED),
+    ("n_kv_heads", 5, B.LL_ERR_UNSUPPORTED),
+    ("d_model", 200, B.LL_ERR_UNSUPPORTED),
+    ("ffn_dim", 1000, B.LL_ERR_UNSUPPORTED),
+    ("vocab", 1000, B.LL_ERR_UNSUPPORTED),
+    ("dtype", 7, B.LL_ERR_UNSUPPORTED),
+    ("max_batch", 257, B.LL_ERR_UNSUPPORTED),
+    ("n_layers", 0, B.LL_ERR_INVALID_ARGUMENT),
+    ("max_ctx", 0, B.LL_ERR_INVALID_ARGUMENT),
+    ("rope_theta", -1.0, B.LL_ERR_INVALID_ARGUMENT),
+    ("rms_eps", float("nan"), B.LL_ERR_INVALID_ARGUMENT),
+])
+def test_config_validation(lib, field, value, status):
+    st, _ = status_of(lib, cfg_for("tiny-f32", **{field: value}))
+    assert st == status
+    assert lib.ll_last_error()
+
+
+def test_group_of_sixteen_rejected(lib):
+    st, _ = status_of(lib, cfg_for("tiny-f32", n_heads=16, n_kv_heads=1))
+    assert st == B.LL_ERR_UNSUPPORTED
+
+
+def test_null_arguments(lib):
+    cfg = cfg_for("tiny-f32")
+    assert lib.ll_workspace_size(None, ctypes.byref(ctypes.c_size_t())) == B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_workspace_size(ctypes.byref(cfg), None) == B.LL_ERR_INVALID_ARGUMENT
+    h = ctypes.c_void_p()
+    assert lib.ll_model_load(ctypes.byref(cfg), None, None, 0, None, ctypes.byref(h)) == \
+        B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_prefill(None, 1, None, None, None, None) == B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_decode_step(None, None, None, None) == B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_kv_reset(None) == B.LL_ERR_INVALID_ARGUMENT
+    lib.ll_model_free(None)
+
+
+def _fake_weights(n_layers, ptr=0x1000):
+    arr = (ctypes.c_void_p * n_layers)(*([ptr] * n_layers))
+    p = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+    return B.LLWeights(ptr, ptr, ptr, p, p, p, p, p, p, p, p, p), arr
+
+
+def test_load_rejects_workspace_problems_before_any_device_call(lib):
+    cfg = cfg_for("tiny-f32")
+    w, keep = _fake_weights(cfg.n_layers)
+    h = ctypes.c_void_p()
+    _, need = status_of(lib, cfg)
+    # NULL workspace
+    assert lib.ll_model_load(ctypes.byref(cfg), ctypes.byref(w), None, need, None,
+                             ctypes.byref(h)) == B.LL_ERR_WORKSPACE
+    # misaligned
+    assert lib.ll_model_load(ctypes.byref(cfg), ctypes.byref(w), 0x10010, need, None,
+                             ctypes.byref(h)) == B.LL_ERR_WORKSPACE
+    # too small
+    assert lib.ll_model_load(ctypes.byref(cfg), ctypes.byref(w), 0x10000, need - 1, None,
+                             ctypes.byref(h)) == B.LL_ERR_WORKSPACE
+    assert "needs" in lib.ll_last_error().decode()
+    # a NULL per-layer pointer
+    arr = (ctypes.c_void_p * cfg.n_layers)(0x1000, None)
+    w.wo = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+    assert lib.ll_model_load(ctypes.byref(cfg), ctypes.byref(w), 0x10000, need, None,
+                             ctypes.byref(h)) == B.LL_ERR_INVALID_ARGUMENT
+    assert not h.value
+
+
+def test_op_argument_validation(lib):
+    # sizes are checked before any launch
+    assert lib.ll_op_gemm(0, 1, 4, 100, 64, 1, 1, 1, 0, None) == B.LL_ERR_UNSUPPORTED
+    assert lib.ll_op_gemm(1, 1, 4, 64, 60, 1, 1, 1, 0, None) == B.LL_ERR_UNSUPPORTED
+    assert lib.ll_op_gemm(2, 1, 4, 64, 64, 1, 1, 1, 0, None) == B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_op_gemm(1, 1, 4, 64, 64, None, 1, 1, 0, None) == B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_op_rmsnorm(1, 4, 6, 1, 1, 1e-5, 1, None) == B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_op_repack(1, 20, 64, 1, 1, None) == B.LL_ERR_UNSUPPORTED
+    lens = (ctypes.c_int32 * 2)(5, 0)
+    assert lib.ll_op_attn_prefill(1, 2, lens, 8, 2, 64, 16, 1, 1, 1, 1, 0x10000, 4096, None) == \
+        B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_op_attn_decode(1, 1, 8, 3, 64, 16, 1, 1, 1, 1, 1, 0x10000, 1 << 20, None) == \
+        B.LL_ERR_UNSUPPORTED
+    assert lib.ll_op_attn_decode(1, 1, 8, 2, 64, 16, 1, 1, 1, 1, 1, 0x10000, 8, None) == \
+        B.LL_ERR_WORKSPACE
+    assert lib.ll_op_lmhead_argmax(1, 2, 100, 64, 1, 1, None, 1, 0x10000, 1 << 20, None) == \
+        B.LL_ERR_UNSUPPORTED
+    assert lib.ll_op_attn_decode_scratch(0, 8, 2, 64, 16) == 0

@@ -1,0 +1,180 @@
+"""Isolated qualification of each hot-path kernel through the per-kernel C entry points
+(include/ll_ops.h), against the oracle's per-op functions on the same rounded inputs.
+
+Floating-point bounds (derived from the arithmetic, not tuned):
+  * GEMM with fp32 accumulation of exact products: |c - c64| <= 4 K u (|A| |W|^T), u = 2^-24
+    (a-priori dot-product bound, any summation order).
+  * RMSNorm: bf16 output rounding 2^-9 |y| plus fp32 noise -> 2^-8 |y| + 1e-6; fp32 1e-5 |y|.
+  * Attention, bf16: P is rounded to bf16 (2^-9 relative) before the PV product and the
+    output is rounded to bf16: |o - o64| <= 4 * 2^-9 * max|v|.  fp32: 1e-5 * max|v|.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from parity import device_tensor, log, rounded
+
+pytestmark = pytest.mark.gpu
+
+U = 2.0 ** -24
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_21836_amd.binding import load_library
+    load_library()
+
+
+def _np(t):
+    import torch
+    return t.float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("rows,d", [(1, 256), (5, 768), (3, 4096)])
+def test_rmsnorm(dtype, rows, d):
+    from paper_2608_21836_amd.binding import op_rmsnorm
+    import torch
+    log(f"rmsnorm {dtype} rows={rows} d={d}")
+    rng = np.random.default_rng(rows * 7 + d)
+    x = (rng.standard_normal((rows, d)) * 3).astype(np.float32)
+    g = rounded(1 + 0.1 * rng.standard_normal(d), dtype)
+    y = op_rmsnorm(torch.from_numpy(x).cuda(), device_tensor(g, dtype), 1e-5)
+    torch.cuda.synchronize()
+    ref = oracle.rmsnorm(x, g, 1e-5)
+    tol = (2.0 ** -8 * np.abs(ref) + 1e-6) if dtype == "bf16" else (1e-5 * np.abs(ref) + 1e-7)
+    assert np.all(np.abs(_np(y) - ref) <= tol)
+
+
+GEMM_SHAPES = [
+    (0, 1, 256, 64), (0, 130, 384, 768), (0, 300, 128, 192), (0, 257, 256, 1408),
+    (1, 1, 32, 64), (1, 1, 256, 768), (1, 15, 96, 192), (1, 16, 256, 512), (1, 17, 64, 64),
+    (1, 32, 128, 4096), (1, 33, 64, 256), (1, 70, 96, 128),
+]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("path,m,n,k", GEMM_SHAPES)
+def test_gemm(dtype, path, m, n, k):
+    from paper_2608_21836_amd.binding import op_gemm, op_repack
+    import torch
+    log(f"gemm path={path} {dtype} m={m} n={n} k={k}")
+    rng = np.random.default_rng(m * 1000 + n + k)
+    a = rounded(rng.standard_normal((m, k)), dtype)
+    w = rounded(rng.standard_normal((n, k)) * 0.05, dtype)
+    c0 = rng.standard_normal((m, n)).astype(np.float32)
+    A, W = device_tensor(a, dtype), device_tensor(w, dtype)
+    wt = op_repack(W)
+    c = op_gemm(path, A, wt, n)
+    cacc = op_gemm(path, A, wt, n, c=torch.from_numpy(c0).cuda(), accumulate=True)
+    torch.cuda.synchronize()
+    ref = a.astype(np.float64) @ w.astype(np.float64).T
+    bound = 4 * k * U * (np.abs(a).astype(np.float64) @ np.abs(w).astype(np.float64).T) + 1e-30
+    assert np.all(np.abs(_np(c) - ref) <= bound)
+    assert np.all(np.abs(_np(cacc) - (ref + c0)) <= bound + 2 * U * np.abs(ref + c0))
+
+
+def _caches(rng, dtype, batch, hkv, max_ctx, hd, lens):
+    """Random caches with every position at or beyond a sequence's length set to NaN, so a
+    read of a stale or out-of-range entry poisons the output."""
+    k = rounded(rng.standard_normal((batch, hkv, max_ctx, hd)), dtype)
+    v = rounded(rng.standard_normal((batch, hkv, max_ctx, hd)), dtype)
+    for b, n in enumerate(lens):
+        k[b, :, n:] = np.nan
+        v[b, :, n:] = np.nan
+    return k, v
+
+
+ATTN_CASES = [
+    ("bf16", 64, 8, 2, [1, 63, 64, 65, 200]),
+    ("bf16", 128, 4, 1, [130, 7]),
+    ("bf16", 128, 8, 8, [96]),
+    ("f32", 64, 4, 4, [33, 1, 128]),
+    ("f32", 128, 4, 2, [70]),
+]
+
+
+@pytest.mark.parametrize("dtype,hd,hq,hkv,lens", ATTN_CASES)
+def test_attn_prefill(dtype, hd, hq, hkv, lens):
+    from paper_2608_21836_amd.binding import op_attn_prefill
+    import torch
+    log(f"attn_prefill {dtype} hd={hd} hq={hq} hkv={hkv} lens={lens}")
+    rng = np.random.default_rng(hd + hq * 10 + len(lens))
+    B, T, max_ctx = len(lens), sum(lens), max(lens) + 3
+    q = rounded(rng.standard_normal((T, hq * hd)), dtype)
+    k, v = _caches(rng, dtype, B, hkv, max_ctx, hd, lens)
+    o = op_attn_prefill(lens, device_tensor(q, dtype), device_tensor(k, dtype),
+                        device_tensor(v, dtype), hq, hkv, hd, max_ctx)
+    torch.cuda.synchronize()
+    o = _np(o)
+    t0 = 0
+    for b, L in enumerate(lens):
+        qb = q[t0:t0 + L].reshape(L, hq, hd).astype(np.float64)
+        kb = k[b, :, :L].transpose(1, 0, 2).astype(np.float64)
+        vb = v[b, :, :L].transpose(1, 0, 2).astype(np.float64)
+        pos = np.arange(L)
+        ref = oracle.causal_gqa_attention(qb, kb, vb, pos, pos).reshape(L, hq * hd)
+        tol = (4 * 2.0 ** -9 if dtype == "bf16" else 1e-5) * np.abs(vb).max()
+        assert np.all(np.abs(o[t0:t0 + L] - ref) <= tol), f"sequence {b}"
+        t0 += L
+
+
+DEC_CASES = [
+    ("bf16", 64, 8, 2, [1, 63, 64, 65, 257, 1000], 1024),
+    ("bf16", 128, 32, 8, [4096, 17, 2049], 4224),
+    ("bf16", 128, 16, 2, [300], 512),
+    ("bf16", 64, 4, 4, [5, 640], 640),
+    ("f32", 64, 4, 4, [48, 2], 48),
+    ("f32", 128, 4, 1, [129], 200),
+]
+
+
+@pytest.mark.parametrize("dtype,hd,hq,hkv,lens,max_ctx", DEC_CASES)
+def test_attn_decode(dtype, hd, hq, hkv, lens, max_ctx):
+    from paper_2608_21836_amd.binding import op_attn_decode
+    import torch
+    log(f"attn_decode {dtype} hd={hd} hq={hq} hkv={hkv} lens={lens} max_ctx={max_ctx}")
+    rng = np.random.default_rng(hd + hq + max_ctx)
+    B = len(lens)
+    q = rounded(rng.standard_normal((B, hq * hd)), dtype)
+    k, v = _caches(rng, dtype, B, hkv, max_ctx, hd, lens)
+    ctx = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    o = op_attn_decode(device_tensor(q, dtype), device_tensor(k, dtype), device_tensor(v, dtype),
+                       ctx, hq, hkv, hd, max_ctx)
+    torch.cuda.synchronize()
+    o = _np(o)
+    for b, L in enumerate(lens):
+        qb = q[b].reshape(1, hq, hd).astype(np.float64)
+        kb = k[b, :, :L].transpose(1, 0, 2).astype(np.float64)
+        vb = v[b, :, :L].transpose(1, 0, 2).astype(np.float64)
+        ref = oracle.causal_gqa_attention(qb, kb, vb, np.array([L - 1]), np.arange(L)).reshape(-1)
+        tol = (2 * 2.0 ** -9 if dtype == "bf16" else 1e-5) * np.abs(vb).max()
+        assert np.all(np.abs(o[b] - ref) <= tol), f"sequence {b}"
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("rows,vocab,k", [(1, 1024, 256), (3, 4096, 768), (33, 32000, 512)])
+def test_lmhead_argmax(dtype, rows, vocab, k):
+    from paper_2608_21836_amd.binding import op_lmhead_argmax, op_repack
+    import torch
+    log(f"lmhead_argmax {dtype} rows={rows} vocab={vocab} k={k}")
+    rng = np.random.default_rng(rows + vocab + k)
+    h = rounded(rng.standard_normal((rows, k)), dtype)
+    w = rng.standard_normal((vocab, k)) * 0.02
+    # planted exact tie at the top for row 0: two identical weight rows aligned with h[0]
+    w[vocab // 3] = w[vocab - 5] = h[0] / np.linalg.norm(h[0])
+    w = rounded(w, dtype)
+    wt = op_repack(device_tensor(w, dtype))
+    nxt, logits = op_lmhead_argmax(device_tensor(h, dtype), wt, vocab)
+    nxt2, none = op_lmhead_argmax(device_tensor(h, dtype), wt, vocab, want_logits=False)
+    torch.cuda.synchronize()
+    lg = logits.cpu().numpy()
+    ref = h.astype(np.float64) @ w.astype(np.float64).T
+    bound = 4 * k * U * (np.abs(h).astype(np.float64) @ np.abs(w).astype(np.float64).T) + 1e-30
+    assert np.all(np.abs(lg - ref) <= bound)
+    assert np.array_equal(nxt.cpu().numpy(), np.argmax(lg, axis=-1))
+    assert np.array_equal(nxt.cpu().numpy(), nxt2.cpu().numpy())
+    assert nxt.cpu().numpy()[0] == vocab // 3
