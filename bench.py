@@ -1,0 +1,248 @@
+#!/usr/bin/env python3
+"""Benchmark of the phase-split decoder forward pass on one MI355X.
+
+One step = one whole job of the workload: reset the KV cache, prefill every prompt, then run
+the workload's greedy decode steps (each a HIP graph replay with the next token fed back on
+the device).  Inputs are seeded and synthetic and already resident in HBM when timing starts.
+
+Printed JSON line:
+  value          whole-job throughput, (prompt tokens + batch * decode steps) / job time
+  prefill_tok_s  prompt tokens / prefill time; decode_tok_s = batch * decode steps / decode time
+  roofline       the kernel class with the largest summed kernel time in one job: its
+                 algorithmic work (bytes for HBM-bound classes, flops for MFMA-bound ones)
+                 over its summed kernel time, against the MI355X peak
+  kernels        every (phase, kernel class): launches, mean kernel time, achieved rate
+  hotspot_eq1    the paper's phase-weighted hotspot score per kernel class
+  cpu_baseline   the fp64 oracle on the host cores, on a bounded sample of the same workload
+Per-kernel times come from a separate instrumented job step (after the timed steps) whose
+launches carry start/stop events stamped by the dispatch itself (hipExtLaunchKernel).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "prefill tok/s + decode tok/s on 1 MI355X; % of MFMA/HBM roofline"
+HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+
+
+def algorithmic_work(cfg, lens, n_decode):
+    """{(phase, class): (work, "flop" | "byte")} summed over one job."""
+    eb = 2 if cfg.dtype == "bf16" else 4
+    B, T = len(lens), sum(lens)
+    d, F, V, L = cfg.d_model, cfg.ffn_dim, cfg.vocab, cfg.n_layers
+    qd, kvd = cfg.q_dim, cfg.kv_dim
+    nqkv = qd + 2 * kvd
+    N = n_decode
+    w = {}
+    # prefill: MFMA-bound GEMMs and attention (causal pairs only), HBM-bound rest
+    w[("prefill", "qkv_rope_append")] = (2.0 * T * nqkv * d * L, "flop")
+    w[("prefill", "o_proj_resid")] = (2.0 * T * d * qd * L, "flop")
+    w[("prefill", "gate_up_swiglu")] = (2.0 * T * 2 * F * d * L, "flop")
+    w[("prefill", "down_resid")] = (2.0 * T * d * F * L, "flop")
+    w[("prefill", "attention")] = (2.0 * cfg.head_dim * cfg.n_heads * sum(x * (x + 1) for x in lens) * L, "flop")
+    w[("prefill", "lm_head_argmax")] = (float(V * d * eb + B * d * eb + B * (V // 32) * 8), "byte")
+    w[("prefill", "rmsnorm")] = (float((2 * L * T + B) * d * (4 + eb)), "byte")
+    w[("prefill", "embed")] = (float(T * d * (eb + 4)), "byte")
+    # decode: every weight byte once per step, plus activations and the KV cache
+    w[("decode", "qkv_rope_append")] = (float(N * L * (nqkv * d * eb + B * d * eb + B * nqkv * eb)), "byte")
+    w[("decode", "o_proj_resid")] = (float(N * L * (d * qd * eb + B * qd * eb + 2 * B * d * 4)), "byte")
+    w[("decode", "gate_up_swiglu")] = (float(N * L * (2 * F * d * eb + B * d * eb + B * F * eb)), "byte")
+    w[("decode", "down_resid")] = (float(N * L * (d * F * eb + B * F * eb + 2 * B * d * 4)), "byte")
+    kv_keys = sum(x + k for x in lens for k in range(1, N + 1))   # keys read, over all steps
+    w[("decode", "attention")] = (float(L * (kv_keys * 2 * kvd * eb + N * B * qd * eb)), "byte")
+    w[("decode", "lm_head_argmax")] = (float(N * (V * d * eb + B * d * eb + B * (V // 32) * 8)), "byte")
+    w[("decode", "rmsnorm")] = (float(N * (2 * L + 1) * B * d * (4 + eb)), "byte")
+    w[("decode", "embed")] = (float(N * B * d * (eb + 4)), "byte")
+    return w
+
+
+def rate(work, unit, ms, dtype):
+    if ms <= 0:
+        return None
+    if unit == "flop":
+        a = work / (ms / 1e3) / 1e12
+        return a, MFMA_PEAK_TFLOPS[dtype], "TFLOP/s", "mfma"
+    a = work / (ms / 1e3) / 1e9
+    return a, HBM_PEAK_GBS, "GB/s", "hbm"
+
+
+def blas_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        n = [i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"]
+        if n:
+            return int(max(n))
+    except Exception:
+        pass
+    return len(os.sched_getaffinity(0))
+
+
+def cpu_baseline(cfg, lens, packed, n_decode, budget_s):
+    """The oracle as it stands, timed on the host: prefill, then decode steps until the
+    budget or the workload's step count is reached.  Tokens/s in the same unit as value."""
+    import numpy as np
+    from oracle import OracleModel, argmax_lowest, split_prompts
+    from synth import gen
+    big = cfg.n_layers * cfg.linear_params_per_layer() * 8 > 16e9
+    w = gen.weights(cfg)
+    om = OracleModel(cfg, w, keep_f64=not big)
+    del w
+    prompts = split_prompts(lens, packed)
+    sample = "all prompts prefilled"
+    if big:   # a prefix of the first prompt keeps the sample within the budget
+        prompts = [prompts[0][:64]]
+        sample = "first 64 tokens of prompt 0 prefilled"
+    t0 = time.perf_counter()
+    logits = om.prefill(prompts)
+    t_pre = time.perf_counter() - t0
+    toks = argmax_lowest(logits)
+    steps = 0
+    t1 = time.perf_counter()
+    while steps < n_decode and (time.perf_counter() - t0) < budget_s:
+        toks = argmax_lowest(om.decode(toks))
+        steps += 1
+    t_dec = time.perf_counter() - t1
+    n_tok = sum(len(p) for p in prompts) + len(prompts) * steps
+    return {"value": round(n_tok / (t_pre + t_dec), 3), "unit": "tok/s", "cores": blas_threads(),
+            "kind": "oracle",
+            "sample": f"{sample} ({sum(len(p) for p in prompts)} tokens, {t_pre:.2f} s), then "
+                      f"{steps} of {n_decode} greedy decode steps ({t_dec:.2f} s); fp64 numpy",
+            "prefill_tok_s": round(sum(len(p) for p in prompts) / t_pre, 3),
+            "decode_tok_s": round(len(prompts) * steps / t_dec, 3) if steps else None}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="125m", help="workload name (synth.configs)")
+    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-timing", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the path has no "
+              "multi-GPU mode", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+    from paper_2608_21836_amd.binding import Model, to_device
+    from synth import gen, get_config
+
+    cfg = get_config(args.config)
+    lens, packed = gen.prompt_tokens(cfg)
+    B, T, N = len(lens), int(sum(lens)), cfg.n_decode
+    torch.cuda.set_device(0)
+    print(f"[bench] {cfg.name}: uploading weights", file=sys.stderr, flush=True)
+    workers = max(1, min(16, len(os.sched_getaffinity(0))))
+    dev_w = {name: to_device(arr, cfg.dtype) for name, arr in gen.iter_weights_parallel(cfg, workers)}
+    dev_w.update({k: to_device(v, cfg.dtype) for k, v in gen.gains(cfg).items()})
+    model = Model(cfg, dev_w, max_batch=B, max_prefill_tokens=T, max_ctx=max(lens) + N)
+    torch.cuda.synchronize()
+    del dev_w
+    torch.cuda.empty_cache()
+    tokens = torch.from_numpy(np.asarray(packed, dtype=np.int32)).cuda()
+    nxt = torch.empty(B, dtype=torch.int32, device="cuda")
+
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    acc = {"pre": 0.0, "dec": 0.0}
+
+    def job(record: bool):
+        model.kv_reset()
+        if record:
+            ev[0].record()
+        model.prefill(lens, tokens, nxt)
+        if record:
+            ev[1].record()
+        for _ in range(N):
+            model.decode_step(nxt, nxt)
+        if record:
+            ev[2].record()
+            ev[2].synchronize()
+            acc["pre"] += ev[0].elapsed_time(ev[1])
+            acc["dec"] += ev[1].elapsed_time(ev[2])
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        job(False)
+    torch.cuda.synchronize()
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        job(False)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall / args.steps * 1e3
+    # phase split from stream events, in separate steps so the timed loop has no host syncs
+    for _ in range(3):
+        job(True)
+    pre_ms, dec_ms = acc["pre"] / 3, acc["dec"] / 3
+    out = {
+        "metric": METRIC, "value": round((T + B * N) / (ms_per_step / 1e3), 3), "unit": "tok/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic (seeded weights and prompts)",
+        "config": {"workload": cfg.name, "layers": cfg.n_layers, "d_model": cfg.d_model,
+                   "heads": f"{cfg.n_heads}/{cfg.n_kv_heads}x{cfg.head_dim}", "ffn": cfg.ffn_dim,
+                   "vocab": cfg.vocab, "batch": B, "prompt_tokens": T, "decode_steps": N},
+        "prefill_ms": round(pre_ms, 4), "decode_ms_per_step": round(dec_ms / N, 5),
+        "prefill_tok_s": round(T / (pre_ms / 1e3), 1),
+        "decode_tok_s": round(B * N / (dec_ms / 1e3), 1),
+    }
+
+    if not args.no_kernel_timing:
+        print("[bench] instrumented job step", file=sys.stderr, flush=True)
+        model.set_kernel_timing(True)
+        job(False)
+        kt = model.kernel_timing()
+        model.set_kernel_timing(False)
+        work = algorithmic_work(cfg, lens, N)
+        rows = []
+        for (phase, cls), (cnt, ms) in sorted(kt.items(), key=lambda kv: -kv[1][1]):
+            r = {"phase": phase, "class": cls, "launches": cnt, "total_ms": round(ms, 4),
+                 "avg_us": round(ms / cnt * 1e3, 3)}
+            if (phase, cls) in work:
+                wv, unit = work[(phase, cls)]
+                a, peak, u, bound = rate(wv, unit, ms, cfg.dtype)
+                r.update({"achieved": round(a, 2), "unit": u, "frac": round(a / peak, 4)})
+            rows.append(r)
+        out["kernels"] = rows
+        dom = next(r for r in rows if "achieved" in r)
+        wv, unit = work[(dom["phase"], dom["class"])]
+        a, peak, u, bound = rate(wv, unit, dom["total_ms"], cfg.dtype)
+        out["roofline"] = {"bound": bound, "achieved": round(a, 2), "peak": peak, "unit": u,
+                           "frac": round(a / peak, 4), "traffic": None,
+                           "kernel": f"{dom['phase']}:{dom['class']}",
+                           "launches": dom["launches"], "avg_us": dom["avg_us"],
+                           "work_per_launch": wv / dom["launches"],
+                           "work_unit": unit}
+        # Eq. 1: s(m) = sum_p w_p t(m, p) / T(p); t and T per phase invocation, w_p = share of
+        # the job's time spent in phase p.
+        inv = {"prefill": 1, "decode": N}
+        phase_ms = {"prefill": pre_ms, "decode": dec_ms / N}
+        wp = {"prefill": pre_ms / (pre_ms + dec_ms), "decode": dec_ms / (pre_ms + dec_ms)}
+        score = {}
+        for (phase, cls), (cnt, ms) in kt.items():
+            score[cls] = score.get(cls, 0.0) + wp[phase] * (ms / inv[phase]) / phase_ms[phase]
+        out["hotspot_eq1"] = {k: round(v, 4) for k, v in sorted(score.items(), key=lambda kv: -kv[1])}
+
+    if not args.no_cpu_baseline:
+        print("[bench] oracle cpu baseline", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(cfg, lens, packed, N, args.cpu_budget)
+    model.close()
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

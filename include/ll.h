@@ -125,6 +125,38 @@ ll_status ll_set_decode_graph(ll_model *m, int32_t enable);
  * outside [0, vocab) was seen (it was replaced by 0, never read out of bounds). */
 ll_status ll_device_flags(ll_model *m, int32_t *flags);
 
+/* Kernel classes of the hot path, for per-module timing.  The paper ranks modules by the
+ * time t(m, p) they take in each phase p relative to the phase latency T(p) (Sec. 3,
+ * Eq. 1); these classes are the modules of this forward pass. */
+typedef enum {
+  LL_K_META = 0,        /* prefill metadata (offsets, positions, tile order) */
+  LL_K_EMBED = 1,       /* embedding gather */
+  LL_K_RMSNORM = 2,     /* RMSNorm (pre-attention, pre-MLP, final) */
+  LL_K_QKV = 3,         /* fused QKV projection + RoPE + KV-cache append */
+  LL_K_ATTN = 4,        /* causal prefill attention, or the per-split decode attention */
+  LL_K_ATTN_COMBINE = 5,/* decode attention: merge of the per-split partial results */
+  LL_K_O = 6,           /* O projection + residual add */
+  LL_K_GATE_UP = 7,     /* gate/up projection + SwiGLU */
+  LL_K_DOWN = 8,        /* down projection + residual add */
+  LL_K_LM_HEAD = 9,     /* LM head + argmax partials */
+  LL_K_ARGMAX = 10,     /* argmax reduction (+ length advance in decode) */
+  LL_K_COUNT = 11
+} ll_kernel_class;
+
+/* Enable (1) or disable (0) per-launch timing.  While enabled, every kernel of ll_prefill
+ * and ll_decode_step is launched with a start/stop HIP event pair stamped by the dispatch
+ * itself (hipExtLaunchKernel), and decode steps launch their kernels directly instead of
+ * replaying the graph.  Host event objects are created as needed; no device memory. */
+ll_status ll_set_kernel_timing(ll_model *m, int32_t enable);
+
+/* Synchronise the model's stream and return the launches and summed kernel milliseconds
+ * recorded since the last read, per phase and class: index phase * LL_K_COUNT + class,
+ * phase 0 = prefill, 1 = decode.  counts and ms hold 2 * LL_K_COUNT entries. */
+ll_status ll_kernel_timing_read(ll_model *m, int32_t *counts, double *ms);
+
+/* Name of a kernel class ("" if out of range). */
+const char *ll_kernel_class_name(int32_t cls);
+
 /* Release host state (graphs, handle).  The workspace is the caller's. */
 void ll_model_free(ll_model *m);
 

@@ -19,6 +19,8 @@ STATUS_NAMES = ["LL_OK", "LL_ERR_INVALID_ARGUMENT", "LL_ERR_UNSUPPORTED", "LL_ER
                 "LL_ERR_STATE", "LL_ERR_WORKSPACE", "LL_ERR_HIP"]
 LL_F32, LL_BF16 = 0, 1
 LL_MAX_BATCH = 256
+LL_K_COUNT = 11
+PHASES = ("prefill", "decode")
 
 
 class LLConfig(ctypes.Structure):
@@ -49,6 +51,9 @@ SIGNATURES = [
     ("ll_seq_lengths", c_int32, [c_void_p, POINTER(c_int32), c_int32, POINTER(c_int32)]),
     ("ll_set_decode_graph", c_int32, [c_void_p, c_int32]),
     ("ll_device_flags", c_int32, [c_void_p, POINTER(c_int32)]),
+    ("ll_set_kernel_timing", c_int32, [c_void_p, c_int32]),
+    ("ll_kernel_timing_read", c_int32, [c_void_p, POINTER(c_int32), POINTER(c_double)]),
+    ("ll_kernel_class_name", c_char_p, [c_int32]),
     ("ll_model_free", None, [c_void_p]),
     ("ll_last_error", c_char_p, []),
     ("ll_op_rmsnorm", c_int32, [c_int32, c_int32, c_int32, c_void_p, c_void_p, c_float,
@@ -203,6 +208,23 @@ class Model:
         n = c_int32(0)
         _check(self.lib.ll_seq_lengths(self.handle, out, LL_MAX_BATCH, ctypes.byref(n)), "ll_seq_lengths")
         return list(out[:n.value])
+
+    def set_kernel_timing(self, enable: bool) -> None:
+        _check(self.lib.ll_set_kernel_timing(self.handle, 1 if enable else 0), "ll_set_kernel_timing")
+
+    def kernel_timing(self) -> Dict[Tuple[str, str], Tuple[int, float]]:
+        """{(phase, kernel class): (launches, summed kernel ms)} since the last read."""
+        counts = (c_int32 * (2 * LL_K_COUNT))()
+        ms = (c_double * (2 * LL_K_COUNT))()
+        _check(self.lib.ll_kernel_timing_read(self.handle, counts, ms), "ll_kernel_timing_read")
+        out = {}
+        for p in range(2):
+            for c in range(LL_K_COUNT):
+                i = p * LL_K_COUNT + c
+                if counts[i]:
+                    name = self.lib.ll_kernel_class_name(c).decode()
+                    out[(PHASES[p], name)] = (counts[i], ms[i])
+        return out
 
     def device_flags(self) -> int:
         f = c_int32(0)

@@ -273,7 +273,7 @@ hipError_t run_prefill(const void *q, int ldq, const void *kc, const void *vc, v
                        const int *cu, const int2 *qtiles, int n_qtiles, int hq, int hkv,
                        int max_ctx, hipStream_t s) {
   const float scale_log2 = kLog2e / sqrtf((float)HD);
-  hipLaunchKernelGGL((k_attn_prefill<T, HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
+  LL_LAUNCH((k_attn_prefill<T, HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
                      reinterpret_cast<const T *>(q), ldq, reinterpret_cast<const T *>(kc),
                      reinterpret_cast<const T *>(vc), reinterpret_cast<T *>(o), ldo, cu, qtiles,
                      hq, hkv, max_ctx, scale_log2);
@@ -286,13 +286,14 @@ hipError_t run_decode_g(const void *q, int ldq, const void *kc, const void *vc, 
                         int chunk, float *part_o, float *part_ml, hipStream_t s) {
   const int nsplit = (max_ctx + chunk - 1) / chunk;
   const float scale_log2 = kLog2e / sqrtf((float)HD);
-  hipLaunchKernelGGL((k_attn_decode<T, HD, G>), dim3(nsplit, hkv, batch), dim3(256), 0, s,
+  LL_LAUNCH((k_attn_decode<T, HD, G>), dim3(nsplit, hkv, batch), dim3(256), 0, s,
                      reinterpret_cast<const T *>(q), ldq, reinterpret_cast<const T *>(kc),
                      reinterpret_cast<const T *>(vc), lens, len_add, hkv, max_ctx, chunk, nsplit,
                      part_o, part_ml, scale_log2);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3(hkv * G, batch), dim3(HD), 0, s, part_o,
+  if (g_launch_timer) g_launch_timer->secondary();
+  LL_LAUNCH((k_attn_combine<T, HD>), dim3(hkv * G, batch), dim3(HD), 0, s, part_o,
                      part_ml, lens, len_add, hkv * G, chunk, nsplit, max_ctx,
                      reinterpret_cast<T *>(o), ldo);
   return hipGetLastError();

@@ -1,8 +1,22 @@
 // Device helpers shared by the gfx950 kernels: element types, 16-byte MFMA operand
 // fragments, conversions and wave reductions.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include "kernels.h"
+
+// Launch through the thread's LaunchTimer when one is installed, else a plain launch.
+#define LL_LAUNCH(kernel, grid, block, shmem, stream, ...)                                    \
+  do {                                                                                      \
+    hipEvent_t ll_ev0_ = nullptr, ll_ev1_ = nullptr;                                        \
+    if (::ll::g_launch_timer && ::ll::g_launch_timer->next(&ll_ev0_, &ll_ev1_))             \
+      hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ll_ev0_, ll_ev1_, 0,          \
+                            __VA_ARGS__);                                                   \
+    else                                                                                    \
+      hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);                  \
+  } while (0)
 
 typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));

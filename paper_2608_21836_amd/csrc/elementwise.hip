@@ -121,10 +121,10 @@ hipError_t launch_embed(int dtype, const int *tokens, int ntok, const void *tabl
                         int d, float *x, int *err, hipStream_t s) {
   if (ntok <= 0) return hipSuccess;
   if (dtype == kF32)
-    hipLaunchKernelGGL(k_embed<float>, dim3(ntok), dim3(256), 0, s, tokens,
+    LL_LAUNCH(k_embed<float>, dim3(ntok), dim3(256), 0, s, tokens,
                        reinterpret_cast<const float *>(table), vocab, d, x, err);
   else
-    hipLaunchKernelGGL(k_embed<bf16>, dim3(ntok), dim3(256), 0, s, tokens,
+    LL_LAUNCH(k_embed<bf16>, dim3(ntok), dim3(256), 0, s, tokens,
                        reinterpret_cast<const bf16 *>(table), vocab, d, x, err);
   return hipGetLastError();
 }
@@ -133,11 +133,11 @@ hipError_t launch_rmsnorm(int dtype, const float *x, int ldx, const int *rowmap,
                           const void *gain, float eps, void *y, int ldy, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (dtype == kF32)
-    hipLaunchKernelGGL(k_rmsnorm<float>, dim3(rows), dim3(256), 0, s, x, ldx, rowmap, d,
+    LL_LAUNCH(k_rmsnorm<float>, dim3(rows), dim3(256), 0, s, x, ldx, rowmap, d,
                        reinterpret_cast<const float *>(gain), eps, reinterpret_cast<float *>(y),
                        ldy);
   else
-    hipLaunchKernelGGL(k_rmsnorm<bf16>, dim3(rows), dim3(256), 0, s, x, ldx, rowmap, d,
+    LL_LAUNCH(k_rmsnorm<bf16>, dim3(rows), dim3(256), 0, s, x, ldx, rowmap, d,
                        reinterpret_cast<const bf16 *>(gain), eps, reinterpret_cast<bf16 *>(y),
                        ldy);
   return hipGetLastError();
@@ -146,7 +146,7 @@ hipError_t launch_rmsnorm(int dtype, const float *x, int ldx, const int *rowmap,
 hipError_t launch_argmax_reduce(const float *pval, const int *pidx, int rows, int n_parts,
                                 int *next, int *lens_inc, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_argmax_reduce, dim3(rows), dim3(256), 0, s, pval, pidx, n_parts, next,
+  LL_LAUNCH(k_argmax_reduce, dim3(rows), dim3(256), 0, s, pval, pidx, n_parts, next,
                      lens_inc);
   return hipGetLastError();
 }
@@ -155,7 +155,7 @@ hipError_t launch_prefill_meta(const PrefillMeta &pm, int total, int *cu, int *r
                                int *row_pos, int *last_row, int *lens_dev, int2 *qtiles,
                                hipStream_t s) {
   const int blocks = std::max(1, (total + 255) / 256);
-  hipLaunchKernelGGL(k_prefill_meta, dim3(blocks), dim3(256), 0, s, pm, total, cu, row_seq,
+  LL_LAUNCH(k_prefill_meta, dim3(blocks), dim3(256), 0, s, pm, total, cu, row_seq,
                      row_pos, last_row, lens_dev, qtiles);
   return hipGetLastError();
 }

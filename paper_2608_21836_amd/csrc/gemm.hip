@@ -323,7 +323,7 @@ template <typename T, typename Epi>
 hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k, const Epi &epi,
                      hipStream_t s) {
   dim3 grid(n / 128, (m + 127) / 128);
-  hipLaunchKernelGGL((k_gemm_tiled<T, Epi>), grid, dim3(256), 0, s,
+  LL_LAUNCH((k_gemm_tiled<T, Epi>), grid, dim3(256), 0, s,
                      reinterpret_cast<const T *>(a), lda,
                      reinterpret_cast<const uint8_t *>(wt), m, k, epi);
   return hipGetLastError();
@@ -337,10 +337,10 @@ hipError_t run_skinny(const void *a, int lda, const void *wt, int m, int n, int 
   for (int mb = 0; mb < m; mb += 32) {
     const int rows = m - mb;
     if (rows <= 16)
-      hipLaunchKernelGGL((k_gemm_skinny<T, 1, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, w,
+      LL_LAUNCH((k_gemm_skinny<T, 1, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, w,
                          m, mb, k, epi);
     else
-      hipLaunchKernelGGL((k_gemm_skinny<T, 2, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, w,
+      LL_LAUNCH((k_gemm_skinny<T, 2, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, w,
                          m, mb, k, epi);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -382,10 +382,10 @@ hipError_t launch_repack(int dtype, const RepackSrc &src, int n, int k, int perm
   const size_t chunks = (size_t)n * k * elem_bytes(dtype) / 16;
   const int blocks = (int)std::min<size_t>((chunks + 255) / 256, 65536);
   if (dtype == kF32)
-    hipLaunchKernelGGL(k_repack<float>, dim3(blocks), dim3(256), 0, s, src, n, k, perm,
+    LL_LAUNCH(k_repack<float>, dim3(blocks), dim3(256), 0, s, src, n, k, perm,
                        head_dim, ffn_dim, reinterpret_cast<uint8_t *>(wt));
   else
-    hipLaunchKernelGGL(k_repack<bf16>, dim3(blocks), dim3(256), 0, s, src, n, k, perm,
+    LL_LAUNCH(k_repack<bf16>, dim3(blocks), dim3(256), 0, s, src, n, k, perm,
                        head_dim, ffn_dim, reinterpret_cast<uint8_t *>(wt));
   return hipGetLastError();
 }

@@ -7,6 +7,17 @@
 
 namespace ll {
 
+// Optional per-launch timing.  While a timer is installed on the calling thread, every kernel
+// launch takes a (start, stop) event pair from it and goes through hipExtLaunchKernel, which
+// stamps the events with the dispatch's own begin and end times.
+struct LaunchTimer {
+  virtual bool next(hipEvent_t *start, hipEvent_t *stop) = 0;
+  // The launcher is about to launch its follow-up kernel (e.g. a split-K combine).
+  virtual void secondary() {}
+  virtual ~LaunchTimer() {}
+};
+extern thread_local LaunchTimer *g_launch_timer;
+
 enum DType : int { kF32 = 0, kBF16 = 1 };
 
 inline size_t elem_bytes(int dtype) { return dtype == kF32 ? 4 : 2; }

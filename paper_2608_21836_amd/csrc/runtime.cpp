@@ -14,9 +14,56 @@
 #include "ll.h"
 #include "ll_ops.h"
 
+namespace ll {
+thread_local LaunchTimer *g_launch_timer = nullptr;
+}
+
 using namespace ll;
 
 namespace {
+
+const char *const kClassNames[LL_K_COUNT] = {
+    "prefill_meta", "embed",          "rmsnorm",       "qkv_rope_append",
+    "attention",    "attn_combine",   "o_proj_resid",  "gate_up_swiglu",
+    "down_resid",   "lm_head_argmax", "argmax_reduce"};
+
+// Collects (phase, kernel class, start, stop) for every launch while installed.
+struct Timer : LaunchTimer {
+  struct Rec {
+    int phase, cls;
+    hipEvent_t a, b;
+  };
+  std::vector<hipEvent_t> pool;
+  std::vector<Rec> recs;
+  int phase = 0, cls = 0;
+  bool next(hipEvent_t *a, hipEvent_t *b) override {
+    while (pool.size() < 2 * recs.size() + 2) {
+      hipEvent_t e;
+      if (hipEventCreate(&e) != hipSuccess) return false;
+      pool.push_back(e);
+    }
+    *a = pool[2 * recs.size()];
+    *b = pool[2 * recs.size() + 1];
+    recs.push_back({phase, cls, *a, *b});
+    return true;
+  }
+  void secondary() override {
+    if (cls == LL_K_ATTN) cls = LL_K_ATTN_COMBINE;
+  }
+  ~Timer() override {
+    for (auto e : pool) (void)hipEventDestroy(e);
+  }
+};
+
+// Installs a model's timer on this thread for the duration of one ll_* call.
+struct TimerScope {
+  LaunchTimer *saved;
+  explicit TimerScope(Timer *t, int phase) : saved(g_launch_timer) {
+    if (t) t->phase = phase;
+    g_launch_timer = t;
+  }
+  ~TimerScope() { g_launch_timer = saved; }
+};
 
 thread_local std::string g_err;
 
@@ -158,10 +205,15 @@ struct ll_model {
   };
   std::vector<Graph> graphs;
   std::vector<float> rope_host;
+  Timer *timer = nullptr;  // per-launch timing (decode then runs without the graph)
+  void mark(int cls) const {
+    if (timer) timer->cls = cls;
+  }
 
   template <typename P = void> P *at(size_t off) const { return reinterpret_cast<P *>(ws + off); }
   void *kc(int l) const { return ws + L.kcache + L.kv_layer_elems * l * elem_bytes(cfg.dtype); }
   void *vc(int l) const { return ws + L.vcache + L.kv_layer_elems * l * elem_bytes(cfg.dtype); }
+  ~ll_model() { delete timer; }
   void drop_graphs() {
     for (auto &g : graphs) (void)hipGraphExecDestroy(g.exec);
     graphs.clear();
@@ -223,12 +275,15 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
   auto gemm = decode ? launch_gemm_skinny : launch_gemm_tiled;
   float *x = m->at<float>(m->L.x);
   for (int l = 0; l < c.n_layers; ++l) {
+    m->mark(LL_K_RMSNORM);
     LL_HIP(launch_rmsnorm(dt, x, d, nullptr, rows, d, m->at(m->L.attn_norm[l]), c.rms_eps,
                           m->at(m->L.h), d, s));
     const int *row_seq = decode ? nullptr : m->at<int>(m->L.row_seq);
     const int *row_pos = decode ? m->at<int>(m->L.lens) : m->at<int>(m->L.row_pos);
+    m->mark(LL_K_QKV);
     LL_HIP(gemm(dt, m->at(m->L.h), d, m->at(m->L.wqkv[l]), rows, m->L.n_qkv, d,
                 qkv_epi(m, l, row_seq, row_pos), s));
+    m->mark(LL_K_ATTN);
     if (decode) {
       LL_HIP(launch_attn_decode(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
                                 m->at<int>(m->L.lens), 1, m->at(m->L.o), qd, rows, c.n_heads,
@@ -240,10 +295,14 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
                                  m->at<int2>(m->L.qtiles), n_qtiles, c.n_heads, c.n_kv_heads,
                                  c.max_ctx, s));
     }
+    m->mark(LL_K_O);
     LL_HIP(gemm(dt, m->at(m->L.o), qd, m->at(m->L.wo[l]), rows, d, qd, resid_epi(m), s));
+    m->mark(LL_K_RMSNORM);
     LL_HIP(launch_rmsnorm(dt, x, d, nullptr, rows, d, m->at(m->L.mlp_norm[l]), c.rms_eps,
                           m->at(m->L.h), d, s));
+    m->mark(LL_K_GATE_UP);
     LL_HIP(gemm(dt, m->at(m->L.h), d, m->at(m->L.wgu[l]), rows, 2 * F, d, swiglu_epi(m), s));
+    m->mark(LL_K_DOWN);
     LL_HIP(gemm(dt, m->at(m->L.act), F, m->at(m->L.wd[l]), rows, d, F, resid_epi(m), s));
   }
   return LL_OK;
@@ -253,10 +312,13 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
 ll_status enqueue_head(ll_model *m, int batch, const int *rowmap, int *next, float *logits,
                        int *lens_inc, hipStream_t s) {
   const ll_config &c = m->cfg;
+  m->mark(LL_K_RMSNORM);
   LL_HIP(launch_rmsnorm(c.dtype, m->at<float>(m->L.x), c.d_model, rowmap, batch, c.d_model,
                         m->at(m->L.final_norm), c.rms_eps, m->at(m->L.hf), c.d_model, s));
+  m->mark(LL_K_LM_HEAD);
   LL_HIP(launch_gemm_skinny(c.dtype, m->at(m->L.hf), c.d_model, m->at(m->L.lm_head), batch,
                             c.vocab, c.d_model, argmax_epi(m, logits), s));
+  m->mark(LL_K_ARGMAX);
   LL_HIP(launch_argmax_reduce(m->at<float>(m->L.pval), m->at<int>(m->L.pidx), batch,
                               m->L.n_parts, next, lens_inc, s));
   return LL_OK;
@@ -265,6 +327,7 @@ ll_status enqueue_head(ll_model *m, int batch, const int *rowmap, int *next, flo
 ll_status enqueue_decode(ll_model *m, const int32_t *in, int32_t *out, float *logits,
                          hipStream_t s) {
   const ll_config &c = m->cfg;
+  m->mark(LL_K_EMBED);
   LL_HIP(launch_embed(c.dtype, in, m->batch, m->at(m->L.embed), c.vocab, c.d_model,
                       m->at<float>(m->L.x), m->at<int>(m->L.err), s));
   ll_status st = enqueue_layers(m, m->batch, true, 0, s);
@@ -404,8 +467,11 @@ ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
   const int T = (int)total;
   hipStream_t s = m->stream;
   const Layout &L = m->L;
+  TimerScope scope(m->timer, 0);
+  m->mark(LL_K_META);
   LL_HIP(launch_prefill_meta(pm, T, m->at<int>(L.cu), m->at<int>(L.row_seq), m->at<int>(L.row_pos),
                              m->at<int>(L.last_row), m->at<int>(L.lens), m->at<int2>(L.qtiles), s));
+  m->mark(LL_K_EMBED);
   LL_HIP(launch_embed(c.dtype, tokens_dev, T, m->at(L.embed), c.vocab, c.d_model,
                       m->at<float>(L.x), m->at<int>(L.err), s));
   ll_status st = enqueue_layers(m, T, false, n_qtiles, s);
@@ -428,7 +494,8 @@ ll_status ll_decode_step(ll_model *m, const int32_t *in_tokens_dev, int32_t *nex
     if (m->lens[b] + 1 > m->cfg.max_ctx)
       return fail(LL_ERR_CAPACITY, "sequence %d at length %d is full (max_ctx %d)", b, m->lens[b],
                   m->cfg.max_ctx);
-  if (m->use_graph) {
+  TimerScope scope(m->timer, 1);
+  if (m->use_graph && !m->timer) {
     hipGraphExec_t exec = nullptr;
     for (auto &g : m->graphs)
       if (g.in == in_tokens_dev && g.out == next_tokens_dev && g.logits == logits_dev &&
@@ -492,6 +559,41 @@ ll_status ll_device_flags(ll_model *m, int32_t *flags) {
   LL_HIP(hipStreamSynchronize(m->stream));
   LL_HIP(hipMemcpy(flags, m->at(m->L.err), 4, hipMemcpyDeviceToHost));
   return LL_OK;
+}
+
+ll_status ll_set_kernel_timing(ll_model *m, int32_t enable) {
+  g_err.clear();
+  if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
+  if (enable && !m->timer) m->timer = new Timer();
+  if (!enable && m->timer) {
+    (void)hipStreamSynchronize(m->stream);
+    delete m->timer;
+    m->timer = nullptr;
+  }
+  return LL_OK;
+}
+
+ll_status ll_kernel_timing_read(ll_model *m, int32_t *counts, double *ms) {
+  g_err.clear();
+  if (!m || !counts || !ms) return fail(LL_ERR_INVALID_ARGUMENT, "NULL argument");
+  for (int i = 0; i < 2 * LL_K_COUNT; ++i) {
+    counts[i] = 0;
+    ms[i] = 0.0;
+  }
+  if (!m->timer) return fail(LL_ERR_STATE, "kernel timing is not enabled");
+  LL_HIP(hipStreamSynchronize(m->stream));
+  for (const auto &r : m->timer->recs) {
+    float t = 0.f;
+    LL_HIP(hipEventElapsedTime(&t, r.a, r.b));
+    counts[r.phase * LL_K_COUNT + r.cls] += 1;
+    ms[r.phase * LL_K_COUNT + r.cls] += t;
+  }
+  m->timer->recs.clear();
+  return LL_OK;
+}
+
+const char *ll_kernel_class_name(int32_t cls) {
+  return (cls >= 0 && cls < LL_K_COUNT) ? kClassNames[cls] : "";
 }
 
 void ll_model_free(ll_model *m) {

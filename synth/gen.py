@@ -90,6 +90,24 @@ def iter_weights(cfg: ModelConfig) -> Iterator[Tuple[str, np.ndarray]]:
         yield name, draw_tensor(cfg, j, shape, std)
 
 
+def iter_weights_parallel(cfg: ModelConfig, workers: int = 8) -> Iterator[Tuple[str, np.ndarray]]:
+    """Same tensors and order as iter_weights, drawn on `workers` threads (numpy's generator
+    releases the GIL), with at most 2 * workers tensors in flight."""
+    import collections
+    from concurrent.futures import ThreadPoolExecutor
+    specs = tensor_shapes(cfg)
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        pending = collections.deque()
+        for name, j, shape, std in specs:
+            pending.append((name, ex.submit(draw_tensor, cfg, j, shape, std)))
+            if len(pending) >= 2 * workers:
+                n, f = pending.popleft()
+                yield n, f.result()
+        while pending:
+            n, f = pending.popleft()
+            yield n, f.result()
+
+
 def gains(cfg: ModelConfig, random_gains: bool = False) -> Dict[str, np.ndarray]:
     """RMSNorm gain vectors: attn_norm/mlp_norm per layer and final_norm."""
     names = []
@@ -111,7 +129,8 @@ def gains(cfg: ModelConfig, random_gains: bool = False) -> Dict[str, np.ndarray]
 
 def weights(cfg: ModelConfig, random_gains: bool = False) -> Dict[str, np.ndarray]:
     """All tensors as fp32 arrays (bf16-exact values for bf16 workloads)."""
-    out = dict(iter_weights(cfg))
+    big = cfg.n_layers * cfg.linear_params_per_layer() > 50_000_000
+    out = dict(iter_weights_parallel(cfg) if big else iter_weights(cfg))
     out.update(gains(cfg, random_gains))
     return out
 
