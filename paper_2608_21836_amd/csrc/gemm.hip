@@ -213,6 +213,118 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const T *__restrict__ A, int
 }
 
 // ------------------------------------------------------------------------------------------
+// Large prefill GEMM: 256 x 256 block tiles, 4 waves of 128 x 128, K steps of two 1 KiB tiles.
+// Operand tiles go straight from global memory into LDS (global_load_lds_dwordx4: each wave
+// fills one 1 KiB tile per instruction, lane l's 16 bytes at offset 16 l, which is exactly the
+// MFMA operand order), double-buffered: the loads of step k+1 are in flight while step k
+// computes.  Blocks are renumbered so that each XCD (workgroups are dealt round-robin to the
+// 8 XCDs) works on a compact group of output tiles and shares A and W tiles in its own L2.
+// ------------------------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void global_void_t;
+
+__device__ __forceinline__ void load_tile_to_lds(const void *src, void *lds_tile) {
+  __builtin_amdgcn_global_load_lds((global_void_t *)src, (lds_void_t *)lds_tile, 16, 0, 0);
+}
+
+// Bijection from dispatch order to a tile order in which XCD x owns a contiguous range.
+__device__ __forceinline__ int xcd_remap(int pid, int n) {
+  constexpr int kXcd = 8;
+  const int per = (n + kXcd - 1) / kXcd;
+  const int tall = n % kXcd == 0 ? kXcd : n % kXcd;
+  const int x = pid % kXcd, local = pid / kXcd;
+  return x < tall ? x * per + local : tall * per + (x - tall) * (per - 1) + local;
+}
+
+template <typename T, typename Epi>
+__global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, int lda,
+                                                     const uint8_t *__restrict__ Wt, int M,
+                                                     int N, int K, Epi epi) {
+  using F = typename Frag<T>::type;
+  constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL;
+  constexpr int BM = 256, BN = 256, GM = 8;
+  __shared__ uint4 smem[2][4096];  // [buf][A: 32 tiles | W: 32 tiles][64 lanes]
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // 8 waves, 2 (M) x 4 (N)
+  const int wm = wave >> 2, wn = wave & 3;
+  const int ntm = (M + BM - 1) / BM, ntn = N / BN;
+  // tile order: XCD-contiguous ranges, each walking groups of GM row-tiles across all columns
+  const int t = xcd_remap(blockIdx.x, ntm * ntn);
+  const int group = t / (GM * ntn), first_m = group * GM;
+  const int gsize = min(ntm - first_m, GM);
+  const int tm = first_m + (t % (GM * ntn)) % gsize, tn = (t % (GM * ntn)) / gsize;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int kb_n = K / TK, nsteps = kb_n / 2;
+
+  // Per step this wave fills A tiles 4w .. 4w+3 (row blocks 2w, 2w+1; both k-tiles) and W
+  // tiles 4w .. 4w+3 (16-row blocks 2w, 2w+1 of this block's columns).
+  const T *a_lane = A + (lane >> 4) * EPL;
+  uint32_t a_row[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+    a_row[q] = (uint32_t)min(m0 + (wave * 2 + q) * 16 + (lane & 15), M - 1);
+  const uint8_t *w_lane = Wt + (((size_t)(n0 / 16 + wave * 2) * kb_n) * 64 + lane) * 16;
+  auto issue = [&](int step, int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int q = i >> 1, kb = i & 1;
+      load_tile_to_lds(a_lane + (size_t)a_row[q] * lda + (step * 2 + kb) * TK,
+                       &smem[buf][(wave * 4 + i) * 64]);
+      load_tile_to_lds(w_lane + ((size_t)q * kb_n + step * 2 + kb) * 1024,
+                       &smem[buf][(32 + wave * 4 + i) * 64]);
+    }
+  };
+
+  f32x4 acc[8][4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](int cur) {
+#pragma unroll
+    for (int kbl = 0; kbl < 2; ++kbl) {
+      F a[8], b[4];
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        a[i] = *reinterpret_cast<const F *>(&smem[cur][((wm * 8 + i) * 2 + kbl) * 64 + lane]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        b[j] = *reinterpret_cast<const F *>(&smem[cur][(32 + (wn * 4 + j) * 2 + kbl) * 64 + lane]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mma_chunk(a[i], b[j], acc[i][j]);
+    }
+  };
+
+  // Straight-line loop body (no branch around the prefetch) so the accumulators stay put in
+  // the accumulation registers across iterations; the last step is peeled.
+  issue(0, 0);
+  for (int step = 0; step + 1 < nsteps; ++step) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    issue(step + 1, (step + 1) & 1);
+    compute(step & 1);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  compute((nsteps - 1) & 1);
+
+  const int ubase = (n0 + wn * 64) >> 5;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = m0 + wm * 128 + i * 16 + (lane >> 4) * 4 + r;
+      if (m < M) {
+#pragma unroll
+        for (int p = 0; p < 2; ++p) epi(m, ubase + p, lane & 15, acc[i][2 * p][r], acc[i][2 * p + 1][r]);
+      }
+    }
+}
+
+// ------------------------------------------------------------------------------------------
 // Decode GEMM (one block per 32 output columns, 8 waves splitting K)
 // ------------------------------------------------------------------------------------------
 template <typename T, int MT, typename Epi>
@@ -319,9 +431,19 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
   }
 }
 
+// The 256 x 256 kernel is used once it fills most of the 256 CUs with one block each.
+constexpr int kBigGemmMinTiles = 192;
+
 template <typename T, typename Epi>
 hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k, const Epi &epi,
                      hipStream_t s) {
+  const int big_tiles = ((m + 255) / 256) * (n / 256);
+  if (n % 256 == 0 && big_tiles >= kBigGemmMinTiles) {
+    LL_LAUNCH((k_gemm_big<T, Epi>), dim3(big_tiles), dim3(512), 0, s,
+              reinterpret_cast<const T *>(a), lda, reinterpret_cast<const uint8_t *>(wt), m, n,
+              k, epi);
+    return hipGetLastError();
+  }
   dim3 grid(n / 128, (m + 127) / 128);
   LL_LAUNCH((k_gemm_tiled<T, Epi>), grid, dim3(256), 0, s,
                      reinterpret_cast<const T *>(a), lda,
