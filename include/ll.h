@@ -131,14 +131,14 @@ ll_status ll_device_flags(ll_model *m, int32_t *flags);
 typedef enum {
   LL_K_META = 0,        /* prefill metadata (offsets, positions, tile order) */
   LL_K_EMBED = 1,       /* embedding gather */
-  LL_K_RMSNORM = 2,     /* RMSNorm (pre-attention, pre-MLP, final) */
+  LL_K_RMSNORM = 2,     /* RMSNorm kernel (decode batches <= 16 normalise inside the GEMM) */
   LL_K_QKV = 3,         /* fused QKV projection + RoPE + KV-cache append */
   LL_K_ATTN = 4,        /* causal prefill attention, or the per-split decode attention */
   LL_K_ATTN_COMBINE = 5,/* decode attention: merge of the per-split partial results */
   LL_K_O = 6,           /* O projection + residual add */
   LL_K_GATE_UP = 7,     /* gate/up projection + SwiGLU */
   LL_K_DOWN = 8,        /* down projection + residual add */
-  LL_K_LM_HEAD = 9,     /* LM head + argmax partials */
+  LL_K_LM_HEAD = 9,     /* LM head + per-block argmax partials */
   LL_K_ARGMAX = 10,     /* argmax reduction (+ length advance in decode) */
   LL_K_COUNT = 11
 } ll_kernel_class;

@@ -55,8 +55,9 @@ ll_status ll_op_attn_prefill(int32_t dtype, int32_t batch, const int32_t *seq_le
 /* Decode attention: one query per sequence over ctx_lens_dev[b] cached keys (same
  * appendix: each KV tile loaded once for its whole query-head group; split over the cache
  * length with an fp32 log-sum-exp combine).  q T [batch, n_heads*head_dim]; caches as
- * above; o T [batch, n_heads*head_dim].  1 <= ctx_lens_dev[b] <= max_ctx.
- * scratch >= ll_op_attn_decode_scratch(...) bytes. */
+ * above; o T [batch, n_heads*head_dim].  1 <= ctx_lens_dev[b] <= max_ctx <= 32768 (larger
+ * values are clamped to max_ctx).  scratch >= ll_op_attn_decode_scratch(...) bytes (split
+ * partials). */
 ll_status ll_op_attn_decode(int32_t dtype, int32_t batch, int32_t n_heads, int32_t n_kv_heads,
                             int32_t head_dim, int32_t max_ctx, const void *q,
                             const void *kcache, const void *vcache, const int32_t *ctx_lens_dev,
@@ -66,7 +67,7 @@ size_t ll_op_attn_decode_scratch(int32_t batch, int32_t n_heads, int32_t n_kv_he
 
 /* LM head with fused greedy argmax: logits = h W^T, next[r] = argmax (lowest index on
  * ties).  h T [rows, k], wt repacked [vocab, k], logits fp32 [rows, vocab] (nullable),
- * next int32 [rows].  scratch >= 8 * rows * vocab / 32 bytes. */
+ * next int32 [rows].  scratch >= 8 * rows * vocab / 32 bytes (per-block partials). */
 ll_status ll_op_lmhead_argmax(int32_t dtype, int32_t rows, int32_t vocab, int32_t k,
                               const void *h, const void *wt, float *logits, int32_t *next,
                               void *scratch, size_t scratch_bytes, void *stream);

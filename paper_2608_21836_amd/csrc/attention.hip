@@ -11,7 +11,8 @@
 //
 // Decode: grid (split, kv head, sequence); a block streams `chunk` cached keys once for all
 // query heads of the group, keeps exact chunk scores in LDS and writes (max, sum, partial
-// output) per head; a combine kernel merges the splits with log-sum-exp weights.
+// output) per head; a second kernel merges the splits with
+// log-sum-exp weights (fixed order, so the result does not depend on block order).
 #include <algorithm>
 
 #include "device_common.h"
@@ -137,8 +138,14 @@ __global__ __launch_bounds__(256) void k_attn_prefill(
   }
 }
 
-constexpr int kMaxChunk = 256;
+constexpr int kMaxChunk = 256;  // keys per decode-attention block
+constexpr int kMaxSplit = 128;  // blocks per (sequence, kv head)
 
+// Decode attention for one (split, kv head, sequence): exact scores of up to kMaxChunk cached
+// keys for all G query heads of the group (each K and V row read once), chunk softmax
+// statistics and the unnormalised partial output.  A second kernel merges the splits: a
+// kernel boundary makes every block's partials visible across XCDs once per launch, where a
+// device-scope fence in each block would write back the L2 once per block.
 template <typename T, int HD, int G>
 __global__ __launch_bounds__(256) void k_attn_decode(
     const T *__restrict__ Q, int ldq, const T *__restrict__ Kc, const T *__restrict__ Vc,
@@ -146,8 +153,9 @@ __global__ __launch_bounds__(256) void k_attn_decode(
     float *__restrict__ part_o, float *__restrict__ part_ml, float scale_log2) {
   using F = typename Frag<T>::type;
   constexpr int EPL = Frag<T>::EPL;
-  constexpr int LPK = HD / EPL;     // lanes per cached row
-  constexpr int NSLOT = 256 / LPK;  // rows in flight per block
+  constexpr int LPK = HD / EPL;           // lanes per cached row
+  constexpr int NSLOT = 256 / LPK;        // rows in flight per pass
+  constexpr int KPT = kMaxChunk / NSLOT;  // rows per thread at the largest chunk
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int S = min(lens[b] + len_add, max_ctx);  // never read past the cache capacity
   const int j0 = split * chunk;
@@ -159,6 +167,7 @@ __global__ __launch_bounds__(256) void k_attn_decode(
   __shared__ float s_p[G][kMaxChunk];
   __shared__ float s_red[4][G][HD];
   __shared__ float s_m[G], s_l[G];
+  const F fz = frag_zero<F>();
 
   float qv[G][EPL];
 #pragma unroll
@@ -171,23 +180,40 @@ __global__ __launch_bounds__(256) void k_attn_decode(
   const T *Kb = Kc + kvbase + dl * EPL;
   const T *Vb = Vc + kvbase + dl * EPL;
 
-  for (int j = j0 + slot; j < j1; j += NSLOT) {
-    const F kk = load_frag_stream<F>(Kb + (size_t)j * HD);
+  // Scores: all of this thread's K rows are requested before the first one is used.
+  F rows[KPT];
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    if (i * NSLOT >= n) break;
+    const int j = j0 + slot + i * NSLOT;
+    rows[i] = j < j1 ? load_frag_stream<F>(Kb + (size_t)j * HD) : fz;
+  }
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    if (i * NSLOT >= n) break;
     float d[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       float a = 0.f;
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) a += qv[g][e] * to_f32(kk[e]);
+      for (int e = 0; e < EPL; ++e) a += qv[g][e] * to_f32(rows[i][e]);
       d[g] = a;
     }
 #pragma unroll
     for (int o = LPK / 2; o > 0; o >>= 1)
 #pragma unroll
       for (int g = 0; g < G; ++g) d[g] += __shfl_xor(d[g], o);
-    if (dl == 0)
+    const int jj = slot + i * NSLOT;
+    if (dl == 0 && jj < n)
 #pragma unroll
-      for (int g = 0; g < G; ++g) s_p[g][j - j0] = d[g];
+      for (int g = 0; g < G; ++g) s_p[g][jj] = d[g];
+  }
+  // V rows of this thread, requested while the chunk softmax runs.
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    if (i * NSLOT >= n) break;
+    const int j = j0 + slot + i * NSLOT;
+    rows[i] = j < j1 ? load_frag_stream<F>(Vb + (size_t)j * HD) : fz;
   }
   __syncthreads();
   for (int g = wave; g < G; g += 4) {
@@ -212,13 +238,17 @@ __global__ __launch_bounds__(256) void k_attn_decode(
   for (int g = 0; g < G; ++g)
 #pragma unroll
     for (int e = 0; e < EPL; ++e) acc[g][e] = 0.f;
-  for (int j = j0 + slot; j < j1; j += NSLOT) {
-    const F vv = load_frag_stream<F>(Vb + (size_t)j * HD);
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const float p = s_p[g][j - j0];
+  for (int i = 0; i < KPT; ++i) {
+    if (i * NSLOT >= n) break;
+    const int jj = slot + i * NSLOT;
+    if (jj < n) {
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[g][e] += p * to_f32(vv[e]);
+      for (int g = 0; g < G; ++g) {
+        const float p = s_p[g][jj];
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[g][e] += p * to_f32(rows[i][e]);
+      }
     }
   }
 #pragma unroll
@@ -236,34 +266,33 @@ __global__ __launch_bounds__(256) void k_attn_decode(
   for (int i = tid; i < G * HD; i += 256) {
     const int g = i / HD, d = i % HD;
     const float v = s_red[0][g][d] + s_red[1][g][d] + s_red[2][g][d] + s_red[3][g][d];
-    const int h = kvh * G + g;
-    part_o[(((size_t)b * hq + h) * nsplit + split) * HD + d] = v;
+    part_o[(((size_t)b * hq + kvh * G + g) * nsplit + split) * HD + d] = v;
   }
   if (tid < G) {
-    const int h = kvh * G + tid;
-    float *ml = part_ml + (((size_t)b * hq + h) * nsplit + split) * 2;
+    float *ml = part_ml + (((size_t)b * hq + kvh * G + tid) * nsplit + split) * 2;
     ml[0] = s_m[tid];
     ml[1] = s_l[tid];
   }
 }
 
+// Merge of the splits of one (query head, sequence): log-sum-exp weights, fixed split order.
 template <typename T, int HD>
 __global__ __launch_bounds__(HD) void k_attn_combine(const float *__restrict__ part_o,
                                                       const float *__restrict__ part_ml,
                                                       const int *__restrict__ lens, int len_add,
-                                                      int hq, int chunk, int nsplit,
-                                                      int max_ctx, T *__restrict__ O, int ldo) {
+                                                      int hq, int chunk, int nsplit, int max_ctx,
+                                                      T *__restrict__ O, int ldo) {
   const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
   const int S = min(lens[b] + len_add, max_ctx);
   const int ns = (S + chunk - 1) / chunk;
   const size_t base = ((size_t)b * hq + h) * nsplit;
   float mx = -INFINITY;
-  for (int s = 0; s < ns; ++s) mx = fmaxf(mx, part_ml[(base + s) * 2]);
+  for (int sp = 0; sp < ns; ++sp) mx = fmaxf(mx, part_ml[(base + sp) * 2]);
   float num = 0.f, den = 0.f;
-  for (int s = 0; s < ns; ++s) {
-    const float w = exp2f(part_ml[(base + s) * 2] - mx);
-    num += w * part_o[(base + s) * HD + d];
-    den += w * part_ml[(base + s) * 2 + 1];
+  for (int sp = 0; sp < ns; ++sp) {
+    const float w = exp2f(part_ml[(base + sp) * 2] - mx);
+    num += w * part_o[(base + sp) * HD + d];
+    den += w * part_ml[(base + sp) * 2 + 1];
   }
   O[(size_t)b * ldo + h * HD + d] = from_f32<T>(num / den);
 }
@@ -287,15 +316,14 @@ hipError_t run_decode_g(const void *q, int ldq, const void *kc, const void *vc, 
   const int nsplit = (max_ctx + chunk - 1) / chunk;
   const float scale_log2 = kLog2e / sqrtf((float)HD);
   LL_LAUNCH((k_attn_decode<T, HD, G>), dim3(nsplit, hkv, batch), dim3(256), 0, s,
-                     reinterpret_cast<const T *>(q), ldq, reinterpret_cast<const T *>(kc),
-                     reinterpret_cast<const T *>(vc), lens, len_add, hkv, max_ctx, chunk, nsplit,
-                     part_o, part_ml, scale_log2);
+            reinterpret_cast<const T *>(q), ldq, reinterpret_cast<const T *>(kc),
+            reinterpret_cast<const T *>(vc), lens, len_add, hkv, max_ctx, chunk, nsplit, part_o,
+            part_ml, scale_log2);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (g_launch_timer) g_launch_timer->secondary();
-  LL_LAUNCH((k_attn_combine<T, HD>), dim3(hkv * G, batch), dim3(HD), 0, s, part_o,
-                     part_ml, lens, len_add, hkv * G, chunk, nsplit, max_ctx,
-                     reinterpret_cast<T *>(o), ldo);
+  LL_LAUNCH((k_attn_combine<T, HD>), dim3(hkv * G, batch), dim3(HD), 0, s, part_o, part_ml, lens,
+            len_add, hkv * G, chunk, nsplit, max_ctx, reinterpret_cast<T *>(o), ldo);
   return hipGetLastError();
 }
 
@@ -303,12 +331,16 @@ template <typename T, int HD>
 hipError_t run_decode(int group, const void *q, int ldq, const void *kc, const void *vc,
                       const int *lens, int len_add, void *o, int ldo, int batch, int hkv,
                       int max_ctx, int chunk, float *part_o, float *part_ml, hipStream_t s) {
+#define LL_DECODE_G(G)                                                                       \
+  return run_decode_g<T, HD, G>(q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, \
+                                chunk, part_o, part_ml, s)
   switch (group) {
-    case 1: return run_decode_g<T, HD, 1>(q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
-    case 2: return run_decode_g<T, HD, 2>(q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
-    case 4: return run_decode_g<T, HD, 4>(q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
-    case 8: return run_decode_g<T, HD, 8>(q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
+    case 1: LL_DECODE_G(1);
+    case 2: LL_DECODE_G(2);
+    case 4: LL_DECODE_G(4);
+    case 8: LL_DECODE_G(8);
   }
+#undef LL_DECODE_G
   return hipErrorInvalidValue;
 }
 
@@ -335,20 +367,29 @@ int attn_decode_chunk(int batch, int hkv, int max_ctx) {
   return chunk;
 }
 
+int attn_decode_max_ctx() { return kMaxChunk * kMaxSplit; }
+
 hipError_t launch_attn_decode(int dtype, int head_dim, const void *q, int ldq, const void *kc,
                               const void *vc, const int *lens, int len_add, void *o, int ldo,
                               int batch, int hq, int hkv, int max_ctx, int chunk, float *part_o,
                               float *part_ml, hipStream_t s) {
   if (batch <= 0) return hipSuccess;
-  if (chunk > kMaxChunk || chunk <= 0 || hq % hkv) return hipErrorInvalidValue;
+  if (chunk > kMaxChunk || chunk <= 0 || hq % hkv || (max_ctx + chunk - 1) / chunk > kMaxSplit)
+    return hipErrorInvalidValue;
+  if (!q || !kc || !vc || !lens || !o || !part_o || !part_ml)
+    return hipErrorInvalidValue;
   const int g = hq / hkv;
+#define LL_DECODE_HD(TT, HD)                                                                 \
+  return run_decode<TT, HD>(g, q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx,  \
+                            chunk, part_o, part_ml, s)
   if (dtype == kF32) {
-    if (head_dim == 64) return run_decode<float, 64>(g, q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
-    if (head_dim == 128) return run_decode<float, 128>(g, q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
+    if (head_dim == 64) LL_DECODE_HD(float, 64);
+    if (head_dim == 128) LL_DECODE_HD(float, 128);
   } else {
-    if (head_dim == 64) return run_decode<bf16, 64>(g, q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
-    if (head_dim == 128) return run_decode<bf16, 128>(g, q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, chunk, part_o, part_ml, s);
+    if (head_dim == 64) LL_DECODE_HD(bf16, 64);
+    if (head_dim == 128) LL_DECODE_HD(bf16, 128);
   }
+#undef LL_DECODE_HD
   return hipErrorInvalidValue;
 }
 

@@ -72,7 +72,11 @@ __global__ __launch_bounds__(256) void k_argmax_reduce(const float *__restrict__
   for (int i = threadIdx.x; i < n_parts; i += 256)
     better(bv, bi, pval[(size_t)r * n_parts + i], pidx[(size_t)r * n_parts + i]);
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) better(bv, bi, __shfl_xor(bv, o), __shfl_xor(bi, o));
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(bv, o);
+    const int oi = __shfl_xor(bi, o);
+    better(bv, bi, ov, oi);
+  }
   __shared__ float sv[4];
   __shared__ int si[4];
   if ((threadIdx.x & 63) == 0) {
@@ -146,8 +150,8 @@ hipError_t launch_rmsnorm(int dtype, const float *x, int ldx, const int *rowmap,
 hipError_t launch_argmax_reduce(const float *pval, const int *pidx, int rows, int n_parts,
                                 int *next, int *lens_inc, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  LL_LAUNCH(k_argmax_reduce, dim3(rows), dim3(256), 0, s, pval, pidx, n_parts, next,
-                     lens_inc);
+  if (!pval || !pidx || !next) return hipErrorInvalidValue;
+  LL_LAUNCH(k_argmax_reduce, dim3(rows), dim3(256), 0, s, pval, pidx, n_parts, next, lens_inc);
   return hipGetLastError();
 }
 

@@ -326,9 +326,16 @@ __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, in
 
 // ------------------------------------------------------------------------------------------
 // Decode GEMM (one block per 32 output columns, 8 waves splitting K)
+//
+// With NORM the A operand is RMSNorm(x) computed on the fly: the kernel streams the fp32
+// residual rows x, multiplies by the gain, rounds to T for the MFMA and accumulates sum(x^2)
+// on the side.  The per-row factor 1/sqrt(mean(x^2) + eps) of RMSNorm does not depend on
+// the column, so it scales the finished dot products in the epilogue:
+//   (x * s * g) . w = s * ((x * g) . w).
 // ------------------------------------------------------------------------------------------
-template <typename T, int MT, typename Epi>
+template <typename T, int MT, bool NORM, typename Epi>
 __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, int lda,
+                                                     NormIn norm,
                                                      const uint8_t *__restrict__ Wt, int M,
                                                      int m_base, int K, Epi epi) {
   using F = typename Frag<T>::type;
@@ -339,18 +346,48 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
   const int kb0 = (wave * kb_n) / NW, kb1 = ((wave + 1) * kb_n) / NW;
   const uint8_t *w0 = Wt + ((size_t)(2 * u) * kb_n * 64 + lane) * 16;
   const uint8_t *w1 = w0 + (size_t)kb_n * 1024;
+  const T *gain = reinterpret_cast<const T *>(norm.gain) + (lane >> 4) * EPL;
 
   f32x4 acc[MT][2];
   const T *arow[MT];
+  const float *xrow[MT];
   bool aok[MT];
+  float ss[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     acc[mt][0] = acc[mt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    ss[mt] = 0.f;
     const int row = m_base + mt * 16 + (lane & 15);
     aok[mt] = row < M;
-    arow[mt] = A + (size_t)(aok[mt] ? row : 0) * lda + (lane >> 4) * EPL;
+    const int r = aok[mt] ? row : 0;
+    if constexpr (NORM) {
+      const int src = norm.rowmap ? norm.rowmap[r] : r;
+      xrow[mt] = norm.x + (size_t)src * norm.ldx + (lane >> 4) * EPL;
+    } else {
+      arow[mt] = A + (size_t)r * lda + (lane >> 4) * EPL;
+    }
   }
   const F fz = frag_zero<F>();
+  auto a_frag = [&](int mt, int kb) -> F {
+    if (!aok[mt]) return fz;
+    if constexpr (NORM) {
+      const float *xp = xrow[mt] + (size_t)kb * TK;
+      const F g = load_frag<F>(gain + (size_t)kb * TK);
+      F a;
+#pragma unroll
+      for (int e4 = 0; e4 < EPL; e4 += 4) {
+        const float4 v = *reinterpret_cast<const float4 *>(xp + e4);
+        ss[mt] += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+        a[e4 + 0] = from_f32<T>(v.x * to_f32(g[e4 + 0]));
+        a[e4 + 1] = from_f32<T>(v.y * to_f32(g[e4 + 1]));
+        a[e4 + 2] = from_f32<T>(v.z * to_f32(g[e4 + 2]));
+        a[e4 + 3] = from_f32<T>(v.w * to_f32(g[e4 + 3]));
+      }
+      return a;
+    } else {
+      return load_frag<F>(arow[mt] + (size_t)kb * TK);
+    }
+  };
   int kb = kb0;
   for (; kb + U <= kb1; kb += U) {
     F b0[U], b1[U];
@@ -363,7 +400,7 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
     for (int q = 0; q < U; ++q)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        const F a = aok[mt] ? load_frag<F>(arow[mt] + (size_t)(kb + q) * TK) : fz;
+        const F a = a_frag(mt, kb + q);
         acc[mt][0] = mma_chunk(a, b0[q], acc[mt][0]);
         acc[mt][1] = mma_chunk(a, b1[q], acc[mt][1]);
       }
@@ -373,17 +410,24 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
     const F b1 = load_frag_stream<F>(w1 + (size_t)kb * 1024);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const F a = aok[mt] ? load_frag<F>(arow[mt] + (size_t)kb * TK) : fz;
+      const F a = a_frag(mt, kb);
       acc[mt][0] = mma_chunk(a, b0, acc[mt][0]);
       acc[mt][1] = mma_chunk(a, b1, acc[mt][1]);
     }
   }
 
   __shared__ f32x4 red[NW][MT * 2][64];
+  __shared__ float red_ss[NW][MT][16];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     red[wave][mt * 2][lane] = acc[mt][0];
     red[wave][mt * 2 + 1][lane] = acc[mt][1];
+    if constexpr (NORM) {
+      float v = ss[mt];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (lane < 16) red_ss[wave][mt][lane] = v;
+    }
   }
   __syncthreads();
   if (wave != 0) return;
@@ -394,6 +438,17 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
     for (int w = 1; w < NW; ++w) {
       s0 += red[w][mt * 2][lane];
       s1 += red[w][mt * 2 + 1][lane];
+    }
+    if constexpr (NORM) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float tot = 0.f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) tot += red_ss[w][mt][(lane >> 4) * 4 + r];
+        const float sc = 1.0f / sqrtf(tot / (float)K + norm.eps);
+        s0[r] *= sc;
+        s1[r] *= sc;
+      }
     }
     const int c = lane & 15;
 #pragma unroll
@@ -452,18 +507,21 @@ hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k
 }
 
 template <typename T, typename Epi>
-hipError_t run_skinny(const void *a, int lda, const void *wt, int m, int n, int k, const Epi &epi,
-                      hipStream_t s) {
+hipError_t run_skinny(const void *a, int lda, const NormIn *norm, const void *wt, int m, int n,
+                      int k, const Epi &epi, hipStream_t s) {
   const T *ap = reinterpret_cast<const T *>(a);
   const uint8_t *w = reinterpret_cast<const uint8_t *>(wt);
+  const NormIn nz = norm ? *norm : NormIn{};
   for (int mb = 0; mb < m; mb += 32) {
-    const int rows = m - mb;
-    if (rows <= 16)
-      LL_LAUNCH((k_gemm_skinny<T, 1, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, w,
-                         m, mb, k, epi);
+    const bool one = m - mb <= 16;
+    if (norm && one)
+      LL_LAUNCH((k_gemm_skinny<T, 1, true, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, nz, w, m, mb, k, epi);
+    else if (norm)
+      LL_LAUNCH((k_gemm_skinny<T, 2, true, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, nz, w, m, mb, k, epi);
+    else if (one)
+      LL_LAUNCH((k_gemm_skinny<T, 1, false, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, nz, w, m, mb, k, epi);
     else
-      LL_LAUNCH((k_gemm_skinny<T, 2, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, w,
-                         m, mb, k, epi);
+      LL_LAUNCH((k_gemm_skinny<T, 2, false, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, nz, w, m, mb, k, epi);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -471,17 +529,27 @@ hipError_t run_skinny(const void *a, int lda, const void *wt, int m, int n, int 
 }
 
 template <typename T, bool kTiled>
-hipError_t dispatch_epi(const void *a, int lda, const void *wt, int m, int n, int k,
-                        const EpiParams &ep, hipStream_t s) {
+hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm, const void *wt, int m, int n,
+                        int k, const EpiParams &ep, hipStream_t s) {
   auto run = [&](const auto &epi) {
     using E = std::decay_t<decltype(epi)>;
     if constexpr (kTiled) {
       if constexpr (E::kArgmax) return hipErrorInvalidValue;
       else return run_tiled<T>(a, lda, wt, m, n, k, epi, s);
     } else {
-      return run_skinny<T>(a, lda, wt, m, n, k, epi, s);
+      return run_skinny<T>(a, lda, norm, wt, m, n, k, epi, s);
     }
   };
+  // Refuse, before any launch, pointer sets that a kernel would dereference as null.
+  if (ep.kind == kEpiArgmax &&
+      (!ep.part_val || !ep.part_idx || ep.n_parts != n / 32))
+    return hipErrorInvalidValue;
+  if ((ep.kind == kEpiStore || ep.kind == kEpiResid) && !ep.out_f32) return hipErrorInvalidValue;
+  if (ep.kind == kEpiSwiglu && !ep.act) return hipErrorInvalidValue;
+  if (ep.kind == kEpiQkv && (!ep.act || !ep.kcache || !ep.vcache || !ep.row_pos ||
+                             !ep.rope_cos || !ep.rope_sin))
+    return hipErrorInvalidValue;
+  if (norm && (!norm->x || !norm->gain)) return hipErrorInvalidValue;
   switch (ep.kind) {
     case kEpiStore: return run(EpiStore{ep.out_f32, ep.ld_out});
     case kEpiResid: return run(EpiResid{ep.out_f32, ep.ld_out});
@@ -515,15 +583,16 @@ hipError_t launch_repack(int dtype, const RepackSrc &src, int n, int k, int perm
 hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, int m, int n,
                              int k, const EpiParams &ep, hipStream_t s) {
   if (m <= 0) return hipSuccess;
-  return dtype == kF32 ? dispatch_epi<float, true>(a, lda, wt, m, n, k, ep, s)
-                       : dispatch_epi<bf16, true>(a, lda, wt, m, n, k, ep, s);
+  return dtype == kF32 ? dispatch_epi<float, true>(a, lda, nullptr, wt, m, n, k, ep, s)
+                       : dispatch_epi<bf16, true>(a, lda, nullptr, wt, m, n, k, ep, s);
 }
 
-hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const void *wt, int m, int n,
-                              int k, const EpiParams &ep, hipStream_t s) {
+hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,
+                              const void *wt, int m, int n, int k, const EpiParams &ep,
+                              hipStream_t s) {
   if (m <= 0) return hipSuccess;
-  return dtype == kF32 ? dispatch_epi<float, false>(a, lda, wt, m, n, k, ep, s)
-                       : dispatch_epi<bf16, false>(a, lda, wt, m, n, k, ep, s);
+  return dtype == kF32 ? dispatch_epi<float, false>(a, lda, norm, wt, m, n, k, ep, s)
+                       : dispatch_epi<bf16, false>(a, lda, norm, wt, m, n, k, ep, s);
 }
 
 }  // namespace ll

@@ -69,18 +69,31 @@ struct EpiParams {
   int n_parts = 0;  // partials per row (= N / 32)
 };
 
+// RMSNorm computed inside the decode GEMM (A = RMSNorm(x[rowmap[r]]) * gain).
+struct NormIn {
+  const float *x = nullptr;
+  int ldx = 0;
+  const int *rowmap = nullptr;  // nullable
+  const void *gain = nullptr;
+  float eps = 0.f;
+};
+
 // Prefill GEMM: LDS-tiled MFMA, 128 x 128 block tiles.  Requires N % 128 == 0, K % 64 == 0.
 hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, int m, int n,
                              int k, const EpiParams &ep, hipStream_t s);
 // Decode GEMM: weights streamed once from HBM into MFMA operands, A read from L2.
-// Requires N % 32 == 0, K % 64 == 0; any M (rows handled 32 at a time).
-hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const void *wt, int m, int n,
-                              int k, const EpiParams &ep, hipStream_t s);
+// Requires N % 32 == 0, K % 64 == 0; any M (rows handled 32 at a time).  With `norm` the A
+// operand is RMSNorm of fp32 rows computed in the kernel (`a` is then unused).
+hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,
+                              const void *wt, int m, int n, int k, const EpiParams &ep,
+                              hipStream_t s);
 
 hipError_t launch_embed(int dtype, const int *tokens, int ntok, const void *table, int vocab,
                         int d, float *x, int *err_flags, hipStream_t s);
 hipError_t launch_rmsnorm(int dtype, const float *x, int ldx, const int *rowmap, int rows,
                           int d, const void *gain, float eps, void *y, int ldy, hipStream_t s);
+// next[r] = column of the largest argmax partial of row r (lowest column on ties); lens_inc[r]
+// += 1 when lens_inc is given.
 hipError_t launch_argmax_reduce(const float *part_val, const int *part_idx, int rows,
                                 int n_parts, int *next, int *lens_inc, hipStream_t s);
 
@@ -100,8 +113,10 @@ hipError_t launch_attn_prefill(int dtype, int head_dim, const void *q, int ldq,
                                const int *cu_seqlens, const int2 *qtiles, int n_qtiles,
                                int n_heads, int n_kv_heads, int max_ctx, hipStream_t s);
 
-// Decode attention: split over the cache length (chunk keys per block) + combine.
+// Decode attention: split over the cache length (chunk keys per block), then a merge kernel.
+// Keys attended per sequence: lens[b] + len_add (clamped to max_ctx).
 int attn_decode_chunk(int batch, int n_kv_heads, int max_ctx);
+int attn_decode_max_ctx();
 hipError_t launch_attn_decode(int dtype, int head_dim, const void *q, int ldq,
                               const void *kcache, const void *vcache, const int *lens,
                               int len_add, void *o, int ldo, int batch, int n_heads,

@@ -129,6 +129,8 @@ ll_status validate_config(const ll_config *c) {
   if (c->vocab % 32) return fail(LL_ERR_UNSUPPORTED, "vocab %d not a multiple of 32", c->vocab);
   if (c->max_batch > LL_MAX_BATCH)
     return fail(LL_ERR_UNSUPPORTED, "max_batch %d > %d", c->max_batch, LL_MAX_BATCH);
+  if (c->max_ctx > attn_decode_max_ctx())
+    return fail(LL_ERR_UNSUPPORTED, "max_ctx %d > %d", c->max_ctx, attn_decode_max_ctx());
   return LL_OK;
 }
 
@@ -267,22 +269,43 @@ EpiParams argmax_epi(const ll_model *m, float *logits) {
   return ep;
 }
 
+// Decode batches up to this size normalise inside the decode GEMM (the fp32 rows are then
+// read by every column block, which stays cheap only for a few rows).
+constexpr int kFusedNormMaxRows = 16;
+
 // The decoder layers for `rows` rows.  decode: one row per sequence at position len[b].
 ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipStream_t s) {
   const ll_config &c = m->cfg;
   const int d = c.d_model, qd = c.n_heads * c.head_dim, F = c.ffn_dim;
   const int dt = c.dtype;
-  auto gemm = decode ? launch_gemm_skinny : launch_gemm_tiled;
+  const bool fuse_norm = decode && rows <= kFusedNormMaxRows;
   float *x = m->at<float>(m->L.x);
-  for (int l = 0; l < c.n_layers; ++l) {
+  auto gemm = [&](const void *a, int lda, const NormIn *nrm, const void *wt, int n, int k,
+                  const EpiParams &ep) {
+    return decode ? launch_gemm_skinny(dt, a, lda, nrm, wt, rows, n, k, ep, s)
+                  : launch_gemm_tiled(dt, a, lda, wt, rows, n, k, ep, s);
+  };
+  // The A operand of a projection that follows an RMSNorm: normalised in the GEMM, or by a
+  // separate row kernel into h.
+  auto normed = [&](size_t gain_off, NormIn *nrm) -> ll_status {
+    if (fuse_norm) {
+      *nrm = NormIn{x, d, nullptr, m->at(gain_off), c.rms_eps};
+      return LL_OK;
+    }
     m->mark(LL_K_RMSNORM);
-    LL_HIP(launch_rmsnorm(dt, x, d, nullptr, rows, d, m->at(m->L.attn_norm[l]), c.rms_eps,
+    LL_HIP(launch_rmsnorm(dt, x, d, nullptr, rows, d, m->at(gain_off), c.rms_eps,
                           m->at(m->L.h), d, s));
+    return LL_OK;
+  };
+  for (int l = 0; l < c.n_layers; ++l) {
+    NormIn nrm;
+    ll_status st = normed(m->L.attn_norm[l], &nrm);
+    if (st != LL_OK) return st;
     const int *row_seq = decode ? nullptr : m->at<int>(m->L.row_seq);
     const int *row_pos = decode ? m->at<int>(m->L.lens) : m->at<int>(m->L.row_pos);
     m->mark(LL_K_QKV);
-    LL_HIP(gemm(dt, m->at(m->L.h), d, m->at(m->L.wqkv[l]), rows, m->L.n_qkv, d,
-                qkv_epi(m, l, row_seq, row_pos), s));
+    LL_HIP(gemm(m->at(m->L.h), d, fuse_norm ? &nrm : nullptr, m->at(m->L.wqkv[l]), m->L.n_qkv,
+                d, qkv_epi(m, l, row_seq, row_pos)));
     m->mark(LL_K_ATTN);
     if (decode) {
       LL_HIP(launch_attn_decode(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
@@ -296,31 +319,36 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
                                  c.max_ctx, s));
     }
     m->mark(LL_K_O);
-    LL_HIP(gemm(dt, m->at(m->L.o), qd, m->at(m->L.wo[l]), rows, d, qd, resid_epi(m), s));
-    m->mark(LL_K_RMSNORM);
-    LL_HIP(launch_rmsnorm(dt, x, d, nullptr, rows, d, m->at(m->L.mlp_norm[l]), c.rms_eps,
-                          m->at(m->L.h), d, s));
+    LL_HIP(gemm(m->at(m->L.o), qd, nullptr, m->at(m->L.wo[l]), d, qd, resid_epi(m)));
+    st = normed(m->L.mlp_norm[l], &nrm);
+    if (st != LL_OK) return st;
     m->mark(LL_K_GATE_UP);
-    LL_HIP(gemm(dt, m->at(m->L.h), d, m->at(m->L.wgu[l]), rows, 2 * F, d, swiglu_epi(m), s));
+    LL_HIP(gemm(m->at(m->L.h), d, fuse_norm ? &nrm : nullptr, m->at(m->L.wgu[l]), 2 * F, d,
+                swiglu_epi(m)));
     m->mark(LL_K_DOWN);
-    LL_HIP(gemm(dt, m->at(m->L.act), F, m->at(m->L.wd[l]), rows, d, F, resid_epi(m), s));
+    LL_HIP(gemm(m->at(m->L.act), F, nullptr, m->at(m->L.wd[l]), d, F, resid_epi(m)));
   }
   return LL_OK;
 }
 
-// Final RMSNorm of one row per sequence, LM head with fused argmax partials, reduction.
+// Final RMSNorm of one row per sequence, the LM head with per-block argmax partials, and the
+// reduction that writes `next` (and advances `lens_inc`).
 ll_status enqueue_head(ll_model *m, int batch, const int *rowmap, int *next, float *logits,
                        int *lens_inc, hipStream_t s) {
   const ll_config &c = m->cfg;
-  m->mark(LL_K_RMSNORM);
-  LL_HIP(launch_rmsnorm(c.dtype, m->at<float>(m->L.x), c.d_model, rowmap, batch, c.d_model,
-                        m->at(m->L.final_norm), c.rms_eps, m->at(m->L.hf), c.d_model, s));
+  EpiParams ep = argmax_epi(m, logits);
+  NormIn nrm{m->at<float>(m->L.x), c.d_model, rowmap, m->at(m->L.final_norm), c.rms_eps};
+  const bool fuse_norm = batch <= kFusedNormMaxRows;
+  if (!fuse_norm) {
+    m->mark(LL_K_RMSNORM);
+    LL_HIP(launch_rmsnorm(c.dtype, m->at<float>(m->L.x), c.d_model, rowmap, batch, c.d_model,
+                          m->at(m->L.final_norm), c.rms_eps, m->at(m->L.hf), c.d_model, s));
+  }
   m->mark(LL_K_LM_HEAD);
-  LL_HIP(launch_gemm_skinny(c.dtype, m->at(m->L.hf), c.d_model, m->at(m->L.lm_head), batch,
-                            c.vocab, c.d_model, argmax_epi(m, logits), s));
+  LL_HIP(launch_gemm_skinny(c.dtype, m->at(m->L.hf), c.d_model, fuse_norm ? &nrm : nullptr,
+                            m->at(m->L.lm_head), batch, c.vocab, c.d_model, ep, s));
   m->mark(LL_K_ARGMAX);
-  LL_HIP(launch_argmax_reduce(m->at<float>(m->L.pval), m->at<int>(m->L.pidx), batch,
-                              m->L.n_parts, next, lens_inc, s));
+  LL_HIP(launch_argmax_reduce(ep.part_val, ep.part_idx, batch, ep.n_parts, next, lens_inc, s));
   return LL_OK;
 }
 
@@ -435,6 +463,7 @@ ll_status ll_model_load(const ll_config *cfg, const ll_weights *w, void *workspa
   LOAD_HIP(hipMemcpyAsync(m->at(L.rcos), hc, (size_t)c.max_ctx * half * 4, hipMemcpyHostToDevice, s));
   LOAD_HIP(hipMemcpyAsync(m->at(L.rsin), hs, (size_t)c.max_ctx * half * 4, hipMemcpyHostToDevice, s));
   LOAD_HIP(hipMemsetAsync(m->at(L.err), 0, 4, s));
+
 #undef LOAD_HIP
   *out = m;
   return LL_OK;
@@ -649,7 +678,7 @@ ll_status ll_op_gemm(int32_t path, int32_t dtype, int32_t m, int32_t n, int32_t 
   ep.out_f32 = c;
   ep.ld_out = n;
   LL_HIP(path == 0 ? launch_gemm_tiled(dtype, a, k, wt, m, n, k, ep, (hipStream_t)stream)
-                   : launch_gemm_skinny(dtype, a, k, wt, m, n, k, ep, (hipStream_t)stream));
+                   : launch_gemm_skinny(dtype, a, k, nullptr, wt, m, n, k, ep, (hipStream_t)stream));
   return LL_OK;
 }
 
@@ -730,6 +759,8 @@ ll_status ll_op_attn_decode(int32_t dtype, int32_t batch, int32_t n_heads, int32
   float *pml = reinterpret_cast<float *>(reinterpret_cast<char *>(scratch) +
                                          align_up((size_t)batch * n_heads * nsplit * head_dim * 4));
   const int qd = n_heads * head_dim;
+  if (max_ctx > attn_decode_max_ctx())
+    return fail(LL_ERR_UNSUPPORTED, "max_ctx %d > %d", max_ctx, attn_decode_max_ctx());
   LL_HIP(launch_attn_decode(dtype, head_dim, q, qd, kcache, vcache, ctx_lens_dev, 0, o, qd, batch,
                             n_heads, n_kv_heads, max_ctx, chunk, po, pml, (hipStream_t)stream));
   return LL_OK;
@@ -754,7 +785,7 @@ ll_status ll_op_lmhead_argmax(int32_t dtype, int32_t rows, int32_t vocab, int32_
   ep.part_idx = reinterpret_cast<int *>(reinterpret_cast<char *>(scratch) + parts * 4);
   ep.n_parts = vocab / 32;
   hipStream_t s = (hipStream_t)stream;
-  LL_HIP(launch_gemm_skinny(dtype, h, k, wt, rows, vocab, k, ep, s));
+  LL_HIP(launch_gemm_skinny(dtype, h, k, nullptr, wt, rows, vocab, k, ep, s));
   LL_HIP(launch_argmax_reduce(ep.part_val, ep.part_idx, rows, ep.n_parts, next, nullptr, s));
   return LL_OK;
 }
