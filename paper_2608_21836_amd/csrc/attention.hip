@@ -14,6 +14,7 @@
 // output) per head; a second kernel merges the splits with
 // log-sum-exp weights (fixed order, so the result does not depend on block order).
 #include <algorithm>
+#include <cmath>
 
 #include "device_common.h"
 #include "kernels.h"
@@ -138,33 +139,36 @@ __global__ __launch_bounds__(256) void k_attn_prefill(
   }
 }
 
-constexpr int kMaxChunk = 256;  // keys per decode-attention block
 constexpr int kMaxSplit = 128;  // blocks per (sequence, kv head)
 
-// Decode attention for one (split, kv head, sequence): exact scores of up to kMaxChunk cached
-// keys for all G query heads of the group (each K and V row read once), chunk softmax
-// statistics and the unnormalised partial output.  A second kernel merges the splits: a
-// kernel boundary makes every block's partials visible across XCDs once per launch, where a
-// device-scope fence in each block would write back the L2 once per block.
-template <typename T, int HD, int G>
+// Decode attention for one (split, kv head, sequence): the block covers up to KPT * NSLOT
+// cached keys in one pass.  Every thread requests all of its K rows before using the first
+// (then all of its V rows), so a block has its whole chunk in flight at once; each K and V row
+// is read once for all G query heads of the group.  With a single split the block normalises
+// and writes the attention output; otherwise it writes (max, sum, unnormalised output) for the
+// merge kernel.  The merge is a separate kernel: a kernel boundary makes every block's
+// partials visible across XCDs once per launch, where a device-scope fence in each block
+// would write back the L2 once per block.
+template <typename T, int HD, int G, int KPT>
 __global__ __launch_bounds__(256) void k_attn_decode(
     const T *__restrict__ Q, int ldq, const T *__restrict__ Kc, const T *__restrict__ Vc,
-    const int *__restrict__ lens, int len_add, int hkv, int max_ctx, int chunk, int nsplit,
-    float *__restrict__ part_o, float *__restrict__ part_ml, float scale_log2) {
+    const int *__restrict__ lens, int len_add, int hkv, int max_ctx, int kpb, int nsplit,
+    float *__restrict__ part_o, float *__restrict__ part_ml, T *__restrict__ O, int ldo,
+    float scale_log2) {
   using F = typename Frag<T>::type;
   constexpr int EPL = Frag<T>::EPL;
-  constexpr int LPK = HD / EPL;           // lanes per cached row
-  constexpr int NSLOT = 256 / LPK;        // rows in flight per pass
-  constexpr int KPT = kMaxChunk / NSLOT;  // rows per thread at the largest chunk
+  constexpr int LPK = HD / EPL;         // lanes per cached row
+  constexpr int NSLOT = 256 / LPK;      // rows in flight per pass
+  constexpr int CH = KPT * NSLOT;       // largest chunk
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int S = min(lens[b] + len_add, max_ctx);  // never read past the cache capacity
-  const int j0 = split * chunk;
+  const int j0 = split * kpb;
   if (j0 >= S) return;
-  const int j1 = min(j0 + chunk, S), n = j1 - j0;
+  const int n = min(min(kpb, CH), S - j0);
   const int tid = threadIdx.x, dl = tid % LPK, slot = tid / LPK;
   const int lane = tid & 63, wave = tid >> 6;
   const int hq = hkv * G;
-  __shared__ float s_p[G][kMaxChunk];
+  __shared__ float s_p[G][CH];
   __shared__ float s_red[4][G][HD];
   __shared__ float s_m[G], s_l[G];
   const F fz = frag_zero<F>();
@@ -176,17 +180,16 @@ __global__ __launch_bounds__(256) void k_attn_decode(
 #pragma unroll
     for (int e = 0; e < EPL; ++e) qv[g][e] = to_f32(qq[e]) * scale_log2;
   }
-  const size_t kvbase = ((size_t)b * hkv + kvh) * max_ctx * HD;
+  const size_t kvbase = ((size_t)b * hkv + kvh) * max_ctx * HD + (size_t)j0 * HD;
   const T *Kb = Kc + kvbase + dl * EPL;
   const T *Vb = Vc + kvbase + dl * EPL;
 
-  // Scores: all of this thread's K rows are requested before the first one is used.
   F rows[KPT];
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
     if (i * NSLOT >= n) break;
-    const int j = j0 + slot + i * NSLOT;
-    rows[i] = j < j1 ? load_frag_stream<F>(Kb + (size_t)j * HD) : fz;
+    const int jj = slot + i * NSLOT;
+    rows[i] = jj < n ? load_frag_stream<F>(Kb + (size_t)jj * HD) : fz;
   }
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
@@ -208,12 +211,12 @@ __global__ __launch_bounds__(256) void k_attn_decode(
 #pragma unroll
       for (int g = 0; g < G; ++g) s_p[g][jj] = d[g];
   }
-  // V rows of this thread, requested while the chunk softmax runs.
+  // V rows, requested while the chunk softmax runs
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
     if (i * NSLOT >= n) break;
-    const int j = j0 + slot + i * NSLOT;
-    rows[i] = j < j1 ? load_frag_stream<F>(Vb + (size_t)j * HD) : fz;
+    const int jj = slot + i * NSLOT;
+    rows[i] = jj < n ? load_frag_stream<F>(Vb + (size_t)jj * HD) : fz;
   }
   __syncthreads();
   for (int g = wave; g < G; g += 4) {
@@ -266,25 +269,29 @@ __global__ __launch_bounds__(256) void k_attn_decode(
   for (int i = tid; i < G * HD; i += 256) {
     const int g = i / HD, d = i % HD;
     const float v = s_red[0][g][d] + s_red[1][g][d] + s_red[2][g][d] + s_red[3][g][d];
-    part_o[(((size_t)b * hq + kvh * G + g) * nsplit + split) * HD + d] = v;
+    if (nsplit == 1)
+      O[(size_t)b * ldo + (kvh * G + g) * HD + d] = from_f32<T>(v / s_l[g]);
+    else
+      part_o[(((size_t)b * hq + kvh * G + g) * nsplit + split) * HD + d] = v;
   }
-  if (tid < G) {
+  if (nsplit > 1 && tid < G) {
     float *ml = part_ml + (((size_t)b * hq + kvh * G + tid) * nsplit + split) * 2;
     ml[0] = s_m[tid];
     ml[1] = s_l[tid];
   }
 }
 
-// Merge of the splits of one (query head, sequence): log-sum-exp weights, fixed split order.
+// Merge of the splits of one (query head, sequence): log-sum-exp weights in a fixed split
+// order, so the result does not depend on which block finished first.
 template <typename T, int HD>
 __global__ __launch_bounds__(HD) void k_attn_combine(const float *__restrict__ part_o,
                                                       const float *__restrict__ part_ml,
                                                       const int *__restrict__ lens, int len_add,
-                                                      int hq, int chunk, int nsplit, int max_ctx,
+                                                      int hq, int kpb, int nsplit, int max_ctx,
                                                       T *__restrict__ O, int ldo) {
   const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
   const int S = min(lens[b] + len_add, max_ctx);
-  const int ns = (S + chunk - 1) / chunk;
+  const int ns = (S + kpb - 1) / kpb;
   const size_t base = ((size_t)b * hq + h) * nsplit;
   float mx = -INFINITY;
   for (int sp = 0; sp < ns; ++sp) mx = fmaxf(mx, part_ml[(base + sp) * 2]);
@@ -309,31 +316,40 @@ hipError_t run_prefill(const void *q, int ldq, const void *kc, const void *vc, v
   return hipGetLastError();
 }
 
+// Rows per thread so that a block covers kMaxChunk keys.  (Measured on MI355X: fewer, larger
+// blocks -- a whole short cache per block, or a loop over chunks inside a block -- were
+// slower than more blocks plus the merge kernel: one CU cannot stream a cache fast enough.)
+constexpr int kMaxChunk = 256;
+template <int HD, int EPL> constexpr int kChunkKpt = kMaxChunk / (256 / (HD / EPL));
+
 template <typename T, int HD, int G>
 hipError_t run_decode_g(const void *q, int ldq, const void *kc, const void *vc, const int *lens,
                         int len_add, void *o, int ldo, int batch, int hkv, int max_ctx,
-                        int chunk, float *part_o, float *part_ml, hipStream_t s) {
-  const int nsplit = (max_ctx + chunk - 1) / chunk;
+                        const AttnDecodePlan &plan, float *part_o, float *part_ml,
+                        hipStream_t s) {
   const float scale_log2 = kLog2e / sqrtf((float)HD);
-  LL_LAUNCH((k_attn_decode<T, HD, G>), dim3(nsplit, hkv, batch), dim3(256), 0, s,
-            reinterpret_cast<const T *>(q), ldq, reinterpret_cast<const T *>(kc),
-            reinterpret_cast<const T *>(vc), lens, len_add, hkv, max_ctx, chunk, nsplit, part_o,
-            part_ml, scale_log2);
+  constexpr int EPL = Frag<T>::EPL;
+  LL_LAUNCH((k_attn_decode<T, HD, G, kChunkKpt<HD, EPL>>), dim3(plan.nsplit, hkv, batch),
+            dim3(256), 0, s, reinterpret_cast<const T *>(q), ldq,
+            reinterpret_cast<const T *>(kc), reinterpret_cast<const T *>(vc), lens, len_add,
+            hkv, max_ctx, plan.kpb, plan.nsplit, part_o, part_ml, reinterpret_cast<T *>(o), ldo,
+            scale_log2);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || plan.nsplit == 1) return e;
   if (g_launch_timer) g_launch_timer->secondary();
   LL_LAUNCH((k_attn_combine<T, HD>), dim3(hkv * G, batch), dim3(HD), 0, s, part_o, part_ml, lens,
-            len_add, hkv * G, chunk, nsplit, max_ctx, reinterpret_cast<T *>(o), ldo);
+            len_add, hkv * G, plan.kpb, plan.nsplit, max_ctx, reinterpret_cast<T *>(o), ldo);
   return hipGetLastError();
 }
 
 template <typename T, int HD>
 hipError_t run_decode(int group, const void *q, int ldq, const void *kc, const void *vc,
                       const int *lens, int len_add, void *o, int ldo, int batch, int hkv,
-                      int max_ctx, int chunk, float *part_o, float *part_ml, hipStream_t s) {
+                      int max_ctx, const AttnDecodePlan &plan, float *part_o, float *part_ml,
+                      hipStream_t s) {
 #define LL_DECODE_G(G)                                                                       \
   return run_decode_g<T, HD, G>(q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, \
-                                chunk, part_o, part_ml, s)
+                                plan, part_o, part_ml, s)
   switch (group) {
     case 1: LL_DECODE_G(1);
     case 2: LL_DECODE_G(2);
@@ -361,27 +377,37 @@ hipError_t launch_attn_prefill(int dtype, int head_dim, const void *q, int ldq, 
   return hipErrorInvalidValue;
 }
 
-int attn_decode_chunk(int batch, int hkv, int max_ctx) {
+AttnDecodePlan attn_decode_plan(int head_dim, int elem_bytes, int batch, int hkv,
+                                int max_ctx) {
+  AttnDecodePlan p;
+  (void)head_dim;
+  (void)elem_bytes;
+  // Chunks of 256 keys, halved (down to 64) until there are ~1024 blocks; a cache that fits
+  // one chunk needs no merge.
   int chunk = kMaxChunk;
   while (chunk > 64 && (long)batch * hkv * ((max_ctx + chunk - 1) / chunk) < 1024) chunk >>= 1;
-  return chunk;
+  while ((max_ctx + chunk - 1) / chunk > kMaxSplit) chunk <<= 1;  // only for caches > 8192 keys
+  p.kpb = chunk;
+  p.nsplit = (max_ctx + chunk - 1) / chunk;
+  return p;
 }
 
-int attn_decode_max_ctx() { return kMaxChunk * kMaxSplit; }
+int attn_decode_max_ctx() { return kMaxSplit * 256; }
 
 hipError_t launch_attn_decode(int dtype, int head_dim, const void *q, int ldq, const void *kc,
                               const void *vc, const int *lens, int len_add, void *o, int ldo,
-                              int batch, int hq, int hkv, int max_ctx, int chunk, float *part_o,
-                              float *part_ml, hipStream_t s) {
+                              int batch, int hq, int hkv, int max_ctx, const AttnDecodePlan &plan,
+                              float *part_o, float *part_ml, hipStream_t s) {
   if (batch <= 0) return hipSuccess;
-  if (chunk > kMaxChunk || chunk <= 0 || hq % hkv || (max_ctx + chunk - 1) / chunk > kMaxSplit)
+  if (plan.kpb <= 0 || plan.nsplit < 1 || plan.nsplit > kMaxSplit || hq % hkv ||
+      (long)plan.kpb * plan.nsplit < max_ctx || plan.kpb > kMaxChunk)
     return hipErrorInvalidValue;
-  if (!q || !kc || !vc || !lens || !o || !part_o || !part_ml)
+  if (!q || !kc || !vc || !lens || !o || (plan.nsplit > 1 && (!part_o || !part_ml)))
     return hipErrorInvalidValue;
   const int g = hq / hkv;
 #define LL_DECODE_HD(TT, HD)                                                                 \
   return run_decode<TT, HD>(g, q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx,  \
-                            chunk, part_o, part_ml, s)
+                            plan, part_o, part_ml, s)
   if (dtype == kF32) {
     if (head_dim == 64) LL_DECODE_HD(float, 64);
     if (head_dim == 128) LL_DECODE_HD(float, 128);

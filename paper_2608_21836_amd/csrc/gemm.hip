@@ -54,29 +54,31 @@ __global__ void k_repack(RepackSrc src, int n, int k, int perm, int hd, int ffn,
 struct EpiStore {
   float *out;
   int ld;
-  static constexpr bool kArgmax = false;
+  static constexpr bool kArgmax = false, kPairs = false;
   __device__ void operator()(int m, int u, int c, float v0, float v1) const {
     float *p = out + (size_t)m * ld + 32 * u + c;
     p[0] = v0;
     p[16] = v1;
   }
+  __device__ void one(int m, int col, float v) const { out[(size_t)m * ld + col] = v; }
 };
 
 struct EpiResid {
   float *out;
   int ld;
-  static constexpr bool kArgmax = false;
+  static constexpr bool kArgmax = false, kPairs = false;
   __device__ void operator()(int m, int u, int c, float v0, float v1) const {
     float *p = out + (size_t)m * ld + 32 * u + c;
     p[0] += v0;
     p[16] += v1;
   }
+  __device__ void one(int m, int col, float v) const { out[(size_t)m * ld + col] += v; }
 };
 
 template <typename T> struct EpiSwiglu {
   T *out;
   int ld;
-  static constexpr bool kArgmax = false;
+  static constexpr bool kArgmax = false, kPairs = true;
   __device__ void operator()(int m, int u, int c, float g, float up) const {
     out[(size_t)m * ld + 16 * u + c] = from_f32<T>(silu_f(g) * up);
   }
@@ -89,7 +91,7 @@ template <typename T> struct EpiQkv {
   const int *row_seq, *row_pos;
   const float *rcos, *rsin;
   int hq, hkv, hd, max_ctx;
-  static constexpr bool kArgmax = false;
+  static constexpr bool kArgmax = false, kPairs = true;
   __device__ void operator()(int m, int u, int c, float v0, float v1) const {
     const int n0 = u * 32;
     const int head = n0 / hd;
@@ -123,7 +125,7 @@ struct EpiArgmax {
   float *pval;
   int *pidx;
   int n_parts;
-  static constexpr bool kArgmax = true;
+  static constexpr bool kArgmax = true, kPairs = true;
 };
 
 // ------------------------------------------------------------------------------------------
@@ -325,7 +327,10 @@ __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, in
 }
 
 // ------------------------------------------------------------------------------------------
-// Decode GEMM (one block per 32 output columns, 8 waves splitting K)
+// Decode GEMM: one block per NB x 16 output columns (NB = 2: one 32-column pair unit; NB = 1:
+// a single 16-column block, for element-wise epilogues when pairs would leave CUs idle), 8
+// waves splitting K, partial sums reduced through LDS.  Each wave requests U weight tiles per
+// n-block before using the first.
 //
 // With NORM the A operand is RMSNorm(x) computed on the fly: the kernel streams the fp32
 // residual rows x, multiplies by the gain, rounds to T for the MFMA and accumulates sum(x^2)
@@ -333,121 +338,131 @@ __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, in
 // the column, so it scales the finished dot products in the epilogue:
 //   (x * s * g) . w = s * ((x * g) . w).
 // ------------------------------------------------------------------------------------------
-template <typename T, int MT, bool NORM, typename Epi>
+template <typename T, int MT, int NB, bool NORM, typename Epi>
 __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, int lda,
                                                      NormIn norm,
                                                      const uint8_t *__restrict__ Wt, int M,
                                                      int m_base, int K, Epi epi) {
   using F = typename Frag<T>::type;
-  constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL, NW = 8, U = 4;
+  constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL, NW = 8, U = 16 / NB;
+  static_assert(!NORM || MT == 1, "the normalised operand is staged for up to 16 rows");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int u = blockIdx.x;
+  const int blk = blockIdx.x;
   const int kb_n = K / TK;
   const int kb0 = (wave * kb_n) / NW, kb1 = ((wave + 1) * kb_n) / NW;
-  const uint8_t *w0 = Wt + ((size_t)(2 * u) * kb_n * 64 + lane) * 16;
-  const uint8_t *w1 = w0 + (size_t)kb_n * 1024;
-  const T *gain = reinterpret_cast<const T *>(norm.gain) + (lane >> 4) * EPL;
+  const uint8_t *wp[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) wp[j] = Wt + ((size_t)(NB * blk + j) * kb_n * 64 + lane) * 16;
+  const F fz = frag_zero<F>();
 
-  f32x4 acc[MT][2];
+  f32x4 acc[MT][NB];
   const T *arow[MT];
-  const float *xrow[MT];
   bool aok[MT];
-  float ss[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
-    acc[mt][0] = acc[mt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-    ss[mt] = 0.f;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) acc[mt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int row = m_base + mt * 16 + (lane & 15);
     aok[mt] = row < M;
-    const int r = aok[mt] ? row : 0;
-    if constexpr (NORM) {
-      const int src = norm.rowmap ? norm.rowmap[r] : r;
-      xrow[mt] = norm.x + (size_t)src * norm.ldx + (lane >> 4) * EPL;
-    } else {
-      arow[mt] = A + (size_t)r * lda + (lane >> 4) * EPL;
-    }
+    arow[mt] = A + (size_t)(aok[mt] ? row : 0) * lda + (lane >> 4) * EPL;
   }
-  const F fz = frag_zero<F>();
-  auto a_frag = [&](int mt, int kb) -> F {
-    if (!aok[mt]) return fz;
-    if constexpr (NORM) {
-      const float *xp = xrow[mt] + (size_t)kb * TK;
-      const F g = load_frag<F>(gain + (size_t)kb * TK);
-      F a;
-#pragma unroll
-      for (int e4 = 0; e4 < EPL; e4 += 4) {
-        const float4 v = *reinterpret_cast<const float4 *>(xp + e4);
-        ss[mt] += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-        a[e4 + 0] = from_f32<T>(v.x * to_f32(g[e4 + 0]));
-        a[e4 + 1] = from_f32<T>(v.y * to_f32(g[e4 + 1]));
-        a[e4 + 2] = from_f32<T>(v.z * to_f32(g[e4 + 2]));
-        a[e4 + 3] = from_f32<T>(v.w * to_f32(g[e4 + 3]));
-      }
-      return a;
-    } else {
-      return load_frag<F>(arow[mt] + (size_t)kb * TK);
-    }
-  };
-  int kb = kb0;
-  for (; kb + U <= kb1; kb += U) {
-    F b0[U], b1[U];
-#pragma unroll
-    for (int q = 0; q < U; ++q) {
-      b0[q] = load_frag_stream<F>(w0 + (size_t)(kb + q) * 1024);
-      b1[q] = load_frag_stream<F>(w1 + (size_t)(kb + q) * 1024);
-    }
+
+  // The first batch of weight tiles is requested before anything else.
+  F bw[U][NB];
+  auto load_w = [&](int kb) {
 #pragma unroll
     for (int q = 0; q < U; ++q)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const F a = a_frag(mt, kb + q);
-        acc[mt][0] = mma_chunk(a, b0[q], acc[mt][0]);
-        acc[mt][1] = mma_chunk(a, b1[q], acc[mt][1]);
+      for (int j = 0; j < NB; ++j)
+        bw[q][j] = kb + q < kb1 ? load_frag_stream<F>(wp[j] + (size_t)(kb + q) * 1024) : fz;
+  };
+  load_w(kb0);
+
+  // NORM: stage (x * gain) of the block's rows in LDS (row stride K + EPL elements to spread
+  // banks) and the per-row sum of squares; the factor 1/sqrt(mean(x^2) + eps) is applied to
+  // the finished dot products.
+  extern __shared__ __attribute__((aligned(16))) uint8_t dyn_smem[];
+  T *sA = reinterpret_cast<T *>(dyn_smem);
+  __shared__ float s_ss[NW][16];
+  const int nrows = min(M - m_base, 16);
+  const int lds_ld = K + EPL;
+  if constexpr (NORM) {
+    const T *g = reinterpret_cast<const T *>(norm.gain);
+    const int k4n = K / 4;
+    for (int r = 0; r < nrows; ++r) {
+      const int src = norm.rowmap ? norm.rowmap[m_base + r] : m_base + r;
+      const float4 *xr = reinterpret_cast<const float4 *>(norm.x + (size_t)src * norm.ldx);
+      float part = 0.f;
+      for (int k4 = threadIdx.x; k4 < k4n; k4 += 512) {
+        const float4 v = xr[k4];
+        part += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+        T *d = sA + (size_t)r * lds_ld + 4 * k4;
+        d[0] = from_f32<T>(v.x * to_f32(g[4 * k4 + 0]));
+        d[1] = from_f32<T>(v.y * to_f32(g[4 * k4 + 1]));
+        d[2] = from_f32<T>(v.z * to_f32(g[4 * k4 + 2]));
+        d[3] = from_f32<T>(v.w * to_f32(g[4 * k4 + 3]));
       }
-  }
-  for (; kb < kb1; ++kb) {
-    const F b0 = load_frag_stream<F>(w0 + (size_t)kb * 1024);
-    const F b1 = load_frag_stream<F>(w1 + (size_t)kb * 1024);
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const F a = a_frag(mt, kb);
-      acc[mt][0] = mma_chunk(a, b0, acc[mt][0]);
-      acc[mt][1] = mma_chunk(a, b1, acc[mt][1]);
+      part = wave_sum(part);
+      if (lane == 0) s_ss[wave][r] = part;
     }
+    __syncthreads();
+  }
+  auto a_frag = [&](int mt, int kb) -> F {
+    if constexpr (NORM) {
+      const int r = lane & 15;
+      return r < nrows ? *reinterpret_cast<const F *>(sA + (size_t)r * lds_ld + kb * TK +
+                                                       (lane >> 4) * EPL)
+                       : fz;
+    } else {
+      return aok[mt] ? load_frag<F>(arow[mt] + (size_t)kb * TK) : fz;
+    }
+  };
+
+  // Batches of U k-tiles, the last one predicated (uniformly per wave); the activation
+  // fragments of a batch are requested together with its weight tiles.
+  for (int kb = kb0; kb < kb1; kb += U) {
+    if (kb != kb0) load_w(kb);
+    F av[U][MT];
+#pragma unroll
+    for (int q = 0; q < U; ++q)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) av[q][mt] = kb + q < kb1 ? a_frag(mt, kb + q) : fz;
+    // Tiles past kb1 were loaded as zeros, so their products add exactly nothing.
+#pragma unroll
+    for (int q = 0; q < U; ++q)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) acc[mt][j] = mma_chunk(av[q][mt], bw[q][j], acc[mt][j]);
   }
 
-  __shared__ f32x4 red[NW][MT * 2][64];
-  __shared__ float red_ss[NW][MT][16];
+  __shared__ f32x4 red[NW][MT * NB][64];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    red[wave][mt * 2][lane] = acc[mt][0];
-    red[wave][mt * 2 + 1][lane] = acc[mt][1];
-    if constexpr (NORM) {
-      float v = ss[mt];
-      v += __shfl_xor(v, 16);
-      v += __shfl_xor(v, 32);
-      if (lane < 16) red_ss[wave][mt][lane] = v;
-    }
-  }
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int j = 0; j < NB; ++j) red[wave][mt * NB + j][lane] = acc[mt][j];
   __syncthreads();
   if (wave != 0) return;
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
-    f32x4 s0 = red[0][mt * 2][lane], s1 = red[0][mt * 2 + 1][lane];
+    f32x4 sv[NB];
 #pragma unroll
-    for (int w = 1; w < NW; ++w) {
-      s0 += red[w][mt * 2][lane];
-      s1 += red[w][mt * 2 + 1][lane];
+    for (int j = 0; j < NB; ++j) {
+      sv[j] = red[0][mt * NB + j][lane];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) sv[j] += red[w][mt * NB + j][lane];
     }
     if constexpr (NORM) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
+        const int rr = (lane >> 4) * 4 + r;
         float tot = 0.f;
+        if (rr < nrows)
 #pragma unroll
-        for (int w = 0; w < NW; ++w) tot += red_ss[w][mt][(lane >> 4) * 4 + r];
+          for (int w = 0; w < NW; ++w) tot += s_ss[w][rr];
         const float sc = 1.0f / sqrtf(tot / (float)K + norm.eps);
-        s0[r] *= sc;
-        s1[r] *= sc;
+#pragma unroll
+        for (int j = 0; j < NB; ++j) sv[j][r] *= sc;
       }
     }
     const int c = lane & 15;
@@ -455,15 +470,16 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
     for (int r = 0; r < 4; ++r) {
       const int m = m_base + mt * 16 + (lane >> 4) * 4 + r;
       if constexpr (Epi::kArgmax) {
-        const int col0 = 32 * u + c;
+        static_assert(NB == 2, "argmax partials cover 32-column units");
+        const int col0 = 32 * blk + c;
         if (m < M && epi.logits) {
-          epi.logits[(size_t)m * epi.ld + col0] = s0[r];
-          epi.logits[(size_t)m * epi.ld + col0 + 16] = s1[r];
+          epi.logits[(size_t)m * epi.ld + col0] = sv[0][r];
+          epi.logits[(size_t)m * epi.ld + col0 + 16] = sv[1][r];
         }
-        float bv = s0[r];
+        float bv = sv[0][r];
         int bi = col0;
-        if (s1[r] > bv) {
-          bv = s1[r];
+        if (sv[1][r] > bv) {
+          bv = sv[1][r];
           bi = col0 + 16;
         }
 #pragma unroll
@@ -476,11 +492,13 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
           }
         }
         if (m < M && c == 0) {
-          epi.pval[(size_t)m * epi.n_parts + u] = bv;
-          epi.pidx[(size_t)m * epi.n_parts + u] = bi;
+          epi.pval[(size_t)m * epi.n_parts + blk] = bv;
+          epi.pidx[(size_t)m * epi.n_parts + blk] = bi;
         }
+      } else if constexpr (NB == 2) {
+        if (m < M) epi(m, blk, c, sv[0][r], sv[1][r]);
       } else {
-        if (m < M) epi(m, u, c, s0[r], s1[r]);
+        if (m < M) epi.one(m, 16 * blk + c, sv[0][r]);
       }
     }
   }
@@ -506,23 +524,42 @@ hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k
   return hipGetLastError();
 }
 
+template <typename T, int MT, int NB, bool NORM, typename Epi>
+hipError_t launch_skinny_one(const T *ap, int lda, const NormIn &nz, const uint8_t *w, int m,
+                             int mb, int n, int k, const Epi &epi, hipStream_t s) {
+  const size_t lds = NORM ? skinny_norm_lds(sizeof(T), m - mb, k) : 0;
+  if (lds > kSkinnyMaxNormLds) return hipErrorInvalidValue;
+  LL_LAUNCH((k_gemm_skinny<T, MT, NB, NORM, Epi>), dim3(n / (16 * NB)), dim3(512), lds, s, ap,
+            lda, nz, w, m, mb, k, epi);
+  return hipGetLastError();
+}
+
+
 template <typename T, typename Epi>
 hipError_t run_skinny(const void *a, int lda, const NormIn *norm, const void *wt, int m, int n,
                       int k, const Epi &epi, hipStream_t s) {
   const T *ap = reinterpret_cast<const T *>(a);
   const uint8_t *w = reinterpret_cast<const uint8_t *>(wt);
   const NormIn nz = norm ? *norm : NormIn{};
+  // Element-wise epilogues take 16-column blocks when 32-column ones would not fill the CUs.
+  const bool single = !Epi::kPairs && n / 32 < 256;
   for (int mb = 0; mb < m; mb += 32) {
     const bool one = m - mb <= 16;
-    if (norm && one)
-      LL_LAUNCH((k_gemm_skinny<T, 1, true, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, nz, w, m, mb, k, epi);
-    else if (norm)
-      LL_LAUNCH((k_gemm_skinny<T, 2, true, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, nz, w, m, mb, k, epi);
-    else if (one)
-      LL_LAUNCH((k_gemm_skinny<T, 1, false, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, nz, w, m, mb, k, epi);
-    else
-      LL_LAUNCH((k_gemm_skinny<T, 2, false, Epi>), dim3(n / 32), dim3(512), 0, s, ap, lda, nz, w, m, mb, k, epi);
-    hipError_t e = hipGetLastError();
+    hipError_t e;
+#define LL_SKINNY(MT, NB, NORM) e = launch_skinny_one<T, MT, NB, NORM>(ap, lda, nz, w, m, mb, n, k, epi, s)
+    if constexpr (Epi::kPairs) {
+      if (norm) { if (one) LL_SKINNY(1, 2, true); else return hipErrorInvalidValue; }
+      else { if (one) LL_SKINNY(1, 2, false); else LL_SKINNY(2, 2, false); }
+    } else {
+      if (norm) {
+        if (!one) return hipErrorInvalidValue;
+        if (single) LL_SKINNY(1, 1, true); else LL_SKINNY(1, 2, true);
+      } else {
+        if (single) { if (one) LL_SKINNY(1, 1, false); else LL_SKINNY(2, 1, false); }
+        else { if (one) LL_SKINNY(1, 2, false); else LL_SKINNY(2, 2, false); }
+      }
+    }
+#undef LL_SKINNY
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

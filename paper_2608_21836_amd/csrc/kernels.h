@@ -83,7 +83,12 @@ hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, 
                              int k, const EpiParams &ep, hipStream_t s);
 // Decode GEMM: weights streamed once from HBM into MFMA operands, A read from L2.
 // Requires N % 32 == 0, K % 64 == 0; any M (rows handled 32 at a time).  With `norm` the A
-// operand is RMSNorm of fp32 rows computed in the kernel (`a` is then unused).
+// operand is RMSNorm of fp32 rows computed in the kernel (`a` is then unused); that needs
+// M <= 16 and skinny_norm_lds(elem, M, K) <= kSkinnyMaxNormLds (the rows are staged in LDS).
+constexpr size_t kSkinnyMaxNormLds = 48 * 1024;
+inline size_t skinny_norm_lds(size_t elem, int rows, int k) {
+  return (size_t)(rows < 16 ? rows : 16) * (k + 16 / elem) * elem;
+}
 hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,
                               const void *wt, int m, int n, int k, const EpiParams &ep,
                               hipStream_t s);
@@ -115,12 +120,19 @@ hipError_t launch_attn_prefill(int dtype, int head_dim, const void *q, int ldq,
 
 // Decode attention: split over the cache length (chunk keys per block), then a merge kernel.
 // Keys attended per sequence: lens[b] + len_add (clamped to max_ctx).
-int attn_decode_chunk(int batch, int n_kv_heads, int max_ctx);
+struct AttnDecodePlan {
+  int kpb = 0;     // cached keys per block
+  int nsplit = 0;  // blocks per (sequence, kv head); 1 = no merge kernel
+};
+AttnDecodePlan attn_decode_plan(int head_dim, int elem_bytes, int batch, int n_kv_heads,
+                                int max_ctx);
 int attn_decode_max_ctx();
+// part_o [batch][n_heads][nsplit][head_dim] and part_ml [batch][n_heads][nsplit][2] fp32 are
+// used only when plan.nsplit > 1.
 hipError_t launch_attn_decode(int dtype, int head_dim, const void *q, int ldq,
                               const void *kcache, const void *vcache, const int *lens,
                               int len_add, void *o, int ldo, int batch, int n_heads,
-                              int n_kv_heads, int max_ctx, int chunk, float *part_o,
-                              float *part_ml, hipStream_t s);
+                              int n_kv_heads, int max_ctx, const AttnDecodePlan &plan,
+                              float *part_o, float *part_ml, hipStream_t s);
 
 }  // namespace ll

@@ -96,7 +96,8 @@ struct Layout {
   size_t cu = 0, row_seq = 0, row_pos = 0, last_row = 0, lens = 0, qtiles = 0, err = 0;
   size_t total = 0;
   size_t kv_layer_elems = 0;
-  int chunk = 0, nsplit = 0, n_parts = 0, max_rows = 0, n_qkv = 0;
+  AttnDecodePlan attn;
+  int n_parts = 0, max_rows = 0, n_qkv = 0;
 };
 
 ll_status validate_config(const ll_config *c) {
@@ -140,8 +141,7 @@ Layout make_layout(const ll_config &c) {
   const size_t d = c.d_model, qd = (size_t)c.n_heads * c.head_dim;
   L.n_qkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
   L.max_rows = std::max(c.max_prefill_tokens, c.max_batch);
-  L.chunk = attn_decode_chunk(c.max_batch, c.n_kv_heads, c.max_ctx);
-  L.nsplit = (c.max_ctx + L.chunk - 1) / L.chunk;
+  L.attn = attn_decode_plan(c.head_dim, (int)eb, c.max_batch, c.n_kv_heads, c.max_ctx);
   L.n_parts = c.vocab / 32;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -172,8 +172,8 @@ Layout make_layout(const ll_config &c) {
   L.o = take(R * qd * eb);
   L.act = take(R * c.ffn_dim * eb);
   L.hf = take((size_t)c.max_batch * d * eb);
-  L.part_o = take((size_t)c.max_batch * c.n_heads * L.nsplit * c.head_dim * 4);
-  L.part_ml = take((size_t)c.max_batch * c.n_heads * L.nsplit * 2 * 4);
+  L.part_o = take((size_t)c.max_batch * c.n_heads * L.attn.nsplit * c.head_dim * 4);
+  L.part_ml = take((size_t)c.max_batch * c.n_heads * L.attn.nsplit * 2 * 4);
   L.pval = take((size_t)c.max_batch * L.n_parts * 4);
   L.pidx = take((size_t)c.max_batch * L.n_parts * 4);
   L.cu = take((c.max_batch + 1) * 4);
@@ -278,7 +278,8 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
   const ll_config &c = m->cfg;
   const int d = c.d_model, qd = c.n_heads * c.head_dim, F = c.ffn_dim;
   const int dt = c.dtype;
-  const bool fuse_norm = decode && rows <= kFusedNormMaxRows;
+  const bool fuse_norm = decode && rows <= kFusedNormMaxRows &&
+                         skinny_norm_lds(elem_bytes(dt), rows, d) <= kSkinnyMaxNormLds;
   float *x = m->at<float>(m->L.x);
   auto gemm = [&](const void *a, int lda, const NormIn *nrm, const void *wt, int n, int k,
                   const EpiParams &ep) {
@@ -310,7 +311,7 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
     if (decode) {
       LL_HIP(launch_attn_decode(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
                                 m->at<int>(m->L.lens), 1, m->at(m->L.o), qd, rows, c.n_heads,
-                                c.n_kv_heads, c.max_ctx, m->L.chunk, m->at<float>(m->L.part_o),
+                                c.n_kv_heads, c.max_ctx, m->L.attn, m->at<float>(m->L.part_o),
                                 m->at<float>(m->L.part_ml), s));
     } else {
       LL_HIP(launch_attn_prefill(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
@@ -338,7 +339,8 @@ ll_status enqueue_head(ll_model *m, int batch, const int *rowmap, int *next, flo
   const ll_config &c = m->cfg;
   EpiParams ep = argmax_epi(m, logits);
   NormIn nrm{m->at<float>(m->L.x), c.d_model, rowmap, m->at(m->L.final_norm), c.rms_eps};
-  const bool fuse_norm = batch <= kFusedNormMaxRows;
+  const bool fuse_norm = batch <= kFusedNormMaxRows &&
+                         skinny_norm_lds(elem_bytes(c.dtype), batch, c.d_model) <= kSkinnyMaxNormLds;
   if (!fuse_norm) {
     m->mark(LL_K_RMSNORM);
     LL_HIP(launch_rmsnorm(c.dtype, m->at<float>(m->L.x), c.d_model, rowmap, batch, c.d_model,
@@ -734,8 +736,8 @@ ll_status ll_op_attn_prefill(int32_t dtype, int32_t batch, const int32_t *seq_le
 size_t ll_op_attn_decode_scratch(int32_t batch, int32_t n_heads, int32_t n_kv_heads,
                                  int32_t head_dim, int32_t max_ctx) {
   if (batch < 1 || n_heads < 1 || n_kv_heads < 1 || head_dim < 1 || max_ctx < 1) return 0;
-  const int chunk = attn_decode_chunk(batch, n_kv_heads, max_ctx);
-  const size_t nsplit = (max_ctx + chunk - 1) / chunk;
+  const size_t nsplit = std::max(attn_decode_plan(head_dim, 4, batch, n_kv_heads, max_ctx).nsplit,
+                                 attn_decode_plan(head_dim, 2, batch, n_kv_heads, max_ctx).nsplit);
   return align_up((size_t)batch * n_heads * nsplit * head_dim * 4) +
          align_up((size_t)batch * n_heads * nsplit * 2 * 4);
 }
@@ -753,8 +755,9 @@ ll_status ll_op_attn_decode(int32_t dtype, int32_t batch, int32_t n_heads, int32
   if ((st = check_ws(scratch)) != LL_OK) return st;
   const size_t need = ll_op_attn_decode_scratch(batch, n_heads, n_kv_heads, head_dim, max_ctx);
   if (scratch_bytes < need) return fail(LL_ERR_WORKSPACE, "scratch needs %zu bytes", need);
-  const int chunk = attn_decode_chunk(batch, n_kv_heads, max_ctx);
-  const size_t nsplit = (max_ctx + chunk - 1) / chunk;
+  const AttnDecodePlan plan =
+      attn_decode_plan(head_dim, (int)elem_bytes(dtype), batch, n_kv_heads, max_ctx);
+  const size_t nsplit = plan.nsplit;
   float *po = reinterpret_cast<float *>(scratch);
   float *pml = reinterpret_cast<float *>(reinterpret_cast<char *>(scratch) +
                                          align_up((size_t)batch * n_heads * nsplit * head_dim * 4));
@@ -762,7 +765,7 @@ ll_status ll_op_attn_decode(int32_t dtype, int32_t batch, int32_t n_heads, int32
   if (max_ctx > attn_decode_max_ctx())
     return fail(LL_ERR_UNSUPPORTED, "max_ctx %d > %d", max_ctx, attn_decode_max_ctx());
   LL_HIP(launch_attn_decode(dtype, head_dim, q, qd, kcache, vcache, ctx_lens_dev, 0, o, qd, batch,
-                            n_heads, n_kv_heads, max_ctx, chunk, po, pml, (hipStream_t)stream));
+                            n_heads, n_kv_heads, max_ctx, plan, po, pml, (hipStream_t)stream));
   return LL_OK;
 }
 
