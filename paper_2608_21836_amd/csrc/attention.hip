@@ -289,19 +289,22 @@ __global__ __launch_bounds__(HD) void k_attn_combine(const float *__restrict__ p
                                                       const int *__restrict__ lens, int len_add,
                                                       int hq, int kpb, int nsplit, int max_ctx,
                                                       T *__restrict__ O, int ldo) {
+  __shared__ float s_m[kMaxSplit], s_l[kMaxSplit], s_w[kMaxSplit];
   const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
   const int S = min(lens[b] + len_add, max_ctx);
   const int ns = (S + kpb - 1) / kpb;
   const size_t base = ((size_t)b * hq + h) * nsplit;
-  float mx = -INFINITY;
-  for (int sp = 0; sp < ns; ++sp) mx = fmaxf(mx, part_ml[(base + sp) * 2]);
-  float num = 0.f, den = 0.f;
-  for (int sp = 0; sp < ns; ++sp) {
-    const float w = exp2f(part_ml[(base + sp) * 2] - mx);
-    num += w * part_o[(base + sp) * HD + d];
-    den += w * part_ml[(base + sp) * 2 + 1];
+  // All split statistics are fetched at once, then every step runs out of LDS.
+  for (int sp = d; sp < ns; sp += HD) {
+    s_m[sp] = part_ml[(base + sp) * 2];
+    s_l[sp] = part_ml[(base + sp) * 2 + 1];
   }
-  O[(size_t)b * ldo + h * HD + d] = from_f32<T>(num / den);
+  __syncthreads();
+  float mx = -INFINITY;
+  for (int sp = 0; sp < ns; ++sp) mx = fmaxf(mx, s_m[sp]);
+  for (int sp = d; sp < ns; sp += HD) s_w[sp] = exp2f(s_m[sp] - mx);
+  __syncthreads();
+  O[(size_t)b * ldo + h * HD + d] = from_f32<T>(merge_splits(part_o + base * HD + d, HD, s_w, s_l, ns));
 }
 
 template <typename T, int HD>
@@ -326,7 +329,7 @@ template <typename T, int HD, int G>
 hipError_t run_decode_g(const void *q, int ldq, const void *kc, const void *vc, const int *lens,
                         int len_add, void *o, int ldo, int batch, int hkv, int max_ctx,
                         const AttnDecodePlan &plan, float *part_o, float *part_ml,
-                        hipStream_t s) {
+                        hipStream_t s, bool skip_merge) {
   const float scale_log2 = kLog2e / sqrtf((float)HD);
   constexpr int EPL = Frag<T>::EPL;
   LL_LAUNCH((k_attn_decode<T, HD, G, kChunkKpt<HD, EPL>>), dim3(plan.nsplit, hkv, batch),
@@ -335,7 +338,7 @@ hipError_t run_decode_g(const void *q, int ldq, const void *kc, const void *vc, 
             hkv, max_ctx, plan.kpb, plan.nsplit, part_o, part_ml, reinterpret_cast<T *>(o), ldo,
             scale_log2);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || plan.nsplit == 1) return e;
+  if (e != hipSuccess || plan.nsplit == 1 || skip_merge) return e;
   if (g_launch_timer) g_launch_timer->secondary();
   LL_LAUNCH((k_attn_combine<T, HD>), dim3(hkv * G, batch), dim3(HD), 0, s, part_o, part_ml, lens,
             len_add, hkv * G, plan.kpb, plan.nsplit, max_ctx, reinterpret_cast<T *>(o), ldo);
@@ -346,10 +349,10 @@ template <typename T, int HD>
 hipError_t run_decode(int group, const void *q, int ldq, const void *kc, const void *vc,
                       const int *lens, int len_add, void *o, int ldo, int batch, int hkv,
                       int max_ctx, const AttnDecodePlan &plan, float *part_o, float *part_ml,
-                      hipStream_t s) {
+                      hipStream_t s, bool skip_merge) {
 #define LL_DECODE_G(G)                                                                       \
   return run_decode_g<T, HD, G>(q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, \
-                                plan, part_o, part_ml, s)
+                                plan, part_o, part_ml, s, skip_merge)
   switch (group) {
     case 1: LL_DECODE_G(1);
     case 2: LL_DECODE_G(2);
@@ -397,7 +400,7 @@ int attn_decode_max_ctx() { return kMaxSplit * 256; }
 hipError_t launch_attn_decode(int dtype, int head_dim, const void *q, int ldq, const void *kc,
                               const void *vc, const int *lens, int len_add, void *o, int ldo,
                               int batch, int hq, int hkv, int max_ctx, const AttnDecodePlan &plan,
-                              float *part_o, float *part_ml, hipStream_t s) {
+                              float *part_o, float *part_ml, hipStream_t s, bool skip_merge) {
   if (batch <= 0) return hipSuccess;
   if (plan.kpb <= 0 || plan.nsplit < 1 || plan.nsplit > kMaxSplit || hq % hkv ||
       (long)plan.kpb * plan.nsplit < max_ctx || plan.kpb > kMaxChunk)
@@ -407,7 +410,7 @@ hipError_t launch_attn_decode(int dtype, int head_dim, const void *q, int ldq, c
   const int g = hq / hkv;
 #define LL_DECODE_HD(TT, HD)                                                                 \
   return run_decode<TT, HD>(g, q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx,  \
-                            plan, part_o, part_ml, s)
+                            plan, part_o, part_ml, s, skip_merge)
   if (dtype == kF32) {
     if (head_dim == 64) LL_DECODE_HD(float, 64);
     if (head_dim == 128) LL_DECODE_HD(float, 128);

@@ -86,3 +86,18 @@ __device__ __forceinline__ float wave_max(float v) {
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)); }
 
 constexpr float kLog2e = 1.4426950408889634f;
+
+// Merge of split-K attention partials, in split order: sum_s w_s o_s / sum_s w_s l_s, where
+// w_s = 2^(m_s - max_s m_s) (log-sum-exp rescaling of each split's unnormalised output o_s and
+// sum l_s).  `po` points at split 0's output element, `stride` floats between splits; w and l
+// usually sit in LDS.
+__device__ __forceinline__ float merge_splits(const float *po, size_t stride, const float *w,
+                                              const float *l, int ns) {
+  float num = 0.f, den = 0.f;
+#pragma unroll 8
+  for (int sp = 0; sp < ns; ++sp) {
+    num += w[sp] * po[sp * stride];
+    den += w[sp] * l[sp];
+  }
+  return num / den;
+}

@@ -332,20 +332,27 @@ __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, in
 // waves splitting K, partial sums reduced through LDS.  Each wave requests U weight tiles per
 // n-block before using the first.
 //
-// With NORM the A operand is RMSNorm(x) computed on the fly: the kernel streams the fp32
-// residual rows x, multiplies by the gain, rounds to T for the MFMA and accumulates sum(x^2)
-// on the side.  The per-row factor 1/sqrt(mean(x^2) + eps) of RMSNorm does not depend on
-// the column, so it scales the finished dot products in the epilogue:
+// Activation source (AM): kAGlobal reads A fragments from global memory next to the weight
+// tiles; kAStaged first copies the block's (up to 16) A rows into LDS, which takes the
+// activation traffic off the L1 path the weight stream uses; kANorm stages RMSNorm(x)
+// computed on the fly: the fp32 residual rows times the gain, rounded to T, with sum(x^2) on
+// the side.  The per-row factor 1/sqrt(mean(x^2) + eps) of RMSNorm does not depend on the
+// column, so it scales the finished dot products in the epilogue:
 //   (x * s * g) . w = s * ((x * g) . w).
+// kAMerge stages the decode-attention output merged from its split partials (log-sum-exp
+// weights, same order as the merge kernel), so the O projection needs no merge launch.
 // ------------------------------------------------------------------------------------------
-template <typename T, int MT, int NB, bool NORM, typename Epi>
+enum AMode : int { kAGlobal = 0, kAStaged = 1, kANorm = 2, kAMerge = 3 };
+
+template <typename T, int MT, int NB, int AM, typename Epi>
 __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, int lda,
-                                                     NormIn norm,
+                                                     NormIn norm, MergeIn merge,
                                                      const uint8_t *__restrict__ Wt, int M,
                                                      int m_base, int K, Epi epi) {
   using F = typename Frag<T>::type;
   constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL, NW = 8, U = 16 / NB;
-  static_assert(!NORM || MT == 1, "the normalised operand is staged for up to 16 rows");
+  static_assert(AM == kAGlobal || MT == 1, "staged operands cover up to 16 rows");
+  constexpr bool NORM = AM == kANorm;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int blk = blockIdx.x;
   const int kb_n = K / TK;
@@ -378,9 +385,7 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
   };
   load_w(kb0);
 
-  // NORM: stage (x * gain) of the block's rows in LDS (row stride K + EPL elements to spread
-  // banks) and the per-row sum of squares; the factor 1/sqrt(mean(x^2) + eps) is applied to
-  // the finished dot products.
+  // Staged modes: the block's rows in LDS, row stride K + EPL elements to spread banks.
   extern __shared__ __attribute__((aligned(16))) uint8_t dyn_smem[];
   T *sA = reinterpret_cast<T *>(dyn_smem);
   __shared__ float s_ss[NW][16];
@@ -406,9 +411,53 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
       if (lane == 0) s_ss[wave][r] = part;
     }
     __syncthreads();
+  } else if constexpr (AM == kAMerge) {
+    // Same steps as the merge kernel: split statistics to LDS, per-(row, head) maximum and
+    // weights, then the weighted sums in split order.
+    __shared__ float s_m[kMergeMaxParts], s_l[kMergeMaxParts], s_w[kMergeMaxParts];
+    const int hq = merge.n_heads, hd = merge.head_dim, nsp = merge.nsplit;
+    const int np = nrows * hq * nsp;
+    const size_t gbase = (size_t)m_base * hq * nsp;
+    auto n_splits = [&](int r) {
+      const int S = min(merge.lens[m_base + r] + merge.len_add, merge.max_ctx);
+      return (S + merge.kpb - 1) / merge.kpb;
+    };
+    for (int p = threadIdx.x; p < np; p += 512) {
+      if (p % nsp < n_splits(p / (hq * nsp))) {
+        s_m[p] = merge.part_ml[(gbase + p) * 2];
+        s_l[p] = merge.part_ml[(gbase + p) * 2 + 1];
+      }
+    }
+    __syncthreads();
+    for (int p = threadIdx.x; p < np; p += 512) {
+      const int sp = p % nsp, ns = n_splits(p / (hq * nsp));
+      if (sp < ns) {
+        float mx = -INFINITY;
+        for (int t = 0; t < ns; ++t) mx = fmaxf(mx, s_m[p - sp + t]);
+        s_w[p] = exp2f(s_m[p] - mx);
+      }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < nrows * K; e += 512) {
+      const int r = e / K, i = e % K;
+      const int h = i / hd, d = i % hd;
+      const int q = (r * hq + h) * nsp;
+      sA[(size_t)r * lds_ld + i] = from_f32<T>(
+          merge_splits(merge.part_o + (gbase + q) * hd + d, hd, s_w + q, s_l + q, n_splits(r)));
+    }
+    __syncthreads();
+  } else if constexpr (AM == kAStaged) {
+    const int cpr = K / EPL;  // 16-byte chunks per row
+#pragma unroll 4
+    for (int i = threadIdx.x; i < nrows * cpr; i += 512) {
+      const int r = i / cpr, c = i % cpr;
+      *reinterpret_cast<F *>(sA + (size_t)r * lds_ld + c * EPL) =
+          load_frag<F>(A + (size_t)(m_base + r) * lda + c * EPL);
+    }
+    __syncthreads();
   }
   auto a_frag = [&](int mt, int kb) -> F {
-    if constexpr (NORM) {
+    if constexpr (AM != kAGlobal) {
       const int r = lane & 15;
       return r < nrows ? *reinterpret_cast<const F *>(sA + (size_t)r * lds_ld + kb * TK +
                                                        (lane >> 4) * EPL)
@@ -524,41 +573,51 @@ hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k
   return hipGetLastError();
 }
 
-template <typename T, int MT, int NB, bool NORM, typename Epi>
-hipError_t launch_skinny_one(const T *ap, int lda, const NormIn &nz, const uint8_t *w, int m,
-                             int mb, int n, int k, const Epi &epi, hipStream_t s) {
-  const size_t lds = NORM ? skinny_norm_lds(sizeof(T), m - mb, k) : 0;
+template <typename T, int MT, int NB, int AM, typename Epi>
+hipError_t launch_skinny_one(const T *ap, int lda, const NormIn &nz, const MergeIn &mg,
+                             const uint8_t *w, int m, int mb, int n, int k, const Epi &epi,
+                             hipStream_t s) {
+  const size_t lds = AM != kAGlobal ? skinny_norm_lds(sizeof(T), m - mb, k) : 0;
   if (lds > kSkinnyMaxNormLds) return hipErrorInvalidValue;
-  LL_LAUNCH((k_gemm_skinny<T, MT, NB, NORM, Epi>), dim3(n / (16 * NB)), dim3(512), lds, s, ap,
-            lda, nz, w, m, mb, k, epi);
+  LL_LAUNCH((k_gemm_skinny<T, MT, NB, AM, Epi>), dim3(n / (16 * NB)), dim3(512), lds, s, ap,
+            lda, nz, mg, w, m, mb, k, epi);
   return hipGetLastError();
 }
 
 
 template <typename T, typename Epi>
-hipError_t run_skinny(const void *a, int lda, const NormIn *norm, const void *wt, int m, int n,
-                      int k, const Epi &epi, hipStream_t s) {
+hipError_t run_skinny(const void *a, int lda, const NormIn *norm, const MergeIn *merge,
+                      const void *wt, int m, int n, int k, const Epi &epi, hipStream_t s) {
   const T *ap = reinterpret_cast<const T *>(a);
   const uint8_t *w = reinterpret_cast<const uint8_t *>(wt);
   const NormIn nz = norm ? *norm : NormIn{};
+  const MergeIn mg = merge ? *merge : MergeIn{};
   // Element-wise epilogues take 16-column blocks when 32-column ones would not fill the CUs.
   const bool single = !Epi::kPairs && n / 32 < 256;
   for (int mb = 0; mb < m; mb += 32) {
     const bool one = m - mb <= 16;
-    hipError_t e;
-#define LL_SKINNY(MT, NB, NORM) e = launch_skinny_one<T, MT, NB, NORM>(ap, lda, nz, w, m, mb, n, k, epi, s)
+    if ((norm || merge) && !one) return hipErrorInvalidValue;
+    // up to 16 rows: A from LDS when the rows fit, else from global memory
+    const int am = !one ? kAGlobal
+                   : norm ? kANorm
+                   : merge ? kAMerge
+                   : skinny_norm_lds(sizeof(T), m - mb, k) <= kSkinnyMaxNormLds ? kAStaged : kAGlobal;
+    hipError_t e = hipErrorInvalidValue;
+#define LL_SKINNY(MT, NB, AM) e = launch_skinny_one<T, MT, NB, AM>(ap, lda, nz, mg, w, m, mb, n, k, epi, s)
+#define LL_SKINNY_NB(NB)                        \
+  do {                                          \
+    if (!one) LL_SKINNY(2, NB, kAGlobal);        \
+    else if (am == kANorm) LL_SKINNY(1, NB, kANorm); \
+    else if (am == kAMerge) LL_SKINNY(1, NB, kAMerge); \
+    else if (am == kAStaged) LL_SKINNY(1, NB, kAStaged); \
+    else LL_SKINNY(1, NB, kAGlobal);             \
+  } while (0)
     if constexpr (Epi::kPairs) {
-      if (norm) { if (one) LL_SKINNY(1, 2, true); else return hipErrorInvalidValue; }
-      else { if (one) LL_SKINNY(1, 2, false); else LL_SKINNY(2, 2, false); }
+      LL_SKINNY_NB(2);
     } else {
-      if (norm) {
-        if (!one) return hipErrorInvalidValue;
-        if (single) LL_SKINNY(1, 1, true); else LL_SKINNY(1, 2, true);
-      } else {
-        if (single) { if (one) LL_SKINNY(1, 1, false); else LL_SKINNY(2, 1, false); }
-        else { if (one) LL_SKINNY(1, 2, false); else LL_SKINNY(2, 2, false); }
-      }
+      if (single) LL_SKINNY_NB(1); else LL_SKINNY_NB(2);
     }
+#undef LL_SKINNY_NB
 #undef LL_SKINNY
     if (e != hipSuccess) return e;
   }
@@ -566,15 +625,15 @@ hipError_t run_skinny(const void *a, int lda, const NormIn *norm, const void *wt
 }
 
 template <typename T, bool kTiled>
-hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm, const void *wt, int m, int n,
-                        int k, const EpiParams &ep, hipStream_t s) {
+hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm, const MergeIn *merge,
+                        const void *wt, int m, int n, int k, const EpiParams &ep, hipStream_t s) {
   auto run = [&](const auto &epi) {
     using E = std::decay_t<decltype(epi)>;
     if constexpr (kTiled) {
       if constexpr (E::kArgmax) return hipErrorInvalidValue;
       else return run_tiled<T>(a, lda, wt, m, n, k, epi, s);
     } else {
-      return run_skinny<T>(a, lda, norm, wt, m, n, k, epi, s);
+      return run_skinny<T>(a, lda, norm, merge, wt, m, n, k, epi, s);
     }
   };
   // Refuse, before any launch, pointer sets that a kernel would dereference as null.
@@ -587,6 +646,12 @@ hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm, const void *
                              !ep.rope_cos || !ep.rope_sin))
     return hipErrorInvalidValue;
   if (norm && (!norm->x || !norm->gain)) return hipErrorInvalidValue;
+  if (norm && merge) return hipErrorInvalidValue;
+  if (merge && (!merge->part_o || !merge->part_ml || !merge->lens || merge->kpb <= 0 ||
+                merge->nsplit <= 0 || merge->max_ctx > merge->kpb * merge->nsplit ||
+                merge->head_dim <= 0 || merge->n_heads * merge->head_dim != k ||
+                (long)m * merge->n_heads * merge->nsplit > kMergeMaxParts))
+    return hipErrorInvalidValue;
   switch (ep.kind) {
     case kEpiStore: return run(EpiStore{ep.out_f32, ep.ld_out});
     case kEpiResid: return run(EpiResid{ep.out_f32, ep.ld_out});
@@ -620,16 +685,16 @@ hipError_t launch_repack(int dtype, const RepackSrc &src, int n, int k, int perm
 hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, int m, int n,
                              int k, const EpiParams &ep, hipStream_t s) {
   if (m <= 0) return hipSuccess;
-  return dtype == kF32 ? dispatch_epi<float, true>(a, lda, nullptr, wt, m, n, k, ep, s)
-                       : dispatch_epi<bf16, true>(a, lda, nullptr, wt, m, n, k, ep, s);
+  return dtype == kF32 ? dispatch_epi<float, true>(a, lda, nullptr, nullptr, wt, m, n, k, ep, s)
+                       : dispatch_epi<bf16, true>(a, lda, nullptr, nullptr, wt, m, n, k, ep, s);
 }
 
 hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,
                               const void *wt, int m, int n, int k, const EpiParams &ep,
-                              hipStream_t s) {
+                              hipStream_t s, const MergeIn *merge) {
   if (m <= 0) return hipSuccess;
-  return dtype == kF32 ? dispatch_epi<float, false>(a, lda, norm, wt, m, n, k, ep, s)
-                       : dispatch_epi<bf16, false>(a, lda, norm, wt, m, n, k, ep, s);
+  return dtype == kF32 ? dispatch_epi<float, false>(a, lda, norm, merge, wt, m, n, k, ep, s)
+                       : dispatch_epi<bf16, false>(a, lda, norm, merge, wt, m, n, k, ep, s);
 }
 
 }  // namespace ll

@@ -78,6 +78,16 @@ struct NormIn {
   float eps = 0.f;
 };
 
+// Split-K decode-attention partials merged inside the decode GEMM that consumes the attention
+// output (A = merged rows, computed exactly as the merge kernel computes them).
+constexpr int kMergeMaxParts = 256;  // rows * n_heads * nsplit
+struct MergeIn {
+  const float *part_o = nullptr;   // [batch][n_heads][nsplit][head_dim]
+  const float *part_ml = nullptr;  // [batch][n_heads][nsplit][2]
+  const int *lens = nullptr;
+  int len_add = 0, kpb = 0, nsplit = 0, n_heads = 0, head_dim = 0, max_ctx = 0;
+};
+
 // Prefill GEMM: LDS-tiled MFMA, 128 x 128 block tiles.  Requires N % 128 == 0, K % 64 == 0.
 hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, int m, int n,
                              int k, const EpiParams &ep, hipStream_t s);
@@ -91,7 +101,7 @@ inline size_t skinny_norm_lds(size_t elem, int rows, int k) {
 }
 hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,
                               const void *wt, int m, int n, int k, const EpiParams &ep,
-                              hipStream_t s);
+                              hipStream_t s, const MergeIn *merge = nullptr);
 
 hipError_t launch_embed(int dtype, const int *tokens, int ntok, const void *table, int vocab,
                         int d, float *x, int *err_flags, hipStream_t s);
@@ -133,6 +143,7 @@ hipError_t launch_attn_decode(int dtype, int head_dim, const void *q, int ldq,
                               const void *kcache, const void *vcache, const int *lens,
                               int len_add, void *o, int ldo, int batch, int n_heads,
                               int n_kv_heads, int max_ctx, const AttnDecodePlan &plan,
-                              float *part_o, float *part_ml, hipStream_t s);
+                              float *part_o, float *part_ml, hipStream_t s,
+                              bool skip_merge = false);
 
 }  // namespace ll

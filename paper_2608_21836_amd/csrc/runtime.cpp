@@ -272,6 +272,8 @@ EpiParams argmax_epi(const ll_model *m, float *logits) {
 // Decode batches up to this size normalise inside the decode GEMM (the fp32 rows are then
 // read by every column block, which stays cheap only for a few rows).
 constexpr int kFusedNormMaxRows = 16;
+// Small decode batches merge the split attention partials inside the O projection when every
+// block can afford to read all of them (each of its blocks reads the whole set from L2).
 
 // The decoder layers for `rows` rows.  decode: one row per sequence at position len[b].
 ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipStream_t s) {
@@ -280,6 +282,23 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
   const int dt = c.dtype;
   const bool fuse_norm = decode && rows <= kFusedNormMaxRows &&
                          skinny_norm_lds(elem_bytes(dt), rows, d) <= kSkinnyMaxNormLds;
+  const AttnDecodePlan &ap = m->L.attn;
+  const bool fuse_merge =
+      decode && ap.nsplit > 1 && rows <= kFusedNormMaxRows &&
+      skinny_norm_lds(elem_bytes(dt), rows, qd) <= kSkinnyMaxNormLds &&
+      (long)rows * c.n_heads * ap.nsplit <= kMergeMaxParts;
+  MergeIn mrg;
+  if (fuse_merge) {
+    mrg.part_o = m->at<float>(m->L.part_o);
+    mrg.part_ml = m->at<float>(m->L.part_ml);
+    mrg.lens = m->at<int>(m->L.lens);
+    mrg.len_add = 1;
+    mrg.kpb = ap.kpb;
+    mrg.nsplit = ap.nsplit;
+    mrg.n_heads = c.n_heads;
+    mrg.head_dim = c.head_dim;
+    mrg.max_ctx = c.max_ctx;
+  }
   float *x = m->at<float>(m->L.x);
   auto gemm = [&](const void *a, int lda, const NormIn *nrm, const void *wt, int n, int k,
                   const EpiParams &ep) {
@@ -311,8 +330,8 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
     if (decode) {
       LL_HIP(launch_attn_decode(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
                                 m->at<int>(m->L.lens), 1, m->at(m->L.o), qd, rows, c.n_heads,
-                                c.n_kv_heads, c.max_ctx, m->L.attn, m->at<float>(m->L.part_o),
-                                m->at<float>(m->L.part_ml), s));
+                                c.n_kv_heads, c.max_ctx, ap, m->at<float>(m->L.part_o),
+                                m->at<float>(m->L.part_ml), s, fuse_merge));
     } else {
       LL_HIP(launch_attn_prefill(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
                                  m->at(m->L.o), qd, m->at<int>(m->L.cu),
@@ -320,7 +339,11 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
                                  c.max_ctx, s));
     }
     m->mark(LL_K_O);
-    LL_HIP(gemm(m->at(m->L.o), qd, nullptr, m->at(m->L.wo[l]), d, qd, resid_epi(m)));
+    if (fuse_merge)
+      LL_HIP(launch_gemm_skinny(dt, nullptr, qd, nullptr, m->at(m->L.wo[l]), rows, d, qd,
+                                resid_epi(m), s, &mrg));
+    else
+      LL_HIP(gemm(m->at(m->L.o), qd, nullptr, m->at(m->L.wo[l]), d, qd, resid_epi(m)));
     st = normed(m->L.mlp_norm[l], &nrm);
     if (st != LL_OK) return st;
     m->mark(LL_K_GATE_UP);
