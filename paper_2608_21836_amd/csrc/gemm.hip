@@ -215,12 +215,17 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const T *__restrict__ A, int
 }
 
 // ------------------------------------------------------------------------------------------
-// Large prefill GEMM: 256 x 256 block tiles, 4 waves of 128 x 128, K steps of two 1 KiB tiles.
+// Large prefill GEMM: 256 x 256 block tiles, 8 waves of 128 x 64, one 1 KiB k-tile per step.
 // Operand tiles go straight from global memory into LDS (global_load_lds_dwordx4: each wave
 // fills one 1 KiB tile per instruction, lane l's 16 bytes at offset 16 l, which is exactly the
-// MFMA operand order), double-buffered: the loads of step k+1 are in flight while step k
-// computes.  Blocks are renumbered so that each XCD (workgroups are dealt round-robin to the
-// 8 XCDs) works on a compact group of output tiles and shares A and W tiles in its own L2.
+// MFMA operand order) through a ring of 4 stages, loads issued 3 steps ahead.  Each step is
+// software-pipelined around its single barrier: the first half of the step's MFMAs runs from
+// fragments already in registers, the wave then waits for the next stage, passes the barrier
+// and reads the next step's fragments from LDS while the second half of the MFMAs runs.  The
+// barrier is a bare s_barrier after an explicit vmcnt wait (a full __syncthreads would also
+// wait for the loads just issued for later stages).  Blocks are renumbered so that each XCD
+// (workgroups are dealt round-robin to the 8 XCDs) works on a compact group of output tiles
+// and shares A and W tiles in its own L2.
 // ------------------------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void global_void_t;
@@ -238,6 +243,11 @@ __device__ __forceinline__ int xcd_remap(int pid, int n) {
   return x < tall ? x * per + local : tall * per + (x - tall) * (per - 1) + local;
 }
 
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 template <typename T, typename Epi>
 __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, int lda,
                                                      const uint8_t *__restrict__ Wt, int M,
@@ -245,7 +255,8 @@ __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, in
   using F = typename Frag<T>::type;
   constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL;
   constexpr int BM = 256, BN = 256, GM = 8;
-  __shared__ uint4 smem[2][4096];  // [buf][A: 32 tiles | W: 32 tiles][64 lanes]
+  constexpr int S = 4, TPS = 32, LPW = TPS / 8;  // stages, tiles per stage, loads per wave
+  __shared__ uint4 smem[S * TPS * 64];  // [stage][A: 16 row tiles | W: 16 column tiles][64]
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // 8 waves, 2 (M) x 4 (N)
   const int wm = wave >> 2, wn = wave & 3;
@@ -256,25 +267,29 @@ __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, in
   const int gsize = min(ntm - first_m, GM);
   const int tm = first_m + (t % (GM * ntn)) % gsize, tn = (t % (GM * ntn)) / gsize;
   const int m0 = tm * BM, n0 = tn * BN;
-  const int kb_n = K / TK, nsteps = kb_n / 2;
+  const int nsteps = K / TK;
 
-  // Per step this wave fills A tiles 4w .. 4w+3 (row blocks 2w, 2w+1; both k-tiles) and W
-  // tiles 4w .. 4w+3 (16-row blocks 2w, 2w+1 of this block's columns).
-  const T *a_lane = A + (lane >> 4) * EPL;
-  uint32_t a_row[2];
+  // Waves 0-3 fill A tiles 4w .. 4w+3 (16-row blocks), waves 4-7 W tiles 4(w-4) .. +3.
+  const bool loads_a = wave < 4;
+  const uint8_t *src[LPW];
 #pragma unroll
-  for (int q = 0; q < 2; ++q)
-    a_row[q] = (uint32_t)min(m0 + (wave * 2 + q) * 16 + (lane & 15), M - 1);
-  const uint8_t *w_lane = Wt + (((size_t)(n0 / 16 + wave * 2) * kb_n) * 64 + lane) * 16;
-  auto issue = [&](int step, int buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int q = i >> 1, kb = i & 1;
-      load_tile_to_lds(a_lane + (size_t)a_row[q] * lda + (step * 2 + kb) * TK,
-                       &smem[buf][(wave * 4 + i) * 64]);
-      load_tile_to_lds(w_lane + ((size_t)q * kb_n + step * 2 + kb) * 1024,
-                       &smem[buf][(32 + wave * 4 + i) * 64]);
+  for (int i = 0; i < LPW; ++i) {
+    const int tt = wave * LPW + i;
+    if (loads_a) {
+      const int row = min(m0 + tt * 16 + (lane & 15), M - 1);
+      src[i] = reinterpret_cast<const uint8_t *>(A + (size_t)row * lda + (lane >> 4) * EPL);
+    } else {
+      src[i] = Wt + (((size_t)(n0 / 16 + tt - 16) * nsteps) * 64 + lane) * 16;
     }
+  }
+  // Steps past the end reload the last tile (the data is never read), so that every step
+  // issues the same number of loads and the vmcnt arithmetic stays fixed.
+  auto issue = [&](int step, int stage) {
+    const int st = min(step, nsteps - 1);
+    const size_t off = loads_a ? (size_t)st * TK * sizeof(T) : (size_t)st * 1024;
+#pragma unroll
+    for (int i = 0; i < LPW; ++i)
+      load_tile_to_lds(src[i] + off, &smem[(stage * TPS + wave * LPW + i) * 64]);
   };
 
   f32x4 acc[8][4];
@@ -283,35 +298,48 @@ __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, in
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto compute = [&](int cur) {
+  auto read_frags = [&](int stage, F *fa, F *fb) {
+    const uint4 *base = &smem[stage * TPS * 64];
 #pragma unroll
-    for (int kbl = 0; kbl < 2; ++kbl) {
-      F a[8], b[4];
+    for (int j = 0; j < 4; ++j) fb[j] = *reinterpret_cast<const F *>(&base[(16 + wn * 4 + j) * 64 + lane]);
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
-        a[i] = *reinterpret_cast<const F *>(&smem[cur][((wm * 8 + i) * 2 + kbl) * 64 + lane]);
+    for (int i = 0; i < 8; ++i) fa[i] = *reinterpret_cast<const F *>(&base[(wm * 8 + i) * 64 + lane]);
+  };
+  auto mma_half = [&](int h, const F *fa, const F *fb) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        b[j] = *reinterpret_cast<const F *>(&smem[cur][(32 + (wn * 4 + j) * 2 + kbl) * 64 + lane]);
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mma_chunk(a[i], b[j], acc[i][j]);
-    }
+      for (int j = 0; j < 4; ++j) acc[h * 4 + i][j] = mma_chunk(fa[h * 4 + i], fb[j], acc[h * 4 + i][j]);
+  };
+  // One step: loads for step s+3, MFMAs (first half), barrier for stage s+1, fragments of
+  // step s+1, MFMAs (second half).  The scheduling barriers keep the compiler from moving
+  // MFMAs that need the new fragments up next to the reads.
+  auto step_body = [&](int s, const F *ca, const F *cb, F *na, F *nb) {
+    issue(s + 3, (s + 3) & 3);
+    mma_half(0, ca, cb);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vmcnt<2 * LPW>();  // stage s+1 landed (stages s+2, s+3 may still be in flight)
+    asm volatile("s_barrier" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    read_frags((s + 1) & 3, na, nb);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_half(1, ca, cb);
+    __builtin_amdgcn_sched_barrier(0);
   };
 
-  // Straight-line loop body (no branch around the prefetch) so the accumulators stay put in
-  // the accumulation registers across iterations; the last step is peeled.
   issue(0, 0);
-  for (int step = 0; step + 1 < nsteps; ++step) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    issue(step + 1, (step + 1) & 1);
-    compute(step & 1);
-  }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  issue(1, 1);
+  issue(2, 2);
+  wait_vmcnt<2 * LPW>();
   __syncthreads();
-  compute((nsteps - 1) & 1);
+  F fa0[8], fb0[4], fa1[8], fb1[4];
+  read_frags(0, fa0, fb0);
+  // nsteps is even (K is a multiple of two k-tiles); the last step reads a stage it never uses.
+  for (int s = 0; s < nsteps; s += 2) {
+    step_body(s, fa0, fb0, fa1, fb1);
+    step_body(s + 1, fa1, fb1, fa0, fb0);
+  }
+  wait_vmcnt<0>();
 
   const int ubase = (n0 + wn * 64) >> 5;
 #pragma unroll
