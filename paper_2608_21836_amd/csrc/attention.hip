@@ -15,6 +15,7 @@
 // log-sum-exp weights (fixed order, so the result does not depend on block order).
 #include <algorithm>
 #include <cmath>
+#include <type_traits>
 
 #include "device_common.h"
 #include "kernels.h"
@@ -136,6 +137,189 @@ __global__ __launch_bounds__(256) void k_attn_prefill(
     for (int ds = 0; ds < NDS; ++ds)
 #pragma unroll
       for (int r = 0; r < 4; ++r) dst[ds * 16 + r] = from_f32<T>(acc[ds][r] * inv);
+  }
+}
+
+// bf16 prefill attention on v_mfma_f32_32x32x16_bf16: one block per (128-query tile, query
+// head), 4 waves of 32 queries, key tiles of 64 through a double-buffered LDS stage.
+//   S^T = K Q^T: A = K rows (DMA'd from the cache straight into LDS in operand order), B = the
+//     wave's Q^T fragments, held in registers for the whole loop.  Lane l owns query l % 32
+//     and, of each 32-key block, the rows 8 (i / 4) + 4 (l / 32) + i % 4: the online-softmax
+//     statistics need one exchange with lane l ^ 32.
+//   O^T += V^T P^T: B = P^T straight from the score registers (no lane movement), because the
+//     16 keys of a P V step are taken in the order the score registers hold them; the V^T
+//     tiles in LDS are written in that same key order.  Two waves build them: each lane loads
+//     8 keys x 8 dims (8 x 16 B), transposes them in registers and writes 8 x 16 B.
+// The other waves issue the K loads.  Loads for tile t + 1 are in flight while tile t
+// computes; the causal mask is applied only on tiles that reach past a wave's first query.
+template <int HD>
+__global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
+    const bf16 *__restrict__ Q, int ldq, const bf16 *__restrict__ Kc, const bf16 *__restrict__ Vc,
+    bf16 *__restrict__ O, int ldo, const int *__restrict__ cu, const int2 *__restrict__ qtiles,
+    int hq, int hkv, int max_ctx, float scale_log2) {
+  constexpr int QT = kAttnQTileWide, BKV = 64;
+  constexpr int NKC = HD / 16;           // 16-dim steps of S^T
+  constexpr int NDB = HD / 32;           // 32-dim output blocks
+  constexpr int NPC = BKV / 16;          // 16-key steps of P V
+  constexpr int KTILES = 2 * NKC;        // K tiles per stage: [32-key block][16-dim step]
+  constexpr int VTILES = NDB * NPC;      // V^T tiles per stage: [dim block][key step]
+  constexpr int STAGE = (KTILES + VTILES) * 64;  // uint4 per stage
+  constexpr int NVT = (HD / 8) * NPC * 2;        // V^T build tasks per stage, one per lane
+  constexpr int VW = NVT / 64;                   // waves building V^T
+  constexpr int KW = 4 - VW;                     // waves loading K
+  static_assert(QT == 128 && VW >= 1 && KW >= 1, "4 waves of 32 queries");
+  __shared__ uint4 smem[2 * STAGE];
+
+  const int2 qt = qtiles[blockIdx.x];
+  const int b = qt.x, h = blockIdx.y, kvh = h / (hq / hkv);
+  const int tok0 = cu[b], L = cu[b + 1] - tok0;
+  const int q0 = qt.y * QT;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 5;
+  const int qw = q0 + wave * 32;  // first query of this wave
+  const int my_q = qw + (lane & 31);
+  const bool q_ok = my_q < L;
+  const size_t kvbase = ((size_t)b * hkv + kvh) * max_ctx * HD;
+  const bf16x8 fz = frag_zero<bf16x8>();
+
+  bf16x8 qf[NKC];
+#pragma unroll
+  for (int c = 0; c < NKC; ++c)
+    qf[c] = q_ok ? load_frag<bf16x8>(Q + (size_t)(tok0 + my_q) * ldq + h * HD + 16 * c + 8 * g) : fz;
+  f32x16 acc[NDB];
+#pragma unroll
+  for (int d = 0; d < NDB; ++d)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[d][i] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const int ntiles = (min(q0 + QT, L) - 1) / BKV + 1;
+
+  // K tile (kb, c): lane l reads key 32 kb + l % 32 (clamped into the sequence; rows past L
+  // are masked), dims 16 c + 8 g.
+  auto k_issue = [&](int kt, int buf) {
+    if (wave >= VW) {
+      for (int ti = wave - VW; ti < KTILES; ti += KW) {
+        const int kb = ti / NKC, c = ti % NKC;
+        const int key = min(kt * BKV + 32 * kb + (lane & 31), L - 1);
+        load_tile_to_lds(Kc + kvbase + (size_t)key * HD + 16 * c + 8 * g,
+                         &smem[buf * STAGE + ti * 64]);
+      }
+    }
+  };
+  // V^T task of lane `tid` (waves < VW): dims 8 dg .. 8 dg + 7, key step pc, key group gg;
+  // element e < 4 is key 16 pc + 4 gg + e, element e >= 4 is key 16 pc + 8 + 4 gg + e - 4.
+  const int dg = tid % (HD / 8), pc = (tid / (HD / 8)) % NPC, gg = tid / (HD / 8 * NPC);
+  uint4 vr[8];
+  auto v_load = [&](int kt) {
+    if (wave < VW) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int key = kt * BKV + 16 * pc + (e < 4 ? 4 * gg + e : 8 + 4 * gg + e - 4);
+        vr[e] = key < L ? *reinterpret_cast<const uint4 *>(Vc + kvbase + (size_t)key * HD + 8 * dg)
+                        : make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+  auto v_store = [&](int buf) {
+    if (wave < VW) {
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        uint32_t d[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t lo = reinterpret_cast<const uint32_t *>(&vr[2 * j])[t >> 1];
+          const uint32_t hi = reinterpret_cast<const uint32_t *>(&vr[2 * j + 1])[t >> 1];
+          d[j] = (t & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+        }
+        const int dim = 8 * dg + t;
+        smem[buf * STAGE + (KTILES + (dim / 32) * NPC + pc) * 64 + (dim % 32) + 32 * gg] =
+            make_uint4(d[0], d[1], d[2], d[3]);
+      }
+    }
+  };
+  auto compute = [&](int kt, int buf) {
+    if (qw >= L || kt * BKV > qw + 31) return;  // nothing for this wave in this tile
+    const uint4 *st = &smem[buf * STAGE];
+    f32x16 sc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sc[kb][i] = 0.f;
+#pragma unroll
+      for (int c = 0; c < NKC; ++c)
+        sc[kb] = mma32(*reinterpret_cast<const bf16x8 *>(&st[(kb * NKC + c) * 64 + lane]), qf[c], sc[kb]);
+    }
+    const bool masked = kt * BKV + BKV - 1 > qw || qw + 31 >= L;
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int key = kt * BKV + 32 * kb + 8 * (i / 4) + 4 * g + (i % 4);
+        const float v = (!masked || (q_ok && key <= my_q)) ? sc[kb][i] * scale_log2 : -INFINITY;
+        sc[kb][i] = v;
+        tmax = fmaxf(tmax, v);
+      }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+    const float m_new = fmaxf(m_run, tmax);
+    const float base = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = exp2f(m_run - base);
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int d = 0; d < NDB; ++d) acc[d] *= alpha;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float p = exp2f(sc[kb][i] - base);
+        sc[kb][i] = p;
+        l_run += p;
+      }
+#pragma unroll
+    for (int c = 0; c < NPC; ++c) {
+      bf16x8 pf;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pf[e] = static_cast<bf16>(sc[c / 2][8 * (c % 2) + e]);
+#pragma unroll
+      for (int d = 0; d < NDB; ++d)
+        acc[d] = mma32(*reinterpret_cast<const bf16x8 *>(&st[(KTILES + d * NPC + c) * 64 + lane]), pf, acc[d]);
+    }
+  };
+
+  k_issue(0, 0);
+  v_load(0);
+  v_store(0);
+  __syncthreads();
+  for (int kt = 0; kt < ntiles; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < ntiles;
+    if (more) {
+      k_issue(kt + 1, cur ^ 1);
+      v_load(kt + 1);
+    }
+    compute(kt, cur);
+    if (more) v_store(cur ^ 1);
+    __syncthreads();
+  }
+
+  l_run += __shfl_xor(l_run, 32);
+  if (q_ok) {
+    const float inv = 1.0f / l_run;
+    bf16 *dst = O + (size_t)(tok0 + my_q) * ldo + h * HD + 4 * g;
+#pragma unroll
+    for (int d = 0; d < NDB; ++d)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bf16 v0 = static_cast<bf16>(acc[d][4 * j] * inv), v1 = static_cast<bf16>(acc[d][4 * j + 1] * inv);
+        const bf16 v2 = static_cast<bf16>(acc[d][4 * j + 2] * inv), v3 = static_cast<bf16>(acc[d][4 * j + 3] * inv);
+        uint2 pk;
+        pk.x = (uint32_t)__builtin_bit_cast(uint16_t, v0) | ((uint32_t)__builtin_bit_cast(uint16_t, v1) << 16);
+        pk.y = (uint32_t)__builtin_bit_cast(uint16_t, v2) | ((uint32_t)__builtin_bit_cast(uint16_t, v3) << 16);
+        *reinterpret_cast<uint2 *>(dst + 32 * d + 8 * j) = pk;
+      }
   }
 }
 
@@ -312,10 +496,17 @@ hipError_t run_prefill(const void *q, int ldq, const void *kc, const void *vc, v
                        const int *cu, const int2 *qtiles, int n_qtiles, int hq, int hkv,
                        int max_ctx, hipStream_t s) {
   const float scale_log2 = kLog2e / sqrtf((float)HD);
-  LL_LAUNCH((k_attn_prefill<T, HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
-                     reinterpret_cast<const T *>(q), ldq, reinterpret_cast<const T *>(kc),
-                     reinterpret_cast<const T *>(vc), reinterpret_cast<T *>(o), ldo, cu, qtiles,
-                     hq, hkv, max_ctx, scale_log2);
+  if constexpr (!std::is_same<T, float>::value) {
+    LL_LAUNCH((k_attn_prefill_wide<HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
+              reinterpret_cast<const bf16 *>(q), ldq, reinterpret_cast<const bf16 *>(kc),
+              reinterpret_cast<const bf16 *>(vc), reinterpret_cast<bf16 *>(o), ldo, cu, qtiles,
+              hq, hkv, max_ctx, scale_log2);
+  } else {
+    LL_LAUNCH((k_attn_prefill<T, HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
+              reinterpret_cast<const T *>(q), ldq, reinterpret_cast<const T *>(kc),
+              reinterpret_cast<const T *>(vc), reinterpret_cast<T *>(o), ldo, cu, qtiles, hq,
+              hkv, max_ctx, scale_log2);
+  }
   return hipGetLastError();
 }
 

@@ -21,6 +21,17 @@
 typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void global_void_t;
+
+// global_load_lds_dwordx4: lane l's 16 bytes from `src` (its own address) land at byte
+// 16 l of the 1 KiB LDS tile; the wave's LDS base goes through M0, so `lds_tile` must be
+// wave-uniform.  Completion is counted by vmcnt.
+__device__ __forceinline__ void load_tile_to_lds(const void *src, void *lds_tile) {
+  __builtin_amdgcn_global_load_lds((global_void_t *)src, (lds_void_t *)lds_tile, 16, 0, 0);
+}
 
 // One lane's 16-byte share of a 16-row MFMA operand tile.
 //   bf16: 8 elements, the tile spans 32 along the contraction axis (v_mfma_f32_16x16x32_bf16)
@@ -47,6 +58,13 @@ __device__ __forceinline__ f32x4 mma_chunk(const f32x4 &a, const f32x4 &b, f32x4
   c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], c, 0, 0, 0);
   c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], c, 0, 0, 0);
   return c;
+}
+
+// 32x32 output tile += A x B over 16 contraction indices (v_mfma_f32_32x32x16_bf16).
+// A lane l: row l % 32, contraction 8 (l / 32) + e; B lane l: column l % 32, same contraction
+// indices.  Output: lane l holds column l % 32, rows 8 (i / 4) + 4 (l / 32) + i % 4, i < 16.
+__device__ __forceinline__ f32x16 mma32(const bf16x8 &a, const bf16x8 &b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
 __device__ __forceinline__ float to_f32(float x) { return x; }

@@ -91,7 +91,7 @@ __global__ __launch_bounds__(256) void k_argmax_reduce(const float *__restrict__
   }
 }
 
-__global__ __launch_bounds__(256) void k_prefill_meta(PrefillMeta pm, int total, int *cu,
+__global__ __launch_bounds__(256) void k_prefill_meta(PrefillMeta pm, int total, int qtile, int *cu,
                                                       int *row_seq, int *row_pos, int *last_row,
                                                       int *lens_dev, int2 *qtiles) {
   const int m = blockIdx.x * blockDim.x + threadIdx.x;
@@ -108,14 +108,14 @@ __global__ __launch_bounds__(256) void k_prefill_meta(PrefillMeta pm, int total,
       acc += pm.lens[b];
       last_row[b] = acc - 1;
       lens_dev[b] = pm.lens[b];
-      maxt = max(maxt, (pm.lens[b] + kAttnQTile - 1) / kAttnQTile);
+      maxt = max(maxt, (pm.lens[b] + qtile - 1) / qtile);
     }
     cu[pm.batch] = acc;
-    // Longest causal work first: tile t of any sequence attends to (t + 1) * 64 keys.
+    // Longest causal work first: tile t of any sequence attends to (t + 1) * qtile keys.
     int n = 0;
     for (int t = maxt - 1; t >= 0; --t)
       for (int b = 0; b < pm.batch; ++b)
-        if (t * kAttnQTile < pm.lens[b]) qtiles[n++] = make_int2(b, t);
+        if (t * qtile < pm.lens[b]) qtiles[n++] = make_int2(b, t);
   }
 }
 
@@ -155,11 +155,12 @@ hipError_t launch_argmax_reduce(const float *pval, const int *pidx, int rows, in
   return hipGetLastError();
 }
 
-hipError_t launch_prefill_meta(const PrefillMeta &pm, int total, int *cu, int *row_seq,
-                               int *row_pos, int *last_row, int *lens_dev, int2 *qtiles,
-                               hipStream_t s) {
+hipError_t launch_prefill_meta(const PrefillMeta &pm, int total, int qtile, int *cu,
+                               int *row_seq, int *row_pos, int *last_row, int *lens_dev,
+                               int2 *qtiles, hipStream_t s) {
+  if (qtile <= 0) return hipErrorInvalidValue;
   const int blocks = std::max(1, (total + 255) / 256);
-  LL_LAUNCH(k_prefill_meta, dim3(blocks), dim3(256), 0, s, pm, total, cu, row_seq,
+  LL_LAUNCH(k_prefill_meta, dim3(blocks), dim3(256), 0, s, pm, total, qtile, cu, row_seq,
                      row_pos, last_row, lens_dev, qtiles);
   return hipGetLastError();
 }

@@ -227,13 +227,6 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const T *__restrict__ A, int
 // (workgroups are dealt round-robin to the 8 XCDs) works on a compact group of output tiles
 // and shares A and W tiles in its own L2.
 // ------------------------------------------------------------------------------------------
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void global_void_t;
-
-__device__ __forceinline__ void load_tile_to_lds(const void *src, void *lds_tile) {
-  __builtin_amdgcn_global_load_lds((global_void_t *)src, (lds_void_t *)lds_tile, 16, 0, 0);
-}
-
 // Bijection from dispatch order to a tile order in which XCD x owns a contiguous range.
 __device__ __forceinline__ int xcd_remap(int pid, int n) {
   constexpr int kXcd = 8;

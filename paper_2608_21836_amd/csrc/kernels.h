@@ -118,10 +118,13 @@ struct PrefillMeta {
   int batch;
   int lens[256];
 };
-hipError_t launch_prefill_meta(const PrefillMeta &pm, int total, int *cu_seqlens, int *row_seq,
-                               int *row_pos, int *last_row, int *lens_dev, int2 *qtiles,
-                               hipStream_t s);
-constexpr int kAttnQTile = 64;  // queries per prefill-attention block
+hipError_t launch_prefill_meta(const PrefillMeta &pm, int total, int qtile, int *cu_seqlens,
+                               int *row_seq, int *row_pos, int *last_row, int *lens_dev,
+                               int2 *qtiles, hipStream_t s);
+constexpr int kAttnQTile = 64;       // queries per block, fp32 prefill attention
+constexpr int kAttnQTileWide = 128;  // queries per block, bf16 prefill attention
+// Query-tile size the prefill attention kernel for (dtype, head_dim) expects in `qtiles`.
+inline int attn_prefill_qtile(int dtype) { return dtype == kF32 ? kAttnQTile : kAttnQTileWide; }
 
 hipError_t launch_attn_prefill(int dtype, int head_dim, const void *q, int ldq,
                                const void *kcache, const void *vcache, void *o, int ldo,

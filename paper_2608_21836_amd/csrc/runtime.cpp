@@ -506,6 +506,7 @@ ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
   if (m->batch != 0) return fail(LL_ERR_STATE, "prefill on a non-empty cache (call ll_kv_reset)");
   long total = 0;
   int n_qtiles = 0;
+  const int qtile = attn_prefill_qtile(c.dtype);
   PrefillMeta pm;
   pm.batch = batch;
   for (int b = 0; b < batch; ++b) {
@@ -513,7 +514,7 @@ ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
     if (L < 1) return fail(LL_ERR_INVALID_ARGUMENT, "seq_lens[%d] = %d < 1", b, L);
     if (L > c.max_ctx) return fail(LL_ERR_CAPACITY, "seq_lens[%d] = %d > max_ctx %d", b, L, c.max_ctx);
     total += L;
-    n_qtiles += (L + kAttnQTile - 1) / kAttnQTile;
+    n_qtiles += (L + qtile - 1) / qtile;
     pm.lens[b] = L;
   }
   if (total > c.max_prefill_tokens)
@@ -523,8 +524,9 @@ ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
   const Layout &L = m->L;
   TimerScope scope(m->timer, 0);
   m->mark(LL_K_META);
-  LL_HIP(launch_prefill_meta(pm, T, m->at<int>(L.cu), m->at<int>(L.row_seq), m->at<int>(L.row_pos),
-                             m->at<int>(L.last_row), m->at<int>(L.lens), m->at<int2>(L.qtiles), s));
+  LL_HIP(launch_prefill_meta(pm, T, qtile, m->at<int>(L.cu), m->at<int>(L.row_seq),
+                             m->at<int>(L.row_pos), m->at<int>(L.last_row), m->at<int>(L.lens),
+                             m->at<int2>(L.qtiles), s));
   m->mark(LL_K_EMBED);
   LL_HIP(launch_embed(c.dtype, tokens_dev, T, m->at(L.embed), c.vocab, c.d_model,
                       m->at<float>(L.x), m->at<int>(L.err), s));
@@ -732,12 +734,13 @@ ll_status ll_op_attn_prefill(int32_t dtype, int32_t batch, const int32_t *seq_le
   pm.batch = batch;
   long total = 0;
   int n_qtiles = 0;
+  const int qtile = attn_prefill_qtile(dtype);
   for (int b = 0; b < batch; ++b) {
     const int L = seq_lens_host[b];
     if (L < 1 || L > max_ctx) return fail(LL_ERR_INVALID_ARGUMENT, "seq_lens[%d] = %d outside [1, max_ctx]", b, L);
     pm.lens[b] = L;
     total += L;
-    n_qtiles += (L + kAttnQTile - 1) / kAttnQTile;
+    n_qtiles += (L + qtile - 1) / qtile;
   }
   if ((st = check_ws(scratch)) != LL_OK) return st;
   size_t off = 0;
@@ -747,7 +750,7 @@ ll_status ll_op_attn_prefill(int32_t dtype, int32_t batch, const int32_t *seq_le
   if (off > scratch_bytes) return fail(LL_ERR_WORKSPACE, "scratch needs %zu bytes", off);
   char *sc = reinterpret_cast<char *>(scratch);
   hipStream_t s = (hipStream_t)stream;
-  LL_HIP(launch_prefill_meta(pm, (int)total, (int *)(sc + o_cu), (int *)(sc + o_seq),
+  LL_HIP(launch_prefill_meta(pm, (int)total, qtile, (int *)(sc + o_cu), (int *)(sc + o_seq),
                              (int *)(sc + o_pos), (int *)(sc + o_last), (int *)(sc + o_lens),
                              (int2 *)(sc + o_qt), s));
   const int qd = n_heads * head_dim;

@@ -94,6 +94,10 @@ ATTN_CASES = [
     ("bf16", 64, 8, 2, [1, 63, 64, 65, 200]),
     ("bf16", 128, 4, 1, [130, 7]),
     ("bf16", 128, 8, 8, [96]),
+    # several 128-query tiles and 64-key tiles, ragged tails, GQA groups of 4
+    ("bf16", 128, 8, 2, [300, 129, 1, 257]),
+    ("bf16", 128, 4, 4, [1030]),
+    ("bf16", 64, 4, 1, [513, 128, 127]),
     ("f32", 64, 4, 4, [33, 1, 128]),
     ("f32", 128, 4, 2, [70]),
 ]
