@@ -216,9 +216,11 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
     if (wave < VW) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
+        // rows past the sequence are read clamped (in bounds) and replaced by zeros: their
+        // probabilities are 0, and the cache there may hold anything, NaN included
         const int key = kt * BKV + 16 * pc + (e < 4 ? 4 * gg + e : 8 + 4 * gg + e - 4);
-        vr[e] = key < L ? *reinterpret_cast<const uint4 *>(Vc + kvbase + (size_t)key * HD + 8 * dg)
-                        : make_uint4(0, 0, 0, 0);
+        const uint4 v = *reinterpret_cast<const uint4 *>(Vc + kvbase + (size_t)min(key, L - 1) * HD + 8 * dg);
+        vr[e] = key < L ? v : make_uint4(0, 0, 0, 0);
       }
     }
   };
@@ -251,30 +253,40 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
       for (int c = 0; c < NKC; ++c)
         sc[kb] = mma32(*reinterpret_cast<const bf16x8 *>(&st[(kb * NKC + c) * 64 + lane]), qf[c], sc[kb]);
     }
-    const bool masked = kt * BKV + BKV - 1 > qw || qw + 31 >= L;
+    // Causal / length mask, only on tiles that reach past the wave's first query.
+    if (kt * BKV + BKV - 1 > qw || qw + 31 >= L) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = kt * BKV + 32 * kb + 8 * (i / 4) + 4 * g + (i % 4);
+          sc[kb][i] = (q_ok & (key <= my_q)) ? sc[kb][i] : -INFINITY;
+        }
+    }
+    // Row maximum of the raw scores; scaling by a positive constant commutes with max.
     float tmax = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int key = kt * BKV + 32 * kb + 8 * (i / 4) + 4 * g + (i % 4);
-        const float v = (!masked || (q_ok && key <= my_q)) ? sc[kb][i] * scale_log2 : -INFINITY;
-        sc[kb][i] = v;
-        tmax = fmaxf(tmax, v);
-      }
+      for (int i = 0; i < 16; ++i) tmax = fmaxf(tmax, sc[kb][i]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-    const float m_new = fmaxf(m_run, tmax);
+    const float m_new = fmaxf(m_run, tmax * scale_log2);
     const float base = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = exp2f(m_run - base);
-    m_run = m_new;
-    l_run *= alpha;
+    // Rescale only when some lane's maximum grew (otherwise every factor is exactly 1).
+    if (__any(m_new > m_run)) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - base);
+      l_run *= alpha;
 #pragma unroll
-    for (int d = 0; d < NDB; ++d) acc[d] *= alpha;
+      for (int d = 0; d < NDB; ++d) acc[d] *= alpha;
+    }
+    m_run = m_new;
+    // p = 2^(s * scale - m); arguments are <= 0, so the hardware exp2 is exact enough
+    // (results below the fp32 normal range flush to 0).
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float p = exp2f(sc[kb][i] - base);
+        const float p = __builtin_amdgcn_exp2f(fmaf(sc[kb][i], scale_log2, -base));
         sc[kb][i] = p;
         l_run += p;
       }
