@@ -40,6 +40,18 @@ ll_status ll_op_repack(int32_t dtype, int32_t n, int32_t k, const void *w, void 
 ll_status ll_op_gemm(int32_t path, int32_t dtype, int32_t m, int32_t n, int32_t k,
                      const void *a, const void *wt, float *c, int32_t accumulate, void *stream);
 
+/* Decode GEMM for batches above 16 rows, split over K: C = A W^T (accumulate = 0) or
+ * C += A W^T.  Each block of 128 output columns covers a slice of K and stages its slice of
+ * A in LDS once for all its columns; fp32 partial sums go to `scratch`, and a second kernel
+ * adds them in split order and writes C.  Same A / wt / C layouts as ll_op_gemm.  Requires
+ * m > 16, n a multiple of 128, k a multiple of 64, and scratch >= ll_op_gemm_splitk_scratch
+ * bytes (LL_ERR_UNSUPPORTED / LL_ERR_WORKSPACE otherwise). */
+ll_status ll_op_gemm_splitk(int32_t dtype, int32_t m, int32_t n, int32_t k, const void *a,
+                            const void *wt, float *c, int32_t accumulate, void *scratch,
+                            size_t scratch_bytes, void *stream);
+/* Scratch bytes ll_op_gemm_splitk needs for this shape; 0 if the shape is not supported. */
+size_t ll_op_gemm_splitk_scratch(int32_t dtype, int32_t m, int32_t n, int32_t k);
+
 /* Causal grouped-query prefill attention over packed ragged sequences (appendix
  * "Deployment Kernel Families": one program per query tile and head, KV head from the head
  * grouping, causal mask in the score update, fp32 online-softmax statistics).

@@ -574,6 +574,119 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
   }
 }
 
+// ------------------------------------------------------------------------------------------
+// Split-K decode GEMM for 17..32 rows (e.g. a batch of 32 sequences).  With whole-K blocks
+// of 32 columns, every block re-reads all of A (32 rows x K) through L1, as many bytes as its
+// weights: the activation traffic, not HBM, then limits the stream.  Here a block of 8 waves
+// owns 128 columns (one 16-column weight tile per wave) and a slice of K; its 32 x slice A
+// tile is DMA'd into LDS once and feeds all 8 waves.  Slices are sized so the grid has
+// ~512 blocks; each block writes fp32 partial sums part[split][m][n], and a second kernel
+// sums the splits in order (deterministic) and applies the epilogue.
+// ------------------------------------------------------------------------------------------
+template <typename T, int KTS>
+__global__ __launch_bounds__(512) void k_gemm_splitk(const T *__restrict__ A, int lda,
+                                                     const uint8_t *__restrict__ Wt, int M,
+                                                     int m_base, int N, int K,
+                                                     float *__restrict__ part) {
+  constexpr int kts = KTS;
+  using F = typename Frag<T>::type;
+  constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL, NW = 8, U = 16;
+  __shared__ uint4 sAk[2 * KTS * 64];  // [k-tile][row block][64]
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int ct = blockIdx.x * NW + wave;  // 16-column weight tile of this wave
+  const int kb_n = K / TK;
+  const int kt0 = blockIdx.y * kts, nk = min(kts, kb_n - kt0);
+  const F fz = frag_zero<F>();
+  const uint8_t *wp = Wt + (((size_t)ct * kb_n + kt0) * 64 + lane) * 16;
+  // A slice first: tile (t, rb) holds rows m_base + 16 rb + l % 16 (clamped to M - 1; those
+  // results are never stored), contraction indices (kt0 + t) TK + EPL (l / 16) + e.
+  // A fixed number of 16-byte loads per lane (slots past 2 nk receive a copy of a valid
+  // tile and are never read), so the code stays straight-line.  The A slice (mostly L2
+  // hits) is stored to LDS before the weight stream starts: a wait for it issued after the
+  // weight loads would also wait for them, since loads complete in order.
+  static_assert((2 * KTS) % NW == 0, "A tiles split evenly over the waves");
+  constexpr int NA = 2 * KTS / NW;
+  {
+    uint4 areg[NA];
+#pragma unroll
+    for (int j = 0; j < NA; ++j) {
+      const int i = wave + NW * j, t = min(i >> 1, nk - 1), rb = i & 1;
+      const int row = min(m_base + 16 * rb + (lane & 15), M - 1);
+      areg[j] = *reinterpret_cast<const uint4 *>(A + (size_t)row * lda + (size_t)(kt0 + t) * TK + (lane >> 4) * EPL);
+    }
+#pragma unroll
+    for (int j = 0; j < NA; ++j) sAk[(wave + NW * j) * 64 + lane] = areg[j];
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  // Then a ring of U weight tiles in flight: each tile's slot is refilled with the tile U
+  // ahead as soon as it has been consumed, so the stream never drains between batches.
+  // (The scheduling barriers keep the loads in ring order, so the wait before tile q is for
+  // the q-th oldest load only.)
+  F bw[U];
+#pragma unroll
+  for (int q = 0; q < U; ++q) {
+    bw[q] = load_frag_stream<F>(wp + (size_t)min(q, nk - 1) * 1024);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // LDS stores complete, then a bare barrier (a full __syncthreads would also wait for the
+  // weight loads in flight).
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+
+  // The slice is a compile-time number of tiles, fully unrolled: straight-line code in which
+  // the compiler's vmcnt bookkeeping sees one load issued per tile consumed and waits only
+  // for the oldest.  Past nk (last split only) the weights are replaced by zeros and A is
+  // read at a clamped (written) tile, so those steps add exactly zero.
+  f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+  for (int tt = 0; tt < KTS; ++tt) {
+    const F w = tt < nk ? bw[tt % U] : fz;
+    const int ta = min(tt, nk - 1);
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+      acc[rb] = mma_chunk(*reinterpret_cast<const F *>(&sAk[(ta * 2 + rb) * 64 + lane]), w, acc[rb]);
+    if (tt + U < KTS) bw[tt % U] = load_frag_stream<F>(wp + (size_t)min(tt + U, nk - 1) * 1024);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  float *dst = part + (size_t)blockIdx.y * M * N + 16 * ct + (lane & 15);
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = m_base + 16 * rb + 4 * (lane >> 4) + r;
+      if (m < M) dst[(size_t)m * N] = acc[rb][r];
+    }
+}
+
+// Sum of the split partials in split order, then the epilogue: per (row, 32-column unit,
+// column c) for pairing epilogues, per (row, column) otherwise.
+template <typename Epi>
+__global__ __launch_bounds__(256) void k_splitk_reduce(const float *__restrict__ part, int nsplit,
+                                                       int M, int N, Epi epi) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  const size_t plane = (size_t)M * N;
+  if constexpr (Epi::kPairs) {
+    if (idx >= (long)M * (N / 2)) return;
+    const int m = (int)(idx / (N / 2)), rem = (int)(idx % (N / 2));
+    const int u = rem / 16, c = rem % 16;
+    const float *p = part + (size_t)m * N + 32 * u + c;
+    float v0 = 0.f, v1 = 0.f;
+    for (int sp = 0; sp < nsplit; ++sp) {
+      v0 += p[sp * plane];
+      v1 += p[sp * plane + 16];
+    }
+    epi(m, u, c, v0, v1);
+  } else {
+    if (idx >= (long)M * N) return;
+    const int m = (int)(idx / N), n = (int)(idx % N);
+    const float *p = part + (size_t)m * N + n;
+    float v = 0.f;
+    for (int sp = 0; sp < nsplit; ++sp) v += p[sp * plane];
+    epi.one(m, n, v);
+  }
+}
+
 // The 256 x 256 kernel is used once it fills most of the 256 CUs with one block each.
 constexpr int kBigGemmMinTiles = 192;
 
@@ -605,6 +718,32 @@ hipError_t launch_skinny_one(const T *ap, int lda, const NormIn &nz, const Merge
   return hipGetLastError();
 }
 
+
+template <typename T, typename Epi>
+hipError_t run_splitk(const void *a, int lda, const void *wt, int m, int n, int k, const Epi &epi,
+                      const SplitKPlan &plan, float *ws, hipStream_t s) {
+  const size_t lds = 0;
+  for (int mb = 0; mb < m; mb += 32) {
+#define LL_SPLITK(KTS)                                                                        \
+  LL_LAUNCH((k_gemm_splitk<T, KTS>), dim3(n / 128, plan.nsplit), dim3(512), lds, s,            \
+            reinterpret_cast<const T *>(a), lda, reinterpret_cast<const uint8_t *>(wt), m, mb, \
+            n, k, ws)
+    switch (plan.kts) {
+      case 8: LL_SPLITK(8); break;
+      case 16: LL_SPLITK(16); break;
+      case 24: LL_SPLITK(24); break;
+      default: return hipErrorInvalidValue;
+    }
+#undef LL_SPLITK
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (g_launch_timer) g_launch_timer->secondary();
+  const long items = Epi::kPairs ? (long)m * (n / 2) : (long)m * n;
+  LL_LAUNCH((k_splitk_reduce<Epi>), dim3((unsigned)((items + 255) / 256)), dim3(256), 0, s, ws,
+            plan.nsplit, m, n, epi);
+  return hipGetLastError();
+}
 
 template <typename T, typename Epi>
 hipError_t run_skinny(const void *a, int lda, const NormIn *norm, const MergeIn *merge,
@@ -647,13 +786,19 @@ hipError_t run_skinny(const void *a, int lda, const NormIn *norm, const MergeIn 
 
 template <typename T, bool kTiled>
 hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm, const MergeIn *merge,
-                        const void *wt, int m, int n, int k, const EpiParams &ep, hipStream_t s) {
+                        const void *wt, int m, int n, int k, const EpiParams &ep, hipStream_t s,
+                        float *ws = nullptr, size_t ws_bytes = 0) {
+  const SplitKPlan plan = splitk_plan(elem_bytes(sizeof(T) == 4 ? kF32 : kBF16), m, n, k);
   auto run = [&](const auto &epi) {
     using E = std::decay_t<decltype(epi)>;
     if constexpr (kTiled) {
       if constexpr (E::kArgmax) return hipErrorInvalidValue;
       else return run_tiled<T>(a, lda, wt, m, n, k, epi, s);
     } else {
+      if constexpr (!E::kArgmax) {
+        if (plan.nsplit > 0 && !norm && !merge && ws && ws_bytes >= plan.ws_bytes)
+          return run_splitk<T>(a, lda, wt, m, n, k, epi, plan, ws, s);
+      }
       return run_skinny<T>(a, lda, norm, merge, wt, m, n, k, epi, s);
     }
   };
@@ -712,10 +857,25 @@ hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, 
 
 hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,
                               const void *wt, int m, int n, int k, const EpiParams &ep,
-                              hipStream_t s, const MergeIn *merge) {
+                              hipStream_t s, const MergeIn *merge, float *ws, size_t ws_bytes) {
   if (m <= 0) return hipSuccess;
-  return dtype == kF32 ? dispatch_epi<float, false>(a, lda, norm, merge, wt, m, n, k, ep, s)
-                       : dispatch_epi<bf16, false>(a, lda, norm, merge, wt, m, n, k, ep, s);
+  return dtype == kF32
+             ? dispatch_epi<float, false>(a, lda, norm, merge, wt, m, n, k, ep, s, ws, ws_bytes)
+             : dispatch_epi<bf16, false>(a, lda, norm, merge, wt, m, n, k, ep, s, ws, ws_bytes);
+}
+
+SplitKPlan splitk_plan(size_t elem, int m, int n, int k) {
+  SplitKPlan p;
+  const int tk = elem == 4 ? 16 : 32;
+  if (m <= 16 || n % 128 != 0 || k % tk != 0) return p;
+  const int kb_n = k / tk, groups = n / 128;
+  int nsplit = std::max(1, std::min(kb_n, (512 + groups - 1) / groups));
+  int kts = (kb_n + nsplit - 1) / nsplit;
+  kts = std::min((kts + 7) / 8 * 8, kSplitKMaxTiles);  // compiled slice lengths: 8, 16, 24
+  p.kts = kts;
+  p.nsplit = (kb_n + kts - 1) / kts;
+  p.ws_bytes = (size_t)p.nsplit * m * n * sizeof(float);
+  return p;
 }
 
 }  // namespace ll

@@ -99,9 +99,20 @@ constexpr size_t kSkinnyMaxNormLds = 48 * 1024;
 inline size_t skinny_norm_lds(size_t elem, int rows, int k) {
   return (size_t)(rows < 16 ? rows : 16) * (k + 16 / elem) * elem;
 }
+// Above 16 rows, with a workspace of at least splitk_plan(...).ws_bytes bytes (`ws`), the
+// decode GEMM splits K over blocks of 128 columns and reduces the fp32 partials in a second
+// kernel (not for the argmax epilogue); without one it takes the whole-K path.
 hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,
                               const void *wt, int m, int n, int k, const EpiParams &ep,
-                              hipStream_t s, const MergeIn *merge = nullptr);
+                              hipStream_t s, const MergeIn *merge = nullptr,
+                              float *ws = nullptr, size_t ws_bytes = 0);
+constexpr int kSplitKMaxTiles = 24;  // k-tiles per split-K block (A slice of 48 KiB in LDS)
+struct SplitKPlan {
+  int nsplit = 0;  // 0: split-K not used for this shape
+  int kts = 0;     // k-tiles per split
+  size_t ws_bytes = 0;
+};
+SplitKPlan splitk_plan(size_t elem, int m, int n, int k);
 
 hipError_t launch_embed(int dtype, const int *tokens, int ntok, const void *table, int vocab,
                         int d, float *x, int *err_flags, hipStream_t s);

@@ -93,6 +93,7 @@ struct Layout {
   size_t kcache = 0, vcache = 0, rcos = 0, rsin = 0;
   size_t x = 0, h = 0, q = 0, o = 0, act = 0, hf = 0;
   size_t part_o = 0, part_ml = 0, pval = 0, pidx = 0;
+  size_t splitk = 0, splitk_bytes = 0;  // fp32 split-K partials of the decode GEMMs
   size_t cu = 0, row_seq = 0, row_pos = 0, last_row = 0, lens = 0, qtiles = 0, err = 0;
   size_t total = 0;
   size_t kv_layer_elems = 0;
@@ -174,6 +175,13 @@ Layout make_layout(const ll_config &c) {
   L.hf = take((size_t)c.max_batch * d * eb);
   L.part_o = take((size_t)c.max_batch * c.n_heads * L.attn.nsplit * c.head_dim * 4);
   L.part_ml = take((size_t)c.max_batch * c.n_heads * L.attn.nsplit * 2 * 4);
+  {
+    const int F = c.ffn_dim;
+    const int shapes[4][2] = {{L.n_qkv, (int)d}, {(int)d, (int)qd}, {2 * F, (int)d}, {(int)d, F}};
+    for (const auto &nk : shapes)
+      L.splitk_bytes = std::max(L.splitk_bytes, splitk_plan(eb, c.max_batch, nk[0], nk[1]).ws_bytes);
+    L.splitk = take(L.splitk_bytes);
+  }
   L.pval = take((size_t)c.max_batch * L.n_parts * 4);
   L.pidx = take((size_t)c.max_batch * L.n_parts * 4);
   L.cu = take((c.max_batch + 1) * 4);
@@ -300,9 +308,11 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
     mrg.max_ctx = c.max_ctx;
   }
   float *x = m->at<float>(m->L.x);
+  float *splitk_ws = m->L.splitk_bytes ? m->at<float>(m->L.splitk) : nullptr;
   auto gemm = [&](const void *a, int lda, const NormIn *nrm, const void *wt, int n, int k,
                   const EpiParams &ep) {
-    return decode ? launch_gemm_skinny(dt, a, lda, nrm, wt, rows, n, k, ep, s)
+    return decode ? launch_gemm_skinny(dt, a, lda, nrm, wt, rows, n, k, ep, s, nullptr,
+                                       splitk_ws, m->L.splitk_bytes)
                   : launch_gemm_tiled(dt, a, lda, wt, rows, n, k, ep, s);
   };
   // The A operand of a projection that follows an RMSNorm: normalised in the GEMM, or by a
@@ -706,6 +716,31 @@ ll_status ll_op_gemm(int32_t path, int32_t dtype, int32_t m, int32_t n, int32_t 
   ep.ld_out = n;
   LL_HIP(path == 0 ? launch_gemm_tiled(dtype, a, k, wt, m, n, k, ep, (hipStream_t)stream)
                    : launch_gemm_skinny(dtype, a, k, nullptr, wt, m, n, k, ep, (hipStream_t)stream));
+  return LL_OK;
+}
+
+size_t ll_op_gemm_splitk_scratch(int32_t dtype, int32_t m, int32_t n, int32_t k) {
+  if ((dtype != LL_F32 && dtype != LL_BF16) || m < 1 || n < 1 || k < 1 || k % 64) return 0;
+  return splitk_plan(elem_bytes(dtype), m, n, k).ws_bytes;
+}
+
+ll_status ll_op_gemm_splitk(int32_t dtype, int32_t m, int32_t n, int32_t k, const void *a,
+                            const void *wt, float *c, int32_t accumulate, void *scratch,
+                            size_t scratch_bytes, void *stream) {
+  g_err.clear();
+  ll_status st = check_dtype(dtype);
+  if (st != LL_OK) return st;
+  if (m < 1 || n < 1 || k < 1) return fail(LL_ERR_INVALID_ARGUMENT, "bad sizes");
+  const size_t need = ll_op_gemm_splitk_scratch(dtype, m, n, k);
+  if (!need) return fail(LL_ERR_UNSUPPORTED, "m > 16, n %% 128 and k %% 64 required");
+  if (!a || !wt || !c || !scratch) return fail(LL_ERR_INVALID_ARGUMENT, "NULL pointer");
+  if (scratch_bytes < need) return fail(LL_ERR_WORKSPACE, "scratch needs %zu bytes", need);
+  EpiParams ep;
+  ep.kind = accumulate ? kEpiResid : kEpiStore;
+  ep.out_f32 = c;
+  ep.ld_out = n;
+  LL_HIP(launch_gemm_skinny(dtype, a, k, nullptr, wt, m, n, k, ep, (hipStream_t)stream, nullptr,
+                            reinterpret_cast<float *>(scratch), scratch_bytes));
   return LL_OK;
 }
 

@@ -79,6 +79,31 @@ def test_gemm(dtype, path, m, n, k):
     assert np.all(np.abs(_np(cacc) - (ref + c0)) <= bound + 2 * U * np.abs(ref + c0))
 
 
+SPLITK_SHAPES = [(17, 128, 64), (32, 512, 256), (32, 4096, 1024), (33, 384, 4096),
+                 (64, 256, 14336), (20, 6144, 512)]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("m,n,k", SPLITK_SHAPES)
+def test_gemm_splitk(dtype, m, n, k):
+    from paper_2608_21836_amd.binding import op_gemm_splitk, op_repack
+    import torch
+    log(f"gemm split-K {dtype} m={m} n={n} k={k}")
+    rng = np.random.default_rng(m * 7 + n + k)
+    a = rounded(rng.standard_normal((m, k)), dtype)
+    w = rounded(rng.standard_normal((n, k)) * 0.05, dtype)
+    c0 = rng.standard_normal((m, n)).astype(np.float32)
+    A, W = device_tensor(a, dtype), device_tensor(w, dtype)
+    wt = op_repack(W)
+    c = op_gemm_splitk(A, wt, n)
+    cacc = op_gemm_splitk(A, wt, n, c=torch.from_numpy(c0).cuda(), accumulate=True)
+    torch.cuda.synchronize()
+    ref = a.astype(np.float64) @ w.astype(np.float64).T
+    bound = 4 * k * U * (np.abs(a).astype(np.float64) @ np.abs(w).astype(np.float64).T) + 1e-30
+    assert np.all(np.abs(_np(c) - ref) <= bound)
+    assert np.all(np.abs(_np(cacc) - (ref + c0)) <= bound + 2 * U * np.abs(ref + c0))
+
+
 def _caches(rng, dtype, batch, hkv, max_ctx, hd, lens):
     """Random caches with every position at or beyond a sequence's length set to NaN, so a
     read of a stale or out-of-range entry poisons the output."""
