@@ -31,6 +31,39 @@ sys.path.insert(0, ROOT)
 METRIC = "prefill tok/s + decode tok/s on 1 MI355X; % of MFMA/HBM roofline"
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+PROFILES = os.path.join(ROOT, "profiles")
+COPY_CAL_BYTES = 256 << 20   # plain copy kernel used to scale the PMC byte counters
+
+
+def sources_sha256(paths) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in paths:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` from the committed PMC summary
+    profiles/<workload>_<phase>_<class>_traffic.md, or None when there is no summary or the
+    kernel sources changed since the counters were taken (their sha256 no longer matches)."""
+    path = os.path.join(PROFILES, f"{workload}_{kernel.replace(':', '_')}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("- ") and ": " in line:
+                k, v = line[2:].split(": ", 1)
+                fields[k.strip()] = v.strip().strip("`")
+    try:
+        srcs = fields["sources"].split()
+        if sources_sha256(srcs) != fields["sources_sha256"]:
+            return None
+        return float(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError, OSError):
+        return None
 
 
 def algorithmic_work(cfg, lens, n_decode):
@@ -128,6 +161,11 @@ def main() -> int:
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="launch decode kernels one by one instead of replaying a HIP graph")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain 256 MiB device copy kernel (reference for the "
+                         "FETCH_SIZE / WRITE_SIZE counters of a rocprofv3 --pmc run)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the path has no "
@@ -148,9 +186,18 @@ def main() -> int:
     dev_w = {name: to_device(arr, cfg.dtype) for name, arr in gen.iter_weights_parallel(cfg, workers)}
     dev_w.update({k: to_device(v, cfg.dtype) for k, v in gen.gains(cfg).items()})
     model = Model(cfg, dev_w, max_batch=B, max_prefill_tokens=T, max_ctx=max(lens) + N)
+    if args.no_graph:
+        model.set_decode_graph(False)
     torch.cuda.synchronize()
     del dev_w
     torch.cuda.empty_cache()
+    if args.copy_calibration:
+        src = torch.ones(COPY_CAL_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)   # reads and writes COPY_CAL_BYTES each
+        torch.cuda.synchronize()
+        del src, dst
     tokens = torch.from_numpy(np.asarray(packed, dtype=np.int32)).cuda()
     nxt = torch.empty(B, dtype=torch.int32, device="cuda")
 
@@ -220,8 +267,9 @@ def main() -> int:
         dom = next(r for r in rows if "achieved" in r)
         wv, unit = work[(dom["phase"], dom["class"])]
         a, peak, u, bound = rate(wv, unit, dom["total_ms"], cfg.dtype)
+        traffic = measured_traffic(cfg.name, f"{dom['phase']}:{dom['class']}")
         out["roofline"] = {"bound": bound, "achieved": round(a, 2), "peak": peak, "unit": u,
-                           "frac": round(a / peak, 4), "traffic": None,
+                           "frac": round(a / peak, 4), "traffic": traffic,
                            "kernel": f"{dom['phase']}:{dom['class']}",
                            "launches": dom["launches"], "avg_us": dom["avg_us"],
                            "work_per_launch": wv / dom["launches"],
