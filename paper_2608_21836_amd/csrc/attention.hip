@@ -3,11 +3,11 @@
 // and fp32 online-softmax statistics, and a decode kernel that loads each KV tile once for
 // the whole query-head group).
 //
-// Prefill: one block per (query tile of 64, query head); 4 waves x 16 queries.  Scores are
-// computed transposed, S^T = K Q^T, so that each lane owns one query column: the softmax
-// statistics and the O^T = V^T P^T accumulator are then lane-local, and P feeds the second
-// MFMA as its B operand without leaving registers.  K and V^T tiles are staged in LDS in
-// MFMA operand order.
+// Prefill: scores are computed transposed, S^T = K Q^T, so that each lane owns one query
+// column: the softmax statistics and the O^T = V^T P^T accumulator are then lane-local, and
+// P feeds the second MFMA as its B operand without leaving registers.  bf16 uses 32x32x16
+// MFMAs over 128-query tiles (k_attn_prefill_wide); fp32 uses 16x16 MFMAs over 64-query
+// tiles (k_attn_prefill).  K and V^T tiles are staged in LDS in MFMA operand order.
 //
 // Decode: grid (split, kv head, sequence); a block streams `chunk` cached keys once for all
 // query heads of the group, keeps exact chunk scores in LDS and writes (max, sum, partial
