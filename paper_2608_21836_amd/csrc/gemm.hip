@@ -241,15 +241,18 @@ __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-template <typename T, typename Epi>
+template <typename T, typename Epi, int BM>
 __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, int lda,
                                                      const uint8_t *__restrict__ Wt, int M,
                                                      int N, int K, Epi epi) {
   using F = typename Frag<T>::type;
   constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL;
-  constexpr int BM = 256, BN = 256, GM = 8;
-  constexpr int S = 4, TPS = 32, LPW = TPS / 8;  // stages, tiles per stage, loads per wave
-  __shared__ uint4 smem[S * TPS * 64];  // [stage][A: 16 row tiles | W: 16 column tiles][64]
+  constexpr int BN = 256, GM = 8;
+  constexpr int NA = BM / 16;                  // A tiles per stage (16-row blocks)
+  constexpr int NI = BM / 32;                  // 16-row blocks per wave
+  constexpr int S = 4, TPS = NA + 16, LPW = TPS / 8;  // stages, tiles per stage, loads per wave
+  static_assert(TPS % 8 == 0, "loads split evenly over the 8 waves");
+  __shared__ uint4 smem[S * TPS * 64];  // [stage][A: NA row tiles | W: 16 column tiles][64]
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // 8 waves, 2 (M) x 4 (N)
   const int wm = wave >> 2, wn = wave & 3;
@@ -262,47 +265,49 @@ __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, in
   const int m0 = tm * BM, n0 = tn * BN;
   const int nsteps = K / TK;
 
-  // Waves 0-3 fill A tiles 4w .. 4w+3 (16-row blocks), waves 4-7 W tiles 4(w-4) .. +3.
-  const bool loads_a = wave < 4;
+  // Wave w fills stage tiles LPW w .. LPW w + LPW - 1: A tiles (16-row blocks) first, then
+  // the 16 W tiles (16-column blocks).
   const uint8_t *src[LPW];
 #pragma unroll
   for (int i = 0; i < LPW; ++i) {
     const int tt = wave * LPW + i;
-    if (loads_a) {
+    if (tt < NA) {
       const int row = min(m0 + tt * 16 + (lane & 15), M - 1);
       src[i] = reinterpret_cast<const uint8_t *>(A + (size_t)row * lda + (lane >> 4) * EPL);
     } else {
-      src[i] = Wt + (((size_t)(n0 / 16 + tt - 16) * nsteps) * 64 + lane) * 16;
+      src[i] = Wt + (((size_t)(n0 / 16 + tt - NA) * nsteps) * 64 + lane) * 16;
     }
   }
   // Steps past the end reload the last tile (the data is never read), so that every step
   // issues the same number of loads and the vmcnt arithmetic stays fixed.
   auto issue = [&](int step, int stage) {
     const int st = min(step, nsteps - 1);
-    const size_t off = loads_a ? (size_t)st * TK * sizeof(T) : (size_t)st * 1024;
 #pragma unroll
-    for (int i = 0; i < LPW; ++i)
+    for (int i = 0; i < LPW; ++i) {
+      const size_t off = wave * LPW + i < NA ? (size_t)st * TK * sizeof(T) : (size_t)st * 1024;
       load_tile_to_lds(src[i] + off, &smem[(stage * TPS + wave * LPW + i) * 64]);
+    }
   };
 
-  f32x4 acc[8][4];
+  f32x4 acc[NI][4];
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   auto read_frags = [&](int stage, F *fa, F *fb) {
     const uint4 *base = &smem[stage * TPS * 64];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) fb[j] = *reinterpret_cast<const F *>(&base[(16 + wn * 4 + j) * 64 + lane]);
+    for (int j = 0; j < 4; ++j) fb[j] = *reinterpret_cast<const F *>(&base[(NA + wn * 4 + j) * 64 + lane]);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) fa[i] = *reinterpret_cast<const F *>(&base[(wm * 8 + i) * 64 + lane]);
+    for (int i = 0; i < NI; ++i) fa[i] = *reinterpret_cast<const F *>(&base[(wm * NI + i) * 64 + lane]);
   };
   auto mma_half = [&](int h, const F *fa, const F *fb) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < NI / 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[h * 4 + i][j] = mma_chunk(fa[h * 4 + i], fb[j], acc[h * 4 + i][j]);
+      for (int j = 0; j < 4; ++j)
+        acc[h * (NI / 2) + i][j] = mma_chunk(fa[h * (NI / 2) + i], fb[j], acc[h * (NI / 2) + i][j]);
   };
   // One step: loads for step s+3, MFMAs (first half), barrier for stage s+1, fragments of
   // step s+1, MFMAs (second half).  The scheduling barriers keep the compiler from moving
@@ -325,7 +330,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, in
   issue(2, 2);
   wait_vmcnt<2 * LPW>();
   __syncthreads();
-  F fa0[8], fb0[4], fa1[8], fb1[4];
+  F fa0[NI], fb0[4], fa1[NI], fb1[4];
   read_frags(0, fa0, fb0);
   // nsteps is even (K is a multiple of two k-tiles); the last step reads a stage it never uses.
   for (int s = 0; s < nsteps; s += 2) {
@@ -336,10 +341,10 @@ __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, in
 
   const int ubase = (n0 + wn * 64) >> 5;
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int m = m0 + wm * 128 + i * 16 + (lane >> 4) * 4 + r;
+      const int m = m0 + wm * (BM / 2) + i * 16 + (lane >> 4) * 4 + r;
       if (m < M) {
 #pragma unroll
         for (int p = 0; p < 2; ++p) epi(m, ubase + p, lane & 15, acc[i][2 * p][r], acc[i][2 * p + 1][r]);
@@ -687,15 +692,28 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float *__restrict__
   }
 }
 
-// The 256 x 256 kernel is used once it fills most of the 256 CUs with one block each.
+// The 256 x 256 kernel is used once it fills most of the 256 CUs with one block each, else
+// (or when its last round of blocks would be mostly empty) the 128 x 256 variant, else the
+// 128 x 128 kernel.
 constexpr int kBigGemmMinTiles = 192;
 
 template <typename T, typename Epi>
 hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k, const Epi &epi,
                      hipStream_t s) {
   const int big_tiles = ((m + 255) / 256) * (n / 256);
-  if (n % 256 == 0 && big_tiles >= kBigGemmMinTiles) {
-    LL_LAUNCH((k_gemm_big<T, Epi>), dim3(big_tiles), dim3(512), 0, s,
+  const int half_tiles = ((m + 127) / 128) * (n / 256);
+  // Fraction of the last round of 256 blocks that has work; the 128-row tiles are preferred
+  // when they fill the rounds clearly better (they run about 5-10 % below the big tiles).
+  auto fill = [](int tiles) { return (double)tiles / (((tiles + 255) / 256) * 256); };
+  const bool prefer_half = fill(half_tiles) * 0.9 > fill(big_tiles);
+  if (n % 256 == 0 && big_tiles >= kBigGemmMinTiles && !prefer_half) {
+    LL_LAUNCH((k_gemm_big<T, Epi, 256>), dim3(big_tiles), dim3(512), 0, s,
+              reinterpret_cast<const T *>(a), lda, reinterpret_cast<const uint8_t *>(wt), m, n,
+              k, epi);
+    return hipGetLastError();
+  }
+  if (n % 256 == 0 && half_tiles >= kBigGemmMinTiles) {
+    LL_LAUNCH((k_gemm_big<T, Epi, 128>), dim3(half_tiles), dim3(512), 0, s,
               reinterpret_cast<const T *>(a), lda, reinterpret_cast<const uint8_t *>(wt), m, n,
               k, epi);
     return hipGetLastError();

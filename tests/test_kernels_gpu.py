@@ -53,6 +53,8 @@ GEMM_SHAPES = [
     (0, 1, 256, 64), (0, 130, 384, 768), (0, 300, 128, 192), (0, 257, 256, 1408),
     # enough 256 x 256 tiles for the large-tile kernel, with ragged M tails
     (0, 2000, 6144, 256), (0, 3000, 4096, 1024), (0, 6144, 2048, 128),
+    # 128 x 256 tiles (too few 256 x 256 tiles), exact and ragged M
+    (0, 2048, 4096, 512), (0, 1530, 4096, 256),
     (1, 1, 32, 64), (1, 1, 256, 768), (1, 15, 96, 192), (1, 16, 256, 512), (1, 17, 64, 64),
     (1, 32, 128, 4096), (1, 33, 64, 256), (1, 70, 96, 128),
 ]
