@@ -365,7 +365,7 @@ __global__ __launch_bounds__(256) void k_attn_decode(
   const int lane = tid & 63, wave = tid >> 6;
   const int hq = hkv * G;
   __shared__ float s_p[G][CH];
-  __shared__ float s_red[4][G][HD];
+  __shared__ float s_red[8][G][HD];  // [wave][32-lane half]
   __shared__ float s_m[G], s_l[G];
   const F fz = frag_zero<F>();
 
@@ -399,9 +399,7 @@ __global__ __launch_bounds__(256) void k_attn_decode(
       d[g] = a;
     }
 #pragma unroll
-    for (int o = LPK / 2; o > 0; o >>= 1)
-#pragma unroll
-      for (int g = 0; g < G; ++g) d[g] += __shfl_xor(d[g], o);
+    for (int g = 0; g < G; ++g) d[g] = group_sum<LPK>(d[g]);
     const int jj = slot + i * NSLOT;
     if (dl == 0 && jj < n)
 #pragma unroll
@@ -450,21 +448,24 @@ __global__ __launch_bounds__(256) void k_attn_decode(
       }
     }
   }
-#pragma unroll
-  for (int o = LPK; o < 64; o <<= 1)
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[g][e] += __shfl_xor(acc[g][e], o);
-  if (lane < LPK)
+  // Slots of one 32-lane half are summed across lanes, the 8 halves of the block in LDS.
+  if constexpr (LPK < 32) {
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) s_red[wave][g][dl * EPL + e] = acc[g][e];
+      for (int e = 0; e < EPL; ++e) acc[g][e] = stride_sum32<LPK>(acc[g][e]);
+  }
+  if ((lane & 31) < LPK)
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) s_red[2 * wave + (lane >> 5)][g][dl * EPL + e] = acc[g][e];
   __syncthreads();
   for (int i = tid; i < G * HD; i += 256) {
     const int g = i / HD, d = i % HD;
-    const float v = s_red[0][g][d] + s_red[1][g][d] + s_red[2][g][d] + s_red[3][g][d];
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) v += s_red[w][g][d];
     if (nsplit == 1)
       O[(size_t)b * ldo + (kvh * G + g) * HD + d] = from_f32<T>(v / s_l[g]);
     else

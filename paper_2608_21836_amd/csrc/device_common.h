@@ -90,6 +90,41 @@ template <typename F> __device__ __forceinline__ F load_frag_stream(const void *
   return __builtin_nontemporal_load(reinterpret_cast<const F *>(p));
 }
 
+// Cross-lane sums on the DPP / swizzle paths (no LDS-crossbar permutes).
+//   dpp_add<CTRL>(v): v + v from the lane the DPP control selects (all lanes enabled)
+template <int CTRL> __device__ __forceinline__ float dpp_add(float v) {
+  const int o = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false);
+  return v + __builtin_bit_cast(float, o);
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141; // lane i <-> 7 - i within 8 (pairs the two quads)
+constexpr int kDppMirror = 0x140;     // lane i <-> 15 - i within 16 (pairs the two halves)
+constexpr int kDppRor8 = 0x128;       // lane i <- (i + 8) mod 16 within 16
+__device__ __forceinline__ float swizzle_xor16_add(float v) {
+  // bit-mask swizzle over 32 lanes: and 0x1f, or 0, xor 0x10
+  const int o = __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), (0x10 << 10) | 0x1f);
+  return v + __builtin_bit_cast(float, o);
+}
+// Sum over aligned groups of W lanes (W = 8, 16 or 32); every lane of a group gets the sum.
+template <int W> __device__ __forceinline__ float group_sum(float v) {
+  static_assert(W == 8 || W == 16 || W == 32, "group of 8, 16 or 32 lanes");
+  v = dpp_add<kDppXor1>(v);
+  v = dpp_add<kDppXor2>(v);
+  v = dpp_add<kDppHalfMirror>(v);
+  if constexpr (W >= 16) v = dpp_add<kDppMirror>(v);
+  if constexpr (W >= 32) v = swizzle_xor16_add(v);
+  return v;
+}
+// Sum over the lanes of one 32-lane half that share (lane % W), W = 8, 16 or 32; every such
+// lane gets the sum.
+template <int W> __device__ __forceinline__ float stride_sum32(float v) {
+  static_assert(W == 8 || W == 16 || W == 32, "stride of 8, 16 or 32 lanes");
+  if constexpr (W <= 8) v = dpp_add<kDppRor8>(v);
+  if constexpr (W <= 16) v = swizzle_xor16_add(v);
+  return v;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
