@@ -125,15 +125,27 @@ template <int W> __device__ __forceinline__ float stride_sum32(float v) {
   return v;
 }
 
+template <int CTRL> __device__ __forceinline__ float dpp_max(float v) {
+  const int o = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false);
+  return fmaxf(v, __builtin_bit_cast(float, o));
+}
+__device__ __forceinline__ float lane_read(float v, int lane) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
+}
+// Whole-wave sum / maximum (every lane active): DPP and swizzle within each 32-lane half, then
+// the two halves' results read from lanes 0 and 32.
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  v = group_sum<32>(v);
+  return lane_read(v, 0) + lane_read(v, 32);
 }
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+  v = dpp_max<kDppXor1>(v);
+  v = dpp_max<kDppXor2>(v);
+  v = dpp_max<kDppHalfMirror>(v);
+  v = dpp_max<kDppMirror>(v);
+  const int o = __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), (0x10 << 10) | 0x1f);
+  v = fmaxf(v, __builtin_bit_cast(float, o));
+  return fmaxf(lane_read(v, 0), lane_read(v, 32));
 }
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)); }

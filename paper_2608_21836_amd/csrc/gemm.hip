@@ -414,17 +414,25 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
   // Staged modes: the block's rows in LDS, row stride K + EPL elements to spread banks.
   extern __shared__ __attribute__((aligned(16))) uint8_t dyn_smem[];
   T *sA = reinterpret_cast<T *>(dyn_smem);
-  __shared__ float s_ss[NW][16];
+  __shared__ float s_ss[NW][16];  // RMSNorm mode: sums of squares of row slices
+  __shared__ int s_wpr;
   const int nrows = min(M - m_base, 16);
   const int lds_ld = K + EPL;
   if constexpr (NORM) {
+    // The 8 waves are spread over the rows (wpr waves per row, each a 1/wpr slice of it), so
+    // every row's loads are in flight together.
     const T *g = reinterpret_cast<const T *>(norm.gain);
     const int k4n = K / 4;
-    for (int r = 0; r < nrows; ++r) {
+    int rows2 = 1;
+    while (rows2 < nrows) rows2 <<= 1;
+    const int wpr = rows2 >= NW ? 1 : NW / rows2;
+    const int sl = wave % wpr;
+    for (int r = wave / wpr; r < nrows; r += NW / wpr) {
       const int src = norm.rowmap ? norm.rowmap[m_base + r] : m_base + r;
       const float4 *xr = reinterpret_cast<const float4 *>(norm.x + (size_t)src * norm.ldx);
       float part = 0.f;
-      for (int k4 = threadIdx.x; k4 < k4n; k4 += 512) {
+#pragma unroll 4
+      for (int k4 = sl * 64 + lane; k4 < k4n; k4 += 64 * wpr) {
         const float4 v = xr[k4];
         part += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
         T *d = sA + (size_t)r * lds_ld + 4 * k4;
@@ -434,8 +442,9 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
         d[3] = from_f32<T>(v.w * to_f32(g[4 * k4 + 3]));
       }
       part = wave_sum(part);
-      if (lane == 0) s_ss[wave][r] = part;
+      if (lane == 0) s_ss[sl][r] = part;
     }
+    s_wpr = wpr;
     __syncthreads();
   } else if constexpr (AM == kAMerge) {
     // Same steps as the merge kernel: split statistics to LDS, per-(row, head) maximum and
@@ -533,8 +542,7 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
         const int rr = (lane >> 4) * 4 + r;
         float tot = 0.f;
         if (rr < nrows)
-#pragma unroll
-          for (int w = 0; w < NW; ++w) tot += s_ss[w][rr];
+          for (int w = 0; w < s_wpr; ++w) tot += s_ss[w][rr];
         const float sc = 1.0f / sqrtf(tot / (float)K + norm.eps);
 #pragma unroll
         for (int j = 0; j < NB; ++j) sv[j][r] *= sc;
