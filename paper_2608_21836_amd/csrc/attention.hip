@@ -504,6 +504,24 @@ __global__ __launch_bounds__(HD) void k_attn_combine(const float *__restrict__ p
   O[(size_t)b * ldo + h * HD + d] = from_f32<T>(merge_splits(part_o + base * HD + d, HD, s_w, s_l, ns));
 }
 
+// The merge for up to kCombineDirectSplits splits: one thread per output element, every
+// load issued up front (one memory round trip, no block-wide steps).
+constexpr int kCombineDirectSplits = 16;
+template <typename T, int HD>
+__global__ __launch_bounds__(HD) void k_attn_combine_direct(const float *__restrict__ part_o,
+                                                            const float *__restrict__ part_ml,
+                                                            const int *__restrict__ lens,
+                                                            int len_add, int hq, int kpb,
+                                                            int nsplit, int max_ctx,
+                                                            T *__restrict__ O, int ldo) {
+  const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
+  const int S = min(lens[b] + len_add, max_ctx);
+  const int ns = (S + kpb - 1) / kpb;
+  const size_t base = ((size_t)b * hq + h) * nsplit;
+  O[(size_t)b * ldo + h * HD + d] = from_f32<T>(
+      merge_splits_direct<kCombineDirectSplits>(part_ml + base * 2, part_o + base * HD + d, HD, ns));
+}
+
 template <typename T, int HD>
 hipError_t run_prefill(const void *q, int ldq, const void *kc, const void *vc, void *o, int ldo,
                        const int *cu, const int2 *qtiles, int n_qtiles, int hq, int hkv,
@@ -544,8 +562,14 @@ hipError_t run_decode_g(const void *q, int ldq, const void *kc, const void *vc, 
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || plan.nsplit == 1 || skip_merge) return e;
   if (g_launch_timer) g_launch_timer->secondary();
-  LL_LAUNCH((k_attn_combine<T, HD>), dim3(hkv * G, batch), dim3(HD), 0, s, part_o, part_ml, lens,
-            len_add, hkv * G, plan.kpb, plan.nsplit, max_ctx, reinterpret_cast<T *>(o), ldo);
+  if (plan.nsplit <= kCombineDirectSplits)
+    LL_LAUNCH((k_attn_combine_direct<T, HD>), dim3(hkv * G, batch), dim3(HD), 0, s, part_o,
+              part_ml, lens, len_add, hkv * G, plan.kpb, plan.nsplit, max_ctx,
+              reinterpret_cast<T *>(o), ldo);
+  else
+    LL_LAUNCH((k_attn_combine<T, HD>), dim3(hkv * G, batch), dim3(HD), 0, s, part_o, part_ml,
+              lens, len_add, hkv * G, plan.kpb, plan.nsplit, max_ctx, reinterpret_cast<T *>(o),
+              ldo);
   return hipGetLastError();
 }
 

@@ -156,6 +156,33 @@ constexpr float kLog2e = 1.4426950408889634f;
 // w_s = 2^(m_s - max_s m_s) (log-sum-exp rescaling of each split's unnormalised output o_s and
 // sum l_s).  `po` points at split 0's output element, `stride` floats between splits; w and l
 // usually sit in LDS.
+// The same merge for at most MAXS splits in one pass, all loads issued up front: `ml` holds
+// (m_s, l_s) pairs; slots past ns load split ns - 1 again and get weight 0.  Used where the
+// split count is small, so the merge costs one memory round trip.
+template <int MAXS>
+__device__ __forceinline__ float merge_splits_direct(const float *ml, const float *po,
+                                                     size_t stride, int ns) {
+  float m[MAXS], l[MAXS], o[MAXS];
+#pragma unroll
+  for (int sp = 0; sp < MAXS; ++sp) {
+    const int s = min(sp, ns - 1);
+    m[sp] = ml[2 * s];
+    l[sp] = ml[2 * s + 1];
+    o[sp] = po[s * stride];
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int sp = 0; sp < MAXS; ++sp) mx = fmaxf(mx, m[sp]);
+  float num = 0.f, den = 0.f;
+#pragma unroll
+  for (int sp = 0; sp < MAXS; ++sp) {
+    const float w = sp < ns ? exp2f(m[sp] - mx) : 0.f;
+    num += w * o[sp];
+    den += w * l[sp];
+  }
+  return num / den;
+}
+
 __device__ __forceinline__ float merge_splits(const float *po, size_t stride, const float *w,
                                               const float *l, int ns) {
   float num = 0.f, den = 0.f;

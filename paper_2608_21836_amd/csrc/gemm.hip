@@ -447,38 +447,18 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
     s_wpr = wpr;
     __syncthreads();
   } else if constexpr (AM == kAMerge) {
-    // Same steps as the merge kernel: split statistics to LDS, per-(row, head) maximum and
-    // weights, then the weighted sums in split order.
-    __shared__ float s_m[kMergeMaxParts], s_l[kMergeMaxParts], s_w[kMergeMaxParts];
+    // Each staged element merges its head's split partials itself: every load is issued up
+    // front (the statistics are the same address across the head's lanes), so the merge
+    // costs one memory round trip and no block-wide steps.
     const int hq = merge.n_heads, hd = merge.head_dim, nsp = merge.nsplit;
-    const int np = nrows * hq * nsp;
-    const size_t gbase = (size_t)m_base * hq * nsp;
-    auto n_splits = [&](int r) {
-      const int S = min(merge.lens[m_base + r] + merge.len_add, merge.max_ctx);
-      return (S + merge.kpb - 1) / merge.kpb;
-    };
-    for (int p = threadIdx.x; p < np; p += 512) {
-      if (p % nsp < n_splits(p / (hq * nsp))) {
-        s_m[p] = merge.part_ml[(gbase + p) * 2];
-        s_l[p] = merge.part_ml[(gbase + p) * 2 + 1];
-      }
-    }
-    __syncthreads();
-    for (int p = threadIdx.x; p < np; p += 512) {
-      const int sp = p % nsp, ns = n_splits(p / (hq * nsp));
-      if (sp < ns) {
-        float mx = -INFINITY;
-        for (int t = 0; t < ns; ++t) mx = fmaxf(mx, s_m[p - sp + t]);
-        s_w[p] = exp2f(s_m[p] - mx);
-      }
-    }
-    __syncthreads();
     for (int e = threadIdx.x; e < nrows * K; e += 512) {
       const int r = e / K, i = e % K;
       const int h = i / hd, d = i % hd;
-      const int q = (r * hq + h) * nsp;
-      sA[(size_t)r * lds_ld + i] = from_f32<T>(
-          merge_splits(merge.part_o + (gbase + q) * hd + d, hd, s_w + q, s_l + q, n_splits(r)));
+      const int S = min(merge.lens[m_base + r] + merge.len_add, merge.max_ctx);
+      const int ns = (S + merge.kpb - 1) / merge.kpb;
+      const size_t q = ((size_t)(m_base + r) * hq + h) * nsp;
+      sA[(size_t)r * lds_ld + i] = from_f32<T>(merge_splits_direct<kMergeMaxSplits>(
+          merge.part_ml + q * 2, merge.part_o + q * hd + d, hd, ns));
     }
     __syncthreads();
   } else if constexpr (AM == kAStaged) {
@@ -842,7 +822,7 @@ hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm, const MergeI
   if (merge && (!merge->part_o || !merge->part_ml || !merge->lens || merge->kpb <= 0 ||
                 merge->nsplit <= 0 || merge->max_ctx > merge->kpb * merge->nsplit ||
                 merge->head_dim <= 0 || merge->n_heads * merge->head_dim != k ||
-                (long)m * merge->n_heads * merge->nsplit > kMergeMaxParts))
+                merge->nsplit > kMergeMaxSplits))
     return hipErrorInvalidValue;
   switch (ep.kind) {
     case kEpiStore: return run(EpiStore{ep.out_f32, ep.ld_out});

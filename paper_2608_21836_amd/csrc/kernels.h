@@ -80,7 +80,7 @@ struct NormIn {
 
 // Split-K decode-attention partials merged inside the decode GEMM that consumes the attention
 // output (A = merged rows, computed exactly as the merge kernel computes them).
-constexpr int kMergeMaxParts = 256;  // rows * n_heads * nsplit
+constexpr int kMergeMaxSplits = 16;  // split partials merged inside the O projection
 struct MergeIn {
   const float *part_o = nullptr;   // [batch][n_heads][nsplit][head_dim]
   const float *part_ml = nullptr;  // [batch][n_heads][nsplit][2]

@@ -282,6 +282,7 @@ EpiParams argmax_epi(const ll_model *m, float *logits) {
 constexpr int kFusedNormMaxRows = 16;
 // Small decode batches merge the split attention partials inside the O projection when every
 // block can afford to read all of them (each of its blocks reads the whole set from L2).
+constexpr size_t kFusedMergeMaxBytes = 128 * 1024;
 
 // The decoder layers for `rows` rows.  decode: one row per sequence at position len[b].
 ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipStream_t s) {
@@ -294,7 +295,8 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
   const bool fuse_merge =
       decode && ap.nsplit > 1 && rows <= kFusedNormMaxRows &&
       skinny_norm_lds(elem_bytes(dt), rows, qd) <= kSkinnyMaxNormLds &&
-      (long)rows * c.n_heads * ap.nsplit <= kMergeMaxParts;
+      ap.nsplit <= kMergeMaxSplits &&
+      (size_t)rows * qd * ap.nsplit * 4 <= kFusedMergeMaxBytes;
   MergeIn mrg;
   if (fuse_merge) {
     mrg.part_o = m->at<float>(m->L.part_o);
