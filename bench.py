@@ -11,6 +11,8 @@ Printed JSON line:
   roofline       the kernel class with the largest summed kernel time in one job: its
                  algorithmic work (bytes for HBM-bound classes, flops for MFMA-bound ones)
                  over its summed kernel time, against the MI355X peak
+  phase_roofline prefill flops over prefill time (vs MFMA peak), decode bytes over decode
+                 time (vs HBM peak), whole phases
   kernels        every (phase, kernel class): launches, mean kernel time, achieved rate
   hotspot_eq1    the paper's phase-weighted hotspot score per kernel class
   cpu_baseline   the fp64 oracle on the host cores, on a bounded sample of the same workload
@@ -245,6 +247,22 @@ def main() -> int:
         "prefill_ms": round(pre_ms, 4), "decode_ms_per_step": round(dec_ms / N, 5),
         "prefill_tok_s": round(T / (pre_ms / 1e3), 1),
         "decode_tok_s": round(B * N / (dec_ms / 1e3), 1),
+    }
+
+    # Whole-phase rates: the phase's summed algorithmic work over its measured time
+    # (prefill: flops of the GEMMs and causal attention; decode: bytes per step).
+    work_all = algorithmic_work(cfg, lens, N)
+    pre_flop = sum(v for (ph, _), (v, u) in work_all.items() if ph == "prefill" and u == "flop")
+    dec_byte = sum(v for (ph, _), (v, u) in work_all.items() if ph == "decode" and u == "byte")
+    out["phase_roofline"] = {
+        "prefill": {"achieved": round(pre_flop / (pre_ms / 1e3) / 1e12, 2), "unit": "TFLOP/s",
+                    "peak": MFMA_PEAK_TFLOPS[cfg.dtype],
+                    "frac": round(pre_flop / (pre_ms / 1e3) / 1e12 / MFMA_PEAK_TFLOPS[cfg.dtype], 4),
+                    "work": "GEMM + causal attention flops"},
+        "decode": {"achieved": round(dec_byte / (dec_ms / 1e3) / 1e9, 2), "unit": "GB/s",
+                   "peak": HBM_PEAK_GBS,
+                   "frac": round(dec_byte / (dec_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                   "work": "weights, KV cache, activations per step"},
     }
 
     if not args.no_kernel_timing:
