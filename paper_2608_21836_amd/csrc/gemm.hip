@@ -10,6 +10,8 @@
 //    into MFMA B operands (non-temporal), A comes from L2; 8 waves split K, reduced in LDS.
 //  * Output columns come in units of 32 = two halves of 16 that land in the same lane, so the
 //    epilogues (RoPE pairs (i, i + hd/2), SwiGLU gate/up pairs) need no cross-lane traffic.
+#include <type_traits>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -680,6 +682,57 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float *__restrict__
   }
 }
 
+// Split sums added to the fp32 residual rows (EpiResid), followed by the RMSNorm of the
+// updated rows for the next projection: one block of 1024 threads per row, each thread one
+// float4 column group per 4096 columns, all split loads in flight together.
+template <typename T>
+__global__ __launch_bounds__(1024) void k_splitk_resid_norm(const float *__restrict__ part,
+                                                            int nsplit, int M, int N,
+                                                            float *__restrict__ x, int ldx,
+                                                            const T *__restrict__ gain, float eps,
+                                                            T *__restrict__ y, int ldy) {
+  const int m = blockIdx.x;
+  const size_t plane4 = (size_t)M * N / 4;
+  const int n4 = N >> 2;
+  const float4 *p4 = reinterpret_cast<const float4 *>(part) + (size_t)m * n4;
+  float4 *xr = reinterpret_cast<float4 *>(x + (size_t)m * ldx);
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < n4; i += 1024) {
+    float4 v = xr[i];
+    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8
+    for (int sp = 0; sp < nsplit; ++sp) {
+      const float4 q = p4[sp * plane4 + i];
+      a.x += q.x;
+      a.y += q.y;
+      a.z += q.z;
+      a.w += q.w;
+    }
+    v.x += a.x;
+    v.y += a.y;
+    v.z += a.z;
+    v.w += a.w;
+    xr[i] = v;
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  __shared__ float s_part[16];
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) s_part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < 16; ++w) tot += s_part[w];
+  const float scale = 1.0f / sqrtf(tot / (float)N + eps);
+  T *yr = y + (size_t)m * ldy;
+  for (int i = threadIdx.x; i < n4; i += 1024) {
+    const float4 v = xr[i];
+    yr[4 * i + 0] = from_f32<T>(v.x * scale * to_f32(gain[4 * i + 0]));
+    yr[4 * i + 1] = from_f32<T>(v.y * scale * to_f32(gain[4 * i + 1]));
+    yr[4 * i + 2] = from_f32<T>(v.z * scale * to_f32(gain[4 * i + 2]));
+    yr[4 * i + 3] = from_f32<T>(v.w * scale * to_f32(gain[4 * i + 3]));
+  }
+}
+
 // The 256 x 256 kernel is used once it fills most of the 256 CUs with one block each, else
 // (or when its last round of blocks would be mostly empty) the 128 x 256 variant, else the
 // 128 x 128 kernel.
@@ -727,7 +780,8 @@ hipError_t launch_skinny_one(const T *ap, int lda, const NormIn &nz, const Merge
 
 template <typename T, typename Epi>
 hipError_t run_splitk(const void *a, int lda, const void *wt, int m, int n, int k, const Epi &epi,
-                      const SplitKPlan &plan, float *ws, hipStream_t s) {
+                      const SplitKPlan &plan, float *ws, hipStream_t s,
+                      const PostNorm *post = nullptr) {
   const size_t lds = 0;
   for (int mb = 0; mb < m; mb += 32) {
 #define LL_SPLITK(KTS)                                                                        \
@@ -745,6 +799,14 @@ hipError_t run_splitk(const void *a, int lda, const void *wt, int m, int n, int 
     if (e != hipSuccess) return e;
   }
   if (g_launch_timer) g_launch_timer->secondary();
+  if constexpr (std::is_same<Epi, EpiResid>::value) {
+    if (post) {
+      LL_LAUNCH((k_splitk_resid_norm<T>), dim3(m), dim3(1024), 0, s, ws, plan.nsplit, m, n, epi.out,
+                epi.ld, reinterpret_cast<const T *>(post->gain), post->eps,
+                reinterpret_cast<T *>(post->out), post->ld_out);
+      return hipGetLastError();
+    }
+  }
   const long items = Epi::kPairs ? (long)m * (n / 2) : (long)m * n;
   LL_LAUNCH((k_splitk_reduce<Epi>), dim3((unsigned)((items + 255) / 256)), dim3(256), 0, s, ws,
             plan.nsplit, m, n, epi);
@@ -793,7 +855,9 @@ hipError_t run_skinny(const void *a, int lda, const NormIn *norm, const MergeIn 
 template <typename T, bool kTiled>
 hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm, const MergeIn *merge,
                         const void *wt, int m, int n, int k, const EpiParams &ep, hipStream_t s,
-                        float *ws = nullptr, size_t ws_bytes = 0) {
+                        float *ws = nullptr, size_t ws_bytes = 0, const PostNorm *post = nullptr,
+                        bool *post_done = nullptr) {
+  if (post_done) *post_done = false;
   const SplitKPlan plan = splitk_plan(elem_bytes(sizeof(T) == 4 ? kF32 : kBF16), m, n, k);
   auto run = [&](const auto &epi) {
     using E = std::decay_t<decltype(epi)>;
@@ -802,8 +866,11 @@ hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm, const MergeI
       else return run_tiled<T>(a, lda, wt, m, n, k, epi, s);
     } else {
       if constexpr (!E::kArgmax) {
-        if (plan.nsplit > 0 && !norm && !merge && ws && ws_bytes >= plan.ws_bytes)
-          return run_splitk<T>(a, lda, wt, m, n, k, epi, plan, ws, s);
+        if (plan.nsplit > 0 && !norm && !merge && ws && ws_bytes >= plan.ws_bytes) {
+          const bool fuse_post = post && std::is_same<E, EpiResid>::value && n % 4 == 0;
+          if (fuse_post && post_done) *post_done = true;
+          return run_splitk<T>(a, lda, wt, m, n, k, epi, plan, ws, s, fuse_post ? post : nullptr);
+        }
       }
       return run_skinny<T>(a, lda, norm, merge, wt, m, n, k, epi, s);
     }
@@ -863,11 +930,15 @@ hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, 
 
 hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,
                               const void *wt, int m, int n, int k, const EpiParams &ep,
-                              hipStream_t s, const MergeIn *merge, float *ws, size_t ws_bytes) {
+                              hipStream_t s, const MergeIn *merge, float *ws, size_t ws_bytes,
+                              const PostNorm *post, bool *post_done) {
+  if (post_done) *post_done = false;
   if (m <= 0) return hipSuccess;
-  return dtype == kF32
-             ? dispatch_epi<float, false>(a, lda, norm, merge, wt, m, n, k, ep, s, ws, ws_bytes)
-             : dispatch_epi<bf16, false>(a, lda, norm, merge, wt, m, n, k, ep, s, ws, ws_bytes);
+  if (post && (!post->gain || !post->out)) return hipErrorInvalidValue;
+  return dtype == kF32 ? dispatch_epi<float, false>(a, lda, norm, merge, wt, m, n, k, ep, s, ws,
+                                                    ws_bytes, post, post_done)
+                       : dispatch_epi<bf16, false>(a, lda, norm, merge, wt, m, n, k, ep, s, ws,
+                                                   ws_bytes, post, post_done);
 }
 
 SplitKPlan splitk_plan(size_t elem, int m, int n, int k) {

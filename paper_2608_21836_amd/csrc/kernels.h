@@ -102,10 +102,20 @@ inline size_t skinny_norm_lds(size_t elem, int rows, int k) {
 // Above 16 rows, with a workspace of at least splitk_plan(...).ws_bytes bytes (`ws`), the
 // decode GEMM splits K over blocks of 128 columns and reduces the fp32 partials in a second
 // kernel (not for the argmax epilogue); without one it takes the whole-K path.
+// With `post` and the residual epilogue, the split-K path also writes the RMSNorm of the
+// updated residual rows (post->out = rows of x times 1/rms times gain, in the workload dtype),
+// and sets *post_done; the other paths leave that to a separate RMSNorm launch.
+struct PostNorm {
+  const void *gain = nullptr;
+  float eps = 0.f;
+  void *out = nullptr;
+  int ld_out = 0;
+};
 hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,
                               const void *wt, int m, int n, int k, const EpiParams &ep,
                               hipStream_t s, const MergeIn *merge = nullptr,
-                              float *ws = nullptr, size_t ws_bytes = 0);
+                              float *ws = nullptr, size_t ws_bytes = 0,
+                              const PostNorm *post = nullptr, bool *post_done = nullptr);
 constexpr int kSplitKMaxTiles = 24;  // k-tiles per split-K block (A slice of 48 KiB in LDS)
 struct SplitKPlan {
   int nsplit = 0;  // 0: split-K not used for this shape

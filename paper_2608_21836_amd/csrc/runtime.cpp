@@ -285,7 +285,10 @@ constexpr int kFusedNormMaxRows = 16;
 constexpr size_t kFusedMergeMaxBytes = 128 * 1024;
 
 // The decoder layers for `rows` rows.  decode: one row per sequence at position len[b].
-ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipStream_t s) {
+// *hf_ready: the last layer's down projection also wrote the final RMSNorm rows into hf.
+ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipStream_t s,
+                         bool *hf_ready = nullptr) {
+  if (hf_ready) *hf_ready = false;
   const ll_config &c = m->cfg;
   const int d = c.d_model, qd = c.n_heads * c.head_dim, F = c.ffn_dim;
   const int dt = c.dtype;
@@ -311,17 +314,32 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
   }
   float *x = m->at<float>(m->L.x);
   float *splitk_ws = m->L.splitk_bytes ? m->at<float>(m->L.splitk) : nullptr;
+  // h_ready: the previous residual GEMM already wrote the next RMSNorm rows into h (split-K
+  // decode GEMMs fold the norm into their final reduction).
+  bool h_ready = false;
   auto gemm = [&](const void *a, int lda, const NormIn *nrm, const void *wt, int n, int k,
-                  const EpiParams &ep) {
+                  const EpiParams &ep, const PostNorm *post = nullptr, bool *post_done = nullptr) {
     return decode ? launch_gemm_skinny(dt, a, lda, nrm, wt, rows, n, k, ep, s, nullptr,
-                                       splitk_ws, m->L.splitk_bytes)
+                                       splitk_ws, m->L.splitk_bytes, post, post_done)
                   : launch_gemm_tiled(dt, a, lda, wt, rows, n, k, ep, s);
   };
-  // The A operand of a projection that follows an RMSNorm: normalised in the GEMM, or by a
-  // separate row kernel into h.
+  auto post_norm = [&](size_t gain_off, size_t out_off) {
+    PostNorm p;
+    p.gain = m->at(gain_off);
+    p.eps = c.rms_eps;
+    p.out = m->at(out_off);
+    p.ld_out = d;
+    return p;
+  };
+  // The A operand of a projection that follows an RMSNorm: normalised in the GEMM, already in
+  // h, or normalised by a separate row kernel into h.
   auto normed = [&](size_t gain_off, NormIn *nrm) -> ll_status {
     if (fuse_norm) {
       *nrm = NormIn{x, d, nullptr, m->at(gain_off), c.rms_eps};
+      return LL_OK;
+    }
+    if (h_ready) {
+      h_ready = false;
       return LL_OK;
     }
     m->mark(LL_K_RMSNORM);
@@ -354,15 +372,28 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
     if (fuse_merge)
       LL_HIP(launch_gemm_skinny(dt, nullptr, qd, nullptr, m->at(m->L.wo[l]), rows, d, qd,
                                 resid_epi(m), s, &mrg));
-    else
-      LL_HIP(gemm(m->at(m->L.o), qd, nullptr, m->at(m->L.wo[l]), d, qd, resid_epi(m)));
+    else {
+      const PostNorm pn = post_norm(m->L.mlp_norm[l], m->L.h);
+      LL_HIP(gemm(m->at(m->L.o), qd, nullptr, m->at(m->L.wo[l]), d, qd, resid_epi(m),
+                  fuse_norm ? nullptr : &pn, &h_ready));
+    }
     st = normed(m->L.mlp_norm[l], &nrm);
     if (st != LL_OK) return st;
     m->mark(LL_K_GATE_UP);
     LL_HIP(gemm(m->at(m->L.h), d, fuse_norm ? &nrm : nullptr, m->at(m->L.wgu[l]), 2 * F, d,
                 swiglu_epi(m)));
     m->mark(LL_K_DOWN);
-    LL_HIP(gemm(m->at(m->L.act), F, nullptr, m->at(m->L.wd[l]), d, F, resid_epi(m)));
+    const bool last = l + 1 == c.n_layers;
+    const PostNorm pn = last ? post_norm(m->L.final_norm, m->L.hf)
+                             : post_norm(m->L.attn_norm[l + 1], m->L.h);
+    bool done = false;
+    LL_HIP(gemm(m->at(m->L.act), F, nullptr, m->at(m->L.wd[l]), d, F, resid_epi(m),
+                fuse_norm ? nullptr : &pn, &done));
+    if (last) {
+      if (hf_ready) *hf_ready = done;
+    } else {
+      h_ready = done;
+    }
   }
   return LL_OK;
 }
@@ -370,13 +401,13 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
 // Final RMSNorm of one row per sequence, the LM head with per-block argmax partials, and the
 // reduction that writes `next` (and advances `lens_inc`).
 ll_status enqueue_head(ll_model *m, int batch, const int *rowmap, int *next, float *logits,
-                       int *lens_inc, hipStream_t s) {
+                       int *lens_inc, hipStream_t s, bool hf_ready = false) {
   const ll_config &c = m->cfg;
   EpiParams ep = argmax_epi(m, logits);
   NormIn nrm{m->at<float>(m->L.x), c.d_model, rowmap, m->at(m->L.final_norm), c.rms_eps};
   const bool fuse_norm = batch <= kFusedNormMaxRows &&
                          skinny_norm_lds(elem_bytes(c.dtype), batch, c.d_model) <= kSkinnyMaxNormLds;
-  if (!fuse_norm) {
+  if (!fuse_norm && !hf_ready) {
     m->mark(LL_K_RMSNORM);
     LL_HIP(launch_rmsnorm(c.dtype, m->at<float>(m->L.x), c.d_model, rowmap, batch, c.d_model,
                           m->at(m->L.final_norm), c.rms_eps, m->at(m->L.hf), c.d_model, s));
@@ -395,9 +426,10 @@ ll_status enqueue_decode(ll_model *m, const int32_t *in, int32_t *out, float *lo
   m->mark(LL_K_EMBED);
   LL_HIP(launch_embed(c.dtype, in, m->batch, m->at(m->L.embed), c.vocab, c.d_model,
                       m->at<float>(m->L.x), m->at<int>(m->L.err), s));
-  ll_status st = enqueue_layers(m, m->batch, true, 0, s);
+  bool hf_ready = false;
+  ll_status st = enqueue_layers(m, m->batch, true, 0, s, &hf_ready);
   if (st != LL_OK) return st;
-  return enqueue_head(m, m->batch, nullptr, out, logits, m->at<int>(m->L.lens), s);
+  return enqueue_head(m, m->batch, nullptr, out, logits, m->at<int>(m->L.lens), s, hf_ready);
 }
 
 ll_status check_ws(const void *p) {
