@@ -64,6 +64,10 @@ SIGNATURES = [
     ("ll_op_gemm_splitk", c_int32, [c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
                                     c_void_p, c_int32, c_void_p, c_size_t, c_void_p]),
     ("ll_op_gemm_splitk_scratch", c_size_t, [c_int32, c_int32, c_int32, c_int32]),
+    ("ll_op_gemm_prefill_splitk", c_int32, [c_int32, c_int32, c_int32, c_int32, c_void_p,
+                                            c_void_p, c_void_p, c_int32, c_void_p, c_size_t,
+                                            c_void_p]),
+    ("ll_op_gemm_prefill_splitk_scratch", c_size_t, [c_int32, c_int32, c_int32, c_int32]),
     ("ll_op_attn_prefill", c_int32, [c_int32, c_int32, POINTER(c_int32), c_int32, c_int32,
                                      c_int32, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
                                      c_void_p, c_size_t, c_void_p]),
@@ -302,6 +306,22 @@ def op_gemm_splitk(a, wt, n: int, c=None, accumulate: bool = False, stream=None)
     _check(lib.ll_op_gemm_splitk(_dt(a), m, n, k, a.data_ptr(), wt.data_ptr(), c.data_ptr(),
                                  1 if accumulate else 0, scratch.data_ptr(), nbytes,
                                  _stream_handle(stream)), "ll_op_gemm_splitk")
+    return c
+
+
+def op_gemm_prefill_splitk(a, wt, n: int, c=None, accumulate: bool = False, stream=None):
+    """Split-K prefill GEMM (short prompts); scratch is allocated here."""
+    import torch
+    m, k = a.shape
+    lib = load_library()
+    nbytes = lib.ll_op_gemm_prefill_splitk_scratch(_dt(a), m, n, k)
+    if c is None:
+        c = torch.empty(m, n, dtype=torch.float32, device="cuda")
+    scratch = torch.empty(max(nbytes, 1), dtype=torch.uint8, device="cuda")
+    _check(lib.ll_op_gemm_prefill_splitk(_dt(a), m, n, k, a.data_ptr(), wt.data_ptr(),
+                                         c.data_ptr(), 1 if accumulate else 0,
+                                         scratch.data_ptr(), nbytes, _stream_handle(stream)),
+           "ll_op_gemm_prefill_splitk")
     return c
 
 

@@ -10,6 +10,7 @@
 //    into MFMA B operands (non-temporal), A comes from L2; 8 waves split K, reduced in LDS.
 //  * Output columns come in units of 32 = two halves of 16 that land in the same lane, so the
 //    epilogues (RoPE pairs (i, i + hd/2), SwiGLU gate/up pairs) need no cross-lane traffic.
+#include <algorithm>
 #include <type_traits>
 
 #include "device_common.h"
@@ -121,6 +122,19 @@ template <typename T> struct EpiQkv {
   }
 };
 
+// fp32 partial sums of one K range of a split GEMM: plane blockIdx.z of [split][M][ld].
+struct EpiPart {
+  float *out;
+  int ld;
+  size_t plane;
+  static constexpr bool kArgmax = false, kPairs = false;
+  __device__ void operator()(int m, int u, int c, float v0, float v1) const {
+    float *p = out + blockIdx.z * plane + (size_t)m * ld + 32 * u + c;
+    p[0] = v0;
+    p[16] = v1;
+  }
+};
+
 struct EpiArgmax {
   float *logits;  // nullable
   int ld;
@@ -133,10 +147,12 @@ struct EpiArgmax {
 // ------------------------------------------------------------------------------------------
 // Prefill GEMM
 // ------------------------------------------------------------------------------------------
+// With a split of K over blockIdx.z, block z covers steps [z * ksteps, (z + 1) * ksteps) (two
+// k-tiles per step) and its epilogue writes the partial sums of that range (EpiPart).
 template <typename T, typename Epi>
 __global__ __launch_bounds__(256) void k_gemm_tiled(const T *__restrict__ A, int lda,
                                                     const uint8_t *__restrict__ Wt, int M,
-                                                    int K, Epi epi) {
+                                                    int K, int ksteps, Epi epi) {
   using F = typename Frag<T>::type;
   constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL;
   constexpr int BM = 128, BN = 128;
@@ -146,7 +162,8 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const T *__restrict__ A, int
   const int wm = wave >> 1, wn = wave & 1;
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
   const int kb_n = K / TK;
-  const int nsteps = kb_n / 2;
+  const int s0 = blockIdx.z * ksteps;
+  const int nsteps = min(ksteps, kb_n / 2 - s0);
   uint4 ra[4], rb[4];
   f32x4 acc[4][4];
 #pragma unroll
@@ -161,12 +178,12 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const T *__restrict__ A, int
       const int c = i * 256 + tid;
       const int row = c >> 3, kc = c & 7;  // 8 chunks of 16 bytes per row and step
       const int gm = m0 + row;
-      ra[i] = gm < M ? *reinterpret_cast<const uint4 *>(A + (size_t)gm * lda + step * 2 * TK +
-                                                        kc * EPL)
+      ra[i] = gm < M ? *reinterpret_cast<const uint4 *>(A + (size_t)gm * lda +
+                                                        (s0 + step) * 2 * TK + kc * EPL)
                      : make_uint4(0u, 0u, 0u, 0u);
       const int nbl = c >> 7, kbl = (c >> 6) & 1;
       rb[i] = *reinterpret_cast<const uint4 *>(
-          wblk + (((size_t)nbl * kb_n + step * 2 + kbl) * 64 + (c & 63)) * 16);
+          wblk + (((size_t)nbl * kb_n + (s0 + step) * 2 + kbl) * 64 + (c & 63)) * 16);
     }
   };
   auto sstore = [&](int buf) {
@@ -367,14 +384,12 @@ __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, in
 // the side.  The per-row factor 1/sqrt(mean(x^2) + eps) of RMSNorm does not depend on the
 // column, so it scales the finished dot products in the epilogue:
 //   (x * s * g) . w = s * ((x * g) . w).
-// kAMerge stages the decode-attention output merged from its split partials (log-sum-exp
-// weights, same order as the merge kernel), so the O projection needs no merge launch.
 // ------------------------------------------------------------------------------------------
-enum AMode : int { kAGlobal = 0, kAStaged = 1, kANorm = 2, kAMerge = 3 };
+enum AMode : int { kAGlobal = 0, kAStaged = 1, kANorm = 2 };
 
 template <typename T, int MT, int NB, int AM, typename Epi>
 __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, int lda,
-                                                     NormIn norm, MergeIn merge,
+                                                     NormIn norm,
                                                      const uint8_t *__restrict__ Wt, int M,
                                                      int m_base, int K, Epi epi) {
   using F = typename Frag<T>::type;
@@ -447,21 +462,6 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
       if (lane == 0) s_ss[sl][r] = part;
     }
     s_wpr = wpr;
-    __syncthreads();
-  } else if constexpr (AM == kAMerge) {
-    // Each staged element merges its head's split partials itself: every load is issued up
-    // front (the statistics are the same address across the head's lanes), so the merge
-    // costs one memory round trip and no block-wide steps.
-    const int hq = merge.n_heads, hd = merge.head_dim, nsp = merge.nsplit;
-    for (int e = threadIdx.x; e < nrows * K; e += 512) {
-      const int r = e / K, i = e % K;
-      const int h = i / hd, d = i % hd;
-      const int S = min(merge.lens[m_base + r] + merge.len_add, merge.max_ctx);
-      const int ns = (S + merge.kpb - 1) / merge.kpb;
-      const size_t q = ((size_t)(m_base + r) * hq + h) * nsp;
-      sA[(size_t)r * lds_ld + i] = from_f32<T>(merge_splits_direct<kMergeMaxSplits>(
-          merge.part_ml + q * 2, merge.part_o + q * hd + d, hd, ns));
-    }
     __syncthreads();
   } else if constexpr (AM == kAStaged) {
     const int cpr = K / EPL;  // 16-byte chunks per row
@@ -738,9 +738,13 @@ __global__ __launch_bounds__(1024) void k_splitk_resid_norm(const float *__restr
 // 128 x 128 kernel.
 constexpr int kBigGemmMinTiles = 192;
 
+template <typename Epi>
+__global__ __launch_bounds__(256) void k_splitk_reduce(const float *__restrict__ part, int nsplit,
+                                                       int M, int N, Epi epi);
+
 template <typename T, typename Epi>
 hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k, const Epi &epi,
-                     hipStream_t s) {
+                     hipStream_t s, float *ws = nullptr, size_t ws_bytes = 0) {
   const int big_tiles = ((m + 255) / 256) * (n / 256);
   const int half_tiles = ((m + 127) / 128) * (n / 256);
   // Fraction of the last round of 256 blocks that has work; the 128-row tiles are preferred
@@ -759,21 +763,37 @@ hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k
               k, epi);
     return hipGetLastError();
   }
+  const int steps = k / (2 * tile_k(sizeof(T) == 4 ? kF32 : kBF16));
+  const SplitKPlan sp = prefill_splitk_plan(sizeof(T), m, n, k);
+  if (sp.nsplit > 1 && ws && ws_bytes >= sp.ws_bytes) {
+    // Too few output tiles to fill the CUs: K is split over blockIdx.z, then the partial sums
+    // are added in split order and the epilogue runs on the totals.
+    LL_LAUNCH((k_gemm_tiled<T, EpiPart>), dim3(n / 128, (m + 127) / 128, sp.nsplit), dim3(256),
+              0, s, reinterpret_cast<const T *>(a), lda, reinterpret_cast<const uint8_t *>(wt),
+              m, k, sp.kts, EpiPart{ws, n, (size_t)m * n});
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (g_launch_timer) g_launch_timer->secondary();
+    const long items = Epi::kPairs ? (long)m * (n / 2) : (long)m * n;
+    LL_LAUNCH((k_splitk_reduce<Epi>), dim3((unsigned)((items + 255) / 256)), dim3(256), 0, s, ws,
+              sp.nsplit, m, n, epi);
+    return hipGetLastError();
+  }
   dim3 grid(n / 128, (m + 127) / 128);
   LL_LAUNCH((k_gemm_tiled<T, Epi>), grid, dim3(256), 0, s,
                      reinterpret_cast<const T *>(a), lda,
-                     reinterpret_cast<const uint8_t *>(wt), m, k, epi);
+                     reinterpret_cast<const uint8_t *>(wt), m, k, steps, epi);
   return hipGetLastError();
 }
 
 template <typename T, int MT, int NB, int AM, typename Epi>
-hipError_t launch_skinny_one(const T *ap, int lda, const NormIn &nz, const MergeIn &mg,
+hipError_t launch_skinny_one(const T *ap, int lda, const NormIn &nz,
                              const uint8_t *w, int m, int mb, int n, int k, const Epi &epi,
                              hipStream_t s) {
   const size_t lds = AM != kAGlobal ? skinny_norm_lds(sizeof(T), m - mb, k) : 0;
   if (lds > kSkinnyMaxNormLds) return hipErrorInvalidValue;
   LL_LAUNCH((k_gemm_skinny<T, MT, NB, AM, Epi>), dim3(n / (16 * NB)), dim3(512), lds, s, ap,
-            lda, nz, mg, w, m, mb, k, epi);
+            lda, nz, w, m, mb, k, epi);
   return hipGetLastError();
 }
 
@@ -814,29 +834,26 @@ hipError_t run_splitk(const void *a, int lda, const void *wt, int m, int n, int 
 }
 
 template <typename T, typename Epi>
-hipError_t run_skinny(const void *a, int lda, const NormIn *norm, const MergeIn *merge,
+hipError_t run_skinny(const void *a, int lda, const NormIn *norm,
                       const void *wt, int m, int n, int k, const Epi &epi, hipStream_t s) {
   const T *ap = reinterpret_cast<const T *>(a);
   const uint8_t *w = reinterpret_cast<const uint8_t *>(wt);
   const NormIn nz = norm ? *norm : NormIn{};
-  const MergeIn mg = merge ? *merge : MergeIn{};
   // Element-wise epilogues take 16-column blocks when 32-column ones would not fill the CUs.
   const bool single = !Epi::kPairs && n / 32 < 256;
   for (int mb = 0; mb < m; mb += 32) {
     const bool one = m - mb <= 16;
-    if ((norm || merge) && !one) return hipErrorInvalidValue;
+    if (norm && !one) return hipErrorInvalidValue;
     // up to 16 rows: A from LDS when the rows fit, else from global memory
     const int am = !one ? kAGlobal
                    : norm ? kANorm
-                   : merge ? kAMerge
                    : skinny_norm_lds(sizeof(T), m - mb, k) <= kSkinnyMaxNormLds ? kAStaged : kAGlobal;
     hipError_t e = hipErrorInvalidValue;
-#define LL_SKINNY(MT, NB, AM) e = launch_skinny_one<T, MT, NB, AM>(ap, lda, nz, mg, w, m, mb, n, k, epi, s)
+#define LL_SKINNY(MT, NB, AM) e = launch_skinny_one<T, MT, NB, AM>(ap, lda, nz, w, m, mb, n, k, epi, s)
 #define LL_SKINNY_NB(NB)                        \
   do {                                          \
     if (!one) LL_SKINNY(2, NB, kAGlobal);        \
     else if (am == kANorm) LL_SKINNY(1, NB, kANorm); \
-    else if (am == kAMerge) LL_SKINNY(1, NB, kAMerge); \
     else if (am == kAStaged) LL_SKINNY(1, NB, kAStaged); \
     else LL_SKINNY(1, NB, kAGlobal);             \
   } while (0)
@@ -853,7 +870,7 @@ hipError_t run_skinny(const void *a, int lda, const NormIn *norm, const MergeIn 
 }
 
 template <typename T, bool kTiled>
-hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm, const MergeIn *merge,
+hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm,
                         const void *wt, int m, int n, int k, const EpiParams &ep, hipStream_t s,
                         float *ws = nullptr, size_t ws_bytes = 0, const PostNorm *post = nullptr,
                         bool *post_done = nullptr) {
@@ -863,16 +880,16 @@ hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm, const MergeI
     using E = std::decay_t<decltype(epi)>;
     if constexpr (kTiled) {
       if constexpr (E::kArgmax) return hipErrorInvalidValue;
-      else return run_tiled<T>(a, lda, wt, m, n, k, epi, s);
+      else return run_tiled<T>(a, lda, wt, m, n, k, epi, s, ws, ws_bytes);
     } else {
       if constexpr (!E::kArgmax) {
-        if (plan.nsplit > 0 && !norm && !merge && ws && ws_bytes >= plan.ws_bytes) {
+        if (plan.nsplit > 0 && !norm && ws && ws_bytes >= plan.ws_bytes) {
           const bool fuse_post = post && std::is_same<E, EpiResid>::value && n % 4 == 0;
           if (fuse_post && post_done) *post_done = true;
           return run_splitk<T>(a, lda, wt, m, n, k, epi, plan, ws, s, fuse_post ? post : nullptr);
         }
       }
-      return run_skinny<T>(a, lda, norm, merge, wt, m, n, k, epi, s);
+      return run_skinny<T>(a, lda, norm, wt, m, n, k, epi, s);
     }
   };
   // Refuse, before any launch, pointer sets that a kernel would dereference as null.
@@ -885,12 +902,6 @@ hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm, const MergeI
                              !ep.rope_cos || !ep.rope_sin))
     return hipErrorInvalidValue;
   if (norm && (!norm->x || !norm->gain)) return hipErrorInvalidValue;
-  if (norm && merge) return hipErrorInvalidValue;
-  if (merge && (!merge->part_o || !merge->part_ml || !merge->lens || merge->kpb <= 0 ||
-                merge->nsplit <= 0 || merge->max_ctx > merge->kpb * merge->nsplit ||
-                merge->head_dim <= 0 || merge->n_heads * merge->head_dim != k ||
-                merge->nsplit > kMergeMaxSplits))
-    return hipErrorInvalidValue;
   switch (ep.kind) {
     case kEpiStore: return run(EpiStore{ep.out_f32, ep.ld_out});
     case kEpiResid: return run(EpiResid{ep.out_f32, ep.ld_out});
@@ -922,23 +933,43 @@ hipError_t launch_repack(int dtype, const RepackSrc &src, int n, int k, int perm
 }
 
 hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, int m, int n,
-                             int k, const EpiParams &ep, hipStream_t s) {
+                             int k, const EpiParams &ep, hipStream_t s, float *ws,
+                             size_t ws_bytes) {
   if (m <= 0) return hipSuccess;
-  return dtype == kF32 ? dispatch_epi<float, true>(a, lda, nullptr, nullptr, wt, m, n, k, ep, s)
-                       : dispatch_epi<bf16, true>(a, lda, nullptr, nullptr, wt, m, n, k, ep, s);
+  return dtype == kF32
+             ? dispatch_epi<float, true>(a, lda, nullptr, wt, m, n, k, ep, s, ws, ws_bytes)
+             : dispatch_epi<bf16, true>(a, lda, nullptr, wt, m, n, k, ep, s, ws, ws_bytes);
 }
 
 hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,
                               const void *wt, int m, int n, int k, const EpiParams &ep,
-                              hipStream_t s, const MergeIn *merge, float *ws, size_t ws_bytes,
+                              hipStream_t s, float *ws, size_t ws_bytes,
                               const PostNorm *post, bool *post_done) {
   if (post_done) *post_done = false;
   if (m <= 0) return hipSuccess;
   if (post && (!post->gain || !post->out)) return hipErrorInvalidValue;
-  return dtype == kF32 ? dispatch_epi<float, false>(a, lda, norm, merge, wt, m, n, k, ep, s, ws,
+  return dtype == kF32 ? dispatch_epi<float, false>(a, lda, norm, wt, m, n, k, ep, s, ws,
                                                     ws_bytes, post, post_done)
-                       : dispatch_epi<bf16, false>(a, lda, norm, merge, wt, m, n, k, ep, s, ws,
+                       : dispatch_epi<bf16, false>(a, lda, norm, wt, m, n, k, ep, s, ws,
                                                    ws_bytes, post, post_done);
+}
+
+SplitKPlan prefill_splitk_plan(size_t elem, int m, int n, int k) {
+  SplitKPlan p;
+  const int tk2 = 2 * (elem == 4 ? 16 : 32);  // contraction span of one step of the tiled GEMM
+  if (m <= 0 || n % 128 != 0 || k % tk2 != 0) return p;
+  const int tiles = ((m + 127) / 128) * (n / 128);
+  // Shapes that k_gemm_big takes, or that fill the CUs without a split, are not split.
+  if (tiles >= kPrefillSplitMinTiles || (n % 256 == 0 && ((m + 127) / 128) * (n / 256) >= 192))
+    return p;
+  const int steps = k / tk2;
+  const int s0 = std::min({kPrefillSplitMax, (kPrefillSplitBlocks + tiles - 1) / tiles, steps / 2});
+  if (s0 < 2) return p;
+  p.kts = (steps + s0 - 1) / s0;  // steps per split
+  p.nsplit = (steps + p.kts - 1) / p.kts;
+  if (p.nsplit < 2) return SplitKPlan{};
+  p.ws_bytes = (size_t)p.nsplit * m * n * sizeof(float);
+  return p;
 }
 
 SplitKPlan splitk_plan(size_t elem, int m, int n, int k) {

@@ -78,19 +78,14 @@ struct NormIn {
   float eps = 0.f;
 };
 
-// Split-K decode-attention partials merged inside the decode GEMM that consumes the attention
-// output (A = merged rows, computed exactly as the merge kernel computes them).
-constexpr int kMergeMaxSplits = 16;  // split partials merged inside the O projection
-struct MergeIn {
-  const float *part_o = nullptr;   // [batch][n_heads][nsplit][head_dim]
-  const float *part_ml = nullptr;  // [batch][n_heads][nsplit][2]
-  const int *lens = nullptr;
-  int len_add = 0, kpb = 0, nsplit = 0, n_heads = 0, head_dim = 0, max_ctx = 0;
-};
-
-// Prefill GEMM: LDS-tiled MFMA, 128 x 128 block tiles.  Requires N % 128 == 0, K % 64 == 0.
+// Prefill GEMM: MFMA with LDS-staged tiles (256 x 256 or 128 x 256 pipelined tiles when they
+// fill the CUs, else 128 x 128).  Requires N % 128 == 0, K % 64 == 0.  When the 128 x 128
+// tiles are too few to fill the CUs and `ws` holds prefill_splitk_plan(...).ws_bytes bytes,
+// K is split over blocks and a second kernel adds the fp32 partials in split order and runs
+// the epilogue (not for the argmax epilogue).
 hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, int m, int n,
-                             int k, const EpiParams &ep, hipStream_t s);
+                             int k, const EpiParams &ep, hipStream_t s, float *ws = nullptr,
+                             size_t ws_bytes = 0);
 // Decode GEMM: weights streamed once from HBM into MFMA operands, A read from L2.
 // Requires N % 32 == 0, K % 64 == 0; any M (rows handled 32 at a time).  With `norm` the A
 // operand is RMSNorm of fp32 rows computed in the kernel (`a` is then unused); that needs
@@ -113,8 +108,7 @@ struct PostNorm {
 };
 hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,
                               const void *wt, int m, int n, int k, const EpiParams &ep,
-                              hipStream_t s, const MergeIn *merge = nullptr,
-                              float *ws = nullptr, size_t ws_bytes = 0,
+                              hipStream_t s, float *ws = nullptr, size_t ws_bytes = 0,
                               const PostNorm *post = nullptr, bool *post_done = nullptr);
 constexpr int kSplitKMaxTiles = 24;  // k-tiles per split-K block (A slice of 48 KiB in LDS)
 struct SplitKPlan {
@@ -123,6 +117,11 @@ struct SplitKPlan {
   size_t ws_bytes = 0;
 };
 SplitKPlan splitk_plan(size_t elem, int m, int n, int k);
+// Split of the 128 x 128 prefill GEMM (kts = steps of two k-tiles per split).
+constexpr int kPrefillSplitMinTiles = 160;  // tiles from which the GEMM is not split
+constexpr int kPrefillSplitBlocks = 320;    // blocks the split aims for
+constexpr int kPrefillSplitMax = 8;
+SplitKPlan prefill_splitk_plan(size_t elem, int m, int n, int k);
 
 hipError_t launch_embed(int dtype, const int *tokens, int ntok, const void *table, int vocab,
                         int d, float *x, int *err_flags, hipStream_t s);

@@ -178,8 +178,19 @@ Layout make_layout(const ll_config &c) {
   {
     const int F = c.ffn_dim;
     const int shapes[4][2] = {{L.n_qkv, (int)d}, {(int)d, (int)qd}, {2 * F, (int)d}, {(int)d, F}};
-    for (const auto &nk : shapes)
+    // One region serves the decode split-K GEMMs (max_batch rows) and the split prefill GEMMs
+    // of short prompts (any row count up to max_prefill_tokens that the split plan takes).
+    for (const auto &nk : shapes) {
       L.splitk_bytes = std::max(L.splitk_bytes, splitk_plan(eb, c.max_batch, nk[0], nk[1]).ws_bytes);
+      const int mmax = std::min(c.max_prefill_tokens, 128 * kPrefillSplitMinTiles);
+      for (int mr = 1; mr <= mmax; mr = mr < 128 ? 128 : mr + 128) {
+        const int mm = std::min(mr, mmax);
+        L.splitk_bytes =
+            std::max(L.splitk_bytes, prefill_splitk_plan(eb, mm, nk[0], nk[1]).ws_bytes);
+      }
+      L.splitk_bytes =
+          std::max(L.splitk_bytes, prefill_splitk_plan(eb, mmax, nk[0], nk[1]).ws_bytes);
+    }
     L.splitk = take(L.splitk_bytes);
   }
   L.pval = take((size_t)c.max_batch * L.n_parts * 4);
@@ -280,10 +291,6 @@ EpiParams argmax_epi(const ll_model *m, float *logits) {
 // Decode batches up to this size normalise inside the decode GEMM (the fp32 rows are then
 // read by every column block, which stays cheap only for a few rows).
 constexpr int kFusedNormMaxRows = 16;
-// Small decode batches merge the split attention partials inside the O projection when every
-// block can afford to read all of them (each of its blocks reads the whole set from L2).
-constexpr size_t kFusedMergeMaxBytes = 128 * 1024;
-
 // The decoder layers for `rows` rows.  decode: one row per sequence at position len[b].
 // *hf_ready: the last layer's down projection also wrote the final RMSNorm rows into hf.
 ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipStream_t s,
@@ -295,23 +302,6 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
   const bool fuse_norm = decode && rows <= kFusedNormMaxRows &&
                          skinny_norm_lds(elem_bytes(dt), rows, d) <= kSkinnyMaxNormLds;
   const AttnDecodePlan &ap = m->L.attn;
-  const bool fuse_merge =
-      decode && ap.nsplit > 1 && rows <= kFusedNormMaxRows &&
-      skinny_norm_lds(elem_bytes(dt), rows, qd) <= kSkinnyMaxNormLds &&
-      ap.nsplit <= kMergeMaxSplits &&
-      (size_t)rows * qd * ap.nsplit * 4 <= kFusedMergeMaxBytes;
-  MergeIn mrg;
-  if (fuse_merge) {
-    mrg.part_o = m->at<float>(m->L.part_o);
-    mrg.part_ml = m->at<float>(m->L.part_ml);
-    mrg.lens = m->at<int>(m->L.lens);
-    mrg.len_add = 1;
-    mrg.kpb = ap.kpb;
-    mrg.nsplit = ap.nsplit;
-    mrg.n_heads = c.n_heads;
-    mrg.head_dim = c.head_dim;
-    mrg.max_ctx = c.max_ctx;
-  }
   float *x = m->at<float>(m->L.x);
   float *splitk_ws = m->L.splitk_bytes ? m->at<float>(m->L.splitk) : nullptr;
   // h_ready: the previous residual GEMM already wrote the next RMSNorm rows into h (split-K
@@ -319,9 +309,10 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
   bool h_ready = false;
   auto gemm = [&](const void *a, int lda, const NormIn *nrm, const void *wt, int n, int k,
                   const EpiParams &ep, const PostNorm *post = nullptr, bool *post_done = nullptr) {
-    return decode ? launch_gemm_skinny(dt, a, lda, nrm, wt, rows, n, k, ep, s, nullptr,
-                                       splitk_ws, m->L.splitk_bytes, post, post_done)
-                  : launch_gemm_tiled(dt, a, lda, wt, rows, n, k, ep, s);
+    return decode ? launch_gemm_skinny(dt, a, lda, nrm, wt, rows, n, k, ep, s, splitk_ws,
+                                       m->L.splitk_bytes, post, post_done)
+                  : launch_gemm_tiled(dt, a, lda, wt, rows, n, k, ep, s, splitk_ws,
+                                      m->L.splitk_bytes);
   };
   auto post_norm = [&](size_t gain_off, size_t out_off) {
     PostNorm p;
@@ -361,7 +352,7 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
       LL_HIP(launch_attn_decode(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
                                 m->at<int>(m->L.lens), 1, m->at(m->L.o), qd, rows, c.n_heads,
                                 c.n_kv_heads, c.max_ctx, ap, m->at<float>(m->L.part_o),
-                                m->at<float>(m->L.part_ml), s, fuse_merge));
+                                m->at<float>(m->L.part_ml), s));
     } else {
       LL_HIP(launch_attn_prefill(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
                                  m->at(m->L.o), qd, m->at<int>(m->L.cu),
@@ -369,10 +360,7 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
                                  c.max_ctx, s));
     }
     m->mark(LL_K_O);
-    if (fuse_merge)
-      LL_HIP(launch_gemm_skinny(dt, nullptr, qd, nullptr, m->at(m->L.wo[l]), rows, d, qd,
-                                resid_epi(m), s, &mrg));
-    else {
+    {
       const PostNorm pn = post_norm(m->L.mlp_norm[l], m->L.h);
       LL_HIP(gemm(m->at(m->L.o), qd, nullptr, m->at(m->L.wo[l]), d, qd, resid_epi(m),
                   fuse_norm ? nullptr : &pn, &h_ready));
@@ -753,6 +741,32 @@ ll_status ll_op_gemm(int32_t path, int32_t dtype, int32_t m, int32_t n, int32_t 
   return LL_OK;
 }
 
+size_t ll_op_gemm_prefill_splitk_scratch(int32_t dtype, int32_t m, int32_t n, int32_t k) {
+  if ((dtype != LL_F32 && dtype != LL_BF16) || m < 1 || n < 1 || k < 1 || k % 64) return 0;
+  return prefill_splitk_plan(elem_bytes(dtype), m, n, k).ws_bytes;
+}
+ll_status ll_op_gemm_prefill_splitk(int32_t dtype, int32_t m, int32_t n, int32_t k,
+                                    const void *a, const void *wt, float *c, int32_t accumulate,
+                                    void *scratch, size_t scratch_bytes, void *stream) {
+  g_err.clear();
+  ll_status st = check_dtype(dtype);
+  if (st != LL_OK) return st;
+  if (m < 1 || n < 1 || k < 1) return fail(LL_ERR_INVALID_ARGUMENT, "bad sizes");
+  const size_t need = ll_op_gemm_prefill_splitk_scratch(dtype, m, n, k);
+  if (!need)
+    return fail(LL_ERR_UNSUPPORTED, "n %% 128, k %% 64 and fewer than %d tiles of 128 x 128 "
+                "required", kPrefillSplitMinTiles);
+  if (!a || !wt || !c || !scratch) return fail(LL_ERR_INVALID_ARGUMENT, "NULL pointer");
+  if (scratch_bytes < need) return fail(LL_ERR_WORKSPACE, "scratch needs %zu bytes", need);
+  EpiParams ep;
+  ep.kind = accumulate ? kEpiResid : kEpiStore;
+  ep.out_f32 = c;
+  ep.ld_out = n;
+  LL_HIP(launch_gemm_tiled(dtype, a, k, wt, m, n, k, ep, (hipStream_t)stream,
+                           reinterpret_cast<float *>(scratch), scratch_bytes));
+  return LL_OK;
+}
+
 size_t ll_op_gemm_splitk_scratch(int32_t dtype, int32_t m, int32_t n, int32_t k) {
   if ((dtype != LL_F32 && dtype != LL_BF16) || m < 1 || n < 1 || k < 1 || k % 64) return 0;
   return splitk_plan(elem_bytes(dtype), m, n, k).ws_bytes;
@@ -773,7 +787,7 @@ ll_status ll_op_gemm_splitk(int32_t dtype, int32_t m, int32_t n, int32_t k, cons
   ep.kind = accumulate ? kEpiResid : kEpiStore;
   ep.out_f32 = c;
   ep.ld_out = n;
-  LL_HIP(launch_gemm_skinny(dtype, a, k, nullptr, wt, m, n, k, ep, (hipStream_t)stream, nullptr,
+  LL_HIP(launch_gemm_skinny(dtype, a, k, nullptr, wt, m, n, k, ep, (hipStream_t)stream,
                             reinterpret_cast<float *>(scratch), scratch_bytes));
   return LL_OK;
 }

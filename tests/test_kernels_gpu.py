@@ -106,6 +106,34 @@ def test_gemm_splitk(dtype, m, n, k):
     assert np.all(np.abs(_np(cacc) - (ref + c0)) <= bound + 2 * U * np.abs(ref + c0))
 
 
+# Short prompts: fewer 128 x 128 output tiles than CUs, so K is split over blocks (125m
+# shapes at 512 tokens, ragged row counts, a single row).
+PREFILL_SPLITK_SHAPES = [(512, 2304, 768), (512, 768, 2048), (300, 768, 768), (130, 4096, 768),
+                         (1, 256, 1024), (77, 1024, 4096)]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("m,n,k", PREFILL_SPLITK_SHAPES)
+def test_gemm_prefill_splitk(dtype, m, n, k):
+    from paper_2608_21836_amd.binding import load_library, op_gemm_prefill_splitk, op_repack
+    import torch
+    log(f"gemm prefill split-K {dtype} m={m} n={n} k={k}")
+    assert load_library().ll_op_gemm_prefill_splitk_scratch(1 if dtype == "bf16" else 0, m, n, k) > 0
+    rng = np.random.default_rng(m * 11 + n + k)
+    a = rounded(rng.standard_normal((m, k)), dtype)
+    w = rounded(rng.standard_normal((n, k)) * 0.05, dtype)
+    c0 = rng.standard_normal((m, n)).astype(np.float32)
+    A, W = device_tensor(a, dtype), device_tensor(w, dtype)
+    wt = op_repack(W)
+    c = op_gemm_prefill_splitk(A, wt, n)
+    cacc = op_gemm_prefill_splitk(A, wt, n, c=torch.from_numpy(c0).cuda(), accumulate=True)
+    torch.cuda.synchronize()
+    ref = a.astype(np.float64) @ w.astype(np.float64).T
+    bound = 4 * k * U * (np.abs(a).astype(np.float64) @ np.abs(w).astype(np.float64).T) + 1e-30
+    assert np.all(np.abs(_np(c) - ref) <= bound)
+    assert np.all(np.abs(_np(cacc) - (ref + c0)) <= bound + 2 * U * np.abs(ref + c0))
+
+
 def _caches(rng, dtype, batch, hkv, max_ctx, hd, lens):
     """Random caches with every position at or beyond a sequence's length set to NaN, so a
     read of a stale or out-of-range entry poisons the output."""
