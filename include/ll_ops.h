@@ -52,11 +52,11 @@ ll_status ll_op_gemm_splitk(int32_t dtype, int32_t m, int32_t n, int32_t k, cons
 /* Scratch bytes ll_op_gemm_splitk needs for this shape; 0 if the shape is not supported. */
 size_t ll_op_gemm_splitk_scratch(int32_t dtype, int32_t m, int32_t n, int32_t k);
 
-/* Prefill GEMM for prompts too short to fill the GPU with 128 x 128 output tiles, split over
+/* Prefill GEMM for prompts too short to fill the GPU with 64 x 128 output tiles, split over
  * K: each block covers a range of K, fp32 partial sums go to `scratch`, and a second kernel
  * adds them in split order and writes C = A W^T (accumulate = 0) or C += A W^T.  Same A / wt /
  * C layouts as ll_op_gemm.  Requires a shape that ll_op_gemm_prefill_splitk_scratch accepts
- * (non-zero: n a multiple of 128, k a multiple of 64, fewer than 160 tiles of 128 x 128) and
+ * (non-zero: n a multiple of 128, k a multiple of 64, fewer than 96 tiles of 64 x 128) and
  * scratch of at least that many bytes (LL_ERR_UNSUPPORTED / LL_ERR_WORKSPACE otherwise). */
 ll_status ll_op_gemm_prefill_splitk(int32_t dtype, int32_t m, int32_t n, int32_t k,
                                     const void *a, const void *wt, float *c, int32_t accumulate,

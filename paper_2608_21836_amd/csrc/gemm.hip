@@ -4,8 +4,9 @@
 //    stored in MFMA operand order, all tiles of a 16-row block contiguous along K.  A wave
 //    then fetches an operand with one fully coalesced 1 KiB read and LDS reads are
 //    conflict-free.
-//  * Prefill (M = prompt tokens): 128 x 128 block tiles, 4 waves of 64 x 64, double-buffered
-//    LDS, v_mfma_f32_16x16x32_bf16 (fp32 workloads: v_mfma_f32_16x16x4_f32).
+//  * Prefill (M = prompt tokens): 256 x 256, 128 x 256 or 64 x 128 block tiles streamed into
+//    LDS through a 4-stage ring, v_mfma_f32_16x16x32_bf16 (fp32 workloads:
+//    v_mfma_f32_16x16x4_f32); short prompts split K over blocks.
 //  * Decode (M = batch <= 32 per launch): every weight byte is read once straight from HBM
 //    into MFMA B operands (non-temporal), A comes from L2; 8 waves split K, reduced in LDS.
 //  * Output columns come in units of 32 = two halves of 16 that land in the same lane, so the
@@ -147,92 +148,6 @@ struct EpiArgmax {
 // ------------------------------------------------------------------------------------------
 // Prefill GEMM
 // ------------------------------------------------------------------------------------------
-// With a split of K over blockIdx.z, block z covers steps [z * ksteps, (z + 1) * ksteps) (two
-// k-tiles per step) and its epilogue writes the partial sums of that range (EpiPart).
-template <typename T, typename Epi>
-__global__ __launch_bounds__(256) void k_gemm_tiled(const T *__restrict__ A, int lda,
-                                                    const uint8_t *__restrict__ Wt, int M,
-                                                    int K, int ksteps, Epi epi) {
-  using F = typename Frag<T>::type;
-  constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL;
-  constexpr int BM = 128, BN = 128;
-  __shared__ uint4 sA[2][1024];  // [buf][(m-block * 2 + k-tile) * 64 + lane]
-  __shared__ uint4 sB[2][1024];  // [buf][(n-block * 2 + k-tile) * 64 + lane]
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const int kb_n = K / TK;
-  const int s0 = blockIdx.z * ksteps;
-  const int nsteps = min(ksteps, kb_n / 2 - s0);
-  uint4 ra[4], rb[4];
-  f32x4 acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const uint8_t *wblk = Wt + (size_t)(n0 / 16) * kb_n * 1024;
-  auto gload = [&](int step) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = i * 256 + tid;
-      const int row = c >> 3, kc = c & 7;  // 8 chunks of 16 bytes per row and step
-      const int gm = m0 + row;
-      ra[i] = gm < M ? *reinterpret_cast<const uint4 *>(A + (size_t)gm * lda +
-                                                        (s0 + step) * 2 * TK + kc * EPL)
-                     : make_uint4(0u, 0u, 0u, 0u);
-      const int nbl = c >> 7, kbl = (c >> 6) & 1;
-      rb[i] = *reinterpret_cast<const uint4 *>(
-          wblk + (((size_t)nbl * kb_n + (s0 + step) * 2 + kbl) * 64 + (c & 63)) * 16);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = i * 256 + tid;
-      const int row = c >> 3, kc = c & 7;
-      sA[buf][((row >> 4) * 2 + (kc >> 2)) * 64 + (row & 15) + 16 * (kc & 3)] = ra[i];
-      sB[buf][c] = rb[i];
-    }
-  };
-
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int step = 0; step < nsteps; ++step) {
-    const int cur = step & 1;
-    if (step + 1 < nsteps) gload(step + 1);
-#pragma unroll
-    for (int kbl = 0; kbl < 2; ++kbl) {
-      F a[4], b[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        a[i] = *reinterpret_cast<const F *>(&sA[cur][((wm * 4 + i) * 2 + kbl) * 64 + lane]);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        b[j] = *reinterpret_cast<const F *>(&sB[cur][((wn * 4 + j) * 2 + kbl) * 64 + lane]);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mma_chunk(a[i], b[j], acc[i][j]);
-    }
-    if (step + 1 < nsteps) sstore(cur ^ 1);
-    __syncthreads();
-  }
-
-  const int ubase = (n0 + wn * 64) >> 5;
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + r;
-      if (m < M) {
-#pragma unroll
-        for (int p = 0; p < 2; ++p) epi(m, ubase + p, lane & 15, acc[i][2 * p][r], acc[i][2 * p + 1][r]);
-      }
-    }
-}
-
 // ------------------------------------------------------------------------------------------
 // Large prefill GEMM: 256 x 256 block tiles, 8 waves of 128 x 64, one 1 KiB k-tile per step.
 // Operand tiles go straight from global memory into LDS (global_load_lds_dwordx4: each wave
@@ -260,21 +175,28 @@ __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-template <typename T, typename Epi, int BM>
-__global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, int lda,
-                                                     const uint8_t *__restrict__ Wt, int M,
-                                                     int N, int K, Epi epi) {
+// The same pipeline at BM x BN = 256 x 256, 128 x 256 or 64 x 128: 2 x (BN / 64) waves, each
+// owning BM / 2 rows and 64 columns.  With a split of K over blockIdx.z, block z covers
+// k-tiles [z * ksteps, (z + 1) * ksteps) (ksteps even) and its epilogue writes that range's
+// partial sums (EpiPart).
+template <typename T, typename Epi, int BM, int BN>
+__global__ __launch_bounds__(BN * 2, 1) void k_gemm_big(const T *__restrict__ A, int lda,
+                                                        const uint8_t *__restrict__ Wt, int M,
+                                                        int N, int K, int ksteps, Epi epi) {
   using F = typename Frag<T>::type;
   constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL;
-  constexpr int BN = 256, GM = 8;
+  constexpr int GM = 8;
+  constexpr int NW = BN / 32, WN = BN / 64;    // waves: 2 (M) x WN (N)
   constexpr int NA = BM / 16;                  // A tiles per stage (16-row blocks)
+  constexpr int NB = BN / 16;                  // W tiles per stage (16-column blocks)
   constexpr int NI = BM / 32;                  // 16-row blocks per wave
-  constexpr int S = 4, TPS = NA + 16, LPW = TPS / 8;  // stages, tiles per stage, loads per wave
-  static_assert(TPS % 8 == 0, "loads split evenly over the 8 waves");
-  __shared__ uint4 smem[S * TPS * 64];  // [stage][A: NA row tiles | W: 16 column tiles][64]
+  constexpr int S = 4, TPS = NA + NB, LPW = TPS / NW;  // stages, tiles per stage, loads per wave
+  static_assert(TPS % NW == 0, "loads split evenly over the waves");
+  static_assert(NI % 2 == 0, "each wave's row blocks split into two halves");
+  __shared__ uint4 smem[S * TPS * 64];  // [stage][A: NA row tiles | W: NB column tiles][64]
   const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // 8 waves, 2 (M) x 4 (N)
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave / WN, wn = wave % WN;
   const int ntm = (M + BM - 1) / BM, ntn = N / BN;
   // tile order: XCD-contiguous ranges, each walking groups of GM row-tiles across all columns
   const int t = xcd_remap(blockIdx.x, ntm * ntn);
@@ -282,7 +204,9 @@ __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, in
   const int gsize = min(ntm - first_m, GM);
   const int tm = first_m + (t % (GM * ntn)) % gsize, tn = (t % (GM * ntn)) / gsize;
   const int m0 = tm * BM, n0 = tn * BN;
-  const int nsteps = K / TK;
+  const int kt_all = K / TK;                   // k-tiles of one 16-row weight block
+  const int kt0 = blockIdx.z * ksteps;
+  const int nsteps = min(ksteps, kt_all - kt0);
 
   // Wave w fills stage tiles LPW w .. LPW w + LPW - 1: A tiles (16-row blocks) first, then
   // the 16 W tiles (16-column blocks).
@@ -292,9 +216,10 @@ __global__ __launch_bounds__(512, 1) void k_gemm_big(const T *__restrict__ A, in
     const int tt = wave * LPW + i;
     if (tt < NA) {
       const int row = min(m0 + tt * 16 + (lane & 15), M - 1);
-      src[i] = reinterpret_cast<const uint8_t *>(A + (size_t)row * lda + (lane >> 4) * EPL);
+      src[i] = reinterpret_cast<const uint8_t *>(A + (size_t)row * lda + (size_t)kt0 * TK +
+                                                 (lane >> 4) * EPL);
     } else {
-      src[i] = Wt + (((size_t)(n0 / 16 + tt - NA) * nsteps) * 64 + lane) * 16;
+      src[i] = Wt + (((size_t)(n0 / 16 + tt - NA) * kt_all + kt0) * 64 + lane) * 16;
     }
   }
   // Steps past the end reload the last tile (the data is never read), so that every step
@@ -735,7 +660,7 @@ __global__ __launch_bounds__(1024) void k_splitk_resid_norm(const float *__restr
 
 // The 256 x 256 kernel is used once it fills most of the 256 CUs with one block each, else
 // (or when its last round of blocks would be mostly empty) the 128 x 256 variant, else the
-// 128 x 128 kernel.
+// 64 x 128 variant.
 constexpr int kBigGemmMinTiles = 192;
 
 template <typename Epi>
@@ -751,26 +676,27 @@ hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k
   // when they fill the rounds clearly better (they run about 5-10 % below the big tiles).
   auto fill = [](int tiles) { return (double)tiles / (((tiles + 255) / 256) * 256); };
   const bool prefer_half = fill(half_tiles) * 0.9 > fill(big_tiles);
+  const int kt = k / tile_k(sizeof(T) == 4 ? kF32 : kBF16);  // k-tiles
+  const T *ap = reinterpret_cast<const T *>(a);
+  const uint8_t *wp = reinterpret_cast<const uint8_t *>(wt);
   if (n % 256 == 0 && big_tiles >= kBigGemmMinTiles && !prefer_half) {
-    LL_LAUNCH((k_gemm_big<T, Epi, 256>), dim3(big_tiles), dim3(512), 0, s,
-              reinterpret_cast<const T *>(a), lda, reinterpret_cast<const uint8_t *>(wt), m, n,
-              k, epi);
+    LL_LAUNCH((k_gemm_big<T, Epi, 256, 256>), dim3(big_tiles), dim3(512), 0, s, ap, lda, wp, m,
+              n, k, kt, epi);
     return hipGetLastError();
   }
   if (n % 256 == 0 && half_tiles >= kBigGemmMinTiles) {
-    LL_LAUNCH((k_gemm_big<T, Epi, 128>), dim3(half_tiles), dim3(512), 0, s,
-              reinterpret_cast<const T *>(a), lda, reinterpret_cast<const uint8_t *>(wt), m, n,
-              k, epi);
+    LL_LAUNCH((k_gemm_big<T, Epi, 128, 256>), dim3(half_tiles), dim3(512), 0, s, ap, lda, wp, m,
+              n, k, kt, epi);
     return hipGetLastError();
   }
-  const int steps = k / (2 * tile_k(sizeof(T) == 4 ? kF32 : kBF16));
+  // Short prompts: 64 x 128 tiles; when even those are too few to fill the CUs, K is split
+  // over blockIdx.z and a second kernel adds the partial sums in split order and runs the
+  // epilogue on the totals.
+  const int mid_tiles = ((m + 63) / 64) * (n / 128);
   const SplitKPlan sp = prefill_splitk_plan(sizeof(T), m, n, k);
   if (sp.nsplit > 1 && ws && ws_bytes >= sp.ws_bytes) {
-    // Too few output tiles to fill the CUs: K is split over blockIdx.z, then the partial sums
-    // are added in split order and the epilogue runs on the totals.
-    LL_LAUNCH((k_gemm_tiled<T, EpiPart>), dim3(n / 128, (m + 127) / 128, sp.nsplit), dim3(256),
-              0, s, reinterpret_cast<const T *>(a), lda, reinterpret_cast<const uint8_t *>(wt),
-              m, k, sp.kts, EpiPart{ws, n, (size_t)m * n});
+    LL_LAUNCH((k_gemm_big<T, EpiPart, 64, 128>), dim3(mid_tiles, 1, sp.nsplit), dim3(256), 0, s,
+              ap, lda, wp, m, n, k, sp.kts, EpiPart{ws, n, (size_t)m * n});
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (g_launch_timer) g_launch_timer->secondary();
@@ -779,10 +705,8 @@ hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k
               sp.nsplit, m, n, epi);
     return hipGetLastError();
   }
-  dim3 grid(n / 128, (m + 127) / 128);
-  LL_LAUNCH((k_gemm_tiled<T, Epi>), grid, dim3(256), 0, s,
-                     reinterpret_cast<const T *>(a), lda,
-                     reinterpret_cast<const uint8_t *>(wt), m, k, steps, epi);
+  LL_LAUNCH((k_gemm_big<T, Epi, 64, 128>), dim3(mid_tiles), dim3(256), 0, s, ap, lda, wp, m, n,
+            k, kt, epi);
   return hipGetLastError();
 }
 
@@ -956,17 +880,17 @@ hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *n
 
 SplitKPlan prefill_splitk_plan(size_t elem, int m, int n, int k) {
   SplitKPlan p;
-  const int tk2 = 2 * (elem == 4 ? 16 : 32);  // contraction span of one step of the tiled GEMM
-  if (m <= 0 || n % 128 != 0 || k % tk2 != 0) return p;
-  const int tiles = ((m + 127) / 128) * (n / 128);
-  // Shapes that k_gemm_big takes, or that fill the CUs without a split, are not split.
-  if (tiles >= kPrefillSplitMinTiles || (n % 256 == 0 && ((m + 127) / 128) * (n / 256) >= 192))
-    return p;
-  const int steps = k / tk2;
-  const int s0 = std::min({kPrefillSplitMax, (kPrefillSplitBlocks + tiles - 1) / tiles, steps / 2});
+  const int tk = elem == 4 ? 16 : 32;
+  if (m <= 0 || n % 128 != 0 || k % (2 * tk) != 0) return p;
+  // Shapes that the 256-column kernels take are not split.
+  if (n % 256 == 0 && ((m + 127) / 128) * (n / 256) >= kBigGemmMinTiles) return p;
+  const int tiles = ((m + 63) / 64) * (n / 128);
+  if (tiles >= kPrefillSplitMinTiles) return p;
+  const int kt = k / tk;
+  const int s0 = std::min({kPrefillSplitMax, (kPrefillSplitBlocks + tiles - 1) / tiles, kt / 4});
   if (s0 < 2) return p;
-  p.kts = (steps + s0 - 1) / s0;  // steps per split
-  p.nsplit = (steps + p.kts - 1) / p.kts;
+  p.kts = ((kt + s0 - 1) / s0 + 1) / 2 * 2;  // k-tiles per split, even
+  p.nsplit = (kt + p.kts - 1) / p.kts;
   if (p.nsplit < 2) return SplitKPlan{};
   p.ws_bytes = (size_t)p.nsplit * m * n * sizeof(float);
   return p;

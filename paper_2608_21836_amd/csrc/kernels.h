@@ -78,11 +78,11 @@ struct NormIn {
   float eps = 0.f;
 };
 
-// Prefill GEMM: MFMA with LDS-staged tiles (256 x 256 or 128 x 256 pipelined tiles when they
-// fill the CUs, else 128 x 128).  Requires N % 128 == 0, K % 64 == 0.  When the 128 x 128
-// tiles are too few to fill the CUs and `ws` holds prefill_splitk_plan(...).ws_bytes bytes,
-// K is split over blocks and a second kernel adds the fp32 partials in split order and runs
-// the epilogue (not for the argmax epilogue).
+// Prefill GEMM: MFMA on tiles streamed into LDS through a 4-stage ring (256 x 256 or
+// 128 x 256 tiles when they fill the CUs, else 64 x 128).  Requires N % 128 == 0, K % 64 == 0.
+// When the 64 x 128 tiles are too few to fill the CUs and `ws` holds
+// prefill_splitk_plan(...).ws_bytes bytes, K is split over blocks and a second kernel adds the
+// fp32 partials in split order and runs the epilogue (not for the argmax epilogue).
 hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, int m, int n,
                              int k, const EpiParams &ep, hipStream_t s, float *ws = nullptr,
                              size_t ws_bytes = 0);
@@ -117,9 +117,9 @@ struct SplitKPlan {
   size_t ws_bytes = 0;
 };
 SplitKPlan splitk_plan(size_t elem, int m, int n, int k);
-// Split of the 128 x 128 prefill GEMM (kts = steps of two k-tiles per split).
-constexpr int kPrefillSplitMinTiles = 160;  // tiles from which the GEMM is not split
-constexpr int kPrefillSplitBlocks = 320;    // blocks the split aims for
+// Split of the 64 x 128-tile prefill GEMM (kts = k-tiles per split, even).
+constexpr int kPrefillSplitMinTiles = 96;  // tiles from which the GEMM is not split
+constexpr int kPrefillSplitBlocks = 256;   // blocks the split aims for
 constexpr int kPrefillSplitMax = 8;
 SplitKPlan prefill_splitk_plan(size_t elem, int m, int n, int k);
 

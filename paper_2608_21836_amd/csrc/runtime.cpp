@@ -182,8 +182,8 @@ Layout make_layout(const ll_config &c) {
     // of short prompts (any row count up to max_prefill_tokens that the split plan takes).
     for (const auto &nk : shapes) {
       L.splitk_bytes = std::max(L.splitk_bytes, splitk_plan(eb, c.max_batch, nk[0], nk[1]).ws_bytes);
-      const int mmax = std::min(c.max_prefill_tokens, 128 * kPrefillSplitMinTiles);
-      for (int mr = 1; mr <= mmax; mr = mr < 128 ? 128 : mr + 128) {
+      const int mmax = std::min(c.max_prefill_tokens, 64 * kPrefillSplitMinTiles);
+      for (int mr = 64; mr < mmax + 64; mr += 64) {
         const int mm = std::min(mr, mmax);
         L.splitk_bytes =
             std::max(L.splitk_bytes, prefill_splitk_plan(eb, mm, nk[0], nk[1]).ws_bytes);
@@ -754,7 +754,7 @@ ll_status ll_op_gemm_prefill_splitk(int32_t dtype, int32_t m, int32_t n, int32_t
   if (m < 1 || n < 1 || k < 1) return fail(LL_ERR_INVALID_ARGUMENT, "bad sizes");
   const size_t need = ll_op_gemm_prefill_splitk_scratch(dtype, m, n, k);
   if (!need)
-    return fail(LL_ERR_UNSUPPORTED, "n %% 128, k %% 64 and fewer than %d tiles of 128 x 128 "
+    return fail(LL_ERR_UNSUPPORTED, "n %% 128, k %% 64 and fewer than %d tiles of 64 x 128 "
                 "required", kPrefillSplitMinTiles);
   if (!a || !wt || !c || !scratch) return fail(LL_ERR_INVALID_ARGUMENT, "NULL pointer");
   if (scratch_bytes < need) return fail(LL_ERR_WORKSPACE, "scratch needs %zu bytes", need);

@@ -50,7 +50,9 @@ def test_rmsnorm(dtype, rows, d):
 
 
 GEMM_SHAPES = [
+    # 64 x 128 tiles (short prompts), with M tails
     (0, 1, 256, 64), (0, 130, 384, 768), (0, 300, 128, 192), (0, 257, 256, 1408),
+    (0, 512, 2304, 768),
     # enough 256 x 256 tiles for the large-tile kernel, with ragged M tails
     (0, 2000, 6144, 256), (0, 3000, 4096, 1024), (0, 6144, 2048, 128),
     # 128 x 256 tiles (too few 256 x 256 tiles), exact and ragged M
@@ -106,9 +108,9 @@ def test_gemm_splitk(dtype, m, n, k):
     assert np.all(np.abs(_np(cacc) - (ref + c0)) <= bound + 2 * U * np.abs(ref + c0))
 
 
-# Short prompts: fewer 128 x 128 output tiles than CUs, so K is split over blocks (125m
-# shapes at 512 tokens, ragged row counts, a single row).
-PREFILL_SPLITK_SHAPES = [(512, 2304, 768), (512, 768, 2048), (300, 768, 768), (130, 4096, 768),
+# Short prompts: too few 64 x 128 output tiles to fill the CUs, so K is split over blocks
+# (125m O and down projections at 512 tokens, ragged row counts, a single row).
+PREFILL_SPLITK_SHAPES = [(512, 768, 2048), (512, 768, 768), (300, 768, 768), (200, 1280, 512),
                          (1, 256, 1024), (77, 1024, 4096)]
 
 
