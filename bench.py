@@ -292,15 +292,11 @@ def main() -> int:
                            "launches": dom["launches"], "avg_us": dom["avg_us"],
                            "work_per_launch": wv / dom["launches"],
                            "work_unit": unit}
-        # Eq. 1: s(m) = sum_p w_p t(m, p) / T(p); t and T per phase invocation, w_p = share of
-        # the job's time spent in phase p.
-        inv = {"prefill": 1, "decode": N}
-        phase_ms = {"prefill": pre_ms, "decode": dec_ms / N}
-        wp = {"prefill": pre_ms / (pre_ms + dec_ms), "decode": dec_ms / (pre_ms + dec_ms)}
-        score = {}
-        for (phase, cls), (cnt, ms) in kt.items():
-            score[cls] = score.get(cls, 0.0) + wp[phase] * (ms / inv[phase]) / phase_ms[phase]
-        out["hotspot_eq1"] = {k: round(v, 4) for k, v in sorted(score.items(), key=lambda kv: -kv[1])}
+        # Eq. 1: s(m) = sum_p w_p t(m, p) / T(p) over the kernel classes
+        from paper_2608_21836_amd.tuner import hotspot_scores
+        score = hotspot_scores({k: v[1] for k, v in kt.items()},
+                               {"prefill": pre_ms, "decode": dec_ms}, {"prefill": 1, "decode": N})
+        out["hotspot_eq1"] = {k: round(v, 4) for k, v in score.items()}
 
     if not args.no_cpu_baseline:
         print("[bench] oracle cpu baseline", file=sys.stderr, flush=True)

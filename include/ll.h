@@ -121,6 +121,32 @@ ll_status ll_seq_lengths(const ll_model *m, int32_t *out, int32_t cap, int32_t *
 /* Enable (1, default) or disable (0) HIP-graph replay of decode steps. */
 ll_status ll_set_decode_graph(ll_model *m, int32_t enable);
 
+/* Implementation variants of the hot path.  Each option chooses between kernels that compute
+ * the same function (results differ only in fp32 summation order); none changes the model.
+ * The paper admits such a variant into the deployed model only when the model's own measured
+ * latency drops by at least a margin delta (Sec. 3.3, Eq. 3) -- see the package's tuner.
+ * Changing an option drops the captured decode graphs (they are captured again on use). */
+typedef enum {
+  LL_OPT_DECODE_GRAPH = 0,     /* 1 (default): decode steps replay a HIP graph; 0: direct launches
+                                  (same as ll_set_decode_graph) */
+  LL_OPT_PREFILL_SPLITK = 1,   /* 1 (default): prefill GEMMs whose 64x128 tiles cannot fill the
+                                  GPU split K over blocks; 0: never split */
+  LL_OPT_DECODE_SPLITK = 2,    /* 1 (default): decode GEMMs above 16 rows split K over blocks of
+                                  128 columns; 0: whole-K blocks */
+  LL_OPT_PREFILL_TILE = 3,     /* 0 (default): prefill GEMM tile family chosen per shape; 1: 256x256,
+                                  2: 128x256, 3: 64x128 (256-column tiles only where the output
+                                  width is a multiple of 256; elsewhere the default) */
+  LL_OPT_ATTN_DECODE_CHUNK = 4,/* 0 (default): cached keys per decode-attention block from the
+                                  load-time plan; 64, 128 or 256 override it (not below the plan's
+                                  value: the workspace holds the plan's number of splits) */
+  LL_OPT_COUNT = 5
+} ll_option;
+
+/* Set / read an option.  LL_ERR_INVALID_ARGUMENT for an unknown option or value,
+ * LL_ERR_UNSUPPORTED for a decode-attention chunk below the load-time plan's. */
+ll_status ll_set_option(ll_model *m, int32_t option, int32_t value);
+ll_status ll_get_option(const ll_model *m, int32_t option, int32_t *value);
+
 /* Synchronise the model's stream and read the device error flags: bit 0 = a token id
  * outside [0, vocab) was seen (it was replaced by 0, never read out of bounds). */
 ll_status ll_device_flags(ll_model *m, int32_t *flags);

@@ -20,6 +20,9 @@ STATUS_NAMES = ["LL_OK", "LL_ERR_INVALID_ARGUMENT", "LL_ERR_UNSUPPORTED", "LL_ER
 LL_F32, LL_BF16 = 0, 1
 LL_MAX_BATCH = 256
 LL_K_COUNT = 11
+# ll_option ids (include/ll.h)
+OPTIONS = {"decode_graph": 0, "prefill_splitk": 1, "decode_splitk": 2, "prefill_tile": 3,
+           "attn_decode_chunk": 4}
 PHASES = ("prefill", "decode")
 
 
@@ -50,6 +53,8 @@ SIGNATURES = [
     ("ll_kv_reset", c_int32, [c_void_p]),
     ("ll_seq_lengths", c_int32, [c_void_p, POINTER(c_int32), c_int32, POINTER(c_int32)]),
     ("ll_set_decode_graph", c_int32, [c_void_p, c_int32]),
+    ("ll_set_option", c_int32, [c_void_p, c_int32, c_int32]),
+    ("ll_get_option", c_int32, [c_void_p, c_int32, POINTER(c_int32)]),
     ("ll_device_flags", c_int32, [c_void_p, POINTER(c_int32)]),
     ("ll_set_kernel_timing", c_int32, [c_void_p, c_int32]),
     ("ll_kernel_timing_read", c_int32, [c_void_p, POINTER(c_int32), POINTER(c_double)]),
@@ -209,6 +214,17 @@ class Model:
 
     def set_decode_graph(self, enable: bool) -> None:
         _check(self.lib.ll_set_decode_graph(self.handle, 1 if enable else 0), "ll_set_decode_graph")
+
+    def set_option(self, name: str, value: int) -> None:
+        _check(self.lib.ll_set_option(self.handle, OPTIONS[name], int(value)), "ll_set_option")
+
+    def get_option(self, name: str) -> int:
+        v = c_int32(0)
+        _check(self.lib.ll_get_option(self.handle, OPTIONS[name], ctypes.byref(v)), "ll_get_option")
+        return v.value
+
+    def options(self) -> Dict[str, int]:
+        return {k: self.get_option(k) for k in OPTIONS}
 
     def seq_lengths(self) -> List[int]:
         out = (c_int32 * LL_MAX_BATCH)()

@@ -669,22 +669,27 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float *__restrict__
 
 template <typename T, typename Epi>
 hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k, const Epi &epi,
-                     hipStream_t s, float *ws = nullptr, size_t ws_bytes = 0) {
+                     hipStream_t s, float *ws = nullptr, size_t ws_bytes = 0, int tile = 0) {
   const int big_tiles = ((m + 255) / 256) * (n / 256);
   const int half_tiles = ((m + 127) / 128) * (n / 256);
   // Fraction of the last round of 256 blocks that has work; the 128-row tiles are preferred
   // when they fill the rounds clearly better (they run about 5-10 % below the big tiles).
   auto fill = [](int tiles) { return (double)tiles / (((tiles + 255) / 256) * 256); };
-  const bool prefer_half = fill(half_tiles) * 0.9 > fill(big_tiles);
+  bool prefer_half = fill(half_tiles) * 0.9 > fill(big_tiles);
+  // A forced tile family (kTile256, kTile128x256, kTileMid) where the shape allows it.
+  if (n % 256 != 0 && tile != kTileMid) tile = kTileAuto;
+  if (tile == kTile256) prefer_half = false;
+  const int min_tiles = tile == kTileAuto ? kBigGemmMinTiles : 1;
+  if (tile == kTileMid) prefer_half = true;
   const int kt = k / tile_k(sizeof(T) == 4 ? kF32 : kBF16);  // k-tiles
   const T *ap = reinterpret_cast<const T *>(a);
   const uint8_t *wp = reinterpret_cast<const uint8_t *>(wt);
-  if (n % 256 == 0 && big_tiles >= kBigGemmMinTiles && !prefer_half) {
+  if (n % 256 == 0 && big_tiles >= min_tiles && !prefer_half && tile != kTile128x256) {
     LL_LAUNCH((k_gemm_big<T, Epi, 256, 256>), dim3(big_tiles), dim3(512), 0, s, ap, lda, wp, m,
               n, k, kt, epi);
     return hipGetLastError();
   }
-  if (n % 256 == 0 && half_tiles >= kBigGemmMinTiles) {
+  if (n % 256 == 0 && half_tiles >= min_tiles && tile != kTileMid) {
     LL_LAUNCH((k_gemm_big<T, Epi, 128, 256>), dim3(half_tiles), dim3(512), 0, s, ap, lda, wp, m,
               n, k, kt, epi);
     return hipGetLastError();
@@ -797,14 +802,14 @@ template <typename T, bool kTiled>
 hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm,
                         const void *wt, int m, int n, int k, const EpiParams &ep, hipStream_t s,
                         float *ws = nullptr, size_t ws_bytes = 0, const PostNorm *post = nullptr,
-                        bool *post_done = nullptr) {
+                        bool *post_done = nullptr, int tile = kTileAuto) {
   if (post_done) *post_done = false;
   const SplitKPlan plan = splitk_plan(elem_bytes(sizeof(T) == 4 ? kF32 : kBF16), m, n, k);
   auto run = [&](const auto &epi) {
     using E = std::decay_t<decltype(epi)>;
     if constexpr (kTiled) {
       if constexpr (E::kArgmax) return hipErrorInvalidValue;
-      else return run_tiled<T>(a, lda, wt, m, n, k, epi, s, ws, ws_bytes);
+      else return run_tiled<T>(a, lda, wt, m, n, k, epi, s, ws, ws_bytes, tile);
     } else {
       if constexpr (!E::kArgmax) {
         if (plan.nsplit > 0 && !norm && ws && ws_bytes >= plan.ws_bytes) {
@@ -858,11 +863,13 @@ hipError_t launch_repack(int dtype, const RepackSrc &src, int n, int k, int perm
 
 hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, int m, int n,
                              int k, const EpiParams &ep, hipStream_t s, float *ws,
-                             size_t ws_bytes) {
+                             size_t ws_bytes, int tile) {
   if (m <= 0) return hipSuccess;
-  return dtype == kF32
-             ? dispatch_epi<float, true>(a, lda, nullptr, wt, m, n, k, ep, s, ws, ws_bytes)
-             : dispatch_epi<bf16, true>(a, lda, nullptr, wt, m, n, k, ep, s, ws, ws_bytes);
+  if (tile < kTileAuto || tile > kTileMid) return hipErrorInvalidValue;
+  return dtype == kF32 ? dispatch_epi<float, true>(a, lda, nullptr, wt, m, n, k, ep, s, ws,
+                                                   ws_bytes, nullptr, nullptr, tile)
+                       : dispatch_epi<bf16, true>(a, lda, nullptr, wt, m, n, k, ep, s, ws,
+                                                  ws_bytes, nullptr, nullptr, tile);
 }
 
 hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,

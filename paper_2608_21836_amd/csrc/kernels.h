@@ -83,9 +83,11 @@ struct NormIn {
 // When the 64 x 128 tiles are too few to fill the CUs and `ws` holds
 // prefill_splitk_plan(...).ws_bytes bytes, K is split over blocks and a second kernel adds the
 // fp32 partials in split order and runs the epilogue (not for the argmax epilogue).
+// `tile` forces a tile family where the shape allows it (256-column tiles need N % 256 == 0).
+enum GemmTile : int { kTileAuto = 0, kTile256 = 1, kTile128x256 = 2, kTileMid = 3 };
 hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, int m, int n,
                              int k, const EpiParams &ep, hipStream_t s, float *ws = nullptr,
-                             size_t ws_bytes = 0);
+                             size_t ws_bytes = 0, int tile = kTileAuto);
 // Decode GEMM: weights streamed once from HBM into MFMA operands, A read from L2.
 // Requires N % 32 == 0, K % 64 == 0; any M (rows handled 32 at a time).  With `norm` the A
 // operand is RMSNorm of fp32 rows computed in the kernel (`a` is then unused); that needs

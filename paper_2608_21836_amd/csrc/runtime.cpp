@@ -217,6 +217,7 @@ struct ll_model {
   int batch = 0;
   std::vector<int> lens;
   bool use_graph = true;
+  int opt[LL_OPT_COUNT] = {1, 1, 1, 0, 0};  // ll_option values (LL_OPT_DECODE_GRAPH mirrors use_graph)
   struct Graph {
     const void *in;
     void *out;
@@ -238,6 +239,17 @@ struct ll_model {
   void drop_graphs() {
     for (auto &g : graphs) (void)hipGraphExecDestroy(g.exec);
     graphs.clear();
+  }
+  // Decode-attention plan: the load-time plan, or the keys-per-block override of
+  // LL_OPT_ATTN_DECODE_CHUNK (never more splits than the workspace holds).
+  AttnDecodePlan attn_plan() const {
+    AttnDecodePlan p = L.attn;
+    const int kpb = opt[LL_OPT_ATTN_DECODE_CHUNK];
+    if (kpb >= p.kpb) {
+      p.kpb = kpb;
+      p.nsplit = (cfg.max_ctx + kpb - 1) / kpb;
+    }
+    return p;
   }
 };
 
@@ -301,18 +313,21 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
   const int dt = c.dtype;
   const bool fuse_norm = decode && rows <= kFusedNormMaxRows &&
                          skinny_norm_lds(elem_bytes(dt), rows, d) <= kSkinnyMaxNormLds;
-  const AttnDecodePlan &ap = m->L.attn;
+  const AttnDecodePlan ap = m->attn_plan();
   float *x = m->at<float>(m->L.x);
   float *splitk_ws = m->L.splitk_bytes ? m->at<float>(m->L.splitk) : nullptr;
+  const bool use_split = decode ? m->opt[LL_OPT_DECODE_SPLITK] : m->opt[LL_OPT_PREFILL_SPLITK];
+  float *gemm_ws = use_split ? splitk_ws : nullptr;
+  const size_t gemm_ws_bytes = use_split ? m->L.splitk_bytes : 0;
   // h_ready: the previous residual GEMM already wrote the next RMSNorm rows into h (split-K
   // decode GEMMs fold the norm into their final reduction).
   bool h_ready = false;
   auto gemm = [&](const void *a, int lda, const NormIn *nrm, const void *wt, int n, int k,
                   const EpiParams &ep, const PostNorm *post = nullptr, bool *post_done = nullptr) {
-    return decode ? launch_gemm_skinny(dt, a, lda, nrm, wt, rows, n, k, ep, s, splitk_ws,
-                                       m->L.splitk_bytes, post, post_done)
-                  : launch_gemm_tiled(dt, a, lda, wt, rows, n, k, ep, s, splitk_ws,
-                                      m->L.splitk_bytes);
+    return decode ? launch_gemm_skinny(dt, a, lda, nrm, wt, rows, n, k, ep, s, gemm_ws,
+                                       gemm_ws_bytes, post, post_done)
+                  : launch_gemm_tiled(dt, a, lda, wt, rows, n, k, ep, s, gemm_ws, gemm_ws_bytes,
+                                      m->opt[LL_OPT_PREFILL_TILE]);
   };
   auto post_norm = [&](size_t gain_off, size_t out_off) {
     PostNorm p;
@@ -635,9 +650,42 @@ ll_status ll_seq_lengths(const ll_model *m, int32_t *out, int32_t cap, int32_t *
 }
 
 ll_status ll_set_decode_graph(ll_model *m, int32_t enable) {
+  return ll_set_option(m, LL_OPT_DECODE_GRAPH, enable != 0);
+}
+
+ll_status ll_set_option(ll_model *m, int32_t option, int32_t value) {
   g_err.clear();
   if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
-  m->use_graph = enable != 0;
+  switch (option) {
+    case LL_OPT_DECODE_GRAPH:
+    case LL_OPT_PREFILL_SPLITK:
+    case LL_OPT_DECODE_SPLITK:
+      if (value != 0 && value != 1) return fail(LL_ERR_INVALID_ARGUMENT, "option %d takes 0 or 1", option);
+      break;
+    case LL_OPT_PREFILL_TILE:
+      if (value < 0 || value > 3) return fail(LL_ERR_INVALID_ARGUMENT, "prefill tile 0..3");
+      break;
+    case LL_OPT_ATTN_DECODE_CHUNK:
+      if (value != 0 && value != 64 && value != 128 && value != 256)
+        return fail(LL_ERR_INVALID_ARGUMENT, "decode-attention chunk 0, 64, 128 or 256");
+      if (value != 0 && value < m->L.attn.kpb)
+        return fail(LL_ERR_UNSUPPORTED, "chunk %d below the load-time plan's %d (the workspace "
+                    "holds %d splits)", value, m->L.attn.kpb, m->L.attn.nsplit);
+      break;
+    default:
+      return fail(LL_ERR_INVALID_ARGUMENT, "unknown option %d", option);
+  }
+  if (m->opt[option] != value) m->drop_graphs();  // captured graphs bake the old choice in
+  m->opt[option] = value;
+  m->use_graph = m->opt[LL_OPT_DECODE_GRAPH] != 0;
+  return LL_OK;
+}
+
+ll_status ll_get_option(const ll_model *m, int32_t option, int32_t *value) {
+  g_err.clear();
+  if (!m || !value) return fail(LL_ERR_INVALID_ARGUMENT, "NULL argument");
+  if (option < 0 || option >= LL_OPT_COUNT) return fail(LL_ERR_INVALID_ARGUMENT, "unknown option %d", option);
+  *value = m->opt[option];
   return LL_OK;
 }
 

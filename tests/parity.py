@@ -68,8 +68,10 @@ def judge(name: str, dtype: str, ref_logits: np.ndarray, gpu_logits: np.ndarray,
                         float((row_err / row_range).max()), int(mism.sum()), unexplained, details)
 
 
-def run_gpu_teacher_forced(cfg, weights, lens, packed, ref_tokens, n_decode, use_graph=True):
-    """Prefill + n_decode teacher-forced steps through the C ABI.
+def run_gpu_teacher_forced(cfg, weights, lens, packed, ref_tokens, n_decode, use_graph=True,
+                           options=None):
+    """Prefill + n_decode teacher-forced steps through the C ABI, with the given ll_option
+    values (name -> value) set after loading.
 
     Returns (logits [n_decode + 1, B, V] fp32, tokens [n_decode + 1, B])."""
     import torch
@@ -80,6 +82,8 @@ def run_gpu_teacher_forced(cfg, weights, lens, packed, ref_tokens, n_decode, use
                   max_ctx=int(max(lens)) + n_decode)
     del dev_w
     model.set_decode_graph(use_graph)
+    for name, value in (options or {}).items():
+        model.set_option(name, value)
     toks = torch.from_numpy(np.asarray(packed, dtype=np.int32)).cuda()
     logits = torch.empty(B, cfg.vocab, dtype=torch.float32, device="cuda")
     nxt = torch.empty(B, dtype=torch.int32, device="cuda")

@@ -147,3 +147,10 @@ def test_op_argument_validation(lib):
     assert lib.ll_op_lmhead_argmax(1, 2, 100, 64, 1, 1, None, 1, 0x10000, 1 << 20, None) == \
         B.LL_ERR_UNSUPPORTED
     assert lib.ll_op_attn_decode_scratch(0, 8, 2, 64, 16) == 0
+
+
+def test_option_calls_reject_a_null_model(lib):
+    v = ctypes.c_int32(0)
+    assert lib.ll_set_option(None, 0, 1) == B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_get_option(None, 0, ctypes.byref(v)) == B.LL_ERR_INVALID_ARGUMENT
+    assert set(B.OPTIONS.values()) == set(range(len(B.OPTIONS)))
