@@ -165,6 +165,9 @@ def main() -> int:
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--no-graph", action="store_true",
                     help="launch decode kernels one by one instead of replaying a HIP graph")
+    ap.add_argument("--no-accepted-options", action="store_true",
+                    help="run the library defaults instead of the implementation options the "
+                         "tuner accepted for this workload (Eq. 3)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 256 MiB device copy kernel (reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters of a rocprofv3 --pmc run)")
@@ -188,6 +191,10 @@ def main() -> int:
     dev_w = {name: to_device(arr, cfg.dtype) for name, arr in gen.iter_weights_parallel(cfg, workers)}
     dev_w.update({k: to_device(v, cfg.dtype) for k, v in gen.gains(cfg).items()})
     model = Model(cfg, dev_w, max_batch=B, max_prefill_tokens=T, max_ctx=max(lens) + N)
+    from paper_2608_21836_amd.tuner import accepted_options
+    options = {} if args.no_accepted_options else accepted_options(cfg.name)
+    for name, value in options.items():
+        model.set_option(name, value)
     if args.no_graph:
         model.set_decode_graph(False)
     torch.cuda.synchronize()
@@ -243,7 +250,8 @@ def main() -> int:
         "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic (seeded weights and prompts)",
         "config": {"workload": cfg.name, "layers": cfg.n_layers, "d_model": cfg.d_model,
                    "heads": f"{cfg.n_heads}/{cfg.n_kv_heads}x{cfg.head_dim}", "ffn": cfg.ffn_dim,
-                   "vocab": cfg.vocab, "batch": B, "prompt_tokens": T, "decode_steps": N},
+                   "vocab": cfg.vocab, "batch": B, "prompt_tokens": T, "decode_steps": N,
+                   "options": model.options()},
         "prefill_ms": round(pre_ms, 4), "decode_ms_per_step": round(dec_ms / N, 5),
         "prefill_tok_s": round(T / (pre_ms / 1e3), 1),
         "decode_tok_s": round(B * N / (dec_ms / 1e3), 1),

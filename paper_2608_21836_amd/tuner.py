@@ -22,7 +22,11 @@ row, max |logit - reference| <= eps * (max - min of the reference row).  Latency
 workload as the bench runs it: KV reset, prefill of every prompt, free-running greedy decode
 steps, timed with stream events.
 
-  python -m paper_2608_21836_amd.tuner --config 125m [--delta 0.01]
+  python -m paper_2608_21836_amd.tuner --config 125m [--delta 0.01] [--write]
+
+With --write the accepted (non-default) option values of the workload are stored in
+accepted_options.json next to this module; bench.py applies them to that workload, as the
+paper deploys accepted patches.
 """
 from __future__ import annotations
 
@@ -35,6 +39,16 @@ from typing import Dict, List, Optional, Sequence, Tuple
 
 if __package__ in (None, ""):
     sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+
+ACCEPTED_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "accepted_options.json")
+
+
+def accepted_options(workload: str) -> Dict[str, int]:
+    """Option values the tuner accepted for `workload` ({} when none were)."""
+    if not os.path.exists(ACCEPTED_PATH):
+        return {}
+    with open(ACCEPTED_PATH) as f:
+        return {k: int(v) for k, v in json.load(f).get(workload, {}).get("options", {}).items()}
 
 # Variants: option name, candidate values (the first is the library default), kernel classes
 # whose time the option changes.
@@ -239,6 +253,10 @@ def main() -> int:
     ap.add_argument("--delta", type=float, default=0.01, help="Eq. 3 acceptance margin")
     ap.add_argument("--eps", type=float, default=2e-2, help="in-model logit tolerance")
     ap.add_argument("--reps", type=int, default=3)
+    ap.add_argument("--write", action="store_true",
+                    help="store the accepted option values in accepted_options.json")
+    ap.add_argument("--store", default=ACCEPTED_PATH,
+                    help="file --write merges into (default: accepted_options.json here)")
     args = ap.parse_args()
     import numpy as np
     import torch
@@ -255,13 +273,25 @@ def main() -> int:
     wl = Workload(list(lens), torch.from_numpy(np.asarray(packed, dtype=np.int32)).cuda(),
                   cfg.n_decode)
     reports = tune(model, wl, args.delta, args.eps, args.reps)
-    print(json.dumps({"workload": cfg.name, "delta": args.delta,
-                      "options": model.options(),
-                      "knobs": [{"option": r.option, "score": round(r.score, 4),
-                                 "baseline_ms": round(r.baseline_ms, 4), "chosen": r.chosen,
-                                 "accepted": r.accepted, "candidates": r.candidates}
-                                for r in reports]}))
+    result = {"workload": cfg.name, "delta": args.delta, "options": model.options(),
+              "knobs": [{"option": r.option, "score": round(r.score, 4),
+                         "baseline_ms": round(r.baseline_ms, 4), "chosen": r.chosen,
+                         "accepted": r.accepted, "candidates": r.candidates}
+                        for r in reports]}
+    print(json.dumps(result))
     model.close()
+    if args.write:
+        store = {}
+        if os.path.exists(args.store):
+            with open(args.store) as f:
+                store = json.load(f)
+        store[cfg.name] = {
+            "delta": args.delta,
+            "options": {r.option: r.chosen for r in reports if r.accepted},
+            "ell": {r.option: r.candidates[r.chosen]["ell"] for r in reports if r.accepted}}
+        with open(args.store, "w") as f:
+            json.dump(store, f, indent=1, sort_keys=True)
+            f.write("\n")
     return 0
 
 
