@@ -39,7 +39,7 @@ typedef enum {
   LL_ERR_INVALID_ARGUMENT = 1, /* null pointer, non-positive size, bad length */
   LL_ERR_UNSUPPORTED = 2,      /* shape the kernels do not cover (rejected at load) */
   LL_ERR_CAPACITY = 3,         /* batch, token or context limit of the config exceeded */
-  LL_ERR_STATE = 4,            /* prefill on a non-empty cache, decode before prefill */
+  LL_ERR_STATE = 4,            /* prefill batch != cached sequences, decode before prefill */
   LL_ERR_WORKSPACE = 5,        /* workspace missing, too small or misaligned */
   LL_ERR_HIP = 6               /* a HIP runtime call or kernel launch failed */
 } ll_status;
@@ -91,14 +91,19 @@ ll_status ll_workspace_size(const ll_config *cfg, size_t *bytes);
 ll_status ll_model_load(const ll_config *cfg, const ll_weights *w, void *workspace,
                         size_t workspace_bytes, void *hip_stream, ll_model **out);
 
-/* Prefill phase (q_len > 1 per sequence, empty cache).
+/* Prefill phase (a block of q_len >= 1 prompt tokens per sequence).
  * batch sequences with host lengths seq_lens_host[batch] (each >= 1); tokens_dev holds the
  * sum(seq_lens) token ids packed in sequence order (device, int32, each in [0, vocab)).
- * Writes next_tokens_dev[batch] (device) = argmax of the logits at each sequence's last
- * prompt position (lowest index on ties) and, if logits_dev is not NULL, the fp32 logits
- * [batch, vocab].  Afterwards sequence b has length seq_lens_host[b].
- * LL_ERR_STATE if the cache is not empty (call ll_kv_reset first); LL_ERR_CAPACITY if
- * batch > max_batch, sum(seq_lens) > max_prefill_tokens or a length > max_ctx. */
+ * On an empty cache this starts `batch` new sequences at position 0.  On a populated cache
+ * (after an earlier ll_prefill, possibly followed by decode steps) it is a further prompt
+ * chunk of the same `batch` sequences: sequence b's tokens enter at positions len[b] ..
+ * len[b] + seq_lens_host[b] - 1 and attend to everything cached before them (chunked
+ * prefill).  Writes next_tokens_dev[batch] (device) = argmax of the logits at each
+ * sequence's last new position (lowest index on ties) and, if logits_dev is not NULL, the
+ * fp32 logits [batch, vocab].  Afterwards len[b] grows by seq_lens_host[b].
+ * LL_ERR_STATE if the cache holds a different number of sequences (ll_kv_reset starts new
+ * ones); LL_ERR_CAPACITY if batch > max_batch, sum(seq_lens) > max_prefill_tokens or some
+ * len[b] + seq_lens_host[b] > max_ctx. */
 ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
                      const int32_t *tokens_dev, int32_t *next_tokens_dev, float *logits_dev);
 

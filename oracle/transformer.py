@@ -197,6 +197,15 @@ class OracleModel:
             out.append(self._run(b, toks, 0, all_logits))
         return out if all_logits else np.stack(out)
 
+    def extend(self, chunks: Sequence[np.ndarray]) -> np.ndarray:
+        """Prefill phase on a populated cache (a further prompt chunk of every sequence):
+        chunk b enters at positions len[b] .. len[b] + len(chunk) - 1, its keys and values are
+        appended after the cached ones, and each query attends to every cached position up
+        to its own.  Returns the logits at each chunk's last position ([B, V])."""
+        assert len(chunks) == len(self.lengths), "a chunk per sequence of the prefill batch"
+        return np.stack([self._run(b, np.asarray(c), self.lengths[b], False)
+                         for b, c in enumerate(chunks)])
+
     def decode(self, tokens: Sequence[int]) -> np.ndarray:
         """Decode phase: one token per sequence at position len[b]; returns [B, V] logits."""
         assert len(tokens) == len(self.lengths), "decode batch must match the prefill batch"

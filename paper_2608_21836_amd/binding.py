@@ -73,9 +73,9 @@ SIGNATURES = [
                                             c_void_p, c_void_p, c_int32, c_void_p, c_size_t,
                                             c_void_p]),
     ("ll_op_gemm_prefill_splitk_scratch", c_size_t, [c_int32, c_int32, c_int32, c_int32]),
-    ("ll_op_attn_prefill", c_int32, [c_int32, c_int32, POINTER(c_int32), c_int32, c_int32,
-                                     c_int32, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
-                                     c_void_p, c_size_t, c_void_p]),
+    ("ll_op_attn_prefill", c_int32, [c_int32, c_int32, POINTER(c_int32), POINTER(c_int32),
+                                     c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
+                                     c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     ("ll_op_attn_decode", c_int32, [c_int32, c_int32, c_int32, c_int32, c_int32, c_int32,
                                     c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                     c_size_t, c_void_p]),
@@ -342,15 +342,17 @@ def op_gemm_prefill_splitk(a, wt, n: int, c=None, accumulate: bool = False, stre
 
 
 def op_attn_prefill(seq_lens, q, kcache, vcache, n_heads, n_kv_heads, head_dim, max_ctx,
-                    stream=None):
+                    stream=None, cached=None):
+    """cached[b]: keys already in the cache before sequence b's queries (default 0)."""
     import torch
     b = len(seq_lens)
     lens = (c_int32 * b)(*[int(x) for x in seq_lens])
+    starts = (c_int32 * b)(*[int(x) for x in cached]) if cached is not None else None
     o = torch.empty_like(q)
-    nbytes = 1024 + 16 * (b + int(sum(seq_lens)))
+    nbytes = 2048 + 16 * (b + int(sum(seq_lens)))
     scratch = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
-    _check(load_library().ll_op_attn_prefill(_dt(q), b, lens, n_heads, n_kv_heads, head_dim,
-                                             max_ctx, q.data_ptr(), kcache.data_ptr(),
+    _check(load_library().ll_op_attn_prefill(_dt(q), b, lens, starts, n_heads, n_kv_heads,
+                                             head_dim, max_ctx, q.data_ptr(), kcache.data_ptr(),
                                              vcache.data_ptr(), o.data_ptr(), scratch.data_ptr(),
                                              nbytes, _stream_handle(stream)), "ll_op_attn_prefill")
     return o

@@ -26,8 +26,8 @@ namespace {
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void k_attn_prefill(
     const T *__restrict__ Q, int ldq, const T *__restrict__ Kc, const T *__restrict__ Vc,
-    T *__restrict__ O, int ldo, const int *__restrict__ cu, const int2 *__restrict__ qtiles,
-    int hq, int hkv, int max_ctx, float scale_log2) {
+    T *__restrict__ O, int ldo, const int *__restrict__ cu, const int *__restrict__ kstart,
+    const int2 *__restrict__ qtiles, int hq, int hkv, int max_ctx, float scale_log2) {
   using F = typename Frag<T>::type;
   constexpr int EPL = Frag<T>::EPL;
   constexpr int KT = 4 * EPL;       // head dims per Q K^T chunk
@@ -43,6 +43,8 @@ __global__ __launch_bounds__(256) void k_attn_prefill(
   const int2 qt = qtiles[blockIdx.x];
   const int b = qt.x, h = blockIdx.y, kvh = h / (hq / hkv);
   const int tok0 = cu[b], L = cu[b + 1] - tok0;
+  // queries sit at positions P0 + i after P0 cached keys; KL keys in all
+  const int P0 = kstart ? kstart[b] : 0, KL = P0 + L;
   const int q0 = qt.y * kAttnQTile;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int my_q = q0 + wave * 16 + (lane & 15);
@@ -60,7 +62,7 @@ __global__ __launch_bounds__(256) void k_attn_prefill(
   float m_run = -INFINITY, l_run = 0.f;
 
   const int q_last = min(q0 + kAttnQTile - 1, L - 1);
-  const int ntiles = q_last / BKV + 1;
+  const int ntiles = (P0 + q_last) / BKV + 1;
   const size_t kvbase = ((size_t)b * hkv + kvh) * max_ctx * HD;
   for (int kt = 0; kt < ntiles; ++kt) {
     __syncthreads();
@@ -68,7 +70,7 @@ __global__ __launch_bounds__(256) void k_attn_prefill(
       const int key = c / CPR, dc = c % CPR;
       const int gk = kt * BKV + key;
       F kv = fz, vv = fz;
-      if (gk < L) {
+      if (gk < KL) {
         kv = load_frag<F>(Kc + kvbase + (size_t)gk * HD + dc * EPL);
         vv = load_frag<F>(Vc + kvbase + (size_t)gk * HD + dc * EPL);
       }
@@ -96,7 +98,7 @@ __global__ __launch_bounds__(256) void k_attn_prefill(
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int key = kt * BKV + ks * 16 + (lane >> 4) * 4 + r;
-        const float v = (key <= my_q && key < L) ? s[ks][r] * scale_log2 : -INFINITY;
+        const float v = (key <= P0 + my_q && my_q < L) ? s[ks][r] * scale_log2 : -INFINITY;
         s[ks][r] = v;
         tmax = fmaxf(tmax, v);
       }
@@ -155,8 +157,8 @@ __global__ __launch_bounds__(256) void k_attn_prefill(
 template <int HD>
 __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
     const bf16 *__restrict__ Q, int ldq, const bf16 *__restrict__ Kc, const bf16 *__restrict__ Vc,
-    bf16 *__restrict__ O, int ldo, const int *__restrict__ cu, const int2 *__restrict__ qtiles,
-    int hq, int hkv, int max_ctx, float scale_log2) {
+    bf16 *__restrict__ O, int ldo, const int *__restrict__ cu, const int *__restrict__ kstart,
+    const int2 *__restrict__ qtiles, int hq, int hkv, int max_ctx, float scale_log2) {
   constexpr int QT = kAttnQTileWide, BKV = 64;
   constexpr int NKC = HD / 16;           // 16-dim steps of S^T
   constexpr int NDB = HD / 32;           // 32-dim output blocks
@@ -173,6 +175,8 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
   const int2 qt = qtiles[blockIdx.x];
   const int b = qt.x, h = blockIdx.y, kvh = h / (hq / hkv);
   const int tok0 = cu[b], L = cu[b + 1] - tok0;
+  // queries sit at positions P0 + i after P0 cached keys; KL keys in all
+  const int P0 = kstart ? kstart[b] : 0, KL = P0 + L;
   const int q0 = qt.y * QT;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -194,15 +198,15 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
     for (int i = 0; i < 16; ++i) acc[d][i] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  const int ntiles = (min(q0 + QT, L) - 1) / BKV + 1;
+  const int ntiles = (P0 + min(q0 + QT, L) - 1) / BKV + 1;
 
-  // K tile (kb, c): lane l reads key 32 kb + l % 32 (clamped into the sequence; rows past L
+  // K tile (kb, c): lane l reads key 32 kb + l % 32 (clamped into the sequence; rows past KL
   // are masked), dims 16 c + 8 g.
   auto k_issue = [&](int kt, int buf) {
     if (wave >= VW) {
       for (int ti = wave - VW; ti < KTILES; ti += KW) {
         const int kb = ti / NKC, c = ti % NKC;
-        const int key = min(kt * BKV + 32 * kb + (lane & 31), L - 1);
+        const int key = min(kt * BKV + 32 * kb + (lane & 31), KL - 1);
         load_tile_to_lds(Kc + kvbase + (size_t)key * HD + 16 * c + 8 * g,
                          &smem[buf * STAGE + ti * 64]);
       }
@@ -219,8 +223,8 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
         // rows past the sequence are read clamped (in bounds) and replaced by zeros: their
         // probabilities are 0, and the cache there may hold anything, NaN included
         const int key = kt * BKV + 16 * pc + (e < 4 ? 4 * gg + e : 8 + 4 * gg + e - 4);
-        const uint4 v = *reinterpret_cast<const uint4 *>(Vc + kvbase + (size_t)min(key, L - 1) * HD + 8 * dg);
-        vr[e] = key < L ? v : make_uint4(0, 0, 0, 0);
+        const uint4 v = *reinterpret_cast<const uint4 *>(Vc + kvbase + (size_t)min(key, KL - 1) * HD + 8 * dg);
+        vr[e] = key < KL ? v : make_uint4(0, 0, 0, 0);
       }
     }
   };
@@ -242,7 +246,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
     }
   };
   auto compute = [&](int kt, int buf) {
-    if (qw >= L || kt * BKV > qw + 31) return;  // nothing for this wave in this tile
+    if (qw >= L || kt * BKV > P0 + qw + 31) return;  // nothing for this wave in this tile
     const uint4 *st = &smem[buf * STAGE];
     f32x16 sc[2];
 #pragma unroll
@@ -254,13 +258,13 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
         sc[kb] = mma32(*reinterpret_cast<const bf16x8 *>(&st[(kb * NKC + c) * 64 + lane]), qf[c], sc[kb]);
     }
     // Causal / length mask, only on tiles that reach past the wave's first query.
-    if (kt * BKV + BKV - 1 > qw || qw + 31 >= L) {
+    if (kt * BKV + BKV - 1 > P0 + qw || qw + 31 >= L) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int key = kt * BKV + 32 * kb + 8 * (i / 4) + 4 * g + (i % 4);
-          sc[kb][i] = (q_ok & (key <= my_q)) ? sc[kb][i] : -INFINITY;
+          sc[kb][i] = (q_ok & (key <= P0 + my_q)) ? sc[kb][i] : -INFINITY;
         }
     }
     // Row maximum of the raw scores; scaling by a positive constant commutes with max.
@@ -524,19 +528,19 @@ __global__ __launch_bounds__(HD) void k_attn_combine_direct(const float *__restr
 
 template <typename T, int HD>
 hipError_t run_prefill(const void *q, int ldq, const void *kc, const void *vc, void *o, int ldo,
-                       const int *cu, const int2 *qtiles, int n_qtiles, int hq, int hkv,
-                       int max_ctx, hipStream_t s) {
+                       const int *cu, const int *kstart, const int2 *qtiles, int n_qtiles,
+                       int hq, int hkv, int max_ctx, hipStream_t s) {
   const float scale_log2 = kLog2e / sqrtf((float)HD);
   if constexpr (!std::is_same<T, float>::value) {
     LL_LAUNCH((k_attn_prefill_wide<HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
               reinterpret_cast<const bf16 *>(q), ldq, reinterpret_cast<const bf16 *>(kc),
-              reinterpret_cast<const bf16 *>(vc), reinterpret_cast<bf16 *>(o), ldo, cu, qtiles,
-              hq, hkv, max_ctx, scale_log2);
+              reinterpret_cast<const bf16 *>(vc), reinterpret_cast<bf16 *>(o), ldo, cu, kstart,
+              qtiles, hq, hkv, max_ctx, scale_log2);
   } else {
     LL_LAUNCH((k_attn_prefill<T, HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
               reinterpret_cast<const T *>(q), ldq, reinterpret_cast<const T *>(kc),
-              reinterpret_cast<const T *>(vc), reinterpret_cast<T *>(o), ldo, cu, qtiles, hq,
-              hkv, max_ctx, scale_log2);
+              reinterpret_cast<const T *>(vc), reinterpret_cast<T *>(o), ldo, cu, kstart, qtiles,
+              hq, hkv, max_ctx, scale_log2);
   }
   return hipGetLastError();
 }
@@ -595,16 +599,20 @@ hipError_t run_decode(int group, const void *q, int ldq, const void *kc, const v
 
 hipError_t launch_attn_prefill(int dtype, int head_dim, const void *q, int ldq, const void *kc,
                                const void *vc, void *o, int ldo, const int *cu,
-                               const int2 *qtiles, int n_qtiles, int hq, int hkv, int max_ctx,
-                               hipStream_t s) {
+                               const int *kstart, const int2 *qtiles, int n_qtiles, int hq,
+                               int hkv, int max_ctx, hipStream_t s) {
   if (n_qtiles <= 0) return hipSuccess;
+#define LL_PREFILL(TT, HD)                                                                   \
+  return run_prefill<TT, HD>(q, ldq, kc, vc, o, ldo, cu, kstart, qtiles, n_qtiles, hq, hkv, \
+                             max_ctx, s)
   if (dtype == kF32) {
-    if (head_dim == 64) return run_prefill<float, 64>(q, ldq, kc, vc, o, ldo, cu, qtiles, n_qtiles, hq, hkv, max_ctx, s);
-    if (head_dim == 128) return run_prefill<float, 128>(q, ldq, kc, vc, o, ldo, cu, qtiles, n_qtiles, hq, hkv, max_ctx, s);
+    if (head_dim == 64) LL_PREFILL(float, 64);
+    if (head_dim == 128) LL_PREFILL(float, 128);
   } else {
-    if (head_dim == 64) return run_prefill<bf16, 64>(q, ldq, kc, vc, o, ldo, cu, qtiles, n_qtiles, hq, hkv, max_ctx, s);
-    if (head_dim == 128) return run_prefill<bf16, 128>(q, ldq, kc, vc, o, ldo, cu, qtiles, n_qtiles, hq, hkv, max_ctx, s);
+    if (head_dim == 64) LL_PREFILL(bf16, 64);
+    if (head_dim == 128) LL_PREFILL(bf16, 128);
   }
+#undef LL_PREFILL
   return hipErrorInvalidValue;
 }
 

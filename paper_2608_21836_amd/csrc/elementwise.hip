@@ -93,29 +93,34 @@ __global__ __launch_bounds__(256) void k_argmax_reduce(const float *__restrict__
 
 __global__ __launch_bounds__(256) void k_prefill_meta(PrefillMeta pm, int total, int qtile, int *cu,
                                                       int *row_seq, int *row_pos, int *last_row,
-                                                      int *lens_dev, int2 *qtiles) {
+                                                      int *lens_dev, int *kstart, int2 *qtiles) {
   const int m = blockIdx.x * blockDim.x + threadIdx.x;
   if (m < total) {
-    int b = 0, start = 0;
-    while (b < pm.batch - 1 && m >= start + pm.lens[b]) start += pm.lens[b++];
+    int b = 0, first = 0;
+    while (b < pm.batch - 1 && m >= first + pm.lens[b]) first += pm.lens[b++];
     row_seq[m] = b;
-    row_pos[m] = m - start;
+    row_pos[m] = pm.start[b] + m - first;
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
-    int acc = 0, maxt = 0;
+    int acc = 0, maxk = 0;
     for (int b = 0; b < pm.batch; ++b) {
       cu[b] = acc;
       acc += pm.lens[b];
       last_row[b] = acc - 1;
-      lens_dev[b] = pm.lens[b];
-      maxt = max(maxt, (pm.lens[b] + qtile - 1) / qtile);
+      lens_dev[b] = pm.start[b] + pm.lens[b];
+      if (kstart) kstart[b] = pm.start[b];
+      maxk = max(maxk, pm.start[b] / qtile + (pm.lens[b] + qtile - 1) / qtile);
     }
     cu[pm.batch] = acc;
-    // Longest causal work first: tile t of any sequence attends to (t + 1) * qtile keys.
+    // Longest causal work first: query tile t of sequence b attends to about
+    // start[b] + (t + 1) * qtile keys, i.e. kk = start[b] / qtile + t key tiles of its size;
+    // each (b, t) appears once, at kk = start[b] / qtile + t.
     int n = 0;
-    for (int t = maxt - 1; t >= 0; --t)
-      for (int b = 0; b < pm.batch; ++b)
-        if (t * qtile < pm.lens[b]) qtiles[n++] = make_int2(b, t);
+    for (int kk = maxk - 1; kk >= 0; --kk)
+      for (int b = 0; b < pm.batch; ++b) {
+        const int t = kk - pm.start[b] / qtile;
+        if (t >= 0 && t * qtile < pm.lens[b]) qtiles[n++] = make_int2(b, t);
+      }
   }
 }
 
@@ -157,11 +162,11 @@ hipError_t launch_argmax_reduce(const float *pval, const int *pidx, int rows, in
 
 hipError_t launch_prefill_meta(const PrefillMeta &pm, int total, int qtile, int *cu,
                                int *row_seq, int *row_pos, int *last_row, int *lens_dev,
-                               int2 *qtiles, hipStream_t s) {
-  if (qtile <= 0) return hipErrorInvalidValue;
+                               int *kstart, int2 *qtiles, hipStream_t s) {
+  if (qtile <= 0 || pm.batch < 1 || pm.batch > 256) return hipErrorInvalidValue;
   const int blocks = std::max(1, (total + 255) / 256);
   LL_LAUNCH(k_prefill_meta, dim3(blocks), dim3(256), 0, s, pm, total, qtile, cu, row_seq,
-                     row_pos, last_row, lens_dev, qtiles);
+                     row_pos, last_row, lens_dev, kstart, qtiles);
   return hipGetLastError();
 }
 

@@ -134,24 +134,32 @@ hipError_t launch_rmsnorm(int dtype, const float *x, int ldx, const int *rowmap,
 hipError_t launch_argmax_reduce(const float *part_val, const int *part_idx, int rows,
                                 int n_parts, int *next, int *lens_inc, hipStream_t s);
 
-// Prefill metadata from host lengths (passed by value): cu_seqlens[B+1], row_seq[T],
-// row_pos[T], last_row[B], lens[B] and the query-tile list ordered by decreasing causal work.
+// Prefill metadata from host lengths (passed by value).  Sequence b contributes lens[b] new
+// tokens at positions start[b] .. start[b] + lens[b] - 1 (start[b] = tokens already cached;
+// 0 for a prefill on an empty cache).  Writes cu_seqlens[B+1] (packed query offsets),
+// row_seq[T], row_pos[T], last_row[B], lens_dev[B] = start + lens, kstart[B] = start
+// (nullable) and the query-tile list ordered by decreasing causal work.
 struct PrefillMeta {
   int batch;
   int lens[256];
+  int start[256];
 };
 hipError_t launch_prefill_meta(const PrefillMeta &pm, int total, int qtile, int *cu_seqlens,
                                int *row_seq, int *row_pos, int *last_row, int *lens_dev,
-                               int2 *qtiles, hipStream_t s);
+                               int *kstart, int2 *qtiles, hipStream_t s);
 constexpr int kAttnQTile = 64;       // queries per block, fp32 prefill attention
 constexpr int kAttnQTileWide = 128;  // queries per block, bf16 prefill attention
 // Query-tile size the prefill attention kernel for (dtype, head_dim) expects in `qtiles`.
 inline int attn_prefill_qtile(int dtype) { return dtype == kF32 ? kAttnQTile : kAttnQTileWide; }
 
+// Causal prefill attention of the packed queries over each sequence's cache: query i of
+// sequence b sits at position kstart[b] + i and attends to cached keys 0 .. kstart[b] + i
+// (kstart nullable: every sequence starts at 0).
 hipError_t launch_attn_prefill(int dtype, int head_dim, const void *q, int ldq,
                                const void *kcache, const void *vcache, void *o, int ldo,
-                               const int *cu_seqlens, const int2 *qtiles, int n_qtiles,
-                               int n_heads, int n_kv_heads, int max_ctx, hipStream_t s);
+                               const int *cu_seqlens, const int *kstart, const int2 *qtiles,
+                               int n_qtiles, int n_heads, int n_kv_heads, int max_ctx,
+                               hipStream_t s);
 
 // Decode attention: split over the cache length (chunk keys per block), then a merge kernel.
 // Keys attended per sequence: lens[b] + len_add (clamped to max_ctx).

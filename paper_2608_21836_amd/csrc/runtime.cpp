@@ -94,6 +94,7 @@ struct Layout {
   size_t x = 0, h = 0, q = 0, o = 0, act = 0, hf = 0;
   size_t part_o = 0, part_ml = 0, pval = 0, pidx = 0;
   size_t splitk = 0, splitk_bytes = 0;  // fp32 split-K partials of the decode GEMMs
+  size_t kstart = 0;                     // cached keys before each sequence's prefill chunk
   size_t cu = 0, row_seq = 0, row_pos = 0, last_row = 0, lens = 0, qtiles = 0, err = 0;
   size_t total = 0;
   size_t kv_layer_elems = 0;
@@ -200,6 +201,7 @@ Layout make_layout(const ll_config &c) {
   L.row_pos = take(R * 4);
   L.last_row = take(c.max_batch * 4);
   L.lens = take(c.max_batch * 4);
+  L.kstart = take(c.max_batch * 4);
   L.qtiles = take((R / kAttnQTile + c.max_batch + 1) * 8);
   L.err = take(4);
   L.total = off;
@@ -371,8 +373,8 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
     } else {
       LL_HIP(launch_attn_prefill(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
                                  m->at(m->L.o), qd, m->at<int>(m->L.cu),
-                                 m->at<int2>(m->L.qtiles), n_qtiles, c.n_heads, c.n_kv_heads,
-                                 c.max_ctx, s));
+                                 m->at<int>(m->L.kstart), m->at<int2>(m->L.qtiles), n_qtiles,
+                                 c.n_heads, c.n_kv_heads, c.max_ctx, s));
     }
     m->mark(LL_K_O);
     {
@@ -550,7 +552,11 @@ ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
   if (batch < 1) return fail(LL_ERR_INVALID_ARGUMENT, "batch %d < 1", batch);
   const ll_config &c = m->cfg;
   if (batch > c.max_batch) return fail(LL_ERR_CAPACITY, "batch %d > max_batch %d", batch, c.max_batch);
-  if (m->batch != 0) return fail(LL_ERR_STATE, "prefill on a non-empty cache (call ll_kv_reset)");
+  // A prefill on a populated cache (chunked prefill) extends the same sequences.
+  const bool chunk = m->batch != 0;
+  if (chunk && batch != m->batch)
+    return fail(LL_ERR_STATE, "prefill of %d sequences on a cache holding %d (a further prefill "
+                "chunk extends the same sequences; ll_kv_reset starts new ones)", batch, m->batch);
   long total = 0;
   int n_qtiles = 0;
   const int qtile = attn_prefill_qtile(c.dtype);
@@ -558,11 +564,15 @@ ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
   pm.batch = batch;
   for (int b = 0; b < batch; ++b) {
     const int L = seq_lens_host[b];
+    const int P0 = chunk ? m->lens[b] : 0;
     if (L < 1) return fail(LL_ERR_INVALID_ARGUMENT, "seq_lens[%d] = %d < 1", b, L);
-    if (L > c.max_ctx) return fail(LL_ERR_CAPACITY, "seq_lens[%d] = %d > max_ctx %d", b, L, c.max_ctx);
+    if ((long)P0 + L > c.max_ctx)
+      return fail(LL_ERR_CAPACITY, "sequence %d: %d cached + %d new tokens > max_ctx %d", b, P0,
+                  L, c.max_ctx);
     total += L;
     n_qtiles += (L + qtile - 1) / qtile;
     pm.lens[b] = L;
+    pm.start[b] = P0;
   }
   if (total > c.max_prefill_tokens)
     return fail(LL_ERR_CAPACITY, "%ld prompt tokens > max_prefill_tokens %d", total, c.max_prefill_tokens);
@@ -573,7 +583,7 @@ ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
   m->mark(LL_K_META);
   LL_HIP(launch_prefill_meta(pm, T, qtile, m->at<int>(L.cu), m->at<int>(L.row_seq),
                              m->at<int>(L.row_pos), m->at<int>(L.last_row), m->at<int>(L.lens),
-                             m->at<int2>(L.qtiles), s));
+                             m->at<int>(L.kstart), m->at<int2>(L.qtiles), s));
   m->mark(LL_K_EMBED);
   LL_HIP(launch_embed(c.dtype, tokens_dev, T, m->at(L.embed), c.vocab, c.d_model,
                       m->at<float>(L.x), m->at<int>(L.err), s));
@@ -581,8 +591,12 @@ ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
   if (st != LL_OK) return st;
   st = enqueue_head(m, batch, m->at<int>(L.last_row), next_tokens_dev, logits_dev, nullptr, s);
   if (st != LL_OK) return st;
-  m->batch = batch;
-  m->lens.assign(seq_lens_host, seq_lens_host + batch);
+  if (chunk) {
+    for (int b = 0; b < batch; ++b) m->lens[b] += seq_lens_host[b];
+  } else {
+    m->batch = batch;
+    m->lens.assign(seq_lens_host, seq_lens_host + batch);
+  }
   return LL_OK;
 }
 
@@ -850,10 +864,10 @@ static ll_status check_heads(int32_t n_heads, int32_t n_kv_heads, int32_t head_d
 }
 
 ll_status ll_op_attn_prefill(int32_t dtype, int32_t batch, const int32_t *seq_lens_host,
-                             int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
-                             int32_t max_ctx, const void *q, const void *kcache,
-                             const void *vcache, void *o, void *scratch, size_t scratch_bytes,
-                             void *stream) {
+                             const int32_t *cached_host, int32_t n_heads, int32_t n_kv_heads,
+                             int32_t head_dim, int32_t max_ctx, const void *q,
+                             const void *kcache, const void *vcache, void *o, void *scratch,
+                             size_t scratch_bytes, void *stream) {
   g_err.clear();
   ll_status st = check_dtype(dtype);
   if (st == LL_OK) st = check_heads(n_heads, n_kv_heads, head_dim);
@@ -867,9 +881,12 @@ ll_status ll_op_attn_prefill(int32_t dtype, int32_t batch, const int32_t *seq_le
   int n_qtiles = 0;
   const int qtile = attn_prefill_qtile(dtype);
   for (int b = 0; b < batch; ++b) {
-    const int L = seq_lens_host[b];
-    if (L < 1 || L > max_ctx) return fail(LL_ERR_INVALID_ARGUMENT, "seq_lens[%d] = %d outside [1, max_ctx]", b, L);
+    const int L = seq_lens_host[b], P0 = cached_host ? cached_host[b] : 0;
+    if (L < 1 || P0 < 0 || (long)P0 + L > max_ctx)
+      return fail(LL_ERR_INVALID_ARGUMENT, "sequence %d: %d cached + %d new keys outside "
+                  "[1, max_ctx]", b, P0, L);
     pm.lens[b] = L;
+    pm.start[b] = P0;
     total += L;
     n_qtiles += (L + qtile - 1) / qtile;
   }
@@ -877,16 +894,18 @@ ll_status ll_op_attn_prefill(int32_t dtype, int32_t batch, const int32_t *seq_le
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o2 = off; off = align_up(off + bytes); return o2; };
   const size_t o_cu = take((batch + 1) * 4), o_seq = take(total * 4), o_pos = take(total * 4),
-               o_last = take(batch * 4), o_lens = take(batch * 4), o_qt = take((size_t)n_qtiles * 8);
+               o_last = take(batch * 4), o_lens = take(batch * 4), o_ks = take(batch * 4),
+               o_qt = take((size_t)n_qtiles * 8);
   if (off > scratch_bytes) return fail(LL_ERR_WORKSPACE, "scratch needs %zu bytes", off);
   char *sc = reinterpret_cast<char *>(scratch);
   hipStream_t s = (hipStream_t)stream;
   LL_HIP(launch_prefill_meta(pm, (int)total, qtile, (int *)(sc + o_cu), (int *)(sc + o_seq),
                              (int *)(sc + o_pos), (int *)(sc + o_last), (int *)(sc + o_lens),
-                             (int2 *)(sc + o_qt), s));
+                             (int *)(sc + o_ks), (int2 *)(sc + o_qt), s));
   const int qd = n_heads * head_dim;
   LL_HIP(launch_attn_prefill(dtype, head_dim, q, qd, kcache, vcache, o, qd, (int *)(sc + o_cu),
-                             (int2 *)(sc + o_qt), n_qtiles, n_heads, n_kv_heads, max_ctx, s));
+                             (int *)(sc + o_ks), (int2 *)(sc + o_qt), n_qtiles, n_heads,
+                             n_kv_heads, max_ctx, s));
   return LL_OK;
 }
 

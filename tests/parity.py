@@ -105,6 +105,62 @@ def run_gpu_teacher_forced(cfg, weights, lens, packed, ref_tokens, n_decode, use
     return np.stack(out_l), np.stack(out_t)
 
 
+def chunk_prompts(prompts, n_chunks):
+    """Each prompt cut into n_chunks consecutive pieces of near-equal length (each >= 1)."""
+    out = []
+    for i in range(n_chunks):
+        out.append([np.array_split(np.asarray(p), n_chunks)[i] for p in prompts])
+    return out
+
+
+def oracle_chunked_run(model, chunks, n_decode):
+    """Oracle: prefill of the first chunks, extend by the others, then n_decode teacher-forced
+    greedy steps.  Returns (logits [n_chunks + n_decode, B, V], tokens)."""
+    from oracle import argmax_lowest
+    logits = [model.prefill(chunks[0])] + [model.extend(c) for c in chunks[1:]]
+    toks = [argmax_lowest(lg) for lg in logits]
+    for _ in range(n_decode):
+        logits.append(model.decode(toks[-1]))
+        toks.append(argmax_lowest(logits[-1]))
+    return np.stack(logits), np.stack(toks)
+
+
+def run_gpu_chunked(cfg, weights, chunks, ref_tokens, n_decode, options=None):
+    """The same through the C ABI: one ll_prefill per chunk (the later ones on the populated
+    cache), then decode steps fed the oracle's tokens."""
+    import torch
+    from paper_2608_21836_amd.binding import Model, upload_weights
+    B = len(chunks[0])
+    total = [sum(len(c[b]) for c in chunks) for b in range(B)]
+    dev_w = upload_weights(cfg, weights)
+    model = Model(cfg, dev_w, max_batch=B, max_prefill_tokens=max(sum(len(x) for x in c) for c in chunks),
+                  max_ctx=max(total) + n_decode)
+    del dev_w
+    for name, value in (options or {}).items():
+        model.set_option(name, value)
+    logits = torch.empty(B, cfg.vocab, dtype=torch.float32, device="cuda")
+    nxt = torch.empty(B, dtype=torch.int32, device="cuda")
+    out_l, out_t = [], []
+    for c in chunks:
+        toks = torch.from_numpy(np.concatenate(c).astype(np.int32)).cuda()
+        model.prefill([len(x) for x in c], toks, nxt, logits)
+        torch.cuda.synchronize()
+        out_l.append(logits.cpu().numpy().copy())
+        out_t.append(nxt.cpu().numpy().copy())
+    n_chunks = len(chunks)
+    inp = torch.empty(B, dtype=torch.int32, device="cuda")
+    for k in range(n_decode):
+        inp.copy_(torch.from_numpy(np.asarray(ref_tokens[n_chunks - 1 + k], dtype=np.int32)))
+        model.decode_step(inp, nxt, logits)
+        torch.cuda.synchronize()
+        out_l.append(logits.cpu().numpy().copy())
+        out_t.append(nxt.cpu().numpy().copy())
+    assert model.seq_lengths() == [t + n_decode for t in total]
+    assert model.device_flags() == 0
+    model.close()
+    return np.stack(out_l), np.stack(out_t)
+
+
 def device_tensor(arr, dtype):
     from paper_2608_21836_amd.binding import to_device
     return to_device(arr, dtype)

@@ -138,8 +138,13 @@ def test_op_argument_validation(lib):
     assert lib.ll_op_rmsnorm(1, 4, 6, 1, 1, 1e-5, 1, None) == B.LL_ERR_INVALID_ARGUMENT
     assert lib.ll_op_repack(1, 20, 64, 1, 1, None) == B.LL_ERR_UNSUPPORTED
     lens = (ctypes.c_int32 * 2)(5, 0)
-    assert lib.ll_op_attn_prefill(1, 2, lens, 8, 2, 64, 16, 1, 1, 1, 1, 0x10000, 4096, None) == \
-        B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_op_attn_prefill(1, 2, lens, None, 8, 2, 64, 16, 1, 1, 1, 1, 0x10000, 4096,
+                                  None) == B.LL_ERR_INVALID_ARGUMENT
+    # cached keys + new tokens beyond max_ctx
+    lens = (ctypes.c_int32 * 1)(5)
+    cached = (ctypes.c_int32 * 1)(12)
+    assert lib.ll_op_attn_prefill(1, 1, lens, cached, 8, 2, 64, 16, 1, 1, 1, 1, 0x10000, 4096,
+                                  None) == B.LL_ERR_INVALID_ARGUMENT
     assert lib.ll_op_attn_decode(1, 1, 8, 3, 64, 16, 1, 1, 1, 1, 1, 0x10000, 1 << 20, None) == \
         B.LL_ERR_UNSUPPORTED
     assert lib.ll_op_attn_decode(1, 1, 8, 2, 64, 16, 1, 1, 1, 1, 1, 0x10000, 8, None) == \

@@ -185,6 +185,45 @@ def test_attn_prefill(dtype, hd, hq, hkv, lens):
         t0 += L
 
 
+# Prefill chunks on populated caches: (dtype, hd, hq, hkv, new tokens, cached keys) per
+# sequence; query i of sequence b sits at position cached[b] + i.
+CHUNK_CASES = [
+    ("bf16", 64, 8, 2, [1, 63, 64, 130], [100, 1, 64, 0]),
+    ("bf16", 128, 32, 8, [200, 17], [1000, 63]),
+    ("bf16", 64, 4, 4, [128], [512]),
+    ("f32", 64, 4, 4, [33, 1, 70], [31, 200, 64]),
+    ("f32", 128, 4, 2, [65], [3]),
+]
+
+
+@pytest.mark.parametrize("dtype,hd,hq,hkv,lens,cached", CHUNK_CASES)
+def test_attn_prefill_chunk(dtype, hd, hq, hkv, lens, cached):
+    from paper_2608_21836_amd.binding import op_attn_prefill
+    import torch
+    log(f"attn_prefill chunk {dtype} hd={hd} hq={hq} hkv={hkv} lens={lens} cached={cached}")
+    rng = np.random.default_rng(hd + hq * 10 + sum(cached))
+    B, T = len(lens), sum(lens)
+    tot = [c + n for c, n in zip(cached, lens)]
+    max_ctx = max(tot) + 5
+    q = rounded(rng.standard_normal((T, hq * hd)), dtype)
+    k, v = _caches(rng, dtype, B, hkv, max_ctx, hd, tot)
+    o = op_attn_prefill(lens, device_tensor(q, dtype), device_tensor(k, dtype),
+                        device_tensor(v, dtype), hq, hkv, hd, max_ctx, cached=cached)
+    torch.cuda.synchronize()
+    o = _np(o)
+    t0 = 0
+    for b, L in enumerate(lens):
+        P0 = cached[b]
+        qb = q[t0:t0 + L].reshape(L, hq, hd).astype(np.float64)
+        kb = k[b, :, :P0 + L].transpose(1, 0, 2).astype(np.float64)
+        vb = v[b, :, :P0 + L].transpose(1, 0, 2).astype(np.float64)
+        ref = oracle.causal_gqa_attention(qb, kb, vb, P0 + np.arange(L), np.arange(P0 + L))
+        ref = ref.reshape(L, hq * hd)
+        tol = (4 * 2.0 ** -9 if dtype == "bf16" else 1e-5) * np.abs(vb).max()
+        assert np.all(np.abs(o[t0:t0 + L] - ref) <= tol), f"sequence {b}"
+        t0 += L
+
+
 DEC_CASES = [
     ("bf16", 64, 8, 2, [1, 63, 64, 65, 257, 1000], 1024),
     ("bf16", 128, 32, 8, [4096, 17, 2049], 4224),

@@ -93,6 +93,27 @@ def test_cached_decode_matches_library_llama():
     assert _rel_err(np.stack(ours), np.stack(ref)) < 1e-5
 
 
+def test_chunked_prefill_matches_library_llama():
+    """A prompt prefilled in chunks on a populated cache (extend) against transformers' LLaMA
+    fed the same chunks with its own key/value cache."""
+    cfg = MICRO.replace(name="micro-hd8", n_heads=2, n_kv_heads=1, head_dim=8, seed=103)
+    w = micro_weights(cfg)
+    toks = np.random.default_rng(9).integers(0, cfg.vocab, size=11)
+    chunks = [toks[:4], toks[4:5], toks[5:11]]
+    om = T.OracleModel(cfg, w)
+    ours = [om.prefill([chunks[0]])[0]] + [om.extend([c])[0] for c in chunks[1:]]
+    assert om.lengths == [11]
+    m = hf_model(cfg, w)
+    with torch.no_grad():
+        out = m(torch.tensor(chunks[0][None]), use_cache=True)
+        ref, past = [out.logits[0, -1].numpy()], out.past_key_values
+        for c in chunks[1:]:
+            out = m(torch.tensor(c[None]), past_key_values=past, use_cache=True)
+            ref.append(out.logits[0, -1].numpy())
+            past = out.past_key_values
+    assert _rel_err(np.stack(ours), np.stack(ref)) < 1e-5
+
+
 # ------------------------------------------------------------------------------------------
 # Brute force: a scalar-loop model written without numpy linear algebra
 # ------------------------------------------------------------------------------------------
@@ -290,6 +311,26 @@ def test_incremental_decode_equals_full_recompute():
     for i, lg in enumerate(steps):
         ref = full[4 + i]
         assert np.max(np.abs(lg - ref)) <= 1e-10 * np.max(np.abs(ref))
+
+
+def test_chunked_prefill_equals_full_recompute():
+    """Prefill chunks of two ragged sequences on populated caches give, at every chunk's
+    last position, the logits of a fresh causal forward over the tokens so far."""
+    cfg = MICRO
+    w = micro_weights()
+    rng = np.random.default_rng(6)
+    seqs = [rng.integers(0, cfg.vocab, size=9), rng.integers(0, cfg.vocab, size=4)]
+    cuts = [[3, 4, 9], [1, 2, 4]]   # chunk ends per sequence (a 1-token chunk included)
+    om = T.OracleModel(cfg, w)
+    got = [om.prefill([s_[:c[0]] for s_, c in zip(seqs, cuts)])]
+    for i in (1, 2):
+        got.append(om.extend([s_[c[i - 1]:c[i]] for s_, c in zip(seqs, cuts)]))
+    for b, s_ in enumerate(seqs):
+        full = T.OracleModel(cfg, w).forward_full(s_)
+        for i, end in enumerate(cuts[b]):
+            ref = full[end - 1]
+            assert np.max(np.abs(got[i][b] - ref)) <= 1e-10 * np.max(np.abs(ref))
+    assert om.lengths == [9, 4]
 
 
 def test_gqa_equals_mha_with_repeated_kv():
