@@ -55,10 +55,28 @@ __global__ void k_repack(RepackSrc src, int n, int k, int perm, int hd, int ffn,
 // Epilogues: called with (row m, 32-column unit u, lane column c, first-half value,
 // second-half value).
 // ------------------------------------------------------------------------------------------
+// Eight consecutive outputs of type T from fp32 values, as 16-byte stores.
+template <typename T> __device__ __forceinline__ void store8(T *dst, const float *v);
+template <> __device__ __forceinline__ void store8<bf16>(bf16 *dst, const float *v) {
+  uint32_t w[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    w[j] = (uint32_t)__builtin_bit_cast(uint16_t, static_cast<bf16>(v[2 * j])) |
+           ((uint32_t)__builtin_bit_cast(uint16_t, static_cast<bf16>(v[2 * j + 1])) << 16);
+  *reinterpret_cast<uint4 *>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+template <> __device__ __forceinline__ void store8<float>(float *dst, const float *v) {
+  reinterpret_cast<float4 *>(dst)[0] = make_float4(v[0], v[1], v[2], v[3]);
+  reinterpret_cast<float4 *>(dst)[1] = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+// kVec8 epilogues also take eight consecutive columns of each half of a 32-column unit at once
+// (vec8(m, u, c0, first[8], second[8]): columns 32 u + c0 .. + 7 and 32 u + 16 + c0 .. + 7),
+// which the prefill GEMM feeds from an LDS transpose of its accumulators.
 struct EpiStore {
   float *out;
   int ld;
-  static constexpr bool kArgmax = false, kPairs = false;
+  static constexpr bool kArgmax = false, kPairs = false, kVec8 = false;
   __device__ void operator()(int m, int u, int c, float v0, float v1) const {
     float *p = out + (size_t)m * ld + 32 * u + c;
     p[0] = v0;
@@ -70,7 +88,7 @@ struct EpiStore {
 struct EpiResid {
   float *out;
   int ld;
-  static constexpr bool kArgmax = false, kPairs = false;
+  static constexpr bool kArgmax = false, kPairs = false, kVec8 = false;
   __device__ void operator()(int m, int u, int c, float v0, float v1) const {
     float *p = out + (size_t)m * ld + 32 * u + c;
     p[0] += v0;
@@ -82,9 +100,15 @@ struct EpiResid {
 template <typename T> struct EpiSwiglu {
   T *out;
   int ld;
-  static constexpr bool kArgmax = false, kPairs = true;
+  static constexpr bool kArgmax = false, kPairs = true, kVec8 = true;
   __device__ void operator()(int m, int u, int c, float g, float up) const {
     out[(size_t)m * ld + 16 * u + c] = from_f32<T>(silu_f(g) * up);
+  }
+  __device__ void vec8(int m, int u, int c0, const float *g, const float *up) const {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = silu_f(g[e]) * up[e];
+    store8<T>(out + (size_t)m * ld + 16 * u + c0, v);
   }
 };
 
@@ -95,7 +119,7 @@ template <typename T> struct EpiQkv {
   const int *row_seq, *row_pos;
   const float *rcos, *rsin;
   int hq, hkv, hd, max_ctx;
-  static constexpr bool kArgmax = false, kPairs = true;
+  static constexpr bool kArgmax = false, kPairs = true, kVec8 = true;
   __device__ void operator()(int m, int u, int c, float v0, float v1) const {
     const int n0 = u * 32;
     const int head = n0 / hd;
@@ -121,6 +145,46 @@ template <typename T> struct EpiQkv {
     dst[i1] = from_f32<T>(v0);
     dst[i2] = from_f32<T>(v1);
   }
+  // The same for pair indices i1 = 16 j + c0 .. + 7 of one unit: eight RoPE pairs, two
+  // 16-byte stores.
+  __device__ void vec8(int m, int u, int c0, const float *a, const float *b) const {
+    const int n0 = u * 32;
+    const int head = n0 / hd;
+    const int j = (n0 - head * hd) >> 5;
+    const int half = hd >> 1;
+    const int i1 = 16 * j + c0, i2 = half + i1;
+    const int pos = row_pos[m];
+    float x[8], y[8];
+    if (head < hq + hkv) {  // rotate-half RoPE on queries and keys
+      const float4 *cp = reinterpret_cast<const float4 *>(rcos + (size_t)pos * half + i1);
+      const float4 *sp = reinterpret_cast<const float4 *>(rsin + (size_t)pos * half + i1);
+      const float4 c4[2] = {cp[0], cp[1]}, s4[2] = {sp[0], sp[1]};
+      const float co[8] = {c4[0].x, c4[0].y, c4[0].z, c4[0].w, c4[1].x, c4[1].y, c4[1].z, c4[1].w};
+      const float si[8] = {s4[0].x, s4[0].y, s4[0].z, s4[0].w, s4[1].x, s4[1].y, s4[1].z, s4[1].w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        x[e] = a[e] * co[e] - b[e] * si[e];
+        y[e] = b[e] * co[e] + a[e] * si[e];
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        x[e] = a[e];
+        y[e] = b[e];
+      }
+    }
+    T *dst;
+    if (head < hq) {
+      dst = q + (size_t)m * ldq + head * hd;
+    } else {
+      const bool is_k = head < hq + hkv;
+      const int kvh = is_k ? head - hq : head - hq - hkv;
+      const int seq = row_seq ? row_seq[m] : m;
+      dst = (is_k ? kc : vc) + (((size_t)seq * hkv + kvh) * max_ctx + pos) * hd;
+    }
+    store8<T>(dst + i1, x);
+    store8<T>(dst + i2, y);
+  }
 };
 
 // fp32 partial sums of one K range of a split GEMM: plane blockIdx.z of [split][M][ld].
@@ -128,7 +192,7 @@ struct EpiPart {
   float *out;
   int ld;
   size_t plane;
-  static constexpr bool kArgmax = false, kPairs = false;
+  static constexpr bool kArgmax = false, kPairs = false, kVec8 = false;
   __device__ void operator()(int m, int u, int c, float v0, float v1) const {
     float *p = out + blockIdx.z * plane + (size_t)m * ld + 32 * u + c;
     p[0] = v0;
@@ -142,7 +206,7 @@ struct EpiArgmax {
   float *pval;
   int *pidx;
   int n_parts;
-  static constexpr bool kArgmax = true, kPairs = true;
+  static constexpr bool kArgmax = true, kPairs = true, kVec8 = false;
 };
 
 // ------------------------------------------------------------------------------------------
@@ -284,16 +348,44 @@ __global__ __launch_bounds__(BN * 2, 1) void k_gemm_big(const T *__restrict__ A,
   wait_vmcnt<0>();
 
   const int ubase = (n0 + wn * 64) >> 5;
+  if constexpr (Epi::kVec8) {
+    // Each 16 x 64 block of the wave's accumulators goes through a wave-private LDS scratch
+    // (the ring is free once every wave has passed the barrier), and is read back row-wise:
+    // lane l takes row l / 4 and eight consecutive columns of both halves of one 32-column
+    // unit, so the epilogue loads and stores 16 bytes at a time.
+    constexpr int LD = 68;  // row stride in floats (a 16-float skew between the 4-row groups)
+    static_assert(NW * 16 * LD * 4 <= S * TPS * 1024, "epilogue scratch fits in the ring");
+    __syncthreads();
+    float *sc = reinterpret_cast<float *>(smem) + wave * (16 * LD);
+    const int rho = lane >> 2, u = (lane >> 1) & 1, c0 = 8 * (lane & 1);
 #pragma unroll
-  for (int i = 0; i < NI; ++i)
+    for (int i = 0; i < NI; ++i) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = m0 + wm * (BM / 2) + i * 16 + (lane >> 4) * 4 + r;
-      if (m < M) {
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int p = 0; p < 2; ++p) epi(m, ubase + p, lane & 15, acc[i][2 * p][r], acc[i][2 * p + 1][r]);
-      }
+        for (int r = 0; r < 4; ++r) sc[(4 * (lane >> 4) + r) * LD + 16 * j + (lane & 15)] = acc[i][j][r];
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      const float4 *f0 = reinterpret_cast<const float4 *>(sc + rho * LD + 32 * u + c0);
+      const float4 *f1 = reinterpret_cast<const float4 *>(sc + rho * LD + 32 * u + 16 + c0);
+      const float4 a0 = f0[0], a1 = f0[1], b0 = f1[0], b1 = f1[1];
+      const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+      const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+      const int m = m0 + wm * (BM / 2) + i * 16 + rho;
+      if (m < M) epi.vec8(m, ubase + u, c0, av, bv);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     }
+  } else {
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + wm * (BM / 2) + i * 16 + (lane >> 4) * 4 + r;
+        if (m < M) {
+#pragma unroll
+          for (int p = 0; p < 2; ++p) epi(m, ubase + p, lane & 15, acc[i][2 * p][r], acc[i][2 * p + 1][r]);
+        }
+      }
+  }
 }
 
 // ------------------------------------------------------------------------------------------
