@@ -6,6 +6,8 @@ TEST INFRASTRUCTURE: only ``tests/``, ``__graft_entry__.smoke()`` and the benchm
 Parity status of each function (pins live in tests/test_oracle_pins.py):
   rmsnorm, rope_frequencies, apply_rope, softmax, causal_gqa_attention, silu/swiglu,
   argmax_lowest, top2_margin, OracleModel (prefill, decode, forward_full) -- all pinned.
+  mamba: softplus, causal_depthwise_conv, selective_scan, OracleMamba (prefill, decode,
+  forward_full) -- all pinned (tests/test_mamba_oracle_pins.py).
 """
 from .transformer import (  # noqa: F401
     OracleModel, apply_rope, argmax_lowest, causal_gqa_attention, rmsnorm, rope_frequencies,

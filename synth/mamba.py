@@ -1,0 +1,141 @@
+"""Shapes, seeds and synthetic weights of the selective state-space (Mamba) workloads.
+
+Like the decoder workloads, this module only draws numbers; it holds no arithmetic of the
+forward pass.  The paper's Mamba-family cases (appendix "Deployment Kernel Families",
+Table A.4) are a prefill recurrent scan and a single-token decode that updates the
+convolution and SSM state of an existing cache; the paper gives no hyper-parameters, so the
+shapes below define the workloads (mamba-130m has the Mamba-130M layer shape of the paper's
+Table 1).
+
+Tensors per layer (names of the standard Mamba mixer):
+  norm      [d]            RMSNorm gain (ones)
+  in_proj   [2 di, d]      workload dtype, N(0, init_std^2)
+  conv_w    [di, d_conv]   fp32, N(0, conv_std^2)      depthwise causal convolution taps
+  conv_b    [di]           fp32, N(0, 0.02^2)
+  x_proj    [R + 2 N, di]  workload dtype, N(0, init_std^2)
+  dt_w      [di, R]        fp32, N(0, R^-1)            dt projection
+  dt_b      [di]           fp32, softplus^-1 of dt log-uniform in [dt_min, dt_max]
+  A_log     [di, N]        fp32, log(1 .. N) in every row (A = -exp(A_log))
+  D         [di]           fp32, ones
+  out_proj  [d, di]        workload dtype, N(0, (init_std / sqrt(2 L))^2)
+and embed [V, d] (workload dtype; the LM head is tied to it) and final_norm [d] (ones).
+Random tensor j draws from default_rng([s, 2, j]) in the order embed, then per layer
+(in_proj, conv_w, conv_b, x_proj, dt_w, dt_b, out_proj); prompts use the streams of gen.py.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, List, Optional, Tuple
+
+import numpy as np
+
+from .gen import round_to_bf16
+
+
+@dataclasses.dataclass(frozen=True)
+class MambaConfig:
+    name: str
+    seed: int
+    dtype: str            # storage of the embedding and projection matrices ("bf16" or "f32")
+    n_layers: int
+    d_model: int
+    d_inner: int
+    d_state: int
+    d_conv: int
+    dt_rank: int
+    vocab: int
+    rms_eps: float = 1e-5
+    batch: int = 1
+    prompt_len: Optional[int] = None
+    prompt_range: Optional[Tuple[int, int]] = None
+    prompt_list: Optional[Tuple[int, ...]] = None
+    n_decode: int = 1
+    init_std: float = 0.02
+    conv_std: float = 0.3
+    dt_min: float = 1e-3
+    dt_max: float = 1e-1
+    family: str = "mamba"
+
+    @property
+    def xdbl_dim(self) -> int:
+        return self.dt_rank + 2 * self.d_state
+
+    def linear_params_per_layer(self) -> int:
+        return (2 * self.d_inner * self.d_model + self.xdbl_dim * self.d_inner +
+                self.d_model * self.d_inner)
+
+    def replace(self, **kw) -> "MambaConfig":
+        return dataclasses.replace(self, **kw)
+
+
+MAMBA_CONFIGS: Dict[str, MambaConfig] = {
+    # The Mamba-130M layer shape: 24 layers, d 768, expand 2, state 16, conv 4, dt rank 48;
+    # vocab 50304 (the GPT-NeoX vocabulary padded to a multiple of 32 for the LM-head tiles).
+    "mamba-130m": MambaConfig(
+        name="mamba-130m", seed=21, dtype="bf16", n_layers=24, d_model=768, d_inner=1536,
+        d_state=16, d_conv=4, dt_rank=48, vocab=50304, batch=1, prompt_len=1024, n_decode=128),
+}
+
+MAMBA_TEST_CONFIGS: Dict[str, MambaConfig] = {
+    # ragged prompts incl. a 1-token one, fp32 and bf16
+    "t-mamba": MambaConfig(
+        name="t-mamba", seed=31, dtype="bf16", n_layers=2, d_model=128, d_inner=256,
+        d_state=16, d_conv=4, dt_rank=8, vocab=512, batch=3, prompt_list=(37, 1, 70),
+        n_decode=5),
+    "t-mamba-f32": MambaConfig(
+        name="t-mamba-f32", seed=32, dtype="f32", n_layers=2, d_model=128, d_inner=256,
+        d_state=16, d_conv=4, dt_rank=8, vocab=512, batch=2, prompt_list=(19, 66),
+        n_decode=4),
+}
+
+
+def tensor_specs(cfg: MambaConfig) -> List[Tuple[str, int, Tuple[int, ...], str]]:
+    """[(name, j, shape, kind)] of the random tensors in stream order."""
+    di, d, R, N = cfg.d_inner, cfg.d_model, cfg.dt_rank, cfg.d_state
+    out = [("embed", 0, (cfg.vocab, d), "mat")]
+    j = 1
+    for layer in range(cfg.n_layers):
+        for name, shape, kind in (("in_proj", (2 * di, d), "mat"), ("conv_w", (di, cfg.d_conv), "conv"),
+                                  ("conv_b", (di,), "bias"), ("x_proj", (cfg.xdbl_dim, di), "mat"),
+                                  ("dt_w", (di, R), "dtw"), ("dt_b", (di,), "dtb"),
+                                  ("out_proj", (d, di), "out")):
+            out.append((f"layers.{layer}.{name}", j, shape, kind))
+            j += 1
+    return out
+
+
+def _draw(cfg: MambaConfig, j: int, shape, kind: str) -> np.ndarray:
+    rng = np.random.default_rng([cfg.seed, 2, j])
+    if kind == "dtb":
+        # dt log-uniform in [dt_min, dt_max]; bias = softplus^-1(dt) = dt + log(-expm1(-dt))
+        u = rng.random(shape)
+        dt = np.exp(u * (math.log(cfg.dt_max) - math.log(cfg.dt_min)) + math.log(cfg.dt_min))
+        return (dt + np.log(-np.expm1(-dt))).astype(np.float32)
+    w = rng.standard_normal(shape, dtype=np.float32)
+    std = {"mat": cfg.init_std, "conv": cfg.conv_std, "bias": 0.02,
+           "dtw": cfg.dt_rank ** -0.5, "out": cfg.init_std / math.sqrt(2 * cfg.n_layers)}[kind]
+    w *= np.float32(std)
+    if kind in ("mat", "out") and cfg.dtype == "bf16":
+        w = round_to_bf16(w)
+    return w
+
+
+def weights(cfg: MambaConfig) -> Dict[str, np.ndarray]:
+    """Every tensor as an fp32 array (bf16-exact values for the bf16 matrices)."""
+    out = {name: _draw(cfg, j, shape, kind) for name, j, shape, kind in tensor_specs(cfg)}
+    a_log = np.log(np.arange(1, cfg.d_state + 1, dtype=np.float32))
+    for layer in range(cfg.n_layers):
+        out[f"layers.{layer}.norm"] = np.ones(cfg.d_model, dtype=np.float32)
+        out[f"layers.{layer}.A_log"] = np.tile(a_log, (cfg.d_inner, 1)).astype(np.float32)
+        out[f"layers.{layer}.D"] = np.ones(cfg.d_inner, dtype=np.float32)
+    out["final_norm"] = np.ones(cfg.d_model, dtype=np.float32)
+    return out
+
+
+def get_mamba_config(name: str) -> MambaConfig:
+    if name in MAMBA_CONFIGS:
+        return MAMBA_CONFIGS[name]
+    if name in MAMBA_TEST_CONFIGS:
+        return MAMBA_TEST_CONFIGS[name]
+    raise KeyError(name)
