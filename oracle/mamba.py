@@ -117,6 +117,12 @@ class OracleMamba:
             out.append(self._run(b, toks, all_logits))
         return out if all_logits else np.stack(out)
 
+    def extend(self, chunks: Sequence[np.ndarray]) -> np.ndarray:
+        """Prefill of a further prompt chunk per sequence on the carried state (the scan and
+        the convolution continue from it); logits at each chunk's last token ([B, V])."""
+        assert len(chunks) == len(self.lengths), "a chunk per held sequence"
+        return np.stack([self._run(b, np.asarray(c), False) for b, c in enumerate(chunks)])
+
     def decode(self, tokens: Sequence[int]) -> np.ndarray:
         """Decode: one token per sequence on the carried state; [B, V] logits."""
         assert len(tokens) == len(self.lengths)

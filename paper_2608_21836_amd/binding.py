@@ -42,8 +42,28 @@ class LLWeights(ctypes.Structure):
                 ("w_up", POINTER(c_void_p)), ("w_down", POINTER(c_void_p))]
 
 
-# (name, restype, argtypes) of every exported symbol; include/ll.h and include/ll_ops.h
-# declare the same set.
+class LLMambaConfig(ctypes.Structure):
+    _fields_ = [("n_layers", c_int32), ("d_model", c_int32), ("d_inner", c_int32),
+                ("d_state", c_int32), ("d_conv", c_int32), ("dt_rank", c_int32),
+                ("vocab", c_int32), ("rms_eps", c_float), ("dtype", c_int32),
+                ("max_batch", c_int32), ("max_prefill_tokens", c_int32)]
+
+
+MAMBA_LAYER_FIELDS = ("norm", "in_proj", "conv_w", "conv_b", "x_proj", "dt_w", "dt_b", "A_log",
+                      "D", "out_proj")
+# tensors kept in fp32 whatever the workload dtype
+MAMBA_F32_FIELDS = ("conv_w", "conv_b", "dt_w", "dt_b", "A_log", "D")
+
+
+class LLMambaWeights(ctypes.Structure):
+    _fields_ = [("embed", c_void_p), ("final_norm", c_void_p)] + \
+        [(f, POINTER(c_void_p)) for f in MAMBA_LAYER_FIELDS]
+
+
+LL_MK_COUNT = 12
+
+# (name, restype, argtypes) of every exported symbol; include/ll.h, include/ll_ops.h and
+# include/ll_mamba.h declare the same set.
 SIGNATURES = [
     ("ll_workspace_size", c_int32, [POINTER(LLConfig), POINTER(c_size_t)]),
     ("ll_model_load", c_int32, [POINTER(LLConfig), POINTER(LLWeights), c_void_p, c_size_t,
@@ -82,6 +102,21 @@ SIGNATURES = [
     ("ll_op_attn_decode_scratch", c_size_t, [c_int32, c_int32, c_int32, c_int32, c_int32]),
     ("ll_op_lmhead_argmax", c_int32, [c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
                                       c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+    ("ll_mamba_workspace_size", c_int32, [POINTER(LLMambaConfig), POINTER(c_size_t)]),
+    ("ll_mamba_load", c_int32, [POINTER(LLMambaConfig), POINTER(LLMambaWeights), c_void_p,
+                                c_size_t, c_void_p, POINTER(c_void_p)]),
+    ("ll_mamba_prefill", c_int32, [c_void_p, c_int32, POINTER(c_int32), c_void_p, c_void_p,
+                                   c_void_p]),
+    ("ll_mamba_decode_step", c_int32, [c_void_p, c_void_p, c_void_p, c_void_p]),
+    ("ll_mamba_reset", c_int32, [c_void_p]),
+    ("ll_mamba_seq_lengths", c_int32, [c_void_p, POINTER(c_int32), c_int32, POINTER(c_int32)]),
+    ("ll_mamba_set_option", c_int32, [c_void_p, c_int32, c_int32]),
+    ("ll_mamba_get_option", c_int32, [c_void_p, c_int32, POINTER(c_int32)]),
+    ("ll_mamba_device_flags", c_int32, [c_void_p, POINTER(c_int32)]),
+    ("ll_mamba_set_kernel_timing", c_int32, [c_void_p, c_int32]),
+    ("ll_mamba_kernel_timing_read", c_int32, [c_void_p, POINTER(c_int32), POINTER(c_double)]),
+    ("ll_mamba_kernel_class_name", c_char_p, [c_int32]),
+    ("ll_mamba_free", None, [c_void_p]),
 ]
 
 _lib = None
@@ -255,6 +290,129 @@ class Model:
         return f.value
 
 
+def make_mamba_config(cfg, max_batch: int, max_prefill_tokens: int) -> LLMambaConfig:
+    """LLMambaConfig from a synth.mamba.MambaConfig-like object."""
+    return LLMambaConfig(cfg.n_layers, cfg.d_model, cfg.d_inner, cfg.d_state, cfg.d_conv,
+                         cfg.dt_rank, cfg.vocab, float(cfg.rms_eps),
+                         LL_BF16 if cfg.dtype == "bf16" else LL_F32, max_batch, max_prefill_tokens)
+
+
+def mamba_workspace_size(cfg: LLMambaConfig) -> int:
+    n = c_size_t(0)
+    _check(load_library().ll_mamba_workspace_size(ctypes.byref(cfg), ctypes.byref(n)),
+           "ll_mamba_workspace_size")
+    return n.value
+
+
+class MambaModel:
+    """One loaded Mamba model: workspace (a torch uint8 tensor), handle and stream.
+
+    ``weights`` maps synth.mamba tensor names to CUDA tensors (upload_mamba_weights)."""
+
+    def __init__(self, cfg, weights: Dict[str, "object"], max_batch: int,
+                 max_prefill_tokens: int, stream=None):
+        import torch
+        self.lib = load_library()
+        self.mcfg = cfg
+        self.cfg = make_mamba_config(cfg, max_batch, max_prefill_tokens)
+        self.stream = stream if stream is not None else torch.cuda.current_stream()
+        nbytes = mamba_workspace_size(self.cfg)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        nl = cfg.n_layers
+        keep, fields = [], {}
+        for key in MAMBA_LAYER_FIELDS:
+            a = (c_void_p * nl)(*[weights[f"layers.{i}.{key}"].data_ptr() for i in range(nl)])
+            keep.append(a)
+            fields[key] = ctypes.cast(a, POINTER(c_void_p))
+        w = LLMambaWeights(weights["embed"].data_ptr(), weights["final_norm"].data_ptr(), **fields)
+        handle = c_void_p()
+        _check(self.lib.ll_mamba_load(ctypes.byref(self.cfg), ctypes.byref(w),
+                                      self.workspace.data_ptr(), nbytes,
+                                      self.stream.cuda_stream, ctypes.byref(handle)),
+               "ll_mamba_load")
+        self.handle = handle
+        self.batch = 0
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            self.lib.ll_mamba_free(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def prefill(self, seq_lens: Sequence[int], tokens, next_tokens=None, logits=None):
+        import torch
+        b = len(seq_lens)
+        lens = (c_int32 * b)(*[int(x) for x in seq_lens])
+        if next_tokens is None:
+            next_tokens = torch.empty(b, dtype=torch.int32, device="cuda")
+        _check(self.lib.ll_mamba_prefill(self.handle, b, lens, tokens.data_ptr(),
+                                         next_tokens.data_ptr(), _ptr(logits)), "ll_mamba_prefill")
+        self.batch = b
+        return next_tokens, logits
+
+    def decode_step(self, in_tokens, next_tokens=None, logits=None):
+        import torch
+        if next_tokens is None:
+            next_tokens = torch.empty(self.batch, dtype=torch.int32, device="cuda")
+        _check(self.lib.ll_mamba_decode_step(self.handle, in_tokens.data_ptr(),
+                                             next_tokens.data_ptr(), _ptr(logits)),
+               "ll_mamba_decode_step")
+        return next_tokens, logits
+
+    def reset(self) -> None:
+        _check(self.lib.ll_mamba_reset(self.handle), "ll_mamba_reset")
+        self.batch = 0
+
+    def set_option(self, name: str, value: int) -> None:
+        _check(self.lib.ll_mamba_set_option(self.handle, OPTIONS[name], int(value)),
+               "ll_mamba_set_option")
+
+    def get_option(self, name: str) -> int:
+        v = c_int32(0)
+        _check(self.lib.ll_mamba_get_option(self.handle, OPTIONS[name], ctypes.byref(v)),
+               "ll_mamba_get_option")
+        return v.value
+
+    def options(self) -> Dict[str, int]:
+        return {k: self.get_option(k) for k in OPTIONS if k != "attn_decode_chunk"}
+
+    def seq_lengths(self) -> List[int]:
+        out = (c_int32 * LL_MAX_BATCH)()
+        n = c_int32(0)
+        _check(self.lib.ll_mamba_seq_lengths(self.handle, out, LL_MAX_BATCH, ctypes.byref(n)),
+               "ll_mamba_seq_lengths")
+        return list(out[:n.value])
+
+    def set_kernel_timing(self, enable: bool) -> None:
+        _check(self.lib.ll_mamba_set_kernel_timing(self.handle, 1 if enable else 0),
+               "ll_mamba_set_kernel_timing")
+
+    def kernel_timing(self) -> Dict[Tuple[str, str], Tuple[int, float]]:
+        """{(phase, kernel class): (launches, summed kernel ms)} since the last read."""
+        counts = (c_int32 * (2 * LL_MK_COUNT))()
+        ms = (c_double * (2 * LL_MK_COUNT))()
+        _check(self.lib.ll_mamba_kernel_timing_read(self.handle, counts, ms),
+               "ll_mamba_kernel_timing_read")
+        out = {}
+        for p in range(2):
+            for c in range(LL_MK_COUNT):
+                i = p * LL_MK_COUNT + c
+                if counts[i]:
+                    name = self.lib.ll_mamba_kernel_class_name(c).decode()
+                    out[(PHASES[p], name)] = (counts[i], ms[i])
+        return out
+
+    def device_flags(self) -> int:
+        f = c_int32(0)
+        _check(self.lib.ll_mamba_device_flags(self.handle, ctypes.byref(f)), "ll_mamba_device_flags")
+        return f.value
+
+
 # ------------------------------------------------------------------------------------------
 # Weights: numpy (synth.gen) -> CUDA tensors of the workload dtype
 # ------------------------------------------------------------------------------------------
@@ -271,6 +429,15 @@ def to_device(arr, dtype: str):
 
 def upload_weights(cfg, weights) -> Dict[str, "object"]:
     return {k: to_device(v, cfg.dtype) for k, v in weights.items()}
+
+
+def upload_mamba_weights(cfg, weights) -> Dict[str, "object"]:
+    """Mamba tensors: the small per-channel ones (conv, dt projection, A_log, D) in fp32, the
+    rest in the workload dtype."""
+    out = {}
+    for k, v in weights.items():
+        out[k] = to_device(v, "f32" if k.rsplit(".", 1)[-1] in MAMBA_F32_FIELDS else cfg.dtype)
+    return out
 
 
 # ------------------------------------------------------------------------------------------

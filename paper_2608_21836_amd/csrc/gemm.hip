@@ -46,8 +46,12 @@ __global__ void k_repack(RepackSrc src, int n, int k, int perm, int hd, int ffn,
     }
     int s = 0;
     while (s < 2 && nlog >= src.rows[s]) nlog -= src.rows[s++];
-    const T *p = reinterpret_cast<const T *>(src.src[s]) + (size_t)nlog * k + kk;
-    *reinterpret_cast<uint4 *>(wt + c * 16) = *reinterpret_cast<const uint4 *>(p);
+    // rows past the stacked sources (padding up to n) are zero
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (src.src[s] && nlog < src.rows[s])
+      v = *reinterpret_cast<const uint4 *>(reinterpret_cast<const T *>(src.src[s]) +
+                                           (size_t)nlog * k + kk);
+    *reinterpret_cast<uint4 *>(wt + c * 16) = v;
   }
 }
 

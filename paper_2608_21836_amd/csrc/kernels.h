@@ -34,7 +34,8 @@ enum RepackPerm : int {
   kPermGlu = 2,   // unit u = gate rows [16u, 16u+16) | up rows [16u, 16u+16)
 };
 
-// Up to three row-major sources stacked along N (e.g. W_q, W_k, W_v), then permuted.
+// Up to three row-major sources stacked along N (e.g. W_q, W_k, W_v), then permuted; rows past
+// the sources (when the rows sum to less than N) are written as zeros.
 struct RepackSrc {
   const void *src[3];
   int rows[3];
@@ -178,5 +179,74 @@ hipError_t launch_attn_decode(int dtype, int head_dim, const void *q, int ldq,
                               int n_kv_heads, int max_ctx, const AttnDecodePlan &plan,
                               float *part_o, float *part_ml, hipStream_t s,
                               bool skip_merge = false);
+
+// ------------------------------------------------------------------------------------------
+// Selective state-space (Mamba) mixer
+// ------------------------------------------------------------------------------------------
+// Per layer: x (rows of the fp32 in_proj output, columns [0, di)) goes through the causal
+// depthwise convolution + SiLU (-> u), x_proj gives (dt_low | B | C) per row, and the scan
+// runs h <- exp(dt A) h + dt u B, y = C.h + D u, y * silu(z) per channel with the state in
+// registers.  Prefill splits each sequence's tokens into chunks scanned in parallel: pass 1
+// scans every chunk but the last from a zero state and keeps its end state and sum of dt,
+// pass 2 chains those per sequence into each chunk's incoming state, pass 3 rescans every
+// chunk from its incoming state and writes y.  Decode is pass 3 alone on one-token chunks.
+constexpr int kScanChannels = 64;   // channels per scan block (one wave)
+constexpr int kScanMinChunk = 16;   // shortest prefill chunk
+constexpr int kScanTargetWaves = 2048;
+constexpr int kChunkLast = 1;       // chunk flag: last chunk of its sequence in this call
+
+// Prefill metadata: cu[B+1] packed row offsets, row_seq[T], last_row[B], the chunk list
+// (seq, first row, rows, flags) in sequence order and seq_chunk0[B+1] (first chunk of each
+// sequence).
+struct MambaMeta {
+  int batch;
+  int lens[256];
+};
+hipError_t launch_mamba_meta(const MambaMeta &mm, int total, int chunk_len, int *cu,
+                             int *row_seq, int *last_row, int4 *chunks, int *seq_chunk0,
+                             hipStream_t s);
+// Chunk length of a prefill of `total` rows over `di` channels, and the largest chunk count
+// any prefill of at most `max_total` rows over `max_batch` sequences produces.
+int mamba_chunk_len(int total, int di);
+int mamba_max_chunks(int max_total, int max_batch, int di);
+
+// u[r, c] = silu(b[c] + sum_k w[c][k] * xs[i - (K-1) + k]) where xs is row r's sequence: the
+// K-1 conv-state rows (zeros when `fresh`), then this call's x rows (fp32 xz[., c]); i is
+// r's index among its sequence's rows (row_seq / cu null: row r is sequence r, index 0).
+// conv_state [batch][K-1][di] fp32 (read only here), w [di][K], b [di].
+hipError_t launch_mamba_conv(int dtype, const float *xz, int ldxz, const int *row_seq,
+                             const int *cu, const float *conv_state, int fresh,
+                             const float *w, const float *b, int rows, int di, int K, void *u,
+                             hipStream_t s);
+
+struct ScanArgs {
+  const float *xdbl = nullptr;  // [rows][ldx]: dt_low (R) | B (N) | C (N), fp32
+  int ldx = 0;
+  const void *u = nullptr;      // T [rows][di] (conv output)
+  const float *xz = nullptr;    // fp32 [rows][ldxz]: x at columns [0, di), z at [di, 2 di)
+  int ldxz = 0;
+  const float *dtwT = nullptr;  // [R][di] dt projection, transposed
+  const float *dt_b = nullptr;  // [di]
+  const float *A2 = nullptr;    // [N][di]  A * log2(e)
+  const float *D = nullptr;     // [di]
+  float *ssm = nullptr;         // [batch][N][di] SSM state of this layer
+  float *conv = nullptr;        // [batch][K-1][di] conv state of this layer
+  void *y = nullptr;            // T [rows][di] gated output
+  float *hloc = nullptr;        // [chunks][N][di] chunk end / incoming states
+  float *dtsum = nullptr;       // [chunks][di] sum of dt over each chunk
+  const int4 *chunks = nullptr; // null: decode, chunk j = row j = sequence j, one row
+  const int *seq_chunk0 = nullptr;
+  const int *cu = nullptr;      // packed row offsets (null in decode)
+  int di = 0, R = 0, N = 0, K = 0;
+  int fresh = 0;                // sequences start from zero conv and SSM state
+  int carry = 0;                // pass 3 incoming state: 0 zero, 1 SSM state, 2 hloc
+};
+// pass 1 over n_chunks chunks, pass 2 over `batch` sequences, pass 3 over n_chunks chunks
+hipError_t launch_scan_chunks(int dtype, const ScanArgs &a, int n_chunks, hipStream_t s);
+hipError_t launch_scan_carry(const ScanArgs &a, int batch, hipStream_t s);
+hipError_t launch_scan_out(int dtype, const ScanArgs &a, int n_chunks, hipStream_t s);
+// dst[j][i] = src[i][j] * scale (after exp when `neg_exp`: dst = -exp(src) * scale), fp32.
+hipError_t launch_transpose_f32(const float *src, int rows, int cols, float *dst, int neg_exp,
+                                float scale, hipStream_t s);
 
 }  // namespace ll

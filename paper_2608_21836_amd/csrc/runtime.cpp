@@ -13,9 +13,11 @@
 #include "kernels.h"
 #include "ll.h"
 #include "ll_ops.h"
+#include "runtime_common.h"
 
 namespace ll {
 thread_local LaunchTimer *g_launch_timer = nullptr;
+thread_local std::string g_err;
 }
 
 using namespace ll;
@@ -26,66 +28,6 @@ const char *const kClassNames[LL_K_COUNT] = {
     "prefill_meta", "embed",          "rmsnorm",       "qkv_rope_append",
     "attention",    "attn_combine",   "o_proj_resid",  "gate_up_swiglu",
     "down_resid",   "lm_head_argmax", "argmax_reduce"};
-
-// Collects (phase, kernel class, start, stop) for every launch while installed.
-struct Timer : LaunchTimer {
-  struct Rec {
-    int phase, cls;
-    hipEvent_t a, b;
-  };
-  std::vector<hipEvent_t> pool;
-  std::vector<Rec> recs;
-  int phase = 0, cls = 0;
-  bool next(hipEvent_t *a, hipEvent_t *b) override {
-    while (pool.size() < 2 * recs.size() + 2) {
-      hipEvent_t e;
-      if (hipEventCreate(&e) != hipSuccess) return false;
-      pool.push_back(e);
-    }
-    *a = pool[2 * recs.size()];
-    *b = pool[2 * recs.size() + 1];
-    recs.push_back({phase, cls, *a, *b});
-    return true;
-  }
-  void secondary() override {
-    if (cls == LL_K_ATTN) cls = LL_K_ATTN_COMBINE;
-  }
-  ~Timer() override {
-    for (auto e : pool) (void)hipEventDestroy(e);
-  }
-};
-
-// Installs a model's timer on this thread for the duration of one ll_* call.
-struct TimerScope {
-  LaunchTimer *saved;
-  explicit TimerScope(Timer *t, int phase) : saved(g_launch_timer) {
-    if (t) t->phase = phase;
-    g_launch_timer = t;
-  }
-  ~TimerScope() { g_launch_timer = saved; }
-};
-
-thread_local std::string g_err;
-
-ll_status fail(ll_status st, const char *fmt, ...) {
-  char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(buf, sizeof(buf), fmt, ap);
-  va_end(ap);
-  g_err = buf;
-  return st;
-}
-
-#define LL_HIP(expr)                                                                  \
-  do {                                                                                \
-    hipError_t e_ = (expr);                                                           \
-    if (e_ != hipSuccess)                                                             \
-      return fail(LL_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));         \
-  } while (0)
-
-constexpr size_t kAlign = 256;
-size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
   size_t embed = 0, final_norm = 0, lm_head = 0;
@@ -437,18 +379,11 @@ ll_status enqueue_decode(ll_model *m, const int32_t *in, int32_t *out, float *lo
   return enqueue_head(m, m->batch, nullptr, out, logits, m->at<int>(m->L.lens), s, hf_ready);
 }
 
-ll_status check_ws(const void *p) {
-  if (!p) return fail(LL_ERR_WORKSPACE, "workspace is NULL");
-  if (reinterpret_cast<uintptr_t>(p) % kAlign)
-    return fail(LL_ERR_WORKSPACE, "workspace not %zu-byte aligned", kAlign);
-  return LL_OK;
-}
-
 }  // namespace
 
 extern "C" {
 
-const char *ll_last_error(void) { return g_err.c_str(); }
+const char *ll_last_error(void) { return ll::g_err.c_str(); }
 
 ll_status ll_workspace_size(const ll_config *cfg, size_t *bytes) {
   g_err.clear();
@@ -714,7 +649,7 @@ ll_status ll_device_flags(ll_model *m, int32_t *flags) {
 ll_status ll_set_kernel_timing(ll_model *m, int32_t enable) {
   g_err.clear();
   if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
-  if (enable && !m->timer) m->timer = new Timer();
+  if (enable && !m->timer) m->timer = new Timer(LL_K_ATTN, LL_K_ATTN_COMBINE);
   if (!enable && m->timer) {
     (void)hipStreamSynchronize(m->stream);
     delete m->timer;
@@ -731,15 +666,7 @@ ll_status ll_kernel_timing_read(ll_model *m, int32_t *counts, double *ms) {
     ms[i] = 0.0;
   }
   if (!m->timer) return fail(LL_ERR_STATE, "kernel timing is not enabled");
-  LL_HIP(hipStreamSynchronize(m->stream));
-  for (const auto &r : m->timer->recs) {
-    float t = 0.f;
-    LL_HIP(hipEventElapsedTime(&t, r.a, r.b));
-    counts[r.phase * LL_K_COUNT + r.cls] += 1;
-    ms[r.phase * LL_K_COUNT + r.cls] += t;
-  }
-  m->timer->recs.clear();
-  return LL_OK;
+  return m->timer->drain(m->stream, LL_K_COUNT, counts, ms);
 }
 
 const char *ll_kernel_class_name(int32_t cls) {

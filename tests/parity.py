@@ -170,3 +170,41 @@ def rounded(arr, dtype):
     """The values a tensor of `dtype` holds (fp32 numpy)."""
     a = np.asarray(arr, dtype=np.float32)
     return gen.round_to_bf16(a) if dtype == "bf16" else a
+
+
+def run_gpu_mamba(cfg, weights, chunks, ref_tokens, n_decode, use_graph=True, options=None):
+    """A Mamba workload through the C ABI: one ll_mamba_prefill per prompt chunk (the later
+    ones continue the held state), then n_decode decode steps fed the oracle's tokens
+    (ref_tokens[len(chunks) - 1 + k] at step k).  Returns (logits [n_chunks + n_decode, B, V],
+    tokens)."""
+    import torch
+    from paper_2608_21836_amd.binding import MambaModel, upload_mamba_weights
+    B = len(chunks[0])
+    dev_w = upload_mamba_weights(cfg, weights)
+    model = MambaModel(cfg, dev_w, max_batch=B,
+                       max_prefill_tokens=max(sum(len(x) for x in c) for c in chunks))
+    del dev_w
+    model.set_option("decode_graph", 1 if use_graph else 0)
+    for name, value in (options or {}).items():
+        model.set_option(name, value)
+    logits = torch.empty(B, cfg.vocab, dtype=torch.float32, device="cuda")
+    nxt = torch.empty(B, dtype=torch.int32, device="cuda")
+    out_l, out_t = [], []
+    for c in chunks:
+        toks = torch.from_numpy(np.concatenate(c).astype(np.int32)).cuda()
+        model.prefill([len(x) for x in c], toks, nxt, logits)
+        torch.cuda.synchronize()
+        out_l.append(logits.cpu().numpy().copy())
+        out_t.append(nxt.cpu().numpy().copy())
+    inp = torch.empty(B, dtype=torch.int32, device="cuda")
+    for k in range(n_decode):
+        inp.copy_(torch.from_numpy(np.asarray(ref_tokens[len(chunks) - 1 + k], dtype=np.int32)))
+        model.decode_step(inp, nxt, logits)
+        torch.cuda.synchronize()
+        out_l.append(logits.cpu().numpy().copy())
+        out_t.append(nxt.cpu().numpy().copy())
+    total = [sum(len(c[b]) for c in chunks) for b in range(B)]
+    assert model.seq_lengths() == [t + n_decode for t in total]
+    assert model.device_flags() == 0
+    model.close()
+    return np.stack(out_l), np.stack(out_t)

@@ -258,6 +258,24 @@ def test_incremental_decode_equals_full_recompute(split):
     np.testing.assert_allclose(np.stack(got), full[split - 1:], rtol=1e-11, atol=1e-12)
 
 
+def test_chunked_prefill_equals_full_recompute():
+    """Prefill, a further chunk on the carried state, then decode: every logit equals the full
+    forward over the concatenated tokens (chunks shorter than the convolution window too)."""
+    cfg = MICRO
+    w = micro_weights(cfg)
+    rng = np.random.default_rng(12)
+    a, b = rng.integers(0, cfg.vocab, size=13), rng.integers(0, cfg.vocab, size=7)
+    o = M.OracleMamba(cfg, w)
+    fa, fb = o.forward_full(a), o.forward_full(b)
+    first = o.prefill([a[:5], b[:2]])
+    second = o.extend([a[5:11], b[2:3]])
+    third = o.extend([a[11:], b[3:]])
+    np.testing.assert_allclose(first, np.stack([fa[4], fb[1]]), rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(second, np.stack([fa[10], fb[2]]), rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(third, np.stack([fa[12], fb[6]]), rtol=1e-11, atol=1e-12)
+    assert o.lengths == [13, 7]
+
+
 def test_causality_and_batch_independence():
     cfg = MICRO
     w = micro_weights(cfg)
