@@ -1,16 +1,17 @@
 #!/usr/bin/env python3
-"""Benchmark of the phase-split decoder forward pass on one MI355X.
+"""Benchmark of the phase-split forward pass (decoder, or the Mamba model) on one MI355X.
 
-One step = one whole job of the workload: reset the KV cache, prefill every prompt, then run
-the workload's greedy decode steps (each a HIP graph replay with the next token fed back on
-the device).  Inputs are seeded and synthetic and already resident in HBM when timing starts.
+One step = one whole job of the workload: reset the KV cache (or the conv / SSM state),
+prefill every prompt, then run the workload's greedy decode steps (each a HIP graph replay
+with the next token fed back on the device).  Inputs are seeded and synthetic and already resident in HBM when timing starts.
 
 Printed JSON line:
   value          whole-job throughput, (prompt tokens + batch * decode steps) / job time
   prefill_tok_s  prompt tokens / prefill time; decode_tok_s = batch * decode steps / decode time
   roofline       the kernel class with the largest summed kernel time in one job: its
-                 algorithmic work (bytes for HBM-bound classes, flops for MFMA-bound ones)
-                 over its summed kernel time, against the MI355X peak
+                 algorithmic work (bytes for HBM-bound classes, flops for MFMA-bound ones,
+                 fp32 vector flops for the ALU-bound scan) over its summed kernel time,
+                 against the MI355X peak
   phase_roofline prefill flops over prefill time (vs MFMA peak), decode bytes over decode
                  time (vs HBM peak), whole phases
   kernels        every (phase, kernel class): launches, mean kernel time, achieved rate
@@ -99,12 +100,70 @@ def algorithmic_work(cfg, lens, n_decode):
     return w
 
 
+def algorithmic_work_mamba(cfg, lens, n_decode, fused):
+    """{(phase, class): (work, "flop" | "alu" | "byte")} summed over one Mamba job.  The
+    projections count MFMA flops (x_proj without its zero padding); the scan counts fp32
+    vector flops per (token, channel): 2 R for the dt projection, 11 for softplus, the skip
+    term and the gate, and 7 per state (dt A, exp, dt u B, the state FMA, the C.h FMA), 5 per
+    state in pass 1 (no output); the rest counts bytes.  With the fused decode step (fused >= 1)
+    the conv bytes belong to in_proj and the x_proj bytes to the scan step, which with fused
+    == 2 also reads the out_proj weights and adds into the residual rows."""
+    eb = 2 if cfg.dtype == "bf16" else 4
+    B, T = len(lens), sum(lens)
+    d, di, NS, R, K, V, L = (cfg.d_model, cfg.d_inner, cfg.d_state, cfg.dt_rank, cfg.d_conv,
+                             cfg.vocab, cfg.n_layers)
+    X = R + 2 * NS
+    N = n_decode
+    params = di * (R + NS + 3 + K) * 4          # dt_w, A, dt_b, D, conv_b, conv_w (fp32)
+    w = {}
+    w[("prefill", "in_proj")] = (2.0 * T * 2 * di * d * L, "flop")
+    w[("prefill", "x_proj")] = (2.0 * T * X * di * L, "flop")
+    w[("prefill", "out_proj_resid")] = (2.0 * T * d * di * L, "flop")
+    w[("prefill", "conv_silu")] = (float(L * (T * di * (4 + eb) + params)), "byte")
+    w[("prefill", "scan")] = (float(L * T * di * (2 * R + 11 + 7 * NS)), "alu")
+    w[("prefill", "scan_chunk")] = (float(L * T * di * (2 * R + 5 + 5 * NS)), "alu")
+    w[("prefill", "lm_head_argmax")] = (float(V * d * eb + B * d * eb + B * (V // 32) * 8), "byte")
+    w[("prefill", "rmsnorm")] = (float((L * T + B) * d * (4 + eb)), "byte")
+    w[("prefill", "embed")] = (float(T * d * (eb + 4)), "byte")
+    w[("decode", "in_proj")] = (float(N * L * (2 * di * d * eb + B * d * 4 + B * 2 * di * 4)), "byte")
+    w[("decode", "conv_silu")] = (float(N * L * (B * di * (4 + eb + (K - 1) * 4) + di * (K + 1) * 4)), "byte")
+    w[("decode", "x_proj")] = (float(N * L * (X * di * eb + B * di * eb + B * X * 4)), "byte")
+    w[("decode", "scan")] = (float(N * L * (2 * B * NS * di * 4 + B * (K - 1) * di * 4 + params
+                                            + B * (di * (2 * eb + 8) + X * 4))), "byte")
+    w[("decode", "out_proj_resid")] = (float(N * L * (d * di * eb + B * di * eb + 2 * B * d * 4)), "byte")
+    if fused:
+        del w[("decode", "conv_silu")], w[("decode", "x_proj")]
+        # in_proj: weights, x rows, u and z out, conv state read and written, conv taps
+        w[("decode", "in_proj")] = (float(N * L * (2 * di * d * eb + B * d * 4 + B * di * (eb + 4)
+                                                   + 2 * B * (K - 1) * di * 4 + di * (K + 1) * 4)),
+                                    "byte")
+        # scan step: x_proj weights, u and z in, y out, SSM state read and written, dt / A / D
+        w[("decode", "scan")] = (float(N * L * (X * di * eb + B * di * (2 * eb + 4)
+                                                + 2 * B * NS * di * 4 + di * (R + NS + 2) * 4)),
+                                 "byte")
+    if fused == 2:
+        # out_proj inside the scan step: its weights and the residual rows, not y
+        op = w.pop(("decode", "out_proj_resid"))[0]
+        w[("decode", "scan")] = (w[("decode", "scan")][0] + op - N * L * 2 * B * di * eb, "byte")
+    w[("decode", "lm_head_argmax")] = (float(N * (V * d * eb + B * d * eb + B * (V // 32) * 8)), "byte")
+    w[("decode", "rmsnorm")] = (float(N * (L + 1) * B * d * (4 + eb)), "byte")
+    w[("decode", "embed")] = (float(N * B * d * (eb + 4)), "byte")
+    return w
+
+
+# fp32 vector peak of the chip: 256 CUs x 128 fp32 FMA lanes x 2 flops x 2.4 GHz
+ALU_PEAK_TFLOPS = 157.3
+
+
 def rate(work, unit, ms, dtype):
     if ms <= 0:
         return None
     if unit == "flop":
         a = work / (ms / 1e3) / 1e12
         return a, MFMA_PEAK_TFLOPS[dtype], "TFLOP/s", "mfma"
+    if unit == "alu":
+        a = work / (ms / 1e3) / 1e12
+        return a, ALU_PEAK_TFLOPS, "TFLOP/s", "alu"
     a = work / (ms / 1e3) / 1e9
     return a, HBM_PEAK_GBS, "GB/s", "hbm"
 
@@ -154,12 +213,38 @@ def cpu_baseline(cfg, lens, packed, n_decode, budget_s):
             "decode_tok_s": round(len(prompts) * steps / t_dec, 3) if steps else None}
 
 
+def cpu_baseline_mamba(cfg, lens, packed, n_decode, budget_s):
+    """The Mamba oracle on the host, as cpu_baseline does for the decoder."""
+    from oracle import argmax_lowest, split_prompts
+    from oracle.mamba import OracleMamba
+    from synth import mamba as SM
+    om = OracleMamba(cfg, SM.weights(cfg))
+    prompts = split_prompts(lens, packed)
+    t0 = time.perf_counter()
+    toks = argmax_lowest(om.prefill(prompts))
+    t_pre = time.perf_counter() - t0
+    steps = 0
+    t1 = time.perf_counter()
+    while steps < n_decode and (time.perf_counter() - t0) < budget_s:
+        toks = argmax_lowest(om.decode(toks))
+        steps += 1
+    t_dec = time.perf_counter() - t1
+    n_pre = sum(len(p) for p in prompts)
+    return {"value": round((n_pre + len(prompts) * steps) / (t_pre + t_dec), 3), "unit": "tok/s",
+            "cores": blas_threads(), "kind": "oracle",
+            "sample": f"all prompts prefilled ({n_pre} tokens, sequential scan, {t_pre:.2f} s), "
+                      f"then {steps} of {n_decode} greedy decode steps ({t_dec:.2f} s); fp64 numpy",
+            "prefill_tok_s": round(n_pre / t_pre, 3),
+            "decode_tok_s": round(len(prompts) * steps / t_dec, 3) if steps else None}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="125m", help="workload name (synth.configs)")
+    ap.add_argument("--config", default="125m",
+                    help="workload name (synth.configs, or a Mamba workload of synth.mamba)")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
@@ -168,6 +253,9 @@ def main() -> int:
     ap.add_argument("--no-accepted-options", action="store_true",
                     help="run the library defaults instead of the implementation options the "
                          "tuner accepted for this workload (Eq. 3)")
+    ap.add_argument("--option", action="append", default=[], metavar="NAME=VALUE",
+                    help="set an implementation option after loading (repeatable; applied "
+                         "after the accepted ones)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 256 MiB device copy kernel (reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters of a rocprofv3 --pmc run)")
@@ -179,24 +267,51 @@ def main() -> int:
 
     import numpy as np
     import torch
-    from paper_2608_21836_amd.binding import Model, to_device
     from synth import gen, get_config
+    from synth import mamba as SM
 
-    cfg = get_config(args.config)
+    torch.cuda.set_device(0)
+    mamba = args.config in SM.MAMBA_CONFIGS or args.config in SM.MAMBA_TEST_CONFIGS
+    cfg = SM.get_mamba_config(args.config) if mamba else get_config(args.config)
     lens, packed = gen.prompt_tokens(cfg)
     B, T, N = len(lens), int(sum(lens)), cfg.n_decode
-    torch.cuda.set_device(0)
     print(f"[bench] {cfg.name}: uploading weights", file=sys.stderr, flush=True)
-    workers = max(1, min(16, len(os.sched_getaffinity(0))))
-    dev_w = {name: to_device(arr, cfg.dtype) for name, arr in gen.iter_weights_parallel(cfg, workers)}
-    dev_w.update({k: to_device(v, cfg.dtype) for k, v in gen.gains(cfg).items()})
-    model = Model(cfg, dev_w, max_batch=B, max_prefill_tokens=T, max_ctx=max(lens) + N)
-    from paper_2608_21836_amd.tuner import accepted_options
-    options = {} if args.no_accepted_options else accepted_options(cfg.name)
-    for name, value in options.items():
-        model.set_option(name, value)
-    if args.no_graph:
-        model.set_decode_graph(False)
+    if mamba:
+        from paper_2608_21836_amd.binding import MambaModel, upload_mamba_weights
+        dev_w = upload_mamba_weights(cfg, SM.weights(cfg))
+        model = MambaModel(cfg, dev_w, max_batch=B, max_prefill_tokens=T)
+        reset = model.reset
+        from paper_2608_21836_amd.tuner import accepted_options
+        options = {} if args.no_accepted_options else accepted_options(cfg.name)
+        options.update(dict(o.split("=", 1) for o in args.option))
+        for name, value in options.items():
+            model.set_option(name, int(value))
+        fused = model.get_option("decode_fused") if B <= 4 else 0
+        work_all = algorithmic_work_mamba(cfg, lens, N, fused)
+        desc = {"workload": cfg.name, "family": "mamba", "layers": cfg.n_layers,
+                "d_model": cfg.d_model, "d_inner": cfg.d_inner, "d_state": cfg.d_state,
+                "d_conv": cfg.d_conv, "dt_rank": cfg.dt_rank, "vocab": cfg.vocab}
+        if args.no_graph:
+            model.set_option("decode_graph", 0)
+    else:
+        from paper_2608_21836_amd.binding import Model, to_device
+        workers = max(1, min(16, len(os.sched_getaffinity(0))))
+        dev_w = {name: to_device(arr, cfg.dtype)
+                 for name, arr in gen.iter_weights_parallel(cfg, workers)}
+        dev_w.update({k: to_device(v, cfg.dtype) for k, v in gen.gains(cfg).items()})
+        model = Model(cfg, dev_w, max_batch=B, max_prefill_tokens=T, max_ctx=max(lens) + N)
+        reset = model.kv_reset
+        work_all = algorithmic_work(cfg, lens, N)
+        desc = {"workload": cfg.name, "layers": cfg.n_layers, "d_model": cfg.d_model,
+                "heads": f"{cfg.n_heads}/{cfg.n_kv_heads}x{cfg.head_dim}", "ffn": cfg.ffn_dim,
+                "vocab": cfg.vocab}
+        from paper_2608_21836_amd.tuner import accepted_options
+        options = {} if args.no_accepted_options else accepted_options(cfg.name)
+        options.update(dict(o.split("=", 1) for o in args.option))
+        for name, value in options.items():
+            model.set_option(name, int(value))
+        if args.no_graph:
+            model.set_decode_graph(False)
     torch.cuda.synchronize()
     del dev_w
     torch.cuda.empty_cache()
@@ -214,7 +329,7 @@ def main() -> int:
     acc = {"pre": 0.0, "dec": 0.0}
 
     def job(record: bool):
-        model.kv_reset()
+        reset()
         if record:
             ev[0].record()
         model.prefill(lens, tokens, nxt)
@@ -243,34 +358,32 @@ def main() -> int:
     for _ in range(3):
         job(True)
     pre_ms, dec_ms = acc["pre"] / 3, acc["dec"] / 3
+    desc.update({"batch": B, "prompt_tokens": T, "decode_steps": N, "options": model.options()})
     out = {
         "metric": METRIC, "value": round((T + B * N) / (ms_per_step / 1e3), 3), "unit": "tok/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic (seeded weights and prompts)",
-        "config": {"workload": cfg.name, "layers": cfg.n_layers, "d_model": cfg.d_model,
-                   "heads": f"{cfg.n_heads}/{cfg.n_kv_heads}x{cfg.head_dim}", "ffn": cfg.ffn_dim,
-                   "vocab": cfg.vocab, "batch": B, "prompt_tokens": T, "decode_steps": N,
-                   "options": model.options()},
+        "config": desc,
         "prefill_ms": round(pre_ms, 4), "decode_ms_per_step": round(dec_ms / N, 5),
         "prefill_tok_s": round(T / (pre_ms / 1e3), 1),
         "decode_tok_s": round(B * N / (dec_ms / 1e3), 1),
     }
 
     # Whole-phase rates: the phase's summed algorithmic work over its measured time
-    # (prefill: flops of the GEMMs and causal attention; decode: bytes per step).
-    work_all = algorithmic_work(cfg, lens, N)
+    # (prefill: MFMA flops of the GEMMs and causal attention; decode: bytes per step).
     pre_flop = sum(v for (ph, _), (v, u) in work_all.items() if ph == "prefill" and u == "flop")
     dec_byte = sum(v for (ph, _), (v, u) in work_all.items() if ph == "decode" and u == "byte")
     out["phase_roofline"] = {
         "prefill": {"achieved": round(pre_flop / (pre_ms / 1e3) / 1e12, 2), "unit": "TFLOP/s",
                     "peak": MFMA_PEAK_TFLOPS[cfg.dtype],
                     "frac": round(pre_flop / (pre_ms / 1e3) / 1e12 / MFMA_PEAK_TFLOPS[cfg.dtype], 4),
-                    "work": "GEMM + causal attention flops"},
+                    "work": "MFMA flops (projections" + ("" if mamba else " + causal attention") + ")"},
         "decode": {"achieved": round(dec_byte / (dec_ms / 1e3) / 1e9, 2), "unit": "GB/s",
                    "peak": HBM_PEAK_GBS,
                    "frac": round(dec_byte / (dec_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
-                   "work": "weights, KV cache, activations per step"},
+                   "work": "weights, " + ("conv and SSM state" if mamba else "KV cache")
+                           + ", activations per step"},
     }
 
     if not args.no_kernel_timing:
@@ -279,19 +392,18 @@ def main() -> int:
         job(False)
         kt = model.kernel_timing()
         model.set_kernel_timing(False)
-        work = algorithmic_work(cfg, lens, N)
         rows = []
         for (phase, cls), (cnt, ms) in sorted(kt.items(), key=lambda kv: -kv[1][1]):
             r = {"phase": phase, "class": cls, "launches": cnt, "total_ms": round(ms, 4),
                  "avg_us": round(ms / cnt * 1e3, 3)}
-            if (phase, cls) in work:
-                wv, unit = work[(phase, cls)]
+            if (phase, cls) in work_all:
+                wv, unit = work_all[(phase, cls)]
                 a, peak, u, bound = rate(wv, unit, ms, cfg.dtype)
                 r.update({"achieved": round(a, 2), "unit": u, "frac": round(a / peak, 4)})
             rows.append(r)
         out["kernels"] = rows
         dom = next(r for r in rows if "achieved" in r)
-        wv, unit = work[(dom["phase"], dom["class"])]
+        wv, unit = work_all[(dom["phase"], dom["class"])]
         a, peak, u, bound = rate(wv, unit, dom["total_ms"], cfg.dtype)
         traffic = measured_traffic(cfg.name, f"{dom['phase']}:{dom['class']}")
         out["roofline"] = {"bound": bound, "achieved": round(a, 2), "peak": peak, "unit": u,
@@ -308,7 +420,8 @@ def main() -> int:
 
     if not args.no_cpu_baseline:
         print("[bench] oracle cpu baseline", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(cfg, lens, packed, N, args.cpu_budget)
+        fn = cpu_baseline_mamba if mamba else cpu_baseline
+        out["cpu_baseline"] = fn(cfg, lens, packed, N, args.cpu_budget)
     model.close()
     print(json.dumps(out), flush=True)
     return 0

@@ -144,7 +144,14 @@ typedef enum {
   LL_OPT_ATTN_DECODE_CHUNK = 4,/* 0 (default): cached keys per decode-attention block from the
                                   load-time plan; 64, 128 or 256 override it (not below the plan's
                                   value: the workspace holds the plan's number of splits) */
-  LL_OPT_COUNT = 5
+  LL_OPT_DECODE_FUSED = 5,     /* Mamba model only (ll_mamba.h): 1 (default): a decode step of at
+                                  most 4 sequences runs the conv step in the in_proj epilogue and
+                                  x_proj inside the scan-step kernel; 2: as 1, and out_proj with
+                                  the residual add inside the scan step too, its 32-channel
+                                  shares added with fp32 atomics (the summation order, hence the
+                                  last bits, can differ between runs); 0: separate conv, x_proj
+                                  and scan kernels.  The decoder rejects it (LL_ERR_UNSUPPORTED) */
+  LL_OPT_COUNT = 6
 } ll_option;
 
 /* Set / read an option.  LL_ERR_INVALID_ARGUMENT for an unknown option or value,

@@ -28,7 +28,7 @@ extern "C" {
 
 typedef struct ll_mamba ll_mamba; /* opaque, library-owned host object */
 
-/* Model shape and capacity.  Supported: d_state = 16; d_conv in [1, 4]; dt_rank in [1, 256];
+/* Model shape and capacity.  Supported: d_state = 16; d_conv in [1, 4]; dt_rank in [1, 160];
  * d_model a multiple of 128; d_inner a multiple of 64; vocab a multiple of 32;
  * max_batch <= LL_MAX_BATCH.  There is no context limit: the state has a fixed size. */
 typedef struct {
@@ -90,8 +90,9 @@ ll_status ll_mamba_reset(ll_mamba *m);
 ll_status ll_mamba_seq_lengths(const ll_mamba *m, int32_t *out, int32_t cap, int32_t *n);
 
 /* Options (ids of ll_option in ll.h): LL_OPT_DECODE_GRAPH, LL_OPT_PREFILL_SPLITK,
- * LL_OPT_DECODE_SPLITK and LL_OPT_PREFILL_TILE, with the values ll.h documents; the others
- * give LL_ERR_UNSUPPORTED.  Changing one drops captured decode graphs. */
+ * LL_OPT_DECODE_SPLITK, LL_OPT_PREFILL_TILE and LL_OPT_DECODE_FUSED, with the values ll.h
+ * documents; LL_OPT_ATTN_DECODE_CHUNK gives LL_ERR_UNSUPPORTED.  Changing one drops captured
+ * decode graphs. */
 ll_status ll_mamba_set_option(ll_mamba *m, int32_t option, int32_t value);
 ll_status ll_mamba_get_option(const ll_mamba *m, int32_t option, int32_t *value);
 
@@ -104,12 +105,13 @@ typedef enum {
   LL_MK_META = 0,       /* prefill metadata (offsets, chunk list) */
   LL_MK_EMBED = 1,      /* embedding gather */
   LL_MK_RMSNORM = 2,    /* RMSNorm kernel (decode batches <= 16 normalise inside the GEMM) */
-  LL_MK_IN_PROJ = 3,    /* in_proj GEMM -> xc | z */
+  LL_MK_IN_PROJ = 3,    /* in_proj GEMM -> xc | z (fused decode: + the conv step and SiLU) */
   LL_MK_CONV = 4,       /* causal depthwise conv + SiLU */
   LL_MK_X_PROJ = 5,     /* x_proj GEMM -> dt_low | B | C */
   LL_MK_SCAN_CHUNK = 6, /* prefill scan pass 1: chunk end states */
   LL_MK_SCAN_CARRY = 7, /* prefill scan pass 2: incoming state of each chunk */
-  LL_MK_SCAN = 8,       /* scan with output and state update (pass 3; the decode step) */
+  LL_MK_SCAN = 8,       /* scan with output and state update (pass 3; the decode step, which
+                           in the fused decode also forms x_proj) */
   LL_MK_OUT_PROJ = 9,   /* out_proj GEMM + residual add */
   LL_MK_LM_HEAD = 10,   /* LM head + per-block argmax partials */
   LL_MK_ARGMAX = 11,    /* argmax reduction */

@@ -22,7 +22,10 @@ LL_MAX_BATCH = 256
 LL_K_COUNT = 11
 # ll_option ids (include/ll.h)
 OPTIONS = {"decode_graph": 0, "prefill_splitk": 1, "decode_splitk": 2, "prefill_tile": 3,
-           "attn_decode_chunk": 4}
+           "attn_decode_chunk": 4, "decode_fused": 5}
+DECODER_OPTIONS = ("decode_graph", "prefill_splitk", "decode_splitk", "prefill_tile",
+                   "attn_decode_chunk")
+MAMBA_OPTIONS = ("decode_graph", "prefill_splitk", "decode_splitk", "prefill_tile", "decode_fused")
 PHASES = ("prefill", "decode")
 
 
@@ -259,7 +262,7 @@ class Model:
         return v.value
 
     def options(self) -> Dict[str, int]:
-        return {k: self.get_option(k) for k in OPTIONS}
+        return {k: self.get_option(k) for k in DECODER_OPTIONS}
 
     def seq_lengths(self) -> List[int]:
         out = (c_int32 * LL_MAX_BATCH)()
@@ -379,7 +382,7 @@ class MambaModel:
         return v.value
 
     def options(self) -> Dict[str, int]:
-        return {k: self.get_option(k) for k in OPTIONS if k != "attn_decode_chunk"}
+        return {k: self.get_option(k) for k in MAMBA_OPTIONS}
 
     def seq_lengths(self) -> List[int]:
         out = (c_int32 * LL_MAX_BATCH)()

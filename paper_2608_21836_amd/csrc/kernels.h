@@ -50,6 +50,8 @@ enum EpiKind : int {
   kEpiSwiglu = 2,  // act[m, j] = silu(gate) * up   (kPermGlu weights)
   kEpiQkv = 3,     // RoPE on q, k; q -> act, k / v -> KV cache  (kPermRope weights)
   kEpiArgmax = 4,  // logits (optional) + per-32-column (max, argmax) partials
+  kEpiConv = 5,    // Mamba decode in_proj: x columns -> conv step + SiLU -> act (u, ld_act =
+                   // d_inner), conv state shifted; z columns -> out_f32 [rows][d_inner]
 };
 
 struct EpiParams {
@@ -68,6 +70,10 @@ struct EpiParams {
   float *part_val = nullptr;
   int *part_idx = nullptr;
   int n_parts = 0;  // partials per row (= N / 32)
+  // Conv (row = sequence): conv_state [rows][K-1][d_inner], taps [d_inner][K], bias [d_inner]
+  float *conv_state = nullptr;
+  const float *conv_w = nullptr, *conv_b = nullptr;
+  int conv_k = 0;
 };
 
 // RMSNorm computed inside the decode GEMM (A = RMSNorm(x[rowmap[r]]) * gain).
@@ -225,11 +231,12 @@ struct ScanArgs {
   const void *u = nullptr;      // T [rows][di] (conv output)
   const float *xz = nullptr;    // fp32 [rows][ldxz]: x at columns [0, di), z at [di, 2 di)
   int ldxz = 0;
-  const float *dtwT = nullptr;  // [R][di] dt projection, transposed
+  const float *dtwT = nullptr;  // [R16][di] dt projection, transposed, rows >= R zero
+                                //   (R16 = R rounded up to a multiple of 16)
   const float *dt_b = nullptr;  // [di]
   const float *A2 = nullptr;    // [N][di]  A * log2(e)
   const float *D = nullptr;     // [di]
-  float *ssm = nullptr;         // [batch][N][di] SSM state of this layer
+  float *ssm = nullptr;         // [batch][di][N] SSM state of this layer
   float *conv = nullptr;        // [batch][K-1][di] conv state of this layer
   void *y = nullptr;            // T [rows][di] gated output
   float *hloc = nullptr;        // [chunks][N][di] chunk end / incoming states
@@ -245,8 +252,34 @@ struct ScanArgs {
 hipError_t launch_scan_chunks(int dtype, const ScanArgs &a, int n_chunks, hipStream_t s);
 hipError_t launch_scan_carry(const ScanArgs &a, int batch, hipStream_t s);
 hipError_t launch_scan_out(int dtype, const ScanArgs &a, int n_chunks, hipStream_t s);
-// dst[j][i] = src[i][j] * scale (after exp when `neg_exp`: dst = -exp(src) * scale), fp32.
-hipError_t launch_transpose_f32(const float *src, int rows, int cols, float *dst, int neg_exp,
-                                float scale, hipStream_t s);
+// One fused decode step of the mixer for rows <= kSsmDecodeMaxRows sequences (row = sequence)
+// and X = R + 2 N <= kSsmDecodeMaxX: x_proj of the conv output u (wx = the repacked x_proj,
+// rows zero-padded to a multiple of 128) for every row, then per
+// channel the dt projection, softplus, the state update h <- exp(dt A) h + dt u B (ssm state
+// [rows][di][N] read and written), y = C.h + D u, y * silu(z), and optionally out_proj with
+// the residual add.  One block per 32 channels; each block forms the whole x_proj product of
+// its rows (from L2) so that no second launch is needed.
+constexpr int kSsmDecodeMaxRows = 4;
+constexpr int kSsmDecodeMaxX = 128;
+struct SsmDecodeArgs {
+  const void *u = nullptr;     // T [rows][di]
+  const float *z = nullptr;    // fp32 [rows][di]
+  const void *wx = nullptr;    // repacked x_proj (ll_op_repack layout), >= 128 rows
+  const float *dtwT = nullptr, *dt_b = nullptr, *A2 = nullptr, *D = nullptr;
+  float *ssm = nullptr;        // [rows][di][N]
+  void *y = nullptr;           // T [rows][di] gated output (when wout is null)
+  int rows = 0, di = 0, R = 0, N = 0;
+  // With wout (the repacked out_proj [d][di]): x[r][0, d) += out_proj(y) instead of writing y,
+  // each block adding its 32-channel share with fp32 atomics (summation order not fixed).
+  const void *wout = nullptr;
+  float *x = nullptr;
+  int ldx = 0, d = 0;
+};
+hipError_t launch_ssm_decode(int dtype, const SsmDecodeArgs &a, hipStream_t s);
+
+// dst[j][i] = src[i][j] * scale (after exp when `neg_exp`: dst = -exp(src) * scale) for
+// j < cols, zero rows for cols <= j < cols_pad; fp32.
+hipError_t launch_transpose_f32(const float *src, int rows, int cols, int cols_pad, float *dst,
+                                int neg_exp, float scale, hipStream_t s);
 
 }  // namespace ll

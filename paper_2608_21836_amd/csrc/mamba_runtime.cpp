@@ -27,7 +27,7 @@ constexpr int kFusedNormMaxRows = 16;
 struct MLayout {
   size_t embed = 0, lm_head = 0, final_norm = 0;
   std::vector<size_t> norm, w_in, w_x, w_out, conv_w, conv_b, dtwT, dt_b, A2, D;
-  size_t conv_state = 0, ssm_state = 0;  // [L][max_batch][K-1][di], [L][max_batch][N][di]
+  size_t conv_state = 0, ssm_state = 0;  // [L][max_batch][K-1][di], [L][max_batch][di][N]
   size_t x = 0, h = 0, xz = 0, u = 0, xdbl = 0, y = 0, hf = 0;
   size_t hloc = 0, dtsum = 0, chunks = 0, seq_chunk0 = 0;
   size_t splitk = 0, splitk_bytes = 0;
@@ -49,7 +49,7 @@ ll_status validate(const ll_mamba_config *c) {
     return fail(LL_ERR_UNSUPPORTED, "dtype %d unknown", c->dtype);
   if (c->d_state != kDState) return fail(LL_ERR_UNSUPPORTED, "d_state %d != 16", c->d_state);
   if (c->d_conv > 4) return fail(LL_ERR_UNSUPPORTED, "d_conv %d > 4", c->d_conv);
-  if (c->dt_rank > 256) return fail(LL_ERR_UNSUPPORTED, "dt_rank %d > 256", c->dt_rank);
+  if (c->dt_rank > 160) return fail(LL_ERR_UNSUPPORTED, "dt_rank %d > 160", c->dt_rank);
   if (c->d_model % 128) return fail(LL_ERR_UNSUPPORTED, "d_model %d not a multiple of 128", c->d_model);
   if (c->d_inner % 64) return fail(LL_ERR_UNSUPPORTED, "d_inner %d not a multiple of 64", c->d_inner);
   if (c->vocab % 32) return fail(LL_ERR_UNSUPPORTED, "vocab %d not a multiple of 32", c->vocab);
@@ -82,7 +82,7 @@ MLayout make_layout(const ll_mamba_config &c) {
     L.w_out.push_back(take(d * di * eb));
     L.conv_w.push_back(take(di * c.d_conv * 4));
     L.conv_b.push_back(take(di * 4));
-    L.dtwT.push_back(take((size_t)c.dt_rank * di * 4));
+    L.dtwT.push_back(take((size_t)((c.dt_rank + 15) / 16 * 16) * di * 4));  // rows padded to 16
     L.dt_b.push_back(take(di * 4));
     L.A2.push_back(take(N * di * 4));
     L.D.push_back(take(di * 4));
@@ -133,7 +133,7 @@ struct ll_mamba {
   hipStream_t cap_stream = nullptr;
   int batch = 0;
   std::vector<int> lens;
-  int opt[LL_OPT_COUNT] = {1, 1, 1, 0, 0};
+  int opt[LL_OPT_COUNT] = {1, 1, 1, 0, 0, 1};
   struct Graph {
     const void *in;
     void *out;
@@ -204,6 +204,12 @@ ScanArgs scan_args(const ll_mamba *m, int l) {
   return a;
 }
 
+// The fused decode step takes up to kSsmDecodeMaxRows sequences and x_proj widths up to
+// kSsmDecodeMaxX.
+bool ssm_decode_fits(const ll_mamba_config &c, int rows) {
+  return rows <= kSsmDecodeMaxRows && c.dt_rank + 2 * c.d_state <= kSsmDecodeMaxX;
+}
+
 // Per-call prefill description (null for decode).
 struct PrefillPlan {
   int n_chunks = 0;
@@ -233,6 +239,8 @@ ll_status enqueue_layers(ll_mamba *m, int rows, const PrefillPlan *pp, hipStream
                   : launch_gemm_tiled(dt, a, lda, wt, rows, n, k, ep, s, gemm_ws, gemm_ws_bytes,
                                       m->opt[LL_OPT_PREFILL_TILE]);
   };
+  const bool fused = decode && m->opt[LL_OPT_DECODE_FUSED] && ssm_decode_fits(c, rows);
+  const bool fused_out = fused && m->opt[LL_OPT_DECODE_FUSED] == 2;
   bool h_ready = false;
   for (int l = 0; l < c.n_layers; ++l) {
     NormIn nrm;
@@ -245,39 +253,77 @@ ll_status enqueue_layers(ll_mamba *m, int rows, const PrefillPlan *pp, hipStream
     }
     h_ready = false;
     m->mark(LL_MK_IN_PROJ);
-    LL_HIP(gemm(m->at(L.h), d, fuse_norm ? &nrm : nullptr, m->at(L.w_in[l]), 2 * di, d,
-                store_epi(m->at<float>(L.xz), 2 * di)));
-    m->mark(LL_MK_CONV);
-    LL_HIP(launch_mamba_conv(dt, m->at<float>(L.xz), 2 * di,
-                             decode ? nullptr : m->at<int>(L.row_seq),
-                             decode ? nullptr : m->at<int>(L.cu), m->conv_state(l),
-                             decode ? 0 : pp->fresh, m->at<float>(L.conv_w[l]),
-                             m->at<float>(L.conv_b[l]), rows, di, c.d_conv, m->at(L.u), s));
-    m->mark(LL_MK_X_PROJ);
-    LL_HIP(gemm(m->at(L.u), di, nullptr, m->at(L.w_x[l]), L.NX, di,
-                store_epi(m->at<float>(L.xdbl), L.NX)));
-    ScanArgs a = scan_args(m, l);
-    if (decode) {
-      a.carry = 1;
-      m->mark(LL_MK_SCAN);
-      LL_HIP(launch_scan_out(dt, a, rows, s));
-    } else {
-      a.chunks = m->at<int4>(L.chunks);
-      a.seq_chunk0 = m->at<int>(L.seq_chunk0);
-      a.cu = m->at<int>(L.cu);
-      a.fresh = pp->fresh;
-      if (pp->multi) {
-        m->mark(LL_MK_SCAN_CHUNK);
-        LL_HIP(launch_scan_chunks(dt, a, pp->n_chunks, s));
-        m->mark(LL_MK_SCAN_CARRY);
-        LL_HIP(launch_scan_carry(a, pp->batch, s));
-        a.carry = 2;
+    if (fused) {
+      // conv step in the in_proj epilogue, then x_proj + dt + scan step + gate in one kernel
+      EpiParams ep;
+      ep.kind = kEpiConv;
+      ep.act = m->at(L.u);
+      ep.ld_act = di;
+      ep.out_f32 = m->at<float>(L.xz);  // z [rows][di]
+      ep.conv_state = m->conv_state(l);
+      ep.conv_w = m->at<float>(L.conv_w[l]);
+      ep.conv_b = m->at<float>(L.conv_b[l]);
+      ep.conv_k = c.d_conv;
+      LL_HIP(gemm(m->at(L.h), d, fuse_norm ? &nrm : nullptr, m->at(L.w_in[l]), 2 * di, d, ep));
+      SsmDecodeArgs sa;
+      sa.u = m->at(L.u);
+      sa.z = m->at<float>(L.xz);
+      sa.wx = m->at(L.w_x[l]);
+      sa.dtwT = m->at<float>(L.dtwT[l]);
+      sa.dt_b = m->at<float>(L.dt_b[l]);
+      sa.A2 = m->at<float>(L.A2[l]);
+      sa.D = m->at<float>(L.D[l]);
+      sa.ssm = m->ssm_state(l);
+      sa.rows = rows;
+      sa.di = di;
+      sa.R = c.dt_rank;
+      sa.N = c.d_state;
+      if (fused_out) {  // out_proj and the residual add inside the step
+        sa.wout = m->at(L.w_out[l]);
+        sa.x = x;
+        sa.ldx = d;
+        sa.d = d;
       } else {
-        a.carry = pp->fresh ? 0 : 1;
+        sa.y = m->at(L.y);
       }
       m->mark(LL_MK_SCAN);
-      LL_HIP(launch_scan_out(dt, a, pp->n_chunks, s));
+      LL_HIP(launch_ssm_decode(dt, sa, s));
+    } else {
+      LL_HIP(gemm(m->at(L.h), d, fuse_norm ? &nrm : nullptr, m->at(L.w_in[l]), 2 * di, d,
+                  store_epi(m->at<float>(L.xz), 2 * di)));
+      m->mark(LL_MK_CONV);
+      LL_HIP(launch_mamba_conv(dt, m->at<float>(L.xz), 2 * di,
+                               decode ? nullptr : m->at<int>(L.row_seq),
+                               decode ? nullptr : m->at<int>(L.cu), m->conv_state(l),
+                               decode ? 0 : pp->fresh, m->at<float>(L.conv_w[l]),
+                               m->at<float>(L.conv_b[l]), rows, di, c.d_conv, m->at(L.u), s));
+      m->mark(LL_MK_X_PROJ);
+      LL_HIP(gemm(m->at(L.u), di, nullptr, m->at(L.w_x[l]), L.NX, di,
+                  store_epi(m->at<float>(L.xdbl), L.NX)));
+      ScanArgs a = scan_args(m, l);
+      if (decode) {
+        a.carry = 1;
+        m->mark(LL_MK_SCAN);
+        LL_HIP(launch_scan_out(dt, a, rows, s));
+      } else {
+        a.chunks = m->at<int4>(L.chunks);
+        a.seq_chunk0 = m->at<int>(L.seq_chunk0);
+        a.cu = m->at<int>(L.cu);
+        a.fresh = pp->fresh;
+        if (pp->multi) {
+          m->mark(LL_MK_SCAN_CHUNK);
+          LL_HIP(launch_scan_chunks(dt, a, pp->n_chunks, s));
+          m->mark(LL_MK_SCAN_CARRY);
+          LL_HIP(launch_scan_carry(a, pp->batch, s));
+          a.carry = 2;
+        } else {
+          a.carry = pp->fresh ? 0 : 1;
+        }
+        m->mark(LL_MK_SCAN);
+        LL_HIP(launch_scan_out(dt, a, pp->n_chunks, s));
+      }
     }
+    if (fused_out) continue;  // out_proj ran inside the fused step
     m->mark(LL_MK_OUT_PROJ);
     const bool last = l + 1 == c.n_layers;
     PostNorm pn;
@@ -410,10 +456,11 @@ ll_status ll_mamba_load(const ll_mamba_config *cfg, const ll_mamba_weights *w, v
     LOAD_HIP(copy(L.conv_b[l], w->conv_b[l], (size_t)di * 4));
     LOAD_HIP(copy(L.dt_b[l], w->dt_b[l], (size_t)di * 4));
     LOAD_HIP(copy(L.D[l], w->D[l], (size_t)di * 4));
-    LOAD_HIP(launch_transpose_f32(w->dt_w[l], di, c.dt_rank, m->at<float>(L.dtwT[l]), 0, 1.f, s));
+    LOAD_HIP(launch_transpose_f32(w->dt_w[l], di, c.dt_rank, (c.dt_rank + 15) / 16 * 16,
+                                  m->at<float>(L.dtwT[l]), 0, 1.f, s));
     // A * log2(e) = -exp(A_log) * log2(e), state-major
-    LOAD_HIP(launch_transpose_f32(w->A_log[l], di, c.d_state, m->at<float>(L.A2[l]), 1,
-                                  1.4426950408889634f, s));
+    LOAD_HIP(launch_transpose_f32(w->A_log[l], di, c.d_state, c.d_state, m->at<float>(L.A2[l]),
+                                  1, 1.4426950408889634f, s));
   }
   LOAD_HIP(hipMemsetAsync(m->at(L.err), 0, 4, s));
 #undef LOAD_HIP
@@ -552,6 +599,9 @@ ll_status ll_mamba_set_option(ll_mamba *m, int32_t option, int32_t value) {
     case LL_OPT_PREFILL_TILE:
       if (value < 0 || value > 3) return fail(LL_ERR_INVALID_ARGUMENT, "prefill tile 0..3");
       break;
+    case LL_OPT_DECODE_FUSED:
+      if (value < 0 || value > 2) return fail(LL_ERR_INVALID_ARGUMENT, "option %d takes 0, 1 or 2", option);
+      break;
     case LL_OPT_ATTN_DECODE_CHUNK:
       return fail(LL_ERR_UNSUPPORTED, "option %d does not apply to this model", option);
     default:
@@ -566,6 +616,8 @@ ll_status ll_mamba_get_option(const ll_mamba *m, int32_t option, int32_t *value)
   g_err.clear();
   if (!m || !value) return fail(LL_ERR_INVALID_ARGUMENT, "NULL argument");
   if (option < 0 || option >= LL_OPT_COUNT) return fail(LL_ERR_INVALID_ARGUMENT, "unknown option %d", option);
+  if (option == LL_OPT_ATTN_DECODE_CHUNK)
+    return fail(LL_ERR_UNSUPPORTED, "option %d does not apply to this model", option);
   *value = m->opt[option];
   return LL_OK;
 }

@@ -161,7 +161,7 @@ struct ll_model {
   int batch = 0;
   std::vector<int> lens;
   bool use_graph = true;
-  int opt[LL_OPT_COUNT] = {1, 1, 1, 0, 0};  // ll_option values (LL_OPT_DECODE_GRAPH mirrors use_graph)
+  int opt[LL_OPT_COUNT] = {1, 1, 1, 0, 0, 0};  // ll_option values (LL_OPT_DECODE_GRAPH mirrors use_graph)
   struct Graph {
     const void *in;
     void *out;
@@ -621,6 +621,8 @@ ll_status ll_set_option(ll_model *m, int32_t option, int32_t value) {
         return fail(LL_ERR_UNSUPPORTED, "chunk %d below the load-time plan's %d (the workspace "
                     "holds %d splits)", value, m->L.attn.kpb, m->L.attn.nsplit);
       break;
+    case LL_OPT_DECODE_FUSED:
+      return fail(LL_ERR_UNSUPPORTED, "option %d applies to the Mamba model only", option);
     default:
       return fail(LL_ERR_INVALID_ARGUMENT, "unknown option %d", option);
   }
@@ -634,6 +636,8 @@ ll_status ll_get_option(const ll_model *m, int32_t option, int32_t *value) {
   g_err.clear();
   if (!m || !value) return fail(LL_ERR_INVALID_ARGUMENT, "NULL argument");
   if (option < 0 || option >= LL_OPT_COUNT) return fail(LL_ERR_INVALID_ARGUMENT, "unknown option %d", option);
+  if (option == LL_OPT_DECODE_FUSED)
+    return fail(LL_ERR_UNSUPPORTED, "option %d applies to the Mamba model only", option);
   *value = m->opt[option];
   return LL_OK;
 }

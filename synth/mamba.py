@@ -87,6 +87,17 @@ MAMBA_TEST_CONFIGS: Dict[str, MambaConfig] = {
         name="t-mamba-f32", seed=32, dtype="f32", n_layers=2, d_model=128, d_inner=256,
         d_state=16, d_conv=4, dt_rank=8, vocab=512, batch=2, prompt_list=(19, 66),
         n_decode=4),
+    # dt rank above 64 (x_proj width 112) and prompts long enough for scan chunks of several
+    # 16-step stages
+    "t-mamba-wide": MambaConfig(
+        name="t-mamba-wide", seed=35, dtype="bf16", n_layers=2, d_model=256, d_inner=512,
+        d_state=16, d_conv=4, dt_rank=80, vocab=1024, batch=2, prompt_list=(3000, 2500),
+        n_decode=3),
+    # 20 ragged prompts: decode above the fused-step and skinny-GEMM row limits (split-K)
+    "t-mamba-b20": MambaConfig(
+        name="t-mamba-b20", seed=34, dtype="bf16", n_layers=2, d_model=256, d_inner=512,
+        d_state=16, d_conv=4, dt_rank=16, vocab=1024, batch=20, prompt_range=(1, 48),
+        n_decode=3),
 }
 
 

@@ -35,8 +35,15 @@ def _report(name, dtype, ref_l, gl, gt):
     return rep
 
 
-CASES = [("t-mamba", True, None), ("t-mamba", False, None), ("t-mamba-f32", True, None),
-         ("t-mamba-f32", False, None), ("t-mamba-long", True, None), ("mamba-130m", True, 16)]
+# (workload, graph replay, decode steps (None: the workload's), options)
+CASES = [("t-mamba", True, None, {}), ("t-mamba", False, None, {"decode_fused": 0}),
+         ("t-mamba-f32", True, None, {}), ("t-mamba-f32", False, None, {"decode_fused": 0}),
+         ("t-mamba-long", True, None, {}), ("t-mamba-b20", True, None, {}),
+         ("t-mamba-b20", False, None, {"decode_splitk": 0, "prefill_splitk": 0}),
+         ("t-mamba", True, None, {"decode_fused": 2}), ("t-mamba-f32", True, None, {"decode_fused": 2}),
+         ("t-mamba-wide", True, None, {}), ("t-mamba-wide", True, None, {"decode_fused": 2}),
+         ("mamba-130m", True, 16, {}), ("mamba-130m", True, 16, {"decode_fused": 0}),
+         ("mamba-130m", True, 16, {"decode_fused": 2})]
 
 
 def _config(name):
@@ -46,9 +53,10 @@ def _config(name):
     return SM.get_mamba_config(name)
 
 
-@pytest.mark.parametrize("name,graph,n_decode", CASES,
-                         ids=[f"{c[0]}-{'graph' if c[1] else 'direct'}" for c in CASES])
-def test_mamba_workload_parity(name, graph, n_decode):
+@pytest.mark.parametrize("name,graph,n_decode,options", CASES,
+                         ids=[f"{c[0]}-{'graph' if c[1] else 'direct'}"
+                              + "".join(f"-{k}{v}" for k, v in c[3].items()) for c in CASES])
+def test_mamba_workload_parity(name, graph, n_decode, options):
     cfg = _config(name)
     nd = n_decode if n_decode is not None else cfg.n_decode
     log(f"mamba parity {name}: oracle ...")
@@ -56,7 +64,8 @@ def test_mamba_workload_parity(name, graph, n_decode):
     lens, packed = gen.prompt_tokens(cfg)
     ref_l, ref_t = teacher_forced_run_mamba(OracleMamba(cfg, w), lens, packed, nd)
     log(f"mamba parity {name}: gpu ...")
-    gl, gt = run_gpu_mamba(cfg, w, [split_prompts(lens, packed)], ref_t, nd, use_graph=graph)
+    gl, gt = run_gpu_mamba(cfg, w, [split_prompts(lens, packed)], ref_t, nd, use_graph=graph,
+                           options=options)
     rep = _report(name, cfg.dtype, ref_l, gl, gt)
     assert rep.ok(cfg.dtype), rep
 
