@@ -371,6 +371,8 @@ class MambaModel:
         _check(self.lib.ll_mamba_reset(self.handle), "ll_mamba_reset")
         self.batch = 0
 
+    kv_reset = reset  # same call name as the decoder's (forget every held sequence)
+
     def set_option(self, name: str, value: int) -> None:
         _check(self.lib.ll_mamba_set_option(self.handle, OPTIONS[name], int(value)),
                "ll_mamba_set_option")

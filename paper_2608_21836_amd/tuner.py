@@ -23,6 +23,7 @@ workload as the bench runs it: KV reset, prefill of every prompt, free-running g
 steps, timed with stream events.
 
   python -m paper_2608_21836_amd.tuner --config 125m [--delta 0.01] [--write]
+  (a Mamba workload name, e.g. mamba-130m, tunes that model's options)
 
 With --write the accepted (non-default) option values of the workload are stored in
 accepted_options.json next to this module; bench.py applies them to that workload, as the
@@ -63,6 +64,17 @@ KNOBS: List[Tuple[str, Tuple[int, ...], Tuple[str, ...]]] = [
     ("decode_graph", (1, 0), ("qkv_rope_append", "attention", "attn_combine", "o_proj_resid",
                               "gate_up_swiglu", "down_resid", "lm_head_argmax", "embed",
                               "argmax_reduce", "rmsnorm")),
+]
+
+
+# The same for the Mamba model (include/ll_mamba.h kernel classes).
+MAMBA_KNOBS: List[Tuple[str, Tuple[int, ...], Tuple[str, ...]]] = [
+    ("decode_fused", (1, 0, 2), ("in_proj", "conv_silu", "x_proj", "scan", "out_proj_resid")),
+    ("prefill_tile", (0, 1, 2, 3), ("in_proj", "x_proj", "out_proj_resid")),
+    ("prefill_splitk", (1, 0), ("in_proj", "x_proj", "out_proj_resid")),
+    ("decode_splitk", (1, 0), ("in_proj", "x_proj", "out_proj_resid")),
+    ("decode_graph", (1, 0), ("in_proj", "conv_silu", "x_proj", "scan", "out_proj_resid",
+                              "lm_head_argmax", "embed", "argmax_reduce", "rmsnorm")),
 ]
 
 
@@ -260,19 +272,29 @@ def main() -> int:
     args = ap.parse_args()
     import numpy as np
     import torch
-    from paper_2608_21836_amd.binding import Model, to_device
     from synth import gen, get_config
-    cfg = get_config(args.config)
-    lens, packed = gen.prompt_tokens(cfg)
+    from synth import mamba as SM
     torch.cuda.set_device(0)
-    w = {n: to_device(a, cfg.dtype) for n, a in gen.iter_weights_parallel(cfg, 16)}
-    w.update({k: to_device(v, cfg.dtype) for k, v in gen.gains(cfg).items()})
-    model = Model(cfg, w, max_batch=len(lens), max_prefill_tokens=int(sum(lens)),
-                  max_ctx=max(lens) + cfg.n_decode)
-    del w
+    if args.config in SM.MAMBA_CONFIGS or args.config in SM.MAMBA_TEST_CONFIGS:
+        from paper_2608_21836_amd.binding import MambaModel, upload_mamba_weights
+        cfg = SM.get_mamba_config(args.config)
+        lens, packed = gen.prompt_tokens(cfg)
+        model = MambaModel(cfg, upload_mamba_weights(cfg, SM.weights(cfg)), max_batch=len(lens),
+                           max_prefill_tokens=int(sum(lens)))
+        knobs = MAMBA_KNOBS
+    else:
+        from paper_2608_21836_amd.binding import Model, to_device
+        cfg = get_config(args.config)
+        lens, packed = gen.prompt_tokens(cfg)
+        w = {n: to_device(a, cfg.dtype) for n, a in gen.iter_weights_parallel(cfg, 16)}
+        w.update({k: to_device(v, cfg.dtype) for k, v in gen.gains(cfg).items()})
+        model = Model(cfg, w, max_batch=len(lens), max_prefill_tokens=int(sum(lens)),
+                      max_ctx=max(lens) + cfg.n_decode)
+        del w
+        knobs = KNOBS
     wl = Workload(list(lens), torch.from_numpy(np.asarray(packed, dtype=np.int32)).cuda(),
                   cfg.n_decode)
-    reports = tune(model, wl, args.delta, args.eps, args.reps)
+    reports = tune(model, wl, args.delta, args.eps, args.reps, knobs=knobs)
     result = {"workload": cfg.name, "delta": args.delta, "options": model.options(),
               "knobs": [{"option": r.option, "score": round(r.score, 4),
                          "baseline_ms": round(r.baseline_ms, 4), "chosen": r.chosen,

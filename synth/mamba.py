@@ -7,18 +7,22 @@ convolution and SSM state of an existing cache; the paper gives no hyper-paramet
 shapes below define the workloads (mamba-130m has the Mamba-130M layer shape of the paper's
 Table 1).
 
-Tensors per layer (names of the standard Mamba mixer):
+Tensors per layer (names of the standard Mamba mixer), fan-in scaled so that every stage of
+the mixer works on O(1) values and the mixers, not the token embedding, make up the residual
+stream (otherwise the tied LM head would mostly see the input token's own embedding and the
+scan would barely move the logits):
   norm      [d]            RMSNorm gain (ones)
-  in_proj   [2 di, d]      workload dtype, N(0, init_std^2)
-  conv_w    [di, d_conv]   fp32, N(0, conv_std^2)      depthwise causal convolution taps
+  in_proj   [2 di, d]      workload dtype, N(0, 1/d)
+  conv_w    [di, d_conv]   fp32, N(0, 1/d_conv)        depthwise causal convolution taps
   conv_b    [di]           fp32, N(0, 0.02^2)
-  x_proj    [R + 2 N, di]  workload dtype, N(0, init_std^2)
-  dt_w      [di, R]        fp32, N(0, R^-1)            dt projection
+  x_proj    [R + 2 N, di]  workload dtype, N(0, 1/di)
+  dt_w      [di, R]        fp32, N(0, 1/R)             dt projection
   dt_b      [di]           fp32, softplus^-1 of dt log-uniform in [dt_min, dt_max]
   A_log     [di, N]        fp32, log(1 .. N) in every row (A = -exp(A_log))
   D         [di]           fp32, ones
-  out_proj  [d, di]        workload dtype, N(0, (init_std / sqrt(2 L))^2)
-and embed [V, d] (workload dtype; the LM head is tied to it) and final_norm [d] (ones).
+  out_proj  [d, di]        workload dtype, N(0, 1/(2 L di))
+and embed [V, d] (workload dtype, N(0, init_std^2); the LM head is tied to it) and
+final_norm [d] (ones).
 Random tensor j draws from default_rng([s, 2, j]) in the order embed, then per layer
 (in_proj, conv_w, conv_b, x_proj, dt_w, dt_b, out_proj); prompts use the streams of gen.py.
 """
@@ -51,8 +55,7 @@ class MambaConfig:
     prompt_range: Optional[Tuple[int, int]] = None
     prompt_list: Optional[Tuple[int, ...]] = None
     n_decode: int = 1
-    init_std: float = 0.02
-    conv_std: float = 0.3
+    init_std: float = 0.02   # embedding
     dt_min: float = 1e-3
     dt_max: float = 1e-1
     family: str = "mamba"
@@ -104,7 +107,7 @@ MAMBA_TEST_CONFIGS: Dict[str, MambaConfig] = {
 def tensor_specs(cfg: MambaConfig) -> List[Tuple[str, int, Tuple[int, ...], str]]:
     """[(name, j, shape, kind)] of the random tensors in stream order."""
     di, d, R, N = cfg.d_inner, cfg.d_model, cfg.dt_rank, cfg.d_state
-    out = [("embed", 0, (cfg.vocab, d), "mat")]
+    out = [("embed", 0, (cfg.vocab, d), "embed")]
     j = 1
     for layer in range(cfg.n_layers):
         for name, shape, kind in (("in_proj", (2 * di, d), "mat"), ("conv_w", (di, cfg.d_conv), "conv"),
@@ -124,10 +127,11 @@ def _draw(cfg: MambaConfig, j: int, shape, kind: str) -> np.ndarray:
         dt = np.exp(u * (math.log(cfg.dt_max) - math.log(cfg.dt_min)) + math.log(cfg.dt_min))
         return (dt + np.log(-np.expm1(-dt))).astype(np.float32)
     w = rng.standard_normal(shape, dtype=np.float32)
-    std = {"mat": cfg.init_std, "conv": cfg.conv_std, "bias": 0.02,
-           "dtw": cfg.dt_rank ** -0.5, "out": cfg.init_std / math.sqrt(2 * cfg.n_layers)}[kind]
+    std = {"embed": cfg.init_std, "mat": shape[-1] ** -0.5, "conv": cfg.d_conv ** -0.5,
+           "bias": 0.02, "dtw": cfg.dt_rank ** -0.5,
+           "out": (2 * cfg.n_layers * shape[-1]) ** -0.5}[kind]
     w *= np.float32(std)
-    if kind in ("mat", "out") and cfg.dtype == "bf16":
+    if kind in ("embed", "mat", "out") and cfg.dtype == "bf16":
         w = round_to_bf16(w)
     return w
 
