@@ -8,6 +8,8 @@ Parity status of each function (pins live in tests/test_oracle_pins.py):
   argmax_lowest, top2_margin, OracleModel (prefill, decode, forward_full) -- all pinned.
   mamba: softplus, causal_depthwise_conv, selective_scan, OracleMamba (prefill, decode,
   forward_full) -- all pinned (tests/test_mamba_oracle_pins.py).
+  mamba2: ssd_scan, OracleMamba2 (prefill, extend, decode, forward_full) -- all pinned
+  (tests/test_mamba2_oracle_pins.py).
 """
 from .transformer import (  # noqa: F401
     OracleModel, apply_rope, argmax_lowest, causal_gqa_attention, rmsnorm, rope_frequencies,
