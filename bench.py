@@ -151,6 +151,40 @@ def algorithmic_work_mamba(cfg, lens, n_decode, fused):
     return w
 
 
+def algorithmic_work_mamba2(cfg, lens, n_decode):
+    """{(phase, class): (work, unit)} summed over one Mamba2 job.  Projections count MFMA
+    flops; the scan counts fp32 vector flops per (token, head row, state): 2 for the decayed
+    state update and 2 for the C.h product (pass 3), 2 in pass 1; the rest counts bytes.
+    Decode: weights once per step, the conv and SSM state read and written, activations."""
+    eb = 2 if cfg.dtype == "bf16" else 4
+    B, T = len(lens), sum(lens)
+    d, di, NS, V, L, K = cfg.d_model, cfg.d_inner, cfg.d_state, cfg.vocab, cfg.n_layers, cfg.d_conv
+    H, CD, NZ = cfg.n_heads, cfg.conv_dim, cfg.in_dim
+    N = n_decode
+    state = di * NS * 4   # one sequence's SSM state of one layer
+    w = {}
+    w[("prefill", "in_proj")] = (2.0 * T * NZ * d * L, "flop")
+    w[("prefill", "out_proj_resid")] = (2.0 * T * d * di * L, "flop")
+    w[("prefill", "conv_silu")] = (float(L * (T * CD * 8 + CD * (K + 1) * 4)), "byte")
+    w[("prefill", "scan")] = (float(L * T * di * NS * 4), "alu")
+    w[("prefill", "scan_chunk")] = (float(L * T * di * NS * 2), "alu")
+    w[("prefill", "gated_rmsnorm")] = (float(L * T * di * (4 + eb)), "byte")
+    w[("prefill", "lm_head_argmax")] = (float(V * d * eb + B * d * eb + B * (V // 32) * 8), "byte")
+    w[("prefill", "rmsnorm")] = (float((L * T + B) * d * (4 + eb)), "byte")
+    w[("prefill", "embed")] = (float(T * d * (eb + 4)), "byte")
+    w[("decode", "in_proj")] = (float(N * L * (NZ * d * eb + B * d * 4 + B * (NZ - CD) * 4
+                                               + B * CD * 4 + 2 * B * (K - 1) * CD * 4
+                                               + CD * (K + 1) * 4)), "byte")
+    w[("decode", "scan")] = (float(N * L * (2 * B * state + B * (CD + di + H) * 4
+                                            + B * di * 4 + H * 12)), "byte")
+    w[("decode", "out_proj_resid")] = (float(N * L * (d * di * eb + B * di * 4 + di * eb
+                                                      + 2 * B * d * 4)), "byte")
+    w[("decode", "lm_head_argmax")] = (float(N * (V * d * eb + B * d * eb + B * (V // 32) * 8)), "byte")
+    w[("decode", "rmsnorm")] = (float(N * (L + 1) * B * d * (4 + eb)), "byte")
+    w[("decode", "embed")] = (float(N * B * d * (eb + 4)), "byte")
+    return w
+
+
 # fp32 vector peak of the chip: 256 CUs x 128 fp32 FMA lanes x 2 flops x 2.4 GHz
 ALU_PEAK_TFLOPS = 157.3
 
@@ -214,11 +248,16 @@ def cpu_baseline(cfg, lens, packed, n_decode, budget_s):
 
 
 def cpu_baseline_mamba(cfg, lens, packed, n_decode, budget_s):
-    """The Mamba oracle on the host, as cpu_baseline does for the decoder."""
+    """The Mamba / Mamba2 oracle on the host, as cpu_baseline does for the decoder."""
     from oracle import argmax_lowest, split_prompts
-    from oracle.mamba import OracleMamba
-    from synth import mamba as SM
-    om = OracleMamba(cfg, SM.weights(cfg))
+    if cfg.family == "mamba2":
+        from oracle.mamba2 import OracleMamba2
+        from synth import mamba2 as S2
+        om = OracleMamba2(cfg, S2.weights(cfg))
+    else:
+        from oracle.mamba import OracleMamba
+        from synth import mamba as SM
+        om = OracleMamba(cfg, SM.weights(cfg))
     prompts = split_prompts(lens, packed)
     t0 = time.perf_counter()
     toks = argmax_lowest(om.prefill(prompts))
@@ -244,7 +283,8 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="125m",
-                    help="workload name (synth.configs, or a Mamba workload of synth.mamba)")
+                    help="workload name (synth.configs, or a Mamba / Mamba2 workload of "
+                         "synth.mamba / synth.mamba2)")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
@@ -270,15 +310,18 @@ def main() -> int:
     from synth import gen, get_config
     from synth import mamba as SM
 
+    from synth import mamba2 as S2
     torch.cuda.set_device(0)
-    mamba = args.config in SM.MAMBA_CONFIGS or args.config in SM.MAMBA_TEST_CONFIGS
-    cfg = SM.get_mamba_config(args.config) if mamba else get_config(args.config)
+    mamba2 = args.config in S2.MAMBA2_CONFIGS or args.config in S2.MAMBA2_TEST_CONFIGS
+    mamba = mamba2 or args.config in SM.MAMBA_CONFIGS or args.config in SM.MAMBA_TEST_CONFIGS
+    cfg = (S2.get_mamba2_config(args.config) if mamba2 else
+           SM.get_mamba_config(args.config) if mamba else get_config(args.config))
     lens, packed = gen.prompt_tokens(cfg)
     B, T, N = len(lens), int(sum(lens)), cfg.n_decode
     print(f"[bench] {cfg.name}: uploading weights", file=sys.stderr, flush=True)
     if mamba:
         from paper_2608_21836_amd.binding import MambaModel, upload_mamba_weights
-        dev_w = upload_mamba_weights(cfg, SM.weights(cfg))
+        dev_w = upload_mamba_weights(cfg, (S2 if mamba2 else SM).weights(cfg))
         model = MambaModel(cfg, dev_w, max_batch=B, max_prefill_tokens=T)
         reset = model.reset
         from paper_2608_21836_amd.tuner import accepted_options
@@ -286,11 +329,18 @@ def main() -> int:
         options.update(dict(o.split("=", 1) for o in args.option))
         for name, value in options.items():
             model.set_option(name, int(value))
-        fused = model.get_option("decode_fused") if B <= 4 else 0
-        work_all = algorithmic_work_mamba(cfg, lens, N, fused)
-        desc = {"workload": cfg.name, "family": "mamba", "layers": cfg.n_layers,
-                "d_model": cfg.d_model, "d_inner": cfg.d_inner, "d_state": cfg.d_state,
-                "d_conv": cfg.d_conv, "dt_rank": cfg.dt_rank, "vocab": cfg.vocab}
+        if mamba2:
+            work_all = algorithmic_work_mamba2(cfg, lens, N)
+            desc = {"workload": cfg.name, "family": "mamba2", "layers": cfg.n_layers,
+                    "d_model": cfg.d_model, "d_inner": cfg.d_inner, "d_state": cfg.d_state,
+                    "heads": f"{cfg.n_heads}x{cfg.head_dim}", "groups": cfg.n_groups,
+                    "d_conv": cfg.d_conv, "vocab": cfg.vocab}
+        else:
+            fused = model.get_option("decode_fused") if B <= 4 else 0
+            work_all = algorithmic_work_mamba(cfg, lens, N, fused)
+            desc = {"workload": cfg.name, "family": "mamba", "layers": cfg.n_layers,
+                    "d_model": cfg.d_model, "d_inner": cfg.d_inner, "d_state": cfg.d_state,
+                    "d_conv": cfg.d_conv, "dt_rank": cfg.dt_rank, "vocab": cfg.vocab}
         if args.no_graph:
             model.set_option("decode_graph", 0)
     else:

@@ -26,6 +26,7 @@ OPTIONS = {"decode_graph": 0, "prefill_splitk": 1, "decode_splitk": 2, "prefill_
 DECODER_OPTIONS = ("decode_graph", "prefill_splitk", "decode_splitk", "prefill_tile",
                    "attn_decode_chunk")
 MAMBA_OPTIONS = ("decode_graph", "prefill_splitk", "decode_splitk", "prefill_tile", "decode_fused")
+MAMBA2_OPTIONS = ("decode_graph", "prefill_splitk", "decode_splitk", "prefill_tile")
 PHASES = ("prefill", "decode")
 
 
@@ -64,6 +65,26 @@ class LLMambaWeights(ctypes.Structure):
 
 
 LL_MK_COUNT = 12
+
+
+class LLMamba2Config(ctypes.Structure):
+    _fields_ = [("n_layers", c_int32), ("d_model", c_int32), ("d_inner", c_int32),
+                ("d_state", c_int32), ("head_dim", c_int32), ("n_groups", c_int32),
+                ("d_conv", c_int32), ("vocab", c_int32), ("rms_eps", c_float),
+                ("dtype", c_int32), ("max_batch", c_int32), ("max_prefill_tokens", c_int32)]
+
+
+MAMBA2_LAYER_FIELDS = ("norm", "in_proj", "conv_w", "conv_b", "dt_b", "A_log", "D", "gnorm",
+                       "out_proj")
+MAMBA2_F32_FIELDS = ("conv_w", "conv_b", "dt_b", "A_log", "D")
+
+
+class LLMamba2Weights(ctypes.Structure):
+    _fields_ = [("embed", c_void_p), ("final_norm", c_void_p)] + \
+        [(f, POINTER(c_void_p)) for f in MAMBA2_LAYER_FIELDS]
+
+
+LL_M2K_COUNT = 12
 
 # (name, restype, argtypes) of every exported symbol; include/ll.h, include/ll_ops.h and
 # include/ll_mamba.h declare the same set.
@@ -120,6 +141,21 @@ SIGNATURES = [
     ("ll_mamba_kernel_timing_read", c_int32, [c_void_p, POINTER(c_int32), POINTER(c_double)]),
     ("ll_mamba_kernel_class_name", c_char_p, [c_int32]),
     ("ll_mamba_free", None, [c_void_p]),
+    ("ll_mamba2_workspace_size", c_int32, [POINTER(LLMamba2Config), POINTER(c_size_t)]),
+    ("ll_mamba2_load", c_int32, [POINTER(LLMamba2Config), POINTER(LLMamba2Weights), c_void_p,
+                                 c_size_t, c_void_p, POINTER(c_void_p)]),
+    ("ll_mamba2_prefill", c_int32, [c_void_p, c_int32, POINTER(c_int32), c_void_p, c_void_p,
+                                    c_void_p]),
+    ("ll_mamba2_decode_step", c_int32, [c_void_p, c_void_p, c_void_p, c_void_p]),
+    ("ll_mamba2_reset", c_int32, [c_void_p]),
+    ("ll_mamba2_seq_lengths", c_int32, [c_void_p, POINTER(c_int32), c_int32, POINTER(c_int32)]),
+    ("ll_mamba2_set_option", c_int32, [c_void_p, c_int32, c_int32]),
+    ("ll_mamba2_get_option", c_int32, [c_void_p, c_int32, POINTER(c_int32)]),
+    ("ll_mamba2_device_flags", c_int32, [c_void_p, POINTER(c_int32)]),
+    ("ll_mamba2_set_kernel_timing", c_int32, [c_void_p, c_int32]),
+    ("ll_mamba2_kernel_timing_read", c_int32, [c_void_p, POINTER(c_int32), POINTER(c_double)]),
+    ("ll_mamba2_kernel_class_name", c_char_p, [c_int32]),
+    ("ll_mamba2_free", None, [c_void_p]),
 ]
 
 _lib = None
@@ -307,38 +343,59 @@ def mamba_workspace_size(cfg: LLMambaConfig) -> int:
     return n.value
 
 
-class MambaModel:
-    """One loaded Mamba model: workspace (a torch uint8 tensor), handle and stream.
+def make_mamba2_config(cfg, max_batch: int, max_prefill_tokens: int) -> LLMamba2Config:
+    """LLMamba2Config from a synth.mamba2.Mamba2Config-like object."""
+    return LLMamba2Config(cfg.n_layers, cfg.d_model, cfg.d_inner, cfg.d_state, cfg.head_dim,
+                          cfg.n_groups, cfg.d_conv, cfg.vocab, float(cfg.rms_eps),
+                          LL_BF16 if cfg.dtype == "bf16" else LL_F32, max_batch,
+                          max_prefill_tokens)
 
-    ``weights`` maps synth.mamba tensor names to CUDA tensors (upload_mamba_weights)."""
+
+class MambaModel:
+    """One loaded Mamba or Mamba2 model (cfg.family "mamba" / "mamba2"): workspace (a torch
+    uint8 tensor), handle and stream.  The two families differ only in the C entry points'
+    prefix (ll_mamba_* / ll_mamba2_*), the config and weight structs and the kernel classes.
+
+    ``weights`` maps synth.mamba / synth.mamba2 tensor names to CUDA tensors
+    (upload_mamba_weights)."""
 
     def __init__(self, cfg, weights: Dict[str, "object"], max_batch: int,
                  max_prefill_tokens: int, stream=None):
         import torch
         self.lib = load_library()
         self.mcfg = cfg
-        self.cfg = make_mamba_config(cfg, max_batch, max_prefill_tokens)
+        self.v2 = getattr(cfg, "family", "mamba") == "mamba2"
+        self.prefix = "ll_mamba2_" if self.v2 else "ll_mamba_"
+        self.n_classes = LL_M2K_COUNT if self.v2 else LL_MK_COUNT
+        self.cfg = (make_mamba2_config if self.v2 else make_mamba_config)(cfg, max_batch,
+                                                                          max_prefill_tokens)
         self.stream = stream if stream is not None else torch.cuda.current_stream()
-        nbytes = mamba_workspace_size(self.cfg)
+        n = c_size_t(0)
+        _check(self._fn("workspace_size")(ctypes.byref(self.cfg), ctypes.byref(n)),
+               self.prefix + "workspace_size")
+        nbytes = n.value
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
         nl = cfg.n_layers
         keep, fields = [], {}
-        for key in MAMBA_LAYER_FIELDS:
+        for key in (MAMBA2_LAYER_FIELDS if self.v2 else MAMBA_LAYER_FIELDS):
             a = (c_void_p * nl)(*[weights[f"layers.{i}.{key}"].data_ptr() for i in range(nl)])
             keep.append(a)
             fields[key] = ctypes.cast(a, POINTER(c_void_p))
-        w = LLMambaWeights(weights["embed"].data_ptr(), weights["final_norm"].data_ptr(), **fields)
+        W = LLMamba2Weights if self.v2 else LLMambaWeights
+        w = W(weights["embed"].data_ptr(), weights["final_norm"].data_ptr(), **fields)
         handle = c_void_p()
-        _check(self.lib.ll_mamba_load(ctypes.byref(self.cfg), ctypes.byref(w),
-                                      self.workspace.data_ptr(), nbytes,
-                                      self.stream.cuda_stream, ctypes.byref(handle)),
-               "ll_mamba_load")
+        _check(self._fn("load")(ctypes.byref(self.cfg), ctypes.byref(w), self.workspace.data_ptr(),
+                                nbytes, self.stream.cuda_stream, ctypes.byref(handle)),
+               self.prefix + "load")
         self.handle = handle
         self.batch = 0
 
+    def _fn(self, name):
+        return getattr(self.lib, self.prefix + name)
+
     def close(self) -> None:
         if getattr(self, "handle", None):
-            self.lib.ll_mamba_free(self.handle)
+            self._fn("free")(self.handle)
             self.handle = None
 
     def __del__(self):
@@ -353,8 +410,8 @@ class MambaModel:
         lens = (c_int32 * b)(*[int(x) for x in seq_lens])
         if next_tokens is None:
             next_tokens = torch.empty(b, dtype=torch.int32, device="cuda")
-        _check(self.lib.ll_mamba_prefill(self.handle, b, lens, tokens.data_ptr(),
-                                         next_tokens.data_ptr(), _ptr(logits)), "ll_mamba_prefill")
+        _check(self._fn("prefill")(self.handle, b, lens, tokens.data_ptr(),
+                                   next_tokens.data_ptr(), _ptr(logits)), self.prefix + "prefill")
         self.batch = b
         return next_tokens, logits
 
@@ -362,59 +419,60 @@ class MambaModel:
         import torch
         if next_tokens is None:
             next_tokens = torch.empty(self.batch, dtype=torch.int32, device="cuda")
-        _check(self.lib.ll_mamba_decode_step(self.handle, in_tokens.data_ptr(),
-                                             next_tokens.data_ptr(), _ptr(logits)),
-               "ll_mamba_decode_step")
+        _check(self._fn("decode_step")(self.handle, in_tokens.data_ptr(),
+                                       next_tokens.data_ptr(), _ptr(logits)),
+               self.prefix + "decode_step")
         return next_tokens, logits
 
     def reset(self) -> None:
-        _check(self.lib.ll_mamba_reset(self.handle), "ll_mamba_reset")
+        _check(self._fn("reset")(self.handle), self.prefix + "reset")
         self.batch = 0
 
     kv_reset = reset  # same call name as the decoder's (forget every held sequence)
 
     def set_option(self, name: str, value: int) -> None:
-        _check(self.lib.ll_mamba_set_option(self.handle, OPTIONS[name], int(value)),
-               "ll_mamba_set_option")
+        _check(self._fn("set_option")(self.handle, OPTIONS[name], int(value)),
+               self.prefix + "set_option")
 
     def get_option(self, name: str) -> int:
         v = c_int32(0)
-        _check(self.lib.ll_mamba_get_option(self.handle, OPTIONS[name], ctypes.byref(v)),
-               "ll_mamba_get_option")
+        _check(self._fn("get_option")(self.handle, OPTIONS[name], ctypes.byref(v)),
+               self.prefix + "get_option")
         return v.value
 
     def options(self) -> Dict[str, int]:
-        return {k: self.get_option(k) for k in MAMBA_OPTIONS}
+        return {k: self.get_option(k) for k in (MAMBA2_OPTIONS if self.v2 else MAMBA_OPTIONS)}
 
     def seq_lengths(self) -> List[int]:
         out = (c_int32 * LL_MAX_BATCH)()
         n = c_int32(0)
-        _check(self.lib.ll_mamba_seq_lengths(self.handle, out, LL_MAX_BATCH, ctypes.byref(n)),
-               "ll_mamba_seq_lengths")
+        _check(self._fn("seq_lengths")(self.handle, out, LL_MAX_BATCH, ctypes.byref(n)),
+               self.prefix + "seq_lengths")
         return list(out[:n.value])
 
     def set_kernel_timing(self, enable: bool) -> None:
-        _check(self.lib.ll_mamba_set_kernel_timing(self.handle, 1 if enable else 0),
-               "ll_mamba_set_kernel_timing")
+        _check(self._fn("set_kernel_timing")(self.handle, 1 if enable else 0),
+               self.prefix + "set_kernel_timing")
 
     def kernel_timing(self) -> Dict[Tuple[str, str], Tuple[int, float]]:
         """{(phase, kernel class): (launches, summed kernel ms)} since the last read."""
-        counts = (c_int32 * (2 * LL_MK_COUNT))()
-        ms = (c_double * (2 * LL_MK_COUNT))()
-        _check(self.lib.ll_mamba_kernel_timing_read(self.handle, counts, ms),
-               "ll_mamba_kernel_timing_read")
+        nc = self.n_classes
+        counts = (c_int32 * (2 * nc))()
+        ms = (c_double * (2 * nc))()
+        _check(self._fn("kernel_timing_read")(self.handle, counts, ms),
+               self.prefix + "kernel_timing_read")
         out = {}
         for p in range(2):
-            for c in range(LL_MK_COUNT):
-                i = p * LL_MK_COUNT + c
+            for c in range(nc):
+                i = p * nc + c
                 if counts[i]:
-                    name = self.lib.ll_mamba_kernel_class_name(c).decode()
+                    name = self._fn("kernel_class_name")(c).decode()
                     out[(PHASES[p], name)] = (counts[i], ms[i])
         return out
 
     def device_flags(self) -> int:
         f = c_int32(0)
-        _check(self.lib.ll_mamba_device_flags(self.handle, ctypes.byref(f)), "ll_mamba_device_flags")
+        _check(self._fn("device_flags")(self.handle, ctypes.byref(f)), self.prefix + "device_flags")
         return f.value
 
 
@@ -437,11 +495,12 @@ def upload_weights(cfg, weights) -> Dict[str, "object"]:
 
 
 def upload_mamba_weights(cfg, weights) -> Dict[str, "object"]:
-    """Mamba tensors: the small per-channel ones (conv, dt projection, A_log, D) in fp32, the
-    rest in the workload dtype."""
+    """Mamba / Mamba2 tensors: the small per-channel / per-head ones (conv, dt, A_log, D) in
+    fp32, the rest in the workload dtype."""
+    f32 = MAMBA2_F32_FIELDS if getattr(cfg, "family", "mamba") == "mamba2" else MAMBA_F32_FIELDS
     out = {}
     for k, v in weights.items():
-        out[k] = to_device(v, "f32" if k.rsplit(".", 1)[-1] in MAMBA_F32_FIELDS else cfg.dtype)
+        out[k] = to_device(v, "f32" if k.rsplit(".", 1)[-1] in f32 else cfg.dtype)
     return out
 
 

@@ -152,6 +152,18 @@ __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+// softplus(x) = max(x, 0) + log1p(exp(-|x|)), with log1p(e) = log(1 + e) * e / ((1 + e) - 1)
+// (exact rounding compensation of 1 + e; e itself when 1 + e rounds to 1).
+__device__ __forceinline__ float softplus_f(float x) {
+  const float e = __expf(-fabsf(x));
+  const float u = 1.f + e;
+  const float l = u == 1.f ? e : __logf(u) * __fdividef(e, u - 1.f);
+  return fmaxf(x, 0.f) + l;
+}
+// 2^x with the hardware instruction (results below the normal range flush to zero).
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float silu_fast(float z) { return __fdividef(z, 1.f + __expf(-z)); }
+
 // Merge of split-K attention partials, in split order: sum_s w_s o_s / sum_s w_s l_s, where
 // w_s = 2^(m_s - max_s m_s) (log-sum-exp rescaling of each split's unnormalised output o_s and
 // sum l_s).  `po` points at split 0's output element, `stride` floats between splits; w and l

@@ -191,38 +191,42 @@ template <typename T> struct EpiQkv {
   }
 };
 
-// Mamba in_proj of a decode step (row m = sequence m): columns [0, di) are the conv inputs x,
-// pushed through one step of the causal depthwise convolution with the sequence's conv state
-// (u = silu(b + sum_k w[k] window[k]), the window being the K-1 held inputs then x; the state
-// then shifts by one and keeps x), columns [di, 2 di) are the gate z, stored as fp32.
-template <typename T> struct EpiConv {
-  T *u;         // [rows][di]
-  float *z;     // [rows][di]
-  float *conv;  // [rows][K-1][di] conv state of this layer
-  const float *w, *b;  // [di][K], [di]
-  int di, K;
+// in_proj of a Mamba / Mamba2 decode step (row m = sequence m): columns [col0, col0 + nc) are
+// the conv inputs, pushed through one step of the causal depthwise convolution with the
+// sequence's conv state (u = silu(b + sum_k w[k] window[k]), the window being the K-1 held
+// inputs then the new value; the state then shifts by one and keeps it), written to u (type U,
+// row stride nc); every other column is stored as fp32 at its own index of `raw` (row stride
+// ld_raw).
+template <typename U> struct EpiConv {
+  U *u;          // [rows][nc]
+  float *raw;    // [rows][ld_raw]
+  int ld_raw;
+  float *conv;   // [rows][K-1][nc] conv state of this layer
+  const float *w, *b;  // [nc][K], [nc]
+  int col0, nc, K;
   static constexpr bool kArgmax = false, kPairs = false, kVec8 = false;
   __device__ void one(int m, int col, float v) const {
-    if (col >= di) {
-      z[(size_t)m * di + col - di] = v;
+    const int ch = col - col0;
+    if (ch < 0 || ch >= nc) {
+      raw[(size_t)m * ld_raw + col] = v;
       return;
     }
-    float *st = conv + (size_t)m * (K - 1) * di + col;
-    const float *wc = w + (size_t)col * K;
+    float *st = conv + (size_t)m * (K - 1) * nc + ch;
+    const float *wc = w + (size_t)ch * K;
     float old[3];
 #pragma unroll
     for (int k = 0; k < 3; ++k)
-      if (k < K - 1) old[k] = st[(size_t)k * di];
-    float acc = b[col];
+      if (k < K - 1) old[k] = st[(size_t)k * nc];
+    float acc = b[ch];
 #pragma unroll
     for (int k = 0; k < 3; ++k)
       if (k < K - 1) acc = fmaf(wc[k], old[k], acc);
     acc = fmaf(wc[K - 1], v, acc);
 #pragma unroll
     for (int k = 0; k < 2; ++k)
-      if (k < K - 2) st[(size_t)k * di] = old[k + 1];
-    if (K > 1) st[(size_t)(K - 2) * di] = v;
-    u[(size_t)m * di + col] = from_f32<T>(silu_f(acc));
+      if (k < K - 2) st[(size_t)k * nc] = old[k + 1];
+    if (K > 1) st[(size_t)(K - 2) * nc] = v;
+    u[(size_t)m * nc + ch] = from_f32<U>(silu_f(acc));
   }
   __device__ void operator()(int m, int uu, int c, float v0, float v1) const {
     one(m, 32 * uu + c, v0);
@@ -962,8 +966,10 @@ hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm,
     return hipErrorInvalidValue;
   if ((ep.kind == kEpiStore || ep.kind == kEpiResid) && !ep.out_f32) return hipErrorInvalidValue;
   if (ep.kind == kEpiSwiglu && !ep.act) return hipErrorInvalidValue;
-  if (ep.kind == kEpiConv && (!ep.act || !ep.out_f32 || !ep.conv_state || !ep.conv_w ||
-                              !ep.conv_b || ep.conv_k < 1 || ep.conv_k > 4 || n != 2 * ep.ld_act))
+  if ((ep.kind == kEpiConv || ep.kind == kEpiConvF32) &&
+      (!ep.act || !ep.out_f32 || !ep.conv_state || !ep.conv_w || !ep.conv_b || ep.conv_k < 1 ||
+       ep.conv_k > 4 || ep.conv_col0 < 0 || ep.conv_n < 1 || ep.conv_col0 + ep.conv_n > n ||
+       ep.ld_out < n))
     return hipErrorInvalidValue;
   if (ep.kind == kEpiQkv && (!ep.act || !ep.kcache || !ep.vcache || !ep.row_pos ||
                              !ep.rope_cos || !ep.rope_sin))
@@ -981,8 +987,12 @@ hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm,
     case kEpiArgmax:
       return run(EpiArgmax{ep.out_f32, ep.ld_out, ep.part_val, ep.part_idx, ep.n_parts});
     case kEpiConv:
-      return run(EpiConv<T>{reinterpret_cast<T *>(ep.act), ep.out_f32, ep.conv_state, ep.conv_w,
-                            ep.conv_b, ep.ld_act, ep.conv_k});
+      return run(EpiConv<T>{reinterpret_cast<T *>(ep.act), ep.out_f32, ep.ld_out, ep.conv_state,
+                            ep.conv_w, ep.conv_b, ep.conv_col0, ep.conv_n, ep.conv_k});
+    case kEpiConvF32:
+      return run(EpiConv<float>{reinterpret_cast<float *>(ep.act), ep.out_f32, ep.ld_out,
+                                ep.conv_state, ep.conv_w, ep.conv_b, ep.conv_col0, ep.conv_n,
+                                ep.conv_k});
   }
   return hipErrorInvalidValue;
 }

@@ -50,8 +50,10 @@ enum EpiKind : int {
   kEpiSwiglu = 2,  // act[m, j] = silu(gate) * up   (kPermGlu weights)
   kEpiQkv = 3,     // RoPE on q, k; q -> act, k / v -> KV cache  (kPermRope weights)
   kEpiArgmax = 4,  // logits (optional) + per-32-column (max, argmax) partials
-  kEpiConv = 5,    // Mamba decode in_proj: x columns -> conv step + SiLU -> act (u, ld_act =
-                   // d_inner), conv state shifted; z columns -> out_f32 [rows][d_inner]
+  kEpiConv = 5,    // Mamba decode in_proj: columns [conv_col0, + conv_n) -> conv step + SiLU
+                   // -> act (element type T, row stride conv_n), conv state shifted; the other
+                   // columns -> out_f32 (fp32, row stride ld_out) at their own index
+  kEpiConvF32 = 6, // the same with act in fp32
 };
 
 struct EpiParams {
@@ -70,10 +72,10 @@ struct EpiParams {
   float *part_val = nullptr;
   int *part_idx = nullptr;
   int n_parts = 0;  // partials per row (= N / 32)
-  // Conv (row = sequence): conv_state [rows][K-1][d_inner], taps [d_inner][K], bias [d_inner]
+  // Conv (row = sequence): conv_state [rows][K-1][conv_n], taps [conv_n][K], bias [conv_n]
   float *conv_state = nullptr;
   const float *conv_w = nullptr, *conv_b = nullptr;
-  int conv_k = 0;
+  int conv_k = 0, conv_col0 = 0, conv_n = 0;
 };
 
 // RMSNorm computed inside the decode GEMM (A = RMSNorm(x[rowmap[r]]) * gain).
@@ -263,7 +265,8 @@ constexpr int kSsmDecodeMaxRows = 4;
 constexpr int kSsmDecodeMaxX = 128;
 struct SsmDecodeArgs {
   const void *u = nullptr;     // T [rows][di]
-  const float *z = nullptr;    // fp32 [rows][di]
+  const float *z = nullptr;    // fp32 [rows][ldz]
+  int ldz = 0;
   const void *wx = nullptr;    // repacked x_proj (ll_op_repack layout), >= 128 rows
   const float *dtwT = nullptr, *dt_b = nullptr, *A2 = nullptr, *D = nullptr;
   float *ssm = nullptr;        // [rows][di][N]
@@ -281,5 +284,38 @@ hipError_t launch_ssm_decode(int dtype, const SsmDecodeArgs &a, hipStream_t s);
 // j < cols, zero rows for cols <= j < cols_pad; fp32.
 hipError_t launch_transpose_f32(const float *src, int rows, int cols, int cols_pad, float *dst,
                                 int neg_exp, float scale, hipStream_t s);
+
+// ------------------------------------------------------------------------------------------
+// Mamba2 mixer
+// ------------------------------------------------------------------------------------------
+// Per layer the in_proj output rows hold z | x B C | dt (fp32, row stride ldz); the causal
+// conv + SiLU over the x B C channels gives xbc.  Each head h (group h / (H / G) of B and C)
+// keeps a state [P][N]: h <- exp(dt A_h) h + dt x B^T, y = h C + D_h x, and the scan writes
+// g = y * silu(z) (fp32) for the gated RMSNorm that precedes out_proj.  One block of 256
+// threads covers 16 rows of a head (16 lanes per row, N / 16 states per lane).  Prefill uses
+// the three passes of the Mamba scan over time chunks; decode is pass 3 on one-token chunks.
+constexpr int kM2Rows = 16;              // head rows per scan block
+constexpr int kM2TargetBlocks = 1024;
+int mamba2_chunk_len(int total, int n_heads, int head_dim);
+int mamba2_max_chunks(int max_total, int max_batch, int n_heads, int head_dim);
+struct M2ScanArgs {
+  const float *zxd = nullptr;   // in_proj rows: z at [0, di), dt at [dt_col, dt_col + H)
+  int ldz = 0, dt_col = 0;
+  const float *xbc = nullptr;   // conv output rows [rows][conv_n]: x | B (G N) | C (G N)
+  const float *dt_b = nullptr, *A2 = nullptr, *D = nullptr;  // [H]; A2 = A * log2(e)
+  float *ssm = nullptr;         // [batch][H][P][N]
+  float *g = nullptr;           // fp32 [rows][di]
+  float *hloc = nullptr;        // [chunks][H][P][N]
+  float *dtsum = nullptr;       // [chunks][H]
+  const int4 *chunks = nullptr; // null: decode (chunk j = row j = sequence j)
+  const int *seq_chunk0 = nullptr, *cu = nullptr;
+  float *conv = nullptr;        // conv state [batch][K-1][conv_n] (updated when update_conv)
+  int conv_col = 0, conv_n = 0, K = 0, update_conv = 0;
+  int di = 0, H = 0, P = 0, N = 0, G = 0;
+  int fresh = 0, carry = 0;     // carry: 0 zero, 1 SSM state, 2 hloc
+};
+hipError_t launch_m2_scan_chunks(const M2ScanArgs &a, int n_chunks, hipStream_t s);
+hipError_t launch_m2_scan_carry(const M2ScanArgs &a, int batch, hipStream_t s);
+hipError_t launch_m2_scan_out(const M2ScanArgs &a, int n_chunks, hipStream_t s);
 
 }  // namespace ll

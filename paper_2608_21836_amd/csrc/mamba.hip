@@ -16,17 +16,6 @@ namespace {
 
 constexpr int kNS = 16;  // SSM state size the scan kernels are built for
 
-// softplus(x) = max(x, 0) + log1p(exp(-|x|)), with log1p(e) = log(1 + e) * e / ((1 + e) - 1)
-// (exact rounding compensation of 1 + e; e itself when 1 + e rounds to 1).
-__device__ __forceinline__ float softplus_f(float x) {
-  const float e = __expf(-fabsf(x));
-  const float u = 1.f + e;
-  const float l = u == 1.f ? e : __logf(u) * __fdividef(e, u - 1.f);
-  return fmaxf(x, 0.f) + l;
-}
-// 2^x with the hardware instruction (results below the normal range flush to zero).
-__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
-__device__ __forceinline__ float silu_fast(float z) { return __fdividef(z, 1.f + __expf(-z)); }
 
 // One block of 256 threads: offsets and chunk list from the per-sequence lengths.
 __global__ __launch_bounds__(256) void k_mamba_meta(MambaMeta mm, int total, int chunk_len,
@@ -297,7 +286,7 @@ __global__ __launch_bounds__(kSsmThreads) void k_ssm_decode(SsmDecodeArgs p) {
 #pragma unroll
   for (int b = 0; b < kSsmDecodeMaxRows; ++b) {
     hs[b] = b < rows ? p.ssm[((size_t)b * di + c) * kNS + n] : 0.f;
-    zs[b] = b < rows ? p.z[(size_t)b * di + c] : 0.f;
+    zs[b] = b < rows ? p.z[(size_t)b * p.ldz + c] : 0.f;
     us[b] = b < rows ? to_f32(u[(size_t)b * di + c]) : 0.f;
   }
 #pragma unroll
@@ -547,7 +536,7 @@ hipError_t launch_scan_out(int dtype, const ScanArgs &a, int n_chunks, hipStream
 hipError_t launch_ssm_decode(int dtype, const SsmDecodeArgs &a, hipStream_t s) {
   if (a.rows <= 0) return hipSuccess;
   const int X = a.R + 2 * kNS;
-  if (!a.u || !a.z || !a.wx || !a.dtwT || !a.dt_b || !a.A2 || !a.D || !a.ssm ||
+  if (!a.u || !a.z || a.ldz < a.di || !a.wx || !a.dtwT || !a.dt_b || !a.A2 || !a.D || !a.ssm ||
       a.rows > kSsmDecodeMaxRows || a.N != kNS || a.R < 1 || X > kSsmDecodeMaxX || a.di <= 0 ||
       a.di % kScanChannels != 0)
     return hipErrorInvalidValue;

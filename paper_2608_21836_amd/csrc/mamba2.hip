@@ -1,0 +1,245 @@
+// Kernels of the Mamba2 mixer on gfx950: the chunked scan over heads (passes 1 and 3, the
+// carry pass) with the state tile of a head in registers.  The conv + SiLU, the projections,
+// the gated RMSNorm (an RMSNorm of g = y * silu(z)) and the LM head run on the shared kernels.
+//
+// The paper's Mamba2 case (appendix "Deployment Kernel Families", Table A.4) loads the compact
+// B and C vectors once per time step and shares them across heads, with the state tile kept in
+// registers across the scan.  Here a block covers 16 rows of one head's [P][N] state (16 lanes
+// per row, N / 16 states per lane); a stage of 16 steps of B, C, x, dt is staged in LDS in one
+// round of loads and read as broadcasts (every row of the block reads the same B and C words).
+#include <hip/hip_runtime.h>
+
+#include "device_common.h"
+#include "kernels.h"
+
+namespace ll {
+namespace {
+
+constexpr int kM2Stage = 16;
+constexpr int kM2Threads = 256;
+
+template <bool kOut, int NPT>
+__global__ __launch_bounds__(kM2Threads) void k_m2_scan(M2ScanArgs p) {
+  constexpr int N = 16 * NPT;
+  __shared__ __attribute__((aligned(16))) float s_B[kM2Stage][N];
+  __shared__ __attribute__((aligned(16))) float s_C[kM2Stage][N];
+  __shared__ float s_x[kM2Stage][kM2Rows];
+  __shared__ float s_dt[kM2Stage], s_dec[kM2Stage];
+  const int j = blockIdx.y;
+  const int4 ch = p.chunks ? p.chunks[j] : make_int4(j, j, 1, kChunkLast);
+  if (!kOut && (ch.w & kChunkLast)) return;  // a sequence's last chunk needs no end state
+  const int tid = threadIdx.x, pr = tid >> 4, nq = tid & 15;
+  const int PB = p.P / kM2Rows;
+  const int h = blockIdx.x / PB, pb = blockIdx.x - h * PB;
+  const int row = pb * kM2Rows + pr;                 // row of the head's state tile
+  const int grp = h / (p.H / p.G);
+  const int di = p.di, GN = p.G * N;
+  const size_t tile = (size_t)p.P * N;               // one head's state
+  const float a2 = p.A2[h], bias = p.dt_b[h], Dh = kOut ? p.D[h] : 0.f;
+  // incoming state: none (zero), the sequence's SSM state (carry 1) or the chunk's slot of hloc
+  // (carry 2), as one base pointer and two strides
+  const float *init = nullptr;
+  size_t init_seq = 0, init_chunk = 0;
+  if (kOut && p.carry == 1) {
+    init = p.ssm;
+    init_seq = (size_t)p.H * tile;
+  } else if (kOut && p.carry == 2) {
+    init = p.hloc;
+    init_chunk = (size_t)p.H * tile;
+  }
+  float st[NPT];
+  {
+    const float *sp = init ? init + (size_t)ch.x * init_seq + (size_t)j * init_chunk +
+                                 (size_t)h * tile + (size_t)row * N + nq
+                           : nullptr;
+#pragma unroll
+    for (int k = 0; k < NPT; ++k) st[k] = sp ? sp[16 * k] : 0.f;
+  }
+  float dsum = 0.f;
+  const int tend = ch.y + ch.z;
+  for (int t0 = ch.y; t0 < tend; t0 += kM2Stage) {
+    const int nt = min(kM2Stage, tend - t0);
+    __syncthreads();  // the previous stage has been read
+    {
+      // B and C rows of the stage: 2 * 16 * N floats, float4 each, all in flight
+      constexpr int V4 = 2 * kM2Stage * N / 4 / kM2Threads;  // float4 per thread
+      float4 v[V4];
+#pragma unroll
+      for (int q = 0; q < V4; ++q) {
+        const int e = (q * kM2Threads + tid) * 4;       // element of [2][16][N]
+        const int which = e / (kM2Stage * N), rem = e - which * (kM2Stage * N);
+        const int r = rem / N, n = rem - r * N;
+        v[q] = r < nt ? *reinterpret_cast<const float4 *>(
+                            p.xbc + (size_t)(t0 + r) * p.conv_n + di + which * GN + grp * N + n)
+                      : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      const float xv = pr < nt ? p.xbc[(size_t)(t0 + pr) * p.conv_n + h * p.P + pb * kM2Rows + nq]
+                               : 0.f;
+      float dtr = 0.f;
+      if (tid < nt) dtr = p.zxd[(size_t)(t0 + tid) * p.ldz + p.dt_col + h];
+#pragma unroll
+      for (int q = 0; q < V4; ++q) {
+        const int e = (q * kM2Threads + tid) * 4;
+        const int which = e / (kM2Stage * N), rem = e - which * (kM2Stage * N);
+        const int r = rem / N, n = rem - r * N;
+        *reinterpret_cast<float4 *>(which ? &s_C[r][n] : &s_B[r][n]) = v[q];
+      }
+      s_x[pr][nq] = xv;  // s_x[step][row]: thread (pr, nq) loads step pr, row nq
+      if (tid < kM2Stage) {
+        const float dt = softplus_f(dtr + bias);
+        s_dt[tid] = dt;
+        s_dec[tid] = exp2_fast(dt * a2);
+      }
+    }
+    float zv[kM2Stage];
+#pragma unroll
+    for (int i = 0; i < kM2Stage; ++i)
+      zv[i] = (kOut && nq == 0 && i < nt) ? p.zxd[(size_t)(t0 + i) * p.ldz + h * p.P + row] : 0.f;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kM2Stage; ++i) {
+      if (i < nt) {
+        const float dt = s_dt[i], dec = s_dec[i];
+        const float xv = s_x[i][pr];
+        const float dtx = dt * xv;
+        float ys = 0.f;
+#pragma unroll
+        for (int k = 0; k < NPT; ++k) {
+          st[k] = fmaf(dec, st[k], dtx * s_B[i][nq + 16 * k]);
+          if (kOut) ys = fmaf(s_C[i][nq + 16 * k], st[k], ys);
+        }
+        if (kOut) {
+          ys = group_sum<16>(ys);
+          if (nq == 0)
+            p.g[(size_t)(t0 + i) * di + h * p.P + row] = fmaf(Dh, xv, ys) * silu_fast(zv[i]);
+        } else {
+          dsum += dt;
+        }
+      }
+    }
+  }
+  if (!kOut) {
+    float *hp = p.hloc + ((size_t)j * p.H + h) * tile + (size_t)row * N + nq;
+#pragma unroll
+    for (int k = 0; k < NPT; ++k) hp[16 * k] = st[k];
+    if (pb == 0 && tid == 0) p.dtsum[(size_t)j * p.H + h] = dsum;
+    return;
+  }
+  if (!(ch.w & kChunkLast)) return;
+  const int seq = ch.x;
+  float *sp = p.ssm + ((size_t)seq * p.H + h) * tile + (size_t)row * N + nq;
+#pragma unroll
+  for (int k = 0; k < NPT; ++k) sp[16 * k] = st[k];
+  if (!p.update_conv) return;
+  // The sequence's last K-1 conv inputs (old conv state followed by this call's rows), spread
+  // over the threads of the sequence's last-chunk blocks.
+  const int K1 = p.K - 1;
+  const int t0s = p.cu[seq], len = p.cu[seq + 1] - t0s;
+  for (int cc = blockIdx.x * kM2Threads + tid; cc < p.conv_n; cc += gridDim.x * kM2Threads) {
+    float nv[3];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      if (q >= K1) continue;
+      const int pos = len + q;
+      nv[q] = pos < K1 ? (p.fresh ? 0.f : p.conv[((size_t)seq * K1 + pos) * p.conv_n + cc])
+                       : p.zxd[(size_t)(t0s + pos - K1) * p.ldz + p.conv_col + cc];
+    }
+#pragma unroll
+    for (int q = 0; q < 3; ++q)
+      if (q < K1) p.conv[((size_t)seq * K1 + q) * p.conv_n + cc] = nv[q];
+  }
+}
+
+// Pass 2: per (sequence, head, row, state) element, chain the chunk end states into each
+// chunk's incoming state (written over hloc), from the SSM state (zero when fresh).
+constexpr int kM2CarryStage = 16;
+
+__global__ __launch_bounds__(256) void k_m2_carry(M2ScanArgs p) {
+  const size_t tile = (size_t)p.P * p.N;
+  const size_t e = (size_t)blockIdx.x * 256 + threadIdx.x;  // element of [H][P][N]
+  if (e >= tile * p.H) return;
+  const int b = blockIdx.y;
+  const int h = (int)(e / tile);
+  const float a2 = p.A2[h];
+  float H = p.fresh ? 0.f : p.ssm[(size_t)b * p.H * tile + e];
+  const int j0 = p.seq_chunk0[b], j1 = p.seq_chunk0[b + 1];
+  const size_t jstride = tile * p.H;
+  for (int jb = j0; jb < j1; jb += kM2CarryStage) {
+    float hl[kM2CarryStage], S[kM2CarryStage];
+#pragma unroll
+    for (int i = 0; i < kM2CarryStage; ++i) {
+      const int jj = jb + i;
+      const bool ok = jj < j1 - 1;
+      hl[i] = ok ? p.hloc[(size_t)jj * jstride + e] : 0.f;
+      S[i] = ok ? p.dtsum[(size_t)jj * p.H + h] : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < kM2CarryStage; ++i) {
+      const int jj = jb + i;
+      if (jj < j1) {
+        p.hloc[(size_t)jj * jstride + e] = H;
+        H = fmaf(exp2_fast(a2 * S[i]), H, hl[i]);
+      }
+    }
+  }
+}
+
+bool m2_args_ok(const M2ScanArgs &a) {
+  return a.zxd && a.xbc && a.dt_b && a.A2 && a.D && a.ssm && a.g && a.H > 0 && a.G > 0 &&
+         a.H % a.G == 0 && a.P > 0 && a.P % kM2Rows == 0 && a.di == a.H * a.P &&
+         (a.N == 32 || a.N == 64 || a.N == 128 || a.N == 256) &&
+         a.conv_n == a.di + 2 * a.G * a.N && a.dt_col >= 0 && a.ldz >= a.dt_col + a.H;
+}
+
+template <bool kOut>
+hipError_t m2_launch(const M2ScanArgs &a, int n_chunks, hipStream_t s) {
+  const dim3 grid(a.H * (a.P / kM2Rows), n_chunks);
+  switch (a.N) {
+    case 32: LL_LAUNCH((k_m2_scan<kOut, 2>), grid, dim3(kM2Threads), 0, s, a); break;
+    case 64: LL_LAUNCH((k_m2_scan<kOut, 4>), grid, dim3(kM2Threads), 0, s, a); break;
+    case 128: LL_LAUNCH((k_m2_scan<kOut, 8>), grid, dim3(kM2Threads), 0, s, a); break;
+    case 256: LL_LAUNCH((k_m2_scan<kOut, 16>), grid, dim3(kM2Threads), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int mamba2_chunk_len(int total, int n_heads, int head_dim) {
+  const long blocks_per_chunk = (long)n_heads * (head_dim / kM2Rows);
+  long len = (total * blocks_per_chunk + kM2TargetBlocks - 1) / kM2TargetBlocks;
+  len = (len + kM2Stage - 1) / kM2Stage * kM2Stage;
+  return (int)std::max<long>(len, kM2Stage);
+}
+
+int mamba2_max_chunks(int max_total, int max_batch, int n_heads, int head_dim) {
+  const long a = (max_total + kM2Stage - 1) / kM2Stage;
+  const long b = (long)kM2TargetBlocks / std::max(1, n_heads * (head_dim / kM2Rows)) + 1;
+  return (int)(std::min(a, b) + max_batch);
+}
+
+hipError_t launch_m2_scan_chunks(const M2ScanArgs &a, int n_chunks, hipStream_t s) {
+  if (n_chunks <= 0) return hipSuccess;
+  if (!m2_args_ok(a) || !a.chunks || !a.hloc || !a.dtsum) return hipErrorInvalidValue;
+  return m2_launch<false>(a, n_chunks, s);
+}
+
+hipError_t launch_m2_scan_carry(const M2ScanArgs &a, int batch, hipStream_t s) {
+  if (batch <= 0) return hipSuccess;
+  if (!m2_args_ok(a) || !a.seq_chunk0 || !a.hloc || !a.dtsum) return hipErrorInvalidValue;
+  const size_t elems = (size_t)a.H * a.P * a.N;
+  LL_LAUNCH(k_m2_carry, dim3((unsigned)((elems + 255) / 256), batch), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_m2_scan_out(const M2ScanArgs &a, int n_chunks, hipStream_t s) {
+  if (n_chunks <= 0) return hipSuccess;
+  if (!m2_args_ok(a) || (a.chunks && !a.cu) || (a.carry == 2 && !a.hloc) || a.carry < 0 ||
+      a.carry > 2 || (a.carry == 0 && !a.fresh) ||
+      (a.update_conv && (!a.conv || !a.cu || a.K < 1 || a.K > 4 || a.conv_col < 0)))
+    return hipErrorInvalidValue;
+  return m2_launch<true>(a, n_chunks, s);
+}
+
+}  // namespace ll

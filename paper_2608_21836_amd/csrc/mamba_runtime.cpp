@@ -258,16 +258,19 @@ ll_status enqueue_layers(ll_mamba *m, int rows, const PrefillPlan *pp, hipStream
       EpiParams ep;
       ep.kind = kEpiConv;
       ep.act = m->at(L.u);
-      ep.ld_act = di;
-      ep.out_f32 = m->at<float>(L.xz);  // z [rows][di]
+      ep.out_f32 = m->at<float>(L.xz);  // z at columns [di, 2 di)
+      ep.ld_out = 2 * di;
       ep.conv_state = m->conv_state(l);
       ep.conv_w = m->at<float>(L.conv_w[l]);
       ep.conv_b = m->at<float>(L.conv_b[l]);
       ep.conv_k = c.d_conv;
+      ep.conv_col0 = 0;
+      ep.conv_n = di;
       LL_HIP(gemm(m->at(L.h), d, fuse_norm ? &nrm : nullptr, m->at(L.w_in[l]), 2 * di, d, ep));
       SsmDecodeArgs sa;
       sa.u = m->at(L.u);
-      sa.z = m->at<float>(L.xz);
+      sa.z = m->at<float>(L.xz) + di;
+      sa.ldz = 2 * di;
       sa.wx = m->at(L.w_x[l]);
       sa.dtwT = m->at<float>(L.dtwT[l]);
       sa.dt_b = m->at<float>(L.dt_b[l]);

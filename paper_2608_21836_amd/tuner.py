@@ -78,6 +78,15 @@ MAMBA_KNOBS: List[Tuple[str, Tuple[int, ...], Tuple[str, ...]]] = [
 ]
 
 
+MAMBA2_KNOBS: List[Tuple[str, Tuple[int, ...], Tuple[str, ...]]] = [
+    ("prefill_tile", (0, 1, 2, 3), ("in_proj", "out_proj_resid")),
+    ("prefill_splitk", (1, 0), ("in_proj", "out_proj_resid")),
+    ("decode_splitk", (1, 0), ("in_proj", "out_proj_resid")),
+    ("decode_graph", (1, 0), ("in_proj", "scan", "out_proj_resid", "lm_head_argmax", "embed",
+                              "argmax_reduce", "rmsnorm", "gated_rmsnorm")),
+]
+
+
 def hotspot_scores(kernel_ms: Dict[Tuple[str, str], float], phase_ms: Dict[str, float],
                    invocations: Dict[str, int]) -> Dict[str, float]:
     """Eq. 1 over one workload.  kernel_ms[(phase, class)]: that class's summed kernel time
@@ -274,8 +283,16 @@ def main() -> int:
     import torch
     from synth import gen, get_config
     from synth import mamba as SM
+    from synth import mamba2 as S2
     torch.cuda.set_device(0)
-    if args.config in SM.MAMBA_CONFIGS or args.config in SM.MAMBA_TEST_CONFIGS:
+    if args.config in S2.MAMBA2_CONFIGS or args.config in S2.MAMBA2_TEST_CONFIGS:
+        from paper_2608_21836_amd.binding import MambaModel, upload_mamba_weights
+        cfg = S2.get_mamba2_config(args.config)
+        lens, packed = gen.prompt_tokens(cfg)
+        model = MambaModel(cfg, upload_mamba_weights(cfg, S2.weights(cfg)), max_batch=len(lens),
+                           max_prefill_tokens=int(sum(lens)))
+        knobs = MAMBA2_KNOBS
+    elif args.config in SM.MAMBA_CONFIGS or args.config in SM.MAMBA_TEST_CONFIGS:
         from paper_2608_21836_amd.binding import MambaModel, upload_mamba_weights
         cfg = SM.get_mamba_config(args.config)
         lens, packed = gen.prompt_tokens(cfg)
