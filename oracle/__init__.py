@@ -10,6 +10,8 @@ Parity status of each function (pins live in tests/test_oracle_pins.py):
   forward_full) -- all pinned (tests/test_mamba_oracle_pins.py).
   mamba2: ssd_scan, OracleMamba2 (prefill, extend, decode, forward_full) -- all pinned
   (tests/test_mamba2_oracle_pins.py).
+  rglru: gelu_tanh, sigmoid, rms_norm_offset, soft_cap, block_diag_apply, rg_lru, OracleRG
+  (prefill, extend, decode, forward_full) -- all pinned (tests/test_rglru_oracle_pins.py).
 """
 from .transformer import (  # noqa: F401
     OracleModel, apply_rope, argmax_lowest, causal_gqa_attention, rmsnorm, rope_frequencies,
