@@ -27,6 +27,7 @@ DECODER_OPTIONS = ("decode_graph", "prefill_splitk", "decode_splitk", "prefill_t
                    "attn_decode_chunk")
 MAMBA_OPTIONS = ("decode_graph", "prefill_splitk", "decode_splitk", "prefill_tile", "decode_fused")
 MAMBA2_OPTIONS = ("decode_graph", "prefill_splitk", "decode_splitk", "prefill_tile")
+RG_OPTIONS = MAMBA2_OPTIONS
 PHASES = ("prefill", "decode")
 
 
@@ -85,6 +86,30 @@ class LLMamba2Weights(ctypes.Structure):
 
 
 LL_M2K_COUNT = 12
+
+
+class LLRGConfig(ctypes.Structure):
+    _fields_ = [("n_layers", c_int32), ("d_model", c_int32), ("lru_width", c_int32),
+                ("n_heads", c_int32), ("mlp_width", c_int32), ("d_conv", c_int32),
+                ("vocab", c_int32), ("rms_eps", c_float), ("embed_scale", c_float),
+                ("logit_cap", c_float), ("dtype", c_int32), ("max_batch", c_int32),
+                ("max_prefill_tokens", c_int32)]
+
+
+RG_LAYER_FIELDS = ("norm_t", "linear_y", "linear_y_b", "linear_x", "linear_x_b", "conv_w",
+                   "conv_b", "gate_a", "gate_a_b", "gate_x", "gate_x_b", "lambda", "linear_out",
+                   "linear_out_b", "norm_c", "mlp_gate", "mlp_gate_b", "mlp_up", "mlp_up_b",
+                   "mlp_down", "mlp_down_b")
+RG_F32_FIELDS = ("linear_y_b", "linear_x_b", "conv_w", "conv_b", "gate_a_b", "gate_x_b",
+                 "lambda", "linear_out_b", "mlp_gate_b", "mlp_up_b", "mlp_down_b")
+
+
+class LLRGWeights(ctypes.Structure):
+    _fields_ = [("embed", c_void_p), ("final_norm", c_void_p)] + \
+        [(f, POINTER(c_void_p)) for f in RG_LAYER_FIELDS]
+
+
+LL_RGK_COUNT = 14
 
 # (name, restype, argtypes) of every exported symbol; include/ll.h, include/ll_ops.h and
 # include/ll_mamba.h declare the same set.
@@ -156,6 +181,21 @@ SIGNATURES = [
     ("ll_mamba2_kernel_timing_read", c_int32, [c_void_p, POINTER(c_int32), POINTER(c_double)]),
     ("ll_mamba2_kernel_class_name", c_char_p, [c_int32]),
     ("ll_mamba2_free", None, [c_void_p]),
+    ("ll_rg_workspace_size", c_int32, [POINTER(LLRGConfig), POINTER(c_size_t)]),
+    ("ll_rg_load", c_int32, [POINTER(LLRGConfig), POINTER(LLRGWeights), c_void_p, c_size_t,
+                             c_void_p, POINTER(c_void_p)]),
+    ("ll_rg_prefill", c_int32, [c_void_p, c_int32, POINTER(c_int32), c_void_p, c_void_p,
+                                c_void_p]),
+    ("ll_rg_decode_step", c_int32, [c_void_p, c_void_p, c_void_p, c_void_p]),
+    ("ll_rg_reset", c_int32, [c_void_p]),
+    ("ll_rg_seq_lengths", c_int32, [c_void_p, POINTER(c_int32), c_int32, POINTER(c_int32)]),
+    ("ll_rg_set_option", c_int32, [c_void_p, c_int32, c_int32]),
+    ("ll_rg_get_option", c_int32, [c_void_p, c_int32, POINTER(c_int32)]),
+    ("ll_rg_device_flags", c_int32, [c_void_p, POINTER(c_int32)]),
+    ("ll_rg_set_kernel_timing", c_int32, [c_void_p, c_int32]),
+    ("ll_rg_kernel_timing_read", c_int32, [c_void_p, POINTER(c_int32), POINTER(c_double)]),
+    ("ll_rg_kernel_class_name", c_char_p, [c_int32]),
+    ("ll_rg_free", None, [c_void_p]),
 ]
 
 _lib = None
@@ -351,12 +391,33 @@ def make_mamba2_config(cfg, max_batch: int, max_prefill_tokens: int) -> LLMamba2
                           max_prefill_tokens)
 
 
-class MambaModel:
-    """One loaded Mamba or Mamba2 model (cfg.family "mamba" / "mamba2"): workspace (a torch
-    uint8 tensor), handle and stream.  The two families differ only in the C entry points'
-    prefix (ll_mamba_* / ll_mamba2_*), the config and weight structs and the kernel classes.
+def make_rg_config(cfg, max_batch: int, max_prefill_tokens: int) -> LLRGConfig:
+    """LLRGConfig from a synth.rglru.RGConfig-like object."""
+    return LLRGConfig(cfg.n_layers, cfg.d_model, cfg.lru_width, cfg.n_heads, cfg.mlp_width,
+                      cfg.d_conv, cfg.vocab, float(cfg.rms_eps), float(cfg.embed_scale),
+                      float(cfg.logit_cap), LL_BF16 if cfg.dtype == "bf16" else LL_F32,
+                      max_batch, max_prefill_tokens)
 
-    ``weights`` maps synth.mamba / synth.mamba2 tensor names to CUDA tensors
+
+# per state-space family: (entry-point prefix, config maker, weight struct, per-layer fields,
+# fp32 fields, kernel class count, option names)
+_FAMILIES = {
+    "mamba": ("ll_mamba_", make_mamba_config, "LLMambaWeights", "MAMBA_LAYER_FIELDS",
+              "MAMBA_F32_FIELDS", "LL_MK_COUNT", "MAMBA_OPTIONS"),
+    "mamba2": ("ll_mamba2_", make_mamba2_config, "LLMamba2Weights", "MAMBA2_LAYER_FIELDS",
+               "MAMBA2_F32_FIELDS", "LL_M2K_COUNT", "MAMBA2_OPTIONS"),
+    "rglru": ("ll_rg_", make_rg_config, "LLRGWeights", "RG_LAYER_FIELDS", "RG_F32_FIELDS",
+              "LL_RGK_COUNT", "RG_OPTIONS"),
+}
+
+
+class MambaModel:
+    """One loaded state-space model of family cfg.family ("mamba", "mamba2" or "rglru"):
+    workspace (a torch uint8 tensor), handle and stream.  The families differ only in the C
+    entry points' prefix (ll_mamba_* / ll_mamba2_* / ll_rg_*), the config and weight structs,
+    the kernel classes and the options that apply.
+
+    ``weights`` maps synth.mamba / synth.mamba2 / synth.rglru tensor names to CUDA tensors
     (upload_mamba_weights)."""
 
     def __init__(self, cfg, weights: Dict[str, "object"], max_batch: int,
@@ -364,11 +425,14 @@ class MambaModel:
         import torch
         self.lib = load_library()
         self.mcfg = cfg
-        self.v2 = getattr(cfg, "family", "mamba") == "mamba2"
-        self.prefix = "ll_mamba2_" if self.v2 else "ll_mamba_"
-        self.n_classes = LL_M2K_COUNT if self.v2 else LL_MK_COUNT
-        self.cfg = (make_mamba2_config if self.v2 else make_mamba_config)(cfg, max_batch,
-                                                                          max_prefill_tokens)
+        self.family = getattr(cfg, "family", "mamba")
+        self.v2 = self.family == "mamba2"
+        prefix, make_cfg, wstruct, lfields, _, ncls, opts = _FAMILIES[self.family]
+        g = globals()
+        self.prefix = prefix
+        self.n_classes = g[ncls]
+        self.option_names = g[opts]
+        self.cfg = make_cfg(cfg, max_batch, max_prefill_tokens)
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         n = c_size_t(0)
         _check(self._fn("workspace_size")(ctypes.byref(self.cfg), ctypes.byref(n)),
@@ -377,11 +441,11 @@ class MambaModel:
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
         nl = cfg.n_layers
         keep, fields = [], {}
-        for key in (MAMBA2_LAYER_FIELDS if self.v2 else MAMBA_LAYER_FIELDS):
+        for key in g[lfields]:
             a = (c_void_p * nl)(*[weights[f"layers.{i}.{key}"].data_ptr() for i in range(nl)])
             keep.append(a)
             fields[key] = ctypes.cast(a, POINTER(c_void_p))
-        W = LLMamba2Weights if self.v2 else LLMambaWeights
+        W = g[wstruct]
         w = W(weights["embed"].data_ptr(), weights["final_norm"].data_ptr(), **fields)
         handle = c_void_p()
         _check(self._fn("load")(ctypes.byref(self.cfg), ctypes.byref(w), self.workspace.data_ptr(),
@@ -441,7 +505,7 @@ class MambaModel:
         return v.value
 
     def options(self) -> Dict[str, int]:
-        return {k: self.get_option(k) for k in (MAMBA2_OPTIONS if self.v2 else MAMBA_OPTIONS)}
+        return {k: self.get_option(k) for k in self.option_names}
 
     def seq_lengths(self) -> List[int]:
         out = (c_int32 * LL_MAX_BATCH)()
@@ -495,9 +559,9 @@ def upload_weights(cfg, weights) -> Dict[str, "object"]:
 
 
 def upload_mamba_weights(cfg, weights) -> Dict[str, "object"]:
-    """Mamba / Mamba2 tensors: the small per-channel / per-head ones (conv, dt, A_log, D) in
-    fp32, the rest in the workload dtype."""
-    f32 = MAMBA2_F32_FIELDS if getattr(cfg, "family", "mamba") == "mamba2" else MAMBA_F32_FIELDS
+    """Mamba / Mamba2 / RG-LRU tensors: the small per-channel / per-head ones (conv, dt,
+    A_log, D; biases and lambda) in fp32, the rest in the workload dtype."""
+    f32 = globals()[_FAMILIES[getattr(cfg, "family", "mamba")][4]]
     out = {}
     for k, v in weights.items():
         out[k] = to_device(v, "f32" if k.rsplit(".", 1)[-1] in f32 else cfg.dtype)

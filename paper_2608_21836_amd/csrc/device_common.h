@@ -163,6 +163,13 @@ __device__ __forceinline__ float softplus_f(float x) {
 // 2^x with the hardware instruction (results below the normal range flush to zero).
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float silu_fast(float z) { return __fdividef(z, 1.f + __expf(-z)); }
+__device__ __forceinline__ float sigmoid_f(float z) { return 1.0f / (1.0f + __expf(-z)); }
+// tanh-approximated GELU, x/2 (1 + tanh(y)) with y = sqrt(2/pi) (x + 0.044715 x^3), written
+// as x * sigmoid(2 y) (the same function: 1 + tanh(y) = 2 sigmoid(2 y)).
+__device__ __forceinline__ float gelu_tanh_f(float x) {
+  const float y2 = 1.5957691216057308f * fmaf(0.044715f * x, x * x, x);
+  return x / (1.0f + __expf(-y2));
+}
 
 // Merge of split-K attention partials, in split order: sum_s w_s o_s / sum_s w_s l_s, where
 // w_s = 2^(m_s - max_s m_s) (log-sum-exp rescaling of each split's unnormalised output o_s and

@@ -12,7 +12,8 @@ namespace {
 template <typename T>
 __global__ __launch_bounds__(256) void k_embed(const int *__restrict__ tokens,
                                                const T *__restrict__ table, int vocab, int d,
-                                               float *__restrict__ x, int *err) {
+                                               float *__restrict__ x, int *err,
+                                               float scale) {
   const int m = blockIdx.x;
   int t = tokens[m];
   if (t < 0 || t >= vocab) {
@@ -21,7 +22,7 @@ __global__ __launch_bounds__(256) void k_embed(const int *__restrict__ tokens,
   }
   const T *src = table + (size_t)t * d;
   float *dst = x + (size_t)m * d;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) dst[i] = to_f32(src[i]);
+  for (int i = threadIdx.x; i < d; i += blockDim.x) dst[i] = to_f32(src[i]) * scale;
 }
 
 // y[r, :] = x[src, :] / sqrt(mean(x[src, :]^2) + eps) * gain, src = rowmap ? rowmap[r] : r.
@@ -127,14 +128,14 @@ __global__ __launch_bounds__(256) void k_prefill_meta(PrefillMeta pm, int total,
 }  // namespace
 
 hipError_t launch_embed(int dtype, const int *tokens, int ntok, const void *table, int vocab,
-                        int d, float *x, int *err, hipStream_t s) {
+                        int d, float *x, int *err, hipStream_t s, float scale) {
   if (ntok <= 0) return hipSuccess;
   if (dtype == kF32)
     LL_LAUNCH(k_embed<float>, dim3(ntok), dim3(256), 0, s, tokens,
-                       reinterpret_cast<const float *>(table), vocab, d, x, err);
+                       reinterpret_cast<const float *>(table), vocab, d, x, err, scale);
   else
     LL_LAUNCH(k_embed<bf16>, dim3(ntok), dim3(256), 0, s, tokens,
-                       reinterpret_cast<const bf16 *>(table), vocab, d, x, err);
+                       reinterpret_cast<const bf16 *>(table), vocab, d, x, err, scale);
   return hipGetLastError();
 }
 

@@ -234,6 +234,121 @@ template <typename U> struct EpiConv {
   }
 };
 
+// out[m, n] += acc + bias[n]
+struct EpiBiasResid {
+  float *out;
+  int ld;
+  const float *bias;
+  static constexpr bool kArgmax = false, kPairs = false, kVec8 = false;
+  __device__ void one(int m, int col, float v) const {
+    out[(size_t)m * ld + col] += v + bias[col];
+  }
+  __device__ void operator()(int m, int u, int c, float v0, float v1) const {
+    one(m, 32 * u + c, v0);
+    one(m, 32 * u + 16 + c, v1);
+  }
+};
+
+template <typename T> struct EpiGeglu {
+  T *out;
+  int ld;
+  const float *bg, *bu;
+  static constexpr bool kArgmax = false, kPairs = true, kVec8 = true;
+  __device__ void operator()(int m, int u, int c, float g, float up) const {
+    const int j = 16 * u + c;
+    out[(size_t)m * ld + j] = from_f32<T>(gelu_tanh_f(g + bg[j]) * (up + bu[j]));
+  }
+  __device__ void vec8(int m, int u, int c0, const float *g, const float *up) const {
+    const int j0 = 16 * u + c0;
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = gelu_tanh_f(g[e] + bg[j0 + e]) * (up[e] + bu[j0 + e]);
+    store8<T>(out + (size_t)m * ld + j0, v);
+  }
+};
+
+// Recurrent-block input projection (see kEpiRgIn).
+template <typename T> struct EpiRgIn {
+  T *gy;             // [rows][W]
+  T *xc;             // decode: conv output [rows][W]
+  float *raw;        // prefill: linear_x output + bias [rows][ld_raw]
+  int ld_raw, W, K;
+  const float *by, *bx;
+  float *conv;       // decode: [rows][K-1][W]
+  const float *w, *b;
+  static constexpr bool kArgmax = false, kPairs = false, kVec8 = false;
+  __device__ void one(int m, int col, float v) const {
+    if (col < W) {
+      gy[(size_t)m * W + col] = from_f32<T>(gelu_tanh_f(v + by[col]));
+      return;
+    }
+    const int ch = col - W;
+    v += bx[ch];
+    if (!conv) {
+      raw[(size_t)m * ld_raw + ch] = v;
+      return;
+    }
+    float *st = conv + (size_t)m * (K - 1) * W + ch;
+    const float *wc = w + (size_t)ch * K;
+    float old[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+      if (k < K - 1) old[k] = st[(size_t)k * W];
+    float acc = b[ch];
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+      if (k < K - 1) acc = fmaf(wc[k], old[k], acc);
+    acc = fmaf(wc[K - 1], v, acc);
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+      if (k < K - 2) st[(size_t)k * W] = old[k + 1];
+    if (K > 1) st[(size_t)(K - 2) * W] = v;
+    xc[(size_t)m * W + ch] = from_f32<T>(acc);
+  }
+  __device__ void operator()(int m, int u, int c, float v0, float v1) const {
+    one(m, 32 * u + c, v0);
+    one(m, 32 * u + 16 + c, v1);
+  }
+};
+
+// RG-LRU gates (see kEpiRglru).  kGroupA: the GEMM kernels start the A operand of a block
+// whose first output column is n0 at column a_off(n0).
+template <typename T> struct EpiRglru {
+  const T *x;            // the gates' input rows [rows][W]
+  const float *ba, *bi, *lam;
+  int W, group_n, group_k;
+  float *aout, *gout;    // prefill
+  const int *row_seq, *cu;
+  int fresh;
+  float *state;          // decode
+  const T *gy;
+  T *out;
+  static constexpr bool kArgmax = false, kPairs = true, kVec8 = false, kGroupA = true;
+  __device__ size_t a_off(int n0) const { return (size_t)(n0 / group_n) * group_k; }
+  __device__ void operator()(int m, int u, int c, float ra, float ix) const {
+    const int j = 16 * u + c;
+    const float r = sigmoid_f(ra + ba[j]), ig = sigmoid_f(ix + bi[j]);
+    const float la = lam[j] * r;
+    const float a = __expf(la);
+    const bool reset = !state && fresh && m == cu[row_seq[m]];
+    const float mult = reset ? 1.f : sqrtf(-expm1f(2.f * la));
+    const float g = to_f32(x[(size_t)m * W + j]) * ig * mult;
+    if (!state) {
+      aout[(size_t)m * W + j] = reset ? 0.f : a;
+      gout[(size_t)m * W + j] = g;
+      return;
+    }
+    float *sp = state + (size_t)m * W + j;
+    const float h = fmaf(a, *sp, g);
+    *sp = h;
+    out[(size_t)m * W + j] = from_f32<T>(h * to_f32(gy[(size_t)m * W + j]));
+  }
+};
+
+template <typename E, typename = void> struct GroupA : std::false_type {};
+template <typename E>
+struct GroupA<E, std::void_t<decltype(E::kGroupA)>> : std::integral_constant<bool, E::kGroupA> {};
+
 // fp32 partial sums of one K range of a split GEMM: plane blockIdx.z of [split][M][ld].
 struct EpiPart {
   float *out;
@@ -315,6 +430,7 @@ __global__ __launch_bounds__(BN * 2, 1) void k_gemm_big(const T *__restrict__ A,
   const int gsize = min(ntm - first_m, GM);
   const int tm = first_m + (t % (GM * ntn)) % gsize, tn = (t % (GM * ntn)) / gsize;
   const int m0 = tm * BM, n0 = tn * BN;
+  if constexpr (GroupA<Epi>::value) A += epi.a_off(n0);
   const int kt_all = K / TK;                   // k-tiles of one 16-row weight block
   const int kt0 = blockIdx.z * ksteps;
   const int nsteps = min(ksteps, kt_all - kt0);
@@ -462,6 +578,7 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
   constexpr bool NORM = AM == kANorm;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int blk = blockIdx.x;
+  if constexpr (GroupA<Epi>::value) A += epi.a_off(16 * NB * blk);
   const int kb_n = K / TK;
   const int kb0 = (wave * kb_n) / NW, kb1 = ((wave + 1) * kb_n) / NW;
   const uint8_t *wp[NB];
@@ -815,6 +932,11 @@ hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k
   // when they fill the rounds clearly better (they run about 5-10 % below the big tiles).
   auto fill = [](int tiles) { return (double)tiles / (((tiles + 255) / 256) * 256); };
   bool prefer_half = fill(half_tiles) * 0.9 > fill(big_tiles);
+  // Grouped-A epilogues: a block's columns must stay in one group, and K is not split.
+  if constexpr (GroupA<Epi>::value) {
+    if (epi.group_n % 256 != 0) tile = kTileMid;
+    ws = nullptr;
+  }
   // A forced tile family (kTile256, kTile128x256, kTileMid) where the shape allows it.
   if (n % 256 != 0 && tile != kTileMid) tile = kTileAuto;
   if (tile == kTile256) prefer_half = false;
@@ -950,7 +1072,7 @@ hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm,
       if constexpr (E::kArgmax) return hipErrorInvalidValue;
       else return run_tiled<T>(a, lda, wt, m, n, k, epi, s, ws, ws_bytes, tile);
     } else {
-      if constexpr (!E::kArgmax) {
+      if constexpr (!E::kArgmax && !GroupA<E>::value) {
         if (plan.nsplit > 0 && !norm && ws && ws_bytes >= plan.ws_bytes) {
           const bool fuse_post = post && std::is_same<E, EpiResid>::value && n % 4 == 0;
           if (fuse_post && post_done) *post_done = true;
@@ -975,6 +1097,20 @@ hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm,
                              !ep.rope_cos || !ep.rope_sin))
     return hipErrorInvalidValue;
   if (norm && (!norm->x || !norm->gain)) return hipErrorInvalidValue;
+  if (ep.kind == kEpiBiasResid && (!ep.out_f32 || !ep.bias)) return hipErrorInvalidValue;
+  if (ep.kind == kEpiGeglu && (!ep.act || !ep.bias || !ep.bias2)) return hipErrorInvalidValue;
+  if (ep.kind == kEpiRgIn &&
+      (!ep.act || !ep.bias || !ep.bias2 || ep.width < 1 || n != 2 * ep.width ||
+       (ep.conv_state ? (!ep.act2 || !ep.conv_w || !ep.conv_b || ep.conv_k < 1 || ep.conv_k > 4)
+                      : (!ep.out_f32 || ep.ld_out < ep.width))))
+    return hipErrorInvalidValue;
+  if (ep.kind == kEpiRglru &&
+      (!ep.rg_x || !ep.bias || !ep.bias2 || !ep.lam || ep.width < 1 || n != 2 * ep.width ||
+       ep.group_n < 128 || ep.group_n % 128 != 0 || n % ep.group_n != 0 ||
+       ep.group_k != ep.group_n / 2 || lda < ep.width || norm || k != ep.group_k ||
+       (ep.rg_state ? (!ep.rg_gy || !ep.act)
+                    : (!ep.out_f32 || !ep.out2 || (ep.rg_fresh && (!ep.row_seq || !ep.cu))))))
+    return hipErrorInvalidValue;
   switch (ep.kind) {
     case kEpiStore: return run(EpiStore{ep.out_f32, ep.ld_out});
     case kEpiResid: return run(EpiResid{ep.out_f32, ep.ld_out});
@@ -993,6 +1129,18 @@ hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm,
       return run(EpiConv<float>{reinterpret_cast<float *>(ep.act), ep.out_f32, ep.ld_out,
                                 ep.conv_state, ep.conv_w, ep.conv_b, ep.conv_col0, ep.conv_n,
                                 ep.conv_k});
+    case kEpiBiasResid: return run(EpiBiasResid{ep.out_f32, ep.ld_out, ep.bias});
+    case kEpiGeglu:
+      return run(EpiGeglu<T>{reinterpret_cast<T *>(ep.act), ep.ld_act, ep.bias, ep.bias2});
+    case kEpiRgIn:
+      return run(EpiRgIn<T>{reinterpret_cast<T *>(ep.act), reinterpret_cast<T *>(ep.act2),
+                            ep.out_f32, ep.ld_out, ep.width, ep.conv_k, ep.bias, ep.bias2,
+                            ep.conv_state, ep.conv_w, ep.conv_b});
+    case kEpiRglru:
+      return run(EpiRglru<T>{reinterpret_cast<const T *>(ep.rg_x), ep.bias, ep.bias2, ep.lam,
+                             ep.width, ep.group_n, ep.group_k, ep.out_f32, ep.out2, ep.row_seq,
+                             ep.cu, ep.rg_fresh, ep.rg_state,
+                             reinterpret_cast<const T *>(ep.rg_gy), reinterpret_cast<T *>(ep.act)});
   }
   return hipErrorInvalidValue;
 }

@@ -54,6 +54,22 @@ enum EpiKind : int {
                    // -> act (element type T, row stride conv_n), conv state shifted; the other
                    // columns -> out_f32 (fp32, row stride ld_out) at their own index
   kEpiConvF32 = 6, // the same with act in fp32
+  kEpiBiasResid = 7,  // out_f32[m, n] += acc + bias[n]
+  kEpiGeglu = 8,      // act[m, j] = gelu_tanh(gate + bias[j]) * (up + bias2[j])  (kPermGlu)
+  kEpiRgIn = 9,       // recurrent-block input projection, columns [0, W) | [W, 2W):
+                      //   act[m, n] = gelu_tanh(acc + bias[n]) (type T, row stride W);
+                      //   v = acc + bias2[n - W]: with conv_state (decode, row = sequence) the
+                      //   conv step without activation -> act2 (type T, stride W), conv state
+                      //   shifted; without, v -> out_f32[m, n - W] (fp32, stride ld_out)
+  kEpiRglru = 10,     // RG-LRU gates on block-diagonal weights: per group of group_n output
+                      //   columns (a head: its recurrence-gate and input-gate rows interleaved
+                      //   as kPermGlu with ffn = group_n / 2) the A operand starts group_k
+                      //   columns further; pair (ra, ix) of channel j gives
+                      //   r = sigmoid(ra + bias[j]), i = sigmoid(ix + bias2[j]),
+                      //   log a = lam[j] r, g = x[m, j] i (reset ? 1 : sqrt(1 - a^2));
+                      //   prefill (no rg_state): out_f32 = (reset ? 0 : a), out2 = g, reset at
+                      //   the first row of a sequence of a fresh prefill (row_seq, cu);
+                      //   decode: h = a rg_state[m, j] + g -> rg_state, act = T(h * gy[m, j])
 };
 
 struct EpiParams {
@@ -76,6 +92,16 @@ struct EpiParams {
   float *conv_state = nullptr;
   const float *conv_w = nullptr, *conv_b = nullptr;
   int conv_k = 0, conv_col0 = 0, conv_n = 0;
+  // Bias epilogues and the recurrent block (kEpiBiasResid, kEpiGeglu, kEpiRgIn, kEpiRglru)
+  const float *bias = nullptr, *bias2 = nullptr;
+  void *act2 = nullptr;
+  float *out2 = nullptr;
+  const float *lam = nullptr;      // -c softplus(lambda) per channel
+  float *rg_state = nullptr;       // [rows][width] recurrent state (decode)
+  const void *rg_x = nullptr;      // the gates' A operand (type T, [rows][width])
+  const void *rg_gy = nullptr;     // gelu branch (type T, [rows][width]) (decode)
+  const int *cu = nullptr;         // first row of each sequence (prefill)
+  int rg_fresh = 0, width = 0, group_n = 0, group_k = 0;
 };
 
 // RMSNorm computed inside the decode GEMM (A = RMSNorm(x[rowmap[r]]) * gain).
@@ -135,7 +161,7 @@ constexpr int kPrefillSplitMax = 8;
 SplitKPlan prefill_splitk_plan(size_t elem, int m, int n, int k);
 
 hipError_t launch_embed(int dtype, const int *tokens, int ntok, const void *table, int vocab,
-                        int d, float *x, int *err_flags, hipStream_t s);
+                        int d, float *x, int *err_flags, hipStream_t s, float scale = 1.f);
 hipError_t launch_rmsnorm(int dtype, const float *x, int ldx, const int *rowmap, int rows,
                           int d, const void *gain, float eps, void *y, int ldy, hipStream_t s);
 // next[r] = column of the largest argmax partial of row r (lowest column on ties); lens_inc[r]
@@ -218,14 +244,15 @@ hipError_t launch_mamba_meta(const MambaMeta &mm, int total, int chunk_len, int 
 int mamba_chunk_len(int total, int di);
 int mamba_max_chunks(int max_total, int max_batch, int di);
 
-// u[r, c] = silu(b[c] + sum_k w[c][k] * xs[i - (K-1) + k]) where xs is row r's sequence: the
+// u[r, c] = act(b[c] + sum_k w[c][k] * xs[i - (K-1) + k]) where xs is row r's sequence: the
 // K-1 conv-state rows (zeros when `fresh`), then this call's x rows (fp32 xz[., c]); i is
-// r's index among its sequence's rows (row_seq / cu null: row r is sequence r, index 0).
+// r's index among its sequence's rows (row_seq / cu null: row r is sequence r, index 0);
+// act = 1: SiLU, 0: none.
 // conv_state [batch][K-1][di] fp32 (read only here), w [di][K], b [di].
 hipError_t launch_mamba_conv(int dtype, const float *xz, int ldxz, const int *row_seq,
                              const int *cu, const float *conv_state, int fresh,
                              const float *w, const float *b, int rows, int di, int K, void *u,
-                             hipStream_t s);
+                             hipStream_t s, int act = 1);
 
 struct ScanArgs {
   const float *xdbl = nullptr;  // [rows][ldx]: dt_low (R) | B (N) | C (N), fp32
@@ -317,5 +344,39 @@ struct M2ScanArgs {
 hipError_t launch_m2_scan_chunks(const M2ScanArgs &a, int n_chunks, hipStream_t s);
 hipError_t launch_m2_scan_carry(const M2ScanArgs &a, int batch, hipStream_t s);
 hipError_t launch_m2_scan_out(const M2ScanArgs &a, int n_chunks, hipStream_t s);
+
+// ------------------------------------------------------------------------------------------
+// RG-LRU recurrent block (Griffin).  The gate GEMM's epilogue (kEpiRglru) writes a (decay, 0 at
+// a reset) and g (normalised, gated input) per (row, channel); the prefill scan runs
+// h_t = a_t h_{t-1} + g_t per channel over time chunks and writes out = T(h * gy).
+// Pass 1 (launch_rg_scan_chunks): (prod a, h_end from zero) of every chunk but each sequence's
+// last.  Pass 3 (launch_rg_scan_out): incoming state chained from the sequence's state (zero
+// when fresh) through its earlier chunks, rescan, output, and at a sequence's last chunk the
+// recurrent state and the last K-1 conv inputs (from raw, after the old conv state).
+// Chunks come from launch_mamba_meta with chunk length rg_chunk_len(longest sequence), so a
+// sequence has at most kRgMaxChunksPerSeq chunks.
+constexpr int kRgMaxChunksPerSeq = 64;
+int rg_chunk_len(int max_len);
+struct RgScanArgs {
+  const float *a = nullptr, *g = nullptr;  // [rows][W]
+  const void *gy = nullptr;                // T [rows][W]
+  void *out = nullptr;                     // T [rows][W]
+  float *state = nullptr;                  // [batch][W]
+  float *hend = nullptr, *aprod = nullptr; // [chunks][W]
+  const int4 *chunks = nullptr;
+  const int *seq_chunk0 = nullptr, *cu = nullptr;
+  float *conv = nullptr;                   // [batch][K-1][W]
+  const float *raw = nullptr;              // conv inputs of this call [rows][ld_raw]
+  int ld_raw = 0, W = 0, K = 0, fresh = 0;
+};
+// gain_t / gain_c = 1 + norm_t / norm_c (type T, [d]); lam_out = -c softplus(lam) ([W]) when
+// lam is given.
+hipError_t launch_rg_prep(int dtype, const void *norm_t, const void *norm_c, int d,
+                          const float *lam, int W, float c, void *gain_t, void *gain_c,
+                          float *lam_out, hipStream_t s);
+// x[i] = cap * tanh(x[i] / cap) over n floats (soft-capped logits).
+hipError_t launch_softcap(float *x, long n, float cap, hipStream_t s);
+hipError_t launch_rg_scan_chunks(const RgScanArgs &a, int n_chunks, hipStream_t s);
+hipError_t launch_rg_scan_out(int dtype, const RgScanArgs &a, int n_chunks, hipStream_t s);
 
 }  // namespace ll

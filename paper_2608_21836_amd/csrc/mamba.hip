@@ -69,7 +69,7 @@ __global__ __launch_bounds__(256) void k_mamba_conv(const float *__restrict__ xz
                                                     const float *__restrict__ conv, int fresh,
                                                     const float *__restrict__ w,
                                                     const float *__restrict__ b, int rows,
-                                                    int di, int K, T *__restrict__ u) {
+                                                    int di, int K, int act, T *__restrict__ u) {
   const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (long)rows * di) return;
   const int r = (int)(idx / di), c = (int)(idx - (long)r * di);
@@ -83,7 +83,7 @@ __global__ __launch_bounds__(256) void k_mamba_conv(const float *__restrict__ xz
     else v = fresh ? 0.f : conv[((size_t)seq * (K - 1) + (K - 1) + q) * di + c];
     acc = fmaf(w[c * K + k], v, acc);
   }
-  u[(size_t)r * di + c] = from_f32<T>(silu_f(acc));
+  u[(size_t)r * di + c] = from_f32<T>(act ? silu_f(acc) : acc);
 }
 
 // Passes 1 (kOut = false) and 3 (kOut = true) of the scan; one wave per (channel block, chunk).
@@ -494,7 +494,8 @@ hipError_t launch_mamba_meta(const MambaMeta &mm, int total, int chunk_len, int 
 
 hipError_t launch_mamba_conv(int dtype, const float *xz, int ldxz, const int *row_seq,
                              const int *cu, const float *conv_state, int fresh, const float *w,
-                             const float *b, int rows, int di, int K, void *u, hipStream_t s) {
+                             const float *b, int rows, int di, int K, void *u, hipStream_t s,
+                             int act) {
   if (rows <= 0) return hipSuccess;
   if (!xz || !w || !b || !u || K < 1 || K > 4 || (!fresh && !conv_state) ||
       ((row_seq == nullptr) != (cu == nullptr)))
@@ -503,10 +504,10 @@ hipError_t launch_mamba_conv(int dtype, const float *xz, int ldxz, const int *ro
   const dim3 grid((unsigned)((n + 255) / 256));
   if (dtype == kF32)
     LL_LAUNCH(k_mamba_conv<float>, grid, dim3(256), 0, s, xz, ldxz, row_seq, cu, conv_state,
-              fresh, w, b, rows, di, K, reinterpret_cast<float *>(u));
+              fresh, w, b, rows, di, K, act, reinterpret_cast<float *>(u));
   else
     LL_LAUNCH(k_mamba_conv<bf16>, grid, dim3(256), 0, s, xz, ldxz, row_seq, cu, conv_state,
-              fresh, w, b, rows, di, K, reinterpret_cast<bf16 *>(u));
+              fresh, w, b, rows, di, K, act, reinterpret_cast<bf16 *>(u));
   return hipGetLastError();
 }
 

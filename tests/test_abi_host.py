@@ -15,7 +15,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 def declared_functions():
     names = set()
-    for h in ("ll.h", "ll_ops.h", "ll_mamba.h", "ll_mamba2.h"):
+    for h in ("ll.h", "ll_ops.h", "ll_mamba.h", "ll_mamba2.h", "ll_rglru.h"):
         text = open(os.path.join(ROOT, "include", h)).read()
         text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
         names |= set(re.findall(r"\b(ll_\w+)\s*\(", text))
