@@ -185,6 +185,46 @@ def algorithmic_work_mamba2(cfg, lens, n_decode):
     return w
 
 
+def algorithmic_work_rg(cfg, lens, n_decode):
+    """{(phase, class): (work, unit)} summed over one RG-LRU job.  Projections (the
+    block-diagonal gates included) count MFMA flops; the conv and the two scan passes count
+    bytes (they stream fp32 rows: the scan reads the decay and gated input of every (token,
+    channel), pass 3 also the gelu branch, and writes the block output).  Decode: weights once
+    per step, biases, conv and recurrent state read and written, activations."""
+    eb = 2 if cfg.dtype == "bf16" else 4
+    B, T = len(lens), sum(lens)
+    d, W, F, bw, K, V, L = (cfg.d_model, cfg.lru_width, cfg.mlp_width, cfg.block_width,
+                            cfg.d_conv, cfg.vocab, cfg.n_layers)
+    N = n_decode
+    w = {}
+    w[("prefill", "in_proj")] = (2.0 * T * 2 * W * d * L, "flop")
+    w[("prefill", "gates")] = (2.0 * T * 2 * W * bw * L, "flop")
+    w[("prefill", "out_proj_resid")] = (2.0 * T * d * W * L, "flop")
+    w[("prefill", "mlp_up")] = (2.0 * T * 2 * F * d * L, "flop")
+    w[("prefill", "mlp_down")] = (2.0 * T * d * F * L, "flop")
+    w[("prefill", "conv")] = (float(L * (T * W * (4 + eb) + W * (K + 1) * 4)), "byte")
+    w[("prefill", "scan_chunk")] = (float(L * T * W * 8), "byte")
+    w[("prefill", "scan")] = (float(L * T * W * (8 + 2 * eb)), "byte")
+    w[("prefill", "lm_head_argmax")] = (float(V * d * eb + B * d * eb + B * (V // 32) * 8), "byte")
+    w[("prefill", "rmsnorm")] = (float((2 * L * T + B) * d * (4 + eb)), "byte")
+    w[("prefill", "embed")] = (float(T * d * (eb + 4)), "byte")
+    w[("decode", "in_proj")] = (float(N * L * (2 * W * d * eb + B * d * 4 + 2 * B * W * eb
+                                               + 2 * B * (K - 1) * W * 4 + W * (K + 3) * 4)),
+                                "byte")
+    w[("decode", "gates")] = (float(N * L * (2 * W * bw * eb + 3 * B * W * eb + 3 * W * 4
+                                             + 2 * B * W * 4)), "byte")
+    w[("decode", "out_proj_resid")] = (float(N * L * (d * W * eb + B * W * eb + d * 4
+                                                      + 2 * B * d * 4)), "byte")
+    w[("decode", "mlp_up")] = (float(N * L * (2 * F * d * eb + B * d * 4 + B * F * eb + 2 * F * 4)),
+                               "byte")
+    w[("decode", "mlp_down")] = (float(N * L * (d * F * eb + B * F * eb + d * 4 + 2 * B * d * 4)),
+                                 "byte")
+    w[("decode", "lm_head_argmax")] = (float(N * (V * d * eb + B * d * eb + B * (V // 32) * 8)), "byte")
+    w[("decode", "rmsnorm")] = (float(N * (2 * L + 1) * B * d * (4 + eb)), "byte")
+    w[("decode", "embed")] = (float(N * B * d * (eb + 4)), "byte")
+    return w
+
+
 # fp32 vector peak of the chip: 256 CUs x 128 fp32 FMA lanes x 2 flops x 2.4 GHz
 ALU_PEAK_TFLOPS = 157.3
 
@@ -247,10 +287,20 @@ def cpu_baseline(cfg, lens, packed, n_decode, budget_s):
             "decode_tok_s": round(len(prompts) * steps / t_dec, 3) if steps else None}
 
 
-def cpu_baseline_mamba(cfg, lens, packed, n_decode, budget_s):
-    """The Mamba / Mamba2 oracle on the host, as cpu_baseline does for the decoder."""
+def cpu_baseline_mamba(cfg, lens, packed, n_decode, budget_s, weights=None):
+    """The Mamba / Mamba2 / RG-LRU oracle on the host, as cpu_baseline does for the decoder.
+    The RG-LRU workload's fp64 prefill of the whole prompt alone would exceed the budget, so
+    its sample is each prompt's first 128 tokens, then decode steps while the budget lasts."""
     from oracle import argmax_lowest, split_prompts
-    if cfg.family == "mamba2":
+    prompts = split_prompts(lens, packed)
+    sample = "all prompts prefilled"
+    if cfg.family == "rglru":
+        from oracle.rglru import OracleRG
+        from synth import rglru as SR
+        om = OracleRG(cfg, weights if weights is not None else SR.weights(cfg))
+        prompts = [p[:128] for p in prompts]
+        sample = "the first 128 tokens of every prompt prefilled"
+    elif cfg.family == "mamba2":
         from oracle.mamba2 import OracleMamba2
         from synth import mamba2 as S2
         om = OracleMamba2(cfg, S2.weights(cfg))
@@ -258,7 +308,6 @@ def cpu_baseline_mamba(cfg, lens, packed, n_decode, budget_s):
         from oracle.mamba import OracleMamba
         from synth import mamba as SM
         om = OracleMamba(cfg, SM.weights(cfg))
-    prompts = split_prompts(lens, packed)
     t0 = time.perf_counter()
     toks = argmax_lowest(om.prefill(prompts))
     t_pre = time.perf_counter() - t0
@@ -271,7 +320,7 @@ def cpu_baseline_mamba(cfg, lens, packed, n_decode, budget_s):
     n_pre = sum(len(p) for p in prompts)
     return {"value": round((n_pre + len(prompts) * steps) / (t_pre + t_dec), 3), "unit": "tok/s",
             "cores": blas_threads(), "kind": "oracle",
-            "sample": f"all prompts prefilled ({n_pre} tokens, sequential scan, {t_pre:.2f} s), "
+            "sample": f"{sample} ({n_pre} tokens, sequential scan, {t_pre:.2f} s), "
                       f"then {steps} of {n_decode} greedy decode steps ({t_dec:.2f} s); fp64 numpy",
             "prefill_tok_s": round(n_pre / t_pre, 3),
             "decode_tok_s": round(len(prompts) * steps / t_dec, 3) if steps else None}
@@ -283,8 +332,8 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="125m",
-                    help="workload name (synth.configs, or a Mamba / Mamba2 workload of "
-                         "synth.mamba / synth.mamba2)")
+                    help="workload name (synth.configs, or a Mamba / Mamba2 / RG-LRU workload "
+                         "of synth.mamba / synth.mamba2 / synth.rglru)")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
@@ -311,17 +360,25 @@ def main() -> int:
     from synth import mamba as SM
 
     from synth import mamba2 as S2
+    from synth import rglru as SR
     torch.cuda.set_device(0)
+    rg = args.config in SR.RG_CONFIGS or args.config in SR.RG_TEST_CONFIGS
     mamba2 = args.config in S2.MAMBA2_CONFIGS or args.config in S2.MAMBA2_TEST_CONFIGS
-    mamba = mamba2 or args.config in SM.MAMBA_CONFIGS or args.config in SM.MAMBA_TEST_CONFIGS
-    cfg = (S2.get_mamba2_config(args.config) if mamba2 else
+    # the state-space families (Mamba, Mamba2, RG-LRU) share the MambaModel binding
+    mamba = rg or mamba2 or args.config in SM.MAMBA_CONFIGS or args.config in SM.MAMBA_TEST_CONFIGS
+    cfg = (SR.get_rg_config(args.config) if rg else
+           S2.get_mamba2_config(args.config) if mamba2 else
            SM.get_mamba_config(args.config) if mamba else get_config(args.config))
+    host_w = None
     lens, packed = gen.prompt_tokens(cfg)
     B, T, N = len(lens), int(sum(lens)), cfg.n_decode
     print(f"[bench] {cfg.name}: uploading weights", file=sys.stderr, flush=True)
     if mamba:
         from paper_2608_21836_amd.binding import MambaModel, upload_mamba_weights
-        dev_w = upload_mamba_weights(cfg, (S2 if mamba2 else SM).weights(cfg))
+        host_w = (SR if rg else S2 if mamba2 else SM).weights(cfg)
+        dev_w = upload_mamba_weights(cfg, host_w)
+        if not rg:
+            host_w = None
         model = MambaModel(cfg, dev_w, max_batch=B, max_prefill_tokens=T)
         reset = model.reset
         from paper_2608_21836_amd.tuner import accepted_options
@@ -329,7 +386,13 @@ def main() -> int:
         options.update(dict(o.split("=", 1) for o in args.option))
         for name, value in options.items():
             model.set_option(name, int(value))
-        if mamba2:
+        if rg:
+            work_all = algorithmic_work_rg(cfg, lens, N)
+            desc = {"workload": cfg.name, "family": "rglru", "layers": cfg.n_layers,
+                    "d_model": cfg.d_model, "lru_width": cfg.lru_width,
+                    "blocks": f"{cfg.n_heads}x{cfg.block_width}", "mlp_width": cfg.mlp_width,
+                    "d_conv": cfg.d_conv, "vocab": cfg.vocab}
+        elif mamba2:
             work_all = algorithmic_work_mamba2(cfg, lens, N)
             desc = {"workload": cfg.name, "family": "mamba2", "layers": cfg.n_layers,
                     "d_model": cfg.d_model, "d_inner": cfg.d_inner, "d_state": cfg.d_state,
@@ -432,7 +495,8 @@ def main() -> int:
         "decode": {"achieved": round(dec_byte / (dec_ms / 1e3) / 1e9, 2), "unit": "GB/s",
                    "peak": HBM_PEAK_GBS,
                    "frac": round(dec_byte / (dec_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
-                   "work": "weights, " + ("conv and SSM state" if mamba else "KV cache")
+                   "work": "weights, " + ("conv and recurrent state" if rg else
+                                          "conv and SSM state" if mamba else "KV cache")
                            + ", activations per step"},
     }
 
@@ -470,8 +534,11 @@ def main() -> int:
 
     if not args.no_cpu_baseline:
         print("[bench] oracle cpu baseline", file=sys.stderr, flush=True)
-        fn = cpu_baseline_mamba if mamba else cpu_baseline
-        out["cpu_baseline"] = fn(cfg, lens, packed, N, args.cpu_budget)
+        if mamba:
+            out["cpu_baseline"] = cpu_baseline_mamba(cfg, lens, packed, N, args.cpu_budget,
+                                                     host_w)
+        else:
+            out["cpu_baseline"] = cpu_baseline(cfg, lens, packed, N, args.cpu_budget)
     model.close()
     print(json.dumps(out), flush=True)
     return 0

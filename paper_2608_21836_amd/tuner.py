@@ -87,6 +87,15 @@ MAMBA2_KNOBS: List[Tuple[str, Tuple[int, ...], Tuple[str, ...]]] = [
 ]
 
 
+RG_KNOBS: List[Tuple[str, Tuple[int, ...], Tuple[str, ...]]] = [
+    ("prefill_tile", (0, 1, 2, 3), ("in_proj", "gates", "out_proj_resid", "mlp_up", "mlp_down")),
+    ("prefill_splitk", (1, 0), ("in_proj", "out_proj_resid", "mlp_up", "mlp_down")),
+    ("decode_splitk", (1, 0), ("in_proj", "out_proj_resid", "mlp_up", "mlp_down")),
+    ("decode_graph", (1, 0), ("in_proj", "gates", "out_proj_resid", "mlp_up", "mlp_down",
+                              "lm_head_argmax", "embed", "argmax_reduce", "rmsnorm")),
+]
+
+
 def hotspot_scores(kernel_ms: Dict[Tuple[str, str], float], phase_ms: Dict[str, float],
                    invocations: Dict[str, int]) -> Dict[str, float]:
     """Eq. 1 over one workload.  kernel_ms[(phase, class)]: that class's summed kernel time
@@ -284,8 +293,16 @@ def main() -> int:
     from synth import gen, get_config
     from synth import mamba as SM
     from synth import mamba2 as S2
+    from synth import rglru as SR
     torch.cuda.set_device(0)
-    if args.config in S2.MAMBA2_CONFIGS or args.config in S2.MAMBA2_TEST_CONFIGS:
+    if args.config in SR.RG_CONFIGS or args.config in SR.RG_TEST_CONFIGS:
+        from paper_2608_21836_amd.binding import MambaModel, upload_mamba_weights
+        cfg = SR.get_rg_config(args.config)
+        lens, packed = gen.prompt_tokens(cfg)
+        model = MambaModel(cfg, upload_mamba_weights(cfg, SR.weights(cfg)), max_batch=len(lens),
+                           max_prefill_tokens=int(sum(lens)))
+        knobs = RG_KNOBS
+    elif args.config in S2.MAMBA2_CONFIGS or args.config in S2.MAMBA2_TEST_CONFIGS:
         from paper_2608_21836_amd.binding import MambaModel, upload_mamba_weights
         cfg = S2.get_mamba2_config(args.config)
         lens, packed = gen.prompt_tokens(cfg)
