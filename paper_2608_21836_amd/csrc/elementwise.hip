@@ -64,29 +64,46 @@ __device__ __forceinline__ void better(float &bv, int &bi, float ov, int oi) {
 }
 
 // next[r] = column of the largest partial (lowest column on ties); lens_inc[r] += 1 if given.
-__global__ __launch_bounds__(256) void k_argmax_reduce(const float *__restrict__ pval,
-                                                       const int *__restrict__ pidx, int n_parts,
-                                                       int *__restrict__ next, int *lens_inc) {
+// One block of 1024 threads per row; each thread requests 8 partials at a time, so a
+// 256000-entry vocabulary (8000 partials) is one round of loads.
+constexpr int kArgThreads = 1024, kArgBatch = 8;
+__global__ __launch_bounds__(kArgThreads) void k_argmax_reduce(const float *__restrict__ pval,
+                                                               const int *__restrict__ pidx,
+                                                               int n_parts, int *__restrict__ next,
+                                                               int *lens_inc) {
   const int r = blockIdx.x;
+  const float *pv = pval + (size_t)r * n_parts;
+  const int *pi = pidx + (size_t)r * n_parts;
   float bv = -INFINITY;
   int bi = 0x7fffffff;
-  for (int i = threadIdx.x; i < n_parts; i += 256)
-    better(bv, bi, pval[(size_t)r * n_parts + i], pidx[(size_t)r * n_parts + i]);
+  for (int i0 = threadIdx.x; i0 < n_parts; i0 += kArgThreads * kArgBatch) {
+    float v[kArgBatch];
+    int ix[kArgBatch];
+#pragma unroll
+    for (int q = 0; q < kArgBatch; ++q) {
+      const int i = i0 + q * kArgThreads;
+      v[q] = i < n_parts ? pv[i] : -INFINITY;
+      ix[q] = i < n_parts ? pi[i] : 0x7fffffff;
+    }
+#pragma unroll
+    for (int q = 0; q < kArgBatch; ++q) better(bv, bi, v[q], ix[q]);
+  }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     const float ov = __shfl_xor(bv, o);
     const int oi = __shfl_xor(bi, o);
     better(bv, bi, ov, oi);
   }
-  __shared__ float sv[4];
-  __shared__ int si[4];
+  constexpr int NWV = kArgThreads / 64;
+  __shared__ float sv[NWV];
+  __shared__ int si[NWV];
   if ((threadIdx.x & 63) == 0) {
     sv[threadIdx.x >> 6] = bv;
     si[threadIdx.x >> 6] = bi;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    for (int w = 1; w < 4; ++w) better(bv, bi, sv[w], si[w]);
+    for (int w = 1; w < NWV; ++w) better(bv, bi, sv[w], si[w]);
     next[r] = bi;
     if (lens_inc) lens_inc[r] += 1;
   }
@@ -157,7 +174,8 @@ hipError_t launch_argmax_reduce(const float *pval, const int *pidx, int rows, in
                                 int *next, int *lens_inc, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (!pval || !pidx || !next) return hipErrorInvalidValue;
-  LL_LAUNCH(k_argmax_reduce, dim3(rows), dim3(256), 0, s, pval, pidx, n_parts, next, lens_inc);
+  LL_LAUNCH(k_argmax_reduce, dim3(rows), dim3(kArgThreads), 0, s, pval, pidx, n_parts, next,
+            lens_inc);
   return hipGetLastError();
 }
 

@@ -159,3 +159,87 @@ def test_option_calls_reject_a_null_model(lib):
     assert lib.ll_set_option(None, 0, 1) == B.LL_ERR_INVALID_ARGUMENT
     assert lib.ll_get_option(None, 0, ctypes.byref(v)) == B.LL_ERR_INVALID_ARGUMENT
     assert set(B.OPTIONS.values()) == set(range(len(B.OPTIONS)))
+
+
+# ------------------------------------------------------------------------------------------
+# State-space families (ll_mamba.h, ll_mamba2.h, ll_rglru.h): host-side checks only
+# ------------------------------------------------------------------------------------------
+def _ssm_families():
+    from synth import mamba as SM
+    from synth import mamba2 as S2
+    from synth import rglru as SR
+    out = []
+    for prefix, make, cfgs in (("ll_mamba_", B.make_mamba_config, {**SM.MAMBA_CONFIGS, **SM.MAMBA_TEST_CONFIGS}),
+                               ("ll_mamba2_", B.make_mamba2_config, {**S2.MAMBA2_CONFIGS, **S2.MAMBA2_TEST_CONFIGS}),
+                               ("ll_rg_", B.make_rg_config, {**SR.RG_CONFIGS, **SR.RG_TEST_CONFIGS})):
+        for name, c in cfgs.items():
+            out.append((prefix, make, c))
+    return out
+
+
+def _ssm_status(lib, prefix, cfg):
+    n = ctypes.c_size_t(0)
+    return getattr(lib, prefix + "workspace_size")(ctypes.byref(cfg), ctypes.byref(n)), n.value
+
+
+@pytest.mark.parametrize("prefix,make,c", _ssm_families(), ids=lambda v: getattr(v, "name", str(v)))
+def test_ssm_workspace_size_of_every_workload(lib, prefix, make, c):
+    lens = c.prompt_list or ([c.prompt_len] * c.batch if c.prompt_len else [c.prompt_range[1]] * c.batch)
+    st, n = _ssm_status(lib, prefix, make(c, c.batch, sum(lens)))
+    assert st == B.LL_OK, lib.ll_last_error()
+    eb = 2 if c.dtype == "bf16" else 4
+    assert n > (2 * c.vocab * c.d_model + c.n_layers * c.linear_params_per_layer()) * eb
+
+
+def _rg_cfg(**over):
+    from synth import rglru as SR
+    cfg = B.make_rg_config(SR.RG_TEST_CONFIGS["t-rg-f32"], 2, 256)
+    for k, v in over.items():
+        setattr(cfg, k, v)
+    return cfg
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("n_heads", 3, B.LL_ERR_UNSUPPORTED),          # blocks of 256 / 3 columns
+    ("lru_width", 320, B.LL_ERR_UNSUPPORTED),      # blocks of 80
+    ("mlp_width", 100, B.LL_ERR_UNSUPPORTED),
+    ("d_model", 200, B.LL_ERR_UNSUPPORTED),
+    ("d_conv", 5, B.LL_ERR_UNSUPPORTED),
+    ("vocab", 1000, B.LL_ERR_UNSUPPORTED),
+    ("max_batch", 257, B.LL_ERR_UNSUPPORTED),
+    ("logit_cap", 0.0, B.LL_ERR_INVALID_ARGUMENT),
+    ("embed_scale", float("inf"), B.LL_ERR_INVALID_ARGUMENT),
+    ("rms_eps", float("nan"), B.LL_ERR_INVALID_ARGUMENT),
+    ("n_layers", 0, B.LL_ERR_INVALID_ARGUMENT),
+])
+def test_rg_config_validation(lib, field, value, status):
+    st, _ = _ssm_status(lib, "ll_rg_", _rg_cfg(**{field: value}))
+    assert st == status
+    assert lib.ll_last_error()
+
+
+def test_rg_null_arguments_and_workspace_checks(lib):
+    cfg = _rg_cfg()
+    assert lib.ll_rg_workspace_size(None, ctypes.byref(ctypes.c_size_t())) == B.LL_ERR_INVALID_ARGUMENT
+    h = ctypes.c_void_p()
+    assert lib.ll_rg_load(ctypes.byref(cfg), None, None, 0, None, ctypes.byref(h)) == \
+        B.LL_ERR_INVALID_ARGUMENT
+    nl = cfg.n_layers
+    arr = (ctypes.c_void_p * nl)(*([0x1000] * nl))
+    p = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+    w = B.LLRGWeights(0x1000, 0x1000, **{f: p for f in B.RG_LAYER_FIELDS})
+    # misaligned workspace, then one too small: rejected before any device call
+    assert lib.ll_rg_load(ctypes.byref(cfg), ctypes.byref(w), 0x1001, 1 << 40, None,
+                          ctypes.byref(h)) != B.LL_OK
+    assert lib.ll_rg_load(ctypes.byref(cfg), ctypes.byref(w), 0x100000, 16, None,
+                          ctypes.byref(h)) == B.LL_ERR_WORKSPACE
+    w.mlp_down_b = None
+    assert lib.ll_rg_load(ctypes.byref(cfg), ctypes.byref(w), 0x100000, 1 << 40, None,
+                          ctypes.byref(h)) == B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_rg_prefill(None, 1, None, None, None, None) == B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_rg_decode_step(None, None, None, None) == B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_rg_reset(None) == B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_rg_set_option(None, 0, 1) == B.LL_ERR_INVALID_ARGUMENT
+    assert lib.ll_rg_kernel_class_name(B.LL_RGK_COUNT) == b""
+    assert lib.ll_rg_kernel_class_name(5) == b"gates"
+    lib.ll_rg_free(None)
