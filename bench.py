@@ -345,6 +345,11 @@ def main() -> int:
     ap.add_argument("--option", action="append", default=[], metavar="NAME=VALUE",
                     help="set an implementation option after loading (repeatable; applied "
                          "after the accepted ones)")
+    ap.add_argument("--kv-page", type=int, default=0,
+                    help="decoder workloads: paged KV cache with pages of this many positions "
+                         "(a multiple of 256; 0 = one contiguous slab per sequence)")
+    ap.add_argument("--kv-pages", type=int, default=0,
+                    help="pages in the pool (0 with --kv-page: exactly the pages the job needs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 256 MiB device copy kernel (reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters of a rocprofv3 --pmc run)")
@@ -412,12 +417,18 @@ def main() -> int:
         dev_w = {name: to_device(arr, cfg.dtype)
                  for name, arr in gen.iter_weights_parallel(cfg, workers)}
         dev_w.update({k: to_device(v, cfg.dtype) for k, v in gen.gains(cfg).items()})
-        model = Model(cfg, dev_w, max_batch=B, max_prefill_tokens=T, max_ctx=max(lens) + N)
+        kv_pages = args.kv_pages
+        if args.kv_page and not kv_pages:
+            kv_pages = sum((int(x) + N + args.kv_page - 1) // args.kv_page for x in lens)
+        model = Model(cfg, dev_w, max_batch=B, max_prefill_tokens=T, max_ctx=max(lens) + N,
+                      kv_page=args.kv_page, kv_pages=kv_pages)
         reset = model.kv_reset
         work_all = algorithmic_work(cfg, lens, N)
         desc = {"workload": cfg.name, "layers": cfg.n_layers, "d_model": cfg.d_model,
                 "heads": f"{cfg.n_heads}/{cfg.n_kv_heads}x{cfg.head_dim}", "ffn": cfg.ffn_dim,
                 "vocab": cfg.vocab}
+        if args.kv_page:
+            desc.update({"kv_page": args.kv_page, "kv_pages": kv_pages})
         from paper_2608_21836_amd.tuner import accepted_options
         options = {} if args.no_accepted_options else accepted_options(cfg.name)
         options.update(dict(o.split("=", 1) for o in args.option))

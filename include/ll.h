@@ -58,6 +58,16 @@ typedef struct {
   int32_t max_batch;          /* sequences per prefill / decode step */
   int32_t max_prefill_tokens; /* total prompt tokens of one prefill */
   int32_t max_ctx;            /* per-sequence cache capacity (prompt + decoded tokens) */
+  /* Paged KV cache (vLLM-style block table; the paper's continuous-batching discussion
+   * names paging as the missing piece for mixed phases).  kv_page = 0: one contiguous slab
+   * of max_ctx positions per (sequence, kv head).  kv_page > 0 (a multiple of 256): the
+   * cache of each layer is a pool of kv_pages pages of kv_page positions for every kv head
+   * (kv_pages = 0: max_batch * ceil(max_ctx / kv_page)); a sequence holds ceil(len /
+   * kv_page) pages, taken from the pool when ll_prefill or ll_decode_step first writes a
+   * position in them and returned by ll_kv_reset, so sequences of different lengths share a
+   * pool smaller than max_batch full contexts.  The block table lives in the workspace. */
+  int32_t kv_page;
+  int32_t kv_pages;
 } ll_config;
 
 #define LL_MAX_BATCH 256
@@ -102,8 +112,9 @@ ll_status ll_model_load(const ll_config *cfg, const ll_weights *w, void *workspa
  * sequence's last new position (lowest index on ties) and, if logits_dev is not NULL, the
  * fp32 logits [batch, vocab].  Afterwards len[b] grows by seq_lens_host[b].
  * LL_ERR_STATE if the cache holds a different number of sequences (ll_kv_reset starts new
- * ones); LL_ERR_CAPACITY if batch > max_batch, sum(seq_lens) > max_prefill_tokens or some
- * len[b] + seq_lens_host[b] > max_ctx. */
+ * ones); LL_ERR_CAPACITY if batch > max_batch, sum(seq_lens) > max_prefill_tokens, some
+ * len[b] + seq_lens_host[b] > max_ctx or (paged cache) the free pages do not cover the new
+ * positions; nothing is enqueued and no state changes then. */
 ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
                      const int32_t *tokens_dev, int32_t *next_tokens_dev, float *logits_dev);
 
@@ -113,12 +124,20 @@ ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
  * advances every length by one.  in_tokens_dev may equal next_tokens_dev (greedy
  * feedback).  The step runs as one HIP graph replay, captured on first use for each
  * (in, out, logits) pointer triple.  LL_ERR_STATE before a prefill; LL_ERR_CAPACITY when
- * some len[b] + 1 > max_ctx. */
+ * some len[b] + 1 > max_ctx or (paged cache) a sequence entering a new page finds the pool
+ * empty.  With a paged cache the new block-table entries are copied to the device on the
+ * model's stream before the step. */
 ll_status ll_decode_step(ll_model *m, const int32_t *in_tokens_dev, int32_t *next_tokens_dev,
                          float *logits_dev);
 
-/* Forget every sequence (all lengths 0); the next call must be ll_prefill. */
+/* Forget every sequence (all lengths 0); the next call must be ll_prefill.  With a paged
+ * cache every page returns to the pool (the call first synchronises the stream, since
+ * block-table copies of earlier steps read host memory that is reused). */
 ll_status ll_kv_reset(ll_model *m);
+
+/* Paged cache: pages held by the current sequences and pages in the pool (both 0 for a
+ * contiguous cache).  Host only. */
+ll_status ll_kv_pages(const ll_model *m, int32_t *used, int32_t *total);
 
 /* Current host-mirrored sequence lengths: writes min(cap, batch) values, *n = batch. */
 ll_status ll_seq_lengths(const ll_model *m, int32_t *out, int32_t cap, int32_t *n);

@@ -36,7 +36,7 @@ class LLConfig(ctypes.Structure):
                 ("n_kv_heads", c_int32), ("head_dim", c_int32), ("ffn_dim", c_int32),
                 ("vocab", c_int32), ("rms_eps", c_float), ("rope_theta", c_double),
                 ("dtype", c_int32), ("max_batch", c_int32), ("max_prefill_tokens", c_int32),
-                ("max_ctx", c_int32)]
+                ("max_ctx", c_int32), ("kv_page", c_int32), ("kv_pages", c_int32)]
 
 
 class LLWeights(ctypes.Structure):
@@ -121,6 +121,7 @@ SIGNATURES = [
     ("ll_decode_step", c_int32, [c_void_p, c_void_p, c_void_p, c_void_p]),
     ("ll_kv_reset", c_int32, [c_void_p]),
     ("ll_seq_lengths", c_int32, [c_void_p, POINTER(c_int32), c_int32, POINTER(c_int32)]),
+    ("ll_kv_pages", c_int32, [c_void_p, POINTER(c_int32), POINTER(c_int32)]),
     ("ll_set_decode_graph", c_int32, [c_void_p, c_int32]),
     ("ll_set_option", c_int32, [c_void_p, c_int32, c_int32]),
     ("ll_get_option", c_int32, [c_void_p, c_int32, POINTER(c_int32)]),
@@ -230,12 +231,13 @@ def _check(status: int, where: str) -> None:
         raise LLError(status, where, msg.decode() if msg else "")
 
 
-def make_config(cfg, max_batch: int, max_prefill_tokens: int, max_ctx: int) -> LLConfig:
-    """LLConfig from a synth.configs.ModelConfig-like object."""
+def make_config(cfg, max_batch: int, max_prefill_tokens: int, max_ctx: int, kv_page: int = 0,
+                kv_pages: int = 0) -> LLConfig:
+    """LLConfig from a synth.configs.ModelConfig-like object (kv_page > 0: paged cache)."""
     return LLConfig(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim,
                     cfg.ffn_dim, cfg.vocab, float(cfg.rms_eps), float(cfg.rope_theta),
                     LL_BF16 if cfg.dtype == "bf16" else LL_F32, max_batch, max_prefill_tokens,
-                    max_ctx)
+                    max_ctx, kv_page, kv_pages)
 
 
 def workspace_size(cfg: LLConfig) -> int:
@@ -261,11 +263,12 @@ class Model:
     """
 
     def __init__(self, cfg, weights: Dict[str, "object"], max_batch: int,
-                 max_prefill_tokens: int, max_ctx: int, stream=None):
+                 max_prefill_tokens: int, max_ctx: int, stream=None, kv_page: int = 0,
+                 kv_pages: int = 0):
         import torch
         self.lib = load_library()
         self.mcfg = cfg
-        self.cfg = make_config(cfg, max_batch, max_prefill_tokens, max_ctx)
+        self.cfg = make_config(cfg, max_batch, max_prefill_tokens, max_ctx, kv_page, kv_pages)
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         nbytes = workspace_size(self.cfg)
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
@@ -345,6 +348,13 @@ class Model:
         n = c_int32(0)
         _check(self.lib.ll_seq_lengths(self.handle, out, LL_MAX_BATCH, ctypes.byref(n)), "ll_seq_lengths")
         return list(out[:n.value])
+
+    def kv_pages(self) -> Tuple[int, int]:
+        """(pages held by the current sequences, pages in the pool); (0, 0) when contiguous."""
+        used, total = c_int32(0), c_int32(0)
+        _check(self.lib.ll_kv_pages(self.handle, ctypes.byref(used), ctypes.byref(total)),
+               "ll_kv_pages")
+        return used.value, total.value
 
     def set_kernel_timing(self, enable: bool) -> None:
         _check(self.lib.ll_set_kernel_timing(self.handle, 1 if enable else 0), "ll_set_kernel_timing")

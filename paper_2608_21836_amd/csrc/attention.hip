@@ -27,7 +27,8 @@ template <typename T, int HD>
 __global__ __launch_bounds__(256) void k_attn_prefill(
     const T *__restrict__ Q, int ldq, const T *__restrict__ Kc, const T *__restrict__ Vc,
     T *__restrict__ O, int ldo, const int *__restrict__ cu, const int *__restrict__ kstart,
-    const int2 *__restrict__ qtiles, int hq, int hkv, int max_ctx, float scale_log2) {
+    const int2 *__restrict__ qtiles, int hq, int hkv, int max_ctx, float scale_log2,
+    KvPaging pg) {
   using F = typename Frag<T>::type;
   constexpr int EPL = Frag<T>::EPL;
   constexpr int KT = 4 * EPL;       // head dims per Q K^T chunk
@@ -63,16 +64,17 @@ __global__ __launch_bounds__(256) void k_attn_prefill(
 
   const int q_last = min(q0 + kAttnQTile - 1, L - 1);
   const int ntiles = (P0 + q_last) / BKV + 1;
-  const size_t kvbase = ((size_t)b * hkv + kvh) * max_ctx * HD;
   for (int kt = 0; kt < ntiles; ++kt) {
     __syncthreads();
+    // the tile's 64 keys lie in one page (its first key is a cached position)
+    const size_t tb = kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD);
     for (int c = tid; c < BKV * CPR; c += 256) {
       const int key = c / CPR, dc = c % CPR;
       const int gk = kt * BKV + key;
       F kv = fz, vv = fz;
       if (gk < KL) {
-        kv = load_frag<F>(Kc + kvbase + (size_t)gk * HD + dc * EPL);
-        vv = load_frag<F>(Vc + kvbase + (size_t)gk * HD + dc * EPL);
+        kv = load_frag<F>(Kc + tb + (size_t)key * HD + dc * EPL);
+        vv = load_frag<F>(Vc + tb + (size_t)key * HD + dc * EPL);
       }
       sK[((key >> 4) * NQC + dc / 4) * 64 + (key & 15) + 16 * (dc & 3)] = kv;
       const int kc = key / PVK, kk = key % PVK;
@@ -158,7 +160,8 @@ template <int HD>
 __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
     const bf16 *__restrict__ Q, int ldq, const bf16 *__restrict__ Kc, const bf16 *__restrict__ Vc,
     bf16 *__restrict__ O, int ldo, const int *__restrict__ cu, const int *__restrict__ kstart,
-    const int2 *__restrict__ qtiles, int hq, int hkv, int max_ctx, float scale_log2) {
+    const int2 *__restrict__ qtiles, int hq, int hkv, int max_ctx, float scale_log2,
+    KvPaging pg) {
   constexpr int QT = kAttnQTileWide, BKV = 64;
   constexpr int NKC = HD / 16;           // 16-dim steps of S^T
   constexpr int NDB = HD / 32;           // 32-dim output blocks
@@ -184,7 +187,6 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
   const int qw = q0 + wave * 32;  // first query of this wave
   const int my_q = qw + (lane & 31);
   const bool q_ok = my_q < L;
-  const size_t kvbase = ((size_t)b * hkv + kvh) * max_ctx * HD;
   const bf16x8 fz = frag_zero<bf16x8>();
 
   bf16x8 qf[NKC];
@@ -202,12 +204,15 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
 
   // K tile (kb, c): lane l reads key 32 kb + l % 32 (clamped into the sequence; rows past KL
   // are masked), dims 16 c + 8 g.
+  // A tile's keys lie in one page (tiles start at cached positions and the clamp stays in
+  // the tile), so one base per tile serves every row.
   auto k_issue = [&](int kt, int buf) {
     if (wave >= VW) {
+      const size_t tb = kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD);
       for (int ti = wave - VW; ti < KTILES; ti += KW) {
         const int kb = ti / NKC, c = ti % NKC;
         const int key = min(kt * BKV + 32 * kb + (lane & 31), KL - 1);
-        load_tile_to_lds(Kc + kvbase + (size_t)key * HD + 16 * c + 8 * g,
+        load_tile_to_lds(Kc + tb + (size_t)(key - kt * BKV) * HD + 16 * c + 8 * g,
                          &smem[buf * STAGE + ti * 64]);
       }
     }
@@ -218,12 +223,14 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
   uint4 vr[8];
   auto v_load = [&](int kt) {
     if (wave < VW) {
+      const size_t tb = kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         // rows past the sequence are read clamped (in bounds) and replaced by zeros: their
         // probabilities are 0, and the cache there may hold anything, NaN included
         const int key = kt * BKV + 16 * pc + (e < 4 ? 4 * gg + e : 8 + 4 * gg + e - 4);
-        const uint4 v = *reinterpret_cast<const uint4 *>(Vc + kvbase + (size_t)min(key, KL - 1) * HD + 8 * dg);
+        const uint4 v = *reinterpret_cast<const uint4 *>(
+            Vc + tb + (size_t)(min(key, KL - 1) - kt * BKV) * HD + 8 * dg);
         vr[e] = key < KL ? v : make_uint4(0, 0, 0, 0);
       }
     }
@@ -354,7 +361,7 @@ __global__ __launch_bounds__(256) void k_attn_decode(
     const T *__restrict__ Q, int ldq, const T *__restrict__ Kc, const T *__restrict__ Vc,
     const int *__restrict__ lens, int len_add, int hkv, int max_ctx, int kpb, int nsplit,
     float *__restrict__ part_o, float *__restrict__ part_ml, T *__restrict__ O, int ldo,
-    float scale_log2) {
+    float scale_log2, KvPaging pg) {
   using F = typename Frag<T>::type;
   constexpr int EPL = Frag<T>::EPL;
   constexpr int LPK = HD / EPL;         // lanes per cached row
@@ -380,7 +387,8 @@ __global__ __launch_bounds__(256) void k_attn_decode(
 #pragma unroll
     for (int e = 0; e < EPL; ++e) qv[g][e] = to_f32(qq[e]) * scale_log2;
   }
-  const size_t kvbase = ((size_t)b * hkv + kvh) * max_ctx * HD + (size_t)j0 * HD;
+  // the chunk (kpb <= 256 keys, aligned) lies in one page
+  const size_t kvbase = kv_row_off(pg, b, kvh, hkv, max_ctx, j0, HD);
   const T *Kb = Kc + kvbase + dl * EPL;
   const T *Vb = Vc + kvbase + dl * EPL;
 
@@ -529,18 +537,18 @@ __global__ __launch_bounds__(HD) void k_attn_combine_direct(const float *__restr
 template <typename T, int HD>
 hipError_t run_prefill(const void *q, int ldq, const void *kc, const void *vc, void *o, int ldo,
                        const int *cu, const int *kstart, const int2 *qtiles, int n_qtiles,
-                       int hq, int hkv, int max_ctx, hipStream_t s) {
+                       int hq, int hkv, int max_ctx, hipStream_t s, const KvPaging &pg) {
   const float scale_log2 = kLog2e / sqrtf((float)HD);
   if constexpr (!std::is_same<T, float>::value) {
     LL_LAUNCH((k_attn_prefill_wide<HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
               reinterpret_cast<const bf16 *>(q), ldq, reinterpret_cast<const bf16 *>(kc),
               reinterpret_cast<const bf16 *>(vc), reinterpret_cast<bf16 *>(o), ldo, cu, kstart,
-              qtiles, hq, hkv, max_ctx, scale_log2);
+              qtiles, hq, hkv, max_ctx, scale_log2, pg);
   } else {
     LL_LAUNCH((k_attn_prefill<T, HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
               reinterpret_cast<const T *>(q), ldq, reinterpret_cast<const T *>(kc),
               reinterpret_cast<const T *>(vc), reinterpret_cast<T *>(o), ldo, cu, kstart, qtiles,
-              hq, hkv, max_ctx, scale_log2);
+              hq, hkv, max_ctx, scale_log2, pg);
   }
   return hipGetLastError();
 }
@@ -555,14 +563,14 @@ template <typename T, int HD, int G>
 hipError_t run_decode_g(const void *q, int ldq, const void *kc, const void *vc, const int *lens,
                         int len_add, void *o, int ldo, int batch, int hkv, int max_ctx,
                         const AttnDecodePlan &plan, float *part_o, float *part_ml,
-                        hipStream_t s, bool skip_merge) {
+                        hipStream_t s, bool skip_merge, const KvPaging &pg) {
   const float scale_log2 = kLog2e / sqrtf((float)HD);
   constexpr int EPL = Frag<T>::EPL;
   LL_LAUNCH((k_attn_decode<T, HD, G, kChunkKpt<HD, EPL>>), dim3(plan.nsplit, hkv, batch),
             dim3(256), 0, s, reinterpret_cast<const T *>(q), ldq,
             reinterpret_cast<const T *>(kc), reinterpret_cast<const T *>(vc), lens, len_add,
             hkv, max_ctx, plan.kpb, plan.nsplit, part_o, part_ml, reinterpret_cast<T *>(o), ldo,
-            scale_log2);
+            scale_log2, pg);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || plan.nsplit == 1 || skip_merge) return e;
   if (g_launch_timer) g_launch_timer->secondary();
@@ -581,10 +589,10 @@ template <typename T, int HD>
 hipError_t run_decode(int group, const void *q, int ldq, const void *kc, const void *vc,
                       const int *lens, int len_add, void *o, int ldo, int batch, int hkv,
                       int max_ctx, const AttnDecodePlan &plan, float *part_o, float *part_ml,
-                      hipStream_t s, bool skip_merge) {
+                      hipStream_t s, bool skip_merge, const KvPaging &pg) {
 #define LL_DECODE_G(G)                                                                       \
   return run_decode_g<T, HD, G>(q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx, \
-                                plan, part_o, part_ml, s, skip_merge)
+                                plan, part_o, part_ml, s, skip_merge, pg)
   switch (group) {
     case 1: LL_DECODE_G(1);
     case 2: LL_DECODE_G(2);
@@ -600,11 +608,13 @@ hipError_t run_decode(int group, const void *q, int ldq, const void *kc, const v
 hipError_t launch_attn_prefill(int dtype, int head_dim, const void *q, int ldq, const void *kc,
                                const void *vc, void *o, int ldo, const int *cu,
                                const int *kstart, const int2 *qtiles, int n_qtiles, int hq,
-                               int hkv, int max_ctx, hipStream_t s) {
+                               int hkv, int max_ctx, hipStream_t s, const KvPaging &pg) {
   if (n_qtiles <= 0) return hipSuccess;
+  if (pg.table && (pg.page_len < 256 || pg.page_len % 256 || pg.max_pages < 1))
+    return hipErrorInvalidValue;
 #define LL_PREFILL(TT, HD)                                                                   \
   return run_prefill<TT, HD>(q, ldq, kc, vc, o, ldo, cu, kstart, qtiles, n_qtiles, hq, hkv, \
-                             max_ctx, s)
+                             max_ctx, s, pg)
   if (dtype == kF32) {
     if (head_dim == 64) LL_PREFILL(float, 64);
     if (head_dim == 128) LL_PREFILL(float, 128);
@@ -636,8 +646,12 @@ int attn_decode_max_ctx() { return kMaxSplit * 256; }
 hipError_t launch_attn_decode(int dtype, int head_dim, const void *q, int ldq, const void *kc,
                               const void *vc, const int *lens, int len_add, void *o, int ldo,
                               int batch, int hq, int hkv, int max_ctx, const AttnDecodePlan &plan,
-                              float *part_o, float *part_ml, hipStream_t s, bool skip_merge) {
+                              float *part_o, float *part_ml, hipStream_t s, bool skip_merge,
+                              const KvPaging &pg) {
   if (batch <= 0) return hipSuccess;
+  if (pg.table && (pg.page_len < 256 || pg.page_len % 256 || pg.max_pages < 1 ||
+                   pg.page_len % plan.kpb))
+    return hipErrorInvalidValue;
   if (plan.kpb <= 0 || plan.nsplit < 1 || plan.nsplit > kMaxSplit || hq % hkv ||
       (long)plan.kpb * plan.nsplit < max_ctx || plan.kpb > kMaxChunk)
     return hipErrorInvalidValue;
@@ -646,7 +660,7 @@ hipError_t launch_attn_decode(int dtype, int head_dim, const void *q, int ldq, c
   const int g = hq / hkv;
 #define LL_DECODE_HD(TT, HD)                                                                 \
   return run_decode<TT, HD>(g, q, ldq, kc, vc, lens, len_add, o, ldo, batch, hkv, max_ctx,  \
-                            plan, part_o, part_ml, s, skip_merge)
+                            plan, part_o, part_ml, s, skip_merge, pg)
   if (dtype == kF32) {
     if (head_dim == 64) LL_DECODE_HD(float, 64);
     if (head_dim == 128) LL_DECODE_HD(float, 128);

@@ -123,6 +123,7 @@ template <typename T> struct EpiQkv {
   const int *row_seq, *row_pos;
   const float *rcos, *rsin;
   int hq, hkv, hd, max_ctx;
+  KvPaging pg;
   static constexpr bool kArgmax = false, kPairs = true, kVec8 = true;
   __device__ void operator()(int m, int u, int c, float v0, float v1) const {
     const int n0 = u * 32;
@@ -144,7 +145,7 @@ template <typename T> struct EpiQkv {
       const bool is_k = head < hq + hkv;
       const int kvh = is_k ? head - hq : head - hq - hkv;
       const int seq = row_seq ? row_seq[m] : m;
-      dst = (is_k ? kc : vc) + (((size_t)seq * hkv + kvh) * max_ctx + pos) * hd;
+      dst = (is_k ? kc : vc) + kv_row_off(pg, seq, kvh, hkv, max_ctx, pos, hd);
     }
     dst[i1] = from_f32<T>(v0);
     dst[i2] = from_f32<T>(v1);
@@ -184,7 +185,7 @@ template <typename T> struct EpiQkv {
       const bool is_k = head < hq + hkv;
       const int kvh = is_k ? head - hq : head - hq - hkv;
       const int seq = row_seq ? row_seq[m] : m;
-      dst = (is_k ? kc : vc) + (((size_t)seq * hkv + kvh) * max_ctx + pos) * hd;
+      dst = (is_k ? kc : vc) + kv_row_off(pg, seq, kvh, hkv, max_ctx, pos, hd);
     }
     store8<T>(dst + i1, x);
     store8<T>(dst + i2, y);
@@ -1119,7 +1120,7 @@ hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm,
       return run(EpiQkv<T>{reinterpret_cast<T *>(ep.act), ep.ld_act,
                            reinterpret_cast<T *>(ep.kcache), reinterpret_cast<T *>(ep.vcache),
                            ep.row_seq, ep.row_pos, ep.rope_cos, ep.rope_sin, ep.n_heads,
-                           ep.n_kv_heads, ep.head_dim, ep.max_ctx});
+                           ep.n_kv_heads, ep.head_dim, ep.max_ctx, ep.kv_paging});
     case kEpiArgmax:
       return run(EpiArgmax{ep.out_f32, ep.ld_out, ep.part_val, ep.part_idx, ep.n_parts});
     case kEpiConv:

@@ -44,6 +44,24 @@ struct RepackSrc {
 hipError_t launch_repack(int dtype, const RepackSrc &src, int n, int k, int perm, int head_dim,
                          int ffn_dim, void *wt, hipStream_t s);
 
+// KV cache addressing.  Contiguous (table null): row pos of (sequence b, kv head h) at
+// element ((b hkv + h) max_ctx + pos) hd.  Paged: the cache of a layer is a pool of pages
+// [page][hkv][page_len][hd]; table[b * max_pages + pos / page_len] names the physical page
+// holding logical page pos / page_len of sequence b.  page_len is a multiple of 256, so every
+// 64-key tile of the prefill attention and every decode chunk (at most 256 keys, aligned)
+// lies in one page.
+struct KvPaging {
+  const int *table = nullptr;
+  int page_len = 0, max_pages = 0;
+};
+__host__ __device__ inline size_t kv_row_off(const KvPaging &pg, int b, int kvh, int hkv,
+                                             int max_ctx, int pos, int hd) {
+  if (!pg.table) return (((size_t)b * hkv + kvh) * max_ctx + pos) * hd;
+  const int lp = pos / pg.page_len;
+  return (((size_t)pg.table[(size_t)b * pg.max_pages + lp] * hkv + kvh) * pg.page_len +
+          (pos - lp * pg.page_len)) * hd;
+}
+
 enum EpiKind : int {
   kEpiStore = 0,   // out_f32[m, n] = acc
   kEpiResid = 1,   // out_f32[m, n] += acc   (residual stream update)
@@ -84,6 +102,7 @@ struct EpiParams {
   const int *row_pos = nullptr;  // position of each row
   const float *rope_cos = nullptr, *rope_sin = nullptr;  // [max_ctx][hd/2]
   int n_heads = 0, n_kv_heads = 0, head_dim = 0, max_ctx = 0;
+  KvPaging kv_paging;  // Qkv: where a cached row lives (default: contiguous)
   // Argmax
   float *part_val = nullptr;
   int *part_idx = nullptr;
@@ -194,7 +213,7 @@ hipError_t launch_attn_prefill(int dtype, int head_dim, const void *q, int ldq,
                                const void *kcache, const void *vcache, void *o, int ldo,
                                const int *cu_seqlens, const int *kstart, const int2 *qtiles,
                                int n_qtiles, int n_heads, int n_kv_heads, int max_ctx,
-                               hipStream_t s);
+                               hipStream_t s, const KvPaging &pg = KvPaging{});
 
 // Decode attention: split over the cache length (chunk keys per block), then a merge kernel.
 // Keys attended per sequence: lens[b] + len_add (clamped to max_ctx).
@@ -212,7 +231,7 @@ hipError_t launch_attn_decode(int dtype, int head_dim, const void *q, int ldq,
                               int len_add, void *o, int ldo, int batch, int n_heads,
                               int n_kv_heads, int max_ctx, const AttnDecodePlan &plan,
                               float *part_o, float *part_ml, hipStream_t s,
-                              bool skip_merge = false);
+                              bool skip_merge = false, const KvPaging &pg = KvPaging{});
 
 // ------------------------------------------------------------------------------------------
 // Selective state-space (Mamba) mixer

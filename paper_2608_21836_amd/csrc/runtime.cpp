@@ -40,6 +40,8 @@ struct Layout {
   size_t cu = 0, row_seq = 0, row_pos = 0, last_row = 0, lens = 0, qtiles = 0, err = 0;
   size_t total = 0;
   size_t kv_layer_elems = 0;
+  size_t kv_table = 0;                   // paged cache: int32 [max_batch][kv_max_pages]
+  int kv_max_pages = 0, kv_pages = 0;
   AttnDecodePlan attn;
   int n_parts = 0, max_rows = 0, n_qkv = 0;
 };
@@ -76,6 +78,12 @@ ll_status validate_config(const ll_config *c) {
     return fail(LL_ERR_UNSUPPORTED, "max_batch %d > %d", c->max_batch, LL_MAX_BATCH);
   if (c->max_ctx > attn_decode_max_ctx())
     return fail(LL_ERR_UNSUPPORTED, "max_ctx %d > %d", c->max_ctx, attn_decode_max_ctx());
+  if (c->kv_page < 0 || c->kv_pages < 0)
+    return fail(LL_ERR_INVALID_ARGUMENT, "kv_page and kv_pages must be >= 0");
+  if (c->kv_page == 0 && c->kv_pages != 0)
+    return fail(LL_ERR_INVALID_ARGUMENT, "kv_pages %d without kv_page", c->kv_pages);
+  if (c->kv_page % 256)
+    return fail(LL_ERR_UNSUPPORTED, "kv_page %d not a multiple of 256", c->kv_page);
   return LL_OK;
 }
 
@@ -104,7 +112,14 @@ Layout make_layout(const ll_config &c) {
   }
   L.final_norm = take(d * eb);
   L.lm_head = take((size_t)c.vocab * d * eb);
-  L.kv_layer_elems = (size_t)c.max_batch * c.n_kv_heads * c.max_ctx * c.head_dim;
+  if (c.kv_page > 0) {
+    L.kv_max_pages = (c.max_ctx + c.kv_page - 1) / c.kv_page;
+    L.kv_pages = c.kv_pages > 0 ? c.kv_pages : c.max_batch * L.kv_max_pages;
+    L.kv_layer_elems = (size_t)L.kv_pages * c.n_kv_heads * c.kv_page * c.head_dim;
+    L.kv_table = take((size_t)c.max_batch * L.kv_max_pages * 4);
+  } else {
+    L.kv_layer_elems = (size_t)c.max_batch * c.n_kv_heads * c.max_ctx * c.head_dim;
+  }
   L.kcache = take(L.kv_layer_elems * c.n_layers * eb);
   L.vcache = take(L.kv_layer_elems * c.n_layers * eb);
   L.rcos = take((size_t)c.max_ctx * (c.head_dim / 2) * 4);
@@ -180,6 +195,47 @@ struct ll_model {
   void *kc(int l) const { return ws + L.kcache + L.kv_layer_elems * l * elem_bytes(cfg.dtype); }
   void *vc(int l) const { return ws + L.vcache + L.kv_layer_elems * l * elem_bytes(cfg.dtype); }
   ~ll_model() { delete timer; }
+
+  // Paged cache: the pool's free pages (a stack, so the first pages handed out are the
+  // highest ids), each sequence's pages in logical order, and the host copy of the block
+  // table whose entries are copied to the device when they are first set.
+  std::vector<int> free_pages;
+  std::vector<std::vector<int>> seq_pages;
+  std::vector<int> table_host;
+  bool paged() const { return cfg.kv_page > 0; }
+  KvPaging paging() const {
+    KvPaging p;
+    if (paged()) {
+      p.table = reinterpret_cast<const int *>(ws + L.kv_table);
+      p.page_len = cfg.kv_page;
+      p.max_pages = L.kv_max_pages;
+    }
+    return p;
+  }
+  void release_pages() {
+    free_pages.resize(L.kv_pages);
+    for (int i = 0; i < L.kv_pages; ++i) free_pages[i] = i;
+    seq_pages.assign(cfg.max_batch, {});
+  }
+  // Pages sequence b lacks to hold `len` positions.
+  int pages_short(int b, long len) const {
+    const long need = (len + cfg.kv_page - 1) / cfg.kv_page;
+    return (int)std::max(0L, need - (long)seq_pages[b].size());
+  }
+  // Give sequence b pages up to `len` positions and copy the new table entries to the device
+  // (the caller has checked the pool).
+  hipError_t grow(int b, long len, hipStream_t s) {
+    const int first = (int)seq_pages[b].size(), n = pages_short(b, len);
+    if (n == 0) return hipSuccess;
+    int *row = table_host.data() + (size_t)b * L.kv_max_pages;
+    for (int i = 0; i < n; ++i) {
+      row[first + i] = free_pages.back();
+      seq_pages[b].push_back(free_pages.back());
+      free_pages.pop_back();
+    }
+    return hipMemcpyAsync(ws + L.kv_table + ((size_t)b * L.kv_max_pages + first) * 4, row + first,
+                          (size_t)n * 4, hipMemcpyHostToDevice, s);
+  }
   void drop_graphs() {
     for (auto &g : graphs) (void)hipGraphExecDestroy(g.exec);
     graphs.clear();
@@ -214,6 +270,7 @@ EpiParams qkv_epi(const ll_model *m, int l, const int *row_seq, const int *row_p
   ep.n_kv_heads = m->cfg.n_kv_heads;
   ep.head_dim = m->cfg.head_dim;
   ep.max_ctx = m->cfg.max_ctx;
+  ep.kv_paging = m->paging();
   return ep;
 }
 
@@ -311,12 +368,12 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
       LL_HIP(launch_attn_decode(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
                                 m->at<int>(m->L.lens), 1, m->at(m->L.o), qd, rows, c.n_heads,
                                 c.n_kv_heads, c.max_ctx, ap, m->at<float>(m->L.part_o),
-                                m->at<float>(m->L.part_ml), s));
+                                m->at<float>(m->L.part_ml), s, false, m->paging()));
     } else {
       LL_HIP(launch_attn_prefill(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
                                  m->at(m->L.o), qd, m->at<int>(m->L.cu),
                                  m->at<int>(m->L.kstart), m->at<int2>(m->L.qtiles), n_qtiles,
-                                 c.n_heads, c.n_kv_heads, c.max_ctx, s));
+                                 c.n_heads, c.n_kv_heads, c.max_ctx, s, m->paging()));
     }
     m->mark(LL_K_O);
     {
@@ -472,6 +529,12 @@ ll_status ll_model_load(const ll_config *cfg, const ll_weights *w, void *workspa
   LOAD_HIP(hipMemcpyAsync(m->at(L.rcos), hc, (size_t)c.max_ctx * half * 4, hipMemcpyHostToDevice, s));
   LOAD_HIP(hipMemcpyAsync(m->at(L.rsin), hs, (size_t)c.max_ctx * half * 4, hipMemcpyHostToDevice, s));
   LOAD_HIP(hipMemsetAsync(m->at(L.err), 0, 4, s));
+  if (m->paged()) {
+    const size_t entries = (size_t)c.max_batch * L.kv_max_pages;
+    LOAD_HIP(hipMemsetAsync(m->at(L.kv_table), 0, entries * 4, s));
+    m->table_host.assign(entries, 0);
+    m->release_pages();
+  }
 
 #undef LOAD_HIP
   *out = m;
@@ -514,6 +577,15 @@ ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
   const int T = (int)total;
   hipStream_t s = m->stream;
   const Layout &L = m->L;
+  if (m->paged()) {
+    long short_pages = 0;
+    for (int b = 0; b < batch; ++b)
+      short_pages += m->pages_short(b, (long)pm.start[b] + pm.lens[b]);
+    if (short_pages > (long)m->free_pages.size())
+      return fail(LL_ERR_CAPACITY, "the prefill needs %ld new KV pages, %zu are free", short_pages,
+                  m->free_pages.size());
+    for (int b = 0; b < batch; ++b) LL_HIP(m->grow(b, (long)pm.start[b] + pm.lens[b], s));
+  }
   TimerScope scope(m->timer, 0);
   m->mark(LL_K_META);
   LL_HIP(launch_prefill_meta(pm, T, qtile, m->at<int>(L.cu), m->at<int>(L.row_seq),
@@ -546,6 +618,14 @@ ll_status ll_decode_step(ll_model *m, const int32_t *in_tokens_dev, int32_t *nex
     if (m->lens[b] + 1 > m->cfg.max_ctx)
       return fail(LL_ERR_CAPACITY, "sequence %d at length %d is full (max_ctx %d)", b, m->lens[b],
                   m->cfg.max_ctx);
+  if (m->paged()) {
+    long short_pages = 0;
+    for (int b = 0; b < m->batch; ++b) short_pages += m->pages_short(b, (long)m->lens[b] + 1);
+    if (short_pages > (long)m->free_pages.size())
+      return fail(LL_ERR_CAPACITY, "the decode step needs %ld new KV pages, %zu are free",
+                  short_pages, m->free_pages.size());
+    for (int b = 0; b < m->batch; ++b) LL_HIP(m->grow(b, (long)m->lens[b] + 1, m->stream));
+  }
   TimerScope scope(m->timer, 1);
   if (m->use_graph && !m->timer) {
     hipGraphExec_t exec = nullptr;
@@ -585,8 +665,21 @@ ll_status ll_decode_step(ll_model *m, const int32_t *in_tokens_dev, int32_t *nex
 ll_status ll_kv_reset(ll_model *m) {
   g_err.clear();
   if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
+  if (m->paged()) {
+    // earlier block-table copies read table_host, whose entries are reused from here on
+    LL_HIP(hipStreamSynchronize(m->stream));
+    m->release_pages();
+  }
   m->batch = 0;
   m->lens.clear();
+  return LL_OK;
+}
+
+ll_status ll_kv_pages(const ll_model *m, int32_t *used, int32_t *total) {
+  g_err.clear();
+  if (!m || !used || !total) return fail(LL_ERR_INVALID_ARGUMENT, "NULL argument");
+  *total = m->paged() ? m->L.kv_pages : 0;
+  *used = m->paged() ? m->L.kv_pages - (int32_t)m->free_pages.size() : 0;
   return LL_OK;
 }
 

@@ -69,7 +69,7 @@ def judge(name: str, dtype: str, ref_logits: np.ndarray, gpu_logits: np.ndarray,
 
 
 def run_gpu_teacher_forced(cfg, weights, lens, packed, ref_tokens, n_decode, use_graph=True,
-                           options=None):
+                           options=None, paging=None):
     """Prefill + n_decode teacher-forced steps through the C ABI, with the given ll_option
     values (name -> value) set after loading.
 
@@ -79,7 +79,7 @@ def run_gpu_teacher_forced(cfg, weights, lens, packed, ref_tokens, n_decode, use
     B = len(lens)
     dev_w = upload_weights(cfg, weights)
     model = Model(cfg, dev_w, max_batch=B, max_prefill_tokens=int(sum(lens)),
-                  max_ctx=int(max(lens)) + n_decode)
+                  max_ctx=int(max(lens)) + n_decode, **(paging or {}))
     del dev_w
     model.set_decode_graph(use_graph)
     for name, value in (options or {}).items():
@@ -125,7 +125,7 @@ def oracle_chunked_run(model, chunks, n_decode):
     return np.stack(logits), np.stack(toks)
 
 
-def run_gpu_chunked(cfg, weights, chunks, ref_tokens, n_decode, options=None):
+def run_gpu_chunked(cfg, weights, chunks, ref_tokens, n_decode, options=None, paging=None):
     """The same through the C ABI: one ll_prefill per chunk (the later ones on the populated
     cache), then decode steps fed the oracle's tokens."""
     import torch
@@ -134,7 +134,7 @@ def run_gpu_chunked(cfg, weights, chunks, ref_tokens, n_decode, options=None):
     total = [sum(len(c[b]) for c in chunks) for b in range(B)]
     dev_w = upload_weights(cfg, weights)
     model = Model(cfg, dev_w, max_batch=B, max_prefill_tokens=max(sum(len(x) for x in c) for c in chunks),
-                  max_ctx=max(total) + n_decode)
+                  max_ctx=max(total) + n_decode, **(paging or {}))
     del dev_w
     for name, value in (options or {}).items():
         model.set_option(name, value)

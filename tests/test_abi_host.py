@@ -75,11 +75,31 @@ def test_workspace_size_of_every_workload(lib, name):
     ("max_ctx", 0, B.LL_ERR_INVALID_ARGUMENT),
     ("rope_theta", -1.0, B.LL_ERR_INVALID_ARGUMENT),
     ("rms_eps", float("nan"), B.LL_ERR_INVALID_ARGUMENT),
+    ("kv_page", 100, B.LL_ERR_UNSUPPORTED),       # pages hold a multiple of 256 positions
+    ("kv_page", -256, B.LL_ERR_INVALID_ARGUMENT),
+    ("kv_pages", 4, B.LL_ERR_INVALID_ARGUMENT),   # a pool size without a page size
 ])
 def test_config_validation(lib, field, value, status):
     st, _ = status_of(lib, cfg_for("tiny-f32", **{field: value}))
     assert st == status
     assert lib.ll_last_error()
+
+
+def test_paged_workspace_holds_the_pool_not_every_context():
+    full = cfg_for("8b-gqa")
+    st0, contiguous = status_of(lib := B.load_library(), full)
+    paged = cfg_for("8b-gqa", kv_page=256)
+    st1, same_pool = status_of(lib, paged)
+    small = cfg_for("8b-gqa", kv_page=256, kv_pages=300)
+    st2, small_pool = status_of(lib, small)
+    assert st0 == st1 == st2 == B.LL_OK
+    # the default pool covers max_batch full contexts (within page rounding); a smaller pool
+    # saves exactly its missing pages (K and V, every layer)
+    assert abs(same_pool - contiguous) < 0.05 * contiguous
+    c = {**CONFIGS, **TEST_CONFIGS}["8b-gqa"]
+    page_bytes = 2 * c.n_layers * c.n_kv_heads * 256 * c.head_dim * 2
+    default_pages = full.max_batch * ((full.max_ctx + 255) // 256)
+    assert abs((same_pool - small_pool) - (default_pages - 300) * page_bytes) < 4096
 
 
 def test_group_of_sixteen_rejected(lib):
