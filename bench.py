@@ -287,6 +287,54 @@ def cpu_baseline(cfg, lens, packed, n_decode, budget_s):
             "decode_tok_s": round(len(prompts) * steps / t_dec, 3) if steps else None}
 
 
+def host_info():
+    """CPU model, BLAS library and threads of the host the oracle runs on."""
+    import numpy as np
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = ""
+    try:
+        cfg = np.show_config(mode="dicts")
+        b = cfg.get("Build Dependencies", {}).get("blas", {})
+        blas = f"{b.get('name', '')} {b.get('version', '')}".strip()
+    except Exception:
+        pass
+    return {"cpu_model": model, "blas": blas}
+
+
+def device_context():
+    """Context figures measured on this GPU (the fractions use the datasheet peaks): a device
+    copy's read + write bandwidth and the bf16 rate of an MFMA-only loop, each from events."""
+    import torch
+    from paper_2608_21836_amd.binding import op_mfma_loop
+    src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")      # 1 GiB
+    dst = torch.empty_like(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    dst.copy_(src)
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record()
+    e1.synchronize()
+    copy_gbs = 5 * 2 * src.numel() * 4 / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del src, dst
+    blocks, iters = 4096, 4096
+    out = op_mfma_loop(blocks, 16)
+    e0.record()
+    op_mfma_loop(blocks, iters, out)
+    e1.record()
+    e1.synchronize()
+    mfma_tflops = blocks * 4 * iters * 8 * 16384 / (e0.elapsed_time(e1) / 1e3) / 1e12
+    return {"copy_GBs": round(copy_gbs, 1), "mfma_loop_bf16_TFLOPs": round(mfma_tflops, 1)}
+
+
 def cpu_baseline_mamba(cfg, lens, packed, n_decode, budget_s, weights=None):
     """The Mamba / Mamba2 / RG-LRU oracle on the host, as cpu_baseline does for the decoder.
     The RG-LRU workload's fp64 prefill of the whole prompt alone would exceed the budget, so
@@ -543,6 +591,7 @@ def main() -> int:
                                {"prefill": pre_ms, "decode": dec_ms}, {"prefill": 1, "decode": N})
         out["hotspot_eq1"] = {k: round(v, 4) for k, v in score.items()}
 
+    out["context"] = device_context()
     if not args.no_cpu_baseline:
         print("[bench] oracle cpu baseline", file=sys.stderr, flush=True)
         if mamba:
@@ -550,6 +599,7 @@ def main() -> int:
                                                      host_w)
         else:
             out["cpu_baseline"] = cpu_baseline(cfg, lens, packed, N, args.cpu_budget)
+        out["cpu_baseline"].update(host_info())
     model.close()
     print(json.dumps(out), flush=True)
     return 0

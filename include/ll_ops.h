@@ -99,6 +99,13 @@ ll_status ll_op_lmhead_argmax(int32_t dtype, int32_t rows, int32_t vocab, int32_
                               const void *h, const void *wt, float *logits, int32_t *next,
                               void *scratch, size_t scratch_bytes, void *stream);
 
+/* Calibration, not part of the model: an MFMA-only loop (no memory traffic inside it) that
+ * measures the bf16 matrix-core rate this GPU sustains, reported beside the datasheet peak.
+ * blocks blocks of 4 waves; each wave runs iters x 8 v_mfma_f32_16x16x32_bf16, i.e.
+ * blocks * 4 * iters * 8 * 16384 flops in all; out_dev fp32 [4 * blocks] receives one sum per
+ * wave. */
+ll_status ll_op_mfma_loop(int32_t blocks, int32_t iters, float *out_dev, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

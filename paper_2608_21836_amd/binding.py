@@ -122,6 +122,7 @@ SIGNATURES = [
     ("ll_kv_reset", c_int32, [c_void_p]),
     ("ll_seq_lengths", c_int32, [c_void_p, POINTER(c_int32), c_int32, POINTER(c_int32)]),
     ("ll_kv_pages", c_int32, [c_void_p, POINTER(c_int32), POINTER(c_int32)]),
+    ("ll_op_mfma_loop", c_int32, [c_int32, c_int32, c_void_p, c_void_p]),
     ("ll_set_decode_graph", c_int32, [c_void_p, c_int32]),
     ("ll_set_option", c_int32, [c_void_p, c_int32, c_int32]),
     ("ll_get_option", c_int32, [c_void_p, c_int32, POINTER(c_int32)]),
@@ -585,6 +586,16 @@ def upload_mamba_weights(cfg, weights) -> Dict[str, "object"]:
 def _dt(t) -> int:
     import torch
     return LL_BF16 if t.dtype == torch.bfloat16 else LL_F32
+
+
+def op_mfma_loop(blocks: int, iters: int, out=None, stream=None):
+    """Calibration MFMA loop (ll_op_mfma_loop); returns the fp32 output tensor."""
+    import torch
+    if out is None:
+        out = torch.empty(4 * blocks, dtype=torch.float32, device="cuda")
+    _check(load_library().ll_op_mfma_loop(blocks, iters, out.data_ptr(), _stream_handle(stream)),
+           "ll_op_mfma_loop")
+    return out
 
 
 def op_rmsnorm(x, gain, eps: float, stream=None):

@@ -142,6 +142,47 @@ __global__ __launch_bounds__(256) void k_prefill_meta(PrefillMeta pm, int total,
   }
 }
 
+// MFMA-only loop for calibration: every wave runs iters rounds of 8 independent
+// v_mfma_f32_16x16x32_bf16 on register operands (no memory traffic in the loop) and writes one
+// float so that the work is kept.
+// The eight chains use different B operands and start values, so that none can be folded
+// into another.
+__global__ __launch_bounds__(256) void k_mfma_loop(int iters, float *__restrict__ out) {
+  bf16x8 a, b0, b1, b2, b3, b4, b5, b6, b7;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float x = 0.5f - 0.001f * e;
+    a[e] = static_cast<bf16>(1.0f + 0.001f * (threadIdx.x & 7));
+    b0[e] = static_cast<bf16>(x);
+    b1[e] = static_cast<bf16>(x - 0.01f);
+    b2[e] = static_cast<bf16>(x - 0.02f);
+    b3[e] = static_cast<bf16>(x - 0.03f);
+    b4[e] = static_cast<bf16>(x - 0.04f);
+    b5[e] = static_cast<bf16>(x - 0.05f);
+    b6[e] = static_cast<bf16>(x - 0.06f);
+    b7[e] = static_cast<bf16>(x - 0.07f);
+  }
+  f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = c0, c2 = c0, c3 = c0, c4 = c0, c5 = c0, c6 = c0,
+        c7 = c0;
+  // in-place accumulation written out, so that no register copies enter the loop
+#define LL_MFMA_STEP(C, B) \
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(C) : "v"(a), "v"(B))
+  for (int it = 0; it < iters; ++it) {
+    LL_MFMA_STEP(c0, b0);
+    LL_MFMA_STEP(c1, b1);
+    LL_MFMA_STEP(c2, b2);
+    LL_MFMA_STEP(c3, b3);
+    LL_MFMA_STEP(c4, b4);
+    LL_MFMA_STEP(c5, b5);
+    LL_MFMA_STEP(c6, b6);
+    LL_MFMA_STEP(c7, b7);
+  }
+#undef LL_MFMA_STEP
+  const f32x4 sum = c0 + c1 + c2 + c3 + c4 + c5 + c6 + c7;
+  const float t = sum[0] + sum[1] + sum[2] + sum[3];
+  if ((threadIdx.x & 63) == 0) out[blockIdx.x * 4 + (threadIdx.x >> 6)] = t;
+}
+
 }  // namespace
 
 hipError_t launch_embed(int dtype, const int *tokens, int ntok, const void *table, int vocab,
@@ -186,6 +227,12 @@ hipError_t launch_prefill_meta(const PrefillMeta &pm, int total, int qtile, int 
   const int blocks = std::max(1, (total + 255) / 256);
   LL_LAUNCH(k_prefill_meta, dim3(blocks), dim3(256), 0, s, pm, total, qtile, cu, row_seq,
                      row_pos, last_row, lens_dev, kstart, qtiles);
+  return hipGetLastError();
+}
+
+hipError_t launch_mfma_loop(int blocks, int iters, float *out, hipStream_t s) {
+  if (blocks < 1 || iters < 1 || !out) return hipErrorInvalidValue;
+  LL_LAUNCH(k_mfma_loop, dim3(blocks), dim3(256), 0, s, iters, out);
   return hipGetLastError();
 }
 

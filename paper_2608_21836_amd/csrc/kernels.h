@@ -185,6 +185,9 @@ hipError_t launch_rmsnorm(int dtype, const float *x, int ldx, const int *rowmap,
                           int d, const void *gain, float eps, void *y, int ldy, hipStream_t s);
 // next[r] = column of the largest argmax partial of row r (lowest column on ties); lens_inc[r]
 // += 1 when lens_inc is given.
+// MFMA-only calibration loop: `blocks` blocks of 4 waves, each wave iters x 8 MFMAs of
+// 16x16x32 bf16 (2 * 16 * 16 * 32 flops each); out receives 4 floats per block.
+hipError_t launch_mfma_loop(int blocks, int iters, float *out, hipStream_t s);
 hipError_t launch_argmax_reduce(const float *part_val, const int *part_idx, int rows,
                                 int n_parts, int *next, int *lens_inc, hipStream_t s);
 

@@ -797,6 +797,14 @@ ll_status ll_op_rmsnorm(int32_t dtype, int32_t rows, int32_t d, const float *x, 
   return LL_OK;
 }
 
+ll_status ll_op_mfma_loop(int32_t blocks, int32_t iters, float *out_dev, void *stream) {
+  g_err.clear();
+  if (blocks < 1 || iters < 1 || !out_dev)
+    return fail(LL_ERR_INVALID_ARGUMENT, "blocks >= 1, iters >= 1 and out_dev must be set");
+  LL_HIP(launch_mfma_loop(blocks, iters, out_dev, (hipStream_t)stream));
+  return LL_OK;
+}
+
 ll_status ll_op_repack(int32_t dtype, int32_t n, int32_t k, const void *w, void *wt, void *stream) {
   g_err.clear();
   ll_status st = check_dtype(dtype);

@@ -280,3 +280,14 @@ def test_lmhead_argmax(dtype, rows, vocab, k):
     assert np.array_equal(nxt.cpu().numpy(), np.argmax(lg, axis=-1))
     assert np.array_equal(nxt.cpu().numpy(), nxt2.cpu().numpy())
     assert nxt.cpu().numpy()[0] == vocab // 3
+
+
+def test_mfma_calibration_loop_runs():
+    """The calibration loop (ll_op_mfma_loop) fills its output and rejects bad arguments."""
+    import torch
+    from paper_2608_21836_amd.binding import LLError, op_mfma_loop
+    out = op_mfma_loop(8, 4)
+    torch.cuda.synchronize()
+    assert out.shape == (32,) and torch.isfinite(out).all()
+    with pytest.raises(LLError):
+        op_mfma_loop(0, 4)
