@@ -412,7 +412,7 @@ __global__ __launch_bounds__(BN * 2, 1) void k_gemm_big(const T *__restrict__ A,
                                                         int N, int K, int ksteps, Epi epi) {
   using F = typename Frag<T>::type;
   constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL;
-  constexpr int GM = 8;
+  constexpr int GM = 4;  // row tiles per group (measured: 4 beats 1, 2, 8 and 16 at 8B shapes)
   constexpr int NW = BN / 32, WN = BN / 64;    // waves: 2 (M) x WN (N)
   constexpr int NA = BM / 16;                  // A tiles per stage (16-row blocks)
   constexpr int NB = BN / 16;                  // W tiles per stage (16-column blocks)
