@@ -94,6 +94,15 @@ MAMBA2_TEST_CONFIGS: Dict[str, Mamba2Config] = {
         name="t-mamba2-f32", seed=52, dtype="f32", n_layers=2, d_model=128, d_inner=256,
         d_state=128, head_dim=64, n_groups=1, d_conv=4, vocab=512, batch=2,
         prompt_list=(19, 130), n_decode=4),
+    # the smallest and largest state sizes the scan kernel takes (N = 32, N = 256)
+    "t-mamba2-n32": Mamba2Config(
+        name="t-mamba2-n32", seed=54, dtype="bf16", n_layers=2, d_model=128, d_inner=256,
+        d_state=32, head_dim=64, n_groups=2, d_conv=4, vocab=512, batch=3,
+        prompt_list=(50, 3, 200), n_decode=4),
+    "t-mamba2-n256": Mamba2Config(
+        name="t-mamba2-n256", seed=55, dtype="f32", n_layers=2, d_model=128, d_inner=256,
+        d_state=256, head_dim=32, n_groups=1, d_conv=4, vocab=512, batch=2,
+        prompt_list=(40, 300), n_decode=4),
     # long prompts (several scan chunks) and 6 sequences (decode above 4 rows)
     "t-mamba2-long": Mamba2Config(
         name="t-mamba2-long", seed=53, dtype="bf16", n_layers=2, d_model=256, d_inner=512,

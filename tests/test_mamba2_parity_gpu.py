@@ -1,7 +1,7 @@
 """Acceptance of the Mamba2 model: whole workloads through ll_mamba2_load / ll_mamba2_prefill /
 ll_mamba2_decode_step, teacher-forced, against the fp64 oracle on the same seeded inputs
 (acceptance rules in parity.py).  Covers ragged batches with one-token prompts, two B/C
-groups, state sizes 64 and 128, prompts long enough for the chunked scan, six sequences,
+groups, state sizes 32, 64, 128 and 256, prompts long enough for the chunked scan, six sequences,
 fp32 and bf16, prefill continued on held state, graph and direct decode, split-K switches and
 the full mamba2-130m workload."""
 import numpy as np
@@ -40,6 +40,7 @@ CASES = [("t-mamba2", True, None, {}), ("t-mamba2", False, None, {}),
          ("t-mamba2-f32", True, None, {}), ("t-mamba2-f32", False, None, {"prefill_splitk": 0}),
          ("t-mamba2-long", True, None, {}),
          ("t-mamba2-long", False, None, {"decode_splitk": 0, "prefill_tile": 3}),
+         ("t-mamba2-n32", True, None, {}), ("t-mamba2-n256", False, None, {}),
          ("mamba2-130m", True, 16, {})]
 
 
