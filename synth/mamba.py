@@ -96,6 +96,12 @@ MAMBA_TEST_CONFIGS: Dict[str, MambaConfig] = {
         name="t-mamba-wide", seed=35, dtype="bf16", n_layers=2, d_model=256, d_inner=512,
         d_state=16, d_conv=4, dt_rank=80, vocab=1024, batch=2, prompt_list=(3000, 2500),
         n_decode=3),
+    # dt rank 160 (Mamba-2.8B's): the largest rank the scan takes; R + 2N = 192 > 128, so
+    # decode takes the unfused path whatever decode_fused says
+    "t-mamba-r160": MambaConfig(
+        name="t-mamba-r160", seed=36, dtype="f32", n_layers=2, d_model=256, d_inner=512,
+        d_state=16, d_conv=4, dt_rank=160, vocab=1024, batch=2, prompt_list=(300, 17),
+        n_decode=4),
     # 20 ragged prompts: decode above the fused-step and skinny-GEMM row limits (split-K)
     "t-mamba-b20": MambaConfig(
         name="t-mamba-b20", seed=34, dtype="bf16", n_layers=2, d_model=256, d_inner=512,

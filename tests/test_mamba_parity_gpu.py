@@ -42,6 +42,7 @@ CASES = [("t-mamba", True, None, {}), ("t-mamba", False, None, {"decode_fused": 
          ("t-mamba-b20", False, None, {"decode_splitk": 0, "prefill_splitk": 0}),
          ("t-mamba", True, None, {"decode_fused": 2}), ("t-mamba-f32", True, None, {"decode_fused": 2}),
          ("t-mamba-wide", True, None, {}), ("t-mamba-wide", True, None, {"decode_fused": 2}),
+         ("t-mamba-r160", True, None, {}),
          ("mamba-130m", True, 16, {}), ("mamba-130m", True, 16, {"decode_fused": 0}),
          ("mamba-130m", True, 16, {"decode_fused": 2})]
 
