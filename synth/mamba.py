@@ -102,6 +102,11 @@ MAMBA_TEST_CONFIGS: Dict[str, MambaConfig] = {
         name="t-mamba-r160", seed=36, dtype="f32", n_layers=2, d_model=256, d_inner=512,
         d_state=16, d_conv=4, dt_rank=160, vocab=1024, batch=2, prompt_list=(300, 17),
         n_decode=4),
+    # a conv of width 2 (one row of conv state)
+    "t-mamba-k2": MambaConfig(
+        name="t-mamba-k2", seed=37, dtype="f32", n_layers=2, d_model=128, d_inner=256,
+        d_state=16, d_conv=2, dt_rank=16, vocab=512, batch=3, prompt_list=(1, 40, 150),
+        n_decode=4),
     # 20 ragged prompts: decode above the fused-step and skinny-GEMM row limits (split-K)
     "t-mamba-b20": MambaConfig(
         name="t-mamba-b20", seed=34, dtype="bf16", n_layers=2, d_model=256, d_inner=512,

@@ -91,6 +91,11 @@ RG_TEST_CONFIGS: Dict[str, RGConfig] = {
         name="t-rg-f32", seed=72, dtype="f32", n_layers=2, d_model=128, lru_width=256, n_heads=4,
         mlp_width=384, d_conv=4, vocab=512, batch=2, prompt_list=(19, 130), n_decode=4,
         norm_std=0.1),
+    # a conv of width 2 (one row of conv state) and blocks of 128
+    "t-rg-k2": RGConfig(
+        name="t-rg-k2", seed=74, dtype="f32", n_layers=2, d_model=128, lru_width=256, n_heads=2,
+        mlp_width=256, d_conv=2, vocab=512, batch=3, prompt_list=(1, 40, 150), n_decode=4,
+        norm_std=0.1),
     # long ragged prompts (several scan chunks) and 20 sequences (decode GEMMs above 16 rows)
     "t-rg-long": RGConfig(
         name="t-rg-long", seed=73, dtype="bf16", n_layers=2, d_model=256, lru_width=512,

@@ -48,6 +48,7 @@ def _config(name):
 CASES = [("t-rg", True, {}), ("t-rg", False, {}),
          ("t-rg-f32", True, {}), ("t-rg-f32", False, {"prefill_splitk": 0}),
          ("t-rg-long", True, {}), ("t-rg-long", False, {"decode_splitk": 0, "prefill_tile": 3}),
+         ("t-rg-k2", True, {}), ("t-rg-k2", False, {}),
          ("rglru-2b-l2", True, {})]
 
 
