@@ -156,7 +156,10 @@ typedef enum {
   LL_OPT_PREFILL_SPLITK = 1,   /* 1 (default): prefill GEMMs whose 64x128 tiles cannot fill the
                                   GPU split K over blocks; 0: never split */
   LL_OPT_DECODE_SPLITK = 2,    /* 1 (default): decode GEMMs above 16 rows split K over blocks of
-                                  128 columns; 0: whole-K blocks */
+                                  128 columns; 0: whole-K blocks; 2: as 1, and up to 16 rows the
+                                  residual GEMMs split K over two blocks per column block that add
+                                  their partial sums with fp32 atomics (more blocks streaming the
+                                  weights; the summation order is then not fixed) */
   LL_OPT_PREFILL_TILE = 3,     /* 0 (default): prefill GEMM tile family chosen per shape; 1: 256x256,
                                   2: 128x256, 3: 64x128 (256-column tiles only where the output
                                   width is a multiple of 256; elsewhere the default) */

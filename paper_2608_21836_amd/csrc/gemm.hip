@@ -92,7 +92,11 @@ struct EpiStore {
 struct EpiResid {
   float *out;
   int ld;
-  static constexpr bool kArgmax = false, kPairs = false, kVec8 = false;
+  static constexpr bool kArgmax = false, kPairs = false, kVec8 = false, kAtomicSplit = true;
+  // K split over blocks: each block adds its partial sum (fp32 atomics; order not fixed)
+  __device__ void add_atomic(int m, int col, float v, bool) const {
+    unsafeAtomicAdd(out + (size_t)m * ld + col, v);
+  }
   __device__ void operator()(int m, int u, int c, float v0, float v1) const {
     float *p = out + (size_t)m * ld + 32 * u + c;
     p[0] += v0;
@@ -240,7 +244,10 @@ struct EpiBiasResid {
   float *out;
   int ld;
   const float *bias;
-  static constexpr bool kArgmax = false, kPairs = false, kVec8 = false;
+  static constexpr bool kArgmax = false, kPairs = false, kVec8 = false, kAtomicSplit = true;
+  __device__ void add_atomic(int m, int col, float v, bool first) const {
+    unsafeAtomicAdd(out + (size_t)m * ld + col, first ? v + bias[col] : v);
+  }
   __device__ void one(int m, int col, float v) const {
     out[(size_t)m * ld + col] += v + bias[col];
   }
@@ -345,6 +352,11 @@ template <typename T> struct EpiRglru {
     out[(size_t)m * W + j] = from_f32<T>(h * to_f32(gy[(size_t)m * W + j]));
   }
 };
+
+template <typename E, typename = void> struct AtomicSplit : std::false_type {};
+template <typename E>
+struct AtomicSplit<E, std::void_t<decltype(E::kAtomicSplit)>>
+    : std::integral_constant<bool, E::kAtomicSplit> {};
 
 template <typename E, typename = void> struct GroupA : std::false_type {};
 template <typename E>
@@ -568,7 +580,7 @@ __global__ __launch_bounds__(BN * 2, 1) void k_gemm_big(const T *__restrict__ A,
 // ------------------------------------------------------------------------------------------
 enum AMode : int { kAGlobal = 0, kAStaged = 1, kANorm = 2 };
 
-template <typename T, int MT, int NB, int AM, typename Epi>
+template <typename T, int MT, int NB, int AM, typename Epi, int KS = 1>
 __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, int lda,
                                                      NormIn norm,
                                                      const uint8_t *__restrict__ Wt, int M,
@@ -581,7 +593,10 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
   const int blk = blockIdx.x;
   if constexpr (GroupA<Epi>::value) A += epi.a_off(16 * NB * blk);
   const int kb_n = K / TK;
-  const int kb0 = (wave * kb_n) / NW, kb1 = ((wave + 1) * kb_n) / NW;
+  // KS > 1: blockIdx.y takes k-tiles [y kb_n / KS, (y + 1) kb_n / KS), split over the waves
+  const int ks0 = KS > 1 ? (int)(blockIdx.y * kb_n / KS) : 0;
+  const int ksn = KS > 1 ? (int)((blockIdx.y + 1) * kb_n / KS) - ks0 : kb_n;
+  const int kb0 = ks0 + (wave * ksn) / NW, kb1 = ks0 + ((wave + 1) * ksn) / NW;
   const uint8_t *wp[NB];
 #pragma unroll
   for (int j = 0; j < NB; ++j) wp[j] = Wt + ((size_t)(NB * blk + j) * kb_n * 64 + lane) * 16;
@@ -741,6 +756,12 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
         if (m < M && c == 0) {
           epi.pval[(size_t)m * epi.n_parts + blk] = bv;
           epi.pidx[(size_t)m * epi.n_parts + blk] = bi;
+        }
+      } else if constexpr (KS > 1) {
+        if (m < M) {
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+            epi.add_atomic(m, 16 * NB * blk + 16 * j + c, sv[j][r], blockIdx.y == 0);
         }
       } else if constexpr (NB == 2) {
         if (m < M) epi(m, blk, c, sv[0][r], sv[1][r]);
@@ -980,9 +1001,17 @@ hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k
 template <typename T, int MT, int NB, int AM, typename Epi>
 hipError_t launch_skinny_one(const T *ap, int lda, const NormIn &nz,
                              const uint8_t *w, int m, int mb, int n, int k, const Epi &epi,
-                             hipStream_t s) {
+                             hipStream_t s, int ksplit = 1) {
   const size_t lds = AM != kAGlobal ? skinny_norm_lds(sizeof(T), m - mb, k) : 0;
   if (lds > kSkinnyMaxNormLds) return hipErrorInvalidValue;
+  if constexpr (AtomicSplit<Epi>::value && !Epi::kPairs) {
+    if (ksplit == 2) {
+      LL_LAUNCH((k_gemm_skinny<T, MT, NB, AM, Epi, 2>), dim3(n / (16 * NB), 2), dim3(512), lds,
+                s, ap, lda, nz, w, m, mb, k, epi);
+      return hipGetLastError();
+    }
+  }
+  if (ksplit != 1) return hipErrorInvalidValue;
   LL_LAUNCH((k_gemm_skinny<T, MT, NB, AM, Epi>), dim3(n / (16 * NB)), dim3(512), lds, s, ap,
             lda, nz, w, m, mb, k, epi);
   return hipGetLastError();
@@ -1026,7 +1055,8 @@ hipError_t run_splitk(const void *a, int lda, const void *wt, int m, int n, int 
 
 template <typename T, typename Epi>
 hipError_t run_skinny(const void *a, int lda, const NormIn *norm,
-                      const void *wt, int m, int n, int k, const Epi &epi, hipStream_t s) {
+                      const void *wt, int m, int n, int k, const Epi &epi, hipStream_t s,
+                      int ksplit = 1) {
   const T *ap = reinterpret_cast<const T *>(a);
   const uint8_t *w = reinterpret_cast<const uint8_t *>(wt);
   const NormIn nz = norm ? *norm : NormIn{};
@@ -1040,7 +1070,8 @@ hipError_t run_skinny(const void *a, int lda, const NormIn *norm,
                    : norm ? kANorm
                    : skinny_norm_lds(sizeof(T), m - mb, k) <= kSkinnyMaxNormLds ? kAStaged : kAGlobal;
     hipError_t e = hipErrorInvalidValue;
-#define LL_SKINNY(MT, NB, AM) e = launch_skinny_one<T, MT, NB, AM>(ap, lda, nz, w, m, mb, n, k, epi, s)
+#define LL_SKINNY(MT, NB, AM) \
+  e = launch_skinny_one<T, MT, NB, AM>(ap, lda, nz, w, m, mb, n, k, epi, s, MT == 1 ? ksplit : 1)
 #define LL_SKINNY_NB(NB)                        \
   do {                                          \
     if (!one) LL_SKINNY(2, NB, kAGlobal);        \
@@ -1064,7 +1095,7 @@ template <typename T, bool kTiled>
 hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm,
                         const void *wt, int m, int n, int k, const EpiParams &ep, hipStream_t s,
                         float *ws = nullptr, size_t ws_bytes = 0, const PostNorm *post = nullptr,
-                        bool *post_done = nullptr, int tile = kTileAuto) {
+                        bool *post_done = nullptr, int tile = kTileAuto, int ksplit = 1) {
   if (post_done) *post_done = false;
   const SplitKPlan plan = splitk_plan(elem_bytes(sizeof(T) == 4 ? kF32 : kBF16), m, n, k);
   auto run = [&](const auto &epi) {
@@ -1080,7 +1111,8 @@ hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm,
           return run_splitk<T>(a, lda, wt, m, n, k, epi, plan, ws, s, fuse_post ? post : nullptr);
         }
       }
-      return run_skinny<T>(a, lda, norm, wt, m, n, k, epi, s);
+      return run_skinny<T>(a, lda, norm, wt, m, n, k, epi, s,
+                           AtomicSplit<E>::value ? ksplit : 1);
     }
   };
   // Refuse, before any launch, pointer sets that a kernel would dereference as null.
@@ -1175,14 +1207,15 @@ hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, 
 hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,
                               const void *wt, int m, int n, int k, const EpiParams &ep,
                               hipStream_t s, float *ws, size_t ws_bytes,
-                              const PostNorm *post, bool *post_done) {
+                              const PostNorm *post, bool *post_done, int ksplit) {
   if (post_done) *post_done = false;
   if (m <= 0) return hipSuccess;
   if (post && (!post->gain || !post->out)) return hipErrorInvalidValue;
+  if (ksplit != 1 && ksplit != 2) return hipErrorInvalidValue;
   return dtype == kF32 ? dispatch_epi<float, false>(a, lda, norm, wt, m, n, k, ep, s, ws,
-                                                    ws_bytes, post, post_done)
+                                                    ws_bytes, post, post_done, kTileAuto, ksplit)
                        : dispatch_epi<bf16, false>(a, lda, norm, wt, m, n, k, ep, s, ws,
-                                                   ws_bytes, post, post_done);
+                                                   ws_bytes, post, post_done, kTileAuto, ksplit);
 }
 
 SplitKPlan prefill_splitk_plan(size_t elem, int m, int n, int k) {

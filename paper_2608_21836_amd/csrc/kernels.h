@@ -162,10 +162,15 @@ struct PostNorm {
   void *out = nullptr;
   int ld_out = 0;
 };
+// ksplit = 2 (residual epilogues, up to 16 rows): K is split over two blocks per column block,
+// each adding its partial sum into the fp32 rows with atomics (the bias once), so twice the
+// blocks stream the weights; the summation order is then not fixed.  Other epilogues ignore
+// it.
 hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,
                               const void *wt, int m, int n, int k, const EpiParams &ep,
                               hipStream_t s, float *ws = nullptr, size_t ws_bytes = 0,
-                              const PostNorm *post = nullptr, bool *post_done = nullptr);
+                              const PostNorm *post = nullptr, bool *post_done = nullptr,
+                              int ksplit = 1);
 constexpr int kSplitKMaxTiles = 24;  // k-tiles per split-K block (A slice of 48 KiB in LDS)
 struct SplitKPlan {
   int nsplit = 0;  // 0: split-K not used for this shape

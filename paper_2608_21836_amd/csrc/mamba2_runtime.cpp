@@ -222,7 +222,8 @@ ll_status enqueue_layers(ll_mamba2 *m, int rows, const PrefillPlan *pp, hipStrea
   auto gemm = [&](const void *a, int lda, const NormIn *nrm, const void *wt, int n, int k,
                   const EpiParams &ep, const PostNorm *post = nullptr, bool *post_done = nullptr) {
     return decode ? launch_gemm_skinny(dt, a, lda, nrm, wt, rows, n, k, ep, s, gemm_ws,
-                                       gemm_ws_bytes, post, post_done)
+                                       gemm_ws_bytes, post, post_done,
+                                       m->opt[LL_OPT_DECODE_SPLITK] == 2 ? 2 : 1)
                   : launch_gemm_tiled(dt, a, lda, wt, rows, n, k, ep, s, gemm_ws, gemm_ws_bytes,
                                       m->opt[LL_OPT_PREFILL_TILE]);
   };
@@ -560,8 +561,10 @@ ll_status ll_mamba2_set_option(ll_mamba2 *m, int32_t option, int32_t value) {
   switch (option) {
     case LL_OPT_DECODE_GRAPH:
     case LL_OPT_PREFILL_SPLITK:
-    case LL_OPT_DECODE_SPLITK:
       if (value != 0 && value != 1) return fail(LL_ERR_INVALID_ARGUMENT, "option %d takes 0 or 1", option);
+      break;
+    case LL_OPT_DECODE_SPLITK:
+      if (value < 0 || value > 2) return fail(LL_ERR_INVALID_ARGUMENT, "decode split-K 0, 1 or 2");
       break;
     case LL_OPT_PREFILL_TILE:
       if (value < 0 || value > 3) return fail(LL_ERR_INVALID_ARGUMENT, "prefill tile 0..3");

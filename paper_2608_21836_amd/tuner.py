@@ -58,7 +58,7 @@ KNOBS: List[Tuple[str, Tuple[int, ...], Tuple[str, ...]]] = [
                                     "down_resid")),
     ("prefill_splitk", (1, 0), ("qkv_rope_append", "o_proj_resid", "gate_up_swiglu",
                                 "down_resid")),
-    ("decode_splitk", (1, 0), ("qkv_rope_append", "o_proj_resid", "gate_up_swiglu",
+    ("decode_splitk", (1, 0, 2), ("qkv_rope_append", "o_proj_resid", "gate_up_swiglu",
                                "down_resid")),
     ("attn_decode_chunk", (0, 64, 128, 256), ("attention", "attn_combine")),
     ("decode_graph", (1, 0), ("qkv_rope_append", "attention", "attn_combine", "o_proj_resid",
@@ -72,7 +72,7 @@ MAMBA_KNOBS: List[Tuple[str, Tuple[int, ...], Tuple[str, ...]]] = [
     ("decode_fused", (1, 0, 2), ("in_proj", "conv_silu", "x_proj", "scan", "out_proj_resid")),
     ("prefill_tile", (0, 1, 2, 3), ("in_proj", "x_proj", "out_proj_resid")),
     ("prefill_splitk", (1, 0), ("in_proj", "x_proj", "out_proj_resid")),
-    ("decode_splitk", (1, 0), ("in_proj", "x_proj", "out_proj_resid")),
+    ("decode_splitk", (1, 0, 2), ("in_proj", "x_proj", "out_proj_resid")),
     ("decode_graph", (1, 0), ("in_proj", "conv_silu", "x_proj", "scan", "out_proj_resid",
                               "lm_head_argmax", "embed", "argmax_reduce", "rmsnorm")),
 ]
@@ -81,7 +81,7 @@ MAMBA_KNOBS: List[Tuple[str, Tuple[int, ...], Tuple[str, ...]]] = [
 MAMBA2_KNOBS: List[Tuple[str, Tuple[int, ...], Tuple[str, ...]]] = [
     ("prefill_tile", (0, 1, 2, 3), ("in_proj", "out_proj_resid")),
     ("prefill_splitk", (1, 0), ("in_proj", "out_proj_resid")),
-    ("decode_splitk", (1, 0), ("in_proj", "out_proj_resid")),
+    ("decode_splitk", (1, 0, 2), ("in_proj", "out_proj_resid")),
     ("decode_graph", (1, 0), ("in_proj", "scan", "out_proj_resid", "lm_head_argmax", "embed",
                               "argmax_reduce", "rmsnorm", "gated_rmsnorm")),
 ]
@@ -90,7 +90,7 @@ MAMBA2_KNOBS: List[Tuple[str, Tuple[int, ...], Tuple[str, ...]]] = [
 RG_KNOBS: List[Tuple[str, Tuple[int, ...], Tuple[str, ...]]] = [
     ("prefill_tile", (0, 1, 2, 3), ("in_proj", "gates", "out_proj_resid", "mlp_up", "mlp_down")),
     ("prefill_splitk", (1, 0), ("in_proj", "out_proj_resid", "mlp_up", "mlp_down")),
-    ("decode_splitk", (1, 0), ("in_proj", "out_proj_resid", "mlp_up", "mlp_down")),
+    ("decode_splitk", (1, 0, 2), ("in_proj", "out_proj_resid", "mlp_up", "mlp_down")),
     ("decode_graph", (1, 0), ("in_proj", "gates", "out_proj_resid", "mlp_up", "mlp_down",
                               "lm_head_argmax", "embed", "argmax_reduce", "rmsnorm")),
 ]

@@ -41,6 +41,7 @@ CASES = [("t-mamba2", True, None, {}), ("t-mamba2", False, None, {}),
          ("t-mamba2-long", True, None, {}),
          ("t-mamba2-long", False, None, {"decode_splitk": 0, "prefill_tile": 3}),
          ("t-mamba2-n32", True, None, {}), ("t-mamba2-n256", False, None, {}),
+         ("t-mamba2-f32", True, None, {"decode_splitk": 2}),
          ("mamba2-130m", True, 16, {})]
 
 

@@ -44,6 +44,7 @@ CASES = [("t-mamba", True, None, {}), ("t-mamba", False, None, {"decode_fused": 
          ("t-mamba-wide", True, None, {}), ("t-mamba-wide", True, None, {"decode_fused": 2}),
          ("t-mamba-r160", True, None, {}),
          ("t-mamba-k2", True, None, {}), ("t-mamba-k2", False, None, {"decode_fused": 0}),
+         ("t-mamba-f32", True, None, {"decode_fused": 0, "decode_splitk": 2}),
          ("mamba-130m", True, 16, {}), ("mamba-130m", True, 16, {"decode_fused": 0}),
          ("mamba-130m", True, 16, {"decode_fused": 2})]
 

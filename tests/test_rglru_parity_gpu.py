@@ -49,6 +49,7 @@ CASES = [("t-rg", True, {}), ("t-rg", False, {}),
          ("t-rg-f32", True, {}), ("t-rg-f32", False, {"prefill_splitk": 0}),
          ("t-rg-long", True, {}), ("t-rg-long", False, {"decode_splitk": 0, "prefill_tile": 3}),
          ("t-rg-k2", True, {}), ("t-rg-k2", False, {}),
+         ("t-rg-f32", True, {"decode_splitk": 2}), ("t-rg", True, {"decode_splitk": 2}),
          ("rglru-2b-l2", True, {})]
 
 

@@ -29,6 +29,9 @@ CASES = [
     ("t-gqa-hd128", {"prefill_tile": 1, "attn_decode_chunk": 128}),
     ("t-f32-ragged", {"prefill_tile": 2, "prefill_splitk": 0}),
     ("t-b32-hd128", {"decode_splitk": 0}),
+    ("t-gqa-hd64", {"decode_splitk": 2}),      # residual GEMMs: K over two blocks, atomics
+    ("t-f32-ragged", {"decode_splitk": 2}),
+    ("125m", {"decode_splitk": 2}),
     ("t-b32-hd128", {"prefill_tile": 1, "attn_decode_chunk": 256}),
 ]
 
