@@ -6,6 +6,9 @@ this module times each hot-path kernel alone, on the shapes the five workloads r
   gemv        decode GEMM, whole-K (ll_op_gemm path 1) and split-K (ll_op_gemm_splitk),
               M = the workload's batch; weights rotate over >= 1 GiB so they stream from HBM
   attn        prefill attention (ll_op_attn_prefill) and decode attention (ll_op_attn_decode)
+  vendor      the vendor library's bf16 GEMM (torch.matmul, i.e. hipBLASLt) on the prefill GEMM
+              shapes: a reference for what this GPU reaches on the same products, not part of the
+              path
 Each line: kernel, workload, shape, mean time per call, achieved rate and the fraction of the
 MI355X peak (HBM 8 TB/s; bf16 MFMA 2.5 PFLOP/s).  Inputs are random; only timing matters
 here (numerics are covered by tests/test_kernels_gpu.py).
@@ -90,6 +93,18 @@ def bench_gemv(cfg, batch, iters):
         torch.cuda.empty_cache()
 
 
+def bench_vendor(cfg, lens, iters):
+    import torch
+    M = int(sum(lens))
+    for name, n, k in linear_shapes(cfg):
+        a = torch.randn(M, k, device="cuda").to(torch.bfloat16)
+        w = torch.randn(n, k, device="cuda").to(torch.bfloat16)
+        us = _timeit(lambda i: torch.matmul(a, w.t()), iters)
+        _line("vendor_gemm", cfg.name, f"{name} M={M} N={n} K={k}", us, 2.0 * M * n * k, "flop")
+        del a, w
+        torch.cuda.empty_cache()
+
+
 def bench_attn(cfg, lens, n_decode, iters):
     import torch
     from paper_2608_21836_amd.binding import op_attn_decode, op_attn_prefill
@@ -133,6 +148,8 @@ def main() -> int:
             bench_gemv(cfg, len(lens), args.iters)
         if "attn" in kinds:
             bench_attn(cfg, lens, cfg.n_decode, args.iters)
+        if "vendor" in kinds:
+            bench_vendor(cfg, lens, args.iters)
     return 0
 
 
