@@ -166,13 +166,18 @@ typedef enum {
   LL_OPT_ATTN_DECODE_CHUNK = 4,/* 0 (default): cached keys per decode-attention block from the
                                   load-time plan; 64, 128 or 256 override it (not below the plan's
                                   value: the workspace holds the plan's number of splits) */
-  LL_OPT_DECODE_FUSED = 5,     /* Mamba model only (ll_mamba.h): 1 (default): a decode step of at
-                                  most 4 sequences runs the conv step in the in_proj epilogue and
-                                  x_proj inside the scan-step kernel; 2: as 1, and out_proj with
-                                  the residual add inside the scan step too, its 32-channel
-                                  shares added with fp32 atomics (the summation order, hence the
-                                  last bits, can differ between runs); 0: separate conv, x_proj
-                                  and scan kernels.  The decoder rejects it (LL_ERR_UNSUPPORTED) */
+  LL_OPT_DECODE_FUSED = 5,     /* Decoder: 0 (default): the decode attention's splits are merged
+                                  by a kernel of their own; 1: a decode step of at most 16
+                                  sequences whose attention uses 2..16 splits merges them while
+                                  the O projection stages its A rows (same arithmetic, same
+                                  bits; one launch per layer fewer).  Mamba model (ll_mamba.h):
+                                  1 (default): a decode step of at most 4 sequences runs the conv
+                                  step in the in_proj epilogue and x_proj inside the scan-step
+                                  kernel; 2: as 1, and out_proj with the residual add inside the
+                                  scan step too, its 32-channel shares added with fp32 atomics
+                                  (the summation order, hence the last bits, can differ between
+                                  runs); 0: separate conv, x_proj and scan kernels.  The Mamba2
+                                  and RG-LRU models reject it (LL_ERR_UNSUPPORTED) */
   LL_OPT_COUNT = 6
 } ll_option;
 

@@ -24,7 +24,7 @@ LL_K_COUNT = 11
 OPTIONS = {"decode_graph": 0, "prefill_splitk": 1, "decode_splitk": 2, "prefill_tile": 3,
            "attn_decode_chunk": 4, "decode_fused": 5}
 DECODER_OPTIONS = ("decode_graph", "prefill_splitk", "decode_splitk", "prefill_tile",
-                   "attn_decode_chunk")
+                   "attn_decode_chunk", "decode_fused")
 MAMBA_OPTIONS = ("decode_graph", "prefill_splitk", "decode_splitk", "prefill_tile", "decode_fused")
 MAMBA2_OPTIONS = ("decode_graph", "prefill_splitk", "decode_splitk", "prefill_tile")
 RG_OPTIONS = MAMBA2_OPTIONS

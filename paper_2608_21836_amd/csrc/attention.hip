@@ -518,7 +518,6 @@ __global__ __launch_bounds__(HD) void k_attn_combine(const float *__restrict__ p
 
 // The merge for up to kCombineDirectSplits splits: one thread per output element, every
 // load issued up front (one memory round trip, no block-wide steps).
-constexpr int kCombineDirectSplits = 16;
 template <typename T, int HD>
 __global__ __launch_bounds__(HD) void k_attn_combine_direct(const float *__restrict__ part_o,
                                                             const float *__restrict__ part_ml,

@@ -577,8 +577,36 @@ __global__ __launch_bounds__(BN * 2, 1) void k_gemm_big(const T *__restrict__ A,
 // the side.  The per-row factor 1/sqrt(mean(x^2) + eps) of RMSNorm does not depend on the
 // column, so it scales the finished dot products in the epilogue:
 //   (x * s * g) . w = s * ((x * g) . w).
+// kAMerge (the decode O projection) stages the merge of the decode attention's split
+// partials, computed exactly as the merge kernel computes it, so the attention output never
+// goes through global memory and the merge kernel's launch disappears.
 // ------------------------------------------------------------------------------------------
-enum AMode : int { kAGlobal = 0, kAStaged = 1, kANorm = 2 };
+enum AMode : int { kAGlobal = 0, kAStaged = 1, kANorm = 2, kAMerge = 3 };
+
+// Rows [m_base, m_base + nrows) of the attention-merge operand into LDS (row stride lds_ld):
+// element (r, h * hd + d) is the merge of head h's splits for sequence m_base + r.  MAXS >= the
+// split count; slots past a row's split count carry weight 0 and add exact zeros, so the value
+// equals the merge kernel's (which merges up to kCombineDirectSplits slots).  Each thread
+// merges two elements at once so that both sets of loads are in flight together.
+template <int MAXS, typename T>
+__device__ __forceinline__ void stage_attn_merge(const AttnMergeIn &mg, T *sA, int lds_ld, int K,
+                                                 int nrows, int m_base) {
+  const int hd = mg.head_dim, hq = K / hd, total = nrows * K;
+  auto merged = [&](int i) -> float {
+    const int r = i / K, c = i - r * K, h = c / hd, d = c - h * hd;
+    const int b = m_base + r;
+    const int S = min(mg.lens[b] + mg.len_add, mg.max_ctx);
+    const int ns = max((S + mg.kpb - 1) / mg.kpb, 1);
+    const size_t base = ((size_t)b * hq + h) * mg.nsplit;
+    return merge_splits_direct<MAXS>(mg.part_ml + base * 2, mg.part_o + base * hd + d, hd, ns);
+  };
+  for (int i = threadIdx.x; i < total; i += 1024) {
+    const int i2 = min(i + 512, total - 1);  // a repeat of the last element when past the end
+    const float v0 = merged(i), v1 = merged(i2);
+    sA[(size_t)(i / K) * lds_ld + i % K] = from_f32<T>(v0);
+    if (i + 512 < total) sA[(size_t)(i2 / K) * lds_ld + i2 % K] = from_f32<T>(v1);
+  }
+}
 
 template <typename T, int MT, int NB, int AM, typename Epi, int KS = 1>
 __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, int lda,
@@ -668,6 +696,12 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
       *reinterpret_cast<F *>(sA + (size_t)r * lds_ld + c * EPL) =
           load_frag<F>(A + (size_t)(m_base + r) * lda + c * EPL);
     }
+    __syncthreads();
+  } else if constexpr (AM == kAMerge) {
+    // weight tiles of the first batch are already in flight
+    if (norm.merge.nsplit <= 4) stage_attn_merge<4>(norm.merge, sA, lds_ld, K, nrows, m_base);
+    else if (norm.merge.nsplit <= 8) stage_attn_merge<8>(norm.merge, sA, lds_ld, K, nrows, m_base);
+    else stage_attn_merge<kCombineDirectSplits>(norm.merge, sA, lds_ld, K, nrows, m_base);
     __syncthreads();
   }
   auto a_frag = [&](int mt, int kb) -> F {
@@ -1067,6 +1101,7 @@ hipError_t run_skinny(const void *a, int lda, const NormIn *norm,
     if (norm && !one) return hipErrorInvalidValue;
     // up to 16 rows: A from LDS when the rows fit, else from global memory
     const int am = !one ? kAGlobal
+                   : norm && norm->merge.part_o ? kAMerge
                    : norm ? kANorm
                    : skinny_norm_lds(sizeof(T), m - mb, k) <= kSkinnyMaxNormLds ? kAStaged : kAGlobal;
     hipError_t e = hipErrorInvalidValue;
@@ -1076,6 +1111,9 @@ hipError_t run_skinny(const void *a, int lda, const NormIn *norm,
   do {                                          \
     if (!one) LL_SKINNY(2, NB, kAGlobal);        \
     else if (am == kANorm) LL_SKINNY(1, NB, kANorm); \
+    else if (am == kAMerge) {                    \
+      if constexpr (std::is_same<Epi, EpiResid>::value) LL_SKINNY(1, NB, kAMerge); \
+    }                                            \
     else if (am == kAStaged) LL_SKINNY(1, NB, kAStaged); \
     else LL_SKINNY(1, NB, kAGlobal);             \
   } while (0)
@@ -1129,7 +1167,15 @@ hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm,
   if (ep.kind == kEpiQkv && (!ep.act || !ep.kcache || !ep.vcache || !ep.row_pos ||
                              !ep.rope_cos || !ep.rope_sin))
     return hipErrorInvalidValue;
-  if (norm && (!norm->x || !norm->gain)) return hipErrorInvalidValue;
+  if (norm && !norm->merge.part_o && (!norm->x || !norm->gain)) return hipErrorInvalidValue;
+  if (norm && norm->merge.part_o) {
+    // The attention-merge operand: decode GEMMs of at most 16 rows with the residual epilogue.
+    const AttnMergeIn &mg = norm->merge;
+    if (kTiled || ep.kind != kEpiResid || m > 16 || !mg.part_ml || !mg.lens ||
+        mg.head_dim < 1 || k % mg.head_dim || mg.kpb < 1 || mg.max_ctx < 1 || mg.nsplit < 2 ||
+        mg.nsplit > kCombineDirectSplits || (long)mg.kpb * mg.nsplit < mg.max_ctx)
+      return hipErrorInvalidValue;
+  }
   if (ep.kind == kEpiBiasResid && (!ep.out_f32 || !ep.bias)) return hipErrorInvalidValue;
   if (ep.kind == kEpiGeglu && (!ep.act || !ep.bias || !ep.bias2)) return hipErrorInvalidValue;
   if (ep.kind == kEpiRgIn &&

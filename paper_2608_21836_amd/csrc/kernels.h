@@ -123,13 +123,29 @@ struct EpiParams {
   int rg_fresh = 0, width = 0, group_n = 0, group_k = 0;
 };
 
-// RMSNorm computed inside the decode GEMM (A = RMSNorm(x[rowmap[r]]) * gain).
+// Decode attention merges at most this many splits in one pass (all loads up front).
+constexpr int kCombineDirectSplits = 16;
+
+// A operand of the decode O projection built from the decode attention's split partials
+// (part_o [row][head][split][head_dim], part_ml [row][head][split][2] = (max, sum), as
+// launch_attn_decode leaves them with skip_merge): row b, column h * head_dim + d holds the
+// merged output of head h, rounded to the GEMM type -- the value the merge kernel would have
+// written.  2 <= nsplit <= kCombineDirectSplits; rows use min(lens[b] + len_add, max_ctx) keys.
+struct AttnMergeIn {
+  const float *part_o = nullptr, *part_ml = nullptr;
+  const int *lens = nullptr;
+  int len_add = 0, head_dim = 0, kpb = 0, nsplit = 0, max_ctx = 0;
+};
+
+// RMSNorm computed inside the decode GEMM (A = RMSNorm(x[rowmap[r]]) * gain), or, when
+// merge.part_o is set (x and gain unused), the attention merge above.
 struct NormIn {
   const float *x = nullptr;
   int ldx = 0;
   const int *rowmap = nullptr;  // nullable
   const void *gain = nullptr;
   float eps = 0.f;
+  AttnMergeIn merge;
 };
 
 // Prefill GEMM: MFMA on tiles streamed into LDS through a 4-stage ring (256 x 256 or

@@ -315,6 +315,16 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
   const bool fuse_norm = decode && rows <= kFusedNormMaxRows &&
                          skinny_norm_lds(elem_bytes(dt), rows, d) <= kSkinnyMaxNormLds;
   const AttnDecodePlan ap = m->attn_plan();
+  // LL_OPT_DECODE_FUSED: the O projection merges the attention splits while staging its A rows
+  // (the merge kernel is not launched).
+  const bool merge_in_o = decode && m->opt[LL_OPT_DECODE_FUSED] && ap.nsplit > 1 &&
+                          ap.nsplit <= kCombineDirectSplits && rows <= kFusedNormMaxRows &&
+                          skinny_norm_lds(elem_bytes(dt), rows, qd) <= kSkinnyMaxNormLds;
+  NormIn merge_a;
+  if (merge_in_o)
+    merge_a.merge = AttnMergeIn{m->at<float>(m->L.part_o), m->at<float>(m->L.part_ml),
+                                m->at<int>(m->L.lens), 1, c.head_dim, ap.kpb, ap.nsplit,
+                                c.max_ctx};
   float *x = m->at<float>(m->L.x);
   float *splitk_ws = m->L.splitk_bytes ? m->at<float>(m->L.splitk) : nullptr;
   const bool use_split = decode ? m->opt[LL_OPT_DECODE_SPLITK] : m->opt[LL_OPT_PREFILL_SPLITK];
@@ -369,7 +379,7 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
       LL_HIP(launch_attn_decode(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
                                 m->at<int>(m->L.lens), 1, m->at(m->L.o), qd, rows, c.n_heads,
                                 c.n_kv_heads, c.max_ctx, ap, m->at<float>(m->L.part_o),
-                                m->at<float>(m->L.part_ml), s, false, m->paging()));
+                                m->at<float>(m->L.part_ml), s, merge_in_o, m->paging()));
     } else {
       LL_HIP(launch_attn_prefill(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
                                  m->at(m->L.o), qd, m->at<int>(m->L.cu),
@@ -379,8 +389,8 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
     m->mark(LL_K_O);
     {
       const PostNorm pn = post_norm(m->L.mlp_norm[l], m->L.h);
-      LL_HIP(gemm(m->at(m->L.o), qd, nullptr, m->at(m->L.wo[l]), d, qd, resid_epi(m),
-                  fuse_norm ? nullptr : &pn, &h_ready));
+      LL_HIP(gemm(m->at(m->L.o), qd, merge_in_o ? &merge_a : nullptr, m->at(m->L.wo[l]), d, qd,
+                  resid_epi(m), fuse_norm ? nullptr : &pn, &h_ready));
     }
     st = normed(m->L.mlp_norm[l], &nrm);
     if (st != LL_OK) return st;
@@ -718,7 +728,8 @@ ll_status ll_set_option(ll_model *m, int32_t option, int32_t value) {
                     "holds %d splits)", value, m->L.attn.kpb, m->L.attn.nsplit);
       break;
     case LL_OPT_DECODE_FUSED:
-      return fail(LL_ERR_UNSUPPORTED, "option %d applies to the Mamba model only", option);
+      if (value != 0 && value != 1) return fail(LL_ERR_INVALID_ARGUMENT, "decode fused 0 or 1");
+      break;
     default:
       return fail(LL_ERR_INVALID_ARGUMENT, "unknown option %d", option);
   }
@@ -732,8 +743,6 @@ ll_status ll_get_option(const ll_model *m, int32_t option, int32_t *value) {
   g_err.clear();
   if (!m || !value) return fail(LL_ERR_INVALID_ARGUMENT, "NULL argument");
   if (option < 0 || option >= LL_OPT_COUNT) return fail(LL_ERR_INVALID_ARGUMENT, "unknown option %d", option);
-  if (option == LL_OPT_DECODE_FUSED)
-    return fail(LL_ERR_UNSUPPORTED, "option %d applies to the Mamba model only", option);
   *value = m->opt[option];
   return LL_OK;
 }

@@ -61,6 +61,7 @@ KNOBS: List[Tuple[str, Tuple[int, ...], Tuple[str, ...]]] = [
     ("decode_splitk", (1, 0, 2), ("qkv_rope_append", "o_proj_resid", "gate_up_swiglu",
                                "down_resid")),
     ("attn_decode_chunk", (0, 64, 128, 256), ("attention", "attn_combine")),
+    ("decode_fused", (0, 1), ("attention", "attn_combine", "o_proj_resid")),
     ("decode_graph", (1, 0), ("qkv_rope_append", "attention", "attn_combine", "o_proj_resid",
                               "gate_up_swiglu", "down_resid", "lm_head_argmax", "embed",
                               "argmax_reduce", "rmsnorm")),

@@ -58,5 +58,5 @@ def test_max_row_error_is_relative_to_each_reference_row():
 def test_every_knob_default_is_listed_first():
     # the first candidate of each knob is the library default (ll.h)
     defaults = {"prefill_tile": 0, "prefill_splitk": 1, "decode_splitk": 1,
-                "attn_decode_chunk": 0, "decode_graph": 1}
+                "attn_decode_chunk": 0, "decode_fused": 0, "decode_graph": 1}
     assert {k[0]: k[1][0] for k in tuner.KNOBS} == defaults

@@ -33,6 +33,10 @@ CASES = [
     ("t-f32-ragged", {"decode_splitk": 2}),
     ("125m", {"decode_splitk": 2}),
     ("t-b32-hd128", {"prefill_tile": 1, "attn_decode_chunk": 256}),
+    ("t-gqa-hd64", {"decode_fused": 1}),       # attention merge inside the O projection
+    ("t-f32-ragged", {"decode_fused": 1}),
+    ("125m", {"decode_fused": 1}),
+    ("t-gqa-hd128", {"decode_fused": 1, "decode_splitk": 2}),
 ]
 
 
@@ -79,3 +83,21 @@ def test_tuner_accepts_only_passing_faster_variants():
     ref_logits, ref_tokens = teacher_forced_run(OracleModel(cfg, w), lens, packed, cfg.n_decode)
     gl, gt = run_gpu_teacher_forced(cfg, w, lens, packed, ref_tokens, cfg.n_decode, options=opts)
     assert judge(cfg.name, cfg.dtype, ref_logits, gl, gt).ok(cfg.dtype)
+
+
+@pytest.mark.parametrize("name", ["t-gqa-hd64", "t-f32-ragged", "125m"])
+def test_merge_in_o_projection_is_bitwise_the_merge_kernel(name):
+    """decode_fused 1 stages the attention merge inside the O projection with the merge
+    kernel's arithmetic, so the logits equal the two-kernel path's bit for bit."""
+    import numpy as np
+    cfg = get_config(name)
+    w = gen.weights(cfg)
+    lens, packed = gen.prompt_tokens(cfg)
+    nd = min(cfg.n_decode, 24)
+    ref_t = np.zeros((nd + 1, len(lens)), dtype=np.int64)      # fixed inputs
+    base_l, base_t = run_gpu_teacher_forced(cfg, w, lens, packed, ref_t, nd)
+    for graph in (1, 0):
+        fl, ft = run_gpu_teacher_forced(cfg, w, lens, packed, ref_t, nd,
+                                        options={"decode_fused": 1, "decode_graph": graph})
+        assert np.array_equal(fl, base_l) and np.array_equal(ft, base_t), \
+            f"graph {graph}: max diff {np.abs(fl - base_l).max()}"
