@@ -51,6 +51,19 @@ def accepted_options(workload: str) -> Dict[str, int]:
     with open(ACCEPTED_PATH) as f:
         return {k: int(v) for k, v in json.load(f).get(workload, {}).get("options", {}).items()}
 
+# (option, value) pairs whose kernels add partial sums with fp32 atomics: the summation order,
+# hence the last bits of the result, can differ between runs.  The tuner may accept them (they
+# pass the same in-model check), and the store records them, so that a deployment that needs
+# bitwise repeatable runs can leave them out; every other variant is bitwise repeatable.
+NONDETERMINISTIC = {("decode_splitk", 2), ("decode_fused", 2)}
+
+
+def deterministic_options(workload: str) -> Dict[str, int]:
+    """accepted_options(workload) without the variants that give up bitwise repeatability."""
+    return {k: v for k, v in accepted_options(workload).items()
+            if (k, v) not in NONDETERMINISTIC}
+
+
 # Variants: option name, candidate values (the first is the library default), kernel classes
 # whose time the option changes.
 KNOBS: List[Tuple[str, Tuple[int, ...], Tuple[str, ...]]] = [
@@ -289,6 +302,12 @@ def main() -> int:
     ap.add_argument("--store", default=ACCEPTED_PATH,
                     help="file --write merges into (default: accepted_options.json here)")
     args = ap.parse_args()
+    if args.write and not os.path.exists(args.store):
+        # --write merges one workload's entry into the store; starting from an empty file
+        # would drop every other workload's accepted options
+        print(f"--write: the store {args.store} does not exist (copy the committed "
+              "accepted_options.json there first)", file=sys.stderr)
+        return 2
     import numpy as np
     import torch
     from synth import gen, get_config
@@ -338,14 +357,15 @@ def main() -> int:
     print(json.dumps(result))
     model.close()
     if args.write:
-        store = {}
-        if os.path.exists(args.store):
-            with open(args.store) as f:
-                store = json.load(f)
+        with open(args.store) as f:   # checked to exist before tuning
+            store = json.load(f)
+        accepted = {r.option: r.chosen for r in reports if r.accepted}
         store[cfg.name] = {
             "delta": args.delta,
-            "options": {r.option: r.chosen for r in reports if r.accepted},
-            "ell": {r.option: r.candidates[r.chosen]["ell"] for r in reports if r.accepted}}
+            "options": accepted,
+            "ell": {r.option: r.candidates[r.chosen]["ell"] for r in reports if r.accepted},
+            "nondeterministic": sorted(o for o, v in accepted.items()
+                                       if (o, v) in NONDETERMINISTIC)}
         with open(args.store, "w") as f:
             json.dump(store, f, indent=1, sort_keys=True)
             f.write("\n")

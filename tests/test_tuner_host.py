@@ -60,3 +60,34 @@ def test_every_knob_default_is_listed_first():
     defaults = {"prefill_tile": 0, "prefill_splitk": 1, "decode_splitk": 1,
                 "attn_decode_chunk": 0, "decode_fused": 0, "decode_graph": 1}
     assert {k[0]: k[1][0] for k in tuner.KNOBS} == defaults
+
+
+def test_accepted_options_cover_every_bench_workload():
+    """Every bench workload keeps its entry in the store (a --write of one workload merges into
+    the file and never drops the others); option names and values are ones the tuner knows, and
+    the non-deterministic variants are recorded as such."""
+    import json
+    with open(tuner.ACCEPTED_PATH) as f:
+        store = json.load(f)
+    assert set(store) == {"125m", "1b-gqa", "7b-mha", "8b-gqa", "mamba-130m", "mamba2-130m",
+                          "rglru-2b"}
+    known = {}
+    for table in (tuner.KNOBS, tuner.MAMBA_KNOBS, tuner.MAMBA2_KNOBS, tuner.RG_KNOBS):
+        for name, values, _ in table:
+            known.setdefault(name, set()).update(values)
+    for wl, entry in store.items():
+        for name, value in entry["options"].items():
+            assert value in known[name], (wl, name, value)
+        assert set(entry["ell"]) == set(entry["options"]), wl
+        assert all(entry["ell"][k] <= 1 - entry["delta"] for k in entry["ell"]), wl
+        nd = {k for k, v in entry["options"].items() if (k, v) in tuner.NONDETERMINISTIC}
+        assert set(entry["nondeterministic"]) == nd, wl
+        assert tuner.deterministic_options(wl) == {k: v for k, v in entry["options"].items()
+                                                   if k not in nd}
+
+
+def test_write_refuses_a_missing_store(tmp_path, monkeypatch):
+    import sys
+    monkeypatch.setattr(sys, "argv", ["tuner", "--config", "125m", "--write",
+                                      "--store", str(tmp_path / "none.json")])
+    assert tuner.main() == 2
