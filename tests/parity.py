@@ -5,8 +5,13 @@ Acceptance rules (the readings listed in the design doc):
   * fp32 workloads: every compared logit within 1e-4 of the oracle, and the greedy token equal
     to the oracle's wherever the oracle's top-2 margin is >= 1e-3.
   * bf16 workloads: per compared row (sequence x step) max |gpu - oracle| <= 2e-2 * (oracle
-    row max - row min).  Greedy-token disagreements at margin >= 1e-3 are counted and
-    reported; each must be explained by precision: margin <= 2 x that row's max logit error.
+    row max - row min).  Greedy-token disagreements at margin >= 1e-3 ("literal" mismatches)
+    are counted and reported with their margins.  Each must be explained by precision: the
+    two competing logits (the oracle's choice and the GPU's) carry errors no larger than
+    ERR_OUTLIER times the row's root-mean-square logit error, i.e. the flip comes from the
+    same rounding noise that moves every logit of the row, not from an error that singles out
+    the top of the row.  (A flip needs e_gpu - e_oracle >= margin, so this also bounds the
+    margin of an accepted flip by 2 * ERR_OUTLIER * rms.)
 Rows compared: the prefill logits at each sequence's last prompt position and every
 teacher-forced decode step (both sides consume the oracle's tokens).
 """
@@ -26,6 +31,9 @@ def log(msg: str) -> None:
     sys.stdout.flush()
 
 
+ERR_OUTLIER = 4.0
+
+
 @dataclasses.dataclass
 class ParityReport:
     name: str
@@ -36,33 +44,43 @@ class ParityReport:
     unexplained_mismatches: int
     details: List[str]
 
-    def ok(self, dtype: str) -> bool:
+    def ok(self, dtype: str, quant: float = 0.0) -> bool:
+        """quant: relative error of stored reference logits (per unit of row range), taken off
+        the bf16 bar so that a stored reference never loosens it."""
         if dtype == "f32":
             return self.max_abs_err <= 1e-4 and self.literal_mismatches == 0
-        return self.worst_rel_row_err <= 2e-2 and self.unexplained_mismatches == 0
+        return self.worst_rel_row_err <= 2e-2 - quant and self.unexplained_mismatches == 0
 
 
 def judge(name: str, dtype: str, ref_logits: np.ndarray, gpu_logits: np.ndarray,
-          gpu_tokens: np.ndarray) -> ParityReport:
-    """ref/gpu logits [steps, B, V]; gpu_tokens [steps, B] (the library's fused argmax)."""
+          gpu_tokens: np.ndarray, ref_margin=None, ref_tokens=None) -> ParityReport:
+    """ref/gpu logits [steps, B, V]; gpu_tokens [steps, B] (the library's fused argmax).
+    ref_margin / ref_tokens: the oracle's fp64 top-2 margins and greedy tokens, when the
+    reference logits are a stored (rounded) copy; computed from ref_logits otherwise."""
     ref = ref_logits.astype(np.float64)
     gpu = gpu_logits.astype(np.float64)
     err = np.abs(gpu - ref)
     row_err = err.max(axis=-1)
     row_range = ref.max(axis=-1) - ref.min(axis=-1)
-    part = np.partition(ref, -2, axis=-1)
-    margin = part[..., -1] - part[..., -2]
-    ref_tok = np.argmax(ref, axis=-1)
+    if ref_margin is None:
+        part = np.partition(ref, -2, axis=-1)
+        margin = part[..., -1] - part[..., -2]
+    else:
+        margin = np.asarray(ref_margin, dtype=np.float64)
+    ref_tok = np.argmax(ref, axis=-1) if ref_tokens is None else np.asarray(ref_tokens)
     # the library's fused argmax must agree bitwise with an argmax over its own logits
     own = np.argmax(gpu_logits, axis=-1)
     assert np.array_equal(own, gpu_tokens), f"{name}: fused argmax disagrees with its logits"
     mism = (gpu_tokens != ref_tok) & (margin >= 1e-3)
+    row_rms = np.sqrt(np.mean((gpu - ref) ** 2, axis=-1))
     details, unexplained = [], 0
     for s, b in zip(*np.nonzero(mism)):
-        explained = margin[s, b] <= 2 * row_err[s, b]
+        i, j = ref_tok[s, b], gpu_tokens[s, b]
+        e_i, e_j = gpu[s, b, i] - ref[s, b, i], gpu[s, b, j] - ref[s, b, j]
+        explained = max(abs(e_i), abs(e_j)) <= ERR_OUTLIER * row_rms[s, b]
         unexplained += int(not explained)
-        details.append(f"step {s} seq {b}: oracle {ref_tok[s, b]} gpu {gpu_tokens[s, b]} margin "
-                       f"{margin[s, b]:.3e} row max err {row_err[s, b]:.3e} "
+        details.append(f"step {s} seq {b}: oracle {i} gpu {j} margin {margin[s, b]:.3e} "
+                       f"errors {e_i:+.3e} / {e_j:+.3e} row rms err {row_rms[s, b]:.3e} "
                        f"{'precision-explained' if explained else 'UNEXPLAINED'}")
     return ParityReport(name, int(np.prod(row_err.shape)), float(err.max()),
                         float((row_err / row_range).max()), int(mism.sum()), unexplained, details)
