@@ -65,19 +65,28 @@ ll_status ll_op_gemm_prefill_splitk(int32_t dtype, int32_t m, int32_t n, int32_t
 size_t ll_op_gemm_prefill_splitk_scratch(int32_t dtype, int32_t m, int32_t n, int32_t k);
 
 /* Causal grouped-query prefill attention over packed ragged sequences (appendix
- * "Deployment Kernel Families": one program per query tile and head, KV head from the head
- * grouping, causal mask in the score update, fp32 online-softmax statistics).
+ * "Deployment Kernel Families", Table A.4: programs over query tiles, KV head from the head
+ * grouping with KV loads shared by the heads of a group, causal mask in the score update,
+ * fp32 online-softmax statistics).  bf16 with n_heads / n_kv_heads >= 2: one block per (query
+ * tile, KV head) covering the whole head group; otherwise one block per (query tile, head).
  * q T [sum(seq_lens), n_heads*head_dim]; kcache/vcache T [batch][n_kv_heads][max_ctx]
  * [head_dim]; o T like q.  Sequence b's queries sit at positions cached_host[b] ..
  * cached_host[b] + seq_lens[b] - 1 (cached_host nullable: all 0) and the cache holds its
  * positions 0 .. cached_host[b] + seq_lens[b] - 1; query i attends to positions
  * 0 .. cached_host[b] + i (a prefill chunk on a populated cache when cached_host[b] > 0).
- * scratch >= 2048 + 16*(batch + sum(seq_lens)) bytes (device metadata). */
+ * scratch >= ll_op_attn_prefill_scratch(...) bytes (device metadata: offsets, positions and
+ * the blocks' work list), 256-byte aligned; LL_ERR_WORKSPACE when smaller. */
 ll_status ll_op_attn_prefill(int32_t dtype, int32_t batch, const int32_t *seq_lens_host,
                              const int32_t *cached_host, int32_t n_heads, int32_t n_kv_heads,
                              int32_t head_dim, int32_t max_ctx, const void *q,
                              const void *kcache, const void *vcache, void *o, void *scratch,
                              size_t scratch_bytes, void *stream);
+
+/* Scratch bytes ll_op_attn_prefill needs for these arguments (same meaning); 0 when they are
+ * invalid.  Host only. */
+size_t ll_op_attn_prefill_scratch(int32_t dtype, int32_t batch, const int32_t *seq_lens_host,
+                                  const int32_t *cached_host, int32_t n_heads,
+                                  int32_t n_kv_heads, int32_t head_dim, int32_t max_ctx);
 
 /* Decode attention: one query per sequence over ctx_lens_dev[b] cached keys (same
  * appendix: each KV tile loaded once for its whole query-head group; split over the cache

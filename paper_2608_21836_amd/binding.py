@@ -147,6 +147,9 @@ SIGNATURES = [
     ("ll_op_attn_prefill", c_int32, [c_int32, c_int32, POINTER(c_int32), POINTER(c_int32),
                                      c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
                                      c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+    ("ll_op_attn_prefill_scratch", c_size_t, [c_int32, c_int32, POINTER(c_int32),
+                                              POINTER(c_int32), c_int32, c_int32, c_int32,
+                                              c_int32]),
     ("ll_op_attn_decode", c_int32, [c_int32, c_int32, c_int32, c_int32, c_int32, c_int32,
                                     c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                     c_size_t, c_void_p]),
@@ -665,7 +668,10 @@ def op_attn_prefill(seq_lens, q, kcache, vcache, n_heads, n_kv_heads, head_dim, 
     lens = (c_int32 * b)(*[int(x) for x in seq_lens])
     starts = (c_int32 * b)(*[int(x) for x in cached]) if cached is not None else None
     o = torch.empty_like(q)
-    nbytes = 2048 + 16 * (b + int(sum(seq_lens)))
+    nbytes = load_library().ll_op_attn_prefill_scratch(_dt(q), b, lens, starts, n_heads,
+                                                       n_kv_heads, head_dim, max_ctx)
+    if nbytes == 0:
+        raise LLError(1, "ll_op_attn_prefill_scratch", "invalid arguments")
     scratch = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
     _check(load_library().ll_op_attn_prefill(_dt(q), b, lens, starts, n_heads, n_kv_heads,
                                              head_dim, max_ctx, q.data_ptr(), kcache.data_ptr(),

@@ -144,18 +144,138 @@ __global__ __launch_bounds__(256) void k_attn_prefill(
   }
 }
 
-// bf16 prefill attention on v_mfma_f32_32x32x16_bf16: one block per (128-query tile, query
-// head), 4 waves of 32 queries, key tiles of 64 through a double-buffered LDS stage.
-//   S^T = K Q^T: A = K rows (DMA'd from the cache straight into LDS in operand order), B = the
-//     wave's Q^T fragments, held in registers for the whole loop.  Lane l owns query l % 32
-//     and, of each 32-key block, the rows 8 (i / 4) + 4 (l / 32) + i % 4: the online-softmax
+// One 64-key tile of bf16 prefill attention for one wave of 32 queries (lane l owns query
+// qw + l % 32), on v_mfma_f32_32x32x16_bf16, from an LDS stage `st` that holds the tile's K in
+// operand order ([32-key block][16-dim step] tiles of 64 x 16 B) followed by its V^T
+// ([32-dim block][16-key step] tiles, keys in the order the score registers hold them).
+//   S^T = K Q^T: A = K rows from LDS, B = the wave's Q^T fragments (registers).  Lane l holds,
+//     of each 32-key block, rows 8 (i / 4) + 4 (l / 32) + i % 4: the online-softmax
 //     statistics need one exchange with lane l ^ 32.
-//   O^T += V^T P^T: B = P^T straight from the score registers (no lane movement), because the
-//     16 keys of a P V step are taken in the order the score registers hold them; the V^T
-//     tiles in LDS are written in that same key order.  Two waves build them: each lane loads
-//     8 keys x 8 dims (8 x 16 B), transposes them in registers and writes 8 x 16 B.
-// The other waves issue the K loads.  Loads for tile t + 1 are in flight while tile t
-// computes; the causal mask is applied only on tiles that reach past a wave's first query.
+//   O^T += V^T P^T: B = P^T straight from the score registers.
+// The causal / length mask runs only on tiles that reach past the wave's first query; the
+// accumulator is rescaled only when some row maximum grew (otherwise every factor is 1).
+template <int HD>
+__device__ __forceinline__ void attn_tile_bf16(const uint4 *__restrict__ st, const bf16x8 *qf,
+                                               f32x16 *acc, float &m_run, float &l_run, int kt,
+                                               int P0, int L, int qw, int my_q, bool q_ok,
+                                               float scale_log2, int lane) {
+  constexpr int BKV = 64, NKC = HD / 16, NDB = HD / 32, NPC = BKV / 16, KTILES = 2 * NKC;
+  const int g = lane >> 5;
+  f32x16 sc[2];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) sc[kb][i] = 0.f;
+#pragma unroll
+    for (int c = 0; c < NKC; ++c)
+      sc[kb] = mma32(*reinterpret_cast<const bf16x8 *>(&st[(kb * NKC + c) * 64 + lane]), qf[c], sc[kb]);
+  }
+  if (kt * BKV + BKV - 1 > P0 + qw || qw + 31 >= L) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int key = kt * BKV + 32 * kb + 8 * (i / 4) + 4 * g + (i % 4);
+        sc[kb][i] = (q_ok & (key <= P0 + my_q)) ? sc[kb][i] : -INFINITY;
+      }
+  }
+  // row maximum of the raw scores; scaling by a positive constant commutes with max
+  float tmax = -INFINITY;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) tmax = fmaxf(tmax, sc[kb][i]);
+  tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+  const float m_new = fmaxf(m_run, tmax * scale_log2);
+  const float base = m_new == -INFINITY ? 0.f : m_new;
+  if (__any(m_new > m_run)) {
+    const float alpha = __builtin_amdgcn_exp2f(m_run - base);
+    l_run *= alpha;
+#pragma unroll
+    for (int d = 0; d < NDB; ++d) acc[d] *= alpha;
+  }
+  m_run = m_new;
+  // p = 2^(s * scale - m); arguments are <= 0, so the hardware exp2 is exact enough (results
+  // below the fp32 normal range flush to 0)
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float p = __builtin_amdgcn_exp2f(fmaf(sc[kb][i], scale_log2, -base));
+      sc[kb][i] = p;
+      l_run += p;
+    }
+#pragma unroll
+  for (int c = 0; c < NPC; ++c) {
+    bf16x8 pf;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) pf[e] = static_cast<bf16>(sc[c / 2][8 * (c % 2) + e]);
+#pragma unroll
+    for (int d = 0; d < NDB; ++d)
+      acc[d] = mma32(*reinterpret_cast<const bf16x8 *>(&st[(KTILES + d * NPC + c) * 64 + lane]), pf, acc[d]);
+  }
+}
+
+// Normalised output rows of one wave: lane l writes dims 32 d + 8 j + 4 (l / 32) .. + 3 of its
+// query (the O^T accumulator layout), 8 bytes at a time.
+template <int HD>
+__device__ __forceinline__ void attn_store_bf16(bf16 *dst, const f32x16 *acc, float inv, int g) {
+  constexpr int NDB = HD / 32;
+  dst += 4 * g;
+#pragma unroll
+  for (int d = 0; d < NDB; ++d)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bf16 v0 = static_cast<bf16>(acc[d][4 * j] * inv), v1 = static_cast<bf16>(acc[d][4 * j + 1] * inv);
+      const bf16 v2 = static_cast<bf16>(acc[d][4 * j + 2] * inv), v3 = static_cast<bf16>(acc[d][4 * j + 3] * inv);
+      uint2 pk;
+      pk.x = (uint32_t)__builtin_bit_cast(uint16_t, v0) | ((uint32_t)__builtin_bit_cast(uint16_t, v1) << 16);
+      pk.y = (uint32_t)__builtin_bit_cast(uint16_t, v2) | ((uint32_t)__builtin_bit_cast(uint16_t, v3) << 16);
+      *reinterpret_cast<uint2 *>(dst + 32 * d + 8 * j) = pk;
+    }
+}
+
+// V^T task of one lane: 8 keys x 8 dims of a 64-key tile (dims 8 dg .. 8 dg + 7, 16-key step
+// pc, key group gg; element e < 4 is key 16 pc + 4 gg + e, e >= 4 is key 16 pc + 8 + 4 gg + e - 4),
+// loaded as 8 rows of 16 B (rows past the sequence read clamped, in bounds, and replaced by
+// zeros: their probabilities are 0 and the cache there may hold anything, NaN included) ...
+template <int HD>
+__device__ __forceinline__ void vt_load(uint4 *vr, const bf16 *Vc, size_t tb, int kt, int KL,
+                                        int task) {
+  constexpr int NPC = 4;
+  const int dg = task % (HD / 8), pc = (task / (HD / 8)) % NPC, gg = task / (HD / 8 * NPC);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int key = kt * 64 + 16 * pc + (e < 4 ? 4 * gg + e : 8 + 4 * gg + e - 4);
+    const uint4 v = *reinterpret_cast<const uint4 *>(Vc + tb + (size_t)(min(key, KL - 1) - kt * 64) * HD + 8 * dg);
+    vr[e] = key < KL ? v : make_uint4(0, 0, 0, 0);
+  }
+}
+// ... and written transposed: 8 fragments of 8 keys, one per dim, into the stage's V^T tiles.
+template <int HD>
+__device__ __forceinline__ void vt_store(uint4 *stage, const uint4 *vr, int task) {
+  constexpr int NPC = 4, KTILES = 2 * (HD / 16);
+  const int dg = task % (HD / 8), pc = (task / (HD / 8)) % NPC, gg = task / (HD / 8 * NPC);
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    uint32_t d[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t lo = reinterpret_cast<const uint32_t *>(&vr[2 * j])[t >> 1];
+      const uint32_t hi = reinterpret_cast<const uint32_t *>(&vr[2 * j + 1])[t >> 1];
+      d[j] = (t & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+    }
+    const int dim = 8 * dg + t;
+    stage[(KTILES + (dim / 32) * NPC + pc) * 64 + (dim % 32) + 32 * gg] = make_uint4(d[0], d[1], d[2], d[3]);
+  }
+}
+
+// bf16 prefill attention, one query head per block (the MHA workloads): one block per
+// (128-query tile, query head), 4 waves of 32 queries, key tiles of 64 through a
+// double-buffered LDS stage.  K tiles are DMA'd from the cache straight into LDS in operand
+// order (global_load_lds); two waves build the V^T tiles (each lane loads 8 keys x 8 dims,
+// transposes them in registers and writes 8 x 16 B), the other two issue the K loads.  Loads
+// for tile t + 1 are in flight while tile t computes (attn_tile_bf16).
 template <int HD>
 __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
     const bf16 *__restrict__ Q, int ldq, const bf16 *__restrict__ Kc, const bf16 *__restrict__ Vc,
@@ -203,9 +323,8 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
   const int ntiles = (P0 + min(q0 + QT, L) - 1) / BKV + 1;
 
   // K tile (kb, c): lane l reads key 32 kb + l % 32 (clamped into the sequence; rows past KL
-  // are masked), dims 16 c + 8 g.
-  // A tile's keys lie in one page (tiles start at cached positions and the clamp stays in
-  // the tile), so one base per tile serves every row.
+  // are masked), dims 16 c + 8 g.  A tile's keys lie in one page (tiles start at cached
+  // positions and the clamp stays in the tile), so one base per tile serves every row.
   auto k_issue = [&](int kt, int buf) {
     if (wave >= VW) {
       const size_t tb = kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD);
@@ -217,99 +336,12 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
       }
     }
   };
-  // V^T task of lane `tid` (waves < VW): dims 8 dg .. 8 dg + 7, key step pc, key group gg;
-  // element e < 4 is key 16 pc + 4 gg + e, element e >= 4 is key 16 pc + 8 + 4 gg + e - 4.
-  const int dg = tid % (HD / 8), pc = (tid / (HD / 8)) % NPC, gg = tid / (HD / 8 * NPC);
   uint4 vr[8];
   auto v_load = [&](int kt) {
-    if (wave < VW) {
-      const size_t tb = kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        // rows past the sequence are read clamped (in bounds) and replaced by zeros: their
-        // probabilities are 0, and the cache there may hold anything, NaN included
-        const int key = kt * BKV + 16 * pc + (e < 4 ? 4 * gg + e : 8 + 4 * gg + e - 4);
-        const uint4 v = *reinterpret_cast<const uint4 *>(
-            Vc + tb + (size_t)(min(key, KL - 1) - kt * BKV) * HD + 8 * dg);
-        vr[e] = key < KL ? v : make_uint4(0, 0, 0, 0);
-      }
-    }
+    if (wave < VW) vt_load<HD>(vr, Vc, kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD), kt, KL, tid);
   };
   auto v_store = [&](int buf) {
-    if (wave < VW) {
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        uint32_t d[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint32_t lo = reinterpret_cast<const uint32_t *>(&vr[2 * j])[t >> 1];
-          const uint32_t hi = reinterpret_cast<const uint32_t *>(&vr[2 * j + 1])[t >> 1];
-          d[j] = (t & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
-        }
-        const int dim = 8 * dg + t;
-        smem[buf * STAGE + (KTILES + (dim / 32) * NPC + pc) * 64 + (dim % 32) + 32 * gg] =
-            make_uint4(d[0], d[1], d[2], d[3]);
-      }
-    }
-  };
-  auto compute = [&](int kt, int buf) {
-    if (qw >= L || kt * BKV > P0 + qw + 31) return;  // nothing for this wave in this tile
-    const uint4 *st = &smem[buf * STAGE];
-    f32x16 sc[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) sc[kb][i] = 0.f;
-#pragma unroll
-      for (int c = 0; c < NKC; ++c)
-        sc[kb] = mma32(*reinterpret_cast<const bf16x8 *>(&st[(kb * NKC + c) * 64 + lane]), qf[c], sc[kb]);
-    }
-    // Causal / length mask, only on tiles that reach past the wave's first query.
-    if (kt * BKV + BKV - 1 > P0 + qw || qw + 31 >= L) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = kt * BKV + 32 * kb + 8 * (i / 4) + 4 * g + (i % 4);
-          sc[kb][i] = (q_ok & (key <= P0 + my_q)) ? sc[kb][i] : -INFINITY;
-        }
-    }
-    // Row maximum of the raw scores; scaling by a positive constant commutes with max.
-    float tmax = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) tmax = fmaxf(tmax, sc[kb][i]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-    const float m_new = fmaxf(m_run, tmax * scale_log2);
-    const float base = m_new == -INFINITY ? 0.f : m_new;
-    // Rescale only when some lane's maximum grew (otherwise every factor is exactly 1).
-    if (__any(m_new > m_run)) {
-      const float alpha = __builtin_amdgcn_exp2f(m_run - base);
-      l_run *= alpha;
-#pragma unroll
-      for (int d = 0; d < NDB; ++d) acc[d] *= alpha;
-    }
-    m_run = m_new;
-    // p = 2^(s * scale - m); arguments are <= 0, so the hardware exp2 is exact enough
-    // (results below the fp32 normal range flush to 0).
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sc[kb][i], scale_log2, -base));
-        sc[kb][i] = p;
-        l_run += p;
-      }
-#pragma unroll
-    for (int c = 0; c < NPC; ++c) {
-      bf16x8 pf;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) pf[e] = static_cast<bf16>(sc[c / 2][8 * (c % 2) + e]);
-#pragma unroll
-      for (int d = 0; d < NDB; ++d)
-        acc[d] = mma32(*reinterpret_cast<const bf16x8 *>(&st[(KTILES + d * NPC + c) * 64 + lane]), pf, acc[d]);
-    }
+    if (wave < VW) vt_store<HD>(&smem[buf * STAGE], vr, tid);
   };
 
   k_issue(0, 0);
@@ -323,27 +355,114 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
       k_issue(kt + 1, cur ^ 1);
       v_load(kt + 1);
     }
-    compute(kt, cur);
+    if (qw < L && kt * BKV <= P0 + qw + 31)  // else nothing for this wave in this tile
+      attn_tile_bf16<HD>(&smem[cur * STAGE], qf, acc, m_run, l_run, kt, P0, L, qw, my_q, q_ok,
+                         scale_log2, lane);
     if (more) v_store(cur ^ 1);
     __syncthreads();
   }
 
   l_run += __shfl_xor(l_run, 32);
-  if (q_ok) {
-    const float inv = 1.0f / l_run;
-    bf16 *dst = O + (size_t)(tok0 + my_q) * ldo + h * HD + 4 * g;
+  if (q_ok) attn_store_bf16<HD>(O + (size_t)(tok0 + my_q) * ldo + h * HD, acc, 1.0f / l_run, g);
+}
+
+// bf16 prefill attention for grouped heads (group G = H_q / H_kv >= 2), after the paper's
+// prefill kernel that shares KV loads according to the head grouping (appendix "Deployment
+// Kernel Families", Table A.4): one block of 8 waves per (query tile, KV head) holds every
+// query head of the group -- wave w takes head kvh G + w / QB and 32 queries of block w % QB
+// (QB = 8 / G; tiles of 32 QB queries) -- so each 64-key K / V tile is read from memory and
+// staged in LDS once for G heads.  All 8 waves DMA the K tiles; the V^T builder role (HD / 64
+// waves' worth of lanes) rotates over the waves from tile to tile so that no wave carries it
+// every time.  Blocks take their (sequence, query tile, KV head) from the work list in
+// XCD-owned ranges (AttnSched).
+template <int HD, int G>
+__global__ __launch_bounds__(512, 1) void k_attn_prefill_gqa(
+    const bf16 *__restrict__ Q, int ldq, const bf16 *__restrict__ Kc, const bf16 *__restrict__ Vc,
+    bf16 *__restrict__ O, int ldo, const int *__restrict__ cu, const int *__restrict__ kstart,
+    const int4 *__restrict__ sched, AttnSched as, int hkv, int max_ctx, float scale_log2,
+    KvPaging pg) {
+  constexpr int NW = 8, QB = NW / G, QT = 32 * QB, BKV = 64;
+  constexpr int NKC = HD / 16, NDB = HD / 32, NPC = BKV / 16;
+  constexpr int KTILES = 2 * NKC, VTILES = NDB * NPC;
+  constexpr int STAGE = (KTILES + VTILES) * 64;   // uint4 per stage
+  constexpr int VW = (HD / 8) * NPC * 2 / 64;     // waves' worth of V^T tasks per stage
+  static_assert(G >= 2 && G <= NW && NW % G == 0 && KTILES % NW == 0, "8 waves over the group");
+  __shared__ uint4 smem[2 * STAGE];
+
+  const int x = blockIdx.x % kXcds, e = as.cut[x] + (int)(blockIdx.x / kXcds);
+  if (e >= as.cut[x + 1]) return;   // this XCD's range is shorter than the longest one
+  const int4 en = sched[e];
+  const int b = en.x, kvh = en.z;
+  const int tok0 = cu[b], L = cu[b + 1] - tok0;
+  const int P0 = kstart ? kstart[b] : 0, KL = P0 + L;
+  const int q0 = en.y * QT;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 5;
+  const int h = kvh * G + wave / QB;
+  const int qw = q0 + 32 * (wave % QB);
+  const int my_q = qw + (lane & 31);
+  const bool q_ok = my_q < L;
+  const bf16x8 fz = frag_zero<bf16x8>();
+
+  bf16x8 qf[NKC];
 #pragma unroll
-    for (int d = 0; d < NDB; ++d)
+  for (int c = 0; c < NKC; ++c)
+    qf[c] = q_ok ? load_frag<bf16x8>(Q + (size_t)(tok0 + my_q) * ldq + h * HD + 16 * c + 8 * g) : fz;
+  f32x16 acc[NDB];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const bf16 v0 = static_cast<bf16>(acc[d][4 * j] * inv), v1 = static_cast<bf16>(acc[d][4 * j + 1] * inv);
-        const bf16 v2 = static_cast<bf16>(acc[d][4 * j + 2] * inv), v3 = static_cast<bf16>(acc[d][4 * j + 3] * inv);
-        uint2 pk;
-        pk.x = (uint32_t)__builtin_bit_cast(uint16_t, v0) | ((uint32_t)__builtin_bit_cast(uint16_t, v1) << 16);
-        pk.y = (uint32_t)__builtin_bit_cast(uint16_t, v2) | ((uint32_t)__builtin_bit_cast(uint16_t, v3) << 16);
-        *reinterpret_cast<uint2 *>(dst + 32 * d + 8 * j) = pk;
-      }
+  for (int d = 0; d < NDB; ++d)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[d][i] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const int ntiles = (P0 + min(q0 + QT, L) - 1) / BKV + 1;
+  auto k_issue = [&](int kt, int buf) {
+    const size_t tb = kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD);
+#pragma unroll
+    for (int i = 0; i < KTILES / NW; ++i) {
+      const int ti = wave + NW * i;
+      const int kb = ti / NKC, c = ti % NKC;
+      const int key = min(kt * BKV + 32 * kb + (lane & 31), KL - 1);
+      load_tile_to_lds(Kc + tb + (size_t)(key - kt * BKV) * HD + 16 * c + 8 * g,
+                       &smem[buf * STAGE + ti * 64]);
+    }
+  };
+  // builder waves of tile kt: VW consecutive waves starting at (VW kt) mod 8
+  auto v_task = [&](int kt) -> int {
+    const int r = (wave - VW * kt) & (NW - 1);
+    return r < VW ? r * 64 + lane : -1;
+  };
+  uint4 vr[8];
+  auto v_load = [&](int kt) {
+    const int task = v_task(kt);
+    if (task >= 0) vt_load<HD>(vr, Vc, kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD), kt, KL, task);
+  };
+  auto v_store = [&](int kt, int buf) {
+    const int task = v_task(kt);
+    if (task >= 0) vt_store<HD>(&smem[buf * STAGE], vr, task);
+  };
+
+  k_issue(0, 0);
+  v_load(0);
+  v_store(0, 0);
+  __syncthreads();
+  for (int kt = 0; kt < ntiles; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < ntiles;
+    if (more) {
+      k_issue(kt + 1, cur ^ 1);
+      v_load(kt + 1);
+    }
+    if (qw < L && kt * BKV <= P0 + qw + 31)
+      attn_tile_bf16<HD>(&smem[cur * STAGE], qf, acc, m_run, l_run, kt, P0, L, qw, my_q, q_ok,
+                         scale_log2, lane);
+    if (more) v_store(kt + 1, cur ^ 1);
+    __syncthreads();
   }
+
+  l_run += __shfl_xor(l_run, 32);
+  if (q_ok) attn_store_bf16<HD>(O + (size_t)(tok0 + my_q) * ldo + h * HD, acc, 1.0f / l_run, g);
 }
 
 constexpr int kMaxSplit = 128;  // blocks per (sequence, kv head)
@@ -533,6 +652,27 @@ __global__ __launch_bounds__(HD) void k_attn_combine_direct(const float *__restr
       merge_splits_direct<kCombineDirectSplits>(part_ml + base * 2, part_o + base * HD + d, HD, ns));
 }
 
+template <int HD>
+hipError_t run_prefill_gqa(int group, const void *q, int ldq, const void *kc, const void *vc,
+                           void *o, int ldo, const int *cu, const int *kstart, const int4 *sched,
+                           const AttnSched &as, int hkv, int max_ctx, hipStream_t s,
+                           const KvPaging &pg) {
+  const float scale_log2 = kLog2e / sqrtf((float)HD);
+#define LL_GQA(G)                                                                             \
+  LL_LAUNCH((k_attn_prefill_gqa<HD, G>), dim3(as.grid), dim3(512), 0, s,                      \
+            reinterpret_cast<const bf16 *>(q), ldq, reinterpret_cast<const bf16 *>(kc),        \
+            reinterpret_cast<const bf16 *>(vc), reinterpret_cast<bf16 *>(o), ldo, cu, kstart, \
+            sched, as, hkv, max_ctx, scale_log2, pg)
+  switch (group) {
+    case 2: LL_GQA(2); break;
+    case 4: LL_GQA(4); break;
+    case 8: LL_GQA(8); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef LL_GQA
+  return hipGetLastError();
+}
+
 template <typename T, int HD>
 hipError_t run_prefill(const void *q, int ldq, const void *kc, const void *vc, void *o, int ldo,
                        const int *cu, const int *kstart, const int2 *qtiles, int n_qtiles,
@@ -604,13 +744,58 @@ hipError_t run_decode(int group, const void *q, int ldq, const void *kc, const v
 
 }  // namespace
 
+AttnSched attn_prefill_sched(const PrefillMeta &pm, int group, int hkv) {
+  AttnSched as;
+  if (group < 2 || group > 8 || 8 % group || hkv < 1 || pm.batch < 1 || pm.batch > 256) return as;
+  as.qtile = attn_gqa_qtile(group);
+  // causal work of an entry ~ key tiles its queries scan; entries in the device's order
+  long total_work = 0;
+  for (int b = 0; b < pm.batch; ++b) {
+    const int nq = (pm.lens[b] + as.qtile - 1) / as.qtile;
+    for (int t = 0; t < nq; ++t)
+      total_work += (long)hkv * ((pm.start[b] + std::min((t + 1) * as.qtile, pm.lens[b]) + 63) / 64);
+    as.n_entries += nq * hkv;
+  }
+  // cut[x] = first entry at which the work done before it reaches x / kXcds of the total
+  long done = 0;
+  int e = 0, x = 1;
+  as.cut[0] = 0;
+  for (int b = 0; b < pm.batch; ++b) {
+    const int nq = (pm.lens[b] + as.qtile - 1) / as.qtile;
+    for (int k = 0; k < hkv; ++k)
+      for (int j = 0; j < nq; ++j, ++e) {
+        while (x < kXcds && done * kXcds >= total_work * x) as.cut[x++] = e;
+        const int t = nq - 1 - j;
+        done += (pm.start[b] + std::min((t + 1) * as.qtile, pm.lens[b]) + 63) / 64;
+      }
+  }
+  while (x <= kXcds) as.cut[x++] = as.n_entries;
+  int longest = 0;
+  for (int i = 0; i < kXcds; ++i) longest = std::max(longest, as.cut[i + 1] - as.cut[i]);
+  as.grid = kXcds * longest;
+  return as;
+}
+
 hipError_t launch_attn_prefill(int dtype, int head_dim, const void *q, int ldq, const void *kc,
                                const void *vc, void *o, int ldo, const int *cu,
                                const int *kstart, const int2 *qtiles, int n_qtiles, int hq,
-                               int hkv, int max_ctx, hipStream_t s, const KvPaging &pg) {
-  if (n_qtiles <= 0) return hipSuccess;
+                               int hkv, int max_ctx, hipStream_t s, const KvPaging &pg,
+                               const int4 *sched, const AttnSched *as) {
   if (pg.table && (pg.page_len < 256 || pg.page_len % 256 || pg.max_pages < 1))
     return hipErrorInvalidValue;
+  if (hkv < 1 || hq % hkv) return hipErrorInvalidValue;
+  if (attn_prefill_gqa(dtype, hq / hkv)) {
+    if (!sched || !as || as->qtile != attn_gqa_qtile(hq / hkv)) return hipErrorInvalidValue;
+    if (as->n_entries <= 0) return hipSuccess;
+    if (head_dim == 64)
+      return run_prefill_gqa<64>(hq / hkv, q, ldq, kc, vc, o, ldo, cu, kstart, sched, *as, hkv,
+                                 max_ctx, s, pg);
+    if (head_dim == 128)
+      return run_prefill_gqa<128>(hq / hkv, q, ldq, kc, vc, o, ldo, cu, kstart, sched, *as, hkv,
+                                  max_ctx, s, pg);
+    return hipErrorInvalidValue;
+  }
+  if (n_qtiles <= 0) return hipSuccess;
 #define LL_PREFILL(TT, HD)                                                                   \
   return run_prefill<TT, HD>(q, ldq, kc, vc, o, ldo, cu, kstart, qtiles, n_qtiles, hq, hkv, \
                              max_ctx, s, pg)

@@ -111,8 +111,25 @@ __global__ __launch_bounds__(kArgThreads) void k_argmax_reduce(const float *__re
 
 __global__ __launch_bounds__(256) void k_prefill_meta(PrefillMeta pm, int total, int qtile, int *cu,
                                                       int *row_seq, int *row_pos, int *last_row,
-                                                      int *lens_dev, int *kstart, int2 *qtiles) {
+                                                      int *lens_dev, int *kstart, int2 *qtiles,
+                                                      int4 *sched, int sched_qt, int n_sched,
+                                                      int hkv) {
   const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (sched && m < n_sched) {
+    // entry m of the grouped-query work list: sequences in order, then KV heads, then query
+    // tiles from the last one
+    int b = 0, base = 0;
+    for (;;) {
+      const int nq = (pm.lens[b] + sched_qt - 1) / sched_qt;
+      if (m < base + nq * hkv || b == pm.batch - 1) {
+        const int r = m - base, kvh = r / nq, j = r - kvh * nq;
+        sched[m] = make_int4(b, nq - 1 - j, kvh, 0);
+        break;
+      }
+      base += nq * hkv;
+      ++b;
+    }
+  }
   if (m < total) {
     int b = 0, first = 0;
     while (b < pm.batch - 1 && m >= first + pm.lens[b]) first += pm.lens[b++];
@@ -222,11 +239,15 @@ hipError_t launch_argmax_reduce(const float *pval, const int *pidx, int rows, in
 
 hipError_t launch_prefill_meta(const PrefillMeta &pm, int total, int qtile, int *cu,
                                int *row_seq, int *row_pos, int *last_row, int *lens_dev,
-                               int *kstart, int2 *qtiles, hipStream_t s) {
+                               int *kstart, int2 *qtiles, hipStream_t s, int4 *sched,
+                               const AttnSched *as, int hkv) {
   if (qtile <= 0 || pm.batch < 1 || pm.batch > 256) return hipErrorInvalidValue;
-  const int blocks = std::max(1, (total + 255) / 256);
+  const int n_sched = sched && as ? as->n_entries : 0;
+  if (sched && (!as || as->qtile <= 0 || hkv < 1)) return hipErrorInvalidValue;
+  const int blocks = std::max(1, (std::max(total, n_sched) + 255) / 256);
   LL_LAUNCH(k_prefill_meta, dim3(blocks), dim3(256), 0, s, pm, total, qtile, cu, row_seq,
-                     row_pos, last_row, lens_dev, kstart, qtiles);
+            row_pos, last_row, lens_dev, kstart, qtiles, n_sched ? sched : nullptr,
+            n_sched ? as->qtile : 1, n_sched, std::max(hkv, 1));
   return hipGetLastError();
 }
 

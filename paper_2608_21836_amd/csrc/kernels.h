@@ -222,9 +222,28 @@ struct PrefillMeta {
   int lens[256];
   int start[256];
 };
+// Grouped-query prefill attention (bf16, group = n_heads / n_kv_heads >= 2): one block of 8
+// waves per (query tile of attn_gqa_qtile(group) queries, KV head) covers every query head of
+// the group, so each K / V tile is read from memory once for the whole group.  The blocks'
+// work list (sequence, query tile, KV head) is written on the device in a fixed order --
+// sequence, KV head, query tiles from the last (the longest) -- and cut into kXcds contiguous
+// ranges of near-equal causal work: workgroup i runs on XCD i % kXcds, which takes range
+// i % kXcds entry by entry, so the tiles of one (sequence, KV head) share that XCD's L2.
+constexpr int kXcds = 8;
+struct AttnSched {
+  int qtile = 0;      // queries per block
+  int n_entries = 0;  // blocks with work
+  int grid = 0;       // workgroups launched (kXcds x the longest range)
+  int cut[kXcds + 1] = {};
+};
+inline bool attn_prefill_gqa(int dtype, int group) { return dtype == kBF16 && group >= 2; }
+inline int attn_gqa_qtile(int group) { return 256 / group; }
+AttnSched attn_prefill_sched(const PrefillMeta &pm, int group, int n_kv_heads);
+// sched (nullable): the work list of the grouped-query kernel, sized by as->n_entries.
 hipError_t launch_prefill_meta(const PrefillMeta &pm, int total, int qtile, int *cu_seqlens,
                                int *row_seq, int *row_pos, int *last_row, int *lens_dev,
-                               int *kstart, int2 *qtiles, hipStream_t s);
+                               int *kstart, int2 *qtiles, hipStream_t s, int4 *sched = nullptr,
+                               const AttnSched *as = nullptr, int n_kv_heads = 0);
 constexpr int kAttnQTile = 64;       // queries per block, fp32 prefill attention
 constexpr int kAttnQTileWide = 128;  // queries per block, bf16 prefill attention
 // Query-tile size the prefill attention kernel for (dtype, head_dim) expects in `qtiles`.
@@ -233,11 +252,14 @@ inline int attn_prefill_qtile(int dtype) { return dtype == kF32 ? kAttnQTile : k
 // Causal prefill attention of the packed queries over each sequence's cache: query i of
 // sequence b sits at position kstart[b] + i and attends to cached keys 0 .. kstart[b] + i
 // (kstart nullable: every sequence starts at 0).
+// With attn_prefill_gqa(dtype, group) the grouped-query kernel runs over `sched` / `as`
+// (qtiles / n_qtiles unused); otherwise one block per (query tile, query head) over qtiles.
 hipError_t launch_attn_prefill(int dtype, int head_dim, const void *q, int ldq,
                                const void *kcache, const void *vcache, void *o, int ldo,
                                const int *cu_seqlens, const int *kstart, const int2 *qtiles,
                                int n_qtiles, int n_heads, int n_kv_heads, int max_ctx,
-                               hipStream_t s, const KvPaging &pg = KvPaging{});
+                               hipStream_t s, const KvPaging &pg = KvPaging{},
+                               const int4 *sched = nullptr, const AttnSched *as = nullptr);
 
 // Decode attention: split over the cache length (chunk keys per block), then a merge kernel.
 // Keys attended per sequence: lens[b] + len_add (clamped to max_ctx).

@@ -37,7 +37,7 @@ struct Layout {
   size_t part_o = 0, part_ml = 0, pval = 0, pidx = 0;
   size_t splitk = 0, splitk_bytes = 0;  // fp32 split-K partials of the decode GEMMs
   size_t kstart = 0;                     // cached keys before each sequence's prefill chunk
-  size_t cu = 0, row_seq = 0, row_pos = 0, last_row = 0, lens = 0, qtiles = 0, err = 0;
+  size_t cu = 0, row_seq = 0, row_pos = 0, last_row = 0, lens = 0, qtiles = 0, sched = 0, err = 0;
   size_t total = 0;
   size_t kv_layer_elems = 0;
   size_t kv_table = 0;                   // paged cache: int32 [max_batch][kv_max_pages]
@@ -160,6 +160,11 @@ Layout make_layout(const ll_config &c) {
   L.lens = take(c.max_batch * 4);
   L.kstart = take(c.max_batch * 4);
   L.qtiles = take((R / kAttnQTile + c.max_batch + 1) * 8);
+  // work list of the grouped-query prefill attention: ceil(L_b / qtile) tiles per sequence and
+  // KV head, each sequence at least one token
+  if (attn_prefill_gqa(c.dtype, c.n_heads / c.n_kv_heads))
+    L.sched = take((R / attn_gqa_qtile(c.n_heads / c.n_kv_heads) + c.max_batch + 1) *
+                   (size_t)c.n_kv_heads * 16);
   L.err = take(4);
   L.total = off;
   return L;
@@ -307,7 +312,7 @@ constexpr int kFusedNormMaxRows = 16;
 // The decoder layers for `rows` rows.  decode: one row per sequence at position len[b].
 // *hf_ready: the last layer's down projection also wrote the final RMSNorm rows into hf.
 ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipStream_t s,
-                         bool *hf_ready = nullptr) {
+                         bool *hf_ready = nullptr, const AttnSched *as = nullptr) {
   if (hf_ready) *hf_ready = false;
   const ll_config &c = m->cfg;
   const int d = c.d_model, qd = c.n_heads * c.head_dim, F = c.ffn_dim;
@@ -384,7 +389,8 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
       LL_HIP(launch_attn_prefill(dt, c.head_dim, m->at(m->L.q), qd, m->kc(l), m->vc(l),
                                  m->at(m->L.o), qd, m->at<int>(m->L.cu),
                                  m->at<int>(m->L.kstart), m->at<int2>(m->L.qtiles), n_qtiles,
-                                 c.n_heads, c.n_kv_heads, c.max_ctx, s, m->paging()));
+                                 c.n_heads, c.n_kv_heads, c.max_ctx, s, m->paging(),
+                                 m->L.sched ? m->at<int4>(m->L.sched) : nullptr, as));
     }
     m->mark(LL_K_O);
     {
@@ -599,13 +605,15 @@ ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
   }
   TimerScope scope(m->timer, 0);
   m->mark(LL_K_META);
+  const AttnSched as = attn_prefill_sched(pm, c.n_heads / c.n_kv_heads, c.n_kv_heads);
   LL_HIP(launch_prefill_meta(pm, T, qtile, m->at<int>(L.cu), m->at<int>(L.row_seq),
                              m->at<int>(L.row_pos), m->at<int>(L.last_row), m->at<int>(L.lens),
-                             m->at<int>(L.kstart), m->at<int2>(L.qtiles), s));
+                             m->at<int>(L.kstart), m->at<int2>(L.qtiles), s,
+                             L.sched ? m->at<int4>(L.sched) : nullptr, &as, c.n_kv_heads));
   m->mark(LL_K_EMBED);
   LL_HIP(launch_embed(c.dtype, tokens_dev, T, m->at(L.embed), c.vocab, c.d_model,
                       m->at<float>(L.x), m->at<int>(L.err), s));
-  ll_status st = enqueue_layers(m, T, false, n_qtiles, s);
+  ll_status st = enqueue_layers(m, T, false, n_qtiles, s, nullptr, &as);
   if (st != LL_OK) return st;
   st = enqueue_head(m, batch, m->at<int>(L.last_row), next_tokens_dev, logits_dev, nullptr, s);
   if (st != LL_OK) return st;
@@ -907,22 +915,24 @@ static ll_status check_heads(int32_t n_heads, int32_t n_kv_heads, int32_t head_d
   return LL_OK;
 }
 
-ll_status ll_op_attn_prefill(int32_t dtype, int32_t batch, const int32_t *seq_lens_host,
-                             const int32_t *cached_host, int32_t n_heads, int32_t n_kv_heads,
-                             int32_t head_dim, int32_t max_ctx, const void *q,
-                             const void *kcache, const void *vcache, void *o, void *scratch,
-                             size_t scratch_bytes, void *stream) {
-  g_err.clear();
-  ll_status st = check_dtype(dtype);
-  if (st == LL_OK) st = check_heads(n_heads, n_kv_heads, head_dim);
-  if (st != LL_OK) return st;
+}  // extern "C"
+
+namespace {
+// Device metadata of ll_op_attn_prefill in its scratch buffer (offsets, 256-byte aligned).
+struct OpAttnPrefillLayout {
+  size_t cu = 0, seq = 0, pos = 0, last = 0, lens = 0, ks = 0, qt = 0, sched = 0, bytes = 0;
+  int n_qtiles = 0, total = 0;
+  AttnSched as;
+  PrefillMeta pm;
+};
+ll_status op_attn_prefill_layout(int dtype, int batch, const int32_t *seq_lens_host,
+                                 const int32_t *cached_host, int n_heads, int n_kv_heads,
+                                 int max_ctx, OpAttnPrefillLayout *lay) {
   if (batch < 1 || batch > LL_MAX_BATCH || !seq_lens_host)
     return fail(LL_ERR_INVALID_ARGUMENT, "batch in [1, %d] and seq_lens_host required", LL_MAX_BATCH);
-  if (!q || !kcache || !vcache || !o || !scratch) return fail(LL_ERR_INVALID_ARGUMENT, "NULL pointer");
-  PrefillMeta pm;
+  PrefillMeta &pm = lay->pm;
   pm.batch = batch;
   long total = 0;
-  int n_qtiles = 0;
   const int qtile = attn_prefill_qtile(dtype);
   for (int b = 0; b < batch; ++b) {
     const int L = seq_lens_host[b], P0 = cached_host ? cached_host[b] : 0;
@@ -932,24 +942,68 @@ ll_status ll_op_attn_prefill(int32_t dtype, int32_t batch, const int32_t *seq_le
     pm.lens[b] = L;
     pm.start[b] = P0;
     total += L;
-    n_qtiles += (L + qtile - 1) / qtile;
+    lay->n_qtiles += (L + qtile - 1) / qtile;
   }
-  if ((st = check_ws(scratch)) != LL_OK) return st;
+  if (total > INT32_MAX / 4) return fail(LL_ERR_INVALID_ARGUMENT, "%ld tokens", total);
+  lay->total = (int)total;
+  if (attn_prefill_gqa(dtype, n_heads / n_kv_heads))
+    lay->as = attn_prefill_sched(pm, n_heads / n_kv_heads, n_kv_heads);
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o2 = off; off = align_up(off + bytes); return o2; };
-  const size_t o_cu = take((batch + 1) * 4), o_seq = take(total * 4), o_pos = take(total * 4),
-               o_last = take(batch * 4), o_lens = take(batch * 4), o_ks = take(batch * 4),
-               o_qt = take((size_t)n_qtiles * 8);
-  if (off > scratch_bytes) return fail(LL_ERR_WORKSPACE, "scratch needs %zu bytes", off);
+  lay->cu = take((batch + 1) * 4);
+  lay->seq = take(total * 4);
+  lay->pos = take(total * 4);
+  lay->last = take(batch * 4);
+  lay->lens = take(batch * 4);
+  lay->ks = take(batch * 4);
+  lay->qt = take((size_t)lay->n_qtiles * 8);
+  lay->sched = take((size_t)lay->as.n_entries * 16);
+  lay->bytes = off;
+  return LL_OK;
+}
+}  // namespace
+
+extern "C" {
+
+size_t ll_op_attn_prefill_scratch(int32_t dtype, int32_t batch, const int32_t *seq_lens_host,
+                                  const int32_t *cached_host, int32_t n_heads,
+                                  int32_t n_kv_heads, int32_t head_dim, int32_t max_ctx) {
+  if (check_dtype(dtype) != LL_OK || check_heads(n_heads, n_kv_heads, head_dim) != LL_OK)
+    return 0;
+  OpAttnPrefillLayout lay;
+  if (op_attn_prefill_layout(dtype, batch, seq_lens_host, cached_host, n_heads, n_kv_heads,
+                             max_ctx, &lay) != LL_OK)
+    return 0;
+  return lay.bytes;
+}
+
+ll_status ll_op_attn_prefill(int32_t dtype, int32_t batch, const int32_t *seq_lens_host,
+                             const int32_t *cached_host, int32_t n_heads, int32_t n_kv_heads,
+                             int32_t head_dim, int32_t max_ctx, const void *q,
+                             const void *kcache, const void *vcache, void *o, void *scratch,
+                             size_t scratch_bytes, void *stream) {
+  g_err.clear();
+  ll_status st = check_dtype(dtype);
+  if (st == LL_OK) st = check_heads(n_heads, n_kv_heads, head_dim);
+  if (st != LL_OK) return st;
+  OpAttnPrefillLayout lay;
+  if ((st = op_attn_prefill_layout(dtype, batch, seq_lens_host, cached_host, n_heads, n_kv_heads,
+                                   max_ctx, &lay)) != LL_OK)
+    return st;
+  if (!q || !kcache || !vcache || !o || !scratch) return fail(LL_ERR_INVALID_ARGUMENT, "NULL pointer");
+  if ((st = check_ws(scratch)) != LL_OK) return st;
+  if (lay.bytes > scratch_bytes) return fail(LL_ERR_WORKSPACE, "scratch needs %zu bytes", lay.bytes);
   char *sc = reinterpret_cast<char *>(scratch);
   hipStream_t s = (hipStream_t)stream;
-  LL_HIP(launch_prefill_meta(pm, (int)total, qtile, (int *)(sc + o_cu), (int *)(sc + o_seq),
-                             (int *)(sc + o_pos), (int *)(sc + o_last), (int *)(sc + o_lens),
-                             (int *)(sc + o_ks), (int2 *)(sc + o_qt), s));
+  int4 *sched = lay.as.n_entries ? (int4 *)(sc + lay.sched) : nullptr;
+  LL_HIP(launch_prefill_meta(lay.pm, lay.total, attn_prefill_qtile(dtype), (int *)(sc + lay.cu),
+                             (int *)(sc + lay.seq), (int *)(sc + lay.pos), (int *)(sc + lay.last),
+                             (int *)(sc + lay.lens), (int *)(sc + lay.ks), (int2 *)(sc + lay.qt),
+                             s, sched, &lay.as, n_kv_heads));
   const int qd = n_heads * head_dim;
-  LL_HIP(launch_attn_prefill(dtype, head_dim, q, qd, kcache, vcache, o, qd, (int *)(sc + o_cu),
-                             (int *)(sc + o_ks), (int2 *)(sc + o_qt), n_qtiles, n_heads,
-                             n_kv_heads, max_ctx, s));
+  LL_HIP(launch_attn_prefill(dtype, head_dim, q, qd, kcache, vcache, o, qd, (int *)(sc + lay.cu),
+                             (int *)(sc + lay.ks), (int2 *)(sc + lay.qt), lay.n_qtiles, n_heads,
+                             n_kv_heads, max_ctx, s, KvPaging{}, sched, &lay.as));
   return LL_OK;
 }
 

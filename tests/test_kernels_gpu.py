@@ -155,6 +155,14 @@ ATTN_CASES = [
     ("bf16", 128, 8, 2, [300, 129, 1, 257]),
     ("bf16", 128, 4, 4, [1030]),
     ("bf16", 64, 4, 1, [513, 128, 127]),
+    # grouped-query kernel (one block per query tile and KV head) at every group size: groups
+    # of 8 at head_dim 64 (32-query tiles), of 4 at 128 (64-query tiles), of 2 (128-query
+    # tiles); many ragged sequences so that the work list is cut over the XCDs mid-sequence
+    ("bf16", 64, 32, 4, [1024, 77, 1, 33]),
+    ("bf16", 64, 16, 2, [300, 31, 32, 257]),
+    ("bf16", 128, 32, 8, [1500, 1, 700, 64]),
+    ("bf16", 128, 8, 4, [129, 255, 2]),
+    ("bf16", 128, 16, 4, [int(x) for x in np.random.default_rng(7).integers(1, 600, 20)]),
     ("f32", 64, 4, 4, [33, 1, 128]),
     ("f32", 128, 4, 2, [70]),
 ]
@@ -191,6 +199,8 @@ CHUNK_CASES = [
     ("bf16", 64, 8, 2, [1, 63, 64, 130], [100, 1, 64, 0]),
     ("bf16", 128, 32, 8, [200, 17], [1000, 63]),
     ("bf16", 64, 4, 4, [128], [512]),
+    ("bf16", 64, 32, 4, [40, 1, 300], [1000, 5, 64]),
+    ("bf16", 128, 32, 8, [65, 128], [63, 2000]),
     ("f32", 64, 4, 4, [33, 1, 70], [31, 200, 64]),
     ("f32", 128, 4, 2, [65], [3]),
 ]
