@@ -811,9 +811,9 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const T *__restrict__ A, in
 // of 32 columns, every block re-reads all of A (32 rows x K) through L1, as many bytes as its
 // weights: the activation traffic, not HBM, then limits the stream.  Here a block of 8 waves
 // owns 128 columns (one 16-column weight tile per wave) and a slice of K; its 32 x slice A
-// tile is DMA'd into LDS once and feeds all 8 waves.  Slices are sized so the grid has
-// ~512 blocks; each block writes fp32 partial sums part[split][m][n], and a second kernel
-// sums the splits in order (deterministic) and applies the epilogue.
+// tile is DMA'd into LDS once and feeds all 8 waves.  Slices are as long as still gives
+// every CU a block (splitk_plan); each block writes fp32 partial sums part[split][m][n], and a
+// second kernel sums the splits in order (deterministic) and applies the epilogue.
 // ------------------------------------------------------------------------------------------
 template <typename T, int KTS>
 __global__ __launch_bounds__(512) void k_gemm_splitk(const T *__restrict__ A, int lda,
@@ -831,28 +831,8 @@ __global__ __launch_bounds__(512) void k_gemm_splitk(const T *__restrict__ A, in
   const int kt0 = blockIdx.y * kts, nk = min(kts, kb_n - kt0);
   const F fz = frag_zero<F>();
   const uint8_t *wp = Wt + (((size_t)ct * kb_n + kt0) * 64 + lane) * 16;
-  // A slice first: tile (t, rb) holds rows m_base + 16 rb + l % 16 (clamped to M - 1; those
-  // results are never stored), contraction indices (kt0 + t) TK + EPL (l / 16) + e.
-  // A fixed number of 16-byte loads per lane (slots past 2 nk receive a copy of a valid
-  // tile and are never read), so the code stays straight-line.  The A slice (mostly L2
-  // hits) is stored to LDS before the weight stream starts: a wait for it issued after the
-  // weight loads would also wait for them, since loads complete in order.
-  static_assert((2 * KTS) % NW == 0, "A tiles split evenly over the waves");
-  constexpr int NA = 2 * KTS / NW;
-  {
-    uint4 areg[NA];
-#pragma unroll
-    for (int j = 0; j < NA; ++j) {
-      const int i = wave + NW * j, t = min(i >> 1, nk - 1), rb = i & 1;
-      const int row = min(m_base + 16 * rb + (lane & 15), M - 1);
-      areg[j] = *reinterpret_cast<const uint4 *>(A + (size_t)row * lda + (size_t)(kt0 + t) * TK + (lane >> 4) * EPL);
-    }
-#pragma unroll
-    for (int j = 0; j < NA; ++j) sAk[(wave + NW * j) * 64 + lane] = areg[j];
-  }
-  __builtin_amdgcn_sched_barrier(0);
-  // Then a ring of U weight tiles in flight: each tile's slot is refilled with the tile U
-  // ahead as soon as it has been consumed, so the stream never drains between batches.
+  // The weight stream starts first: a ring of U tiles in flight, each slot refilled with the
+  // tile U ahead as soon as it has been consumed, so the stream never drains between batches.
   // (The scheduling barriers keep the loads in ring order, so the wait before tile q is for
   // the q-th oldest load only.)
   F bw[U];
@@ -861,9 +841,22 @@ __global__ __launch_bounds__(512) void k_gemm_splitk(const T *__restrict__ A, in
     bw[q] = load_frag_stream<F>(wp + (size_t)min(q, nk - 1) * 1024);
     __builtin_amdgcn_sched_barrier(0);
   }
-  // LDS stores complete, then a bare barrier (a full __syncthreads would also wait for the
-  // weight loads in flight).
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  // Then the A slice, DMA'd into LDS in operand order while the weights are in flight: tile
+  // (t, rb) holds rows m_base + 16 rb + l % 16 (clamped to M - 1; those results are never
+  // stored), contraction indices (kt0 + t) TK + EPL (l / 16) + e.  A fixed number of tiles
+  // per wave (slots past 2 nk receive a copy of a valid tile and are never read), so the code
+  // stays straight-line.  Waiting for the slice also waits for the first U weight tiles,
+  // which the first steps need anyway; the load latencies overlap instead of adding up.
+  static_assert((2 * KTS) % NW == 0, "A tiles split evenly over the waves");
+  constexpr int NA = 2 * KTS / NW;
+#pragma unroll
+  for (int j = 0; j < NA; ++j) {
+    const int i = wave + NW * j, t = min(i >> 1, nk - 1), rb = i & 1;
+    const int row = min(m_base + 16 * rb + (lane & 15), M - 1);
+    load_tile_to_lds(A + (size_t)row * lda + (size_t)(kt0 + t) * TK + (lane >> 4) * EPL,
+                     &sAk[(size_t)i * 64]);
+  }
+  asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
   __builtin_amdgcn_sched_barrier(0);
 
   // The slice is a compile-time number of tiles, fully unrolled: straight-line code in which
@@ -1066,6 +1059,11 @@ hipError_t run_splitk(const void *a, int lda, const void *wt, int m, int n, int 
       case 8: LL_SPLITK(8); break;
       case 16: LL_SPLITK(16); break;
       case 24: LL_SPLITK(24); break;
+      case 32: LL_SPLITK(32); break;
+      case 40: LL_SPLITK(40); break;
+      case 48: LL_SPLITK(48); break;
+      case 56: LL_SPLITK(56); break;
+      case 64: LL_SPLITK(64); break;
       default: return hipErrorInvalidValue;
     }
 #undef LL_SPLITK
@@ -1287,9 +1285,19 @@ SplitKPlan splitk_plan(size_t elem, int m, int n, int k) {
   const int tk = elem == 4 ? 16 : 32;
   if (m <= 16 || n % 128 != 0 || k % tk != 0) return p;
   const int kb_n = k / tk, groups = n / 128;
-  int nsplit = std::max(1, std::min(kb_n, (512 + groups - 1) / groups));
-  int kts = (kb_n + nsplit - 1) / nsplit;
-  kts = std::min((kts + 7) / 8 * 8, kSplitKMaxTiles);  // compiled slice lengths: 8, 16, 24
+  // As few K slices as still give every CU a block: each slice's fp32 partials are written and
+  // read again by the reduction, so fewer, longer slices (up to 64 k-tiles, a 128 KiB A slice
+  // in LDS) move fewer bytes.  Take the longest compiled slice (8, 16, .., 64 k-tiles) that
+  // still gives kSplitKBlocks blocks, preferring one that divides K evenly (an uneven last
+  // slice leaves its blocks idle early).
+  int kts = 8, best_even = 0;
+  for (int t = 8; t <= kSplitKMaxTiles; t += 8) {
+    const int ns = (kb_n + t - 1) / t;
+    if ((long)ns * groups < kSplitKBlocks) break;
+    kts = t;
+    if (kb_n % t == 0) best_even = t;
+  }
+  if (best_even) kts = best_even;
   p.kts = kts;
   p.nsplit = (kb_n + kts - 1) / kts;
   p.ws_bytes = (size_t)p.nsplit * m * n * sizeof(float);

@@ -187,7 +187,8 @@ hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *n
                               hipStream_t s, float *ws = nullptr, size_t ws_bytes = 0,
                               const PostNorm *post = nullptr, bool *post_done = nullptr,
                               int ksplit = 1);
-constexpr int kSplitKMaxTiles = 24;  // k-tiles per split-K block (A slice of 48 KiB in LDS)
+constexpr int kSplitKMaxTiles = 64;  // k-tiles per split-K block (A slice of up to 128 KiB in LDS)
+constexpr int kSplitKBlocks = 256;   // blocks the decode split-K plan aims for
 struct SplitKPlan {
   int nsplit = 0;  // 0: split-K not used for this shape
   int kts = 0;     // k-tiles per split

@@ -84,7 +84,10 @@ def test_gemm(dtype, path, m, n, k):
 
 
 SPLITK_SHAPES = [(17, 128, 64), (32, 512, 256), (32, 4096, 1024), (33, 384, 4096),
-                 (64, 256, 14336), (20, 6144, 512)]
+                 (64, 256, 14336), (20, 6144, 512),
+                 # every compiled slice length: 64 (8B gate/up), 56 (8B down), 32, 40, 48
+                 (32, 16384, 4096), (32, 4096, 14336), (32, 4096, 8192), (32, 4096, 10240),
+                 (32, 4096, 12288)]
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
