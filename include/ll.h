@@ -139,6 +139,15 @@ ll_status ll_kv_reset(ll_model *m);
  * contiguous cache).  Host only. */
 ll_status ll_kv_pages(const ll_model *m, int32_t *used, int32_t *total);
 
+/* The regions of the model's workspace, in address order: writes min(cap, count) entries of
+ * byte offset from the workspace start, size in bytes and name (a string owned by the model,
+ * valid until ll_model_free: "embed", "layers.<l>.wqkv", "kcache", "x", ...); *n = count.
+ * Every region is followed by a gap of at least 256 bytes that no kernel writes, so a caller
+ * (a test harness, a debugging allocator) can fill the gaps with a pattern and check after
+ * any call that no kernel wrote past a region's end.  Host only. */
+ll_status ll_workspace_regions(const ll_model *m, int32_t cap, uint64_t *offsets,
+                               uint64_t *bytes, const char **names, int32_t *n);
+
 /* Current host-mirrored sequence lengths: writes min(cap, batch) values, *n = batch. */
 ll_status ll_seq_lengths(const ll_model *m, int32_t *out, int32_t cap, int32_t *n);
 

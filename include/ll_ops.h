@@ -40,6 +40,14 @@ ll_status ll_op_repack(int32_t dtype, int32_t n, int32_t k, const void *w, void 
 ll_status ll_op_gemm(int32_t path, int32_t dtype, int32_t m, int32_t n, int32_t k,
                      const void *a, const void *wt, float *c, int32_t accumulate, void *stream);
 
+/* The prefill GEMM with the gate/up projection's SwiGLU epilogue: act[m, 16 u + c] =
+ * silu(g) * v, where g and v are columns 32 u + c and 32 u + 16 + c (c < 16) of A W^T, i.e. W
+ * holds the gate and up rows interleaved in blocks of 16 (gate rows 16 u .. 16 u + 15, then
+ * up rows 16 u .. 16 u + 15, for u = 0 .. n / 32 - 1) before ll_op_repack.  A T row-major
+ * (lda = K), act T row-major [M, N/2].  N a multiple of 128, K a multiple of 64. */
+ll_status ll_op_gemm_swiglu(int32_t dtype, int32_t m, int32_t n, int32_t k, const void *a,
+                            const void *wt, void *act, void *stream);
+
 /* Decode GEMM for batches above 16 rows, split over K: C = A W^T (accumulate = 0) or
  * C += A W^T.  Each block of 128 output columns covers a slice of K and stages its slice of
  * A in LDS once for all its columns; fp32 partial sums go to `scratch`, and a second kernel

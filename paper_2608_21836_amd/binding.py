@@ -8,7 +8,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from ctypes import POINTER, c_char_p, c_double, c_float, c_int32, c_size_t, c_void_p
+from ctypes import POINTER, c_char_p, c_double, c_float, c_int32, c_size_t, c_uint64, c_void_p
 from typing import Dict, List, Optional, Sequence, Tuple
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libll.so")
@@ -121,6 +121,8 @@ SIGNATURES = [
     ("ll_decode_step", c_int32, [c_void_p, c_void_p, c_void_p, c_void_p]),
     ("ll_kv_reset", c_int32, [c_void_p]),
     ("ll_seq_lengths", c_int32, [c_void_p, POINTER(c_int32), c_int32, POINTER(c_int32)]),
+    ("ll_workspace_regions", c_int32, [c_void_p, c_int32, POINTER(c_uint64), POINTER(c_uint64),
+                                       POINTER(c_char_p), POINTER(c_int32)]),
     ("ll_kv_pages", c_int32, [c_void_p, POINTER(c_int32), POINTER(c_int32)]),
     ("ll_op_mfma_loop", c_int32, [c_int32, c_int32, c_void_p, c_void_p]),
     ("ll_set_decode_graph", c_int32, [c_void_p, c_int32]),
@@ -137,6 +139,8 @@ SIGNATURES = [
     ("ll_op_repack", c_int32, [c_int32, c_int32, c_int32, c_void_p, c_void_p, c_void_p]),
     ("ll_op_gemm", c_int32, [c_int32, c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
                              c_void_p, c_int32, c_void_p]),
+    ("ll_op_gemm_swiglu", c_int32, [c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
+                                    c_void_p, c_void_p]),
     ("ll_op_gemm_splitk", c_int32, [c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
                                     c_void_p, c_int32, c_void_p, c_size_t, c_void_p]),
     ("ll_op_gemm_splitk_scratch", c_size_t, [c_int32, c_int32, c_int32, c_int32]),
@@ -268,14 +272,19 @@ class Model:
 
     def __init__(self, cfg, weights: Dict[str, "object"], max_batch: int,
                  max_prefill_tokens: int, max_ctx: int, stream=None, kv_page: int = 0,
-                 kv_pages: int = 0):
+                 kv_pages: int = 0, guard_bytes: int = 0):
+        """guard_bytes (a multiple of 256): extra bytes allocated before and after the
+        workspace (self.guarded), for checks that nothing is written outside it."""
         import torch
         self.lib = load_library()
         self.mcfg = cfg
         self.cfg = make_config(cfg, max_batch, max_prefill_tokens, max_ctx, kv_page, kv_pages)
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         nbytes = workspace_size(self.cfg)
-        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        if guard_bytes % 256:
+            raise ValueError("guard_bytes must be a multiple of 256")
+        self.guarded = torch.empty(nbytes + 2 * guard_bytes, dtype=torch.uint8, device="cuda")
+        self.workspace = self.guarded[guard_bytes:guard_bytes + nbytes]
         nl = cfg.n_layers
 
         def arr(key):
@@ -346,6 +355,17 @@ class Model:
 
     def options(self) -> Dict[str, int]:
         return {k: self.get_option(k) for k in DECODER_OPTIONS}
+
+    def regions(self) -> List[Tuple[str, int, int]]:
+        """[(name, byte offset in the workspace, bytes)] of the workspace layout."""
+        n = c_int32(0)
+        _check(self.lib.ll_workspace_regions(self.handle, 0, None, None, None, ctypes.byref(n)),
+               "ll_workspace_regions")
+        cap = n.value
+        off, nb, names = (c_uint64 * cap)(), (c_uint64 * cap)(), (c_char_p * cap)()
+        _check(self.lib.ll_workspace_regions(self.handle, cap, off, nb, names, ctypes.byref(n)),
+               "ll_workspace_regions")
+        return [(names[i].decode(), int(off[i]), int(nb[i])) for i in range(cap)]
 
     def seq_lengths(self) -> List[int]:
         out = (c_int32 * LL_MAX_BATCH)()
@@ -521,6 +541,17 @@ class MambaModel:
     def options(self) -> Dict[str, int]:
         return {k: self.get_option(k) for k in self.option_names}
 
+    def regions(self) -> List[Tuple[str, int, int]]:
+        """[(name, byte offset in the workspace, bytes)] of the workspace layout."""
+        n = c_int32(0)
+        _check(self.lib.ll_workspace_regions(self.handle, 0, None, None, None, ctypes.byref(n)),
+               "ll_workspace_regions")
+        cap = n.value
+        off, nb, names = (c_uint64 * cap)(), (c_uint64 * cap)(), (c_char_p * cap)()
+        _check(self.lib.ll_workspace_regions(self.handle, cap, off, nb, names, ctypes.byref(n)),
+               "ll_workspace_regions")
+        return [(names[i].decode(), int(off[i]), int(nb[i])) for i in range(cap)]
+
     def seq_lengths(self) -> List[int]:
         out = (c_int32 * LL_MAX_BATCH)()
         n = c_int32(0)
@@ -695,6 +726,19 @@ def op_attn_decode(q, kcache, vcache, ctx_lens, n_heads, n_kv_heads, head_dim, m
     return o
 
 
+def op_gemm_swiglu(a, wt, n: int, act=None, stream=None):
+    """ll_op_gemm_swiglu: act [M, n/2] (a's dtype) from the prefill GEMM with the SwiGLU
+    epilogue; wt repacked from gate/up rows interleaved in blocks of 16."""
+    import torch
+    m, k = a.shape
+    if act is None:
+        act = torch.empty(m, n // 2, dtype=a.dtype, device="cuda")
+    _check(load_library().ll_op_gemm_swiglu(_dt(a), m, n, k, a.data_ptr(), wt.data_ptr(),
+                                            act.data_ptr(), _stream_handle(stream)),
+           "ll_op_gemm_swiglu")
+    return act
+
+
 def op_lmhead_argmax(h, wt, vocab: int, want_logits: bool = True, stream=None):
     import torch
     rows, k = h.shape
@@ -706,3 +750,4 @@ def op_lmhead_argmax(h, wt, vocab: int, want_logits: bool = True, stream=None):
                                               _ptr(logits), nxt.data_ptr(), scratch.data_ptr(),
                                               nbytes, _stream_handle(stream)), "ll_op_lmhead_argmax")
     return nxt, logits
+

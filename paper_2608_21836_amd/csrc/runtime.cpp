@@ -44,6 +44,11 @@ struct Layout {
   int kv_max_pages = 0, kv_pages = 0;
   AttnDecodePlan attn;
   int n_parts = 0, max_rows = 0, n_qkv = 0;
+  struct Region {
+    std::string name;
+    size_t off, bytes;
+  };
+  std::vector<Region> regions;  // every region of the workspace, in address order
 };
 
 ll_status validate_config(const ll_config *c) {
@@ -96,43 +101,46 @@ Layout make_layout(const ll_config &c) {
   L.attn = attn_decode_plan(c.head_dim, (int)eb, c.max_batch, c.n_kv_heads, c.max_ctx);
   L.n_parts = c.vocab / 32;
   size_t off = 0;
-  auto take = [&](size_t bytes) {
+  // Every region is followed by a guard gap of kGuardBytes that no kernel writes, so that a
+  // write past the end of a region is detectable (ll_workspace_regions lists the regions).
+  auto take = [&](std::string name, size_t bytes) {
     const size_t o = off;
-    off = align_up(off + bytes);
+    L.regions.push_back({std::move(name), o, bytes});
+    off = align_up(off + bytes) + kGuardBytes;
     return o;
   };
-  L.embed = take((size_t)c.vocab * d * eb);
+  L.embed = take("embed", (size_t)c.vocab * d * eb);
   for (int l = 0; l < c.n_layers; ++l) {
-    L.wqkv.push_back(take((size_t)L.n_qkv * d * eb));
-    L.wo.push_back(take(d * qd * eb));
-    L.wgu.push_back(take(2 * (size_t)c.ffn_dim * d * eb));
-    L.wd.push_back(take(d * c.ffn_dim * eb));
-    L.attn_norm.push_back(take(d * eb));
-    L.mlp_norm.push_back(take(d * eb));
+    L.wqkv.push_back(take("layers." + std::to_string(l) + ".wqkv", (size_t)L.n_qkv * d * eb));
+    L.wo.push_back(take("layers." + std::to_string(l) + ".wo", d * qd * eb));
+    L.wgu.push_back(take("layers." + std::to_string(l) + ".wgu", 2 * (size_t)c.ffn_dim * d * eb));
+    L.wd.push_back(take("layers." + std::to_string(l) + ".wd", d * c.ffn_dim * eb));
+    L.attn_norm.push_back(take("layers." + std::to_string(l) + ".attn_norm", d * eb));
+    L.mlp_norm.push_back(take("layers." + std::to_string(l) + ".mlp_norm", d * eb));
   }
-  L.final_norm = take(d * eb);
-  L.lm_head = take((size_t)c.vocab * d * eb);
+  L.final_norm = take("final_norm", d * eb);
+  L.lm_head = take("lm_head", (size_t)c.vocab * d * eb);
   if (c.kv_page > 0) {
     L.kv_max_pages = (c.max_ctx + c.kv_page - 1) / c.kv_page;
     L.kv_pages = c.kv_pages > 0 ? c.kv_pages : c.max_batch * L.kv_max_pages;
     L.kv_layer_elems = (size_t)L.kv_pages * c.n_kv_heads * c.kv_page * c.head_dim;
-    L.kv_table = take((size_t)c.max_batch * L.kv_max_pages * 4);
+    L.kv_table = take("kv_table", (size_t)c.max_batch * L.kv_max_pages * 4);
   } else {
     L.kv_layer_elems = (size_t)c.max_batch * c.n_kv_heads * c.max_ctx * c.head_dim;
   }
-  L.kcache = take(L.kv_layer_elems * c.n_layers * eb);
-  L.vcache = take(L.kv_layer_elems * c.n_layers * eb);
-  L.rcos = take((size_t)c.max_ctx * (c.head_dim / 2) * 4);
-  L.rsin = take((size_t)c.max_ctx * (c.head_dim / 2) * 4);
+  L.kcache = take("kcache", L.kv_layer_elems * c.n_layers * eb);
+  L.vcache = take("vcache", L.kv_layer_elems * c.n_layers * eb);
+  L.rcos = take("rcos", (size_t)c.max_ctx * (c.head_dim / 2) * 4);
+  L.rsin = take("rsin", (size_t)c.max_ctx * (c.head_dim / 2) * 4);
   const size_t R = L.max_rows;
-  L.x = take(R * d * 4);
-  L.h = take(R * d * eb);
-  L.q = take(R * qd * eb);
-  L.o = take(R * qd * eb);
-  L.act = take(R * c.ffn_dim * eb);
-  L.hf = take((size_t)c.max_batch * d * eb);
-  L.part_o = take((size_t)c.max_batch * c.n_heads * L.attn.nsplit * c.head_dim * 4);
-  L.part_ml = take((size_t)c.max_batch * c.n_heads * L.attn.nsplit * 2 * 4);
+  L.x = take("x", R * d * 4);
+  L.h = take("h", R * d * eb);
+  L.q = take("q", R * qd * eb);
+  L.o = take("o", R * qd * eb);
+  L.act = take("act", R * c.ffn_dim * eb);
+  L.hf = take("hf", (size_t)c.max_batch * d * eb);
+  L.part_o = take("part_o", (size_t)c.max_batch * c.n_heads * L.attn.nsplit * c.head_dim * 4);
+  L.part_ml = take("part_ml", (size_t)c.max_batch * c.n_heads * L.attn.nsplit * 2 * 4);
   {
     const int F = c.ffn_dim;
     const int shapes[4][2] = {{L.n_qkv, (int)d}, {(int)d, (int)qd}, {2 * F, (int)d}, {(int)d, F}};
@@ -149,23 +157,23 @@ Layout make_layout(const ll_config &c) {
       L.splitk_bytes =
           std::max(L.splitk_bytes, prefill_splitk_plan(eb, mmax, nk[0], nk[1]).ws_bytes);
     }
-    L.splitk = take(L.splitk_bytes);
+    L.splitk = take("splitk", L.splitk_bytes);
   }
-  L.pval = take((size_t)c.max_batch * L.n_parts * 4);
-  L.pidx = take((size_t)c.max_batch * L.n_parts * 4);
-  L.cu = take((c.max_batch + 1) * 4);
-  L.row_seq = take(R * 4);
-  L.row_pos = take(R * 4);
-  L.last_row = take(c.max_batch * 4);
-  L.lens = take(c.max_batch * 4);
-  L.kstart = take(c.max_batch * 4);
-  L.qtiles = take((R / kAttnQTile + c.max_batch + 1) * 8);
+  L.pval = take("pval", (size_t)c.max_batch * L.n_parts * 4);
+  L.pidx = take("pidx", (size_t)c.max_batch * L.n_parts * 4);
+  L.cu = take("cu", (c.max_batch + 1) * 4);
+  L.row_seq = take("row_seq", R * 4);
+  L.row_pos = take("row_pos", R * 4);
+  L.last_row = take("last_row", c.max_batch * 4);
+  L.lens = take("lens", c.max_batch * 4);
+  L.kstart = take("kstart", c.max_batch * 4);
+  L.qtiles = take("qtiles", (R / kAttnQTile + c.max_batch + 1) * 8);
   // work list of the grouped-query prefill attention: ceil(L_b / qtile) tiles per sequence and
   // KV head, each sequence at least one token
   if (attn_prefill_gqa(c.dtype, c.n_heads / c.n_kv_heads))
-    L.sched = take((R / attn_gqa_qtile(c.n_heads / c.n_kv_heads) + c.max_batch + 1) *
+    L.sched = take("sched", (R / attn_gqa_qtile(c.n_heads / c.n_kv_heads) + c.max_batch + 1) *
                    (size_t)c.n_kv_heads * 16);
-  L.err = take(4);
+  L.err = take("err", 4);
   L.total = off;
   return L;
 }
@@ -702,6 +710,22 @@ ll_status ll_kv_pages(const ll_model *m, int32_t *used, int32_t *total) {
   return LL_OK;
 }
 
+ll_status ll_workspace_regions(const ll_model *m, int32_t cap, uint64_t *offsets,
+                               uint64_t *bytes, const char **names, int32_t *n) {
+  g_err.clear();
+  if (!m || !n) return fail(LL_ERR_INVALID_ARGUMENT, "model and n must be set");
+  if (cap < 0 || (cap > 0 && (!offsets || !bytes || !names)))
+    return fail(LL_ERR_INVALID_ARGUMENT, "cap %d needs offsets, bytes and names", cap);
+  const auto &rg = m->L.regions;
+  for (int32_t i = 0; i < cap && i < (int32_t)rg.size(); ++i) {
+    offsets[i] = rg[i].off;
+    bytes[i] = rg[i].bytes;
+    names[i] = rg[i].name.c_str();
+  }
+  *n = (int32_t)rg.size();
+  return LL_OK;
+}
+
 ll_status ll_seq_lengths(const ll_model *m, int32_t *out, int32_t cap, int32_t *n) {
   g_err.clear();
   if (!m || !n || (cap > 0 && !out)) return fail(LL_ERR_INVALID_ARGUMENT, "NULL argument");
@@ -852,6 +876,22 @@ ll_status ll_op_gemm(int32_t path, int32_t dtype, int32_t m, int32_t n, int32_t 
   ep.ld_out = n;
   LL_HIP(path == 0 ? launch_gemm_tiled(dtype, a, k, wt, m, n, k, ep, (hipStream_t)stream)
                    : launch_gemm_skinny(dtype, a, k, nullptr, wt, m, n, k, ep, (hipStream_t)stream));
+  return LL_OK;
+}
+
+ll_status ll_op_gemm_swiglu(int32_t dtype, int32_t m, int32_t n, int32_t k, const void *a,
+                            const void *wt, void *act, void *stream) {
+  g_err.clear();
+  ll_status st = check_dtype(dtype);
+  if (st != LL_OK) return st;
+  if (m < 0 || n < 1 || k < 1) return fail(LL_ERR_INVALID_ARGUMENT, "bad sizes");
+  if (k % 64 || n % 128) return fail(LL_ERR_UNSUPPORTED, "k %% 64 and n %% 128 required");
+  if (m && (!a || !wt || !act)) return fail(LL_ERR_INVALID_ARGUMENT, "NULL pointer");
+  EpiParams ep;
+  ep.kind = kEpiSwiglu;
+  ep.act = act;
+  ep.ld_act = n / 2;
+  LL_HIP(launch_gemm_tiled(dtype, a, k, wt, m, n, k, ep, (hipStream_t)stream));
   return LL_OK;
 }
 

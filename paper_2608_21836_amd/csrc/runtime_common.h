@@ -34,6 +34,9 @@ inline ll_status fail(ll_status st, const char *fmt, ...) {
   } while (0)
 
 constexpr size_t kAlign = 256;
+// Gap after every workspace region of the decoder's layout that no kernel writes (a write past
+// a region's end lands there, where a guard check sees it).
+constexpr size_t kGuardBytes = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 inline ll_status check_ws(const void *p) {

@@ -2,7 +2,8 @@
 
 The paper qualifies a kernel in isolation before accepting it inside the model (Sec. 2.2);
 this module times each hot-path kernel alone, on the shapes the five workloads run:
-  gemm        prefill GEMM (ll_op_gemm path 0), M = the workload's prompt tokens
+  gemm        prefill GEMM (ll_op_gemm path 0), M = the workload's prompt tokens; the
+              gate/up shape also with its SwiGLU epilogue (ll_op_gemm_swiglu)
   gemv        decode GEMM, whole-K (ll_op_gemm path 1) and split-K (ll_op_gemm_splitk),
               M = the workload's batch; weights rotate over >= 1 GiB so they stream from HBM
   attn        prefill attention (ll_op_attn_prefill) and decode attention (ll_op_attn_decode)
@@ -60,7 +61,7 @@ def linear_shapes(cfg):
 
 def bench_gemm(cfg, lens, iters):
     import torch
-    from paper_2608_21836_amd.binding import op_gemm, op_repack
+    from paper_2608_21836_amd.binding import op_gemm, op_gemm_swiglu, op_repack
     T = int(sum(lens))
     a = (torch.randn(T, max(k for _, _, k in linear_shapes(cfg)), device="cuda") * 0.5).to(torch.bfloat16)
     for name, n, k in linear_shapes(cfg):
@@ -69,6 +70,12 @@ def bench_gemm(cfg, lens, iters):
         c = torch.empty(T, n, device="cuda")
         us = _timeit(lambda i: op_gemm(0, ak, wt, n, c=c), iters)
         _line("prefill_gemm", cfg.name, f"{name} M={T} N={n} K={k}", us, 2.0 * T * n * k, "flop")
+        if name == "gate_up":   # the workload's own epilogue: SwiGLU, act [M, F] in bf16
+            act = torch.empty(T, n // 2, dtype=torch.bfloat16, device="cuda")
+            us = _timeit(lambda i: op_gemm_swiglu(ak, wt, n, act=act), iters)
+            _line("prefill_gemm_swiglu", cfg.name, f"{name} M={T} N={n} K={k}", us,
+                  2.0 * T * n * k, "flop")
+            del act
         del ak, wt, c
         torch.cuda.empty_cache()
 

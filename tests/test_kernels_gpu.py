@@ -83,6 +83,37 @@ def test_gemm(dtype, path, m, n, k):
     assert np.all(np.abs(_np(cacc) - (ref + c0)) <= bound + 2 * U * np.abs(ref + c0))
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("m,n,k", [(300, 1024, 512), (4100, 2048, 256), (64, 256, 1024)])
+def test_gemm_swiglu(dtype, m, n, k):
+    """The prefill GEMM with the SwiGLU epilogue against silu(a W_g^T) * (a W_u^T) in fp64,
+    under the dot-product bound plus the rounding of the output and of silu's inputs."""
+    from paper_2608_21836_amd.binding import op_gemm_swiglu, op_repack
+    import torch
+    log(f"gemm swiglu {dtype} m={m} n={n} k={k}")
+    rng = np.random.default_rng(m + n + k)
+    f = n // 2
+    a = rounded(rng.standard_normal((m, k)), dtype)
+    wg = rounded(rng.standard_normal((f, k)) * 0.05, dtype)
+    wu = rounded(rng.standard_normal((f, k)) * 0.05, dtype)
+    # rows interleaved in blocks of 16: gate 16 u .., then up 16 u .., per 32-row unit
+    w = np.empty((n, k), dtype=np.float32)
+    for u in range(f // 16):
+        w[32 * u:32 * u + 16] = wg[16 * u:16 * u + 16]
+        w[32 * u + 16:32 * u + 32] = wu[16 * u:16 * u + 16]
+    act = op_gemm_swiglu(device_tensor(a, dtype), op_repack(device_tensor(w, dtype)), n)
+    torch.cuda.synchronize()
+    a64 = a.astype(np.float64)
+    g, up = a64 @ wg.astype(np.float64).T, a64 @ wu.astype(np.float64).T
+    ref = g / (1.0 + np.exp(-g)) * up
+    bg = 4 * k * U * (np.abs(a64) @ np.abs(wg.astype(np.float64)).T)
+    bu = 4 * k * U * (np.abs(a64) @ np.abs(wu.astype(np.float64)).T)
+    # d(silu)/dg <= 1.1; the output's own rounding (bf16: 8-bit significand, 2^-8 relative)
+    out_u = 2.0 ** -8 if dtype == "bf16" else 2.0 ** -23
+    bound = 1.1 * bg * np.abs(up) + np.abs(g) * bu + (out_u + 4e-6) * np.abs(ref) + 1e-30
+    assert np.all(np.abs(_np(act).astype(np.float64) - ref) <= bound)
+
+
 SPLITK_SHAPES = [(17, 128, 64), (32, 512, 256), (32, 4096, 1024), (33, 384, 4096),
                  (64, 256, 14336), (20, 6144, 512),
                  # every compiled slice length: 64 (8B gate/up), 56 (8B down), 32, 40, 48
