@@ -38,7 +38,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "prefill tok/s + decode tok/s on 1 MI355X; % of MFMA/HBM roofline"
 HBM_PEAK_GBS = 8000.0
-MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f16": 2500.0, "f32": 157.3}   # dense MFMA peaks
 PROFILES = os.path.join(ROOT, "profiles")
 COPY_CAL_BYTES = 256 << 20   # plain copy kernel used to scale the PMC byte counters
 
@@ -430,6 +430,10 @@ def main() -> int:
     ap.add_argument("--option", action="append", default=[], metavar="NAME=VALUE",
                     help="set an implementation option after loading (repeatable; applied "
                          "after the accepted ones)")
+    ap.add_argument("--bf16-operands", action="store_true",
+                    help="decoder workloads with bf16 weights: keep activations, KV cache and "
+                         "MFMA operands in bf16 instead of converting the weights exactly to fp16 "
+                         "at load (the default)")
     ap.add_argument("--kv-page", type=int, default=0,
                     help="decoder workloads: paged KV cache with pages of this many positions "
                          "(a multiple of 256; 0 = one contiguous slab per sequence)")
@@ -460,6 +464,7 @@ def main() -> int:
            S2.get_mamba2_config(args.config) if mamba2 else
            SM.get_mamba_config(args.config) if mamba else get_config(args.config))
     host_w = None
+    op_dtype = cfg.dtype   # the operand type the kernels compute in
     lens, packed = gen.prompt_tokens(cfg)
     B, T, N = len(lens), int(sum(lens)), cfg.n_decode
     print(f"[bench] {cfg.name}: uploading weights", file=sys.stderr, flush=True)
@@ -506,10 +511,15 @@ def main() -> int:
         if args.kv_page and not kv_pages:
             kv_pages = sum((int(x) + N + args.kv_page - 1) // args.kv_page for x in lens)
         model = Model(cfg, dev_w, max_batch=B, max_prefill_tokens=T, max_ctx=max(lens) + N,
-                      kv_page=args.kv_page, kv_pages=kv_pages)
+                      kv_page=args.kv_page, kv_pages=kv_pages,
+                      f16_compute=False if args.bf16_operands else None)
+        if cfg.dtype == "bf16" and not args.bf16_operands:
+            op_dtype = "f16"
         reset = model.kv_reset
         work_all = algorithmic_work(cfg, lens, N)
-        desc = {"workload": cfg.name, "layers": cfg.n_layers, "d_model": cfg.d_model,
+        desc = {"workload": cfg.name, "weights": cfg.dtype + (
+                    " (converted exactly to fp16 at load)" if op_dtype == "f16" else ""),
+                "layers": cfg.n_layers, "d_model": cfg.d_model,
                 "heads": f"{cfg.n_heads}/{cfg.n_kv_heads}x{cfg.head_dim}", "ffn": cfg.ffn_dim,
                 "vocab": cfg.vocab}
         if args.kv_page:
@@ -572,7 +582,7 @@ def main() -> int:
         "metric": METRIC, "value": round((T + B * N) / (ms_per_step / 1e3), 3), "unit": "tok/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic (seeded weights and prompts)",
+        "vs_baseline": None, "dtype": op_dtype, "data": "synthetic (seeded weights and prompts)",
         "config": desc,
         "prefill_ms": round(pre_ms, 4), "decode_ms_per_step": round(dec_ms / N, 5),
         "prefill_tok_s": round(T / (pre_ms / 1e3), 1),
@@ -607,8 +617,8 @@ def main() -> int:
     dec_byte = sum(v for (ph, _), (v, u) in work_all.items() if ph == "decode" and u == "byte")
     out["phase_roofline"] = {
         "prefill": {"achieved": round(pre_flop / (pre_ms / 1e3) / 1e12, 2), "unit": "TFLOP/s",
-                    "peak": MFMA_PEAK_TFLOPS[cfg.dtype],
-                    "frac": round(pre_flop / (pre_ms / 1e3) / 1e12 / MFMA_PEAK_TFLOPS[cfg.dtype], 4),
+                    "peak": MFMA_PEAK_TFLOPS[op_dtype],
+                    "frac": round(pre_flop / (pre_ms / 1e3) / 1e12 / MFMA_PEAK_TFLOPS[op_dtype], 4),
                     "work": "MFMA flops (projections" + ("" if mamba else " + causal attention") + ")"},
         "decode": {"achieved": round(dec_byte / (dec_ms / 1e3) / 1e9, 2), "unit": "GB/s",
                    "peak": HBM_PEAK_GBS,
@@ -625,7 +635,7 @@ def main() -> int:
                  "avg_us": round(ms / cnt * 1e3, 3)}
             if (phase, cls) in work_all:
                 wv, unit = work_all[(phase, cls)]
-                a, peak, u, bound = rate(wv, unit, ms, cfg.dtype)
+                a, peak, u, bound = rate(wv, unit, ms, op_dtype)
                 r.update({"achieved": round(a, 2), "unit": u, "frac": round(a / peak, 4)})
             rows.append(r)
         over = [f"{r['phase']}:{r['class']}" for r in rows if r.get("frac", 0.0) > 1.0]
@@ -645,7 +655,7 @@ def main() -> int:
                                      "decode": round(ev_dec / dec_ms, 4)}}
         dom = next(r for r in rows if "achieved" in r)
         wv, unit = work_all[(dom["phase"], dom["class"])]
-        a, peak, u, bound = rate(wv, unit, dom["total_ms"], cfg.dtype)
+        a, peak, u, bound = rate(wv, unit, dom["total_ms"], op_dtype)
         traffic = measured_traffic(cfg.name, f"{dom['phase']}:{dom['class']}")
         out["roofline"] = {"bound": bound, "achieved": round(a, 2), "peak": peak, "unit": u,
                            "frac": round(a / peak, 4), "traffic": traffic,

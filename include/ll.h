@@ -44,7 +44,9 @@ typedef enum {
   LL_ERR_HIP = 6               /* a HIP runtime call or kernel launch failed */
 } ll_status;
 
-typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
+/* LL_F16 names fp16 operands; it is accepted by the per-kernel entry points (ll_ops.h), while
+ * a model's weights are LL_F32 or LL_BF16 and ll_config.f16_compute chooses fp16 operands. */
+typedef enum { LL_F32 = 0, LL_BF16 = 1, LL_F16 = 2 } ll_dtype;
 
 /* Model shape and capacity.  Supported: head_dim in {64, 128}; n_heads a multiple of
  * n_kv_heads with n_heads / n_kv_heads in {1, 2, 4, 8}; d_model, n_heads*head_dim and
@@ -68,6 +70,14 @@ typedef struct {
    * pool smaller than max_batch full contexts.  The block table lives in the workspace. */
   int32_t kv_page;
   int32_t kv_pages;
+  /* LL_BF16 weights only.  0: GEMM inputs, activations and the KV cache in bf16.  1: the
+   * weights are converted to fp16 at load -- exact for every bf16 value of magnitude in
+   * [2^-17, 65504], since bf16's 8-bit significand fits fp16's 11 (smaller magnitudes round to
+   * fp16's subnormal grid of 2^-24; a larger one becomes inf and sets bit 1 of the device
+   * flags) -- and GEMM inputs, activations and the KV cache are fp16: the same bytes and the
+   * same MFMA rate, with 8x finer rounding of every activation.  Activations must then stay
+   * within the fp16 range (|v| <= 65504); the residual stream and all accumulation stay fp32. */
+  int32_t f16_compute;
 } ll_config;
 
 #define LL_MAX_BATCH 256
@@ -196,7 +206,8 @@ ll_status ll_set_option(ll_model *m, int32_t option, int32_t value);
 ll_status ll_get_option(const ll_model *m, int32_t option, int32_t *value);
 
 /* Synchronise the model's stream and read the device error flags: bit 0 = a token id
- * outside [0, vocab) was seen (it was replaced by 0, never read out of bounds). */
+ * outside [0, vocab) was seen (it was replaced by 0, never read out of bounds); bit 1 = a
+ * weight outside the fp16 range met the conversion of f16_compute. */
 ll_status ll_device_flags(ll_model *m, int32_t *flags);
 
 /* Kernel classes of the hot path, for per-module timing.  The paper ranks modules by the

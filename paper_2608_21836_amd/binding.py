@@ -17,7 +17,7 @@ LL_OK, LL_ERR_INVALID_ARGUMENT, LL_ERR_UNSUPPORTED, LL_ERR_CAPACITY, LL_ERR_STAT
     LL_ERR_WORKSPACE, LL_ERR_HIP = range(7)
 STATUS_NAMES = ["LL_OK", "LL_ERR_INVALID_ARGUMENT", "LL_ERR_UNSUPPORTED", "LL_ERR_CAPACITY",
                 "LL_ERR_STATE", "LL_ERR_WORKSPACE", "LL_ERR_HIP"]
-LL_F32, LL_BF16 = 0, 1
+LL_F32, LL_BF16, LL_F16 = 0, 1, 2
 LL_MAX_BATCH = 256
 LL_K_COUNT = 11
 # ll_option ids (include/ll.h)
@@ -36,7 +36,8 @@ class LLConfig(ctypes.Structure):
                 ("n_kv_heads", c_int32), ("head_dim", c_int32), ("ffn_dim", c_int32),
                 ("vocab", c_int32), ("rms_eps", c_float), ("rope_theta", c_double),
                 ("dtype", c_int32), ("max_batch", c_int32), ("max_prefill_tokens", c_int32),
-                ("max_ctx", c_int32), ("kv_page", c_int32), ("kv_pages", c_int32)]
+                ("max_ctx", c_int32), ("kv_page", c_int32), ("kv_pages", c_int32),
+                ("f16_compute", c_int32)]
 
 
 class LLWeights(ctypes.Structure):
@@ -240,12 +241,15 @@ def _check(status: int, where: str) -> None:
 
 
 def make_config(cfg, max_batch: int, max_prefill_tokens: int, max_ctx: int, kv_page: int = 0,
-                kv_pages: int = 0) -> LLConfig:
-    """LLConfig from a synth.configs.ModelConfig-like object (kv_page > 0: paged cache)."""
+                kv_pages: int = 0, f16_compute: Optional[bool] = None) -> LLConfig:
+    """LLConfig from a synth.configs.ModelConfig-like object (kv_page > 0: paged cache).
+    f16_compute (bf16 weights only): fp16 operands, the default for bf16 weights."""
+    bf16 = cfg.dtype == "bf16"
+    f16 = bf16 if f16_compute is None else bool(f16_compute)
     return LLConfig(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim,
                     cfg.ffn_dim, cfg.vocab, float(cfg.rms_eps), float(cfg.rope_theta),
-                    LL_BF16 if cfg.dtype == "bf16" else LL_F32, max_batch, max_prefill_tokens,
-                    max_ctx, kv_page, kv_pages)
+                    LL_BF16 if bf16 else LL_F32, max_batch, max_prefill_tokens,
+                    max_ctx, kv_page, kv_pages, 1 if f16 else 0)
 
 
 def workspace_size(cfg: LLConfig) -> int:
@@ -272,13 +276,14 @@ class Model:
 
     def __init__(self, cfg, weights: Dict[str, "object"], max_batch: int,
                  max_prefill_tokens: int, max_ctx: int, stream=None, kv_page: int = 0,
-                 kv_pages: int = 0, guard_bytes: int = 0):
+                 kv_pages: int = 0, guard_bytes: int = 0, f16_compute: Optional[bool] = None):
         """guard_bytes (a multiple of 256): extra bytes allocated before and after the
         workspace (self.guarded), for checks that nothing is written outside it."""
         import torch
         self.lib = load_library()
         self.mcfg = cfg
-        self.cfg = make_config(cfg, max_batch, max_prefill_tokens, max_ctx, kv_page, kv_pages)
+        self.cfg = make_config(cfg, max_batch, max_prefill_tokens, max_ctx, kv_page, kv_pages,
+                               f16_compute)
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         nbytes = workspace_size(self.cfg)
         if guard_bytes % 256:
@@ -596,6 +601,8 @@ def to_device(arr, dtype: str):
     if dtype == "bf16":
         bits = (np.ascontiguousarray(arr, dtype=np.float32).view(np.uint32) >> 16).astype(np.uint16)
         return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).cuda()
+    if dtype == "f16":
+        return torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float16)).cuda()
     return torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32)).cuda()
 
 
@@ -619,7 +626,7 @@ def upload_mamba_weights(cfg, weights) -> Dict[str, "object"]:
 
 def _dt(t) -> int:
     import torch
-    return LL_BF16 if t.dtype == torch.bfloat16 else LL_F32
+    return {torch.bfloat16: LL_BF16, torch.float16: LL_F16}.get(t.dtype, LL_F32)
 
 
 def op_mfma_loop(blocks: int, iters: int, out=None, stream=None):

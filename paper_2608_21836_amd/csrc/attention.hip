@@ -154,11 +154,13 @@ __global__ __launch_bounds__(256) void k_attn_prefill(
 //   O^T += V^T P^T: B = P^T straight from the score registers.
 // The causal / length mask runs only on tiles that reach past the wave's first query; the
 // accumulator is rescaled only when some row maximum grew (otherwise every factor is 1).
-template <int HD>
-__device__ __forceinline__ void attn_tile_bf16(const uint4 *__restrict__ st, const bf16x8 *qf,
+template <typename H, int HD>
+__device__ __forceinline__ void attn_tile16(const uint4 *__restrict__ st,
+                                            const typename Frag<H>::type *qf,
                                                f32x16 *acc, float &m_run, float &l_run, int kt,
                                                int P0, int L, int qw, int my_q, bool q_ok,
                                                float scale_log2, int lane) {
+  using V = typename Frag<H>::type;
   constexpr int BKV = 64, NKC = HD / 16, NDB = HD / 32, NPC = BKV / 16, KTILES = 2 * NKC;
   const int g = lane >> 5;
   f32x16 sc[2];
@@ -168,7 +170,7 @@ __device__ __forceinline__ void attn_tile_bf16(const uint4 *__restrict__ st, con
     for (int i = 0; i < 16; ++i) sc[kb][i] = 0.f;
 #pragma unroll
     for (int c = 0; c < NKC; ++c)
-      sc[kb] = mma32(*reinterpret_cast<const bf16x8 *>(&st[(kb * NKC + c) * 64 + lane]), qf[c], sc[kb]);
+      sc[kb] = mma32(*reinterpret_cast<const V *>(&st[(kb * NKC + c) * 64 + lane]), qf[c], sc[kb]);
   }
   if (kt * BKV + BKV - 1 > P0 + qw || qw + 31 >= L) {
 #pragma unroll
@@ -207,27 +209,27 @@ __device__ __forceinline__ void attn_tile_bf16(const uint4 *__restrict__ st, con
     }
 #pragma unroll
   for (int c = 0; c < NPC; ++c) {
-    bf16x8 pf;
+    V pf;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) pf[e] = static_cast<bf16>(sc[c / 2][8 * (c % 2) + e]);
+    for (int e = 0; e < 8; ++e) pf[e] = static_cast<H>(sc[c / 2][8 * (c % 2) + e]);
 #pragma unroll
     for (int d = 0; d < NDB; ++d)
-      acc[d] = mma32(*reinterpret_cast<const bf16x8 *>(&st[(KTILES + d * NPC + c) * 64 + lane]), pf, acc[d]);
+      acc[d] = mma32(*reinterpret_cast<const V *>(&st[(KTILES + d * NPC + c) * 64 + lane]), pf, acc[d]);
   }
 }
 
 // Normalised output rows of one wave: lane l writes dims 32 d + 8 j + 4 (l / 32) .. + 3 of its
 // query (the O^T accumulator layout), 8 bytes at a time.
-template <int HD>
-__device__ __forceinline__ void attn_store_bf16(bf16 *dst, const f32x16 *acc, float inv, int g) {
+template <typename H, int HD>
+__device__ __forceinline__ void attn_store16(H *dst, const f32x16 *acc, float inv, int g) {
   constexpr int NDB = HD / 32;
   dst += 4 * g;
 #pragma unroll
   for (int d = 0; d < NDB; ++d)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const bf16 v0 = static_cast<bf16>(acc[d][4 * j] * inv), v1 = static_cast<bf16>(acc[d][4 * j + 1] * inv);
-      const bf16 v2 = static_cast<bf16>(acc[d][4 * j + 2] * inv), v3 = static_cast<bf16>(acc[d][4 * j + 3] * inv);
+      const H v0 = static_cast<H>(acc[d][4 * j] * inv), v1 = static_cast<H>(acc[d][4 * j + 1] * inv);
+      const H v2 = static_cast<H>(acc[d][4 * j + 2] * inv), v3 = static_cast<H>(acc[d][4 * j + 3] * inv);
       uint2 pk;
       pk.x = (uint32_t)__builtin_bit_cast(uint16_t, v0) | ((uint32_t)__builtin_bit_cast(uint16_t, v1) << 16);
       pk.y = (uint32_t)__builtin_bit_cast(uint16_t, v2) | ((uint32_t)__builtin_bit_cast(uint16_t, v3) << 16);
@@ -239,8 +241,8 @@ __device__ __forceinline__ void attn_store_bf16(bf16 *dst, const f32x16 *acc, fl
 // pc, key group gg; element e < 4 is key 16 pc + 4 gg + e, e >= 4 is key 16 pc + 8 + 4 gg + e - 4),
 // loaded as 8 rows of 16 B (rows past the sequence read clamped, in bounds, and replaced by
 // zeros: their probabilities are 0 and the cache there may hold anything, NaN included) ...
-template <int HD>
-__device__ __forceinline__ void vt_load(uint4 *vr, const bf16 *Vc, size_t tb, int kt, int KL,
+template <typename H, int HD>
+__device__ __forceinline__ void vt_load(uint4 *vr, const H *Vc, size_t tb, int kt, int KL,
                                         int task) {
   constexpr int NPC = 4;
   const int dg = task % (HD / 8), pc = (task / (HD / 8)) % NPC, gg = task / (HD / 8 * NPC);
@@ -276,10 +278,10 @@ __device__ __forceinline__ void vt_store(uint4 *stage, const uint4 *vr, int task
 // order (global_load_lds); two waves build the V^T tiles (each lane loads 8 keys x 8 dims,
 // transposes them in registers and writes 8 x 16 B), the other two issue the K loads.  Loads
 // for tile t + 1 are in flight while tile t computes (attn_tile_bf16).
-template <int HD>
+template <typename H, int HD>
 __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
-    const bf16 *__restrict__ Q, int ldq, const bf16 *__restrict__ Kc, const bf16 *__restrict__ Vc,
-    bf16 *__restrict__ O, int ldo, const int *__restrict__ cu, const int *__restrict__ kstart,
+    const H *__restrict__ Q, int ldq, const H *__restrict__ Kc, const H *__restrict__ Vc,
+    H *__restrict__ O, int ldo, const int *__restrict__ cu, const int *__restrict__ kstart,
     const int2 *__restrict__ qtiles, int hq, int hkv, int max_ctx, float scale_log2,
     KvPaging pg) {
   constexpr int QT = kAttnQTileWide, BKV = 64;
@@ -307,12 +309,13 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
   const int qw = q0 + wave * 32;  // first query of this wave
   const int my_q = qw + (lane & 31);
   const bool q_ok = my_q < L;
-  const bf16x8 fz = frag_zero<bf16x8>();
+  using V = typename Frag<H>::type;
+  const V fz = frag_zero<V>();
 
-  bf16x8 qf[NKC];
+  V qf[NKC];
 #pragma unroll
   for (int c = 0; c < NKC; ++c)
-    qf[c] = q_ok ? load_frag<bf16x8>(Q + (size_t)(tok0 + my_q) * ldq + h * HD + 16 * c + 8 * g) : fz;
+    qf[c] = q_ok ? load_frag<V>(Q + (size_t)(tok0 + my_q) * ldq + h * HD + 16 * c + 8 * g) : fz;
   f32x16 acc[NDB];
 #pragma unroll
   for (int d = 0; d < NDB; ++d)
@@ -338,7 +341,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
   };
   uint4 vr[8];
   auto v_load = [&](int kt) {
-    if (wave < VW) vt_load<HD>(vr, Vc, kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD), kt, KL, tid);
+    if (wave < VW) vt_load<H, HD>(vr, Vc, kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD), kt, KL, tid);
   };
   auto v_store = [&](int buf) {
     if (wave < VW) vt_store<HD>(&smem[buf * STAGE], vr, tid);
@@ -356,14 +359,14 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
       v_load(kt + 1);
     }
     if (qw < L && kt * BKV <= P0 + qw + 31)  // else nothing for this wave in this tile
-      attn_tile_bf16<HD>(&smem[cur * STAGE], qf, acc, m_run, l_run, kt, P0, L, qw, my_q, q_ok,
+      attn_tile16<H, HD>(&smem[cur * STAGE], qf, acc, m_run, l_run, kt, P0, L, qw, my_q, q_ok,
                          scale_log2, lane);
     if (more) v_store(cur ^ 1);
     __syncthreads();
   }
 
   l_run += __shfl_xor(l_run, 32);
-  if (q_ok) attn_store_bf16<HD>(O + (size_t)(tok0 + my_q) * ldo + h * HD, acc, 1.0f / l_run, g);
+  if (q_ok) attn_store16<H, HD>(O + (size_t)(tok0 + my_q) * ldo + h * HD, acc, 1.0f / l_run, g);
 }
 
 // bf16 prefill attention for grouped heads (group G = H_q / H_kv >= 2), after the paper's
@@ -375,10 +378,10 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
 // waves' worth of lanes) rotates over the waves from tile to tile so that no wave carries it
 // every time.  Blocks take their (sequence, query tile, KV head) from the work list in
 // XCD-owned ranges (AttnSched).
-template <int HD, int G>
+template <typename H, int HD, int G>
 __global__ __launch_bounds__(512, 1) void k_attn_prefill_gqa(
-    const bf16 *__restrict__ Q, int ldq, const bf16 *__restrict__ Kc, const bf16 *__restrict__ Vc,
-    bf16 *__restrict__ O, int ldo, const int *__restrict__ cu, const int *__restrict__ kstart,
+    const H *__restrict__ Q, int ldq, const H *__restrict__ Kc, const H *__restrict__ Vc,
+    H *__restrict__ O, int ldo, const int *__restrict__ cu, const int *__restrict__ kstart,
     const int4 *__restrict__ sched, AttnSched as, int hkv, int max_ctx, float scale_log2,
     KvPaging pg) {
   constexpr int NW = 8, QB = NW / G, QT = 32 * QB, BKV = 64;
@@ -403,12 +406,13 @@ __global__ __launch_bounds__(512, 1) void k_attn_prefill_gqa(
   const int qw = q0 + 32 * (wave % QB);
   const int my_q = qw + (lane & 31);
   const bool q_ok = my_q < L;
-  const bf16x8 fz = frag_zero<bf16x8>();
+  using V = typename Frag<H>::type;
+  const V fz = frag_zero<V>();
 
-  bf16x8 qf[NKC];
+  V qf[NKC];
 #pragma unroll
   for (int c = 0; c < NKC; ++c)
-    qf[c] = q_ok ? load_frag<bf16x8>(Q + (size_t)(tok0 + my_q) * ldq + h * HD + 16 * c + 8 * g) : fz;
+    qf[c] = q_ok ? load_frag<V>(Q + (size_t)(tok0 + my_q) * ldq + h * HD + 16 * c + 8 * g) : fz;
   f32x16 acc[NDB];
 #pragma unroll
   for (int d = 0; d < NDB; ++d)
@@ -436,7 +440,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_prefill_gqa(
   uint4 vr[8];
   auto v_load = [&](int kt) {
     const int task = v_task(kt);
-    if (task >= 0) vt_load<HD>(vr, Vc, kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD), kt, KL, task);
+    if (task >= 0) vt_load<H, HD>(vr, Vc, kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD), kt, KL, task);
   };
   auto v_store = [&](int kt, int buf) {
     const int task = v_task(kt);
@@ -455,14 +459,14 @@ __global__ __launch_bounds__(512, 1) void k_attn_prefill_gqa(
       v_load(kt + 1);
     }
     if (qw < L && kt * BKV <= P0 + qw + 31)
-      attn_tile_bf16<HD>(&smem[cur * STAGE], qf, acc, m_run, l_run, kt, P0, L, qw, my_q, q_ok,
+      attn_tile16<H, HD>(&smem[cur * STAGE], qf, acc, m_run, l_run, kt, P0, L, qw, my_q, q_ok,
                          scale_log2, lane);
     if (more) v_store(kt + 1, cur ^ 1);
     __syncthreads();
   }
 
   l_run += __shfl_xor(l_run, 32);
-  if (q_ok) attn_store_bf16<HD>(O + (size_t)(tok0 + my_q) * ldo + h * HD, acc, 1.0f / l_run, g);
+  if (q_ok) attn_store16<H, HD>(O + (size_t)(tok0 + my_q) * ldo + h * HD, acc, 1.0f / l_run, g);
 }
 
 constexpr int kMaxSplit = 128;  // blocks per (sequence, kv head)
@@ -652,16 +656,16 @@ __global__ __launch_bounds__(HD) void k_attn_combine_direct(const float *__restr
       merge_splits_direct<kCombineDirectSplits>(part_ml + base * 2, part_o + base * HD + d, HD, ns));
 }
 
-template <int HD>
+template <typename H, int HD>
 hipError_t run_prefill_gqa(int group, const void *q, int ldq, const void *kc, const void *vc,
                            void *o, int ldo, const int *cu, const int *kstart, const int4 *sched,
                            const AttnSched &as, int hkv, int max_ctx, hipStream_t s,
                            const KvPaging &pg) {
   const float scale_log2 = kLog2e / sqrtf((float)HD);
 #define LL_GQA(G)                                                                             \
-  LL_LAUNCH((k_attn_prefill_gqa<HD, G>), dim3(as.grid), dim3(512), 0, s,                      \
-            reinterpret_cast<const bf16 *>(q), ldq, reinterpret_cast<const bf16 *>(kc),        \
-            reinterpret_cast<const bf16 *>(vc), reinterpret_cast<bf16 *>(o), ldo, cu, kstart, \
+  LL_LAUNCH((k_attn_prefill_gqa<H, HD, G>), dim3(as.grid), dim3(512), 0, s,                   \
+            reinterpret_cast<const H *>(q), ldq, reinterpret_cast<const H *>(kc),              \
+            reinterpret_cast<const H *>(vc), reinterpret_cast<H *>(o), ldo, cu, kstart,        \
             sched, as, hkv, max_ctx, scale_log2, pg)
   switch (group) {
     case 2: LL_GQA(2); break;
@@ -679,9 +683,9 @@ hipError_t run_prefill(const void *q, int ldq, const void *kc, const void *vc, v
                        int hq, int hkv, int max_ctx, hipStream_t s, const KvPaging &pg) {
   const float scale_log2 = kLog2e / sqrtf((float)HD);
   if constexpr (!std::is_same<T, float>::value) {
-    LL_LAUNCH((k_attn_prefill_wide<HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
-              reinterpret_cast<const bf16 *>(q), ldq, reinterpret_cast<const bf16 *>(kc),
-              reinterpret_cast<const bf16 *>(vc), reinterpret_cast<bf16 *>(o), ldo, cu, kstart,
+    LL_LAUNCH((k_attn_prefill_wide<T, HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
+              reinterpret_cast<const T *>(q), ldq, reinterpret_cast<const T *>(kc),
+              reinterpret_cast<const T *>(vc), reinterpret_cast<T *>(o), ldo, cu, kstart,
               qtiles, hq, hkv, max_ctx, scale_log2, pg);
   } else {
     LL_LAUNCH((k_attn_prefill<T, HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
@@ -787,12 +791,17 @@ hipError_t launch_attn_prefill(int dtype, int head_dim, const void *q, int ldq, 
   if (attn_prefill_gqa(dtype, hq / hkv)) {
     if (!sched || !as || as->qtile != attn_gqa_qtile(hq / hkv)) return hipErrorInvalidValue;
     if (as->n_entries <= 0) return hipSuccess;
-    if (head_dim == 64)
-      return run_prefill_gqa<64>(hq / hkv, q, ldq, kc, vc, o, ldo, cu, kstart, sched, *as, hkv,
-                                 max_ctx, s, pg);
-    if (head_dim == 128)
-      return run_prefill_gqa<128>(hq / hkv, q, ldq, kc, vc, o, ldo, cu, kstart, sched, *as, hkv,
-                                  max_ctx, s, pg);
+#define LL_GQA_HD(H, HD)                                                                      \
+  return run_prefill_gqa<H, HD>(hq / hkv, q, ldq, kc, vc, o, ldo, cu, kstart, sched, *as, hkv, \
+                                max_ctx, s, pg)
+    if (dtype == kF16) {
+      if (head_dim == 64) LL_GQA_HD(f16, 64);
+      if (head_dim == 128) LL_GQA_HD(f16, 128);
+    } else {
+      if (head_dim == 64) LL_GQA_HD(bf16, 64);
+      if (head_dim == 128) LL_GQA_HD(bf16, 128);
+    }
+#undef LL_GQA_HD
     return hipErrorInvalidValue;
   }
   if (n_qtiles <= 0) return hipSuccess;
@@ -802,6 +811,9 @@ hipError_t launch_attn_prefill(int dtype, int head_dim, const void *q, int ldq, 
   if (dtype == kF32) {
     if (head_dim == 64) LL_PREFILL(float, 64);
     if (head_dim == 128) LL_PREFILL(float, 128);
+  } else if (dtype == kF16) {
+    if (head_dim == 64) LL_PREFILL(f16, 64);
+    if (head_dim == 128) LL_PREFILL(f16, 128);
   } else {
     if (head_dim == 64) LL_PREFILL(bf16, 64);
     if (head_dim == 128) LL_PREFILL(bf16, 128);
@@ -848,6 +860,9 @@ hipError_t launch_attn_decode(int dtype, int head_dim, const void *q, int ldq, c
   if (dtype == kF32) {
     if (head_dim == 64) LL_DECODE_HD(float, 64);
     if (head_dim == 128) LL_DECODE_HD(float, 128);
+  } else if (dtype == kF16) {
+    if (head_dim == 64) LL_DECODE_HD(f16, 64);
+    if (head_dim == 128) LL_DECODE_HD(f16, 128);
   } else {
     if (head_dim == 64) LL_DECODE_HD(bf16, 64);
     if (head_dim == 128) LL_DECODE_HD(bf16, 128);

@@ -20,6 +20,8 @@
 
 typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16;
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
@@ -46,11 +48,19 @@ template <> struct Frag<float> {
   typedef f32x4 type;
   static constexpr int EPL = 4;
 };
+//   fp16: as bf16 (v_mfma_f32_16x16x32_f16)
+template <> struct Frag<f16> {
+  typedef f16x8 type;
+  static constexpr int EPL = 8;
+};
 
 // 16x16 output tile += A-fragment x B-fragment over one 16-byte-per-lane chunk.
 // Output layout: lane l holds rows 4*(l/16) + r (r < 4) of column l % 16.
 __device__ __forceinline__ f32x4 mma_chunk(const bf16x8 &a, const bf16x8 &b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma_chunk(const f16x8 &a, const f16x8 &b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
 __device__ __forceinline__ f32x4 mma_chunk(const f32x4 &a, const f32x4 &b, f32x4 c) {
   c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], c, 0, 0, 0);
@@ -66,13 +76,18 @@ __device__ __forceinline__ f32x4 mma_chunk(const f32x4 &a, const f32x4 &b, f32x4
 __device__ __forceinline__ f32x16 mma32(const bf16x8 &a, const bf16x8 &b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
+__device__ __forceinline__ f32x16 mma32(const f16x8 &a, const f16x8 &b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
 
 __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ float to_f32(bf16 x) { return static_cast<float>(x); }
+__device__ __forceinline__ float to_f32(f16 x) { return static_cast<float>(x); }
 
 template <typename T> __device__ __forceinline__ T from_f32(float x);
 template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return static_cast<bf16>(x); }
+template <> __device__ __forceinline__ f16 from_f32<f16>(float x) { return static_cast<f16>(x); }
 
 template <typename F> __device__ __forceinline__ F frag_zero() {
   F z;

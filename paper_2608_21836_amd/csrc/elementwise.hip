@@ -200,6 +200,17 @@ __global__ __launch_bounds__(256) void k_mfma_loop(int iters, float *__restrict_
   if ((threadIdx.x & 63) == 0) out[blockIdx.x * 4 + (threadIdx.x >> 6)] = t;
 }
 
+// Element-wise bf16 -> fp16 (exact for magnitudes in [2^-17, 65504]; beyond 65504 the value
+// becomes inf and bit 1 of *err is set).
+__global__ __launch_bounds__(256) void k_bf16_to_f16(const bf16 *__restrict__ src,
+                                                     f16 *__restrict__ dst, size_t n, int *err) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
+    const float v = static_cast<float>(src[i]);
+    if (fabsf(v) > 65504.f && !__builtin_isnan(v) && err) atomicOr(err, 2);
+    dst[i] = static_cast<f16>(v);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_embed(int dtype, const int *tokens, int ntok, const void *table, int vocab,
@@ -208,6 +219,9 @@ hipError_t launch_embed(int dtype, const int *tokens, int ntok, const void *tabl
   if (dtype == kF32)
     LL_LAUNCH(k_embed<float>, dim3(ntok), dim3(256), 0, s, tokens,
                        reinterpret_cast<const float *>(table), vocab, d, x, err, scale);
+  else if (dtype == kF16)
+    LL_LAUNCH(k_embed<f16>, dim3(ntok), dim3(256), 0, s, tokens,
+                       reinterpret_cast<const f16 *>(table), vocab, d, x, err, scale);
   else
     LL_LAUNCH(k_embed<bf16>, dim3(ntok), dim3(256), 0, s, tokens,
                        reinterpret_cast<const bf16 *>(table), vocab, d, x, err, scale);
@@ -221,10 +235,23 @@ hipError_t launch_rmsnorm(int dtype, const float *x, int ldx, const int *rowmap,
     LL_LAUNCH(k_rmsnorm<float>, dim3(rows), dim3(256), 0, s, x, ldx, rowmap, d,
                        reinterpret_cast<const float *>(gain), eps, reinterpret_cast<float *>(y),
                        ldy);
+  else if (dtype == kF16)
+    LL_LAUNCH(k_rmsnorm<f16>, dim3(rows), dim3(256), 0, s, x, ldx, rowmap, d,
+                       reinterpret_cast<const f16 *>(gain), eps, reinterpret_cast<f16 *>(y),
+                       ldy);
   else
     LL_LAUNCH(k_rmsnorm<bf16>, dim3(rows), dim3(256), 0, s, x, ldx, rowmap, d,
                        reinterpret_cast<const bf16 *>(gain), eps, reinterpret_cast<bf16 *>(y),
                        ldy);
+  return hipGetLastError();
+}
+
+hipError_t launch_bf16_to_f16(const void *src, void *dst, size_t n, int *err, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  if (!src || !dst) return hipErrorInvalidValue;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 65536);
+  LL_LAUNCH(k_bf16_to_f16, dim3(blocks), dim3(256), 0, s, reinterpret_cast<const bf16 *>(src),
+            reinterpret_cast<f16 *>(dst), n, err);
   return hipGetLastError();
 }
 

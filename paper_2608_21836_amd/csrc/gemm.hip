@@ -23,8 +23,36 @@ namespace {
 // ------------------------------------------------------------------------------------------
 // Repack
 // ------------------------------------------------------------------------------------------
-template <typename T>
-__global__ void k_repack(RepackSrc src, int n, int k, int perm, int hd, int ffn, uint8_t *wt) {
+// S: element type of the sources, T: of the tiles (bf16 -> fp16 converts each element; every
+// bf16 value of magnitude in [2^-17, 65504] is exact in fp16, smaller ones round to fp16's
+// subnormal grid of 2^-24; larger ones become inf, flagged in err bit 1).
+template <typename T> struct Chunk16 {  // 16 bytes of elements
+  T e[16 / sizeof(T)];
+};
+template <typename S, typename T>
+__device__ __forceinline__ uint4 convert16(uint4 v, int *err) {
+  if constexpr (std::is_same<S, T>::value) {
+    return v;
+  } else {
+    static_assert(sizeof(S) == 2 && sizeof(T) == 2, "16-bit conversions only");
+    const Chunk16<S> in = __builtin_bit_cast(Chunk16<S>, v);
+    Chunk16<T> out;
+    bool bad = false;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float f = to_f32(in.e[e]);
+      bad |= fabsf(f) > 65504.f && !__builtin_isnan(f);
+      out.e[e] = from_f32<T>(f);
+    }
+    if (bad && err) atomicOr(err, 2);
+    return __builtin_bit_cast(uint4, out);
+  }
+}
+
+template <typename S, typename T = S>
+__global__ void k_repack(RepackSrc src, int n, int k, int perm, int hd, int ffn, uint8_t *wt,
+                         int *err) {
+  static_assert(sizeof(S) == sizeof(T), "same element size");
   constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL;
   const int kb_n = k / TK;
   const size_t total = (size_t)n * k / EPL;  // 16-byte chunks
@@ -49,8 +77,9 @@ __global__ void k_repack(RepackSrc src, int n, int k, int perm, int hd, int ffn,
     // rows past the stacked sources (padding up to n) are zero
     uint4 v = make_uint4(0u, 0u, 0u, 0u);
     if (src.src[s] && nlog < src.rows[s])
-      v = *reinterpret_cast<const uint4 *>(reinterpret_cast<const T *>(src.src[s]) +
-                                           (size_t)nlog * k + kk);
+      v = convert16<S, T>(*reinterpret_cast<const uint4 *>(reinterpret_cast<const S *>(src.src[s]) +
+                                                           (size_t)nlog * k + kk),
+                          err);
     *reinterpret_cast<uint4 *>(wt + c * 16) = v;
   }
 }
@@ -61,13 +90,19 @@ __global__ void k_repack(RepackSrc src, int n, int k, int perm, int hd, int ffn,
 // ------------------------------------------------------------------------------------------
 // Eight consecutive outputs of type T from fp32 values, as 16-byte stores.
 template <typename T> __device__ __forceinline__ void store8(T *dst, const float *v);
-template <> __device__ __forceinline__ void store8<bf16>(bf16 *dst, const float *v) {
+template <typename H> __device__ __forceinline__ void store8_16(H *dst, const float *v) {
   uint32_t w[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j)
-    w[j] = (uint32_t)__builtin_bit_cast(uint16_t, static_cast<bf16>(v[2 * j])) |
-           ((uint32_t)__builtin_bit_cast(uint16_t, static_cast<bf16>(v[2 * j + 1])) << 16);
+    w[j] = (uint32_t)__builtin_bit_cast(uint16_t, static_cast<H>(v[2 * j])) |
+           ((uint32_t)__builtin_bit_cast(uint16_t, static_cast<H>(v[2 * j + 1])) << 16);
   *reinterpret_cast<uint4 *>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+template <> __device__ __forceinline__ void store8<bf16>(bf16 *dst, const float *v) {
+  store8_16(dst, v);
+}
+template <> __device__ __forceinline__ void store8<f16>(f16 *dst, const float *v) {
+  store8_16(dst, v);
 }
 template <> __device__ __forceinline__ void store8<float>(float *dst, const float *v) {
   reinterpret_cast<float4 *>(dst)[0] = make_float4(v[0], v[1], v[2], v[3]);
@@ -1225,15 +1260,21 @@ hipError_t dispatch_epi(const void *a, int lda, const NormIn *norm,
 }  // namespace
 
 hipError_t launch_repack(int dtype, const RepackSrc &src, int n, int k, int perm, int head_dim,
-                         int ffn_dim, void *wt, hipStream_t s) {
+                         int ffn_dim, void *wt, hipStream_t s, int src_dtype, int *err) {
+  if (src_dtype < 0) src_dtype = dtype;
   const size_t chunks = (size_t)n * k * elem_bytes(dtype) / 16;
   const int blocks = (int)std::min<size_t>((chunks + 255) / 256, 65536);
-  if (dtype == kF32)
-    LL_LAUNCH(k_repack<float>, dim3(blocks), dim3(256), 0, s, src, n, k, perm,
-                       head_dim, ffn_dim, reinterpret_cast<uint8_t *>(wt));
+  uint8_t *w = reinterpret_cast<uint8_t *>(wt);
+  if (dtype == kF32 && src_dtype == kF32)
+    LL_LAUNCH((k_repack<float>), dim3(blocks), dim3(256), 0, s, src, n, k, perm, head_dim, ffn_dim, w, err);
+  else if (dtype == kBF16 && src_dtype == kBF16)
+    LL_LAUNCH((k_repack<bf16>), dim3(blocks), dim3(256), 0, s, src, n, k, perm, head_dim, ffn_dim, w, err);
+  else if (dtype == kF16 && src_dtype == kF16)
+    LL_LAUNCH((k_repack<f16>), dim3(blocks), dim3(256), 0, s, src, n, k, perm, head_dim, ffn_dim, w, err);
+  else if (dtype == kF16 && src_dtype == kBF16)
+    LL_LAUNCH((k_repack<bf16, f16>), dim3(blocks), dim3(256), 0, s, src, n, k, perm, head_dim, ffn_dim, w, err);
   else
-    LL_LAUNCH(k_repack<bf16>, dim3(blocks), dim3(256), 0, s, src, n, k, perm,
-                       head_dim, ffn_dim, reinterpret_cast<uint8_t *>(wt));
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
@@ -1242,10 +1283,14 @@ hipError_t launch_gemm_tiled(int dtype, const void *a, int lda, const void *wt, 
                              size_t ws_bytes, int tile) {
   if (m <= 0) return hipSuccess;
   if (tile < kTileAuto || tile > kTileMid) return hipErrorInvalidValue;
-  return dtype == kF32 ? dispatch_epi<float, true>(a, lda, nullptr, wt, m, n, k, ep, s, ws,
-                                                   ws_bytes, nullptr, nullptr, tile)
-                       : dispatch_epi<bf16, true>(a, lda, nullptr, wt, m, n, k, ep, s, ws,
-                                                  ws_bytes, nullptr, nullptr, tile);
+  if (dtype == kF32)
+    return dispatch_epi<float, true>(a, lda, nullptr, wt, m, n, k, ep, s, ws, ws_bytes, nullptr,
+                                     nullptr, tile);
+  if (dtype == kF16)
+    return dispatch_epi<f16, true>(a, lda, nullptr, wt, m, n, k, ep, s, ws, ws_bytes, nullptr,
+                                   nullptr, tile);
+  return dispatch_epi<bf16, true>(a, lda, nullptr, wt, m, n, k, ep, s, ws, ws_bytes, nullptr,
+                                  nullptr, tile);
 }
 
 hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *norm,
@@ -1256,10 +1301,14 @@ hipError_t launch_gemm_skinny(int dtype, const void *a, int lda, const NormIn *n
   if (m <= 0) return hipSuccess;
   if (post && (!post->gain || !post->out)) return hipErrorInvalidValue;
   if (ksplit != 1 && ksplit != 2) return hipErrorInvalidValue;
-  return dtype == kF32 ? dispatch_epi<float, false>(a, lda, norm, wt, m, n, k, ep, s, ws,
-                                                    ws_bytes, post, post_done, kTileAuto, ksplit)
-                       : dispatch_epi<bf16, false>(a, lda, norm, wt, m, n, k, ep, s, ws,
-                                                   ws_bytes, post, post_done, kTileAuto, ksplit);
+  if (dtype == kF32)
+    return dispatch_epi<float, false>(a, lda, norm, wt, m, n, k, ep, s, ws, ws_bytes, post,
+                                      post_done, kTileAuto, ksplit);
+  if (dtype == kF16)
+    return dispatch_epi<f16, false>(a, lda, norm, wt, m, n, k, ep, s, ws, ws_bytes, post,
+                                    post_done, kTileAuto, ksplit);
+  return dispatch_epi<bf16, false>(a, lda, norm, wt, m, n, k, ep, s, ws, ws_bytes, post,
+                                   post_done, kTileAuto, ksplit);
 }
 
 SplitKPlan prefill_splitk_plan(size_t elem, int m, int n, int k) {

@@ -18,7 +18,10 @@ struct LaunchTimer {
 };
 extern thread_local LaunchTimer *g_launch_timer;
 
-enum DType : int { kF32 = 0, kBF16 = 1 };
+// Operand types.  kF16 carries a bf16 model's weights converted exactly to fp16 (bf16's 8-bit
+// significand fits fp16's 11; magnitudes in [2^-17, 65504]) with activations, KV cache and MFMA
+// operands in fp16: the same bytes and MFMA rate as bf16 at 8x finer rounding.
+enum DType : int { kF32 = 0, kBF16 = 1, kF16 = 2 };
 
 inline size_t elem_bytes(int dtype) { return dtype == kF32 ? 4 : 2; }
 
@@ -41,8 +44,11 @@ struct RepackSrc {
   int rows[3];
 };
 
+// src_dtype (-1: dtype) is the sources' element type: kBF16 sources may be repacked into kF16
+// tiles (exact conversion; a value beyond the fp16 range sets bit 1 of *err when err is given).
 hipError_t launch_repack(int dtype, const RepackSrc &src, int n, int k, int perm, int head_dim,
-                         int ffn_dim, void *wt, hipStream_t s);
+                         int ffn_dim, void *wt, hipStream_t s, int src_dtype = -1,
+                         int *err = nullptr);
 
 // KV cache addressing.  Contiguous (table null): row pos of (sequence b, kv head h) at
 // element ((b hkv + h) max_ctx + pos) hd.  Paged: the cache of a layer is a pool of pages
@@ -203,6 +209,8 @@ SplitKPlan prefill_splitk_plan(size_t elem, int m, int n, int k);
 
 hipError_t launch_embed(int dtype, const int *tokens, int ntok, const void *table, int vocab,
                         int d, float *x, int *err_flags, hipStream_t s, float scale = 1.f);
+// dst[i] = fp16(src[i]) for n bf16 values (see kF16); an out-of-range value sets bit 1 of *err.
+hipError_t launch_bf16_to_f16(const void *src, void *dst, size_t n, int *err, hipStream_t s);
 hipError_t launch_rmsnorm(int dtype, const float *x, int ldx, const int *rowmap, int rows,
                           int d, const void *gain, float eps, void *y, int ldy, hipStream_t s);
 // next[r] = column of the largest argmax partial of row r (lowest column on ties); lens_inc[r]
@@ -237,7 +245,7 @@ struct AttnSched {
   int grid = 0;       // workgroups launched (kXcds x the longest range)
   int cut[kXcds + 1] = {};
 };
-inline bool attn_prefill_gqa(int dtype, int group) { return dtype == kBF16 && group >= 2; }
+inline bool attn_prefill_gqa(int dtype, int group) { return dtype != kF32 && group >= 2; }
 inline int attn_gqa_qtile(int group) { return 256 / group; }
 AttnSched attn_prefill_sched(const PrefillMeta &pm, int group, int n_kv_heads);
 // sched (nullable): the work list of the grouped-query kernel, sized by as->n_entries.

@@ -89,6 +89,10 @@ ll_status validate_config(const ll_config *c) {
     return fail(LL_ERR_INVALID_ARGUMENT, "kv_pages %d without kv_page", c->kv_pages);
   if (c->kv_page % 256)
     return fail(LL_ERR_UNSUPPORTED, "kv_page %d not a multiple of 256", c->kv_page);
+  if (c->f16_compute != 0 && c->f16_compute != 1)
+    return fail(LL_ERR_INVALID_ARGUMENT, "f16_compute %d not 0 or 1", c->f16_compute);
+  if (c->f16_compute && c->dtype != LL_BF16)
+    return fail(LL_ERR_INVALID_ARGUMENT, "f16_compute needs bf16 weights");
   return LL_OK;
 }
 
@@ -170,7 +174,7 @@ Layout make_layout(const ll_config &c) {
   L.qtiles = take("qtiles", (R / kAttnQTile + c.max_batch + 1) * 8);
   // work list of the grouped-query prefill attention: ceil(L_b / qtile) tiles per sequence and
   // KV head, each sequence at least one token
-  if (attn_prefill_gqa(c.dtype, c.n_heads / c.n_kv_heads))
+  if (attn_prefill_gqa(compute_dtype(c), c.n_heads / c.n_kv_heads))
     L.sched = take("sched", (R / attn_gqa_qtile(c.n_heads / c.n_kv_heads) + c.max_batch + 1) *
                    (size_t)c.n_kv_heads * 16);
   L.err = take("err", 4);
@@ -324,7 +328,7 @@ ll_status enqueue_layers(ll_model *m, int rows, bool decode, int n_qtiles, hipSt
   if (hf_ready) *hf_ready = false;
   const ll_config &c = m->cfg;
   const int d = c.d_model, qd = c.n_heads * c.head_dim, F = c.ffn_dim;
-  const int dt = c.dtype;
+  const int dt = compute_dtype(c);
   const bool fuse_norm = decode && rows <= kFusedNormMaxRows &&
                          skinny_norm_lds(elem_bytes(dt), rows, d) <= kSkinnyMaxNormLds;
   const AttnDecodePlan ap = m->attn_plan();
@@ -435,14 +439,14 @@ ll_status enqueue_head(ll_model *m, int batch, const int *rowmap, int *next, flo
   EpiParams ep = argmax_epi(m, logits);
   NormIn nrm{m->at<float>(m->L.x), c.d_model, rowmap, m->at(m->L.final_norm), c.rms_eps};
   const bool fuse_norm = batch <= kFusedNormMaxRows &&
-                         skinny_norm_lds(elem_bytes(c.dtype), batch, c.d_model) <= kSkinnyMaxNormLds;
+                         skinny_norm_lds(elem_bytes(compute_dtype(c)), batch, c.d_model) <= kSkinnyMaxNormLds;
   if (!fuse_norm && !hf_ready) {
     m->mark(LL_K_RMSNORM);
-    LL_HIP(launch_rmsnorm(c.dtype, m->at<float>(m->L.x), c.d_model, rowmap, batch, c.d_model,
+    LL_HIP(launch_rmsnorm(compute_dtype(c), m->at<float>(m->L.x), c.d_model, rowmap, batch, c.d_model,
                           m->at(m->L.final_norm), c.rms_eps, m->at(m->L.hf), c.d_model, s));
   }
   m->mark(LL_K_LM_HEAD);
-  LL_HIP(launch_gemm_skinny(c.dtype, m->at(m->L.hf), c.d_model, fuse_norm ? &nrm : nullptr,
+  LL_HIP(launch_gemm_skinny(compute_dtype(c), m->at(m->L.hf), c.d_model, fuse_norm ? &nrm : nullptr,
                             m->at(m->L.lm_head), batch, c.vocab, c.d_model, ep, s));
   m->mark(LL_K_ARGMAX);
   LL_HIP(launch_argmax_reduce(ep.part_val, ep.part_idx, batch, ep.n_parts, next, lens_inc, s));
@@ -453,7 +457,7 @@ ll_status enqueue_decode(ll_model *m, const int32_t *in, int32_t *out, float *lo
                          hipStream_t s) {
   const ll_config &c = m->cfg;
   m->mark(LL_K_EMBED);
-  LL_HIP(launch_embed(c.dtype, in, m->batch, m->at(m->L.embed), c.vocab, c.d_model,
+  LL_HIP(launch_embed(compute_dtype(c), in, m->batch, m->at(m->L.embed), c.vocab, c.d_model,
                       m->at<float>(m->L.x), m->at<int>(m->L.err), s));
   bool hf_ready = false;
   ll_status st = enqueue_layers(m, m->batch, true, 0, s, &hf_ready);
@@ -518,29 +522,33 @@ ll_status ll_model_load(const ll_config *cfg, const ll_weights *w, void *workspa
       return bail(fail(LL_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_)));       \
   } while (0)
 
-  LOAD_HIP(hipMemcpyAsync(m->at(L.embed), w->tok_embed, (size_t)c.vocab * d * eb,
-                          hipMemcpyDeviceToDevice, s));
-  LOAD_HIP(hipMemcpyAsync(m->at(L.final_norm), w->final_norm, d * eb, hipMemcpyDeviceToDevice, s));
+  const int cdt = compute_dtype(c);
+  int *err = m->at<int>(L.err);
+  LOAD_HIP(hipMemsetAsync(err, 0, 4, s));
+  // Vectors copied as they are, or converted to fp16 (f16_compute).
+  auto copy_vec = [&](size_t off, const void *src, size_t n) {
+    return cdt == c.dtype ? hipMemcpyAsync(m->at(off), src, n * eb, hipMemcpyDeviceToDevice, s)
+                          : launch_bf16_to_f16(src, m->at(off), n, err, s);
+  };
+  auto repack = [&](const RepackSrc &src, int n, int k, int perm, size_t off) {
+    return launch_repack(cdt, src, n, k, perm, c.head_dim, c.ffn_dim, m->at(off), s, c.dtype, err);
+  };
+  LOAD_HIP(copy_vec(L.embed, w->tok_embed, (size_t)c.vocab * d));
+  LOAD_HIP(copy_vec(L.final_norm, w->final_norm, d));
   for (int l = 0; l < c.n_layers; ++l) {
     RepackSrc qkv{{w->wq[l], w->wk[l], w->wv[l]}, {qd, kvd, kvd}};
-    LOAD_HIP(launch_repack(c.dtype, qkv, L.n_qkv, d, kPermRope, c.head_dim, c.ffn_dim,
-                           m->at(L.wqkv[l]), s));
+    LOAD_HIP(repack(qkv, L.n_qkv, d, kPermRope, L.wqkv[l]));
     RepackSrc wo{{w->wo[l], nullptr, nullptr}, {d, 0, 0}};
-    LOAD_HIP(launch_repack(c.dtype, wo, d, qd, kPermNone, c.head_dim, c.ffn_dim, m->at(L.wo[l]), s));
+    LOAD_HIP(repack(wo, d, qd, kPermNone, L.wo[l]));
     RepackSrc gu{{w->w_gate[l], w->w_up[l], nullptr}, {c.ffn_dim, c.ffn_dim, 0}};
-    LOAD_HIP(launch_repack(c.dtype, gu, 2 * c.ffn_dim, d, kPermGlu, c.head_dim, c.ffn_dim,
-                           m->at(L.wgu[l]), s));
+    LOAD_HIP(repack(gu, 2 * c.ffn_dim, d, kPermGlu, L.wgu[l]));
     RepackSrc wd{{w->w_down[l], nullptr, nullptr}, {d, 0, 0}};
-    LOAD_HIP(launch_repack(c.dtype, wd, d, c.ffn_dim, kPermNone, c.head_dim, c.ffn_dim,
-                           m->at(L.wd[l]), s));
-    LOAD_HIP(hipMemcpyAsync(m->at(L.attn_norm[l]), w->attn_norm[l], d * eb,
-                            hipMemcpyDeviceToDevice, s));
-    LOAD_HIP(hipMemcpyAsync(m->at(L.mlp_norm[l]), w->mlp_norm[l], d * eb,
-                            hipMemcpyDeviceToDevice, s));
+    LOAD_HIP(repack(wd, d, c.ffn_dim, kPermNone, L.wd[l]));
+    LOAD_HIP(copy_vec(L.attn_norm[l], w->attn_norm[l], d));
+    LOAD_HIP(copy_vec(L.mlp_norm[l], w->mlp_norm[l], d));
   }
   RepackSrc lm{{w->lm_head, nullptr, nullptr}, {c.vocab, 0, 0}};
-  LOAD_HIP(launch_repack(c.dtype, lm, c.vocab, d, kPermNone, c.head_dim, c.ffn_dim,
-                         m->at(L.lm_head), s));
+  LOAD_HIP(repack(lm, c.vocab, d, kPermNone, L.lm_head));
   // RoPE table in fp64 on the host, stored as fp32: [pos][i] = cos / sin(pos * theta^(-2i/hd)).
   const int half = c.head_dim / 2;
   m->rope_host.resize((size_t)2 * c.max_ctx * half);
@@ -553,7 +561,6 @@ ll_status ll_model_load(const ll_config *cfg, const ll_weights *w, void *workspa
     }
   LOAD_HIP(hipMemcpyAsync(m->at(L.rcos), hc, (size_t)c.max_ctx * half * 4, hipMemcpyHostToDevice, s));
   LOAD_HIP(hipMemcpyAsync(m->at(L.rsin), hs, (size_t)c.max_ctx * half * 4, hipMemcpyHostToDevice, s));
-  LOAD_HIP(hipMemsetAsync(m->at(L.err), 0, 4, s));
   if (m->paged()) {
     const size_t entries = (size_t)c.max_batch * L.kv_max_pages;
     LOAD_HIP(hipMemsetAsync(m->at(L.kv_table), 0, entries * 4, s));
@@ -582,7 +589,7 @@ ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
                 "chunk extends the same sequences; ll_kv_reset starts new ones)", batch, m->batch);
   long total = 0;
   int n_qtiles = 0;
-  const int qtile = attn_prefill_qtile(c.dtype);
+  const int qtile = attn_prefill_qtile(compute_dtype(c));
   PrefillMeta pm;
   pm.batch = batch;
   for (int b = 0; b < batch; ++b) {
@@ -619,7 +626,7 @@ ll_status ll_prefill(ll_model *m, int32_t batch, const int32_t *seq_lens_host,
                              m->at<int>(L.kstart), m->at<int2>(L.qtiles), s,
                              L.sched ? m->at<int4>(L.sched) : nullptr, &as, c.n_kv_heads));
   m->mark(LL_K_EMBED);
-  LL_HIP(launch_embed(c.dtype, tokens_dev, T, m->at(L.embed), c.vocab, c.d_model,
+  LL_HIP(launch_embed(compute_dtype(c), tokens_dev, T, m->at(L.embed), c.vocab, c.d_model,
                       m->at<float>(L.x), m->at<int>(L.err), s));
   ll_status st = enqueue_layers(m, T, false, n_qtiles, s, nullptr, &as);
   if (st != LL_OK) return st;
@@ -826,7 +833,8 @@ void ll_model_free(ll_model *m) {
 // ----------------------------------------------------------------------------------------
 
 static ll_status check_dtype(int32_t dtype) {
-  if (dtype != LL_F32 && dtype != LL_BF16) return fail(LL_ERR_UNSUPPORTED, "dtype %d unknown", dtype);
+  if (dtype != LL_F32 && dtype != LL_BF16 && dtype != LL_F16)
+    return fail(LL_ERR_UNSUPPORTED, "dtype %d unknown", dtype);
   return LL_OK;
 }
 

@@ -39,6 +39,12 @@ constexpr size_t kAlign = 256;
 constexpr size_t kGuardBytes = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+// Operand type of a decoder's kernels: the storage dtype, or fp16 for bf16 weights with
+// f16_compute (converted at load).
+inline int compute_dtype(const ll_config &c) {
+  return c.dtype == LL_BF16 && c.f16_compute ? kF16 : c.dtype;
+}
+
 inline ll_status check_ws(const void *p) {
   if (!p) return fail(LL_ERR_WORKSPACE, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(p) % kAlign)

@@ -87,7 +87,7 @@ def judge(name: str, dtype: str, ref_logits: np.ndarray, gpu_logits: np.ndarray,
 
 
 def run_gpu_teacher_forced(cfg, weights, lens, packed, ref_tokens, n_decode, use_graph=True,
-                           options=None, paging=None):
+                           options=None, paging=None, f16_compute=None):
     """Prefill + n_decode teacher-forced steps through the C ABI, with the given ll_option
     values (name -> value) set after loading.
 
@@ -97,7 +97,7 @@ def run_gpu_teacher_forced(cfg, weights, lens, packed, ref_tokens, n_decode, use
     B = len(lens)
     dev_w = upload_weights(cfg, weights)
     model = Model(cfg, dev_w, max_batch=B, max_prefill_tokens=int(sum(lens)),
-                  max_ctx=int(max(lens)) + n_decode, **(paging or {}))
+                  max_ctx=int(max(lens)) + n_decode, f16_compute=f16_compute, **(paging or {}))
     del dev_w
     model.set_decode_graph(use_graph)
     for name, value in (options or {}).items():
@@ -187,6 +187,8 @@ def device_tensor(arr, dtype):
 def rounded(arr, dtype):
     """The values a tensor of `dtype` holds (fp32 numpy)."""
     a = np.asarray(arr, dtype=np.float32)
+    if dtype == "f16":
+        return a.astype(np.float16).astype(np.float32)
     return gen.round_to_bf16(a) if dtype == "bf16" else a
 
 

@@ -33,7 +33,7 @@ def _np(t):
     return t.float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
 @pytest.mark.parametrize("rows,d", [(1, 256), (5, 768), (3, 4096)])
 def test_rmsnorm(dtype, rows, d):
     from paper_2608_21836_amd.binding import op_rmsnorm
@@ -45,7 +45,8 @@ def test_rmsnorm(dtype, rows, d):
     y = op_rmsnorm(torch.from_numpy(x).cuda(), device_tensor(g, dtype), 1e-5)
     torch.cuda.synchronize()
     ref = oracle.rmsnorm(x, g, 1e-5)
-    tol = (2.0 ** -8 * np.abs(ref) + 1e-6) if dtype == "bf16" else (1e-5 * np.abs(ref) + 1e-7)
+    rel = {"bf16": 2.0 ** -8, "f16": 2.0 ** -11, "f32": 1e-5}[dtype]
+    tol = rel * np.abs(ref) + (1e-6 if dtype != "f32" else 1e-7)
     assert np.all(np.abs(_np(y) - ref) <= tol)
 
 
@@ -62,7 +63,7 @@ GEMM_SHAPES = [
 ]
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
 @pytest.mark.parametrize("path,m,n,k", GEMM_SHAPES)
 def test_gemm(dtype, path, m, n, k):
     from paper_2608_21836_amd.binding import op_gemm, op_repack
@@ -181,6 +182,9 @@ def _caches(rng, dtype, batch, hkv, max_ctx, hd, lens):
     return k, v
 
 
+# P and the output are rounded to the operand type: bf16 8-bit, fp16 11-bit significands
+ATTN_TOL = {"bf16": 4 * 2.0 ** -9, "f16": 4 * 2.0 ** -11, "f32": 1e-5}
+
 ATTN_CASES = [
     ("bf16", 64, 8, 2, [1, 63, 64, 65, 200]),
     ("bf16", 128, 4, 1, [130, 7]),
@@ -197,6 +201,10 @@ ATTN_CASES = [
     ("bf16", 128, 32, 8, [1500, 1, 700, 64]),
     ("bf16", 128, 8, 4, [129, 255, 2]),
     ("bf16", 128, 16, 4, [int(x) for x in np.random.default_rng(7).integers(1, 600, 20)]),
+    # fp16 operands (a bf16 model with f16_compute): both kernels
+    ("f16", 128, 32, 8, [1500, 1, 700, 64]),
+    ("f16", 64, 32, 4, [1024, 77, 1, 33]),
+    ("f16", 128, 4, 4, [1030]),
     ("f32", 64, 4, 4, [33, 1, 128]),
     ("f32", 128, 4, 2, [70]),
 ]
@@ -222,7 +230,7 @@ def test_attn_prefill(dtype, hd, hq, hkv, lens):
         vb = v[b, :, :L].transpose(1, 0, 2).astype(np.float64)
         pos = np.arange(L)
         ref = oracle.causal_gqa_attention(qb, kb, vb, pos, pos).reshape(L, hq * hd)
-        tol = (4 * 2.0 ** -9 if dtype == "bf16" else 1e-5) * np.abs(vb).max()
+        tol = ATTN_TOL[dtype] * np.abs(vb).max()
         assert np.all(np.abs(o[t0:t0 + L] - ref) <= tol), f"sequence {b}"
         t0 += L
 
@@ -235,6 +243,7 @@ CHUNK_CASES = [
     ("bf16", 64, 4, 4, [128], [512]),
     ("bf16", 64, 32, 4, [40, 1, 300], [1000, 5, 64]),
     ("bf16", 128, 32, 8, [65, 128], [63, 2000]),
+    ("f16", 128, 32, 8, [65, 128], [63, 2000]),
     ("f32", 64, 4, 4, [33, 1, 70], [31, 200, 64]),
     ("f32", 128, 4, 2, [65], [3]),
 ]
@@ -263,7 +272,7 @@ def test_attn_prefill_chunk(dtype, hd, hq, hkv, lens, cached):
         vb = v[b, :, :P0 + L].transpose(1, 0, 2).astype(np.float64)
         ref = oracle.causal_gqa_attention(qb, kb, vb, P0 + np.arange(L), np.arange(P0 + L))
         ref = ref.reshape(L, hq * hd)
-        tol = (4 * 2.0 ** -9 if dtype == "bf16" else 1e-5) * np.abs(vb).max()
+        tol = ATTN_TOL[dtype] * np.abs(vb).max()
         assert np.all(np.abs(o[t0:t0 + L] - ref) <= tol), f"sequence {b}"
         t0 += L
 
@@ -272,6 +281,7 @@ DEC_CASES = [
     ("bf16", 64, 8, 2, [1, 63, 64, 65, 257, 1000], 1024),
     ("bf16", 128, 32, 8, [4096, 17, 2049], 4224),
     ("bf16", 128, 16, 2, [300], 512),
+    ("f16", 128, 32, 8, [4096, 17, 2049], 4224),
     ("bf16", 64, 4, 4, [5, 640], 640),
     ("f32", 64, 4, 4, [48, 2], 48),
     ("f32", 128, 4, 1, [129], 200),
@@ -297,11 +307,11 @@ def test_attn_decode(dtype, hd, hq, hkv, lens, max_ctx):
         kb = k[b, :, :L].transpose(1, 0, 2).astype(np.float64)
         vb = v[b, :, :L].transpose(1, 0, 2).astype(np.float64)
         ref = oracle.causal_gqa_attention(qb, kb, vb, np.array([L - 1]), np.arange(L)).reshape(-1)
-        tol = (2 * 2.0 ** -9 if dtype == "bf16" else 1e-5) * np.abs(vb).max()
+        tol = ATTN_TOL[dtype] / 2 * np.abs(vb).max()
         assert np.all(np.abs(o[b] - ref) <= tol), f"sequence {b}"
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
 @pytest.mark.parametrize("rows,vocab,k", [(1, 1024, 256), (3, 4096, 768), (33, 32000, 512)])
 def test_lmhead_argmax(dtype, rows, vocab, k):
     from paper_2608_21836_amd.binding import op_lmhead_argmax, op_repack

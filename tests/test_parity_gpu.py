@@ -49,6 +49,25 @@ def test_workload_parity(name, n_decode):
     assert rep.ok(cfg.dtype), rep
 
 
+@pytest.mark.parametrize("name", ["t-gqa-hd64", "t-b32-hd128", "125m"])
+def test_bf16_operand_parity(name):
+    """The bf16-operand path (f16_compute = 0: activations, KV cache and MFMA operands in
+    bf16) against the oracle; the other parity tests run the default fp16 operands."""
+    cfg = get_config(name)
+    w = gen.weights(cfg)
+    lens, packed = gen.prompt_tokens(cfg)
+    ref_logits, ref_tokens = teacher_forced_run(OracleModel(cfg, w), lens, packed, cfg.n_decode)
+    gl, gt = run_gpu_teacher_forced(cfg, w, lens, packed, ref_tokens, cfg.n_decode,
+                                    f16_compute=False)
+    rep = judge(name, cfg.dtype, ref_logits, gl, gt)
+    log(f"parity bf16 operands {name}: rows={rep.rows} max_abs={rep.max_abs_err:.3e} "
+        f"worst_row_rel={rep.worst_rel_row_err:.3e} literal_mismatch={rep.literal_mismatches} "
+        f"unexplained={rep.unexplained_mismatches}")
+    for d in rep.details:
+        log("  " + d)
+    assert rep.ok(cfg.dtype), rep
+
+
 @pytest.mark.parametrize("name,n_chunks", [("t-gqa-hd128", 3), ("t-f32-ragged", 2),
                                             ("t-gqa-hd64-long", 2), ("125m", 3)])
 def test_chunked_prefill_parity(name, n_chunks):
