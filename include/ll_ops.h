@@ -116,6 +116,18 @@ ll_status ll_op_lmhead_argmax(int32_t dtype, int32_t rows, int32_t vocab, int32_
                               const void *h, const void *wt, float *logits, int32_t *next,
                               void *scratch, size_t scratch_bytes, void *stream);
 
+/* ll_op_lmhead_argmax for callers that cannot allocate: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation.  Same arguments, kernels and results,
+ * without the scratch: the per-block partials live in a static device array of 2 MiB that the
+ * library holds on each GPU it runs on until the process ends (its address is resolved once
+ * per device, on the first call with that device current).  rows * vocab / 32 <= 262144
+ * (LL_ERR_CAPACITY otherwise, nothing enqueued).  No allocation of any kind.  Every call on a
+ * GPU shares that GPU's array: calls that overlap on one GPU (other streams, other threads)
+ * race; each partial is written before it is read, so nothing needs clearing between calls. */
+ll_status ll_op_lmhead_argmax_noalloc(int32_t dtype, int32_t rows, int32_t vocab, int32_t k,
+                                      const void *h, const void *wt, float *logits,
+                                      int32_t *next, void *stream);
+
 /* Calibration, not part of the model: an MFMA-only loop (no memory traffic inside it) that
  * measures the bf16 matrix-core rate this GPU sustains, reported beside the datasheet peak.
  * blocks blocks of 4 waves; each wave runs iters x 8 v_mfma_f32_16x16x32_bf16, i.e.

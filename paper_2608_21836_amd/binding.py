@@ -161,6 +161,8 @@ SIGNATURES = [
     ("ll_op_attn_decode_scratch", c_size_t, [c_int32, c_int32, c_int32, c_int32, c_int32]),
     ("ll_op_lmhead_argmax", c_int32, [c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
                                       c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+    ("ll_op_lmhead_argmax_noalloc", c_int32, [c_int32, c_int32, c_int32, c_int32, c_void_p,
+                                              c_void_p, c_void_p, c_void_p, c_void_p]),
     ("ll_mamba_workspace_size", c_int32, [POINTER(LLMambaConfig), POINTER(c_size_t)]),
     ("ll_mamba_load", c_int32, [POINTER(LLMambaConfig), POINTER(LLMambaWeights), c_void_p,
                                 c_size_t, c_void_p, POINTER(c_void_p)]),
@@ -758,3 +760,14 @@ def op_lmhead_argmax(h, wt, vocab: int, want_logits: bool = True, stream=None):
                                               nbytes, _stream_handle(stream)), "ll_op_lmhead_argmax")
     return nxt, logits
 
+
+def op_lmhead_argmax_noalloc(h, wt, vocab: int, logits=None, nxt=None, stream=None):
+    """ll_op_lmhead_argmax_noalloc: the LM head with fused argmax, partials in the library's
+    static device array (nothing allocated by the library).  logits / nxt: caller tensors
+    (logits nullable)."""
+    rows, k = h.shape
+    _check(load_library().ll_op_lmhead_argmax_noalloc(_dt(h), rows, vocab, k, h.data_ptr(),
+                                                      wt.data_ptr(), _ptr(logits),
+                                                      nxt.data_ptr(), _stream_handle(stream)),
+           "ll_op_lmhead_argmax_noalloc")
+    return nxt, logits

@@ -20,7 +20,8 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["gemm.hip", "attention.hip", "elementwise.hip", "mamba.hip", "mamba2.hip", "rglru.hip",
-           "runtime.cpp", "mamba_runtime.cpp", "mamba2_runtime.cpp", "rglru_runtime.cpp"]
+           "noalloc.hip", "runtime.cpp", "mamba_runtime.cpp", "mamba2_runtime.cpp",
+           "rglru_runtime.cpp"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-I", INCLUDE, "-I", CSRC, "-Wno-unused-result"]
