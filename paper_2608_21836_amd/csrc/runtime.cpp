@@ -904,7 +904,9 @@ ll_status ll_op_gemm_swiglu(int32_t dtype, int32_t m, int32_t n, int32_t k, cons
 }
 
 size_t ll_op_gemm_prefill_splitk_scratch(int32_t dtype, int32_t m, int32_t n, int32_t k) {
-  if ((dtype != LL_F32 && dtype != LL_BF16) || m < 1 || n < 1 || k < 1 || k % 64) return 0;
+  if ((dtype != LL_F32 && dtype != LL_BF16 && dtype != LL_F16) || m < 1 || n < 1 || k < 1 ||
+      k % 64)
+    return 0;
   return prefill_splitk_plan(elem_bytes(dtype), m, n, k).ws_bytes;
 }
 ll_status ll_op_gemm_prefill_splitk(int32_t dtype, int32_t m, int32_t n, int32_t k,
@@ -930,7 +932,9 @@ ll_status ll_op_gemm_prefill_splitk(int32_t dtype, int32_t m, int32_t n, int32_t
 }
 
 size_t ll_op_gemm_splitk_scratch(int32_t dtype, int32_t m, int32_t n, int32_t k) {
-  if ((dtype != LL_F32 && dtype != LL_BF16) || m < 1 || n < 1 || k < 1 || k % 64) return 0;
+  if ((dtype != LL_F32 && dtype != LL_BF16 && dtype != LL_F16) || m < 1 || n < 1 || k < 1 ||
+      k % 64)
+    return 0;
   return splitk_plan(elem_bytes(dtype), m, n, k).ws_bytes;
 }
 

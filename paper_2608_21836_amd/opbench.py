@@ -11,8 +11,9 @@ this module times each hot-path kernel alone, on the shapes the five workloads r
               shapes: a reference for what this GPU reaches on the same products, not part of the
               path
 Each line: kernel, workload, shape, mean time per call, achieved rate and the fraction of the
-MI355X peak (HBM 8 TB/s; bf16 MFMA 2.5 PFLOP/s).  Inputs are random; only timing matters
-here (numerics are covered by tests/test_kernels_gpu.py).
+MI355X peak (HBM 8 TB/s; fp16 / bf16 MFMA 2.5 PFLOP/s).  Operands are fp16, as the decoder
+runs bf16 weights by default (--bf16 for bf16 operands).  Inputs are random; only timing
+matters here (numerics are covered by tests/test_kernels_gpu.py).
 
   python -m paper_2608_21836_amd.opbench [--only gemm,gemv,attn] [--workloads 7b-mha,8b-gqa]
 """
@@ -27,6 +28,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK = 8.0e12
+DT = None   # operand type (torch.float16 or torch.bfloat16), set in main
 MFMA_PEAK = 2.5e15
 
 
@@ -63,15 +65,15 @@ def bench_gemm(cfg, lens, iters):
     import torch
     from paper_2608_21836_amd.binding import op_gemm, op_gemm_swiglu, op_repack
     T = int(sum(lens))
-    a = (torch.randn(T, max(k for _, _, k in linear_shapes(cfg)), device="cuda") * 0.5).to(torch.bfloat16)
+    a = (torch.randn(T, max(k for _, _, k in linear_shapes(cfg)), device="cuda") * 0.5).to(DT)
     for name, n, k in linear_shapes(cfg):
         ak = a[:, :k].contiguous()
-        wt = op_repack((torch.randn(n, k, device="cuda") * 0.02).to(torch.bfloat16))
+        wt = op_repack((torch.randn(n, k, device="cuda") * 0.02).to(DT))
         c = torch.empty(T, n, device="cuda")
         us = _timeit(lambda i: op_gemm(0, ak, wt, n, c=c), iters)
         _line("prefill_gemm", cfg.name, f"{name} M={T} N={n} K={k}", us, 2.0 * T * n * k, "flop")
         if name == "gate_up":   # the workload's own epilogue: SwiGLU, act [M, F] in bf16
-            act = torch.empty(T, n // 2, dtype=torch.bfloat16, device="cuda")
+            act = torch.empty(T, n // 2, dtype=DT, device="cuda")
             us = _timeit(lambda i: op_gemm_swiglu(ak, wt, n, act=act), iters)
             _line("prefill_gemm_swiglu", cfg.name, f"{name} M={T} N={n} K={k}", us,
                   2.0 * T * n * k, "flop")
@@ -87,8 +89,8 @@ def bench_gemv(cfg, batch, iters):
     for name, n, k in linear_shapes(cfg):
         wbytes = n * k * 2
         reps = max(2, min(64, (1 << 30) // wbytes + 1))
-        wts = [op_repack((torch.randn(n, k, device="cuda") * 0.02).to(torch.bfloat16)) for _ in range(reps)]
-        a = torch.randn(batch, k, device="cuda").to(torch.bfloat16)
+        wts = [op_repack((torch.randn(n, k, device="cuda") * 0.02).to(DT)) for _ in range(reps)]
+        a = torch.randn(batch, k, device="cuda").to(DT)
         c = torch.zeros(batch, n, device="cuda")
         work = wbytes + batch * k * 2 + 2 * batch * n * 4
         us = _timeit(lambda i: op_gemm(1, a, wts[i % reps], n, c=c, accumulate=True), 3 * reps)
@@ -104,8 +106,8 @@ def bench_vendor(cfg, lens, iters):
     import torch
     M = int(sum(lens))
     for name, n, k in linear_shapes(cfg):
-        a = torch.randn(M, k, device="cuda").to(torch.bfloat16)
-        w = torch.randn(n, k, device="cuda").to(torch.bfloat16)
+        a = torch.randn(M, k, device="cuda").to(DT)
+        w = torch.randn(n, k, device="cuda").to(DT)
         us = _timeit(lambda i: torch.matmul(a, w.t()), iters)
         _line("vendor_gemm", cfg.name, f"{name} M={M} N={n} K={k}", us, 2.0 * M * n * k, "flop")
         del a, w
@@ -117,16 +119,16 @@ def bench_attn(cfg, lens, n_decode, iters):
     from paper_2608_21836_amd.binding import op_attn_decode, op_attn_prefill
     B, T, hd = len(lens), int(sum(lens)), cfg.head_dim
     max_ctx = max(lens) + n_decode
-    q = torch.randn(T, cfg.q_dim, device="cuda").to(torch.bfloat16)
-    kc = torch.randn(B, cfg.n_kv_heads, max_ctx, hd, device="cuda").to(torch.bfloat16)
-    vc = torch.randn(B, cfg.n_kv_heads, max_ctx, hd, device="cuda").to(torch.bfloat16)
+    q = torch.randn(T, cfg.q_dim, device="cuda").to(DT)
+    kc = torch.randn(B, cfg.n_kv_heads, max_ctx, hd, device="cuda").to(DT)
+    vc = torch.randn(B, cfg.n_kv_heads, max_ctx, hd, device="cuda").to(DT)
     us = _timeit(lambda i: op_attn_prefill(lens, q, kc, vc, cfg.n_heads, cfg.n_kv_heads, hd, max_ctx),
                  iters)
     flops = 2.0 * hd * cfg.n_heads * sum(x * (x + 1) for x in lens)
     _line("prefill_attention", cfg.name, f"B={B} T={T} H={cfg.n_heads}/{cfg.n_kv_heads}x{hd}", us,
           flops, "flop")
     ctx = torch.tensor([x + n_decode // 2 for x in lens], dtype=torch.int32, device="cuda")
-    qd = torch.randn(B, cfg.q_dim, device="cuda").to(torch.bfloat16)
+    qd = torch.randn(B, cfg.q_dim, device="cuda").to(DT)
     us = _timeit(lambda i: op_attn_decode(qd, kc, vc, ctx, cfg.n_heads, cfg.n_kv_heads, hd, max_ctx),
                  iters * 10)
     kv = sum(x + n_decode // 2 for x in lens) * 2 * cfg.kv_dim * 2 + B * cfg.q_dim * 2
@@ -139,8 +141,11 @@ def main() -> int:
     ap.add_argument("--only", default="gemm,gemv,attn")
     ap.add_argument("--workloads", default="1b-gqa,7b-mha,8b-gqa")
     ap.add_argument("--iters", type=int, default=5)
+    ap.add_argument("--bf16", action="store_true", help="bf16 operands instead of fp16")
     args = ap.parse_args()
     import torch
+    global DT
+    DT = torch.bfloat16 if args.bf16 else torch.float16
     from synth import gen, get_config
     kinds = set(args.only.split(","))
     torch.cuda.set_device(0)
