@@ -4,9 +4,11 @@
 //    stored in MFMA operand order, all tiles of a 16-row block contiguous along K.  A wave
 //    then fetches an operand with one fully coalesced 1 KiB read and LDS reads are
 //    conflict-free.
-//  * Prefill (M = prompt tokens): 256 x 256, 128 x 256 or 64 x 128 block tiles streamed into
-//    LDS through a 4-stage ring, v_mfma_f32_16x16x32_bf16 (fp32 workloads:
-//    v_mfma_f32_16x16x4_f32); short prompts split K over blocks.
+//  * Prefill (M = prompt tokens): 256 x 256 or 128 x 256 block tiles for 16-bit operands
+//    (k_gemm_pp: whole-cache-line loads into LDS rings, two wave groups in a ping-pong of
+//    memory and MFMA phases, v_mfma_f32_16x16x32), 256 x 256, 128 x 256 or 64 x 128 tiles
+//    through a 4-stage ring otherwise (k_gemm_big; fp32 workloads: v_mfma_f32_16x16x4_f32);
+//    short prompts split K over blocks.
 //  * Decode (M = batch <= 32 per launch): every weight byte is read once straight from HBM
 //    into MFMA B operands (non-temporal), A comes from L2; 8 waves split K, reduced in LDS.
 //  * Output columns come in units of 32 = two halves of 16 that land in the same lane, so the
@@ -600,6 +602,181 @@ __global__ __launch_bounds__(BN * 2, 1) void k_gemm_big(const T *__restrict__ A,
 }
 
 // ------------------------------------------------------------------------------------------
+// Large prefill GEMM for 16-bit operands: BM x 256 block tiles (BM = 256 or 128), 8 waves of
+// BM / 2 x 64, v_mfma_f32_16x16x32, in a ping-pong schedule.
+//  * Loads.  The texture path spends its time per cache line touched, so a load instruction
+//    is cheapest when its 64 lanes cover whole 128-byte lines.  A W tile (1 KiB, contiguous)
+//    does; a 16-row x 32-element A tile would touch 16 half lines.  A is therefore staged 64
+//    k-elements (one line per row) at a time: an instruction loads 8 whole rows, lane l
+//    taking 16-byte chunk (l % 8) ^ ((r / 2) % 8) of row r = l / 8 (+ 8) of a 16-row block,
+//    which lands at byte 16 l of the instruction's 1 KiB.  Row r of the block thus holds its
+//    chunk c at 16-byte slot 8 r + (c ^ ((r / 2) % 8)): the MFMA fragment reads (16 rows, one
+//    chunk) hit 16 distinct 16-byte bank groups.  W keeps one 32-element tile per stage.
+//    Rings: A 3 x (BM x 64), W 4 x (256 x 32) (160 KiB at BM = 256).  At k-step s (32
+//    elements) every wave issues its share of the W tiles of step s + 3 and of half s % 2 of
+//    the A panel s / 2 + 2.
+//  * Schedule: the two wave groups (wm = 0, 1; wave w runs on SIMD w % 4, so every SIMD holds
+//    one wave of each) alternate between a memory phase (fragments of step s from LDS,
+//    loads) and a compute phase (all MFMAs of step s, at raised priority), half a step apart:
+//    group 1 passes one extra barrier first.  While one wave of a SIMD runs its MFMAs back to
+//    back, the other issues its LDS reads and loads.
+//  * Ordering: before the barrier that ends its memory phase a wave finishes its LDS reads
+//    (lgkmcnt 0) and confirms that its loads issued two or more steps earlier have landed
+//    (vmcnt: every step issues the same number); a stage is refilled only after the memory
+//    phases that last read it (both groups') have ended at a barrier.
+// Blocks walk the same XCD-aware tile order as k_gemm_big.  K is a multiple of 64.
+// ------------------------------------------------------------------------------------------
+template <typename T, typename Epi, int BM>
+__global__ __launch_bounds__(512, 1) void k_gemm_pp(const T *__restrict__ A, int lda,
+                                                   const uint8_t *__restrict__ Wt, int M, int N,
+                                                   int K, Epi epi) {
+  using F = typename Frag<T>::type;
+  static_assert(sizeof(T) == 2, "16-bit operands");
+  constexpr int BN = 256, TK = 32, GM = 4;
+  constexpr int NA = BM / 16;       // 16-row blocks of the block tile
+  constexpr int NB = BN / 16;       // 16-column W tiles per k-step
+  constexpr int NI = BM / 32;       // 16-row blocks per wave
+  constexpr int AW = NA / 8;        // A instructions (1 KiB) per wave per k-step
+  constexpr int WW = NB / 8;        // W instructions per wave per k-step
+  constexpr int LPW = AW + WW;      // loads per wave per k-step
+  constexpr int ASTAGE = NA * 128;  // uint4 per A stage (BM rows x 64 elements)
+  constexpr int WSTAGE = NB * 64;   // uint4 per W stage
+  static_assert(NA % 8 == 0, "an A panel splits evenly over 8 waves and two k-steps");
+  __shared__ uint4 smem[3 * ASTAGE + 4 * WSTAGE];
+  uint4 *const sA = smem;
+  uint4 *const sW = smem + 3 * ASTAGE;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave / 4, wn = wave % 4;
+  const int ntm = (M + BM - 1) / BM, ntn = N / BN;
+  const int t = xcd_remap(blockIdx.x, ntm * ntn);
+  const int group = t / (GM * ntn), first_m = group * GM;
+  const int gsize = min(ntm - first_m, GM);
+  const int tm = first_m + (t % (GM * ntn)) % gsize, tn = (t % (GM * ntn)) / gsize;
+  const int m0 = tm * BM, n0 = tn * BN;
+  if constexpr (GroupA<Epi>::value) A += epi.a_off(n0);
+  const int nsteps = K / TK, npanels = nsteps / 2;
+
+  // A instruction q (0 .. 2 NA - 1) of a panel covers rows 8 q .. 8 q + 7 of the block tile
+  // (16-row block q / 2, half q % 2); k-step parity p issues q = p NA + AW wave + i.
+  const T *asrc[2][AW];
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+#pragma unroll
+    for (int i = 0; i < AW; ++i) {
+      const int q = p * NA + AW * wave + i, r = 8 * (q & 1) + (lane >> 3);
+      const int row = min(m0 + 16 * (q >> 1) + r, M - 1);
+      asrc[p][i] = A + (size_t)row * lda + 8 * ((lane & 7) ^ ((r >> 1) & 7));
+    }
+  const uint8_t *wsrc[WW];
+#pragma unroll
+  for (int i = 0; i < WW; ++i)
+    wsrc[i] = Wt + ((size_t)(n0 / 16 + WW * wave + i) * nsteps * 64 + lane) * 16;
+  auto load_w = [&](int step, int stage) {
+    const int st = min(step, nsteps - 1);
+#pragma unroll
+    for (int i = 0; i < WW; ++i)
+      load_tile_to_lds(wsrc[i] + (size_t)st * 1024, &sW[stage * WSTAGE + (WW * wave + i) * 64]);
+  };
+  auto load_a = [&](int panel, int p) {
+    const int pn = min(panel, npanels - 1);
+#pragma unroll
+    for (int i = 0; i < AW; ++i)
+      load_tile_to_lds(asrc[p][i] + (size_t)pn * 64,
+                       &sA[(panel % 3) * ASTAGE + (p * NA + AW * wave + i) * 64]);
+  };
+  // Steps and panels past the end reload the last ones (never read), so that every step
+  // issues the same number of loads and the vmcnt arithmetic stays fixed.
+  load_w(0, 0);
+  load_w(1, 1);
+  load_w(2, 2);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    load_a(j, 0);
+    load_a(j, 1);
+  }
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  // fragment slots: lane l reads row l % 16 of a 16-row block, chunk 4 kc + l / 16
+  const int r16 = lane & 15;
+  const int aoff0 = 8 * r16 + ((lane >> 4) ^ ((r16 >> 1) & 7));
+  const int aoff1 = 8 * r16 + ((4 + (lane >> 4)) ^ ((r16 >> 1) & 7));
+  f32x4 acc[NI][4];
+#pragma unroll
+  for (int i = 0; i < NI; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (wm == 1) asm volatile("s_barrier" ::: "memory");
+  F fa[NI], fb[4];
+  for (int s = 0; s < nsteps; ++s) {
+    __builtin_amdgcn_sched_barrier(0);
+    const int panel = s >> 1;
+    const uint4 *pa = &sA[(panel % 3) * ASTAGE + wm * NI * 128 + ((s & 1) ? aoff1 : aoff0)];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) fa[i] = *reinterpret_cast<const F *>(&pa[i * 128]);
+    const uint4 *pw = &sW[(s & 3) * WSTAGE + wn * 4 * 64 + lane];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) fb[j] = *reinterpret_cast<const F *>(&pw[j * 64]);
+    load_w(s + 3, (s + 3) & 3);
+    load_a(panel + 2, s & 1);
+    wait_vmcnt<2 * LPW>();
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = mma_chunk(fa[i], fb[j], acc[i][j]);
+    __builtin_amdgcn_s_setprio(0);
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_barrier" ::: "memory");
+  }
+  if (wm == 0) asm volatile("s_barrier" ::: "memory");
+  wait_vmcnt<0>();
+
+  const int ubase = (n0 + wn * 64) >> 5;
+  if constexpr (Epi::kVec8) {
+    // Each 16 x 64 block of the wave's accumulators goes through a wave-private LDS scratch
+    // (the rings are free once every wave has passed the barrier) and is read back row-wise:
+    // lane l takes row l / 4 and eight consecutive columns of both halves of one 32-column
+    // unit, so the epilogue loads and stores 16 bytes at a time.
+    constexpr int LD = 68;  // row stride in floats (a 16-float skew between the 4-row groups)
+    static_assert(8 * 16 * LD * 4 <= (int)sizeof(smem), "epilogue scratch fits in the rings");
+    __syncthreads();
+    float *sc = reinterpret_cast<float *>(smem) + wave * (16 * LD);
+    const int rho = lane >> 2, u = (lane >> 1) & 1, c0 = 8 * (lane & 1);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sc[(4 * (lane >> 4) + r) * LD + 16 * j + (lane & 15)] = acc[i][j][r];
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      const float4 *f0 = reinterpret_cast<const float4 *>(sc + rho * LD + 32 * u + c0);
+      const float4 *f1 = reinterpret_cast<const float4 *>(sc + rho * LD + 32 * u + 16 + c0);
+      const float4 a0 = f0[0], a1 = f0[1], b0 = f1[0], b1 = f1[1];
+      const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+      const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+      const int m = m0 + wm * (BM / 2) + i * 16 + rho;
+      if (m < M) epi.vec8(m, ubase + u, c0, av, bv);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + wm * (BM / 2) + i * 16 + (lane >> 4) * 4 + r;
+        if (m < M) {
+#pragma unroll
+          for (int p = 0; p < 2; ++p) epi(m, ubase + p, lane & 15, acc[i][2 * p][r], acc[i][2 * p + 1][r]);
+        }
+      }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
 // Decode GEMM: one block per NB x 16 output columns (NB = 2: one 32-column pair unit; NB = 1:
 // a single 16-column block, for element-wise epilogues when pairs would leave CUs idle), 8
 // waves splitting K, partial sums reduced through LDS.  Each wave requests U weight tiles per
@@ -1030,13 +1207,21 @@ hipError_t run_tiled(const void *a, int lda, const void *wt, int m, int n, int k
   const T *ap = reinterpret_cast<const T *>(a);
   const uint8_t *wp = reinterpret_cast<const uint8_t *>(wt);
   if (n % 256 == 0 && big_tiles >= min_tiles && !prefer_half && tile != kTile128x256) {
-    LL_LAUNCH((k_gemm_big<T, Epi, 256, 256>), dim3(big_tiles), dim3(512), 0, s, ap, lda, wp, m,
-              n, k, kt, epi);
+    if constexpr (sizeof(T) == 2)
+      LL_LAUNCH((k_gemm_pp<T, Epi, 256>), dim3(big_tiles), dim3(512), 0, s, ap, lda, wp, m, n, k,
+                epi);
+    else
+      LL_LAUNCH((k_gemm_big<T, Epi, 256, 256>), dim3(big_tiles), dim3(512), 0, s, ap, lda, wp, m,
+                n, k, kt, epi);
     return hipGetLastError();
   }
   if (n % 256 == 0 && half_tiles >= min_tiles && tile != kTileMid) {
-    LL_LAUNCH((k_gemm_big<T, Epi, 128, 256>), dim3(half_tiles), dim3(512), 0, s, ap, lda, wp, m,
-              n, k, kt, epi);
+    if constexpr (sizeof(T) == 2)
+      LL_LAUNCH((k_gemm_pp<T, Epi, 128>), dim3(half_tiles), dim3(512), 0, s, ap, lda, wp, m, n, k,
+                epi);
+    else
+      LL_LAUNCH((k_gemm_big<T, Epi, 128, 256>), dim3(half_tiles), dim3(512), 0, s, ap, lda, wp, m,
+                n, k, kt, epi);
     return hipGetLastError();
   }
   // Short prompts: 64 x 128 tiles; when even those are too few to fill the CUs, K is split
