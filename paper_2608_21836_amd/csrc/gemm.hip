@@ -617,9 +617,11 @@ __global__ __launch_bounds__(BN * 2, 1) void k_gemm_big(const T *__restrict__ A,
 //    the A panel s / 2 + 2.
 //  * Schedule: the two wave groups (wm = 0, 1; wave w runs on SIMD w % 4, so every SIMD holds
 //    one wave of each) alternate between a memory phase (fragments of step s from LDS,
-//    loads) and a compute phase (all MFMAs of step s, at raised priority), half a step apart:
-//    group 1 passes one extra barrier first.  While one wave of a SIMD runs its MFMAs back to
-//    back, the other issues its LDS reads and loads.
+//    loads) and a compute phase (all MFMAs of step s), half a step apart: group 1 passes one
+//    extra barrier first.  While one wave of a SIMD runs its MFMAs back to back, the other
+//    issues its LDS reads and loads.  (Raising the compute wave's priority with s_setprio
+//    measured 1-2 % slower; reading the next step's fragments inside the compute phase,
+//    10 % slower.)
 //  * Ordering: before the barrier that ends its memory phase a wave finishes its LDS reads
 //    (lgkmcnt 0) and confirms that its loads issued two or more steps earlier have landed
 //    (vmcnt: every step issues the same number); a stage is refilled only after the memory
@@ -709,28 +711,32 @@ __global__ __launch_bounds__(512, 1) void k_gemm_pp(const T *__restrict__ A, int
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (wm == 1) asm volatile("s_barrier" ::: "memory");
   F fa[NI], fb[4];
-  for (int s = 0; s < nsteps; ++s) {
+  // one k-step; P = s % 2 (the A chunk within the panel and the half of the panel to load)
+  auto step = [&](int s, auto P) {
+    constexpr int p = decltype(P)::value;
     __builtin_amdgcn_sched_barrier(0);
     const int panel = s >> 1;
-    const uint4 *pa = &sA[(panel % 3) * ASTAGE + wm * NI * 128 + ((s & 1) ? aoff1 : aoff0)];
+    const uint4 *pa = &sA[(panel % 3) * ASTAGE + wm * NI * 128 + (p ? aoff1 : aoff0)];
 #pragma unroll
     for (int i = 0; i < NI; ++i) fa[i] = *reinterpret_cast<const F *>(&pa[i * 128]);
     const uint4 *pw = &sW[(s & 3) * WSTAGE + wn * 4 * 64 + lane];
 #pragma unroll
     for (int j = 0; j < 4; ++j) fb[j] = *reinterpret_cast<const F *>(&pw[j * 64]);
     load_w(s + 3, (s + 3) & 3);
-    load_a(panel + 2, s & 1);
+    load_a(panel + 2, p);
     wait_vmcnt<2 * LPW>();
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int i = 0; i < NI; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = mma_chunk(fa[i], fb[j], acc[i][j]);
-    __builtin_amdgcn_s_setprio(0);
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_barrier" ::: "memory");
+  };
+  for (int s = 0; s < nsteps; s += 2) {   // nsteps is even
+    step(s, std::integral_constant<int, 0>());
+    step(s + 1, std::integral_constant<int, 1>());
   }
   if (wm == 0) asm volatile("s_barrier" ::: "memory");
   wait_vmcnt<0>();
