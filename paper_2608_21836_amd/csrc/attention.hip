@@ -144,14 +144,61 @@ __global__ __launch_bounds__(256) void k_attn_prefill(
   }
 }
 
-// One 64-key tile of bf16 prefill attention for one wave of 32 queries (lane l owns query
-// qw + l % 32), on v_mfma_f32_32x32x16_bf16, from an LDS stage `st` that holds the tile's K in
-// operand order ([32-key block][16-dim step] tiles of 64 x 16 B) followed by its V^T
-// ([32-dim block][16-key step] tiles, keys in the order the score registers hold them).
+// V tile of a stage: the tile's 64 keys as natural [key][dim] rows, DMA'd straight from the
+// cache like K, with the 16-byte chunks of each row XOR-swizzled: chunk c of row k sits at
+// slot c ^ vswz(k).  The transposed fragment reads of the P V product (below) then hit 64
+// distinct banks per 32 lanes.
+template <int HD> __device__ __forceinline__ constexpr int vswz(int row) {
+  return 4 * ((row / (128 / HD)) % (HD / 32));
+}
+
+// DMA instruction q of a stage's V tile (HD / 8 of them per 64 keys): lane l fills slot
+// (64 q + l) % (HD / 8) of row (64 q + l) / (HD / 8); rows past the sequence read the last key
+// (their probabilities are 0).  `tb` is the cache offset of the tile's first key.
+template <typename H, int HD>
+__device__ __forceinline__ void v_issue(const H *Vc, size_t tb, int kt, int KL, int q, int lane,
+                                        uint4 *vstage) {
+  constexpr int SPR = HD / 8;
+  const int idx = 64 * q + lane, row = idx / SPR, slot = idx % SPR;
+  const int key = min(kt * 64 + row, KL - 1);
+  load_tile_to_lds(Vc + tb + (size_t)(key - kt * 64) * HD + 8 * (slot ^ vswz<HD>(row)),
+                   &vstage[64 * q]);
+}
+
+// Byte offsets, within a V tile, of lane l's transposed reads for 32-dim block d (key step 0,
+// first half).  ds_read_b64_tr_b16 (measured on gfx950): in each group of 16 lanes, lane
+// 4 r + c supplies the address of 4 consecutive 16-bit elements, and lane j receives element
+// j % 4 of the elements of lanes 4 r + j / 4, r = 0..3.  Lane 4 r + c of group G therefore
+// points at key row 4 (G / 2) + r, dims 32 d + 16 (G % 2) + 4 c: lane j of the group gets
+// dim 32 d + 16 (G % 2) + j of four consecutive keys, which is the A operand of V^T P^T with
+// the keys in the order the score registers hold them (4 (l / 32) + e, then 8 + 4 (l / 32) + e).
+template <int HD>
+__device__ __forceinline__ void v_tr_offsets(int lane, int *voff) {
+  const int G = lane >> 4, j = lane & 15, r = j >> 2, c = j & 3;
+  const int row = 4 * (G >> 1) + r, x = vswz<HD>(row) / 4;
+#pragma unroll
+  for (int d = 0; d < HD / 32; ++d)
+    voff[d] = row * HD * 2 + (4 * (d ^ x) + 2 * (G & 1) + (c >> 1)) * 16 + 8 * (c & 1);
+}
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+template <typename V, int HD>
+__device__ __forceinline__ V v_frag_tr(const char *vtile, int off) {
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(vtile + off));
+  const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(vtile + off + 8 * HD * 2));
+  return __builtin_bit_cast(V, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// One 64-key tile of 16-bit prefill attention for one wave of 32 queries (lane l owns query
+// qw + l % 32), on v_mfma_f32_32x32x16, from an LDS stage `st` that holds the tile's K in
+// operand order ([32-key block][16-dim step] tiles of 64 x 16 B) followed by its V tile
+// (natural rows, swizzled; voff from v_tr_offsets).
 //   S^T = K Q^T: A = K rows from LDS, B = the wave's Q^T fragments (registers).  Lane l holds,
 //     of each 32-key block, rows 8 (i / 4) + 4 (l / 32) + i % 4: the online-softmax
 //     statistics need one exchange with lane l ^ 32.
-//   O^T += V^T P^T: B = P^T straight from the score registers.
+//   O^T += V^T P^T: A = V^T by transposed LDS reads, B = P^T straight from the score registers.
 // The causal / length mask runs only on tiles that reach past the wave's first query; the
 // accumulator is rescaled only when some row maximum grew (otherwise every factor is 1).
 template <typename H, int HD>
@@ -159,19 +206,36 @@ __device__ __forceinline__ void attn_tile16(const uint4 *__restrict__ st,
                                             const typename Frag<H>::type *qf,
                                                f32x16 *acc, float &m_run, float &l_run, int kt,
                                                int P0, int L, int qw, int my_q, bool q_ok,
-                                               float scale_log2, int lane) {
+                                               float scale_log2, int lane, const int *voff) {
   using V = typename Frag<H>::type;
   constexpr int BKV = 64, NKC = HD / 16, NDB = HD / 32, NPC = BKV / 16, KTILES = 2 * NKC;
   const int g = lane >> 5;
+  // All K fragments of the tile are requested before the first MFMA, and the two 32-key
+  // chains alternate, so neither LDS latency nor MFMA result latency sits between MFMAs.
+  V kf[2][NKC];
+#pragma unroll
+  for (int c = 0; c < NKC; ++c)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) kf[kb][c] = *reinterpret_cast<const V *>(&st[(kb * NKC + c) * 64 + lane]);
+  __builtin_amdgcn_sched_barrier(0);
   f32x16 sc[2];
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
+  for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int i = 0; i < 16; ++i) sc[kb][i] = 0.f;
 #pragma unroll
-    for (int c = 0; c < NKC; ++c)
-      sc[kb] = mma32(*reinterpret_cast<const V *>(&st[(kb * NKC + c) * 64 + lane]), qf[c], sc[kb]);
-  }
+  for (int c = 0; c < NKC; ++c)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) sc[kb] = mma32(kf[kb][c], qf[c], sc[kb]);
+  __builtin_amdgcn_sched_barrier(0);
+  // The V^T fragments of the tile are requested now; the softmax below covers their latency.
+  const char *vt = reinterpret_cast<const char *>(st + KTILES * 64);
+  V vf[NPC][NDB];
+#pragma unroll
+  for (int c = 0; c < NPC; ++c)
+#pragma unroll
+    for (int d = 0; d < NDB; ++d) vf[c][d] = v_frag_tr<V, HD>(vt, voff[d] + 16 * c * HD * 2);
+  __builtin_amdgcn_sched_barrier(0);
   if (kt * BKV + BKV - 1 > P0 + qw || qw + 31 >= L) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -213,8 +277,7 @@ __device__ __forceinline__ void attn_tile16(const uint4 *__restrict__ st,
 #pragma unroll
     for (int e = 0; e < 8; ++e) pf[e] = static_cast<H>(sc[c / 2][8 * (c % 2) + e]);
 #pragma unroll
-    for (int d = 0; d < NDB; ++d)
-      acc[d] = mma32(*reinterpret_cast<const V *>(&st[(KTILES + d * NPC + c) * 64 + lane]), pf, acc[d]);
+    for (int d = 0; d < NDB; ++d) acc[d] = mma32(vf[c][d], pf, acc[d]);
   }
 }
 
@@ -237,47 +300,11 @@ __device__ __forceinline__ void attn_store16(H *dst, const f32x16 *acc, float in
     }
 }
 
-// V^T task of one lane: 8 keys x 8 dims of a 64-key tile (dims 8 dg .. 8 dg + 7, 16-key step
-// pc, key group gg; element e < 4 is key 16 pc + 4 gg + e, e >= 4 is key 16 pc + 8 + 4 gg + e - 4),
-// loaded as 8 rows of 16 B (rows past the sequence read clamped, in bounds, and replaced by
-// zeros: their probabilities are 0 and the cache there may hold anything, NaN included) ...
-template <typename H, int HD>
-__device__ __forceinline__ void vt_load(uint4 *vr, const H *Vc, size_t tb, int kt, int KL,
-                                        int task) {
-  constexpr int NPC = 4;
-  const int dg = task % (HD / 8), pc = (task / (HD / 8)) % NPC, gg = task / (HD / 8 * NPC);
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int key = kt * 64 + 16 * pc + (e < 4 ? 4 * gg + e : 8 + 4 * gg + e - 4);
-    const uint4 v = *reinterpret_cast<const uint4 *>(Vc + tb + (size_t)(min(key, KL - 1) - kt * 64) * HD + 8 * dg);
-    vr[e] = key < KL ? v : make_uint4(0, 0, 0, 0);
-  }
-}
-// ... and written transposed: 8 fragments of 8 keys, one per dim, into the stage's V^T tiles.
-template <int HD>
-__device__ __forceinline__ void vt_store(uint4 *stage, const uint4 *vr, int task) {
-  constexpr int NPC = 4, KTILES = 2 * (HD / 16);
-  const int dg = task % (HD / 8), pc = (task / (HD / 8)) % NPC, gg = task / (HD / 8 * NPC);
-#pragma unroll
-  for (int t = 0; t < 8; ++t) {
-    uint32_t d[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t lo = reinterpret_cast<const uint32_t *>(&vr[2 * j])[t >> 1];
-      const uint32_t hi = reinterpret_cast<const uint32_t *>(&vr[2 * j + 1])[t >> 1];
-      d[j] = (t & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
-    }
-    const int dim = 8 * dg + t;
-    stage[(KTILES + (dim / 32) * NPC + pc) * 64 + (dim % 32) + 32 * gg] = make_uint4(d[0], d[1], d[2], d[3]);
-  }
-}
-
-// bf16 prefill attention, one query head per block (the MHA workloads): one block per
+// 16-bit prefill attention, one query head per block (the MHA workloads): one block per
 // (128-query tile, query head), 4 waves of 32 queries, key tiles of 64 through a
-// double-buffered LDS stage.  K tiles are DMA'd from the cache straight into LDS in operand
-// order (global_load_lds); two waves build the V^T tiles (each lane loads 8 keys x 8 dims,
-// transposes them in registers and writes 8 x 16 B), the other two issue the K loads.  Loads
-// for tile t + 1 are in flight while tile t computes (attn_tile_bf16).
+// double-buffered LDS stage.  K (operand order) and V (natural rows, swizzled) are DMA'd from
+// the cache straight into LDS (global_load_lds), the work split evenly over the 4 waves; the
+// loads for tile t + 1 are in flight while tile t computes (attn_tile16).
 template <typename H, int HD>
 __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
     const H *__restrict__ Q, int ldq, const H *__restrict__ Kc, const H *__restrict__ Vc,
@@ -285,16 +312,12 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
     const int2 *__restrict__ qtiles, int hq, int hkv, int max_ctx, float scale_log2,
     KvPaging pg) {
   constexpr int QT = kAttnQTileWide, BKV = 64;
-  constexpr int NKC = HD / 16;           // 16-dim steps of S^T
-  constexpr int NDB = HD / 32;           // 32-dim output blocks
-  constexpr int NPC = BKV / 16;          // 16-key steps of P V
-  constexpr int KTILES = 2 * NKC;        // K tiles per stage: [32-key block][16-dim step]
-  constexpr int VTILES = NDB * NPC;      // V^T tiles per stage: [dim block][key step]
-  constexpr int STAGE = (KTILES + VTILES) * 64;  // uint4 per stage
-  constexpr int NVT = (HD / 8) * NPC * 2;        // V^T build tasks per stage, one per lane
-  constexpr int VW = NVT / 64;                   // waves building V^T
-  constexpr int KW = 4 - VW;                     // waves loading K
-  static_assert(QT == 128 && VW >= 1 && KW >= 1, "4 waves of 32 queries");
+  constexpr int NKC = HD / 16;                 // 16-dim steps of S^T
+  constexpr int NDB = HD / 32;                 // 32-dim output blocks
+  constexpr int KTILES = 2 * NKC;              // K tiles per stage: [32-key block][16-dim step]
+  constexpr int VINS = BKV * HD * 2 / 1024;    // 1 KiB DMA instructions of a V tile
+  constexpr int STAGE = (KTILES + VINS) * 64;  // uint4 per stage
+  static_assert(QT == 128 && KTILES % 4 == 0 && VINS % 4 == 0, "4 waves of 32 queries");
   __shared__ uint4 smem[2 * STAGE];
 
   const int2 qt = qtiles[blockIdx.x];
@@ -322,46 +345,38 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[d][i] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
+  int voff[NDB];
+  v_tr_offsets<HD>(lane, voff);
 
   const int ntiles = (P0 + min(q0 + QT, L) - 1) / BKV + 1;
 
   // K tile (kb, c): lane l reads key 32 kb + l % 32 (clamped into the sequence; rows past KL
   // are masked), dims 16 c + 8 g.  A tile's keys lie in one page (tiles start at cached
   // positions and the clamp stays in the tile), so one base per tile serves every row.
-  auto k_issue = [&](int kt, int buf) {
-    if (wave >= VW) {
-      const size_t tb = kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD);
-      for (int ti = wave - VW; ti < KTILES; ti += KW) {
-        const int kb = ti / NKC, c = ti % NKC;
-        const int key = min(kt * BKV + 32 * kb + (lane & 31), KL - 1);
-        load_tile_to_lds(Kc + tb + (size_t)(key - kt * BKV) * HD + 16 * c + 8 * g,
-                         &smem[buf * STAGE + ti * 64]);
-      }
+  auto issue = [&](int kt, int buf) {
+    const size_t tb = kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD);
+#pragma unroll
+    for (int i = 0; i < KTILES / 4; ++i) {
+      const int ti = wave + 4 * i, kb = ti / NKC, c = ti % NKC;
+      const int key = min(kt * BKV + 32 * kb + (lane & 31), KL - 1);
+      load_tile_to_lds(Kc + tb + (size_t)(key - kt * BKV) * HD + 16 * c + 8 * g,
+                       &smem[buf * STAGE + ti * 64]);
     }
-  };
-  uint4 vr[8];
-  auto v_load = [&](int kt) {
-    if (wave < VW) vt_load<H, HD>(vr, Vc, kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD), kt, KL, tid);
-  };
-  auto v_store = [&](int buf) {
-    if (wave < VW) vt_store<HD>(&smem[buf * STAGE], vr, tid);
+#pragma unroll
+    for (int i = 0; i < VINS / 4; ++i)
+      v_issue<H, HD>(Vc, tb, kt, KL, wave + 4 * i, lane, &smem[buf * STAGE + KTILES * 64]);
   };
 
-  k_issue(0, 0);
-  v_load(0);
-  v_store(0);
+  issue(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   for (int kt = 0; kt < ntiles; ++kt) {
     const int cur = kt & 1;
-    const bool more = kt + 1 < ntiles;
-    if (more) {
-      k_issue(kt + 1, cur ^ 1);
-      v_load(kt + 1);
-    }
+    if (kt + 1 < ntiles) issue(kt + 1, cur ^ 1);
     if (qw < L && kt * BKV <= P0 + qw + 31)  // else nothing for this wave in this tile
       attn_tile16<H, HD>(&smem[cur * STAGE], qf, acc, m_run, l_run, kt, P0, L, qw, my_q, q_ok,
-                         scale_log2, lane);
-    if (more) v_store(cur ^ 1);
+                         scale_log2, lane, voff);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
 
@@ -369,15 +384,13 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
   if (q_ok) attn_store16<H, HD>(O + (size_t)(tok0 + my_q) * ldo + h * HD, acc, 1.0f / l_run, g);
 }
 
-// bf16 prefill attention for grouped heads (group G = H_q / H_kv >= 2), after the paper's
+// 16-bit prefill attention for grouped heads (group G = H_q / H_kv >= 2), after the paper's
 // prefill kernel that shares KV loads according to the head grouping (appendix "Deployment
 // Kernel Families", Table A.4): one block of 8 waves per (query tile, KV head) holds every
 // query head of the group -- wave w takes head kvh G + w / QB and 32 queries of block w % QB
 // (QB = 8 / G; tiles of 32 QB queries) -- so each 64-key K / V tile is read from memory and
-// staged in LDS once for G heads.  All 8 waves DMA the K tiles; the V^T builder role (HD / 64
-// waves' worth of lanes) rotates over the waves from tile to tile so that no wave carries it
-// every time.  Blocks take their (sequence, query tile, KV head) from the work list in
-// XCD-owned ranges (AttnSched).
+// staged in LDS once for G heads.  The 8 waves share the K and V DMA evenly.  Blocks take
+// their (sequence, query tile, KV head) from the work list in XCD-owned ranges (AttnSched).
 template <typename H, int HD, int G>
 __global__ __launch_bounds__(512, 1) void k_attn_prefill_gqa(
     const H *__restrict__ Q, int ldq, const H *__restrict__ Kc, const H *__restrict__ Vc,
@@ -386,10 +399,11 @@ __global__ __launch_bounds__(512, 1) void k_attn_prefill_gqa(
     KvPaging pg) {
   constexpr int NW = 8, QB = NW / G, QT = 32 * QB, BKV = 64;
   constexpr int NKC = HD / 16, NDB = HD / 32, NPC = BKV / 16;
-  constexpr int KTILES = 2 * NKC, VTILES = NDB * NPC;
-  constexpr int STAGE = (KTILES + VTILES) * 64;   // uint4 per stage
-  constexpr int VW = (HD / 8) * NPC * 2 / 64;     // waves' worth of V^T tasks per stage
-  static_assert(G >= 2 && G <= NW && NW % G == 0 && KTILES % NW == 0, "8 waves over the group");
+  constexpr int KTILES = 2 * NKC;
+  constexpr int VINS = BKV * HD * 2 / 1024;        // 1 KiB DMA instructions of a V tile
+  constexpr int STAGE = (KTILES + VINS) * 64;      // uint4 per stage
+  static_assert(G >= 2 && G <= NW && NW % G == 0 && KTILES % NW == 0 && VINS % NW == 0,
+                "8 waves over the group");
   __shared__ uint4 smem[2 * STAGE];
 
   const int x = blockIdx.x % kXcds, e = as.cut[x] + (int)(blockIdx.x / kXcds);
@@ -420,8 +434,11 @@ __global__ __launch_bounds__(512, 1) void k_attn_prefill_gqa(
     for (int i = 0; i < 16; ++i) acc[d][i] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
+  int voff[NDB];
+  v_tr_offsets<HD>(lane, voff);
+
   const int ntiles = (P0 + min(q0 + QT, L) - 1) / BKV + 1;
-  auto k_issue = [&](int kt, int buf) {
+  auto issue = [&](int kt, int buf) {
     const size_t tb = kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD);
 #pragma unroll
     for (int i = 0; i < KTILES / NW; ++i) {
@@ -431,37 +448,21 @@ __global__ __launch_bounds__(512, 1) void k_attn_prefill_gqa(
       load_tile_to_lds(Kc + tb + (size_t)(key - kt * BKV) * HD + 16 * c + 8 * g,
                        &smem[buf * STAGE + ti * 64]);
     }
-  };
-  // builder waves of tile kt: VW consecutive waves starting at (VW kt) mod 8
-  auto v_task = [&](int kt) -> int {
-    const int r = (wave - VW * kt) & (NW - 1);
-    return r < VW ? r * 64 + lane : -1;
-  };
-  uint4 vr[8];
-  auto v_load = [&](int kt) {
-    const int task = v_task(kt);
-    if (task >= 0) vt_load<H, HD>(vr, Vc, kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD), kt, KL, task);
-  };
-  auto v_store = [&](int kt, int buf) {
-    const int task = v_task(kt);
-    if (task >= 0) vt_store<HD>(&smem[buf * STAGE], vr, task);
+#pragma unroll
+    for (int i = 0; i < VINS / NW; ++i)
+      v_issue<H, HD>(Vc, tb, kt, KL, wave + NW * i, lane, &smem[buf * STAGE + KTILES * 64]);
   };
 
-  k_issue(0, 0);
-  v_load(0);
-  v_store(0, 0);
+  issue(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   for (int kt = 0; kt < ntiles; ++kt) {
     const int cur = kt & 1;
-    const bool more = kt + 1 < ntiles;
-    if (more) {
-      k_issue(kt + 1, cur ^ 1);
-      v_load(kt + 1);
-    }
+    if (kt + 1 < ntiles) issue(kt + 1, cur ^ 1);
     if (qw < L && kt * BKV <= P0 + qw + 31)
       attn_tile16<H, HD>(&smem[cur * STAGE], qf, acc, m_run, l_run, kt, P0, L, qw, my_q, q_ok,
-                         scale_log2, lane);
-    if (more) v_store(kt + 1, cur ^ 1);
+                         scale_log2, lane, voff);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
 
