@@ -152,17 +152,20 @@ template <int HD> __device__ __forceinline__ constexpr int vswz(int row) {
   return 4 * ((row / (128 / HD)) % (HD / 32));
 }
 
-// DMA instruction q of a stage's V tile (HD / 8 of them per 64 keys): lane l fills slot
-// (64 q + l) % (HD / 8) of row (64 q + l) / (HD / 8); rows past the sequence read the last key
-// (their probabilities are 0).  `tb` is the cache offset of the tile's first key.
-template <typename H, int HD>
-__device__ __forceinline__ void v_issue(const H *Vc, size_t tb, int kt, int KL, int q, int lane,
-                                        uint4 *vstage) {
+// Per-lane source of DMA instruction q of a stage's V tile (HD / 8 of them per 64 keys): lane l
+// fills slot (64 q + l) % (HD / 8) of row (64 q + l) / (HD / 8), i.e. 8 elements of that key
+// row from column 8 (slot ^ vswz(row)).
+template <int HD> __device__ __forceinline__ int2 v_src(int q, int lane) {
   constexpr int SPR = HD / 8;
   const int idx = 64 * q + lane, row = idx / SPR, slot = idx % SPR;
-  const int key = min(kt * 64 + row, KL - 1);
-  load_tile_to_lds(Vc + tb + (size_t)(key - kt * 64) * HD + 8 * (slot ^ vswz<HD>(row)),
-                   &vstage[64 * q]);
+  return make_int2(row, 8 * (slot ^ vswz<HD>(row)));
+}
+
+// One 1 KiB DMA of a K or V tile: rows past the sequence (row > lim, the tile's last valid
+// row) read row lim instead; their probabilities are 0.  `base` is the tile's first key row.
+template <typename H, int HD>
+__device__ __forceinline__ void kv_dma(const H *base, int2 rc, int lim, uint4 *dst) {
+  load_tile_to_lds(base + (unsigned)(min(rc.x, lim) * HD + rc.y), dst);
 }
 
 // Byte offsets, within a V tile, of lane l's transposed reads for 32-dim block d (key step 0,
@@ -191,6 +194,35 @@ __device__ __forceinline__ V v_frag_tr(const char *vtile, int off) {
   return __builtin_bit_cast(V, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
+// Value of lane l ^ 32 combined with lane l's own (v_permlane32_swap exchanges the two
+// halves of the wave; the pair it returns holds both values in some order).
+__device__ __forceinline__ float xhalf_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xhalf_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+// acc + the 8 probabilities of a packed P^T operand, as rounded to the operand type (the
+// weights the P V product applies), two at a time with fp32 accumulation (v_dot2).
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float sum_frag(const f16x8 &p, float acc) {
+  const f16x2_t one = {(_Float16)1.f, (_Float16)1.f};
+  acc = __builtin_amdgcn_fdot2(__builtin_shufflevector(p, p, 0, 1), one, acc, false);
+  acc = __builtin_amdgcn_fdot2(__builtin_shufflevector(p, p, 2, 3), one, acc, false);
+  acc = __builtin_amdgcn_fdot2(__builtin_shufflevector(p, p, 4, 5), one, acc, false);
+  return __builtin_amdgcn_fdot2(__builtin_shufflevector(p, p, 6, 7), one, acc, false);
+}
+__device__ __forceinline__ float sum_frag(const bf16x8 &p, float acc) {
+  const bf16x2_t one = {(__bf16)1.f, (__bf16)1.f};
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 0, 1), one, acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 2, 3), one, acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 4, 5), one, acc, false);
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 6, 7), one, acc, false);
+}
+
 // One 64-key tile of 16-bit prefill attention for one wave of 32 queries (lane l owns query
 // qw + l % 32), on v_mfma_f32_32x32x16, from an LDS stage `st` that holds the tile's K in
 // operand order ([32-key block][16-dim step] tiles of 64 x 16 B) followed by its V tile
@@ -199,43 +231,44 @@ __device__ __forceinline__ V v_frag_tr(const char *vtile, int off) {
 //     of each 32-key block, rows 8 (i / 4) + 4 (l / 32) + i % 4: the online-softmax
 //     statistics need one exchange with lane l ^ 32.
 //   O^T += V^T P^T: A = V^T by transposed LDS reads, B = P^T straight from the score registers.
-// The causal / length mask runs only on tiles that reach past the wave's first query; the
-// accumulator is rescaled only when some row maximum grew (otherwise every factor is 1).
+// S^T of one 64-key tile.  K fragments are requested two 16-dim steps ahead of their MFMAs
+// (LDS latency off the MFMA chain at modest register cost), and the two 32-key chains
+// alternate so that MFMA result latency is not exposed either.
 template <typename H, int HD>
-__device__ __forceinline__ void attn_tile16(const uint4 *__restrict__ st,
-                                            const typename Frag<H>::type *qf,
-                                               f32x16 *acc, float &m_run, float &l_run, int kt,
-                                               int P0, int L, int qw, int my_q, bool q_ok,
-                                               float scale_log2, int lane, const int *voff) {
+__device__ __forceinline__ void attn_s16(const uint4 *__restrict__ st,
+                                         const typename Frag<H>::type *qf, int lane, f32x16 *sc) {
   using V = typename Frag<H>::type;
-  constexpr int BKV = 64, NKC = HD / 16, NDB = HD / 32, NPC = BKV / 16, KTILES = 2 * NKC;
-  const int g = lane >> 5;
-  // All K fragments of the tile are requested before the first MFMA, and the two 32-key
-  // chains alternate, so neither LDS latency nor MFMA result latency sits between MFMAs.
-  V kf[2][NKC];
+  constexpr int NKC = HD / 16, AHEAD = 2;
+  V kf[NKC][2];
+  auto kload = [&](int c) {
 #pragma unroll
-  for (int c = 0; c < NKC; ++c)
+    for (int kb = 0; kb < 2; ++kb) kf[c][kb] = *reinterpret_cast<const V *>(&st[(kb * NKC + c) * 64 + lane]);
+  };
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) kf[kb][c] = *reinterpret_cast<const V *>(&st[(kb * NKC + c) * 64 + lane]);
-  __builtin_amdgcn_sched_barrier(0);
-  f32x16 sc[2];
+  for (int c = 0; c < AHEAD; ++c) kload(c);
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int i = 0; i < 16; ++i) sc[kb][i] = 0.f;
 #pragma unroll
-  for (int c = 0; c < NKC; ++c)
+  for (int c = 0; c < NKC; ++c) {
+    if (c + AHEAD < NKC) kload(c + AHEAD);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) sc[kb] = mma32(kf[kb][c], qf[c], sc[kb]);
-  __builtin_amdgcn_sched_barrier(0);
-  // The V^T fragments of the tile are requested now; the softmax below covers their latency.
-  const char *vt = reinterpret_cast<const char *>(st + KTILES * 64);
-  V vf[NPC][NDB];
-#pragma unroll
-  for (int c = 0; c < NPC; ++c)
-#pragma unroll
-    for (int d = 0; d < NDB; ++d) vf[c][d] = v_frag_tr<V, HD>(vt, voff[d] + 16 * c * HD * 2);
-  __builtin_amdgcn_sched_barrier(0);
+    for (int kb = 0; kb < 2; ++kb) sc[kb] = mma32(kf[c][kb], qf[c], sc[kb]);
+  }
+}
+
+// Online softmax of a tile's scores: causal / length mask (only on tiles that reach past the
+// wave's first query), running maximum and sum, rescale of the accumulator (only when some
+// row maximum grew; otherwise every factor is 1), and the probabilities packed as the P^T
+// operands of the four 16-key steps.
+template <typename H, int HD>
+__device__ __forceinline__ void attn_softmax16(f32x16 *sc, f32x16 *acc, float &m_run,
+                                               float &l_run, int kt, int P0, int L, int qw,
+                                               int my_q, bool q_ok, float scale_log2, int lane,
+                                               typename Frag<H>::type *pf) {
+  constexpr int BKV = 64, NDB = HD / 32, NPC = BKV / 16;
+  const int g = lane >> 5;
   if (kt * BKV + BKV - 1 > P0 + qw || qw + 31 >= L) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -251,7 +284,7 @@ __device__ __forceinline__ void attn_tile16(const uint4 *__restrict__ st,
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int i = 0; i < 16; ++i) tmax = fmaxf(tmax, sc[kb][i]);
-  tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+  tmax = xhalf_max(tmax);
   const float m_new = fmaxf(m_run, tmax * scale_log2);
   const float base = m_new == -INFINITY ? 0.f : m_new;
   if (__any(m_new > m_run)) {
@@ -266,19 +299,54 @@ __device__ __forceinline__ void attn_tile16(const uint4 *__restrict__ st,
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const float p = __builtin_amdgcn_exp2f(fmaf(sc[kb][i], scale_log2, -base));
-      sc[kb][i] = p;
-      l_run += p;
-    }
+    for (int i = 0; i < 16; ++i) sc[kb][i] = __builtin_amdgcn_exp2f(fmaf(sc[kb][i], scale_log2, -base));
 #pragma unroll
   for (int c = 0; c < NPC; ++c) {
-    V pf;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) pf[e] = static_cast<H>(sc[c / 2][8 * (c % 2) + e]);
-#pragma unroll
-    for (int d = 0; d < NDB; ++d) acc[d] = mma32(vf[c][d], pf, acc[d]);
+    for (int e = 0; e < 8; ++e) pf[c][e] = static_cast<H>(sc[c / 2][8 * (c % 2) + e]);
+    l_run = sum_frag(pf[c], l_run);
   }
+}
+
+// V^T fragments of a stage's V tile.
+template <typename H, int HD>
+__device__ __forceinline__ void attn_vload16(const uint4 *__restrict__ st, const int *voff,
+                                             typename Frag<H>::type (*vf)[HD / 32]) {
+  constexpr int NPC = 4, KTILES = 2 * (HD / 16);
+  const char *vt = reinterpret_cast<const char *>(st + KTILES * 64);
+#pragma unroll
+  for (int c = 0; c < NPC; ++c)
+#pragma unroll
+    for (int d = 0; d < HD / 32; ++d)
+      vf[c][d] = v_frag_tr<typename Frag<H>::type, HD>(vt, voff[d] + 16 * c * HD * 2);
+}
+
+template <typename H, int HD>
+__device__ __forceinline__ void attn_pv16(typename Frag<H>::type (*vf)[HD / 32],
+                                          const typename Frag<H>::type *pf, f32x16 *acc) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int d = 0; d < HD / 32; ++d) acc[d] = mma32(vf[c][d], pf[c], acc[d]);
+}
+
+// One whole tile: scores, then the V^T fragments are requested (the softmax covers their
+// latency), softmax, P V.
+template <typename H, int HD>
+__device__ __forceinline__ void attn_tile16(const uint4 *__restrict__ st,
+                                            const typename Frag<H>::type *qf, f32x16 *acc,
+                                            float &m_run, float &l_run, int kt, int P0, int L,
+                                            int qw, int my_q, bool q_ok, float scale_log2,
+                                            int lane, const int *voff) {
+  using V = typename Frag<H>::type;
+  f32x16 sc[2];
+  attn_s16<H, HD>(st, qf, lane, sc);
+  V vf[4][HD / 32];
+  attn_vload16<H, HD>(st, voff, vf);
+  __builtin_amdgcn_sched_barrier(0);
+  V pf[4];
+  attn_softmax16<H, HD>(sc, acc, m_run, l_run, kt, P0, L, qw, my_q, q_ok, scale_log2, lane, pf);
+  attn_pv16<H, HD>(vf, pf, acc);
 }
 
 // Normalised output rows of one wave: lane l writes dims 32 d + 8 j + 4 (l / 32) .. + 3 of its
@@ -353,18 +421,23 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
   // K tile (kb, c): lane l reads key 32 kb + l % 32 (clamped into the sequence; rows past KL
   // are masked), dims 16 c + 8 g.  A tile's keys lie in one page (tiles start at cached
   // positions and the clamp stays in the tile), so one base per tile serves every row.
+  int2 ksrc[KTILES / 4], vsrc[VINS / 4];   // (row in the tile, column) of each DMA of the wave
+#pragma unroll
+  for (int i = 0; i < KTILES / 4; ++i) {
+    const int ti = wave + 4 * i;
+    ksrc[i] = make_int2(32 * (ti / NKC) + (lane & 31), 16 * (ti % NKC) + 8 * g);
+  }
+#pragma unroll
+  for (int i = 0; i < VINS / 4; ++i) vsrc[i] = v_src<HD>(wave + 4 * i, lane);
   auto issue = [&](int kt, int buf) {
     const size_t tb = kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD);
+    const int lim = KL - 1 - kt * BKV;
 #pragma unroll
-    for (int i = 0; i < KTILES / 4; ++i) {
-      const int ti = wave + 4 * i, kb = ti / NKC, c = ti % NKC;
-      const int key = min(kt * BKV + 32 * kb + (lane & 31), KL - 1);
-      load_tile_to_lds(Kc + tb + (size_t)(key - kt * BKV) * HD + 16 * c + 8 * g,
-                       &smem[buf * STAGE + ti * 64]);
-    }
+    for (int i = 0; i < KTILES / 4; ++i)
+      kv_dma<H, HD>(Kc + tb, ksrc[i], lim, &smem[buf * STAGE + (wave + 4 * i) * 64]);
 #pragma unroll
     for (int i = 0; i < VINS / 4; ++i)
-      v_issue<H, HD>(Vc, tb, kt, KL, wave + 4 * i, lane, &smem[buf * STAGE + KTILES * 64]);
+      kv_dma<H, HD>(Vc + tb, vsrc[i], lim, &smem[buf * STAGE + (KTILES + wave + 4 * i) * 64]);
   };
 
   issue(0, 0);
@@ -380,7 +453,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
     __syncthreads();
   }
 
-  l_run += __shfl_xor(l_run, 32);
+  l_run = xhalf_sum(l_run);
   if (q_ok) attn_store16<H, HD>(O + (size_t)(tok0 + my_q) * ldo + h * HD, acc, 1.0f / l_run, g);
 }
 
@@ -438,19 +511,23 @@ __global__ __launch_bounds__(512, 1) void k_attn_prefill_gqa(
   v_tr_offsets<HD>(lane, voff);
 
   const int ntiles = (P0 + min(q0 + QT, L) - 1) / BKV + 1;
+  int2 ksrc[KTILES / NW], vsrc[VINS / NW];   // (row in the tile, column) of each DMA of the wave
+#pragma unroll
+  for (int i = 0; i < KTILES / NW; ++i) {
+    const int ti = wave + NW * i;
+    ksrc[i] = make_int2(32 * (ti / NKC) + (lane & 31), 16 * (ti % NKC) + 8 * g);
+  }
+#pragma unroll
+  for (int i = 0; i < VINS / NW; ++i) vsrc[i] = v_src<HD>(wave + NW * i, lane);
   auto issue = [&](int kt, int buf) {
     const size_t tb = kv_row_off(pg, b, kvh, hkv, max_ctx, kt * BKV, HD);
+    const int lim = KL - 1 - kt * BKV;
 #pragma unroll
-    for (int i = 0; i < KTILES / NW; ++i) {
-      const int ti = wave + NW * i;
-      const int kb = ti / NKC, c = ti % NKC;
-      const int key = min(kt * BKV + 32 * kb + (lane & 31), KL - 1);
-      load_tile_to_lds(Kc + tb + (size_t)(key - kt * BKV) * HD + 16 * c + 8 * g,
-                       &smem[buf * STAGE + ti * 64]);
-    }
+    for (int i = 0; i < KTILES / NW; ++i)
+      kv_dma<H, HD>(Kc + tb, ksrc[i], lim, &smem[buf * STAGE + (wave + NW * i) * 64]);
 #pragma unroll
     for (int i = 0; i < VINS / NW; ++i)
-      v_issue<H, HD>(Vc, tb, kt, KL, wave + NW * i, lane, &smem[buf * STAGE + KTILES * 64]);
+      kv_dma<H, HD>(Vc + tb, vsrc[i], lim, &smem[buf * STAGE + (KTILES + wave + NW * i) * 64]);
   };
 
   issue(0, 0);
@@ -466,7 +543,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_prefill_gqa(
     __syncthreads();
   }
 
-  l_run += __shfl_xor(l_run, 32);
+  l_run = xhalf_sum(l_run);
   if (q_ok) attn_store16<H, HD>(O + (size_t)(tok0 + my_q) * ldo + h * HD, acc, 1.0f / l_run, g);
 }
 
