@@ -145,28 +145,10 @@ RgLayout make_layout(const ll_rg_config &c) {
 
 }  // namespace
 
-struct ll_rg {
+struct ll_rg : ll::StateModel {
   ll_rg_config cfg;
   RgLayout L;
-  char *ws = nullptr;
-  hipStream_t stream = nullptr;
-  hipStream_t cap_stream = nullptr;
-  int batch = 0;
-  std::vector<int> lens;
-  int opt[LL_OPT_COUNT] = {1, 1, 1, 0, 0, 0};
-  struct Graph {
-    const void *in;
-    void *out;
-    void *logits;
-    int batch;
-    hipGraphExec_t exec;
-  };
-  std::vector<Graph> graphs;
-  Timer *timer = nullptr;
-  void mark(int cls) const {
-    if (timer) timer->cls = cls;
-  }
-  template <typename P = void> P *at(size_t off) const { return reinterpret_cast<P *>(ws + off); }
+  ll_rg() : StateModel("ll_rg_reset", false) {}
   size_t K1() const { return (size_t)std::max(cfg.d_conv - 1, 1); }
   float *conv_state(int l) const {
     return at<float>(L.conv_state) + (size_t)l * cfg.max_batch * K1() * cfg.lru_width;
@@ -174,11 +156,6 @@ struct ll_rg {
   float *rec_state(int l) const {
     return at<float>(L.rec_state) + (size_t)l * cfg.max_batch * cfg.lru_width;
   }
-  void drop_graphs() {
-    for (auto &g : graphs) (void)hipGraphExecDestroy(g.exec);
-    graphs.clear();
-  }
-  ~ll_rg() { delete timer; }
 };
 
 namespace {
@@ -479,25 +456,18 @@ ll_status ll_rg_prefill(ll_rg *m, int32_t batch, const int32_t *seq_lens_host,
   if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
   if (!seq_lens_host || !tokens_dev || !next_tokens_dev)
     return fail(LL_ERR_INVALID_ARGUMENT, "seq_lens_host, tokens_dev and next_tokens_dev must be set");
-  if (batch < 1) return fail(LL_ERR_INVALID_ARGUMENT, "batch %d < 1", batch);
   const ll_rg_config &c = m->cfg;
-  if (batch > c.max_batch) return fail(LL_ERR_CAPACITY, "batch %d > max_batch %d", batch, c.max_batch);
-  const bool cont = m->batch != 0;
-  if (cont && batch != m->batch)
-    return fail(LL_ERR_STATE, "prefill of %d sequences on state of %d (a further chunk extends "
-                "the same sequences; ll_rg_reset starts new ones)", batch, m->batch);
   long total = 0;
+  ll_status vst = m->check_prefill(batch, seq_lens_host, c.max_batch, c.max_prefill_tokens, &total);
+  if (vst != LL_OK) return vst;
+  const bool cont = m->batch != 0;
   int max_len = 0;
   MambaMeta mm;
   mm.batch = batch;
   for (int b = 0; b < batch; ++b) {
-    if (seq_lens_host[b] < 1) return fail(LL_ERR_INVALID_ARGUMENT, "seq_lens[%d] = %d < 1", b, seq_lens_host[b]);
-    total += seq_lens_host[b];
     max_len = std::max(max_len, (int)seq_lens_host[b]);
     mm.lens[b] = seq_lens_host[b];
   }
-  if (total > c.max_prefill_tokens)
-    return fail(LL_ERR_CAPACITY, "%ld prompt tokens > max_prefill_tokens %d", total, c.max_prefill_tokens);
   const int T = (int)total;
   const int clen = rg_chunk_len(max_len);
   PrefillPlan pp;
@@ -524,12 +494,7 @@ ll_status ll_rg_prefill(ll_rg *m, int32_t batch, const int32_t *seq_lens_host,
   if (st != LL_OK) return st;
   st = enqueue_head(m, batch, m->at<int>(L.last_row), next_tokens_dev, logits_dev, s);
   if (st != LL_OK) return st;
-  if (cont) {
-    for (int b = 0; b < batch; ++b) m->lens[b] += seq_lens_host[b];
-  } else {
-    m->batch = batch;
-    m->lens.assign(seq_lens_host, seq_lens_host + batch);
-  }
+  m->commit_prefill(batch, seq_lens_host);
   return LL_OK;
 }
 
@@ -539,134 +504,57 @@ ll_status ll_rg_decode_step(ll_rg *m, const int32_t *in_tokens_dev, int32_t *nex
   if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
   if (!in_tokens_dev || !next_tokens_dev)
     return fail(LL_ERR_INVALID_ARGUMENT, "in_tokens_dev and next_tokens_dev must be set");
-  if (m->batch == 0) return fail(LL_ERR_STATE, "decode before prefill");
-  TimerScope scope(m->timer, 1);
-  if (m->opt[LL_OPT_DECODE_GRAPH] && !m->timer) {
-    hipGraphExec_t exec = nullptr;
-    for (auto &g : m->graphs)
-      if (g.in == in_tokens_dev && g.out == next_tokens_dev && g.logits == logits_dev &&
-          g.batch == m->batch)
-        exec = g.exec;
-    if (!exec) {
-      if (!m->cap_stream) LL_HIP(hipStreamCreateWithFlags(&m->cap_stream, hipStreamNonBlocking));
-      LL_HIP(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
-      ll_status st = enqueue_decode(m, in_tokens_dev, next_tokens_dev, logits_dev, m->cap_stream);
-      hipGraph_t graph = nullptr;
-      hipError_t ec = hipStreamEndCapture(m->cap_stream, &graph);
-      if (st != LL_OK) {
-        if (graph) (void)hipGraphDestroy(graph);
-        return st;
-      }
-      if (ec != hipSuccess) return fail(LL_ERR_HIP, "hipStreamEndCapture: %s", hipGetErrorString(ec));
-      ec = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
-      (void)hipGraphDestroy(graph);
-      if (ec != hipSuccess) return fail(LL_ERR_HIP, "hipGraphInstantiate: %s", hipGetErrorString(ec));
-      if (m->graphs.size() >= 8) {
-        (void)hipGraphExecDestroy(m->graphs.front().exec);
-        m->graphs.erase(m->graphs.begin());
-      }
-      m->graphs.push_back({in_tokens_dev, next_tokens_dev, logits_dev, m->batch, exec});
-    }
-    LL_HIP(hipGraphLaunch(exec, m->stream));
-  } else {
-    ll_status st = enqueue_decode(m, in_tokens_dev, next_tokens_dev, logits_dev, m->stream);
-    if (st != LL_OK) return st;
-  }
-  for (auto &l : m->lens) ++l;
-  return LL_OK;
+  return m->decode(in_tokens_dev, next_tokens_dev, logits_dev, [&](hipStream_t s) {
+    return enqueue_decode(m, in_tokens_dev, next_tokens_dev, logits_dev, s);
+  });
 }
 
 ll_status ll_rg_reset(ll_rg *m) {
   g_err.clear();
   if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
-  m->batch = 0;
-  m->lens.clear();
-  return LL_OK;
+  return m->reset();
 }
 
 ll_status ll_rg_seq_lengths(const ll_rg *m, int32_t *out, int32_t cap, int32_t *n) {
   g_err.clear();
-  if (!m || !n || (cap > 0 && !out)) return fail(LL_ERR_INVALID_ARGUMENT, "NULL argument");
-  *n = m->batch;
-  for (int b = 0; b < m->batch && b < cap; ++b) out[b] = m->lens[b];
-  return LL_OK;
+  if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
+  return m->seq_lengths(out, cap, n);
 }
 
 ll_status ll_rg_set_option(ll_rg *m, int32_t option, int32_t value) {
   g_err.clear();
   if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
-  switch (option) {
-    case LL_OPT_DECODE_GRAPH:
-    case LL_OPT_PREFILL_SPLITK:
-      if (value != 0 && value != 1) return fail(LL_ERR_INVALID_ARGUMENT, "option %d takes 0 or 1", option);
-      break;
-    case LL_OPT_DECODE_SPLITK:
-      if (value < 0 || value > 2) return fail(LL_ERR_INVALID_ARGUMENT, "decode split-K 0, 1 or 2");
-      break;
-    case LL_OPT_PREFILL_TILE:
-      if (value < 0 || value > 3) return fail(LL_ERR_INVALID_ARGUMENT, "prefill tile 0..3");
-      break;
-    case LL_OPT_ATTN_DECODE_CHUNK:
-    case LL_OPT_DECODE_FUSED:
-      return fail(LL_ERR_UNSUPPORTED, "option %d does not apply to this model", option);
-    default:
-      return fail(LL_ERR_INVALID_ARGUMENT, "unknown option %d", option);
-  }
-  if (m->opt[option] != value) m->drop_graphs();
-  m->opt[option] = value;
-  return LL_OK;
+  return m->set_option(option, value);
 }
 
 ll_status ll_rg_get_option(const ll_rg *m, int32_t option, int32_t *value) {
   g_err.clear();
-  if (!m || !value) return fail(LL_ERR_INVALID_ARGUMENT, "NULL argument");
-  if (option < 0 || option >= LL_OPT_COUNT) return fail(LL_ERR_INVALID_ARGUMENT, "unknown option %d", option);
-  if (option == LL_OPT_ATTN_DECODE_CHUNK || option == LL_OPT_DECODE_FUSED)
-    return fail(LL_ERR_UNSUPPORTED, "option %d does not apply to this model", option);
-  *value = m->opt[option];
-  return LL_OK;
+  if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
+  return m->get_option(option, value);
 }
 
 ll_status ll_rg_device_flags(ll_rg *m, int32_t *flags) {
   g_err.clear();
-  if (!m || !flags) return fail(LL_ERR_INVALID_ARGUMENT, "NULL argument");
-  LL_HIP(hipStreamSynchronize(m->stream));
-  LL_HIP(hipMemcpy(flags, m->at(m->L.err), 4, hipMemcpyDeviceToHost));
-  return LL_OK;
+  if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
+  return m->device_flags(m->L.err, flags);
 }
 
 ll_status ll_rg_set_kernel_timing(ll_rg *m, int32_t enable) {
   g_err.clear();
   if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
-  if (enable && !m->timer) m->timer = new Timer();
-  if (!enable && m->timer) {
-    (void)hipStreamSynchronize(m->stream);
-    delete m->timer;
-    m->timer = nullptr;
-  }
-  return LL_OK;
+  return m->set_kernel_timing(enable);
 }
 
 ll_status ll_rg_kernel_timing_read(ll_rg *m, int32_t *counts, double *ms) {
   g_err.clear();
-  if (!m || !counts || !ms) return fail(LL_ERR_INVALID_ARGUMENT, "NULL argument");
-  for (int i = 0; i < 2 * LL_RGK_COUNT; ++i) {
-    counts[i] = 0;
-    ms[i] = 0.0;
-  }
-  if (!m->timer) return fail(LL_ERR_STATE, "kernel timing is not enabled");
-  return m->timer->drain(m->stream, LL_RGK_COUNT, counts, ms);
+  if (!m) return fail(LL_ERR_INVALID_ARGUMENT, "model is NULL");
+  return m->kernel_timing_read(LL_RGK_COUNT, counts, ms);
 }
 
 const char *ll_rg_kernel_class_name(int32_t cls) {
   return (cls >= 0 && cls < LL_RGK_COUNT) ? kRgClassNames[cls] : "";
 }
 
-void ll_rg_free(ll_rg *m) {
-  if (!m) return;
-  m->drop_graphs();
-  if (m->cap_stream) (void)hipStreamDestroy(m->cap_stream);
-  delete m;
-}
+void ll_rg_free(ll_rg *m) { delete m; }
 
 }  // extern "C"
