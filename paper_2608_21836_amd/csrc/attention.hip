@@ -259,9 +259,15 @@ __device__ __forceinline__ void attn_s16(const uint4 *__restrict__ st,
 }
 
 // Online softmax of a tile's scores: causal / length mask (only on tiles that reach past the
-// wave's first query), running maximum and sum, rescale of the accumulator (only when some
-// row maximum grew; otherwise every factor is 1), and the probabilities packed as the P^T
-// operands of the four 16-key steps.
+// wave's first query), running maximum and sum, rescale of the accumulator, and the
+// probabilities packed as the P^T operands of the four 16-key steps.
+// The reference maximum moves lazily: only when some row's score maximum exceeds it by more
+// than kSoftmaxSlack (log2 units) are the accumulator and sum rescaled (for every row, to the
+// true running maximum).  Until then the probabilities are taken against the smaller, stale
+// reference and lie in (0, 2^kSoftmaxSlack]; the common factor cancels exactly in the final
+// division by the sum, and fp16 / bf16 hold such values with the same relative precision as
+// values below 1.  On most tiles the 64 accumulator multiplies per lane are skipped.
+constexpr float kSoftmaxSlack = 8.f;
 template <typename H, int HD>
 __device__ __forceinline__ void attn_softmax16(f32x16 *sc, f32x16 *acc, float &m_run,
                                                float &l_run, int kt, int P0, int L, int qw,
@@ -285,17 +291,18 @@ __device__ __forceinline__ void attn_softmax16(f32x16 *sc, f32x16 *acc, float &m
 #pragma unroll
     for (int i = 0; i < 16; ++i) tmax = fmaxf(tmax, sc[kb][i]);
   tmax = xhalf_max(tmax);
-  const float m_new = fmaxf(m_run, tmax * scale_log2);
-  const float base = m_new == -INFINITY ? 0.f : m_new;
-  if (__any(m_new > m_run)) {
-    const float alpha = __builtin_amdgcn_exp2f(m_run - base);
+  const float m_cand = tmax * scale_log2;
+  if (__any(m_cand > m_run + kSoftmaxSlack)) {
+    const float m_new = fmaxf(m_run, m_cand);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - (m_new == -INFINITY ? 0.f : m_new));
     l_run *= alpha;
 #pragma unroll
     for (int d = 0; d < NDB; ++d) acc[d] *= alpha;
+    m_run = m_new;
   }
-  m_run = m_new;
-  // p = 2^(s * scale - m); arguments are <= 0, so the hardware exp2 is exact enough (results
-  // below the fp32 normal range flush to 0)
+  const float base = m_run == -INFINITY ? 0.f : m_run;
+  // p = 2^(s * scale - m); arguments are <= kSoftmaxSlack, so the hardware exp2 is exact
+  // enough (results below the fp32 normal range flush to 0)
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -443,14 +450,20 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
   issue(0, 0);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  for (int kt = 0; kt < ntiles; ++kt) {
-    const int cur = kt & 1;
+  // tile kt from stage CUR (= kt % 2; the loop is unrolled by two so that stage offsets are
+  // compile-time constants)
+  auto tile = [&](int kt, auto CUR) {
+    constexpr int cur = decltype(CUR)::value;
     if (kt + 1 < ntiles) issue(kt + 1, cur ^ 1);
     if (qw < L && kt * BKV <= P0 + qw + 31)  // else nothing for this wave in this tile
       attn_tile16<H, HD>(&smem[cur * STAGE], qf, acc, m_run, l_run, kt, P0, L, qw, my_q, q_ok,
                          scale_log2, lane, voff);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+  };
+  for (int kt = 0; kt < ntiles; kt += 2) {
+    tile(kt, std::integral_constant<int, 0>());
+    if (kt + 1 < ntiles) tile(kt + 1, std::integral_constant<int, 1>());
   }
 
   l_run = xhalf_sum(l_run);
@@ -533,14 +546,20 @@ __global__ __launch_bounds__(512, 1) void k_attn_prefill_gqa(
   issue(0, 0);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  for (int kt = 0; kt < ntiles; ++kt) {
-    const int cur = kt & 1;
+  // tile kt from stage CUR (= kt % 2; the loop is unrolled by two so that stage offsets are
+  // compile-time constants)
+  auto tile = [&](int kt, auto CUR) {
+    constexpr int cur = decltype(CUR)::value;
     if (kt + 1 < ntiles) issue(kt + 1, cur ^ 1);
-    if (qw < L && kt * BKV <= P0 + qw + 31)
+    if (qw < L && kt * BKV <= P0 + qw + 31)  // else nothing for this wave in this tile
       attn_tile16<H, HD>(&smem[cur * STAGE], qf, acc, m_run, l_run, kt, P0, L, qw, my_q, q_ok,
                          scale_log2, lane, voff);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+  };
+  for (int kt = 0; kt < ntiles; kt += 2) {
+    tile(kt, std::integral_constant<int, 0>());
+    if (kt + 1 < ntiles) tile(kt + 1, std::integral_constant<int, 1>());
   }
 
   l_run = xhalf_sum(l_run);
