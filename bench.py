@@ -188,11 +188,37 @@ def algorithmic_work_mamba(cfg, lens, n_decode, fused):
     return w
 
 
+SSD_CHUNK = 64   # chunk length of the matrix-form Mamba2 prefill scan (16-bit models)
+
+
+def ssd_scan_flops(cfg, lens):
+    """MFMA flops of the matrix-form prefill scan of one layer, as (pass 3, pass 1): per chunk of
+    q steps, C B^T below the diagonal once per B/C group (q (q+1) / 2 * N * 2), the masked
+    decayed scores times x per head (q (q+1) / 2 * P * 2), the incoming state's contribution
+    per head (q * N * P * 2, all but a fresh sequence's first chunk) and the end state per
+    head (P * q * N * 2: pass 1 for every chunk but a sequence's last, pass 3 for the last)."""
+    NS, P, H, G = cfg.d_state, cfg.head_dim, cfg.n_heads, cfg.n_groups
+    out = end = 0.0
+    for n in lens:
+        qs = [min(SSD_CHUNK, n - i) for i in range(0, n, SSD_CHUNK)]
+        for c, q in enumerate(qs):
+            out += G * q * (q + 1) * NS + H * q * (q + 1) * P
+            if c > 0:
+                out += H * 2.0 * q * NS * P
+            if c + 1 < len(qs):
+                end += H * 2.0 * P * q * NS
+            else:
+                out += H * 2.0 * P * q * NS
+    return out, end
+
+
 def algorithmic_work_mamba2(cfg, lens, n_decode):
     """{(phase, class): (work, unit)} summed over one Mamba2 job.  Projections count MFMA
-    flops; the scan counts fp32 vector flops per (token, head row, state): 2 for the decayed
-    state update and 2 for the C.h product (pass 3), 2 in pass 1; the rest counts bytes.
-    Decode: weights once per step, the conv and SSM state read and written, activations."""
+    flops; the prefill scan of 16-bit models counts the MFMA flops of its matrix form
+    (ssd_scan_flops), that of fp32 models fp32 vector flops per (token, head row, state): 2
+    for the decayed state update and 2 for the C.h product (pass 3), 2 in pass 1; the rest
+    counts bytes.  Decode: weights once per step, the conv and SSM state read and written,
+    activations."""
     eb = 2 if cfg.dtype == "bf16" else 4
     B, T = len(lens), sum(lens)
     d, di, NS, V, L, K = cfg.d_model, cfg.d_inner, cfg.d_state, cfg.vocab, cfg.n_layers, cfg.d_conv
@@ -203,8 +229,13 @@ def algorithmic_work_mamba2(cfg, lens, n_decode):
     w[("prefill", "in_proj")] = (2.0 * T * NZ * d * L, "flop")
     w[("prefill", "out_proj_resid")] = (2.0 * T * d * di * L, "flop")
     w[("prefill", "conv_silu")] = (float(L * (T * CD * 8 + CD * (K + 1) * 4)), "byte")
-    w[("prefill", "scan")] = (float(L * T * di * NS * 4), "alu")
-    w[("prefill", "scan_chunk")] = (float(L * T * di * NS * 2), "alu")
+    if cfg.dtype == "bf16":
+        out, end = ssd_scan_flops(cfg, lens)
+        w[("prefill", "scan")] = (L * out, "flop")
+        w[("prefill", "scan_chunk")] = (L * end, "flop")
+    else:
+        w[("prefill", "scan")] = (float(L * T * di * NS * 4), "alu")
+        w[("prefill", "scan_chunk")] = (float(L * T * di * NS * 2), "alu")
     w[("prefill", "gated_rmsnorm")] = (float(L * T * di * (4 + eb)), "byte")
     w[("prefill", "lm_head_argmax")] = (float(V * d * eb + B * d * eb + B * (V // 32) * 8), "byte")
     w[("prefill", "rmsnorm")] = (float((L * T + B) * d * (4 + eb)), "byte")

@@ -398,6 +398,9 @@ hipError_t launch_transpose_f32(const float *src, int rows, int cols, int cols_p
 constexpr int kM2Rows = 16;              // head rows per scan block
 constexpr int kM2TargetBlocks = 1024;
 int mamba2_chunk_len(int total, int n_heads, int head_dim);
+// The matrix-form prefill scan: chunk length, and the shapes it is instantiated for.
+constexpr int kM2SsdChunk = 64;
+bool mamba2_ssd_ok(int head_dim, int d_state);
 int mamba2_max_chunks(int max_total, int max_batch, int n_heads, int head_dim);
 struct M2ScanArgs {
   const float *zxd = nullptr;   // in_proj rows: z at [0, di), dt at [dt_col, dt_col + H)
@@ -414,6 +417,8 @@ struct M2ScanArgs {
   int conv_col = 0, conv_n = 0, K = 0, update_conv = 0;
   int di = 0, H = 0, P = 0, N = 0, G = 0;
   int fresh = 0, carry = 0;     // carry: 0 zero, 1 SSM state, 2 hloc
+  int mfma = 0;                 // prefill chunks through the matrix-form scan (k_m2_ssd):
+                                // chunks of at most kM2SsdChunk steps, fp16 operands
 };
 hipError_t launch_m2_scan_chunks(const M2ScanArgs &a, int n_chunks, hipStream_t s);
 hipError_t launch_m2_scan_carry(const M2ScanArgs &a, int batch, hipStream_t s);

@@ -184,6 +184,235 @@ __global__ __launch_bounds__(256) void k_m2_carry(M2ScanArgs p) {
   }
 }
 
+// ------------------------------------------------------------------------------------------
+// Prefill scan of 16-bit models as matrix products (the chunked state-space-duality form of
+// the same recurrence), on v_mfma_f32_16x16x32_f16 with fp32 accumulation.  One block of 4
+// waves per (head h, chunk of Q <= 64 steps).  With dA_t = dt_t A (log2 units) and
+// c_t = dA_{t0} + .. + dA_t, the recurrence h_t = 2^dA_t h_{t-1} + dt_t x_t B_t^T gives
+//   h_t = 2^c_t h_init + sum_{s <= t} 2^(c_t - c_s) dt_s x_s B_s^T,
+//   y_t = C_t h_t^T = 2^c_t (C_t h_init^T) + sum_{s <= t} (C_t . B_s) 2^(c_t - c_s) dt_s x_s,
+// i.e. Y = diag(2^c) C Hinit^T + (S o L) X with S = C B^T and L[t][s] = 2^(c_t - c_s) dt_s
+// (s <= t, else 0), and the chunk's end state h_end = 2^c_last h_init + X^T diag(w) B with
+// w_s = dt_s 2^(c_last - c_s).  Pass 1 (kOut false) writes h_end from a zero state for every
+// chunk but a sequence's last; pass 3 writes g = (y + D x) silu(z) for every chunk and, at a
+// sequence's last chunk, the SSM state and the conv state.
+// Operands are staged in LDS as fp16 ([t][n] rows of C and B; x, w B and the masked decayed
+// scores transposed where the product needs the contraction index contiguous); every row is
+// padded by 8 elements so that the 16 rows of a fragment read fall in distinct bank groups.
+// ------------------------------------------------------------------------------------------
+
+// LDS layout (fp16 elements).  Pass 3: C and B rows, x transposed, the masked decayed scores and
+// the incoming state; the transposed w B of the end state reuses the space of the last two once
+// the outputs are done.  Pass 1: w B and x, both transposed.
+template <bool kOut, int N, int P>
+struct SsdLds {
+  static constexpr int LDN = N + 8, LDQ = kM2SsdChunk + 8;  // padded rows
+  static constexpr int C = 0;                               // [Q][LDN]
+  static constexpr int B = kOut ? C + kM2SsdChunk * LDN : 0;  // [Q][LDN]
+  static constexpr int XT = kOut ? B + kM2SsdChunk * LDN : 0;  // [P][LDQ]
+  static constexpr int M = XT + P * LDQ;                      // [Q][LDQ]
+  static constexpr int HI = M + kM2SsdChunk * LDQ;            // [P][LDN]
+  static constexpr int BT = M;                                // [N][LDQ]
+  static constexpr int TOTAL =
+      kOut ? (HI + P * LDN > BT + N * LDQ ? HI + P * LDN : BT + N * LDQ) : BT + N * LDQ;
+};
+
+template <bool kOut, int N, int P>
+__global__ __launch_bounds__(256) void k_m2_ssd(M2ScanArgs p) {
+  constexpr int Q = kM2SsdChunk;
+  using Lds = SsdLds<kOut, N, P>;
+  constexpr int LDN = Lds::LDN, LDQ = Lds::LDQ;
+  static_assert(P % 16 == 0 && N % 32 == 0, "16-row output tiles, 32-wide contraction steps");
+  __shared__ __attribute__((aligned(16))) _Float16 sm[Lds::TOTAL];
+  __shared__ float s_c[Q], s_dt[Q];
+  _Float16 *const sC = sm + Lds::C, *const sB = sm + Lds::B, *const sBT = sm + Lds::BT;
+  _Float16 *const sXT = sm + Lds::XT, *const sM = sm + Lds::M, *const sH = sm + Lds::HI;
+
+  const int j = blockIdx.y, h = blockIdx.x;
+  const int4 ch = p.chunks[j];
+  const bool last = ch.w & kChunkLast;
+  if (!kOut && last) return;  // a sequence's last chunk needs no end state
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, kq = lane >> 4;
+  const int t0 = ch.y, nt = ch.z;
+  const int grp = h / (p.H / p.G);
+  const int di = p.di, GN = p.G * N;
+  const float a2 = p.A2[h], bias = p.dt_b[h];
+  const size_t tile = (size_t)P * N;
+  const float *init = nullptr;  // incoming state (fp32): the SSM state or the carried one
+  if (kOut && p.carry == 1) init = p.ssm + ((size_t)ch.x * p.H + h) * tile;
+  if (kOut && p.carry == 2) init = p.hloc + ((size_t)j * p.H + h) * tile;
+  const float *xbc = p.xbc + (size_t)t0 * p.conv_n;
+
+  // dt and the cumulative dt of the chunk (steps past its end: dt = 0)
+  if (tid < Q)
+    s_dt[tid] = tid < nt ? softplus_f(p.zxd[(size_t)(t0 + tid) * p.ldz + p.dt_col + h] + bias) : 0.f;
+  __syncthreads();
+  if (tid == 0) {
+    float c = 0.f;
+    for (int t = 0; t < Q; ++t) {
+      c += s_dt[t];
+      s_c[t] = c;
+    }
+    if (!kOut) p.dtsum[(size_t)j * p.H + h] = c;
+  }
+  // operands in fp16; rows past the chunk are zero
+  constexpr int NV = N / 4, PV = P / 4;
+  if (kOut) {
+    for (int i = tid; i < Q * NV; i += 256) {
+      const int t = i / NV, n = 4 * (i % NV);
+      float4 bv = make_float4(0.f, 0.f, 0.f, 0.f), cv = bv;
+      if (t < nt) {
+        const float *row = xbc + (size_t)t * p.conv_n + di + grp * N + n;
+        bv = *reinterpret_cast<const float4 *>(row);
+        cv = *reinterpret_cast<const float4 *>(row + GN);
+      }
+      _Float16 *b = sB + t * LDN + n, *c = sC + t * LDN + n;
+      b[0] = (_Float16)bv.x; b[1] = (_Float16)bv.y; b[2] = (_Float16)bv.z; b[3] = (_Float16)bv.w;
+      c[0] = (_Float16)cv.x; c[1] = (_Float16)cv.y; c[2] = (_Float16)cv.z; c[3] = (_Float16)cv.w;
+    }
+    if (init) {
+      for (int i = tid; i < P * NV; i += 256) {
+        const int q = i / NV, n = 4 * (i % NV);
+        const float4 v = *reinterpret_cast<const float4 *>(init + (size_t)q * N + n);
+        _Float16 *d = sH + q * LDN + n;
+        d[0] = (_Float16)v.x; d[1] = (_Float16)v.y; d[2] = (_Float16)v.z; d[3] = (_Float16)v.w;
+      }
+    }
+  }
+  for (int i = tid; i < Q * PV; i += 256) {
+    const int t = i / PV, q = 4 * (i % PV);
+    float4 xv = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (t < nt) xv = *reinterpret_cast<const float4 *>(xbc + (size_t)t * p.conv_n + h * P + q);
+    sXT[(q + 0) * LDQ + t] = (_Float16)xv.x;
+    sXT[(q + 1) * LDQ + t] = (_Float16)xv.y;
+    sXT[(q + 2) * LDQ + t] = (_Float16)xv.z;
+    sXT[(q + 3) * LDQ + t] = (_Float16)xv.w;
+  }
+  __syncthreads();
+  const float c_last = s_c[Q - 1];
+
+  if (kOut) {
+    const int tw = 16 * wave;  // the wave's 16 rows t
+    // S = C B^T (tiles of s up to the diagonal), masked and decayed into
+    // M[t][s] = S[t][s] 2^(A (c_t - c_s)) dt_s for s <= t
+    for (int jt = 0; jt < Q / 16; ++jt) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      if (jt <= wave) {
+#pragma unroll
+        for (int kk = 0; kk < N / 32; ++kk) {
+          const f16x8 a = *reinterpret_cast<const f16x8 *>(sC + (tw + r16) * LDN + 32 * kk + 8 * kq);
+          const f16x8 b = *reinterpret_cast<const f16x8 *>(sB + (16 * jt + r16) * LDN + 32 * kk + 8 * kq);
+          acc = mma_chunk(a, b, acc);
+        }
+      }
+      const int sc = 16 * jt + r16;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = tw + 4 * kq + i;
+        const float m = sc <= t ? acc[i] * exp2_fast(a2 * (s_c[t] - s_c[sc])) * s_dt[sc] : 0.f;
+        sM[t * LDQ + sc] = (_Float16)m;
+      }
+    }
+    __syncthreads();
+    // Y = 2^(A c_t) (C Hinit^T) + M X, then g = (y + D x) silu(z)
+    f32x4 y[P / 16];
+#pragma unroll
+    for (int jp = 0; jp < P / 16; ++jp) y[jp] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (init) {
+#pragma unroll
+      for (int kk = 0; kk < N / 32; ++kk) {
+        const f16x8 a = *reinterpret_cast<const f16x8 *>(sC + (tw + r16) * LDN + 32 * kk + 8 * kq);
+#pragma unroll
+        for (int jp = 0; jp < P / 16; ++jp) {
+          const f16x8 b = *reinterpret_cast<const f16x8 *>(sH + (16 * jp + r16) * LDN + 32 * kk + 8 * kq);
+          y[jp] = mma_chunk(a, b, y[jp]);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float e = exp2_fast(a2 * s_c[tw + 4 * kq + i]);
+#pragma unroll
+        for (int jp = 0; jp < P / 16; ++jp) y[jp][i] *= e;
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < Q / 32; ++kk) {
+      const f16x8 a = *reinterpret_cast<const f16x8 *>(sM + (tw + r16) * LDQ + 32 * kk + 8 * kq);
+#pragma unroll
+      for (int jp = 0; jp < P / 16; ++jp) {
+        const f16x8 b = *reinterpret_cast<const f16x8 *>(sXT + (16 * jp + r16) * LDQ + 32 * kk + 8 * kq);
+        y[jp] = mma_chunk(a, b, y[jp]);
+      }
+    }
+    const float Dh = p.D[h];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = tw + 4 * kq + i;
+      if (t < nt) {
+        const size_t row = (size_t)(t0 + t);
+#pragma unroll
+        for (int jp = 0; jp < P / 16; ++jp) {
+          const int col = h * P + 16 * jp + r16;
+          const float xv = p.xbc[row * p.conv_n + col];
+          const float zv = p.zxd[row * p.ldz + col];
+          p.g[row * di + col] = fmaf(Dh, xv, y[jp][i]) * silu_fast(zv);
+        }
+      }
+    }
+    if (!last) return;
+    __syncthreads();  // M and Hinit are read; their space takes w B
+  }
+
+  // h_end = 2^(A c_last) h_init + X^T diag(w) B, w_s = dt_s 2^(A (c_last - c_s)): w B staged
+  // transposed from the fp32 rows, then 16 x 16 tiles of [P][N] over the waves
+  for (int i = tid; i < Q * N; i += 256) {
+    const int t = i / N, n = i % N;
+    const float w = s_dt[t] * exp2_fast(a2 * (c_last - s_c[t]));
+    const float bv = t < nt ? xbc[(size_t)t * p.conv_n + di + grp * N + n] : 0.f;
+    sBT[n * LDQ + t] = (_Float16)(bv * w);
+  }
+  __syncthreads();
+  float *dst = kOut ? p.ssm + ((size_t)ch.x * p.H + h) * tile : p.hloc + ((size_t)j * p.H + h) * tile;
+  const float e_last = exp2_fast(a2 * c_last);
+  for (int q = wave; q < (P / 16) * (N / 16); q += 4) {
+    const int tp = q / (N / 16), tn = q % (N / 16);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < Q / 32; ++kk) {
+      const f16x8 a = *reinterpret_cast<const f16x8 *>(sXT + (16 * tp + r16) * LDQ + 32 * kk + 8 * kq);
+      const f16x8 b = *reinterpret_cast<const f16x8 *>(sBT + (16 * tn + r16) * LDQ + 32 * kk + 8 * kq);
+      acc = mma_chunk(a, b, acc);
+    }
+    const int n = 16 * tn + r16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int pr = 16 * tp + 4 * kq + i;
+      float v = acc[i];
+      if (init) v = fmaf(e_last, init[(size_t)pr * N + n], v);
+      dst[(size_t)pr * N + n] = v;
+    }
+  }
+  if (!kOut || !p.update_conv) return;
+  // The sequence's last K-1 conv inputs (old conv state followed by this call's rows), spread
+  // over the threads of the sequence's last-chunk blocks.
+  const int seq = ch.x, K1 = p.K - 1;
+  const int t0s = p.cu[seq], len = p.cu[seq + 1] - t0s;
+  for (int cc = blockIdx.x * 256 + tid; cc < p.conv_n; cc += gridDim.x * 256) {
+    float nv[3];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      if (q >= K1) continue;
+      const int pos = len + q;
+      nv[q] = pos < K1 ? (p.fresh ? 0.f : p.conv[((size_t)seq * K1 + pos) * p.conv_n + cc])
+                       : p.zxd[(size_t)(t0s + pos - K1) * p.ldz + p.conv_col + cc];
+    }
+#pragma unroll
+    for (int q = 0; q < 3; ++q)
+      if (q < K1) p.conv[((size_t)seq * K1 + q) * p.conv_n + cc] = nv[q];
+  }
+}
+
 bool m2_args_ok(const M2ScanArgs &a) {
   return a.zxd && a.xbc && a.dt_b && a.A2 && a.D && a.ssm && a.g && a.H > 0 && a.G > 0 &&
          a.H % a.G == 0 && a.P > 0 && a.P % kM2Rows == 0 && a.di == a.H * a.P &&
@@ -191,8 +420,25 @@ bool m2_args_ok(const M2ScanArgs &a) {
          a.conv_n == a.di + 2 * a.G * a.N && a.dt_col >= 0 && a.ldz >= a.dt_col + a.H;
 }
 
+template <bool kOut, int P>
+hipError_t ssd_launch_p(const M2ScanArgs &a, int n_chunks, hipStream_t s) {
+  const dim3 grid(a.H, n_chunks);
+  switch (a.N) {
+    case 32: LL_LAUNCH((k_m2_ssd<kOut, 32, P>), grid, dim3(256), 0, s, a); break;
+    case 64: LL_LAUNCH((k_m2_ssd<kOut, 64, P>), grid, dim3(256), 0, s, a); break;
+    case 128: LL_LAUNCH((k_m2_ssd<kOut, 128, P>), grid, dim3(256), 0, s, a); break;
+    case 256: LL_LAUNCH((k_m2_ssd<kOut, 256, P>), grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 template <bool kOut>
 hipError_t m2_launch(const M2ScanArgs &a, int n_chunks, hipStream_t s) {
+  if (a.mfma && a.chunks) {
+    if (!mamba2_ssd_ok(a.P, a.N)) return hipErrorInvalidValue;
+    return a.P == 32 ? ssd_launch_p<kOut, 32>(a, n_chunks, s) : ssd_launch_p<kOut, 64>(a, n_chunks, s);
+  }
   const dim3 grid(a.H * (a.P / kM2Rows), n_chunks);
   switch (a.N) {
     case 32: LL_LAUNCH((k_m2_scan<kOut, 2>), grid, dim3(kM2Threads), 0, s, a); break;
@@ -205,6 +451,11 @@ hipError_t m2_launch(const M2ScanArgs &a, int n_chunks, hipStream_t s) {
 }
 
 }  // namespace
+
+bool mamba2_ssd_ok(int head_dim, int d_state) {
+  return (head_dim == 32 || head_dim == 64) &&
+         (d_state == 32 || d_state == 64 || d_state == 128 || d_state == 256);
+}
 
 int mamba2_chunk_len(int total, int n_heads, int head_dim) {
   const long blocks_per_chunk = (long)n_heads * (head_dim / kM2Rows);

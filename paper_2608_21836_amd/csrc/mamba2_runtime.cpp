@@ -61,6 +61,12 @@ ll_status validate(const ll_mamba2_config *c) {
   return LL_OK;
 }
 
+// 16-bit models run the prefill scan in its matrix form on MFMA (fp16 operands); fp32 models
+// keep the fp32 step recurrence.
+bool use_ssd(const ll_mamba2_config &c) {
+  return c.dtype != LL_F32 && mamba2_ssd_ok(c.head_dim, c.d_state);
+}
+
 M2Layout make_layout(const ll_mamba2_config &c) {
   M2Layout L;
   const size_t eb = elem_bytes(c.dtype);
@@ -70,6 +76,9 @@ M2Layout make_layout(const ll_mamba2_config &c) {
   L.NZ = (c.d_inner + L.CD + L.H + 127) / 128 * 128;  // in_proj rows padded to 128 columns
   L.max_rows = std::max(c.max_prefill_tokens, c.max_batch);
   L.max_chunks = mamba2_max_chunks(c.max_prefill_tokens, c.max_batch, L.H, c.head_dim);
+  if (use_ssd(c))
+    L.max_chunks = std::max(L.max_chunks, (c.max_prefill_tokens + kM2SsdChunk - 1) / kM2SsdChunk +
+                                              c.max_batch);
   L.n_parts = c.vocab / 32;
   const size_t K1 = std::max(c.d_conv - 1, 1), H = L.H, CD = L.CD, NZ = L.NZ;
   size_t off = 0;
@@ -250,6 +259,7 @@ ll_status enqueue_layers(ll_mamba2 *m, int rows, const PrefillPlan *pp, hipStrea
       a.cu = m->at<int>(L.cu);
       a.fresh = pp->fresh;
       a.update_conv = 1;
+      a.mfma = use_ssd(c);
       if (pp->multi) {
         m->mark(LL_M2K_SCAN_CHUNK);
         LL_HIP(launch_m2_scan_chunks(a, pp->n_chunks, s));
@@ -431,7 +441,7 @@ ll_status ll_mamba2_prefill(ll_mamba2 *m, int32_t batch, const int32_t *seq_lens
     mm.lens[b] = seq_lens_host[b];
   }
   const int T = (int)total;
-  const int clen = mamba2_chunk_len(T, m->L.H, c.head_dim);
+  const int clen = use_ssd(c) ? kM2SsdChunk : mamba2_chunk_len(T, m->L.H, c.head_dim);
   PrefillPlan pp;
   pp.fresh = !cont;
   pp.batch = batch;
