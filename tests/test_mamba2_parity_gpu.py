@@ -84,3 +84,19 @@ def test_mamba2_chunked_prefill_parity(name, n_chunks):
     gl, gt = run_gpu_mamba(cfg, w, chunks, ref_t, nd)
     rep = _report(f"{name}-chunked", cfg.dtype, ref_l, gl, gt)
     assert rep.ok(cfg.dtype), rep
+
+
+# The matrix-form prefill scan of 16-bit models at the shapes the other cases leave out:
+# head dim 32 with state 256 and with state 128 (multi-chunk prompts, ragged last chunks).
+@pytest.mark.parametrize("name", ["t-mamba2-n256", "t-mamba2-f32"])
+def test_mamba2_matrix_scan_bf16(name):
+    base = S2.get_mamba2_config(name)
+    cfg = base.replace(name=f"{name}-bf16", dtype="bf16", head_dim=32, prompt_list=(40, 300))
+    log(f"mamba2 parity {cfg.name}: oracle ...")
+    w = S2.weights(cfg)
+    lens, packed = gen.prompt_tokens(cfg)
+    ref_l, ref_t = teacher_forced_run_mamba2(OracleMamba2(cfg, w), lens, packed, cfg.n_decode)
+    gl, gt = run_gpu_mamba(cfg, w, [split_prompts(lens, packed)], ref_t, cfg.n_decode,
+                           use_graph=True, options={})
+    rep = _report(cfg.name, cfg.dtype, ref_l, gl, gt)
+    assert rep.ok(cfg.dtype), rep
