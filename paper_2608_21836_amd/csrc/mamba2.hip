@@ -204,6 +204,13 @@ __global__ __launch_bounds__(256) void k_m2_carry(M2ScanArgs p) {
 // LDS layout (fp16 elements).  Pass 3: C and B rows, x transposed, the masked decayed scores and
 // the incoming state; the transposed w B of the end state reuses the space of the last two once
 // the outputs are done.  Pass 1: w B and x, both transposed.
+__device__ __forceinline__ void store4_f16(_Float16 *d, float4 v) {
+  d[0] = (_Float16)v.x;
+  d[1] = (_Float16)v.y;
+  d[2] = (_Float16)v.z;
+  d[3] = (_Float16)v.w;
+}
+
 template <bool kOut, int N, int P>
 struct SsdLds {
   static constexpr int LDN = N + 8, LDQ = kM2SsdChunk + 8;  // padded rows
@@ -244,50 +251,71 @@ __global__ __launch_bounds__(256) void k_m2_ssd(M2ScanArgs p) {
   if (kOut && p.carry == 2) init = p.hloc + ((size_t)j * p.H + h) * tile;
   const float *xbc = p.xbc + (size_t)t0 * p.conv_n;
 
-  // dt and the cumulative dt of the chunk (steps past its end: dt = 0)
-  if (tid < Q)
-    s_dt[tid] = tid < nt ? softplus_f(p.zxd[(size_t)(t0 + tid) * p.ldz + p.dt_col + h] + bias) : 0.f;
-  __syncthreads();
-  if (tid == 0) {
-    float c = 0.f;
-    for (int t = 0; t < Q; ++t) {
-      c += s_dt[t];
-      s_c[t] = c;
+  // dt and the cumulative dt of the chunk (steps past its end: dt = 0), as an inclusive scan
+  // over the lanes of wave 0 (lane t = step t)
+  static_assert(Q == 64, "one step per lane of a wave");
+  if (wave == 0) {
+    const float dtv = lane < nt ? softplus_f(p.zxd[(size_t)(t0 + lane) * p.ldz + p.dt_col + h] + bias) : 0.f;
+    float c = dtv;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const float u = __shfl_up(c, o, 64);
+      if (lane >= o) c += u;
     }
-    if (!kOut) p.dtsum[(size_t)j * p.H + h] = c;
+    s_dt[lane] = dtv;
+    s_c[lane] = c;
+    if (!kOut && lane == 63) p.dtsum[(size_t)j * p.H + h] = c;
   }
-  // operands in fp16; rows past the chunk are zero
+  // Operands in fp16; rows past the chunk are zero.  Every thread requests all of its loads
+  // before its first LDS store, so the global latencies overlap instead of adding up.
   constexpr int NV = N / 4, PV = P / 4;
-  if (kOut) {
-    for (int i = tid; i < Q * NV; i += 256) {
-      const int t = i / NV, n = 4 * (i % NV);
-      float4 bv = make_float4(0.f, 0.f, 0.f, 0.f), cv = bv;
-      if (t < nt) {
+  constexpr int NBC = Q * NV / 256, NH = P * NV / 256, NX = Q * PV / 256;
+  static_assert(Q * NV % 256 == 0 && P * NV % 256 == 0 && Q * PV % 256 == 0, "whole rounds");
+  {
+    float4 xv[NX];
+#pragma unroll
+    for (int k = 0; k < NX; ++k) {
+      const int i = tid + 256 * k, t = i / PV, q = 4 * (i % PV);
+      xv[k] = t < nt ? *reinterpret_cast<const float4 *>(xbc + (size_t)t * p.conv_n + h * P + q)
+                     : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    if (kOut) {
+      float4 bv[NBC], cv[NBC];
+#pragma unroll
+      for (int k = 0; k < NBC; ++k) {
+        const int i = tid + 256 * k, t = i / NV, n = 4 * (i % NV);
         const float *row = xbc + (size_t)t * p.conv_n + di + grp * N + n;
-        bv = *reinterpret_cast<const float4 *>(row);
-        cv = *reinterpret_cast<const float4 *>(row + GN);
+        bv[k] = t < nt ? *reinterpret_cast<const float4 *>(row) : make_float4(0.f, 0.f, 0.f, 0.f);
+        cv[k] = t < nt ? *reinterpret_cast<const float4 *>(row + GN) : make_float4(0.f, 0.f, 0.f, 0.f);
       }
-      _Float16 *b = sB + t * LDN + n, *c = sC + t * LDN + n;
-      b[0] = (_Float16)bv.x; b[1] = (_Float16)bv.y; b[2] = (_Float16)bv.z; b[3] = (_Float16)bv.w;
-      c[0] = (_Float16)cv.x; c[1] = (_Float16)cv.y; c[2] = (_Float16)cv.z; c[3] = (_Float16)cv.w;
-    }
-    if (init) {
-      for (int i = tid; i < P * NV; i += 256) {
-        const int q = i / NV, n = 4 * (i % NV);
-        const float4 v = *reinterpret_cast<const float4 *>(init + (size_t)q * N + n);
-        _Float16 *d = sH + q * LDN + n;
-        d[0] = (_Float16)v.x; d[1] = (_Float16)v.y; d[2] = (_Float16)v.z; d[3] = (_Float16)v.w;
+#pragma unroll
+      for (int k = 0; k < NBC; ++k) {
+        const int i = tid + 256 * k, t = i / NV, n = 4 * (i % NV);
+        store4_f16(sB + t * LDN + n, bv[k]);
+        store4_f16(sC + t * LDN + n, cv[k]);
+      }
+      if (init) {
+        float4 hv[NH];
+#pragma unroll
+        for (int k = 0; k < NH; ++k) {
+          const int i = tid + 256 * k, q = i / NV, n = 4 * (i % NV);
+          hv[k] = *reinterpret_cast<const float4 *>(init + (size_t)q * N + n);
+        }
+#pragma unroll
+        for (int k = 0; k < NH; ++k) {
+          const int i = tid + 256 * k, q = i / NV, n = 4 * (i % NV);
+          store4_f16(sH + q * LDN + n, hv[k]);
+        }
       }
     }
-  }
-  for (int i = tid; i < Q * PV; i += 256) {
-    const int t = i / PV, q = 4 * (i % PV);
-    float4 xv = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (t < nt) xv = *reinterpret_cast<const float4 *>(xbc + (size_t)t * p.conv_n + h * P + q);
-    sXT[(q + 0) * LDQ + t] = (_Float16)xv.x;
-    sXT[(q + 1) * LDQ + t] = (_Float16)xv.y;
-    sXT[(q + 2) * LDQ + t] = (_Float16)xv.z;
-    sXT[(q + 3) * LDQ + t] = (_Float16)xv.w;
+#pragma unroll
+    for (int k = 0; k < NX; ++k) {
+      const int i = tid + 256 * k, t = i / PV, q = 4 * (i % PV);
+      sXT[(q + 0) * LDQ + t] = (_Float16)xv[k].x;
+      sXT[(q + 1) * LDQ + t] = (_Float16)xv[k].y;
+      sXT[(q + 2) * LDQ + t] = (_Float16)xv[k].z;
+      sXT[(q + 3) * LDQ + t] = (_Float16)xv[k].w;
+    }
   }
   __syncthreads();
   const float c_last = s_c[Q - 1];
@@ -346,18 +374,25 @@ __global__ __launch_bounds__(256) void k_m2_ssd(M2ScanArgs p) {
       }
     }
     const float Dh = p.D[h];
+    float xo[4][P / 16], zo[4][P / 16];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const size_t row = (size_t)(t0 + min(tw + 4 * kq + i, nt - 1));
+#pragma unroll
+      for (int jp = 0; jp < P / 16; ++jp) {
+        const int col = h * P + 16 * jp + r16;
+        xo[i][jp] = p.xbc[row * p.conv_n + col];
+        zo[i][jp] = p.zxd[row * p.ldz + col];
+      }
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int t = tw + 4 * kq + i;
       if (t < nt) {
         const size_t row = (size_t)(t0 + t);
 #pragma unroll
-        for (int jp = 0; jp < P / 16; ++jp) {
-          const int col = h * P + 16 * jp + r16;
-          const float xv = p.xbc[row * p.conv_n + col];
-          const float zv = p.zxd[row * p.ldz + col];
-          p.g[row * di + col] = fmaf(Dh, xv, y[jp][i]) * silu_fast(zv);
-        }
+        for (int jp = 0; jp < P / 16; ++jp)
+          p.g[row * di + h * P + 16 * jp + r16] = fmaf(Dh, xo[i][jp], y[jp][i]) * silu_fast(zo[i][jp]);
       }
     }
     if (!last) return;
@@ -366,17 +401,40 @@ __global__ __launch_bounds__(256) void k_m2_ssd(M2ScanArgs p) {
 
   // h_end = 2^(A c_last) h_init + X^T diag(w) B, w_s = dt_s 2^(A (c_last - c_s)): w B staged
   // transposed from the fp32 rows, then 16 x 16 tiles of [P][N] over the waves
-  for (int i = tid; i < Q * N; i += 256) {
-    const int t = i / N, n = i % N;
-    const float w = s_dt[t] * exp2_fast(a2 * (c_last - s_c[t]));
-    const float bv = t < nt ? xbc[(size_t)t * p.conv_n + di + grp * N + n] : 0.f;
-    sBT[n * LDQ + t] = (_Float16)(bv * w);
+  {
+    float4 bv[NBC];
+#pragma unroll
+    for (int k = 0; k < NBC; ++k) {
+      const int i = tid + 256 * k, t = i / NV, n = 4 * (i % NV);
+      bv[k] = t < nt ? *reinterpret_cast<const float4 *>(xbc + (size_t)t * p.conv_n + di + grp * N + n)
+                     : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int k = 0; k < NBC; ++k) {
+      const int i = tid + 256 * k, t = i / NV, n = 4 * (i % NV);
+      const float w = s_dt[t] * exp2_fast(a2 * (c_last - s_c[t]));
+      sBT[(n + 0) * LDQ + t] = (_Float16)(bv[k].x * w);
+      sBT[(n + 1) * LDQ + t] = (_Float16)(bv[k].y * w);
+      sBT[(n + 2) * LDQ + t] = (_Float16)(bv[k].z * w);
+      sBT[(n + 3) * LDQ + t] = (_Float16)(bv[k].w * w);
+    }
   }
   __syncthreads();
   float *dst = kOut ? p.ssm + ((size_t)ch.x * p.H + h) * tile : p.hloc + ((size_t)j * p.H + h) * tile;
   const float e_last = exp2_fast(a2 * c_last);
-  for (int q = wave; q < (P / 16) * (N / 16); q += 4) {
-    const int tp = q / (N / 16), tn = q % (N / 16);
+  constexpr int TPW = (P / 16) * (N / 16) / 4;  // 16 x 16 tiles per wave
+  static_assert((P / 16) * (N / 16) % 4 == 0, "tiles split evenly over the waves");
+  float iv[TPW][4];
+#pragma unroll
+  for (int r = 0; r < TPW; ++r) {
+    const int q = wave + 4 * r, tp = q / (N / 16), tn = q % (N / 16);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      iv[r][i] = init ? init[(size_t)(16 * tp + 4 * kq + i) * N + 16 * tn + r16] : 0.f;
+  }
+#pragma unroll
+  for (int r = 0; r < TPW; ++r) {
+    const int q = wave + 4 * r, tp = q / (N / 16), tn = q % (N / 16);
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < Q / 32; ++kk) {
@@ -387,10 +445,7 @@ __global__ __launch_bounds__(256) void k_m2_ssd(M2ScanArgs p) {
     const int n = 16 * tn + r16;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int pr = 16 * tp + 4 * kq + i;
-      float v = acc[i];
-      if (init) v = fmaf(e_last, init[(size_t)pr * N + n], v);
-      dst[(size_t)pr * N + n] = v;
+      dst[(size_t)(16 * tp + 4 * kq + i) * N + n] = fmaf(e_last, iv[r][i], acc[i]);
     }
   }
   if (!kOut || !p.update_conv) return;
