@@ -129,7 +129,7 @@ struct EpiStore {
 struct EpiResid {
   float *out;
   int ld;
-  static constexpr bool kArgmax = false, kPairs = false, kVec8 = false, kAtomicSplit = true;
+  static constexpr bool kArgmax = false, kPairs = false, kVec8 = true, kAtomicSplit = true;
   // K split over blocks: each block adds its partial sum (fp32 atomics; order not fixed)
   __device__ void add_atomic(int m, int col, float v, bool) const {
     unsafeAtomicAdd(out + (size_t)m * ld + col, v);
@@ -140,6 +140,25 @@ struct EpiResid {
     p[16] += v1;
   }
   __device__ void one(int m, int col, float v) const { out[(size_t)m * ld + col] += v; }
+  // 16-byte read-modify-writes when the rows are 16-byte aligned
+  __device__ void vec8(int m, int u, int c0, const float *a, const float *b) const {
+    float *r = out + (size_t)m * ld + 32 * u + c0;
+    if (((ld & 3) | (int)(reinterpret_cast<uintptr_t>(out) & 15)) != 0) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        r[e] += a[e];
+        r[16 + e] += b[e];
+      }
+      return;
+    }
+    float4 *p = reinterpret_cast<float4 *>(r), *q = reinterpret_cast<float4 *>(r + 16);
+    float4 p0 = p[0], p1 = p[1], q0 = q[0], q1 = q[1];
+    p0.x += a[0]; p0.y += a[1]; p0.z += a[2]; p0.w += a[3];
+    p1.x += a[4]; p1.y += a[5]; p1.z += a[6]; p1.w += a[7];
+    q0.x += b[0]; q0.y += b[1]; q0.z += b[2]; q0.w += b[3];
+    q1.x += b[4]; q1.y += b[5]; q1.z += b[6]; q1.w += b[7];
+    p[0] = p0; p[1] = p1; q[0] = q0; q[1] = q1;
+  }
 };
 
 template <typename T> struct EpiSwiglu {
