@@ -650,7 +650,10 @@ def main() -> int:
         "prefill": {"achieved": round(pre_flop / (pre_ms / 1e3) / 1e12, 2), "unit": "TFLOP/s",
                     "peak": MFMA_PEAK_TFLOPS[op_dtype],
                     "frac": round(pre_flop / (pre_ms / 1e3) / 1e12 / MFMA_PEAK_TFLOPS[op_dtype], 4),
-                    "work": "MFMA flops (projections" + ("" if mamba else " + causal attention") + ")"},
+                    "work": "MFMA flops (projections" + (
+                        " + causal attention" if not mamba else
+                        " + matrix-form scan" if work_all.get(("prefill", "scan"), (0, ""))[1] == "flop"
+                        else "") + ")"},
         "decode": {"achieved": round(dec_byte / (dec_ms / 1e3) / 1e9, 2), "unit": "GB/s",
                    "peak": HBM_PEAK_GBS,
                    "frac": round(dec_byte / (dec_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
