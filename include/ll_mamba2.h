@@ -13,6 +13,10 @@
  *     h_t = exp(dt_t A) h_{t-1} + dt_t x_t B_t^T,   y_t = h_t C_t + D x_t,
  *   x += out_proj( RMSNorm(y * silu(z)) * gnorm ),
  * then a final RMSNorm and an LM head tied to the embedding, greedy argmax.
+ * Prefill of bf16 models evaluates the scan over chunks of 64 steps in its matrix form
+ * (C B^T masked and decayed, times x, plus the incoming state's term) on fp16 MFMAs with fp32
+ * accumulation, which is the same recurrence unrolled; fp32 models and decode run the step
+ * recurrence in fp32.
  *
  * Conventions are those of ll.h (statuses, ll_last_error, no device allocation, work on the
  * caller's stream, one host thread per handle).
