@@ -1059,7 +1059,7 @@ __global__ __launch_bounds__(512) void k_gemm_splitk(const T *__restrict__ A, in
                                                      float *__restrict__ part) {
   constexpr int kts = KTS;
   using F = typename Frag<T>::type;
-  constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL, NW = 8, U = 16;
+  constexpr int EPL = Frag<T>::EPL, TK = 4 * EPL, NW = 8, U = 32;
   __shared__ uint4 sAk[2 * KTS * 64];  // [k-tile][row block][64]
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1068,8 +1068,9 @@ __global__ __launch_bounds__(512) void k_gemm_splitk(const T *__restrict__ A, in
   const int kt0 = blockIdx.y * kts, nk = min(kts, kb_n - kt0);
   const F fz = frag_zero<F>();
   const uint8_t *wp = Wt + (((size_t)ct * kb_n + kt0) * 64 + lane) * 16;
-  // The weight stream starts first: a ring of U tiles in flight, each slot refilled with the
-  // tile U ahead as soon as it has been consumed, so the stream never drains between batches.
+  // The weight stream starts first: a ring of U tiles (32 KiB per wave) in flight, each slot
+  // refilled with the tile U ahead as soon as it has been consumed, so the stream never drains
+  // between batches (32 tiles measured 3 % faster than 16 on the 8b-gqa gate/up shape).
   // (The scheduling barriers keep the loads in ring order, so the wait before tile q is for
   // the q-th oldest load only.)
   F bw[U];
