@@ -141,6 +141,48 @@ def test_ssd_scan_closed_forms():
     np.testing.assert_allclose(hT, np.exp(Tn * dt[0] * A)[:, None, None] * h0, rtol=1e-12)
 
 
+def _chunked_matrix_form(x, dt, A, B, C, D, h0, goh, Q):
+    """The same scan as products over chunks of Q steps (state-space duality form), written
+    out independently of the oracle: per chunk and head, with c the running sum of dt,
+    y = diag(e^{A c}) C h_in^T + ((C B^T) o L) x + D x, L[t, s] = e^{A (c_t - c_s)} dt_s (s <= t),
+    and h_out = e^{A c_last} h_in + x^T diag(dt_s e^{A (c_last - c_s)}) B."""
+    Tn, H, P = x.shape
+    h = np.array(h0, dtype=np.float64)
+    y = np.empty((Tn, H, P))
+    for t0 in range(0, Tn, Q):
+        q = min(Q, Tn - t0)
+        for hh in range(H):
+            Bc, Cc = B[t0:t0 + q, goh[hh]], C[t0:t0 + q, goh[hh]]      # [q, N]
+            xc, dc = x[t0:t0 + q, hh], dt[t0:t0 + q, hh]                 # [q, P], [q]
+            c = np.cumsum(dc)
+            L = np.tril(np.exp(A[hh] * (c[:, None] - c[None, :])) * dc[None, :])
+            y[t0:t0 + q, hh] = (np.exp(A[hh] * c)[:, None] * (Cc @ h[hh].T)
+                                + ((Cc @ Bc.T) * L) @ xc + D[hh] * xc)
+            w = dc * np.exp(A[hh] * (c[-1] - c))
+            h[hh] = np.exp(A[hh] * c[-1]) * h[hh] + xc.T @ (w[:, None] * Bc)
+    return y, h
+
+
+@pytest.mark.parametrize("Q", [1, 7, 64])
+def test_ssd_scan_equals_its_chunked_matrix_form(Q):
+    """The identity the GPU's prefill scan of 16-bit models evaluates (chunks of 64 steps as
+    matrix products) pinned against the step recurrence: several chunks, a ragged last one,
+    two B/C groups and a nonzero incoming state."""
+    rng = np.random.default_rng(12)
+    Tn, H, P, N, G = 150, 4, 5, 6, 2
+    goh = np.arange(H) // (H // G)
+    x = rng.standard_normal((Tn, H, P))
+    dt = np.exp(rng.uniform(-4, 0, (Tn, H)))
+    A = -np.exp(rng.standard_normal(H))
+    B, C = rng.standard_normal((Tn, G, N)), rng.standard_normal((Tn, G, N))
+    D = rng.standard_normal(H)
+    h0 = rng.standard_normal((H, P, N))
+    y_ref, h_ref = M2.ssd_scan(x, dt, A, B, C, D, h0, goh)
+    y, h = _chunked_matrix_form(x, dt, A, B, C, D, h0, goh, Q)
+    np.testing.assert_allclose(y, y_ref, rtol=1e-10, atol=1e-11)
+    np.testing.assert_allclose(h, h_ref, rtol=1e-10, atol=1e-11)
+
+
 @pytest.mark.parametrize("split", [1, 4, 11])
 def test_incremental_decode_and_continuation_equal_full_recompute(split):
     cfg = MICRO
