@@ -379,7 +379,8 @@ def host_info():
 
 def device_context():
     """Context figures measured on this GPU (the fractions use the datasheet peaks): a device
-    copy's read + write bandwidth and the bf16 rate of an MFMA-only loop, each from events."""
+    copy's read + write bandwidth, a read-only stream's bandwidth and the bf16 rate of an
+    MFMA-only loop, each from events."""
     import torch
     from paper_2608_21836_amd.binding import op_mfma_loop
     src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")      # 1 GiB
@@ -392,7 +393,17 @@ def device_context():
     e1.record()
     e1.synchronize()
     copy_gbs = 5 * 2 * src.numel() * 4 / (e0.elapsed_time(e1) / 1e3) / 1e9
-    del src, dst
+    # read-only stream over the same 1 GiB (ll_op_read_stream), 64 KiB per block
+    from paper_2608_21836_amd.binding import op_read_stream
+    rb = src.numel() * 4 // 65536
+    sums = op_read_stream(src, rb)
+    e0.record()
+    for _ in range(5):
+        op_read_stream(src, rb, sums)
+    e1.record()
+    e1.synchronize()
+    read_gbs = 5 * src.numel() * 4 / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del src, dst, sums
     blocks, iters = 4096, 4096
     out = op_mfma_loop(blocks, 16)
     e0.record()
@@ -400,7 +411,8 @@ def device_context():
     e1.record()
     e1.synchronize()
     mfma_tflops = blocks * 4 * iters * 8 * 16384 / (e0.elapsed_time(e1) / 1e3) / 1e12
-    return {"copy_GBs": round(copy_gbs, 1), "mfma_loop_bf16_TFLOPs": round(mfma_tflops, 1)}
+    return {"copy_GBs": round(copy_gbs, 1), "read_GBs": round(read_gbs, 1),
+            "mfma_loop_bf16_TFLOPs": round(mfma_tflops, 1)}
 
 
 def cpu_baseline_mamba(cfg, lens, packed, n_decode, budget_s, weights=None):

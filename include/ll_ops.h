@@ -135,6 +135,16 @@ ll_status ll_op_lmhead_argmax_noalloc(int32_t dtype, int32_t rows, int32_t vocab
  * wave. */
 ll_status ll_op_mfma_loop(int32_t blocks, int32_t iters, float *out_dev, void *stream);
 
+/* Calibration, not part of the model: a read-only stream over n fp32 values of src_dev (device,
+ * n a multiple of 4, 16-byte aligned) by blocks of 256 threads, block b reading the b-th of
+ * `blocks` contiguous, equal ranges with eight non-temporal 16-byte loads in flight per
+ * thread; out_dev fp32 [blocks] receives each block's sum of what it read (the sum of all of
+ * them is the sum of src).  Measures the HBM read rate this GPU sustains,
+ * reported beside the datasheet peak.  LL_ERR_INVALID_ARGUMENT for n < 0, n not a multiple of
+ * 4, blocks < 1, a NULL out_dev, or a NULL / misaligned src_dev with n > 0. */
+ll_status ll_op_read_stream(const float *src_dev, int64_t n, int32_t blocks, float *out_dev,
+                            void *stream);
+
 #ifdef __cplusplus
 }
 #endif

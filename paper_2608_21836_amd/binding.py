@@ -8,7 +8,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from ctypes import POINTER, c_char_p, c_double, c_float, c_int32, c_size_t, c_uint64, c_void_p
+from ctypes import POINTER, c_char_p, c_double, c_float, c_int32, c_int64, c_size_t, c_uint64, c_void_p
 from typing import Dict, List, Optional, Sequence, Tuple
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libll.so")
@@ -126,6 +126,7 @@ SIGNATURES = [
                                        POINTER(c_char_p), POINTER(c_int32)]),
     ("ll_kv_pages", c_int32, [c_void_p, POINTER(c_int32), POINTER(c_int32)]),
     ("ll_op_mfma_loop", c_int32, [c_int32, c_int32, c_void_p, c_void_p]),
+    ("ll_op_read_stream", c_int32, [c_void_p, c_int64, c_int32, c_void_p, c_void_p]),
     ("ll_set_decode_graph", c_int32, [c_void_p, c_int32]),
     ("ll_set_option", c_int32, [c_void_p, c_int32, c_int32]),
     ("ll_get_option", c_int32, [c_void_p, c_int32, POINTER(c_int32)]),
@@ -638,6 +639,17 @@ def op_mfma_loop(blocks: int, iters: int, out=None, stream=None):
         out = torch.empty(4 * blocks, dtype=torch.float32, device="cuda")
     _check(load_library().ll_op_mfma_loop(blocks, iters, out.data_ptr(), _stream_handle(stream)),
            "ll_op_mfma_loop")
+    return out
+
+
+def op_read_stream(src, blocks: int, out=None, stream=None):
+    """Calibration read stream over an fp32 device tensor (ll_op_read_stream); returns the
+    per-block sums."""
+    import torch
+    if out is None:
+        out = torch.empty(blocks, dtype=torch.float32, device="cuda")
+    _check(load_library().ll_op_read_stream(src.data_ptr(), src.numel(), blocks, out.data_ptr(),
+                                            _stream_handle(stream)), "ll_op_read_stream")
     return out
 
 

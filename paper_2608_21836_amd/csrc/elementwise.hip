@@ -278,6 +278,42 @@ hipError_t launch_prefill_meta(const PrefillMeta &pm, int total, int qtile, int 
   return hipGetLastError();
 }
 
+// Calibration: a read-only stream over n4 float4 in which block b reads its own contiguous
+// range [b per, (b + 1) per) (per = ceil(n4 / blocks)), eight non-temporal 16-byte loads in
+// flight per thread; each block writes the sum of what it read to out[block].  (Contiguous
+// ranges per block stream measurably faster than a grid-stride walk over the same bytes.)
+__global__ __launch_bounds__(256) void k_read_stream(const f32x4 *__restrict__ src, long n4,
+                                                     float *__restrict__ out) {
+  constexpr int U = 8;
+  const long per = (n4 + gridDim.x - 1) / gridDim.x;
+  const long lo = min((long)blockIdx.x * per, n4), hi = min(lo + per, n4);
+  float acc = 0.f;
+  long i = lo + threadIdx.x;
+  for (; i + (U - 1) * 256 < hi; i += U * 256) {
+    f32x4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(src + i + u * 256);
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc += (v[u][0] + v[u][1]) + (v[u][2] + v[u][3]);
+  }
+  for (; i < hi; i += 256) {
+    const f32x4 v = __builtin_nontemporal_load(src + i);
+    acc += (v[0] + v[1]) + (v[2] + v[3]);
+  }
+  __shared__ float s_w[4];
+  acc = wave_sum(acc);
+  if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) out[blockIdx.x] = (s_w[0] + s_w[1]) + (s_w[2] + s_w[3]);
+}
+
+hipError_t launch_read_stream(const float *src, long n, int blocks, float *out, hipStream_t s) {
+  if (n < 0 || n % 4 || blocks < 1 || !out || (n && !src)) return hipErrorInvalidValue;
+  LL_LAUNCH(k_read_stream, dim3(blocks), dim3(256), 0, s, reinterpret_cast<const f32x4 *>(src),
+            n / 4, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_mfma_loop(int blocks, int iters, float *out, hipStream_t s) {
   if (blocks < 1 || iters < 1 || !out) return hipErrorInvalidValue;
   LL_LAUNCH(k_mfma_loop, dim3(blocks), dim3(256), 0, s, iters, out);

@@ -218,6 +218,7 @@ hipError_t launch_rmsnorm(int dtype, const float *x, int ldx, const int *rowmap,
 // MFMA-only calibration loop: `blocks` blocks of 4 waves, each wave iters x 8 MFMAs of
 // 16x16x32 bf16 (2 * 16 * 16 * 32 flops each); out receives 4 floats per block.
 hipError_t launch_mfma_loop(int blocks, int iters, float *out, hipStream_t s);
+hipError_t launch_read_stream(const float *src, long n, int blocks, float *out, hipStream_t s);
 hipError_t launch_argmax_reduce(const float *part_val, const int *part_idx, int rows,
                                 int n_parts, int *next, int *lens_inc, hipStream_t s);
 

@@ -857,6 +857,17 @@ ll_status ll_op_mfma_loop(int32_t blocks, int32_t iters, float *out_dev, void *s
   return LL_OK;
 }
 
+ll_status ll_op_read_stream(const float *src_dev, int64_t n, int32_t blocks, float *out_dev,
+                            void *stream) {
+  g_err.clear();
+  if (n < 0 || n % 4 || blocks < 1 || !out_dev)
+    return fail(LL_ERR_INVALID_ARGUMENT, "n >= 0 a multiple of 4, blocks >= 1 and out_dev required");
+  if (n > 0 && (!src_dev || (reinterpret_cast<uintptr_t>(src_dev) & 15)))
+    return fail(LL_ERR_INVALID_ARGUMENT, "src_dev must be set and 16-byte aligned");
+  LL_HIP(launch_read_stream(src_dev, (long)n, blocks, out_dev, (hipStream_t)stream));
+  return LL_OK;
+}
+
 ll_status ll_op_repack(int32_t dtype, int32_t n, int32_t k, const void *w, void *wt, void *stream) {
   g_err.clear();
   ll_status st = check_dtype(dtype);

@@ -345,3 +345,21 @@ def test_mfma_calibration_loop_runs():
     assert out.shape == (32,) and torch.isfinite(out).all()
     with pytest.raises(LLError):
         op_mfma_loop(0, 4)
+
+
+@pytest.mark.parametrize("n,blocks", [(0, 4), (12, 3), ((1 << 20) + 12, 64), ((1 << 22) + 4, 2048)])
+def test_read_stream_calibration_sums_everything_once(n, blocks):
+    """The read-stream calibration (ll_op_read_stream) reads every element exactly once: with
+    small integers the per-block sums are exact in fp32, so their total equals the buffer's
+    sum (the tail past the unrolled rounds included); bad arguments are rejected."""
+    import torch
+    from paper_2608_21836_amd.binding import LLError, op_read_stream
+    src = (torch.arange(n, device="cuda", dtype=torch.int64) % 3).to(torch.float32)
+    out = op_read_stream(src, blocks)
+    torch.cuda.synchronize()
+    assert out.shape == (blocks,)
+    assert int(out.double().sum().item()) == int(src.double().sum().item())
+    with pytest.raises(LLError):
+        op_read_stream(src[:2] if n else torch.empty(2, device="cuda"), blocks)   # n % 4 != 0
+    with pytest.raises(LLError):
+        op_read_stream(src, 0)
