@@ -41,8 +41,11 @@ __global__ __launch_bounds__(256) void k_attn_prefill(
   __shared__ F sK[NKS * NQC * 64];
   __shared__ __attribute__((aligned(16))) T sV[NDS * NPV * 64 * EPL];
 
-  const int2 qt = qtiles[blockIdx.x];
-  const int b = qt.x, h = blockIdx.y, kvh = h / (hq / hkv);
+  // grid (head, query tile): blocks are dealt round-robin to the 8 XCDs in dispatch order, so
+  // head-fastest order gives every XCD the same mix of short and long causal tiles (the tile
+  // list is ordered longest first)
+  const int2 qt = qtiles[blockIdx.y];
+  const int b = qt.x, h = blockIdx.x, kvh = h / (hq / hkv);
   const int tok0 = cu[b], L = cu[b + 1] - tok0;
   // queries sit at positions P0 + i after P0 cached keys; KL keys in all
   const int P0 = kstart ? kstart[b] : 0, KL = P0 + L;
@@ -395,8 +398,11 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
   static_assert(QT == 128 && KTILES % 4 == 0 && VINS % 4 == 0, "4 waves of 32 queries");
   __shared__ uint4 smem[2 * STAGE];
 
-  const int2 qt = qtiles[blockIdx.x];
-  const int b = qt.x, h = blockIdx.y, kvh = h / (hq / hkv);
+  // grid (head, query tile): blocks are dealt round-robin to the 8 XCDs in dispatch order, so
+  // head-fastest order gives every XCD the same mix of short and long causal tiles (the tile
+  // list is ordered longest first)
+  const int2 qt = qtiles[blockIdx.y];
+  const int b = qt.x, h = blockIdx.x, kvh = h / (hq / hkv);
   const int tok0 = cu[b], L = cu[b + 1] - tok0;
   // queries sit at positions P0 + i after P0 cached keys; KL keys in all
   const int P0 = kstart ? kstart[b] : 0, KL = P0 + L;
@@ -780,12 +786,12 @@ hipError_t run_prefill(const void *q, int ldq, const void *kc, const void *vc, v
                        int hq, int hkv, int max_ctx, hipStream_t s, const KvPaging &pg) {
   const float scale_log2 = kLog2e / sqrtf((float)HD);
   if constexpr (!std::is_same<T, float>::value) {
-    LL_LAUNCH((k_attn_prefill_wide<T, HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
+    LL_LAUNCH((k_attn_prefill_wide<T, HD>), dim3(hq, n_qtiles), dim3(256), 0, s,
               reinterpret_cast<const T *>(q), ldq, reinterpret_cast<const T *>(kc),
               reinterpret_cast<const T *>(vc), reinterpret_cast<T *>(o), ldo, cu, kstart,
               qtiles, hq, hkv, max_ctx, scale_log2, pg);
   } else {
-    LL_LAUNCH((k_attn_prefill<T, HD>), dim3(n_qtiles, hq), dim3(256), 0, s,
+    LL_LAUNCH((k_attn_prefill<T, HD>), dim3(hq, n_qtiles), dim3(256), 0, s,
               reinterpret_cast<const T *>(q), ldq, reinterpret_cast<const T *>(kc),
               reinterpret_cast<const T *>(vc), reinterpret_cast<T *>(o), ldo, cu, kstart, qtiles,
               hq, hkv, max_ctx, scale_log2, pg);
