@@ -42,9 +42,12 @@ __global__ __launch_bounds__(256) void k_attn_prefill(
   __shared__ __attribute__((aligned(16))) T sV[NDS * NPV * 64 * EPL];
 
   // grid (head, query tile): blocks are dealt round-robin to the 8 XCDs in dispatch order, so
-  // head-fastest order gives every XCD the same mix of short and long causal tiles (the tile
-  // list is ordered longest first)
-  const int2 qt = qtiles[blockIdx.y];
+  // head-fastest order gives every XCD the same mix of short and long causal tiles; the tile
+  // list is ordered longest first and its second half is walked backwards, so that the blocks
+  // dispatched second to a CU's slots are the short ones
+  const int ny = gridDim.y, yh = (ny + 1) / 2;
+  const int yi = blockIdx.y < yh ? blockIdx.y : ny - 1 - (blockIdx.y - yh);
+  const int2 qt = qtiles[yi];
   const int b = qt.x, h = blockIdx.x, kvh = h / (hq / hkv);
   const int tok0 = cu[b], L = cu[b + 1] - tok0;
   // queries sit at positions P0 + i after P0 cached keys; KL keys in all
@@ -399,9 +402,12 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill_wide(
   __shared__ uint4 smem[2 * STAGE];
 
   // grid (head, query tile): blocks are dealt round-robin to the 8 XCDs in dispatch order, so
-  // head-fastest order gives every XCD the same mix of short and long causal tiles (the tile
-  // list is ordered longest first)
-  const int2 qt = qtiles[blockIdx.y];
+  // head-fastest order gives every XCD the same mix of short and long causal tiles; the tile
+  // list is ordered longest first and its second half is walked backwards, so that the blocks
+  // dispatched second to a CU's slots are the short ones
+  const int ny = gridDim.y, yh = (ny + 1) / 2;
+  const int yi = blockIdx.y < yh ? blockIdx.y : ny - 1 - (blockIdx.y - yh);
+  const int2 qt = qtiles[yi];
   const int b = qt.x, h = blockIdx.x, kvh = h / (hq / hkv);
   const int tok0 = cu[b], L = cu[b + 1] - tok0;
   // queries sit at positions P0 + i after P0 cached keys; KL keys in all
