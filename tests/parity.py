@@ -1,7 +1,7 @@
 """Shared helpers for the GPU parity tests: running a workload through the C ABI and judging
 it against the oracle.
 
-Acceptance rules (the readings listed in the design doc):
+Acceptance rules:
   * fp32 workloads: every compared logit within 1e-4 of the oracle, and the greedy token equal
     to the oracle's wherever the oracle's top-2 margin is >= 1e-3.
   * bf16 workloads: per compared row (sequence x step) max |gpu - oracle| <= 2e-2 * (oracle
